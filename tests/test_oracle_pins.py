@@ -1,0 +1,330 @@
+"""Pins of the CPU oracle against what the paper and the mathematics fix (no GPU).
+
+Each test checks the oracle against something other than itself: the paper's printed table
+sizes, hand-computed worked examples, closed forms of the table, Mitchell's published error
+bound, IEEE products computed by numpy, library convolutions in float64, and a bit-level
+mirror of Algorithm 2 over every mantissa pair.
+"""
+import json
+import os
+
+import numpy as np
+import pytest
+
+import oracle
+from closed_forms import (alg2_mirror, bits_equal_nan_class, daz, exact_lut_closed_form,
+                          mitchell_lut_closed_form, special_values, trunc_bits)
+from paper_2209_04161_amd import workloads as W
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
+
+
+def _read_hex_table(name):
+    vals = []
+    with open(os.path.join(GOLDEN, name)) as f:
+        for line in f:
+            line = line.strip()
+            if line and not line.startswith("#"):
+                vals.append(int(line, 16))
+    return np.array(vals, dtype=np.uint32)
+
+
+# ---------------------------------------------------------------- Algorithm 1 (table) ------
+
+def test_table_sizes_match_paper():
+    """Sec. 'Lookup Table Generation' / 'AMSim': 2^(2M) entries of 4 bytes; 16 B, 65.53 kB, 16.8 MB."""
+    with open(os.path.join(GOLDEN, "lut_sizes.json")) as f:
+        g = json.load(f)
+    for m, nbytes in g["sizes_bytes"].items():
+        t = oracle.lut(oracle.MITCHELL, int(m))
+        assert t.dtype == np.uint32
+        assert t.nbytes == nbytes
+
+
+def test_mitchell_m1_worked_example():
+    assert np.array_equal(oracle.lut(oracle.MITCHELL, 1), _read_hex_table("mitchell_m1_lut.txt"))
+
+
+def test_exact_m1_worked_example():
+    assert np.array_equal(oracle.lut(oracle.EXACT_TRUNC, 1), _read_hex_table("exact_m1_lut.txt"))
+
+
+@pytest.mark.parametrize("m", list(range(1, 12)))
+def test_table_closed_forms(m):
+    assert np.array_equal(oracle.lut(oracle.MITCHELL, m), mitchell_lut_closed_form(m))
+    assert np.array_equal(oracle.lut(oracle.EXACT_TRUNC, m), exact_lut_closed_form(m))
+
+
+def test_asymmetric_model_table_is_not_symmetric():
+    """The operand-order test model must really distinguish its operands."""
+    t = oracle.lut(oracle.ASYM, 5).reshape(32, 32)
+    assert not np.array_equal(t, t.T)
+
+
+# ---------------------------------------------------------------- models -----------------
+
+def _mantissa_grid(m):
+    n = 1 << m
+    k = np.arange(n, dtype=np.float64)
+    x = (1.0 + k / n).astype(np.float32)
+    a = np.repeat(x, n)
+    b = np.tile(x, n)
+    return a, b
+
+
+def test_mitchell_error_bound():
+    """Mitchell (1962): the log multiplier never overestimates; its worst relative error is -1/9,
+    reached when both fractions are 1/2."""
+    m = 7
+    a, b = _mantissa_grid(m)
+    approx = oracle.mul(oracle.MITCHELL, m, a, b).astype(np.float64)
+    exact = a.astype(np.float64) * b.astype(np.float64)
+    rel = approx / exact - 1.0
+    assert rel.max() <= 0.0
+    assert rel.min() >= -1.0 / 9.0 - 1e-15
+    worst = np.argmin(rel)
+    assert a[worst] == 1.5 and b[worst] == 1.5
+    assert abs(rel[worst] + 1.0 / 9.0) < 1e-15
+
+
+def test_mitchell_power_of_two_operand_is_exact():
+    """With a zero fraction (power-of-two operand) Mitchell's log and antilog are exact, so the
+    product equals the other operand truncated to M bits times the power of two."""
+    rng = np.random.default_rng(11)
+    b = rng.uniform(-4, 4, 5000).astype(np.float32)
+    e = rng.integers(-30, 30, 5000)
+    a = np.ldexp(np.ones(5000), e).astype(np.float32) * np.where(rng.random(5000) < 0.5, -1, 1).astype(np.float32)
+    for m in (1, 4, 7, 11):
+        got = oracle.mul(oracle.MITCHELL, m, a, b)
+        want = a * trunc_bits(b, m)   # exact in float32: a power of two times a float
+        assert np.array_equal(got.view(np.uint32), want.view(np.uint32))
+
+
+@pytest.mark.parametrize("m", [1, 3, 7, 10, 11])
+def test_exact_trunc_equals_ieee_product_of_truncated_operands(m):
+    """bfloat16-style truncation then an exact multiply: numpy's IEEE float32 product of the
+    truncated operands (exact, since both significands have at most 12 bits)."""
+    rng = np.random.default_rng(100 + m)
+    a = (rng.standard_normal(20000) * np.exp2(rng.integers(-40, 40, 20000))).astype(np.float32)
+    b = (rng.standard_normal(20000) * np.exp2(rng.integers(-40, 40, 20000))).astype(np.float32)
+    got = oracle.mul(oracle.EXACT_TRUNC, m, a, b)
+    want = trunc_bits(a, m) * trunc_bits(b, m)
+    assert np.array_equal(got.view(np.uint32), want.view(np.uint32))
+
+
+def test_special_values_follow_ieee_after_denormals_read_as_zero():
+    """Where Algorithm 2's reading coincides with IEEE 754 (NaN in, Inf*0, signed zeros, Inf*x),
+    the oracle equals numpy's float32 product of the operands with denormals read as zero."""
+    s = special_values()
+    a = np.repeat(s, s.size)
+    b = np.tile(s, s.size)
+    got = oracle.mul(oracle.EXACT_TRUNC, 11, a, b)
+    ia, ib = daz(a), daz(b)
+    with np.errstate(all="ignore"):
+        ieee = ia * ib
+    special = np.isnan(ia) | np.isnan(ib) | np.isinf(ia) | np.isinf(ib) | (ia == 0) | (ib == 0)
+    assert special.sum() > 300
+    assert bits_equal_nan_class(got[special], ieee[special]).all()
+
+
+def test_zero_and_overflow_rules_of_algorithm_2():
+    """Algorithm 2: zero when the un-normalised biased exponent Ea+Eb-127 <= 0 (tested before the
+    carry), infinity when it is >= 255 or when the carry lifts it to 255."""
+    f = np.float32
+    cases = [
+        (f(2.0 ** -63), f(2.0 ** -64), 0.0),                 # Exp = 0            -> 0
+        (f(-1.5 * 2.0 ** -63), f(1.5 * 2.0 ** -64), -0.0),   # Exp = 0 with carry -> -0 (before carry)
+        (f(2.0 ** -63), f(2.0 ** -63), 2.0 ** -126),         # Exp = 1            -> FLT_MIN
+        (f(2.0 ** 64), f(2.0 ** 64), np.inf),                # Exp = 255          -> inf
+        (f(-2.0 ** 63), f(2.0 ** 64), -(2.0 ** 127)),        # Exp = 254 no carry -> -2^127
+        (f(1.5 * 2.0 ** 63), f(1.5 * 2.0 ** 64), np.inf),    # Exp = 254 + carry  -> inf
+    ]
+    for a, b, want in cases:
+        got = oracle.mul(oracle.MITCHELL, 7, np.array([a]), np.array([b]))[0]
+        assert np.array_equal(np.float32(got).view(np.uint32), np.float32(want).view(np.uint32)), (a, b, got, want)
+
+
+def _exponent_grid_pairs(m, rng):
+    """Every mantissa pair (top M bits, random low bits) x exponent pairs around the range
+    limits x the four sign combinations."""
+    n = 1 << m
+    k = np.arange(n, dtype=np.uint32)
+    ka = np.repeat(k, n)
+    kb = np.tile(k, n)
+    exps = [(127, 127), (1, 1), (1, 126), (63, 64), (64, 64), (64, 63), (126, 128), (200, 54),
+            (254, 1), (127, 127 + 126), (128, 127 + 126), (127 + 64, 127 + 63), (2, 125), (60, 66),
+            (191, 191)]
+    A, B = [], []
+    for ea, eb in exps:
+        for sa in (0, 1):
+            for sb in (0, 1):
+                low_a = rng.integers(0, 1 << (23 - m), ka.size, dtype=np.uint32)
+                low_b = rng.integers(0, 1 << (23 - m), kb.size, dtype=np.uint32)
+                ua = (np.uint32(sa) << 31) | (np.uint32(ea) << 23) | (ka << (23 - m)) | low_a
+                ub = (np.uint32(sb) << 31) | (np.uint32(eb) << 23) | (kb << (23 - m)) | low_b
+                A.append(ua)
+                B.append(ub)
+    return np.concatenate(A).view(np.float32), np.concatenate(B).view(np.float32)
+
+
+@pytest.mark.parametrize("model,closed", [(oracle.MITCHELL, mitchell_lut_closed_form),
+                                          (oracle.EXACT_TRUNC, exact_lut_closed_form)])
+@pytest.mark.parametrize("m", [1, 2, 5, 7])
+def test_oracle_product_equals_algorithm_2_on_every_mantissa_pair(model, closed, m):
+    """Brute force: the oracle's direct model call == Algorithm 2's bit assembly from the
+    closed-form table, for all 2^(2M) mantissa pairs x an exponent grid x signs, plus the
+    full cross product of special values."""
+    rng = np.random.default_rng(m)
+    a, b = _exponent_grid_pairs(m, rng)
+    s = special_values()
+    a = np.concatenate([a, np.repeat(s, s.size)])
+    b = np.concatenate([b, np.tile(s, s.size)])
+    got = oracle.mul(model, m, a, b)
+    want = alg2_mirror(a, b, closed(m), m)
+    ok = bits_equal_nan_class(got, want)
+    assert ok.all(), (a[~ok][:5], b[~ok][:5], got[~ok][:5], want[~ok][:5])
+
+
+def test_oracle_product_equals_algorithm_2_m11_sampled():
+    m = 11
+    rng = np.random.default_rng(1234)
+    n = 400000
+    ua = rng.integers(0, 2 ** 32, n, dtype=np.uint64).astype(np.uint32)
+    ub = rng.integers(0, 2 ** 32, n, dtype=np.uint64).astype(np.uint32)
+    a, b = ua.view(np.float32), ub.view(np.float32)
+    for model, closed in ((oracle.MITCHELL, mitchell_lut_closed_form), (oracle.EXACT_TRUNC, exact_lut_closed_form)):
+        got = oracle.mul(model, m, a, b)
+        want = alg2_mirror(a, b, closed(m), m)
+        assert bits_equal_nan_class(got, want).all()
+
+
+# ---------------------------------------------------------------- GEMM ------------------
+
+@pytest.mark.parametrize("transa,transb", [(False, False), (True, False), (False, True), (True, True)])
+def test_gemm_equals_float64_matmul_for_exact_model(transa, transb):
+    """With the exact-M model on inputs already truncated to M bits every product is exact, so
+    the oracle's GEMM is numpy's float64 matmul up to summation order."""
+    m = 7
+    M, N, K = 37, 29, 53
+    A = trunc_bits(W.uniform((K, M) if transa else (M, K), -1, 1, 5), m)
+    B = trunc_bits(W.uniform((N, K) if transb else (K, N), -1, 1, 6), m)
+    C, S = oracle.gemm(oracle.EXACT_TRUNC, m, A, B, transa, transb)
+    ref = (A.T if transa else A).astype(np.float64) @ (B.T if transb else B).astype(np.float64)
+    sref = np.abs((A.T if transa else A).astype(np.float64)) @ np.abs((B.T if transb else B).astype(np.float64))
+    assert np.all(np.abs(C.astype(np.float64) - ref) <= 1e-12 * sref + np.abs(ref) * 2.0 ** -24)
+    assert np.allclose(S, sref, rtol=1e-12, atol=0)
+
+
+def test_gemm_operand_order():
+    """Asymmetric model (first operand truncated to M bits, second to M-1): the first operand of
+    every product must be A."""
+    m = 6
+    A = W.uniform((19, 23), -2, 2, 7)
+    B = W.uniform((23, 17), -2, 2, 8)
+    C, _ = oracle.gemm(oracle.ASYM, m, A, B)
+    ref = trunc_bits(A, m).astype(np.float64) @ trunc_bits(B, m - 1).astype(np.float64)
+    swapped = trunc_bits(A, m - 1).astype(np.float64) @ trunc_bits(B, m).astype(np.float64)
+    assert np.allclose(C, ref, rtol=1e-6, atol=1e-6)
+    assert not np.allclose(C, swapped, rtol=1e-6, atol=1e-6)
+
+
+def test_gemm_empty_sum_is_negative_zero_and_k1_is_the_product():
+    A = W.uniform((5, 1), -1, 1, 9)
+    B = W.uniform((1, 4), -1, 1, 10)
+    C, S = oracle.gemm(oracle.MITCHELL, 7, A, B)
+    prod = oracle.mul(oracle.MITCHELL, 7, np.repeat(A[:, 0], 4), np.tile(B[0], 5)).reshape(5, 4)
+    assert np.array_equal(C.view(np.uint32), prod.view(np.uint32))
+    C0, _ = oracle.gemm(oracle.MITCHELL, 7, np.zeros((3, 0), np.float32), np.zeros((0, 2), np.float32))
+    assert np.all(C0.view(np.uint32) == 0x80000000)
+
+
+def test_gemm_sampled_indices_match_full():
+    A = W.uniform((40, 31), -1, 1, 12)
+    B = W.uniform((31, 22), -1, 1, 13)
+    C, S = oracle.gemm(oracle.MITCHELL, 7, A, B)
+    idx = np.array([0, 5, 21, 100, 40 * 22 - 1])
+    Cs, Ss = oracle.gemm(oracle.MITCHELL, 7, A, B, idx=idx)
+    assert np.array_equal(Cs, C.reshape(-1)[idx]) and np.array_equal(Ss, S.reshape(-1)[idx])
+
+
+# ---------------------------------------------------------------- convolution -----------
+
+torch = pytest.importorskip("torch")
+F = torch.nn.functional
+
+CONV_CASES = [
+    W.conv_desc(2, 7, 6, 3, 4, 3, 3, 1, 1),
+    W.conv_desc(2, 9, 8, 2, 3, 3, 3, 2, 1),
+    W.conv_desc(1, 11, 10, 3, 2, 5, 5, 2, pads=(2, 1, 0, 3)),
+    W.conv_desc(3, 5, 5, 4, 2, 1, 1, 1, 0),
+    W.conv_desc(2, 8, 9, 2, 3, 7, 7, 2, 3),
+    W.conv_desc(1, 6, 6, 1, 2, 2, 3, 3, pads=(1, 0, 2, 1)),
+]
+
+
+def _torch_conv_passes(p, x, w, dy):
+    """float64 reference via torch: forward, and both gradients through autograd."""
+    xt = torch.tensor(x, dtype=torch.float64).permute(0, 3, 1, 2).contiguous().requires_grad_(True)
+    wt = torch.tensor(w, dtype=torch.float64).permute(3, 2, 0, 1).contiguous().requires_grad_(True)
+    xp = F.pad(xt, (p["pad_left"], p["pad_right"], p["pad_top"], p["pad_bottom"]))
+    y = F.conv2d(xp, wt, stride=(p["stride_h"], p["stride_w"]))
+    dyt = torch.tensor(dy, dtype=torch.float64).permute(0, 3, 1, 2)
+    y.backward(dyt)
+    return (y.detach().permute(0, 2, 3, 1).numpy(), xt.grad.permute(0, 2, 3, 1).numpy(),
+            wt.grad.permute(2, 3, 1, 0).numpy())
+
+
+def _conv_inputs(p, seed, mx, mw, mdy):
+    oh, ow = W.conv_out_hw(p)
+    x = trunc_bits(W.uniform((p["n"], p["h"], p["w"], p["c_in"]), -1, 1, seed), mx)
+    w = trunc_bits(W.uniform((p["kh"], p["kw"], p["c_in"], p["c_out"]), -1, 1, seed + 1), mw)
+    dy = trunc_bits(W.uniform((p["n"], oh, ow, p["c_out"]), -1, 1, seed + 2), mdy)
+    return x, w, dy
+
+
+@pytest.mark.parametrize("ci", range(len(CONV_CASES)))
+def test_conv_equals_torch_float64_for_exact_model(ci):
+    p = CONV_CASES[ci]
+    m = 7
+    x, w, dy = _conv_inputs(p, 20 + ci, m, m, m)
+    y_ref, dx_ref, dw_ref = _torch_conv_passes(p, x, w, dy)
+    y, _ = oracle.conv2d_fwd(oracle.EXACT_TRUNC, m, p, x, w)
+    dx, _ = oracle.conv2d_bwd_data(oracle.EXACT_TRUNC, m, p, dy, w)
+    dw, _ = oracle.conv2d_bwd_weight(oracle.EXACT_TRUNC, m, p, x, dy)
+    for got, ref in ((y, y_ref), (dx, dx_ref), (dw, dw_ref)):
+        assert got.shape == ref.shape
+        assert np.allclose(got, ref, rtol=1e-6, atol=1e-6)
+
+
+@pytest.mark.parametrize("ci", [1, 2])
+def test_conv_operand_order(ci):
+    """Asymmetric model pins the first operand of each pass: fwd amul(x, w), bwd_data
+    amul(dy, w), bwd_weight amul(x, dy)."""
+    p = CONV_CASES[ci]
+    m = 6
+    x, w, dy = _conv_inputs(p, 40 + ci, 23, 23, 23)
+    y_ref, _, _ = _torch_conv_passes(p, trunc_bits(x, m), trunc_bits(w, m - 1), dy)
+    _, dx_ref, _ = _torch_conv_passes(p, x, trunc_bits(w, m - 1), trunc_bits(dy, m))
+    _, _, dw_ref = _torch_conv_passes(p, trunc_bits(x, m), w, trunc_bits(dy, m - 1))
+    y, _ = oracle.conv2d_fwd(oracle.ASYM, m, p, x, w)
+    dx, _ = oracle.conv2d_bwd_data(oracle.ASYM, m, p, dy, w)
+    dw, _ = oracle.conv2d_bwd_weight(oracle.ASYM, m, p, x, dy)
+    assert np.allclose(y, y_ref, rtol=1e-5, atol=1e-6)
+    assert np.allclose(dx, dx_ref, rtol=1e-5, atol=1e-6)
+    assert np.allclose(dw, dw_ref, rtol=1e-5, atol=1e-6)
+    # and the swapped reading would fail
+    y_sw, _, _ = _torch_conv_passes(p, trunc_bits(x, m - 1), trunc_bits(w, m), dy)
+    assert not np.allclose(y, y_sw, rtol=1e-5, atol=1e-6)
+
+
+def test_conv_sampled_indices_match_full():
+    p = CONV_CASES[2]
+    x, w, dy = _conv_inputs(p, 60, 23, 23, 23)
+    y, _ = oracle.conv2d_fwd(oracle.MITCHELL, 7, p, x, w)
+    idx = np.array([0, 7, y.size // 2, y.size - 1])
+    ys, _ = oracle.conv2d_fwd(oracle.MITCHELL, 7, p, x, w, idx=idx)
+    assert np.array_equal(ys, y.reshape(-1)[idx])
+    dw, _ = oracle.conv2d_bwd_weight(oracle.MITCHELL, 7, p, x, dy)
+    idx = np.array([1, dw.size - 1])
+    dws, _ = oracle.conv2d_bwd_weight(oracle.MITCHELL, 7, p, x, dy, idx=idx)
+    assert np.array_equal(dws, dw.reshape(-1)[idx])
