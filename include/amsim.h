@@ -1,0 +1,159 @@
+/*
+ * amsim.h -- C ABI of the MI355X (gfx950) approximate-multiplier GEMM / convolution library.
+ *
+ * The library simulates an approximate floating-point multiplier the way AMSim does in
+ * ApproxTrain (arXiv 2209.04161): every FP32 product a*b is replaced by
+ *   sign(a) XOR sign(b), exponent Ea + Eb - 127 (+ carry), mantissa from a lookup table
+ *   indexed by the concatenated top-M mantissa bits of a and b (Algorithm 2),
+ * and products are accumulated in FP32 (Sec. "Experiment Setup", Datatype paragraph).
+ * The table comes from a C functional model of the multiplier (Algorithm 1).
+ *
+ * Conventions for every entry point:
+ *   - Return value: AMSIM_OK (0) or a negative AMSIM_ERR_* code.  Nothing throws across the
+ *     ABI and nothing prints.  On error no output is written and nothing is launched.
+ *   - "device" pointers are HIP device allocations owned by the caller (e.g. torch tensors);
+ *     "host" pointers are ordinary host memory owned by the caller.  Device pointers must be
+ *     4-byte aligned; the library allocates nothing and frees nothing.
+ *   - `stream` is a hipStream_t passed as void* (NULL = the null stream).  Device entry
+ *     points only enqueue work on that stream: they do not synchronise and return before the
+ *     work completes.  A HIP launch error is reported as AMSIM_ERR_HIP.
+ *   - `lut` is a device copy of the table built by lut_build: uint32[2^(2*m_bits)], entry
+ *     k * 2^M + j holds carry << 23 | mantissa(23 bits) for first-operand mantissa k and
+ *     second-operand mantissa j.  Only its low 24 bits are read.
+ *   - m_bits (the paper's M) must be in [1, 11]; M <= 7 keeps the table in LDS, 8..11 reads it
+ *     from global memory.
+ *   - Products: zero/denormal operands give a signed zero, NaN operands NaN, Inf times a
+ *     zero/denormal operand NaN, Inf times anything else a signed Inf; otherwise zero if
+ *     Ea + Eb - 127 <= 0 (checked before the carry), Inf if it is >= 255 or the carry lifts
+ *     it to 255, else sign | (Ea + Eb - 127 + carry) << 23 | mantissa.
+ *   - Sums start from -0.0 and are FP32 with denormal results flushed to zero; summation
+ *     order is unspecified (the results of one call are deterministic run to run).
+ */
+#ifndef AMSIM_H
+#define AMSIM_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define AMSIM_OK 0
+#define AMSIM_ERR_INVALID_ARG (-1) /* null pointer, bad size/stride/shape */
+#define AMSIM_ERR_UNSUPPORTED (-2) /* m_bits outside [1, 11] or a shape beyond the limits */
+#define AMSIM_ERR_MODEL (-3)       /* the model cannot be represented by a mantissa table */
+#define AMSIM_ERR_WORKSPACE (-4)   /* workspace missing or smaller than the size query says */
+#define AMSIM_ERR_HIP (-5)         /* a HIP runtime call or kernel launch failed */
+#define AMSIM_ERR_IO (-6)          /* file could not be read/written or has a bad header */
+
+/* Human-readable name of a status code (static string, never NULL). */
+const char *amsim_status_string(int status);
+
+/* Library version, major * 10000 + minor * 100 + patch. */
+int amsim_version(void);
+
+/* ----------------------------------------------------------------- functional models ----
+ * A designer's approximate multiplier (Algorithm 1's input approx_mul): takes two FP32 values,
+ * returns their approximate FP32 product.  lut_build calls it only with positive, normal
+ * operands whose exponent fields keep the product's exponent in range.  `ctx` is passed through.
+ */
+typedef float (*amsim_model_fn)(float a, float b, void *ctx);
+
+/* Built-in models; ctx points to an int holding M (1..11).
+ * Mitchell's logarithmic multiplier (the paper's MIT16 at M = 7): log2(1 + x) ~= x on both
+ * operands truncated to M mantissa bits, antilog 2^(c + f) ~= 2^c (1 + f). */
+float amsim_model_mitchell(float a, float b, void *ctx);
+/* Exact product of the operands truncated to M mantissa bits (bfloat16 truncation at M = 7,
+ * Sec. "Experiment Setup": format conversion is bit truncation). */
+float amsim_model_exact_trunc(float a, float b, void *ctx);
+
+/* ----------------------------------------------------------------- table generation -----
+ * lut_build: Algorithm 1.  Fills out[k * 2^M + j] = carry << 23 | mantissa(C) for
+ * C = model(A, B, ctx), A = +1.k and B = +1.j (exponent field 127, k and j in the top M
+ * mantissa bits), carry = 1 iff Exp(C) > Exp(A) + Exp(B) - 127.
+ *   m_bits  M in [1, 11]                           (else AMSIM_ERR_UNSUPPORTED)
+ *   model   host function pointer, non-NULL        (else AMSIM_ERR_INVALID_ARG)
+ *   out     host uint32 array of out_len entries, out_len >= 2^(2M) (else INVALID_ARG)
+ * Returns AMSIM_ERR_MODEL if the model's product is not positive and finite, its exponent is
+ * neither Exp(A)+Exp(B)-127 nor one more, or a rebuild of a sample of entries at other legal
+ * exponents and all four sign combinations disagrees (the model must depend on the
+ * mantissas only, Sec. "Lookup Table Generation").  Runs on the calling thread. */
+int lut_build(int m_bits, amsim_model_fn model, void *ctx, uint32_t *out, size_t out_len);
+
+/* Table file (Sec. "Lookup Table Generation": tables are generated once and loaded at run
+ * time).  Format: 16-byte header {"AMLT", uint32 version = 1, uint32 M, uint32 0}, then
+ * 2^(2M) little-endian uint32 entries.
+ * lut_save writes `lut` (host, len >= 2^(2M) entries) to `path`.
+ * lut_load reads `path` into `out` (host, out_len entries); *m_bits receives M.  Passing
+ * out = NULL only reads the header.  Errors: AMSIM_ERR_IO, AMSIM_ERR_INVALID_ARG. */
+int lut_save(const char *path, int m_bits, const uint32_t *lut, size_t len);
+int lut_load(const char *path, int *m_bits, uint32_t *out, size_t out_len);
+
+/* ----------------------------------------------------------------- GEMM -----------------
+ * approx_gemm: C = op(A) * op(B) with every product approximate (the paper's GEMM kernel with
+ * AMSim, Sec. "Other Custom CUDA Kernels"; dense layers map onto it, Sec. "AMDENSE").
+ * Row-major storage.  op(A) is m x k: A is m x k (lda >= k) or, with trans_a, k x m
+ * (lda >= m).  op(B) is k x n: B is k x n (ldb >= n) or, with trans_b, n x k (ldb >= k).
+ * C is m x n (ldc >= n) and is overwritten (no alpha/beta).  The product of element (i, kk)
+ * of op(A) with element (kk, j) of op(B) takes op(A)'s element as the first operand (the
+ * table's high index).  m or n == 0: nothing is done.  k == 0: C is filled with -0.0.
+ * All matrix pointers and `lut` are device memory; `workspace` is device memory of at least
+ * the size amsim_gemm_workspace_size reports (may be NULL when that size is 0). */
+int amsim_gemm_workspace_size(int trans_a, int trans_b, int64_t m, int64_t n, int64_t k, int m_bits,
+                              size_t *bytes);
+int approx_gemm(int trans_a, int trans_b, int64_t m, int64_t n, int64_t k, const float *A, int64_t lda,
+                const float *B, int64_t ldb, float *C, int64_t ldc, const uint32_t *lut, int m_bits,
+                void *workspace, size_t workspace_bytes, void *stream);
+
+/* ----------------------------------------------------------------- 2-D convolution ------
+ * NHWC activations, HWIO weights ([kh][kw][c_in][c_out]), explicit four-sided zero padding
+ * (TF "SAME" is an asymmetric pad), stride >= 1, no dilation or groups (none in the paper).
+ * OH = (h + pad_top + pad_bottom - kh) / stride_h + 1, OW likewise; both must be >= 1.
+ * All sizes must be >= 1 (pads >= 0) and every tensor must have fewer than 2^31 elements
+ * (else AMSIM_ERR_UNSUPPORTED). */
+typedef struct amsim_conv2d {
+    int n, h, w, c_in, c_out, kh, kw, stride_h, stride_w, pad_top, pad_bottom, pad_left, pad_right;
+} amsim_conv2d;
+
+#define AMSIM_CONV_FWD 0
+#define AMSIM_CONV_BWD_DATA 1
+#define AMSIM_CONV_BWD_WEIGHT 2
+
+/* Device workspace bytes a pass needs for this shape and M (0 allowed for NULL workspace). */
+int amsim_conv2d_workspace_size(const amsim_conv2d *desc, int pass, int m_bits, size_t *bytes);
+
+/* Forward propagation (Algorithm 3): y[n,oh,ow,co] = sum_{kh,kw,ci}
+ * amul(x[n, oh*sh+kh-pt, ow*sw+kw-pl, ci], w[kh,kw,ci,co]); padded taps contribute nothing.
+ * x: device [n][h][w][c_in], w: device HWIO, y: device [n][OH][OW][c_out] (overwritten). */
+int approx_conv2d_fwd(const amsim_conv2d *desc, const float *x, const float *w, float *y, const uint32_t *lut,
+                      int m_bits, void *workspace, size_t workspace_bytes, void *stream);
+
+/* Preceding-layer gradient (Algorithm 4, second half): dx[n,h,w,ci] = sum over (kh,kw,co) and
+ * output positions (oh,ow) with oh*sh+kh-pt == h and ow*sw+kw-pl == w of
+ * amul(dy[n,oh,ow,co], w[kh,kw,ci,co]) -- the padded, dilated error against the transposed and
+ * reversed weights, without materialising either.  dy: device [n][OH][OW][c_out], w: device
+ * HWIO, dx: device [n][h][w][c_in] (overwritten; positions no output reads get -0.0). */
+int approx_conv2d_bwd_data(const amsim_conv2d *desc, const float *dy, const float *w, float *dx,
+                           const uint32_t *lut, int m_bits, void *workspace, size_t workspace_bytes, void *stream);
+
+/* Weights gradient (Algorithm 4, first half): dw[kh,kw,ci,co] = sum over (n,oh,ow) whose tap
+ * lies inside the image of amul(x[n, oh*sh+kh-pt, ow*sw+kw-pl, ci], dy[n,oh,ow,co]) -- the
+ * stride dilation of the error is implicit.  x: device NHWC, dy: device [n][OH][OW][c_out],
+ * dw: device HWIO (overwritten). */
+int approx_conv2d_bwd_weight(const amsim_conv2d *desc, const float *x, const float *dy, float *dw,
+                             const uint32_t *lut, int m_bits, void *workspace, size_t workspace_bytes,
+                             void *stream);
+
+/* ----------------------------------------------------------------- element-wise --------
+ * approx_mul_ew: c[i] = amul(a[i], b[i]) for i < n -- Algorithm 2 exactly as the GEMM and
+ * convolution kernels evaluate it, exposed so that single products can be checked bit for
+ * bit.  a, b, c, lut: device memory (c may alias neither input).  n == 0: nothing is done. */
+int approx_mul_ew(int64_t n, const float *a, const float *b, float *c, const uint32_t *lut, int m_bits,
+                  void *stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* AMSIM_H */

@@ -1,0 +1,290 @@
+"""Python binding of libamsim.so (argument marshalling only).
+
+Every function here has the name of the C entry point it calls.  Tensors are torch tensors:
+device memory comes from torch, the stream is torch's current stream, and the raw pointers go
+through the C ABI.  All computation happens in the library's HIP kernels; if the library is
+not built this module raises instead of computing anything another way.
+"""
+import ctypes
+import os
+
+import numpy as np
+
+from . import build as _build
+
+AMSIM_OK = 0
+AMSIM_ERR_INVALID_ARG = -1
+AMSIM_ERR_UNSUPPORTED = -2
+AMSIM_ERR_MODEL = -3
+AMSIM_ERR_WORKSPACE = -4
+AMSIM_ERR_HIP = -5
+AMSIM_ERR_IO = -6
+
+AMSIM_CONV_FWD = 0
+AMSIM_CONV_BWD_DATA = 1
+AMSIM_CONV_BWD_WEIGHT = 2
+
+MODEL_FN = ctypes.CFUNCTYPE(ctypes.c_float, ctypes.c_float, ctypes.c_float, ctypes.c_void_p)
+
+
+class AmsimError(RuntimeError):
+    def __init__(self, status, where):
+        self.status = status
+        super().__init__("%s: %s (status %d)" % (where, amsim_status_string(status), status))
+
+
+class amsim_conv2d(ctypes.Structure):
+    _fields_ = [(name, ctypes.c_int) for name in (
+        "n", "h", "w", "c_in", "c_out", "kh", "kw", "stride_h", "stride_w",
+        "pad_top", "pad_bottom", "pad_left", "pad_right")]
+
+
+_lib = None
+
+
+def library_path() -> str:
+    return _build.LIB
+
+
+def lib():
+    """Load the built library (no fallback: a missing library is an error)."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    path = library_path()
+    if not os.path.exists(path):
+        raise RuntimeError("libamsim.so is not built (%s); run __graft_entry__.build() or "
+                           "python -m paper_2209_04161_amd.build" % path)
+    L = ctypes.CDLL(path)
+    vp, i64, sz = ctypes.c_void_p, ctypes.c_int64, ctypes.c_size_t
+    u32p = ctypes.POINTER(ctypes.c_uint32)
+    szp = ctypes.POINTER(ctypes.c_size_t)
+    cp = ctypes.POINTER(amsim_conv2d)
+    sigs = {
+        "amsim_status_string": ([ctypes.c_int], ctypes.c_char_p),
+        "amsim_version": ([], ctypes.c_int),
+        "amsim_model_mitchell": ([ctypes.c_float, ctypes.c_float, vp], ctypes.c_float),
+        "amsim_model_exact_trunc": ([ctypes.c_float, ctypes.c_float, vp], ctypes.c_float),
+        "lut_build": ([ctypes.c_int, vp, vp, u32p, sz], ctypes.c_int),
+        "lut_save": ([ctypes.c_char_p, ctypes.c_int, u32p, sz], ctypes.c_int),
+        "lut_load": ([ctypes.c_char_p, ctypes.POINTER(ctypes.c_int), u32p, sz], ctypes.c_int),
+        "amsim_gemm_workspace_size": ([ctypes.c_int, ctypes.c_int, i64, i64, i64, ctypes.c_int, szp], ctypes.c_int),
+        "approx_gemm": ([ctypes.c_int, ctypes.c_int, i64, i64, i64, vp, i64, vp, i64, vp, i64, vp, ctypes.c_int,
+                         vp, sz, vp], ctypes.c_int),
+        "amsim_conv2d_workspace_size": ([cp, ctypes.c_int, ctypes.c_int, szp], ctypes.c_int),
+        "approx_conv2d_fwd": ([cp, vp, vp, vp, vp, ctypes.c_int, vp, sz, vp], ctypes.c_int),
+        "approx_conv2d_bwd_data": ([cp, vp, vp, vp, vp, ctypes.c_int, vp, sz, vp], ctypes.c_int),
+        "approx_conv2d_bwd_weight": ([cp, vp, vp, vp, vp, ctypes.c_int, vp, sz, vp], ctypes.c_int),
+        "approx_mul_ew": ([i64, vp, vp, vp, vp, ctypes.c_int, vp], ctypes.c_int),
+    }
+    for name, (args, res) in sigs.items():
+        fn = getattr(L, name)
+        fn.argtypes = args
+        fn.restype = res
+    _lib = L
+    return L
+
+
+def amsim_status_string(status: int) -> str:
+    return lib().amsim_status_string(int(status)).decode()
+
+
+def _check(status, where):
+    if status != AMSIM_OK:
+        raise AmsimError(status, where)
+
+
+# ------------------------------------------------------------------ tables ----------------
+
+def _model_pointer(model):
+    """Returns (function pointer as void*, keep-alive object)."""
+    L = lib()
+    if model in ("mitchell", "exact_trunc"):
+        fn = getattr(L, "amsim_model_" + model)
+        return ctypes.cast(fn, ctypes.c_void_p), fn
+    if callable(model):
+        cb = MODEL_FN(lambda a, b, ctx: float(model(a, b)))
+        return ctypes.cast(cb, ctypes.c_void_p), cb
+    raise ValueError("model must be 'mitchell', 'exact_trunc' or a callable (a, b) -> float")
+
+
+def lut_build(m_bits: int, model="mitchell") -> np.ndarray:
+    """Algorithm 1 on the host: uint32[2^(2M)] table for a built-in or Python-callable model."""
+    n = 1 << (2 * int(m_bits)) if 1 <= int(m_bits) <= 11 else 0
+    out = np.zeros(max(n, 1), dtype=np.uint32)
+    fptr, keep = _model_pointer(model)
+    ctx = ctypes.c_int(int(m_bits))
+    status = lib().lut_build(int(m_bits), fptr, ctypes.cast(ctypes.byref(ctx), ctypes.c_void_p),
+                             out.ctypes.data_as(ctypes.POINTER(ctypes.c_uint32)), out.size if n else 0)
+    del keep
+    _check(status, "lut_build")
+    return out
+
+
+def lut_save(path: str, m_bits: int, table: np.ndarray) -> None:
+    table = np.ascontiguousarray(table, dtype=np.uint32)
+    _check(lib().lut_save(os.fsencode(path), int(m_bits), table.ctypes.data_as(ctypes.POINTER(ctypes.c_uint32)),
+                          table.size), "lut_save")
+
+
+def lut_load(path: str):
+    """Returns (m_bits, table)."""
+    m = ctypes.c_int(0)
+    _check(lib().lut_load(os.fsencode(path), ctypes.byref(m), None, 0), "lut_load")
+    out = np.empty(1 << (2 * m.value), dtype=np.uint32)
+    _check(lib().lut_load(os.fsencode(path), ctypes.byref(m), out.ctypes.data_as(ctypes.POINTER(ctypes.c_uint32)),
+                          out.size), "lut_load")
+    return m.value, out
+
+
+def model_value(model: str, m_bits: int, a: float, b: float) -> float:
+    """Call a built-in functional model directly (host)."""
+    ctx = ctypes.c_int(int(m_bits))
+    fn = getattr(lib(), "amsim_model_" + model)
+    return float(fn(a, b, ctypes.cast(ctypes.byref(ctx), ctypes.c_void_p)))
+
+
+# ------------------------------------------------------------------ device calls ----------
+
+def _torch():
+    import torch
+    return torch
+
+
+def _ptr(t):
+    return ctypes.c_void_p(t.data_ptr()) if t is not None else None
+
+
+def _stream():
+    return ctypes.c_void_p(_torch().cuda.current_stream().cuda_stream)
+
+
+def device_lut(table: np.ndarray, device="cuda"):
+    """Upload a table to the device as an int32 tensor holding the uint32 bits."""
+    torch = _torch()
+    return torch.from_numpy(np.ascontiguousarray(table, dtype=np.uint32).view(np.int32)).to(device)
+
+
+def _check_f32(t, name):
+    torch = _torch()
+    if t.dtype != torch.float32 or not t.is_cuda or not t.is_contiguous():
+        raise ValueError("%s must be a contiguous float32 CUDA tensor" % name)
+
+
+def _check_lut(lut, m_bits):
+    torch = _torch()
+    if lut.dtype not in (torch.int32,) or not lut.is_cuda or lut.numel() < (1 << (2 * m_bits)):
+        raise ValueError("lut must be an int32 CUDA tensor of 2^(2M) entries")
+
+
+def amsim_gemm_workspace_size(trans_a, trans_b, m, n, k, m_bits) -> int:
+    b = ctypes.c_size_t(0)
+    _check(lib().amsim_gemm_workspace_size(int(trans_a), int(trans_b), m, n, k, int(m_bits), ctypes.byref(b)),
+           "amsim_gemm_workspace_size")
+    return b.value
+
+
+def _workspace(nbytes, device):
+    torch = _torch()
+    return torch.empty(max(int(nbytes), 1), dtype=torch.uint8, device=device)
+
+
+def approx_gemm(A, B, lut, m_bits, trans_a=False, trans_b=False, out=None, workspace=None):
+    """C = op(A) @ op(B) with approximate products (row-major float32 CUDA tensors)."""
+    torch = _torch()
+    _check_f32(A, "A")
+    _check_f32(B, "B")
+    _check_lut(lut, m_bits)
+    m = A.shape[1] if trans_a else A.shape[0]
+    k = A.shape[0] if trans_a else A.shape[1]
+    kb = B.shape[1] if trans_b else B.shape[0]
+    n = B.shape[0] if trans_b else B.shape[1]
+    if k != kb:
+        raise ValueError("inner dimensions differ")
+    if out is None:
+        out = torch.empty((m, n), dtype=torch.float32, device=A.device)
+    ldc = out.stride(0) if out.dim() == 2 else n
+    ws_bytes = amsim_gemm_workspace_size(trans_a, trans_b, m, n, k, m_bits)
+    if workspace is None:
+        workspace = _workspace(ws_bytes, A.device)
+    _check(lib().approx_gemm(int(trans_a), int(trans_b), m, n, k, _ptr(A), A.shape[1], _ptr(B), B.shape[1],
+                             _ptr(out), ldc, _ptr(lut), int(m_bits), _ptr(workspace), workspace.numel(), _stream()),
+           "approx_gemm")
+    return out
+
+
+def conv_desc_struct(d: dict) -> amsim_conv2d:
+    return amsim_conv2d(**{k: int(d[k]) for k, _ in amsim_conv2d._fields_})
+
+
+def conv_out_hw(d):
+    oh = (d["h"] + d["pad_top"] + d["pad_bottom"] - d["kh"]) // d["stride_h"] + 1
+    ow = (d["w"] + d["pad_left"] + d["pad_right"] - d["kw"]) // d["stride_w"] + 1
+    return oh, ow
+
+
+def amsim_conv2d_workspace_size(desc: dict, pass_id: int, m_bits: int) -> int:
+    b = ctypes.c_size_t(0)
+    s = conv_desc_struct(desc)
+    _check(lib().amsim_conv2d_workspace_size(ctypes.byref(s), int(pass_id), int(m_bits), ctypes.byref(b)),
+           "amsim_conv2d_workspace_size")
+    return b.value
+
+
+def _conv_call(fn_name, pass_id, desc, in0, in1, out, lut, m_bits, workspace):
+    s = conv_desc_struct(desc)
+    ws_bytes = amsim_conv2d_workspace_size(desc, pass_id, m_bits)
+    if workspace is None:
+        workspace = _workspace(ws_bytes, in0.device)
+    fn = getattr(lib(), fn_name)
+    _check(fn(ctypes.byref(s), _ptr(in0), _ptr(in1), _ptr(out), _ptr(lut), int(m_bits), _ptr(workspace),
+              workspace.numel(), _stream()), fn_name)
+    return out
+
+
+def approx_conv2d_fwd(desc, x, w, lut, m_bits, out=None, workspace=None):
+    """y (NHWC) from x (NHWC) and w (HWIO)."""
+    torch = _torch()
+    _check_f32(x, "x")
+    _check_f32(w, "w")
+    _check_lut(lut, m_bits)
+    oh, ow = conv_out_hw(desc)
+    if out is None:
+        out = torch.empty((desc["n"], oh, ow, desc["c_out"]), dtype=torch.float32, device=x.device)
+    return _conv_call("approx_conv2d_fwd", AMSIM_CONV_FWD, desc, x, w, out, lut, m_bits, workspace)
+
+
+def approx_conv2d_bwd_data(desc, dy, w, lut, m_bits, out=None, workspace=None):
+    """dx (NHWC) from dy (NHWC) and w (HWIO)."""
+    torch = _torch()
+    _check_f32(dy, "dy")
+    _check_f32(w, "w")
+    _check_lut(lut, m_bits)
+    if out is None:
+        out = torch.empty((desc["n"], desc["h"], desc["w"], desc["c_in"]), dtype=torch.float32, device=dy.device)
+    return _conv_call("approx_conv2d_bwd_data", AMSIM_CONV_BWD_DATA, desc, dy, w, out, lut, m_bits, workspace)
+
+
+def approx_conv2d_bwd_weight(desc, x, dy, lut, m_bits, out=None, workspace=None):
+    """dw (HWIO) from x (NHWC) and dy (NHWC)."""
+    torch = _torch()
+    _check_f32(x, "x")
+    _check_f32(dy, "dy")
+    _check_lut(lut, m_bits)
+    if out is None:
+        out = torch.empty((desc["kh"], desc["kw"], desc["c_in"], desc["c_out"]), dtype=torch.float32, device=x.device)
+    return _conv_call("approx_conv2d_bwd_weight", AMSIM_CONV_BWD_WEIGHT, desc, x, dy, out, lut, m_bits, workspace)
+
+
+def approx_mul_ew(a, b, lut, m_bits, out=None):
+    torch = _torch()
+    _check_f32(a, "a")
+    _check_f32(b, "b")
+    _check_lut(lut, m_bits)
+    if a.shape != b.shape:
+        raise ValueError("shapes differ")
+    if out is None:
+        out = torch.empty_like(a)
+    _check(lib().approx_mul_ew(a.numel(), _ptr(a), _ptr(b), _ptr(out), _ptr(lut), int(m_bits), _stream()),
+           "approx_mul_ew")
+    return out

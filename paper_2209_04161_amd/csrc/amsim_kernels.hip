@@ -1,0 +1,922 @@
+// amsim_kernels.hip -- HIP kernels for gfx950 and the device-side C entry points of the
+// approximate-multiplier library (ApproxTrain's AMSim, arXiv 2209.04161, Algorithms 2-4).
+//
+// How a product is evaluated (Algorithm 2, rewritten for the vector ALU):
+//   Each operand is decoded once into a 32-bit word
+//     head (bits 31..22): sign | exponent field | quiet-NaN bit   (mantissa cleared)
+//     idx  (bits 21..0) : the operand's top-M mantissa bits, pre-shifted into its part of
+//                         the table offset
+//   head read as a float is +-2^(E-127) for a normal operand, +-0 for a zero/denormal one,
+//   +-Inf or NaN for the specials.  The product is
+//     c = v * (pa * pb),   v = float((entry & 0xFFFFFF) + 0x3F800000) = 2^carry * 1.mantissa
+//   with f32 denormals flushed to zero: pa*pb underflows to a signed zero exactly when
+//   Ea + Eb - 127 <= 0 (the zero rule, before the carry), overflows to a signed Inf when it
+//   is >= 255, and v * (pa*pb) is exact, or Inf when the carry lifts the exponent to 255.
+//   IEEE arithmetic gives the NaN/Inf policy for special operands.  The sum uses
+//   fma(v, pa*pb, acc): pa*pb is rounded on its own, and v*(pa*pb) is exact, so the fma equals
+//   acc + c rounded once.
+//
+// Kernel shape: lanes of a wave own output rows (64*TM rows per wave), the wave's TN output
+// columns are wave-uniform (their operand words come through scalar loads), waves of a
+// workgroup take neighbouring column groups.  For M <= 7 the table lives in LDS, stored
+// transposed (second-operand mantissa major) so that the lanes' first-operand mantissas --
+// the varying part of the index -- fall into different banks.  For M = 8..11 the table is
+// read from global memory (L2 / MALL).  Products are never fed to MFMA: they are not IEEE.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cstdint>
+#include <mutex>
+#include <type_traits>
+
+#include "amsim.h"
+
+namespace {
+
+constexpr uint32_t kIdxMask = 0x003FFFFFu;
+constexpr uint32_t kHeadMask = 0xFFC00000u;
+constexpr int kWaves = 4;           // waves per workgroup (column groups)
+constexpr int kThreads = 64 * kWaves;
+constexpr int kMaxLdsBits = 7;      // table in LDS for M <= 7 (64 KiB)
+
+// ------------------------------------------------------------------ device helpers -------
+
+__device__ __forceinline__ uint32_t amsim_decode(uint32_t u, int m, int shift)
+{
+    const uint32_t e = (u >> 23) & 0xFFu;
+    uint32_t head;
+    if (e == 0u)
+        head = u & 0x80000000u;                                        // +-0 (denormals too)
+    else if (e == 0xFFu)
+        head = (u & 0xFF800000u) | ((u & 0x007FFFFFu) ? 0x00400000u : 0u);  // +-Inf / qNaN
+    else
+        head = u & 0xFF800000u;                                        // +-2^(E-127)
+    const uint32_t idx = ((u >> (23 - m)) & ((1u << m) - 1u)) << shift;
+    return head | idx;
+}
+
+__device__ __forceinline__ float head_value(uint32_t w) { return __uint_as_float(w & kHeadMask); }
+
+__device__ __forceinline__ float table_value(uint32_t entry)
+{
+    return __uint_as_float((entry & 0x00FFFFFFu) + 0x3F800000u);
+}
+
+// One k-step of the register tile: acc[r][t] += amul(a_r, b_t) for TM lane rows and TN
+// wave-uniform columns.  `aw` are the lane's decoded first-operand words, `brow` points at
+// TN decoded second-operand words (uniform address -> scalar loads).
+template <int TM, int TN, bool LDS>
+__device__ __forceinline__ void amsim_mac(float (&acc)[TM][TN], const uint32_t (&aw)[TM],
+                                          const uint32_t *__restrict__ brow, const uint32_t *__restrict__ glut)
+{
+    extern __shared__ uint32_t lds_lut[];
+    uint32_t aoff[TM];
+    float pa[TM];
+#pragma unroll
+    for (int r = 0; r < TM; ++r) {
+        aoff[r] = aw[r] & kIdxMask;
+        pa[r] = head_value(aw[r]);
+    }
+#pragma unroll
+    for (int t = 0; t < TN; ++t) {
+        const uint32_t bw = brow[t];
+        const uint32_t boff = bw & kIdxMask;
+        const float pb = head_value(bw);
+#pragma unroll
+        for (int r = 0; r < TM; ++r) {
+            float v;
+            if constexpr (LDS)
+                v = *reinterpret_cast<const float *>(reinterpret_cast<const char *>(lds_lut) + (aoff[r] + boff));
+            else
+                v = table_value(glut[aoff[r] + boff]);
+            acc[r][t] = __builtin_fmaf(v, pa[r] * pb, acc[r][t]);
+        }
+    }
+}
+
+// Copy the prepared (transposed, rebiased) table into LDS.  entries is a multiple of 4.
+template <bool LDS>
+__device__ __forceinline__ void stage_table(const uint32_t *__restrict__ lut_t, int entries)
+{
+    if constexpr (LDS) {
+        extern __shared__ uint32_t lds_lut[];
+        const uint4 *src = reinterpret_cast<const uint4 *>(lut_t);
+        uint4 *dst = reinterpret_cast<uint4 *>(lds_lut);
+        for (int i = threadIdx.x; i < entries / 4; i += blockDim.x) dst[i] = src[i];
+        __syncthreads();
+    }
+}
+
+template <int TM, int TN>
+__device__ __forceinline__ void init_acc(float (&acc)[TM][TN])
+{
+#pragma unroll
+    for (int r = 0; r < TM; ++r)
+#pragma unroll
+        for (int t = 0; t < TN; ++t) acc[r][t] = -0.0f;
+}
+
+__device__ __forceinline__ int wave_id() { return __builtin_amdgcn_readfirstlane(threadIdx.x >> 6); }
+
+// ------------------------------------------------------------------ pre-pass kernels -----
+
+// Transposed, rebiased copy of the table: out[j * n + k] = (lut[k * n + j] & 0xFFFFFF) + 0x3F800000.
+__global__ void prep_table_kernel(const uint32_t *__restrict__ lut, uint32_t *__restrict__ out, int m)
+{
+    const int n = 1 << m;
+    const int total = n * n;
+    for (int i = blockIdx.x * blockDim.x + threadIdx.x; i < total; i += gridDim.x * blockDim.x) {
+        const int k = i / n, j = i % n;
+        out[j * n + k] = (lut[i] & 0x00FFFFFFu) + 0x3F800000u;
+    }
+}
+
+// dst[(b * rows + r) * dld + c] = decode(src[b * sb + r * sr + c * sc]) for r < rows, c < cols;
+// padding columns c in [cols, dld) are written as decoded +0.
+__global__ void decode_kernel(const float *__restrict__ src, int64_t sb, int64_t sr, int64_t sc, int batches,
+                              int rows, int cols, uint32_t *__restrict__ dst, int dld, int m, int shift)
+{
+    const int64_t per = int64_t(rows) * dld;
+    const int64_t total = per * batches;
+    for (int64_t i = int64_t(blockIdx.x) * blockDim.x + threadIdx.x; i < total;
+         i += int64_t(gridDim.x) * blockDim.x) {
+        const int b = int(i / per);
+        const int64_t rem = i - b * per;
+        const int r = int(rem / dld), c = int(rem % dld);
+        uint32_t w = 0u;
+        if (c < cols) w = amsim_decode(__float_as_uint(src[b * sb + int64_t(r) * sr + int64_t(c) * sc]), m, shift);
+        dst[i] = w;
+    }
+}
+
+// Tiled transpose-decode for the GEMM first operand: src is `rows x cols` with strides
+// (sr, sc); dst[c * dld + r] = decode(src(r, c)), rows padded to dld with decoded +0.
+__global__ __launch_bounds__(256) void decode_t_kernel(const float *__restrict__ src, int64_t sr, int64_t sc, int rows,
+                                                       int cols, uint32_t *__restrict__ dst, int dld, int m, int shift)
+{
+    __shared__ uint32_t tile[64][65];
+    const int r0 = blockIdx.x * 64;
+    const int tx = threadIdx.x & 63, ty = threadIdx.x >> 6;
+    for (int c0 = blockIdx.y * 64; c0 < cols; c0 += gridDim.y * 64) {
+        for (int i = ty; i < 64; i += 4) {
+            const int r = r0 + i, c = c0 + tx;
+            uint32_t w = 0u;
+            if (r < rows && c < cols) w = amsim_decode(__float_as_uint(src[int64_t(r) * sr + int64_t(c) * sc]), m, shift);
+            tile[i][tx] = w;
+        }
+        __syncthreads();
+        for (int i = ty; i < 64; i += 4) {
+            const int c = c0 + i, r = r0 + tx;
+            if (c < cols && r < dld) dst[int64_t(c) * dld + r] = tile[tx][i];
+        }
+        __syncthreads();
+    }
+}
+
+// C[r][c] = sum over z of part[z][r][c], z in order (deterministic).
+__global__ void reduce_splits_kernel(const float *__restrict__ part, int splits, int rows, int cols,
+                                     float *__restrict__ C, int64_t ldc)
+{
+    const int64_t total = int64_t(rows) * cols;
+    for (int64_t i = int64_t(blockIdx.x) * blockDim.x + threadIdx.x; i < total;
+         i += int64_t(gridDim.x) * blockDim.x) {
+        float s = part[i];
+        for (int z = 1; z < splits; ++z) s += part[int64_t(z) * total + i];
+        const int64_t r = i / cols, c = i % cols;
+        C[r * ldc + c] = s;
+    }
+}
+
+__global__ void fill_kernel(float *__restrict__ C, int rows, int cols, int64_t ldc, float v)
+{
+    const int64_t total = int64_t(rows) * cols;
+    for (int64_t i = int64_t(blockIdx.x) * blockDim.x + threadIdx.x; i < total;
+         i += int64_t(gridDim.x) * blockDim.x)
+        C[(i / cols) * ldc + (i % cols)] = v;
+}
+
+// Element-wise products through the same decode/combine path as the GEMM kernels, with the
+// table read from global memory in its canonical layout (index = ka * 2^M + kb).
+__global__ void mul_ew_kernel(int64_t n, const float *__restrict__ a, const float *__restrict__ b,
+                              float *__restrict__ c, const uint32_t *__restrict__ lut, int m)
+{
+    for (int64_t i = int64_t(blockIdx.x) * blockDim.x + threadIdx.x; i < n; i += int64_t(gridDim.x) * blockDim.x) {
+        const uint32_t wa = amsim_decode(__float_as_uint(a[i]), m, m);
+        const uint32_t wb = amsim_decode(__float_as_uint(b[i]), m, 0);
+        const float v = table_value(lut[(wa & kIdxMask) + (wb & kIdxMask)]);
+        c[i] = v * (head_value(wa) * head_value(wb));
+    }
+}
+
+// ------------------------------------------------------------------ GEMM kernel ---------
+// Ad: decoded op(A) stored k-major, Ad[k * Mp + i] (Mp = rows padded to the row tile).
+// Bd: decoded op(B) row-major, Bd[k * Np + j] (Np = columns padded to the column tile).
+// Split z of gridDim.z sums k in [z * kchunk, min(K, (z+1) * kchunk)).  out is C (ldc) when
+// gridDim.z == 1, else the split's slab of the partial-sum buffer (ld = N).
+template <int TM, int TN, bool LDS>
+__global__ __launch_bounds__(kThreads) void gemm_kernel(const uint32_t *__restrict__ Ad, int Mp,
+                                                        const uint32_t *__restrict__ Bd, int Np, int M, int N, int K,
+                                                        int kchunk, float *__restrict__ out, int64_t ldc,
+                                                        const uint32_t *__restrict__ lut, int entries)
+{
+    stage_table<LDS>(lut, entries);
+    const int lane = threadIdx.x & 63;
+    const int row0 = blockIdx.x * (64 * TM) + lane;
+    const int col0 = (blockIdx.y * kWaves + wave_id()) * TN;
+    const int kbeg = blockIdx.z * kchunk;
+    const int kend = min(K, kbeg + kchunk);
+    float acc[TM][TN];
+    init_acc(acc);
+    if (col0 < Np) {
+        for (int k = kbeg; k < kend; ++k) {
+            uint32_t aw[TM];
+#pragma unroll
+            for (int r = 0; r < TM; ++r) aw[r] = Ad[int64_t(k) * Mp + row0 + 64 * r];
+            amsim_mac<TM, TN, LDS>(acc, aw, Bd + int64_t(k) * Np + col0, lut);
+        }
+    }
+    float *dst = out;
+    int64_t ld = ldc;
+    if (gridDim.z > 1) {
+        dst = out + int64_t(blockIdx.z) * M * N;
+        ld = N;
+    }
+#pragma unroll
+    for (int r = 0; r < TM; ++r) {
+        const int row = row0 + 64 * r;
+        if (row >= M) continue;
+#pragma unroll
+        for (int t = 0; t < TN; ++t) {
+            const int col = col0 + t;
+            if (col < N) dst[int64_t(row) * ld + col] = acc[r][t];
+        }
+    }
+}
+
+// ------------------------------------------------------------------ convolution kernels --
+
+struct ConvShape {
+    int n, h, w, ci, co, kh, kw, sh, sw, pt, pl, oh, ow;
+};
+
+// Forward: rows (n, oh, ow) on lanes, columns co.  Xd: decoded x (NHWC, first-operand idx),
+// Wd: decoded w as [kh*kw*ci][COp].
+template <int TM, int TN, bool LDS>
+__global__ __launch_bounds__(kThreads) void conv_fwd_kernel(const uint32_t *__restrict__ Xd,
+                                                            const uint32_t *__restrict__ Wd, int COp, ConvShape s,
+                                                            float *__restrict__ y, const uint32_t *__restrict__ lut,
+                                                            int entries)
+{
+    stage_table<LDS>(lut, entries);
+    const int lane = threadIdx.x & 63;
+    const int rows = s.n * s.oh * s.ow;
+    const int row0 = blockIdx.x * (64 * TM) + lane;
+    const int col0 = (blockIdx.y * kWaves + wave_id()) * TN;
+    int xbase[TM], ih0[TM], iw0[TM];
+#pragma unroll
+    for (int r = 0; r < TM; ++r) {
+        const int row = row0 + 64 * r;
+        const int rr = row < rows ? row : rows - 1;
+        const int ow = rr % s.ow, oh = (rr / s.ow) % s.oh, n = rr / (s.ow * s.oh);
+        xbase[r] = n * s.h * s.w * s.ci;
+        ih0[r] = oh * s.sh - s.pt;
+        iw0[r] = ow * s.sw - s.pl;
+    }
+    float acc[TM][TN];
+    init_acc(acc);
+    if (col0 < COp) {
+        for (int kh = 0; kh < s.kh; ++kh) {
+            for (int kw = 0; kw < s.kw; ++kw) {
+                int pix[TM];
+#pragma unroll
+                for (int r = 0; r < TM; ++r) {
+                    const int ih = ih0[r] + kh, iw = iw0[r] + kw;
+                    const bool ok = unsigned(ih) < unsigned(s.h) && unsigned(iw) < unsigned(s.w);
+                    pix[r] = ok ? xbase[r] + (ih * s.w + iw) * s.ci : -1;
+                }
+                const uint32_t *brow = Wd + int64_t((kh * s.kw + kw) * s.ci) * COp + col0;
+                for (int c = 0; c < s.ci; ++c) {
+                    uint32_t aw[TM];
+#pragma unroll
+                    for (int r = 0; r < TM; ++r) aw[r] = pix[r] >= 0 ? Xd[pix[r] + c] : 0u;
+                    amsim_mac<TM, TN, LDS>(acc, aw, brow + int64_t(c) * COp, lut);
+                }
+            }
+        }
+    }
+#pragma unroll
+    for (int r = 0; r < TM; ++r) {
+        const int row = row0 + 64 * r;
+        if (row >= rows) continue;
+#pragma unroll
+        for (int t = 0; t < TN; ++t) {
+            const int col = col0 + t;
+            if (col < s.co) y[int64_t(row) * s.co + col] = acc[r][t];
+        }
+    }
+}
+
+// Backward-data, one stride phase (ph, pw) per blockIdx.z: rows (n, hq, wq) with
+// h = hq*sh + ph, w = wq*sw + pw on lanes, columns ci.  Only taps kh = ph + pt (mod sh) read a
+// real error element, at oh = hq + (ph + pt - kh) / sh (likewise w); the dilation zeros of
+// the other taps are never multiplied.  Dyd: decoded dy (NHWC), Wtd: decoded weights as
+// [kh][kw][co][CIp].
+template <int TM, int TN, bool LDS>
+__global__ __launch_bounds__(kThreads) void conv_bwd_data_kernel(const uint32_t *__restrict__ Dyd,
+                                                                 const uint32_t *__restrict__ Wtd, int CIp,
+                                                                 ConvShape s, float *__restrict__ dx,
+                                                                 const uint32_t *__restrict__ lut, int entries)
+{
+    stage_table<LDS>(lut, entries);
+    const int ph = blockIdx.z / s.sw, pw = blockIdx.z % s.sw;
+    const int hq_n = ph < s.h ? (s.h - ph + s.sh - 1) / s.sh : 0;
+    const int wq_n = pw < s.w ? (s.w - pw + s.sw - 1) / s.sw : 0;
+    const int rows = s.n * hq_n * wq_n;
+    if (int(blockIdx.x) * 64 * TM >= rows) return;  // uniform over the workgroup
+    const int lane = threadIdx.x & 63;
+    const int row0 = blockIdx.x * (64 * TM) + lane;
+    const int col0 = (blockIdx.y * kWaves + wave_id()) * TN;
+    int nb[TM], hq[TM], wq[TM];
+#pragma unroll
+    for (int r = 0; r < TM; ++r) {
+        const int row = row0 + 64 * r;
+        const int rr = row < rows ? row : rows - 1;
+        wq[r] = rr % wq_n;
+        hq[r] = (rr / wq_n) % hq_n;
+        nb[r] = rr / (wq_n * hq_n);
+    }
+    float acc[TM][TN];
+    init_acc(acc);
+    const int kh0 = (ph + s.pt) % s.sh, kw0 = (pw + s.pl) % s.sw;
+    if (col0 < CIp) {
+        for (int kh = kh0; kh < s.kh; kh += s.sh) {
+            const int dh = (ph + s.pt - kh) / s.sh;  // exact division
+            for (int kw = kw0; kw < s.kw; kw += s.sw) {
+                const int dw = (pw + s.pl - kw) / s.sw;
+                int pix[TM];
+#pragma unroll
+                for (int r = 0; r < TM; ++r) {
+                    const int oh = hq[r] + dh, ow = wq[r] + dw;
+                    const bool ok = unsigned(oh) < unsigned(s.oh) && unsigned(ow) < unsigned(s.ow);
+                    pix[r] = ok ? ((nb[r] * s.oh + oh) * s.ow + ow) * s.co : -1;
+                }
+                const uint32_t *brow = Wtd + int64_t((kh * s.kw + kw) * s.co) * CIp + col0;
+                for (int c = 0; c < s.co; ++c) {
+                    uint32_t aw[TM];
+#pragma unroll
+                    for (int r = 0; r < TM; ++r) aw[r] = pix[r] >= 0 ? Dyd[pix[r] + c] : 0u;
+                    amsim_mac<TM, TN, LDS>(acc, aw, brow + int64_t(c) * CIp, lut);
+                }
+            }
+        }
+    }
+#pragma unroll
+    for (int r = 0; r < TM; ++r) {
+        const int row = row0 + 64 * r;
+        if (row >= rows) continue;
+        const int h = hq[r] * s.sh + ph, w = wq[r] * s.sw + pw;
+        const int64_t base = (int64_t(nb[r] * s.h + h) * s.w + w) * s.ci;
+#pragma unroll
+        for (int t = 0; t < TN; ++t) {
+            const int col = col0 + t;
+            if (col < s.ci) dx[base + col] = acc[r][t];
+        }
+    }
+}
+
+// Backward-weight: rows (kh, kw, ci) on lanes, columns co, reduction over (n, oh, ow) split
+// into chunks of whole output rows (n, oh) across blockIdx.z.  Xd: decoded x (NHWC),
+// Dyd: decoded dy as [n*oh*ow][COp].  out: dw (split == 1) or the split's partial slab.
+template <int TM, int TN, bool LDS>
+__global__ __launch_bounds__(kThreads) void conv_bwd_weight_kernel(const uint32_t *__restrict__ Xd,
+                                                                   const uint32_t *__restrict__ Dyd, int COp,
+                                                                   ConvShape s, int rows_per_split,
+                                                                   float *__restrict__ out,
+                                                                   const uint32_t *__restrict__ lut, int entries)
+{
+    stage_table<LDS>(lut, entries);
+    const int lane = threadIdx.x & 63;
+    const int R = s.kh * s.kw * s.ci;
+    const int row0 = blockIdx.x * (64 * TM) + lane;
+    const int col0 = (blockIdx.y * kWaves + wave_id()) * TN;
+    int tkh[TM], tkw[TM], tci[TM];
+#pragma unroll
+    for (int r = 0; r < TM; ++r) {
+        const int row = row0 + 64 * r;
+        const int rr = row < R ? row : R - 1;
+        tci[r] = rr % s.ci;
+        tkw[r] = (rr / s.ci) % s.kw;
+        tkh[r] = rr / (s.ci * s.kw);
+    }
+    float acc[TM][TN];
+    init_acc(acc);
+    const int nrows = s.n * s.oh;  // (n, oh) output rows
+    const int rbeg = blockIdx.z * rows_per_split;
+    const int rend = min(nrows, rbeg + rows_per_split);
+    if (col0 < COp) {
+        for (int orow = rbeg; orow < rend; ++orow) {
+            const int n = orow / s.oh, oh = orow % s.oh;
+            int hbase[TM];
+#pragma unroll
+            for (int r = 0; r < TM; ++r) {
+                const int ih = oh * s.sh + tkh[r] - s.pt;
+                hbase[r] = unsigned(ih) < unsigned(s.h) ? (n * s.h + ih) * s.w : -1;
+            }
+            const uint32_t *brow = Dyd + int64_t(orow) * s.ow * COp + col0;
+            for (int ow = 0; ow < s.ow; ++ow) {
+                uint32_t aw[TM];
+#pragma unroll
+                for (int r = 0; r < TM; ++r) {
+                    const int iw = ow * s.sw + tkw[r] - s.pl;
+                    const bool ok = hbase[r] >= 0 && unsigned(iw) < unsigned(s.w);
+                    aw[r] = ok ? Xd[(hbase[r] + iw) * s.ci + tci[r]] : 0u;
+                }
+                amsim_mac<TM, TN, LDS>(acc, aw, brow + int64_t(ow) * COp, lut);
+            }
+        }
+    }
+    float *dst = out + int64_t(blockIdx.z) * R * s.co;
+#pragma unroll
+    for (int r = 0; r < TM; ++r) {
+        const int row = row0 + 64 * r;
+        if (row >= R) continue;
+#pragma unroll
+        for (int t = 0; t < TN; ++t) {
+            const int col = col0 + t;
+            if (col < s.co) dst[int64_t(row) * s.co + col] = acc[r][t];
+        }
+    }
+}
+
+// ------------------------------------------------------------------ host dispatch -------
+
+constexpr size_t kAlign = 256;
+
+inline size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
+inline int64_t round_up(int64_t x, int64_t m) { return (x + m - 1) / m * m; }
+inline int64_t ceil_div(int64_t x, int64_t m) { return (x + m - 1) / m; }
+
+inline bool lds_path(int m_bits) { return m_bits <= kMaxLdsBits; }
+inline size_t table_bytes(int m_bits) { return size_t(4) << (2 * m_bits); }
+
+// Tile choice: TN = 16 uniform columns per wave for wide outputs, 4 for narrow ones; TM the
+// largest of 8/4/2/1 that still gives at least two workgroups per CU (or the smallest when
+// the problem is small).  Split the reduction when the tile grid is too small to fill the
+// chip and the reduction is long.
+struct Tile {
+    int tm, tn, split;
+};
+
+constexpr int kTargetWgs = 512;  // 256 CUs x 2 workgroups (LDS: 2 x 64 KiB tables per CU)
+
+Tile choose_tile(int64_t rows, int64_t cols, int64_t red, int64_t red_unit, bool allow_split)
+{
+    Tile t;
+    t.tn = cols > 8 ? 16 : 4;
+    const int64_t col_tiles = ceil_div(cols, int64_t(t.tn) * kWaves);
+    t.tm = 1;
+    for (int tm : {8, 4, 2}) {
+        if (ceil_div(rows, 64 * tm) * col_tiles >= kTargetWgs) {
+            t.tm = tm;
+            break;
+        }
+    }
+    t.split = 1;
+    if (allow_split) {
+        const int64_t tiles = ceil_div(rows, 64 * t.tm) * col_tiles;
+        // keep at least ~1024 products per lane per split
+        const int64_t max_split = std::max<int64_t>(1, red / std::max<int64_t>(1, 1024 / std::max<int64_t>(1, red_unit)));
+        if (tiles < kTargetWgs) t.split = int(std::min<int64_t>(ceil_div(kTargetWgs, tiles), max_split));
+        t.split = std::max(1, std::min(t.split, 1024));
+    }
+    return t;
+}
+
+std::once_flag g_attr_once;
+hipError_t g_attr_err = hipSuccess;
+
+template <typename K>
+void allow_big_lds(K kernel)
+{
+    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void *>(kernel),
+                                       hipFuncAttributeMaxDynamicSharedMemorySize, int(table_bytes(kMaxLdsBits)));
+    if (e != hipSuccess) g_attr_err = e;
+}
+
+#define AMSIM_FOR_TILES(X)                                                                                   \
+    X(8, 16) X(4, 16) X(2, 16) X(1, 16) X(8, 4) X(4, 4) X(2, 4) X(1, 4)
+
+void set_attributes()
+{
+#define X(TM, TN)                                          \
+    allow_big_lds(gemm_kernel<TM, TN, true>);              \
+    allow_big_lds(conv_fwd_kernel<TM, TN, true>);          \
+    allow_big_lds(conv_bwd_data_kernel<TM, TN, true>);     \
+    allow_big_lds(conv_bwd_weight_kernel<TM, TN, true>);
+    AMSIM_FOR_TILES(X)
+#undef X
+}
+
+int ensure_attributes()
+{
+    std::call_once(g_attr_once, set_attributes);
+    return g_attr_err == hipSuccess ? AMSIM_OK : AMSIM_ERR_HIP;
+}
+
+int launch_status()
+{
+    return hipGetLastError() == hipSuccess ? AMSIM_OK : AMSIM_ERR_HIP;
+}
+
+inline int grid_for(int64_t total, int block = 256)
+{
+    return int(std::max<int64_t>(1, std::min<int64_t>(ceil_div(total, block), 8192)));
+}
+
+// Workspace layout shared by the size queries and the launches.
+struct Plan {
+    Tile tile;
+    bool lds;
+    size_t off_table, off_a, off_b, off_part, total;
+    int64_t a_ld, b_ld;  // padded leading dims of the decoded operands
+};
+
+bool valid_m(int m_bits) { return m_bits >= 1 && m_bits <= 11; }
+
+Plan plan_gemm(int64_t m, int64_t n, int64_t k, int m_bits)
+{
+    Plan p{};
+    p.tile = choose_tile(m, n, k, 1, true);
+    p.lds = lds_path(m_bits);
+    p.a_ld = round_up(m, 64 * p.tile.tm);
+    p.b_ld = round_up(n, int64_t(p.tile.tn) * kWaves);
+    size_t o = 0;
+    p.off_table = o;
+    if (p.lds) o += align_up(table_bytes(m_bits));
+    p.off_a = o;
+    o += align_up(size_t(k) * p.a_ld * 4);
+    p.off_b = o;
+    o += align_up(size_t(k) * p.b_ld * 4);
+    p.off_part = o;
+    if (p.tile.split > 1) o += align_up(size_t(p.tile.split) * m * n * 4);
+    p.total = o;
+    return p;
+}
+
+ConvShape shape_of(const amsim_conv2d *d)
+{
+    ConvShape s;
+    s.n = d->n; s.h = d->h; s.w = d->w; s.ci = d->c_in; s.co = d->c_out; s.kh = d->kh; s.kw = d->kw;
+    s.sh = d->stride_h; s.sw = d->stride_w; s.pt = d->pad_top; s.pl = d->pad_left;
+    s.oh = (d->h + d->pad_top + d->pad_bottom - d->kh) / d->stride_h + 1;
+    s.ow = (d->w + d->pad_left + d->pad_right - d->kw) / d->stride_w + 1;
+    return s;
+}
+
+int check_conv(const amsim_conv2d *d)
+{
+    if (!d) return AMSIM_ERR_INVALID_ARG;
+    if (d->n < 1 || d->h < 1 || d->w < 1 || d->c_in < 1 || d->c_out < 1 || d->kh < 1 || d->kw < 1 ||
+        d->stride_h < 1 || d->stride_w < 1 || d->pad_top < 0 || d->pad_bottom < 0 || d->pad_left < 0 ||
+        d->pad_right < 0)
+        return AMSIM_ERR_INVALID_ARG;
+    const int64_t hp = int64_t(d->h) + d->pad_top + d->pad_bottom, wp = int64_t(d->w) + d->pad_left + d->pad_right;
+    if (hp < d->kh || wp < d->kw) return AMSIM_ERR_INVALID_ARG;
+    const int64_t oh = (hp - d->kh) / d->stride_h + 1, ow = (wp - d->kw) / d->stride_w + 1;
+    const int64_t lim = int64_t(1) << 31;
+    const int64_t x = int64_t(d->n) * d->h * d->w * d->c_in;
+    const int64_t y = int64_t(d->n) * oh * ow * d->c_out;
+    const int64_t w = int64_t(d->kh) * d->kw * d->c_in * d->c_out;
+    if (x >= lim || y >= lim || w >= lim || int64_t(d->kh) * d->kw * d->c_out * (d->c_in + 64) >= lim ||
+        int64_t(d->n) * oh * ow * (d->c_out + 64) >= lim || int64_t(d->kh) * d->kw * d->c_in * (d->c_out + 64) >= lim ||
+        d->pad_top >= d->kh + d->stride_h * 4096 || d->pad_left >= d->kw + d->stride_w * 4096 ||
+        int64_t(d->stride_h) * d->stride_w > 65535 || d->c_in > 65535 * 64 || d->c_out > 65535 * 64)
+        return AMSIM_ERR_UNSUPPORTED;
+    return AMSIM_OK;
+}
+
+Plan plan_conv(const amsim_conv2d *d, int pass, int m_bits)
+{
+    const ConvShape s = shape_of(d);
+    Plan p{};
+    p.lds = lds_path(m_bits);
+    size_t o = 0;
+    p.off_table = o;
+    if (p.lds) o += align_up(table_bytes(m_bits));
+    const int64_t npix_in = int64_t(s.n) * s.h * s.w, npix_out = int64_t(s.n) * s.oh * s.ow;
+    if (pass == AMSIM_CONV_FWD) {
+        p.tile = choose_tile(npix_out, s.co, 1, 1, false);
+        p.b_ld = round_up(s.co, int64_t(p.tile.tn) * kWaves);
+        p.off_a = o;  // decoded x
+        o += align_up(size_t(npix_in) * s.ci * 4);
+        p.off_b = o;  // decoded w [kh*kw*ci][COp]
+        o += align_up(size_t(s.kh) * s.kw * s.ci * p.b_ld * 4);
+    } else if (pass == AMSIM_CONV_BWD_DATA) {
+        const int64_t rows = s.n * ceil_div(s.h, s.sh) * ceil_div(s.w, s.sw);
+        p.tile = choose_tile(rows, s.ci, 1, 1, false);
+        p.b_ld = round_up(s.ci, int64_t(p.tile.tn) * kWaves);
+        p.off_a = o;  // decoded dy
+        o += align_up(size_t(npix_out) * s.co * 4);
+        p.off_b = o;  // decoded w^T [kh][kw][co][CIp]
+        o += align_up(size_t(s.kh) * s.kw * s.co * p.b_ld * 4);
+    } else {
+        const int64_t R = int64_t(s.kh) * s.kw * s.ci;
+        p.tile = choose_tile(R, s.co, int64_t(s.n) * s.oh, s.ow, true);
+        p.b_ld = round_up(s.co, int64_t(p.tile.tn) * kWaves);
+        p.off_a = o;  // decoded x
+        o += align_up(size_t(npix_in) * s.ci * 4);
+        p.off_b = o;  // decoded dy [n*oh*ow][COp]
+        o += align_up(size_t(npix_out) * p.b_ld * 4);
+        p.off_part = o;
+        if (p.tile.split > 1) o += align_up(size_t(p.tile.split) * R * s.co * 4);
+    }
+    p.total = o;
+    return p;
+}
+
+int prep_table(const uint32_t *lut, int m_bits, char *ws, const Plan &p, hipStream_t st, const uint32_t **table)
+{
+    if (p.lds) {
+        uint32_t *t = reinterpret_cast<uint32_t *>(ws + p.off_table);
+        hipLaunchKernelGGL(prep_table_kernel, dim3(grid_for(int64_t(1) << (2 * m_bits))), dim3(256), 0, st, lut, t,
+                           m_bits);
+        *table = t;
+    } else {
+        *table = lut;
+    }
+    return launch_status();
+}
+
+// Shift of the decoded index field: the lane (first) operand carries ka, the uniform (second)
+// operand kb.  LDS: byte offset into the transposed table (kb * 2^M + ka) * 4.  Global: entry
+// index into the canonical table ka * 2^M + kb.
+inline int shift_first(int m_bits) { return lds_path(m_bits) ? 2 : m_bits; }
+inline int shift_second(int m_bits) { return lds_path(m_bits) ? m_bits + 2 : 0; }
+
+template <int TM, int TN, bool LDS>
+void launch_gemm_t(dim3 grid, hipStream_t st, const uint32_t *Ad, int Mp, const uint32_t *Bd, int Np, int M, int N,
+                   int K, int kchunk, float *out, int64_t ldc, const uint32_t *table, int m_bits)
+{
+    const int entries = 1 << (2 * m_bits);
+    const size_t lds = LDS ? size_t(entries) * 4 : 0;
+    hipLaunchKernelGGL((gemm_kernel<TM, TN, LDS>), grid, dim3(kThreads), lds, st, Ad, Mp, Bd, Np, M, N, K, kchunk,
+                       out, ldc, table, entries);
+}
+
+template <bool LDS, typename F>
+void dispatch_tile(const Tile &t, F &&f)
+{
+    // f is a generic lambda taking std::integral_constant-like tags
+#define X(TM, TN)                                                  \
+    if (t.tm == TM && t.tn == TN) {                                \
+        f(std::integral_constant<int, TM>{}, std::integral_constant<int, TN>{}); \
+        return;                                                    \
+    }
+    AMSIM_FOR_TILES(X)
+#undef X
+}
+
+}  // namespace
+
+// ==================================================================== C entry points =====
+
+extern "C" {
+
+int amsim_gemm_workspace_size(int trans_a, int trans_b, int64_t m, int64_t n, int64_t k, int m_bits, size_t *bytes)
+{
+    (void)trans_a;
+    (void)trans_b;
+    if (!bytes) return AMSIM_ERR_INVALID_ARG;
+    if (!valid_m(m_bits)) return AMSIM_ERR_UNSUPPORTED;
+    if (m < 0 || n < 0 || k < 0) return AMSIM_ERR_INVALID_ARG;
+    if (m == 0 || n == 0 || k == 0) {
+        *bytes = 0;
+        return AMSIM_OK;
+    }
+    const Plan p = plan_gemm(m, n, k, m_bits);
+    *bytes = p.total;
+    return AMSIM_OK;
+}
+
+int approx_gemm(int trans_a, int trans_b, int64_t m, int64_t n, int64_t k, const float *A, int64_t lda,
+                const float *B, int64_t ldb, float *C, int64_t ldc, const uint32_t *lut, int m_bits, void *workspace,
+                size_t workspace_bytes, void *stream)
+{
+    if (!valid_m(m_bits)) return AMSIM_ERR_UNSUPPORTED;
+    if (m < 0 || n < 0 || k < 0) return AMSIM_ERR_INVALID_ARG;
+    if (m == 0 || n == 0) return AMSIM_OK;
+    if (!C || ldc < n) return AMSIM_ERR_INVALID_ARG;
+    const int64_t lim = int64_t(1) << 31;
+    if (m >= lim || n >= lim || k >= lim) return AMSIM_ERR_UNSUPPORTED;
+    hipStream_t st = static_cast<hipStream_t>(stream);
+    if (k == 0) {
+        hipLaunchKernelGGL(fill_kernel, dim3(grid_for(m * n)), dim3(256), 0, st, C, int(m), int(n), ldc, -0.0f);
+        return launch_status();
+    }
+    if (!A || !B || !lut) return AMSIM_ERR_INVALID_ARG;
+    if (lda < (trans_a ? m : k) || ldb < (trans_b ? k : n)) return AMSIM_ERR_INVALID_ARG;
+    const Plan p = plan_gemm(m, n, k, m_bits);
+    if (k * p.a_ld >= lim || k * p.b_ld >= lim || int64_t(p.tile.split) * m * n >= lim ||
+        p.b_ld / (int64_t(p.tile.tn) * kWaves) > 65535)
+        return AMSIM_ERR_UNSUPPORTED;
+    if (p.total > 0 && (!workspace || workspace_bytes < p.total)) return AMSIM_ERR_WORKSPACE;
+    if (p.lds && ensure_attributes() != AMSIM_OK) return AMSIM_ERR_HIP;
+    char *ws = static_cast<char *>(workspace);
+    const uint32_t *table;
+    if (prep_table(lut, m_bits, ws, p, st, &table) != AMSIM_OK) return AMSIM_ERR_HIP;
+
+    uint32_t *Ad = reinterpret_cast<uint32_t *>(ws + p.off_a);
+    uint32_t *Bd = reinterpret_cast<uint32_t *>(ws + p.off_b);
+    // op(A)(i, kk): row stride / column stride in A's storage
+    const int64_t a_sr = trans_a ? 1 : lda, a_sc = trans_a ? lda : 1;
+    hipLaunchKernelGGL(decode_t_kernel, dim3(unsigned(ceil_div(p.a_ld, 64)), unsigned(std::min<int64_t>(ceil_div(k, 64), 4096))), dim3(256), 0,
+                       st, A, a_sr, a_sc, int(m), int(k), Ad, int(p.a_ld), m_bits, shift_first(m_bits));
+    const int64_t b_sr = trans_b ? 1 : ldb, b_sc = trans_b ? ldb : 1;
+    hipLaunchKernelGGL(decode_kernel, dim3(grid_for(k * p.b_ld)), dim3(256), 0, st, B, int64_t(0), b_sr, b_sc, 1,
+                       int(k), int(n), Bd, int(p.b_ld), m_bits, shift_second(m_bits));
+    if (launch_status() != AMSIM_OK) return AMSIM_ERR_HIP;
+
+    const Tile t = p.tile;
+    const int kchunk = int(ceil_div(k, t.split));
+    const int splits = int(ceil_div(k, kchunk));
+    dim3 grid(unsigned(p.a_ld / (64 * t.tm)), unsigned(p.b_ld / (int64_t(t.tn) * kWaves)), unsigned(splits));
+    float *out = splits > 1 ? reinterpret_cast<float *>(ws + p.off_part) : C;
+    auto run = [&](auto tm, auto tn) {
+        if (p.lds)
+            launch_gemm_t<decltype(tm)::value, decltype(tn)::value, true>(grid, st, Ad, int(p.a_ld), Bd, int(p.b_ld),
+                                                                          int(m), int(n), int(k), kchunk, out, ldc,
+                                                                          table, m_bits);
+        else
+            launch_gemm_t<decltype(tm)::value, decltype(tn)::value, false>(grid, st, Ad, int(p.a_ld), Bd, int(p.b_ld),
+                                                                           int(m), int(n), int(k), kchunk, out, ldc,
+                                                                           table, m_bits);
+    };
+    dispatch_tile<true>(t, run);
+    if (launch_status() != AMSIM_OK) return AMSIM_ERR_HIP;
+    if (splits > 1) {
+        hipLaunchKernelGGL(reduce_splits_kernel, dim3(grid_for(m * n)), dim3(256), 0, st,
+                           reinterpret_cast<const float *>(ws + p.off_part), splits, int(m), int(n), C, ldc);
+        if (launch_status() != AMSIM_OK) return AMSIM_ERR_HIP;
+    }
+    return AMSIM_OK;
+}
+
+int amsim_conv2d_workspace_size(const amsim_conv2d *desc, int pass, int m_bits, size_t *bytes)
+{
+    if (!bytes) return AMSIM_ERR_INVALID_ARG;
+    if (!valid_m(m_bits)) return AMSIM_ERR_UNSUPPORTED;
+    if (pass < AMSIM_CONV_FWD || pass > AMSIM_CONV_BWD_WEIGHT) return AMSIM_ERR_INVALID_ARG;
+    const int rc = check_conv(desc);
+    if (rc != AMSIM_OK) return rc;
+    *bytes = plan_conv(desc, pass, m_bits).total;
+    return AMSIM_OK;
+}
+
+static int conv_common(const amsim_conv2d *desc, int pass, const void *in0, const void *in1, void *out,
+                       const uint32_t *lut, int m_bits, void *workspace, size_t workspace_bytes, Plan *p)
+{
+    if (!valid_m(m_bits)) return AMSIM_ERR_UNSUPPORTED;
+    const int rc = check_conv(desc);
+    if (rc != AMSIM_OK) return rc;
+    if (!in0 || !in1 || !out || !lut) return AMSIM_ERR_INVALID_ARG;
+    *p = plan_conv(desc, pass, m_bits);
+    if (p->total > 0 && (!workspace || workspace_bytes < p->total)) return AMSIM_ERR_WORKSPACE;
+    if (p->lds && ensure_attributes() != AMSIM_OK) return AMSIM_ERR_HIP;
+    return AMSIM_OK;
+}
+
+int approx_conv2d_fwd(const amsim_conv2d *desc, const float *x, const float *w, float *y, const uint32_t *lut,
+                      int m_bits, void *workspace, size_t workspace_bytes, void *stream)
+{
+    Plan p;
+    int rc = conv_common(desc, AMSIM_CONV_FWD, x, w, y, lut, m_bits, workspace, workspace_bytes, &p);
+    if (rc != AMSIM_OK) return rc;
+    hipStream_t st = static_cast<hipStream_t>(stream);
+    const ConvShape s = shape_of(desc);
+    char *ws = static_cast<char *>(workspace);
+    const uint32_t *table;
+    if (prep_table(lut, m_bits, ws, p, st, &table) != AMSIM_OK) return AMSIM_ERR_HIP;
+    uint32_t *Xd = reinterpret_cast<uint32_t *>(ws + p.off_a);
+    uint32_t *Wd = reinterpret_cast<uint32_t *>(ws + p.off_b);
+    const int64_t nx = int64_t(s.n) * s.h * s.w * s.ci;
+    hipLaunchKernelGGL(decode_kernel, dim3(grid_for(nx)), dim3(256), 0, st, x, int64_t(0), int64_t(s.ci), int64_t(1), 1,
+                       int(nx / s.ci), s.ci, Xd, s.ci, m_bits, shift_first(m_bits));
+    const int kk = s.kh * s.kw * s.ci;
+    hipLaunchKernelGGL(decode_kernel, dim3(grid_for(int64_t(kk) * p.b_ld)), dim3(256), 0, st, w, int64_t(0),
+                       int64_t(s.co), int64_t(1), 1, kk, s.co, Wd, int(p.b_ld), m_bits, shift_second(m_bits));
+    if (launch_status() != AMSIM_OK) return AMSIM_ERR_HIP;
+    const Tile t = p.tile;
+    const int64_t rows = int64_t(s.n) * s.oh * s.ow;
+    dim3 grid(unsigned(ceil_div(rows, 64 * t.tm)), unsigned(p.b_ld / (int64_t(t.tn) * kWaves)), 1);
+    const int entries = 1 << (2 * m_bits);
+    auto run = [&](auto tm, auto tn) {
+        constexpr int TM = decltype(tm)::value, TN = decltype(tn)::value;
+        if (p.lds)
+            hipLaunchKernelGGL((conv_fwd_kernel<TM, TN, true>), grid, dim3(kThreads), size_t(entries) * 4, st, Xd, Wd,
+                               int(p.b_ld), s, y, table, entries);
+        else
+            hipLaunchKernelGGL((conv_fwd_kernel<TM, TN, false>), grid, dim3(kThreads), 0, st, Xd, Wd, int(p.b_ld), s,
+                               y, table, entries);
+    };
+    dispatch_tile<true>(t, run);
+    return launch_status();
+}
+
+int approx_conv2d_bwd_data(const amsim_conv2d *desc, const float *dy, const float *w, float *dx,
+                           const uint32_t *lut, int m_bits, void *workspace, size_t workspace_bytes, void *stream)
+{
+    Plan p;
+    int rc = conv_common(desc, AMSIM_CONV_BWD_DATA, dy, w, dx, lut, m_bits, workspace, workspace_bytes, &p);
+    if (rc != AMSIM_OK) return rc;
+    hipStream_t st = static_cast<hipStream_t>(stream);
+    const ConvShape s = shape_of(desc);
+    char *ws = static_cast<char *>(workspace);
+    const uint32_t *table;
+    if (prep_table(lut, m_bits, ws, p, st, &table) != AMSIM_OK) return AMSIM_ERR_HIP;
+    uint32_t *Dyd = reinterpret_cast<uint32_t *>(ws + p.off_a);
+    uint32_t *Wtd = reinterpret_cast<uint32_t *>(ws + p.off_b);
+    const int64_t ndy = int64_t(s.n) * s.oh * s.ow * s.co;
+    hipLaunchKernelGGL(decode_kernel, dim3(grid_for(ndy)), dim3(256), 0, st, dy, int64_t(0), int64_t(s.co), int64_t(1),
+                       1, int(ndy / s.co), s.co, Dyd, s.co, m_bits, shift_first(m_bits));
+    // w[kh][kw][ci][co] -> Wt[kh][kw][co][ci]: batches (kh,kw), rows co, cols ci
+    hipLaunchKernelGGL(decode_kernel, dim3(grid_for(int64_t(s.kh) * s.kw * s.co * p.b_ld)), dim3(256), 0, st, w,
+                       int64_t(s.ci) * s.co, int64_t(1), int64_t(s.co), s.kh * s.kw, s.co, s.ci, Wtd, int(p.b_ld),
+                       m_bits, shift_second(m_bits));
+    if (launch_status() != AMSIM_OK) return AMSIM_ERR_HIP;
+    const Tile t = p.tile;
+    const int64_t rows = int64_t(s.n) * ceil_div(s.h, s.sh) * ceil_div(s.w, s.sw);  // largest phase
+    dim3 grid(unsigned(ceil_div(rows, 64 * t.tm)), unsigned(p.b_ld / (int64_t(t.tn) * kWaves)),
+              unsigned(s.sh * s.sw));
+    const int entries = 1 << (2 * m_bits);
+    auto run = [&](auto tm, auto tn) {
+        constexpr int TM = decltype(tm)::value, TN = decltype(tn)::value;
+        if (p.lds)
+            hipLaunchKernelGGL((conv_bwd_data_kernel<TM, TN, true>), grid, dim3(kThreads), size_t(entries) * 4, st,
+                               Dyd, Wtd, int(p.b_ld), s, dx, table, entries);
+        else
+            hipLaunchKernelGGL((conv_bwd_data_kernel<TM, TN, false>), grid, dim3(kThreads), 0, st, Dyd, Wtd,
+                               int(p.b_ld), s, dx, table, entries);
+    };
+    dispatch_tile<true>(t, run);
+    return launch_status();
+}
+
+int approx_conv2d_bwd_weight(const amsim_conv2d *desc, const float *x, const float *dy, float *dw,
+                             const uint32_t *lut, int m_bits, void *workspace, size_t workspace_bytes, void *stream)
+{
+    Plan p;
+    int rc = conv_common(desc, AMSIM_CONV_BWD_WEIGHT, x, dy, dw, lut, m_bits, workspace, workspace_bytes, &p);
+    if (rc != AMSIM_OK) return rc;
+    hipStream_t st = static_cast<hipStream_t>(stream);
+    const ConvShape s = shape_of(desc);
+    char *ws = static_cast<char *>(workspace);
+    const uint32_t *table;
+    if (prep_table(lut, m_bits, ws, p, st, &table) != AMSIM_OK) return AMSIM_ERR_HIP;
+    uint32_t *Xd = reinterpret_cast<uint32_t *>(ws + p.off_a);
+    uint32_t *Dyd = reinterpret_cast<uint32_t *>(ws + p.off_b);
+    const int64_t nx = int64_t(s.n) * s.h * s.w * s.ci;
+    hipLaunchKernelGGL(decode_kernel, dim3(grid_for(nx)), dim3(256), 0, st, x, int64_t(0), int64_t(s.ci), int64_t(1), 1,
+                       int(nx / s.ci), s.ci, Xd, s.ci, m_bits, shift_first(m_bits));
+    const int64_t npo = int64_t(s.n) * s.oh * s.ow;
+    hipLaunchKernelGGL(decode_kernel, dim3(grid_for(npo * p.b_ld)), dim3(256), 0, st, dy, int64_t(0), int64_t(s.co),
+                       int64_t(1), 1, int(npo), s.co, Dyd, int(p.b_ld), m_bits, shift_second(m_bits));
+    if (launch_status() != AMSIM_OK) return AMSIM_ERR_HIP;
+    const Tile t = p.tile;
+    const int R = s.kh * s.kw * s.ci;
+    const int nrows = s.n * s.oh;
+    const int per = int(ceil_div(nrows, t.split));
+    const int splits = int(ceil_div(nrows, per));
+    dim3 grid(unsigned(ceil_div(R, 64 * t.tm)), unsigned(p.b_ld / (int64_t(t.tn) * kWaves)), unsigned(splits));
+    float *out = splits > 1 ? reinterpret_cast<float *>(ws + p.off_part) : dw;
+    const int entries = 1 << (2 * m_bits);
+    auto run = [&](auto tm, auto tn) {
+        constexpr int TM = decltype(tm)::value, TN = decltype(tn)::value;
+        if (p.lds)
+            hipLaunchKernelGGL((conv_bwd_weight_kernel<TM, TN, true>), grid, dim3(kThreads), size_t(entries) * 4, st,
+                               Xd, Dyd, int(p.b_ld), s, per, out, table, entries);
+        else
+            hipLaunchKernelGGL((conv_bwd_weight_kernel<TM, TN, false>), grid, dim3(kThreads), 0, st, Xd, Dyd,
+                               int(p.b_ld), s, per, out, table, entries);
+    };
+    dispatch_tile<true>(t, run);
+    if (launch_status() != AMSIM_OK) return AMSIM_ERR_HIP;
+    if (splits > 1) {
+        hipLaunchKernelGGL(reduce_splits_kernel, dim3(grid_for(int64_t(R) * s.co)), dim3(256), 0, st,
+                           reinterpret_cast<const float *>(ws + p.off_part), splits, R, s.co, dw, int64_t(s.co));
+        return launch_status();
+    }
+    return AMSIM_OK;
+}
+
+int approx_mul_ew(int64_t n, const float *a, const float *b, float *c, const uint32_t *lut, int m_bits, void *stream)
+{
+    if (!valid_m(m_bits)) return AMSIM_ERR_UNSUPPORTED;
+    if (n < 0) return AMSIM_ERR_INVALID_ARG;
+    if (n == 0) return AMSIM_OK;
+    if (!a || !b || !c || !lut) return AMSIM_ERR_INVALID_ARG;
+    hipStream_t st = static_cast<hipStream_t>(stream);
+    hipLaunchKernelGGL(mul_ew_kernel, dim3(grid_for(n)), dim3(256), 0, st, n, a, b, c, lut, m_bits);
+    return launch_status();
+}
+
+}  // extern "C"

@@ -1,0 +1,375 @@
+"""GPU parity: the HIP path through the C ABI against the CPU oracle.
+
+Products are compared bit for bit (element-wise routine; GEMM/conv shapes whose every output
+is a single product); sums within 1e-5 * sum|p| + 2^-126 per output.  Small shapes are compared
+on every output; the full-size workloads on seeded samples of outputs that the oracle
+computes one by one, in the same launch configuration the benchmark times.
+"""
+import numpy as np
+import pytest
+
+import oracle
+from cases import mantissa_pairs_grid, outer_operands, random_bits, special_cross
+from parity import assert_bits_equal, assert_within_tolerance
+from paper_2209_04161_amd import workloads as W
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+
+MODELS = {"mitchell": oracle.MITCHELL, "exact_trunc": oracle.EXACT_TRUNC}
+
+
+@pytest.fixture(scope="module")
+def B():
+    from paper_2209_04161_amd import binding
+    binding.lib()
+    return binding
+
+
+_LUTS = {}
+
+
+def dev_lut(B, model, m):
+    key = (model, m)
+    if key not in _LUTS:
+        _LUTS[key] = B.device_lut(B.lut_build(m, model))
+    return _LUTS[key]
+
+
+def cuda(x):
+    return torch.from_numpy(np.ascontiguousarray(x)).cuda()
+
+
+def host(t):
+    torch.cuda.synchronize()
+    return t.cpu().numpy()
+
+
+# ------------------------------------------------------------------ single products ------
+
+@pytest.mark.parametrize("model", ["mitchell", "exact_trunc"])
+@pytest.mark.parametrize("m", [1, 4, 7])
+def test_mul_ew_every_mantissa_pair(B, model, m):
+    a, b = mantissa_pairs_grid(m, seed=m)
+    sa, sb = special_cross()
+    a = np.concatenate([a, sa])
+    b = np.concatenate([b, sb])
+    got = host(B.approx_mul_ew(cuda(a), cuda(b), dev_lut(B, model, m), m))
+    assert_bits_equal(got, oracle.mul(MODELS[model], m, a, b), "mul_ew %s M=%d" % (model, m))
+
+
+@pytest.mark.parametrize("model", ["mitchell", "exact_trunc"])
+@pytest.mark.parametrize("m", [8, 11])
+def test_mul_ew_wide_tables_random_bits(B, model, m):
+    a = random_bits(1 << 21, 100 + m)
+    b = random_bits(1 << 21, 200 + m)
+    sa, sb = special_cross()
+    a = np.concatenate([a, sa])
+    b = np.concatenate([b, sb])
+    got = host(B.approx_mul_ew(cuda(a), cuda(b), dev_lut(B, model, m), m))
+    assert_bits_equal(got, oracle.mul(MODELS[model], m, a, b), "mul_ew %s M=%d" % (model, m))
+
+
+@pytest.mark.parametrize("m", [1, 5, 7, 9, 11])
+def test_gemm_k1_products_bit_exact(B, m):
+    """K = 1: every output is one product (sum starts at -0.0), through the full GEMM kernel."""
+    a, b = outer_operands(m, seed=m)
+    C = host(B.approx_gemm(cuda(a), cuda(b), dev_lut(B, "mitchell", m), m))
+    want = oracle.mul(oracle.MITCHELL, m, np.repeat(a[:, 0], b.shape[1]), np.tile(b[0], a.shape[0]))
+    assert_bits_equal(C, want, "gemm K=1 M=%d" % m)
+
+
+def test_gemm_k1_special_values_bit_exact(B):
+    from closed_forms import special_values
+    s = special_values()
+    a, b = s.reshape(-1, 1), s.reshape(1, -1)
+    for m in (7, 11):
+        C = host(B.approx_gemm(cuda(a), cuda(b), dev_lut(B, "exact_trunc", m), m))
+        want = oracle.mul(oracle.EXACT_TRUNC, m, np.repeat(s, s.size), np.tile(s, s.size))
+        assert_bits_equal(C, want, "gemm K=1 specials M=%d" % m)
+
+
+def test_conv_single_product_shapes_bit_exact(B):
+    """1x1 conv with one input channel (fwd), one output position (bwd_weight) and one output
+    channel with a 1x1 kernel (bwd_data): every output is a single product."""
+    m = 7
+    lut = dev_lut(B, "mitchell", m)
+    p = W.conv_desc(2, 5, 7, 1, 70, 1, 1, 1, 0)
+    x = random_bits(2 * 5 * 7, 1).reshape(2, 5, 7, 1)
+    w = random_bits(70, 2).reshape(1, 1, 1, 70)
+    y = host(B.approx_conv2d_fwd(p, cuda(x), cuda(w), lut, m))
+    want = oracle.mul(oracle.MITCHELL, m, np.repeat(x.reshape(-1), 70), np.tile(w.reshape(-1), 70))
+    assert_bits_equal(y, want, "conv fwd 1x1 ci=1")
+    # bwd_weight with a single output position: dw[kh,kw,ci,co] = amul(x[0,kh,kw,ci], dy[0,0,0,co])
+    p = W.conv_desc(1, 3, 3, 5, 66, 3, 3, 1, 0)
+    x = random_bits(45, 3).reshape(1, 3, 3, 5)
+    dy = random_bits(66, 4).reshape(1, 1, 1, 66)
+    dw = host(B.approx_conv2d_bwd_weight(p, cuda(x), cuda(dy), lut, m))
+    want = oracle.mul(oracle.MITCHELL, m, np.repeat(x.reshape(-1), 66), np.tile(dy.reshape(-1), 45))
+    assert_bits_equal(dw, want, "conv bwd_weight single position")
+    # bwd_data with 1x1 kernel, c_out = 1: dx[n,h,w,ci] = amul(dy[n,h,w,0], w[0,0,ci,0])
+    p = W.conv_desc(2, 4, 6, 67, 1, 1, 1, 1, 0)
+    dy = random_bits(48, 5).reshape(2, 4, 6, 1)
+    w = random_bits(67, 6).reshape(1, 1, 67, 1)
+    dx = host(B.approx_conv2d_bwd_data(p, cuda(dy), cuda(w), lut, m))
+    want = oracle.mul(oracle.MITCHELL, m, np.repeat(dy.reshape(-1), 67), np.tile(w.reshape(-1), 48))
+    assert_bits_equal(dx, want, "conv bwd_data 1x1 co=1")
+
+
+# ------------------------------------------------------------------ GEMM sums ------------
+
+GEMM_SHAPES = [(64, 64, 64), (1, 1, 1), (3, 17, 63), (65, 1000, 17), (130, 7, 300), (257, 129, 513),
+               (700, 20, 33), (64, 16, 8192)]
+
+
+@pytest.mark.parametrize("shape", GEMM_SHAPES)
+@pytest.mark.parametrize("m", [7, 11])
+def test_gemm_matches_oracle(B, shape, m):
+    M, N, K = shape
+    A = W.uniform((M, K), -1, 1, 1000 + M)
+    Bm = W.uniform((K, N), -1, 1, 2000 + N)
+    C = host(B.approx_gemm(cuda(A), cuda(Bm), dev_lut(B, "mitchell", m), m))
+    ref, S = oracle.gemm(oracle.MITCHELL, m, A, Bm)
+    assert_within_tolerance(C, ref, S, "gemm %s M=%d" % (shape, m))
+
+
+@pytest.mark.parametrize("ta,tb", [(True, False), (False, True), (True, True)])
+@pytest.mark.parametrize("m", [3, 7, 8])
+def test_gemm_transposes(B, ta, tb, m):
+    M, N, K = 77, 45, 91
+    A = W.normal((K, M) if ta else (M, K), 1.0, 31)
+    Bm = W.normal((N, K) if tb else (K, N), 1.0, 32)
+    C = host(B.approx_gemm(cuda(A), cuda(Bm), dev_lut(B, "exact_trunc", m), m, trans_a=ta, trans_b=tb))
+    ref, S = oracle.gemm(oracle.EXACT_TRUNC, m, A, Bm, ta, tb)
+    assert_within_tolerance(C, ref, S, "gemm trans %s %s" % (ta, tb))
+
+
+def test_gemm_leading_dimension_canary_and_k0(B):
+    """ldc > n: the padding columns of C keep their sentinel; k = 0 writes -0.0."""
+    m = 7
+    A = W.uniform((33, 20), -1, 1, 41)
+    Bm = W.uniform((20, 10), -1, 1, 42)
+    buf = torch.full((33, 17), 12345.0, dtype=torch.float32, device="cuda")
+    out = buf[:, :10]
+    B.lib()
+    lut = dev_lut(B, "mitchell", m)
+    B.approx_gemm(cuda(A), cuda(Bm), lut, m, out=out)
+    got = host(buf)
+    assert np.all(got[:, 10:] == 12345.0)
+    ref, S = oracle.gemm(oracle.MITCHELL, m, A, Bm)
+    assert_within_tolerance(got[:, :10], ref, S, "gemm ldc")
+    z = B.approx_gemm(cuda(np.zeros((5, 0), np.float32)), cuda(np.zeros((0, 3), np.float32)), lut, m)
+    assert np.all(host(z).view(np.uint32) == 0x80000000)
+
+
+def test_gemm_deterministic(B):
+    A = W.normal((300, 500), 1.0, 51)
+    Bm = W.normal((500, 200), 1.0, 52)
+    lut = dev_lut(B, "mitchell", 7)
+    c1 = host(B.approx_gemm(cuda(A), cuda(Bm), lut, 7))
+    c2 = host(B.approx_gemm(cuda(A), cuda(Bm), lut, 7))
+    assert np.array_equal(c1.view(np.uint32), c2.view(np.uint32))
+
+
+# ------------------------------------------------------------------ convolution ----------
+
+CONV_CASES = [
+    W.conv_desc(2, 7, 6, 3, 4, 3, 3, 1, 1),
+    W.conv_desc(2, 9, 8, 2, 3, 3, 3, 2, 1),
+    W.conv_desc(1, 11, 10, 3, 2, 5, 5, 2, pads=(2, 1, 0, 3)),
+    W.conv_desc(3, 5, 5, 4, 2, 1, 1, 1, 0),
+    W.conv_desc(2, 8, 9, 2, 3, 7, 7, 2, 3),
+    W.conv_desc(1, 6, 6, 1, 2, 2, 3, 3, pads=(1, 0, 2, 1)),
+    W.conv_desc(2, 13, 12, 20, 70, 3, 3, 1, 1),
+    W.conv_desc(3, 10, 10, 65, 17, 3, 3, 2, 1),
+    W.conv_desc(2, 9, 9, 16, 33, 1, 1, 2, 0),
+    W.conv_desc(2, 28, 28, 1, 6, 5, 5, 1, 2),
+]
+
+
+def _conv_inputs(p, seed):
+    oh, ow = W.conv_out_hw(p)
+    x = W.uniform((p["n"], p["h"], p["w"], p["c_in"]), -1, 1, seed)
+    w = W.uniform((p["kh"], p["kw"], p["c_in"], p["c_out"]), -1, 1, seed + 1)
+    dy = W.uniform((p["n"], oh, ow, p["c_out"]), -1, 1, seed + 2)
+    return x, w, dy
+
+
+@pytest.mark.parametrize("ci", range(len(CONV_CASES)))
+@pytest.mark.parametrize("m", [7, 10])
+def test_conv_passes_match_oracle(B, ci, m):
+    p = CONV_CASES[ci]
+    x, w, dy = _conv_inputs(p, 300 + ci)
+    lut = dev_lut(B, "mitchell", m)
+    y = host(B.approx_conv2d_fwd(p, cuda(x), cuda(w), lut, m))
+    ref, S = oracle.conv2d_fwd(oracle.MITCHELL, m, p, x, w)
+    assert_within_tolerance(y, ref, S, "fwd %d" % ci)
+    dx = host(B.approx_conv2d_bwd_data(p, cuda(dy), cuda(w), lut, m))
+    ref, S = oracle.conv2d_bwd_data(oracle.MITCHELL, m, p, dy, w)
+    assert_within_tolerance(dx, ref, S, "bwd_data %d" % ci)
+    dw = host(B.approx_conv2d_bwd_weight(p, cuda(x), cuda(dy), lut, m))
+    ref, S = oracle.conv2d_bwd_weight(oracle.MITCHELL, m, p, x, dy)
+    assert_within_tolerance(dw, ref, S, "bwd_weight %d" % ci)
+
+
+def test_operand_order_with_asymmetric_table(B):
+    """A table from an asymmetric model (first operand truncated to M bits, second to M-1) pins
+    the first operand of GEMM and of every convolution pass."""
+    m = 5
+
+    def asym(a, b):
+        ua = np.float32(a).view(np.uint32) & np.uint32((0xFFFFFFFF << (23 - m)) & 0xFFFFFFFF)
+        ub = np.float32(b).view(np.uint32) & np.uint32((0xFFFFFFFF << (24 - m)) & 0xFFFFFFFF)
+        return float(ua.view(np.float32) * ub.view(np.float32))
+
+    lut = B.device_lut(B.lut_build(m, asym))
+    A = W.uniform((70, 40), -2, 2, 61)
+    Bm = W.uniform((40, 30), -2, 2, 62)
+    C = host(B.approx_gemm(cuda(A), cuda(Bm), lut, m))
+    ref, S = oracle.gemm(oracle.ASYM, m, A, Bm)
+    assert_within_tolerance(C, ref, S, "gemm asym")
+    p = CONV_CASES[1]
+    x, w, dy = _conv_inputs(p, 63)
+    y = host(B.approx_conv2d_fwd(p, cuda(x), cuda(w), lut, m))
+    ref, S = oracle.conv2d_fwd(oracle.ASYM, m, p, x, w)
+    assert_within_tolerance(y, ref, S, "fwd asym")
+    dx = host(B.approx_conv2d_bwd_data(p, cuda(dy), cuda(w), lut, m))
+    ref, S = oracle.conv2d_bwd_data(oracle.ASYM, m, p, dy, w)
+    assert_within_tolerance(dx, ref, S, "bwd_data asym")
+    dw = host(B.approx_conv2d_bwd_weight(p, cuda(x), cuda(dy), lut, m))
+    ref, S = oracle.conv2d_bwd_weight(oracle.ASYM, m, p, x, dy)
+    assert_within_tolerance(dw, ref, S, "bwd_weight asym")
+
+
+# ------------------------------------------------------------------ full-size workloads --
+
+def _sample(total, count, seed):
+    rng = np.random.default_rng(seed)
+    idx = rng.choice(total, size=min(count, total), replace=False)
+    return np.sort(np.concatenate([idx, [0, total - 1]]).astype(np.int64))
+
+
+def _check_conv_full(B, p, m, seed, stem=False, samples=(2048, 2048, 512)):
+    x, w, dy = W.resnet_conv_inputs(p, seed=seed, stem=stem)
+    lut = dev_lut(B, "mitchell", m)
+    xd, wd, dyd = cuda(x), cuda(w), cuda(dy)
+    y = host(B.approx_conv2d_fwd(p, xd, wd, lut, m)).reshape(-1)
+    idx = _sample(y.size, samples[0], seed)
+    ref, S = oracle.conv2d_fwd(oracle.MITCHELL, m, p, x, w, idx=idx)
+    assert_within_tolerance(y[idx], ref, S, "fwd")
+    dx = host(B.approx_conv2d_bwd_data(p, dyd, wd, lut, m)).reshape(-1)
+    idx = _sample(dx.size, samples[1], seed + 1)
+    ref, S = oracle.conv2d_bwd_data(oracle.MITCHELL, m, p, dy, w, idx=idx)
+    assert_within_tolerance(dx[idx], ref, S, "bwd_data")
+    dw = host(B.approx_conv2d_bwd_weight(p, xd, dyd, lut, m)).reshape(-1)
+    idx = _sample(dw.size, samples[2], seed + 2)
+    ref, S = oracle.conv2d_bwd_weight(oracle.MITCHELL, m, p, x, dy, idx=idx)
+    assert_within_tolerance(dw[idx], ref, S, "bwd_weight")
+    return y
+
+
+def test_resnet_3x3_conv_full_size(B):
+    cfg = W.RESNET_3X3
+    _check_conv_full(B, cfg["conv"], cfg["m_bits"], seed=3000)
+
+
+@pytest.mark.parametrize("li", range(len(W.RESNET50_LAYERS)))
+def test_resnet50_layers_full_size(B, li):
+    cfg = W.RESNET50_LAYERS[li]
+    _check_conv_full(B, cfg["conv"], cfg["m_bits"], seed=4000 + 10 * li, stem=(li == 0), samples=(1024, 1024, 256))
+
+
+@pytest.mark.parametrize("m", [7, 11])
+def test_gemm_4096_full_size(B, m):
+    cfg = W.GEMM_LARGE
+    A, Bm = W.gemm_inputs(cfg["M"], cfg["N"], cfg["K"], "normal", seed=5000)
+    C = host(B.approx_gemm(cuda(A), cuda(Bm), dev_lut(B, "mitchell", m), m)).reshape(-1)
+    idx = _sample(C.size, 1024, 5000 + m)
+    ref, S = oracle.gemm(oracle.MITCHELL, m, A, Bm, idx=idx)
+    assert_within_tolerance(C[idx], ref, S, "gemm 4096 M=%d" % m)
+
+
+def test_conv_deterministic(B):
+    p = W.RESNET_3X3["conv"]
+    x, w, dy = W.resnet_conv_inputs(p, seed=3100)
+    lut = dev_lut(B, "mitchell", 7)
+    xd, wd, dyd = cuda(x), cuda(w), cuda(dy)
+    for fn, args in ((B.approx_conv2d_fwd, (xd, wd)), (B.approx_conv2d_bwd_data, (dyd, wd)),
+                     (B.approx_conv2d_bwd_weight, (xd, dyd))):
+        r1 = host(fn(p, *args, lut, 7))
+        r2 = host(fn(p, *args, lut, 7))
+        assert np.array_equal(r1.view(np.uint32), r2.view(np.uint32))
+
+
+def test_lenet5_stack_fwd_bwd(B):
+    """LeNet-5 layer stack, batch 64, exact bfloat16-truncation multiplier (M = 7).  ReLU,
+    max-pool and the loss gradient run as plain torch ops; every approximate layer call is
+    checked against the oracle fed the same layer inputs."""
+    cfg = W.LENET5
+    m = cfg["m_bits"]
+    lut = dev_lut(B, "exact_trunc", m)
+    F = torch.nn.functional
+    c1, c2 = cfg["conv1"], cfg["conv2"]
+    bs = cfg["batch"]
+    x0 = W.uniform((bs, 28, 28, 1), 0.0, 1.0, 6000)
+    w1 = W.glorot_uniform((5, 5, 1, 6), 25 * 1, 25 * 6, 6001)
+    w2 = W.glorot_uniform((5, 5, 6, 16), 25 * 6, 25 * 16, 6002)
+    fcw = [W.glorot_uniform((i, o), i, o, 6003 + j) for j, (i, o) in enumerate(cfg["fc"])]
+    labels = np.random.default_rng(6010).integers(0, 10, bs)
+
+    def check(got_t, ref_S, what):
+        got = host(got_t)
+        assert_within_tolerance(got, ref_S[0], ref_S[1], what)
+
+    def pool(t):  # NHWC 2x2 max-pool via torch
+        return F.max_pool2d(t.permute(0, 3, 1, 2), 2).permute(0, 2, 3, 1).contiguous()
+
+    X0 = cuda(x0)
+    Y1 = B.approx_conv2d_fwd(c1, X0, cuda(w1), lut, m)
+    check(Y1, oracle.conv2d_fwd(oracle.EXACT_TRUNC, m, c1, x0, w1), "conv1 fwd")
+    A1 = torch.relu(Y1)
+    P1 = pool(A1).requires_grad_(False)
+    p1 = host(P1)
+    Y2 = B.approx_conv2d_fwd(c2, P1, cuda(w2), lut, m)
+    check(Y2, oracle.conv2d_fwd(oracle.EXACT_TRUNC, m, c2, p1, w2), "conv2 fwd")
+    A2 = torch.relu(Y2)
+    P2 = pool(A2)
+    h = P2.reshape(bs, 400).contiguous()
+    acts, pre = [h], []
+    for j, wj in enumerate(fcw):
+        hj = host(acts[-1])
+        z = B.approx_gemm(acts[-1], cuda(wj), lut, m)
+        check(z, oracle.gemm(oracle.EXACT_TRUNC, m, hj, wj), "fc%d fwd" % (j + 1))
+        pre.append(z)
+        acts.append(torch.relu(z).contiguous() if j < 2 else z)
+    logits = acts[-1]
+    g = (torch.softmax(logits, dim=1) - F.one_hot(torch.from_numpy(labels).cuda(), 10).float()) / bs
+    g = g.contiguous()
+    for j in (2, 1, 0):
+        wj = fcw[j]
+        aj = host(acts[j])
+        gh = host(g)
+        dW = B.approx_gemm(acts[j], g, lut, m, trans_a=True)
+        check(dW, oracle.gemm(oracle.EXACT_TRUNC, m, aj, gh, True, False), "fc%d bwd_weight" % (j + 1))
+        dX = B.approx_gemm(g, cuda(wj), lut, m, trans_b=True)
+        check(dX, oracle.gemm(oracle.EXACT_TRUNC, m, gh, wj, False, True), "fc%d bwd_data" % (j + 1))
+        g = dX if j == 0 else (dX * (pre[j - 1] > 0).float()).contiguous()
+    # back through pool2 / relu2 into conv2
+    P2g = g.reshape(bs, 5, 5, 16)
+    A2r = A2.detach().clone().requires_grad_(True)
+    pool(A2r).backward(P2g)
+    dY2 = (A2r.grad * (Y2 > 0).float()).contiguous()
+    dy2 = host(dY2)
+    dW2 = B.approx_conv2d_bwd_weight(c2, P1, dY2, lut, m)
+    check(dW2, oracle.conv2d_bwd_weight(oracle.EXACT_TRUNC, m, c2, p1, dy2), "conv2 bwd_weight")
+    dP1 = B.approx_conv2d_bwd_data(c2, dY2, cuda(w2), lut, m)
+    check(dP1, oracle.conv2d_bwd_data(oracle.EXACT_TRUNC, m, c2, dy2, w2), "conv2 bwd_data")
+    A1r = A1.detach().clone().requires_grad_(True)
+    pool(A1r).backward(dP1)
+    dY1 = (A1r.grad * (Y1 > 0).float()).contiguous()
+    dy1 = host(dY1)
+    dW1 = B.approx_conv2d_bwd_weight(c1, X0, dY1, lut, m)
+    check(dW1, oracle.conv2d_bwd_weight(oracle.EXACT_TRUNC, m, c1, x0, dy1), "conv1 bwd_weight")
+    dX0 = B.approx_conv2d_bwd_data(c1, dY1, cuda(w1), lut, m)
+    check(dX0, oracle.conv2d_bwd_data(oracle.EXACT_TRUNC, m, c1, dy1, w1), "conv1 bwd_data")
