@@ -1,0 +1,302 @@
+#!/usr/bin/env python3
+"""Throughput of the approximate-multiplier hot path on one MI355X.
+
+One step = approx_gemm 4096x4096x4096 (Mitchell multiplier, M = 7, table in LDS) plus the
+ResNet-style 3x3 convolution (batch 128, 64 -> 64 channels at 32x32, stride 1, pad 1, NHWC,
+Mitchell M = 7) forward, backward-data and backward-weight.  Inputs are seeded synthetic
+tensors resident in HBM before the timed region; outputs and workspaces are preallocated.
+value = approximate multiply-accumulates per second over the timed steps (whole job).
+
+Prints one JSON line.  Besides the contract fields it carries
+  roofline      the GEMM kernel (the dominant one): algorithmic FLOP (2 per approx-MAC) per
+                launch over its average launch duration, measured with HIP events recorded on
+                its stream inside the timed region, against the FP32 vector peak
+  cpu_baseline  the CPU oracle timed on a seeded sample of the same step's outputs
+  extra         per-kernel rates, the M = 11 global-table GEMM, the ResNet-50 layers and the
+                LeNet-5 stack
+"""
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+METRIC = "approx-MACs/s (G/s) and % FP32 VALU peak: approx_gemm 4096³ + ResNet conv fwd+bwd"
+FP32_VECTOR_PEAK_TFLOPS = 157.3   # MI355X published FP32 vector peak (dense)
+FLOP_PER_APPROX_MAC = 2           # one multiply + one add
+TRAFFIC_PROFILE = os.path.join(ROOT, "profiles", "gemm_4096_m7_traffic.txt")
+KERNEL_SOURCE = os.path.join(ROOT, "paper_2209_04161_amd", "csrc", "amsim_kernels.hip")
+
+
+def log(msg):
+    print("[bench] " + msg, file=sys.stderr, flush=True)
+
+
+def kernel_source_hash():
+    with open(KERNEL_SOURCE, "rb") as f:
+        return hashlib.sha256(f.read()).hexdigest()
+
+
+def read_traffic():
+    """HBM bytes per GEMM launch from the committed rocprofv3 --pmc summary, or None when the
+    kernel source changed since the counters were taken."""
+    if not os.path.exists(TRAFFIC_PROFILE):
+        return None
+    fields = {}
+    with open(TRAFFIC_PROFILE) as f:
+        for line in f:
+            if ":" in line and not line.startswith("#"):
+                k, v = line.split(":", 1)
+                fields[k.strip()] = v.strip()
+    if fields.get("kernel_source_sha256") != kernel_source_hash():
+        return None
+    try:
+        return float(fields["hbm_bytes_per_launch"])
+    except (KeyError, ValueError):
+        return None
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--cpu-fraction", type=float, default=0.1,
+                    help="fraction of each part's outputs the CPU oracle computes for cpu_baseline")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-extra", action="store_true")
+    ap.add_argument("--calibrate-copy", action="store_true",
+                    help="also run a plain 256 MiB device copy three times (reference for HBM byte counters)")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print("bench.py measures one GPU only: this build has no multi-GPU path (each GPU would run "
+              "its own shard of the batch/rows; see the design notes). Run with --gpus 1.", file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    from paper_2209_04161_amd import binding as B
+    from paper_2209_04161_amd import workloads as W
+
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        sys.exit(2)
+    B.lib()  # fails loudly if the HIP library is not built
+    dev = torch.device("cuda:0")
+    m_bits = 7
+    lut = B.device_lut(B.lut_build(m_bits, "mitchell"), dev)
+
+    g = W.GEMM_LARGE
+    M, N, K = g["M"], g["N"], g["K"]
+    A_h, B_h = W.gemm_inputs(M, N, K, "normal", seed=5000)
+    A = torch.from_numpy(A_h).to(dev)
+    Bm = torch.from_numpy(B_h).to(dev)
+    C = torch.empty((M, N), dtype=torch.float32, device=dev)
+    ws_g = torch.empty(B.amsim_gemm_workspace_size(0, 0, M, N, K, m_bits), dtype=torch.uint8, device=dev)
+
+    cv = W.RESNET_3X3["conv"]
+    x_h, w_h, dy_h = W.resnet_conv_inputs(cv, seed=3000)
+    x, w, dy = (torch.from_numpy(t).to(dev) for t in (x_h, w_h, dy_h))
+    y = torch.empty_like(dy)
+    dx = torch.empty_like(x)
+    dw = torch.empty_like(w)
+    ws_c = [torch.empty(max(1, B.amsim_conv2d_workspace_size(cv, p, m_bits)), dtype=torch.uint8, device=dev)
+            for p in range(3)]
+
+    gemm_macs = M * N * K
+    conv_macs = W.conv_macs(cv)
+    step_macs = gemm_macs + 3 * conv_macs
+
+    def step():
+        B.approx_gemm(A, Bm, lut, m_bits, out=C, workspace=ws_g)
+        B.approx_conv2d_fwd(cv, x, w, lut, m_bits, out=y, workspace=ws_c[0])
+        B.approx_conv2d_bwd_data(cv, dy, w, lut, m_bits, out=dx, workspace=ws_c[1])
+        B.approx_conv2d_bwd_weight(cv, x, dy, lut, m_bits, out=dw, workspace=ws_c[2])
+
+    for i in range(args.warmup):
+        step()
+        torch.cuda.synchronize()
+        log("warmup step %d done" % (i + 1))
+
+    if args.calibrate_copy:
+        src = torch.ones(64 << 20, dtype=torch.float32, device=dev)
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        log("copy calibration: 3 copies of %d bytes" % (src.numel() * 4))
+        del src, dst
+
+    B.amsim_profile_start(8 * args.steps + 8)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        step()
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    B.amsim_profile_stop()
+    elapsed = t1 - t0
+    log("timed %d steps in %.3f s" % (args.steps, elapsed))
+
+    value = step_macs * args.steps / elapsed / 1e9
+    kernels = {}
+    for kind, macs in (("gemm", gemm_macs), ("conv_fwd", conv_macs), ("conv_bwd_data", conv_macs),
+                       ("conv_bwd_weight", conv_macs)):
+        n, ms = B.amsim_profile_read(kind)
+        avg = ms / max(n, 1)
+        kernels[kind] = {"launches": n, "avg_ms": round(avg, 4),
+                         "gmacs_per_s": round(macs / (avg * 1e-3) / 1e9, 1) if n else None,
+                         "pct_fp32_vector_peak": round(100 * FLOP_PER_APPROX_MAC * macs / (avg * 1e-3) /
+                                                       (FP32_VECTOR_PEAK_TFLOPS * 1e12), 2) if n else None}
+    g_avg_s = kernels["gemm"]["avg_ms"] * 1e-3
+    achieved = FLOP_PER_APPROX_MAC * gemm_macs / g_avg_s / 1e12
+    roofline = {"bound": "alu", "achieved": round(achieved, 3), "peak": FP32_VECTOR_PEAK_TFLOPS,
+                "unit": "TFLOP/s", "frac": round(achieved / FP32_VECTOR_PEAK_TFLOPS, 4),
+                "traffic": read_traffic(), "kernel": "gemm_kernel (approx_gemm 4096^3, Mitchell M=7, LDS table)"}
+
+    out = {
+        "metric": METRIC,
+        "value": round(value, 1),
+        "unit": "G approx-MAC/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(elapsed / args.steps * 1e3, 3),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic",
+        "config": {"workload": "approx_gemm 4096x4096x4096 normal(0,1) + ResNet 3x3 conv 64->64 @32x32 batch 128 "
+                               "fwd+bwd_data+bwd_weight (half-normal x, He-normal w, N(0,1) dy), Mitchell multiplier, "
+                               "M=7 (65536-byte table in LDS)",
+                   "approx_macs_per_step": step_macs, "m_bits": m_bits, "multiplier": "mitchell"},
+        "pct_fp32_vector_peak": round(100 * FLOP_PER_APPROX_MAC * value * 1e9 / (FP32_VECTOR_PEAK_TFLOPS * 1e12), 2),
+        "roofline": roofline,
+        "kernels": kernels,
+    }
+
+    if not args.no_extra:
+        out["extra"] = extras(B, W, torch, np, dev, lut, m_bits, A, Bm, C)
+
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(args.cpu_fraction, A_h, B_h, cv, x_h, w_h, dy_h, m_bits)
+        out["gpu_over_cpu"] = round(value / out["cpu_baseline"]["value"], 1)
+
+    print(json.dumps(out), flush=True)
+
+
+def _time_call(torch, fn, reps):
+    fn()
+    torch.cuda.synchronize()
+    e0 = torch.cuda.Event(enable_timing=True)
+    e1 = torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(reps):
+        fn()
+    e1.record()
+    torch.cuda.synchronize()
+    return e0.elapsed_time(e1) / reps  # ms per call
+
+
+def extras(B, W, torch, np, dev, lut7, m7, A, Bm, C):
+    """Rates of the other workloads (not part of the timed step)."""
+    ex = {}
+    M, N, K = A.shape[0], Bm.shape[1], A.shape[1]
+    lut11 = B.device_lut(B.lut_build(11, "mitchell"), dev)
+    ws = torch.empty(B.amsim_gemm_workspace_size(0, 0, M, N, K, 11), dtype=torch.uint8, device=dev)
+    ms = _time_call(torch, lambda: B.approx_gemm(A, Bm, lut11, 11, out=C, workspace=ws), 2)
+    ex["gemm_4096_m11_global_table"] = {"ms": round(ms, 2), "gmacs_per_s": round(M * N * K / ms / 1e6, 1)}
+    log("M=11 GEMM done")
+    for cfg in W.RESNET50_LAYERS:
+        p = cfg["conv"]
+        x_h, w_h, dy_h = W.resnet_conv_inputs(p, seed=4000, stem=(cfg is W.RESNET50_LAYERS[0]))
+        x, w, dy = (torch.from_numpy(t).to(dev) for t in (x_h, w_h, dy_h))
+        macs = W.conv_macs(p)
+        r = {}
+        for name, fn in (("fwd", lambda: B.approx_conv2d_fwd(p, x, w, lut7, m7)),
+                         ("bwd_data", lambda: B.approx_conv2d_bwd_data(p, dy, w, lut7, m7)),
+                         ("bwd_weight", lambda: B.approx_conv2d_bwd_weight(p, x, dy, lut7, m7))):
+            ms = _time_call(torch, fn, 5)
+            r[name] = {"ms": round(ms, 3), "gmacs_per_s": round(macs / ms / 1e6, 1)}
+        ex[cfg["name"]] = r
+    log("ResNet-50 layers done")
+    # LeNet-5 stack, batch 64, exact bfloat16-truncation table: fwd + bwd of the approximate layers
+    cfg = W.LENET5
+    lutb = B.device_lut(B.lut_build(cfg["m_bits"], "exact_trunc"), dev)
+    mb = cfg["m_bits"]
+    c1, c2 = cfg["conv1"], cfg["conv2"]
+    x0 = torch.from_numpy(W.uniform((64, 28, 28, 1), 0, 1, 6000)).to(dev)
+    w1 = torch.from_numpy(W.glorot_uniform((5, 5, 1, 6), 25, 150, 6001)).to(dev)
+    w2 = torch.from_numpy(W.glorot_uniform((5, 5, 6, 16), 150, 400, 6002)).to(dev)
+    fcw = [torch.from_numpy(W.glorot_uniform((i, o), i, o, 6003 + j)).to(dev) for j, (i, o) in enumerate(cfg["fc"])]
+    p1 = torch.rand((64, 14, 14, 6), device=dev)
+    dy1 = torch.randn((64, 28, 28, 6), device=dev)
+    dy2 = torch.randn((64, 10, 10, 16), device=dev)
+    acts = [torch.rand((64, i), device=dev) for i, _ in cfg["fc"]]
+    grads = [torch.randn((64, o), device=dev) for _, o in cfg["fc"]]
+    lenet_macs = 2 * W.conv_macs(c1) + 3 * W.conv_macs(c2) + 3 * sum(64 * i * o for i, o in cfg["fc"])
+
+    def lenet():
+        B.approx_conv2d_fwd(c1, x0, w1, lutb, mb)
+        B.approx_conv2d_fwd(c2, p1, w2, lutb, mb)
+        for a, wj in zip(acts, fcw):
+            B.approx_gemm(a, wj, lutb, mb)
+        for a, gj, wj in zip(acts, grads, fcw):
+            B.approx_gemm(a, gj, lutb, mb, trans_a=True)
+            B.approx_gemm(gj, wj, lutb, mb, trans_b=True)
+        B.approx_conv2d_bwd_weight(c2, p1, dy2, lutb, mb)
+        B.approx_conv2d_bwd_data(c2, dy2, w2, lutb, mb)
+        B.approx_conv2d_bwd_weight(c1, x0, dy1, lutb, mb)
+
+    ms = _time_call(torch, lenet, 10)
+    ex["lenet5_b64_fwd_bwd"] = {"ms": round(ms, 3), "approx_macs": lenet_macs,
+                               "gmacs_per_s": round(lenet_macs / ms / 1e6, 1)}
+    log("LeNet-5 stack done")
+    return ex
+
+
+def cpu_baseline(frac, A_h, B_h, cv, x_h, w_h, dy_h, m_bits):
+    """The CPU oracle (as it stands) on a seeded sample of every part of the step: the same
+    fraction of each part's outputs, each output computed in full."""
+    import numpy as np
+
+    import oracle
+    from paper_2209_04161_amd import workloads as W
+
+    rng = np.random.default_rng(777)
+    M, K = A_h.shape
+    N = B_h.shape[1]
+    oh, ow = W.conv_out_hw(cv)
+    n_y = cv["n"] * oh * ow * cv["c_out"]
+    n_dx = cv["n"] * cv["h"] * cv["w"] * cv["c_in"]
+    n_dw = cv["kh"] * cv["kw"] * cv["c_in"] * cv["c_out"]
+    k_fwd = cv["kh"] * cv["kw"] * cv["c_in"]
+    k_bwd_w = cv["n"] * oh * ow
+    parts = [("gemm", M * N, K), ("fwd", n_y, k_fwd), ("bwd_data", n_dx, k_fwd), ("bwd_weight", n_dw, k_bwd_w)]
+    sample = {name: np.sort(rng.choice(total, max(1, int(round(frac * total))), replace=False))
+              for name, total, _ in parts}
+    macs = sum(sample[name].size * k for name, _, k in parts)
+    log("cpu_baseline: oracle on %d outputs (%.3g approx-MACs)" % (sum(s.size for s in sample.values()), macs))
+    t0 = time.perf_counter()
+    oracle.gemm(oracle.MITCHELL, m_bits, A_h, B_h, idx=sample["gemm"])
+    oracle.conv2d_fwd(oracle.MITCHELL, m_bits, cv, x_h, w_h, idx=sample["fwd"])
+    oracle.conv2d_bwd_data(oracle.MITCHELL, m_bits, cv, dy_h, w_h, idx=sample["bwd_data"])
+    oracle.conv2d_bwd_weight(oracle.MITCHELL, m_bits, cv, x_h, dy_h, idx=sample["bwd_weight"])
+    dt = time.perf_counter() - t0
+    log("cpu_baseline: %.1f s" % dt)
+    return {"value": round(macs / dt / 1e9, 4), "unit": "G approx-MAC/s", "cores": oracle.num_threads(),
+            "kind": "oracle", "seconds": round(dt, 2),
+            "sample": "%.1f%% of the outputs of each part of the step (GEMM 4096^3, conv fwd, bwd_data, "
+                      "bwd_weight), seeded uniform without replacement, each output computed in full: "
+                      "%d approx-MACs" % (100 * frac, macs)}
+
+
+if __name__ == "__main__":
+    main()

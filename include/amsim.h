@@ -152,6 +152,27 @@ int approx_conv2d_bwd_weight(const amsim_conv2d *desc, const float *x, const flo
 int approx_mul_ew(int64_t n, const float *a, const float *b, float *c, const uint32_t *lut, int m_bits,
                   void *stream);
 
+/* ----------------------------------------------------------------- kernel timing -------
+ * Measurement support (no paper counterpart; the paper reports per-batch wall time only).
+ * Between amsim_profile_start and amsim_profile_stop, every launch of a main kernel -- the
+ * GEMM kernel of approx_gemm and the three convolution kernels, not their decode pre-passes
+ * -- is bracketed by two HIP events recorded on the stream it is launched on.
+ *   amsim_profile_start(max_launches): creates that many event pairs (host-side HIP calls; do
+ *     it outside any timed region) and starts recording; AMSIM_ERR_INVALID_ARG if
+ *     max_launches < 1, AMSIM_ERR_HIP on event creation failure.  Launches beyond the
+ *     capacity are not timed.  Calling it again discards the previous records.
+ *   amsim_profile_stop(): stops recording and waits for the recorded events.
+ *   amsim_profile_read(kind, &launches, &total_ms): launches and summed durations (ms) of one
+ *     kernel kind (AMSIM_KERNEL_*) since the last start; valid after amsim_profile_stop.
+ * The timer state is process-wide and guarded by a lock. */
+#define AMSIM_KERNEL_GEMM 0
+#define AMSIM_KERNEL_CONV_FWD 1
+#define AMSIM_KERNEL_CONV_BWD_DATA 2
+#define AMSIM_KERNEL_CONV_BWD_WEIGHT 3
+int amsim_profile_start(int max_launches);
+int amsim_profile_stop(void);
+int amsim_profile_read(int kind, int *launches, double *total_ms);
+
 #ifdef __cplusplus
 }
 #endif

@@ -24,6 +24,12 @@ AMSIM_CONV_FWD = 0
 AMSIM_CONV_BWD_DATA = 1
 AMSIM_CONV_BWD_WEIGHT = 2
 
+AMSIM_KERNEL_GEMM = 0
+AMSIM_KERNEL_CONV_FWD = 1
+AMSIM_KERNEL_CONV_BWD_DATA = 2
+AMSIM_KERNEL_CONV_BWD_WEIGHT = 3
+KERNEL_KINDS = {"gemm": 0, "conv_fwd": 1, "conv_bwd_data": 2, "conv_bwd_weight": 3}
+
 MODEL_FN = ctypes.CFUNCTYPE(ctypes.c_float, ctypes.c_float, ctypes.c_float, ctypes.c_void_p)
 
 
@@ -76,6 +82,10 @@ def lib():
         "approx_conv2d_bwd_data": ([cp, vp, vp, vp, vp, ctypes.c_int, vp, sz, vp], ctypes.c_int),
         "approx_conv2d_bwd_weight": ([cp, vp, vp, vp, vp, ctypes.c_int, vp, sz, vp], ctypes.c_int),
         "approx_mul_ew": ([i64, vp, vp, vp, vp, ctypes.c_int, vp], ctypes.c_int),
+        "amsim_profile_start": ([ctypes.c_int], ctypes.c_int),
+        "amsim_profile_stop": ([], ctypes.c_int),
+        "amsim_profile_read": ([ctypes.c_int, ctypes.POINTER(ctypes.c_int), ctypes.POINTER(ctypes.c_double)],
+                               ctypes.c_int),
     }
     for name, (args, res) in sigs.items():
         fn = getattr(L, name)
@@ -288,3 +298,23 @@ def approx_mul_ew(a, b, lut, m_bits, out=None):
     _check(lib().approx_mul_ew(a.numel(), _ptr(a), _ptr(b), _ptr(out), _ptr(lut), int(m_bits), _stream()),
            "approx_mul_ew")
     return out
+
+
+# ------------------------------------------------------------------ kernel timing --------
+
+def amsim_profile_start(max_launches: int = 4096) -> None:
+    _check(lib().amsim_profile_start(int(max_launches)), "amsim_profile_start")
+
+
+def amsim_profile_stop() -> None:
+    _check(lib().amsim_profile_stop(), "amsim_profile_stop")
+
+
+def amsim_profile_read(kind) -> tuple:
+    """(launches, total_ms) of one main-kernel kind since the last amsim_profile_start."""
+    if isinstance(kind, str):
+        kind = KERNEL_KINDS[kind]
+    n = ctypes.c_int(0)
+    ms = ctypes.c_double(0.0)
+    _check(lib().amsim_profile_read(int(kind), ctypes.byref(n), ctypes.byref(ms)), "amsim_profile_read")
+    return n.value, ms.value

@@ -28,6 +28,7 @@
 #include <cstdint>
 #include <mutex>
 #include <type_traits>
+#include <vector>
 
 #include "amsim.h"
 
@@ -676,6 +677,60 @@ void dispatch_tile(const Tile &t, F &&f)
 #undef X
 }
 
+
+// ------------------------------------------------------------------ kernel timer --------
+
+struct KernelTimer {
+    std::mutex mu;
+    bool active = false;
+    std::vector<hipEvent_t> begin, end;
+    std::vector<int> kind;
+    size_t used = 0;
+    int launches[4] = {0, 0, 0, 0};
+    double total_ms[4] = {0, 0, 0, 0};
+};
+
+KernelTimer &timer()
+{
+    static KernelTimer t;
+    return t;
+}
+
+// Brackets one main-kernel launch with events on its stream while profiling is active.
+class TimedLaunch {
+  public:
+    TimedLaunch(int kind, hipStream_t st) : st_(st)
+    {
+        KernelTimer &t = timer();
+        std::lock_guard<std::mutex> g(t.mu);
+        if (t.active && t.used < t.begin.size()) {
+            slot_ = long(t.used++);
+            t.kind[size_t(slot_)] = kind;
+            hipEventRecord(t.begin[size_t(slot_)], st_);
+        }
+    }
+    ~TimedLaunch()
+    {
+        if (slot_ < 0) return;
+        KernelTimer &t = timer();
+        std::lock_guard<std::mutex> g(t.mu);
+        hipEventRecord(t.end[size_t(slot_)], st_);
+    }
+
+  private:
+    hipStream_t st_;
+    long slot_ = -1;
+};
+
+void destroy_events(KernelTimer &t)
+{
+    for (hipEvent_t e : t.begin) hipEventDestroy(e);
+    for (hipEvent_t e : t.end) hipEventDestroy(e);
+    t.begin.clear();
+    t.end.clear();
+    t.kind.clear();
+}
+
 }  // namespace
 
 // ==================================================================== C entry points =====
@@ -751,7 +806,10 @@ int approx_gemm(int trans_a, int trans_b, int64_t m, int64_t n, int64_t k, const
                                                                            int(m), int(n), int(k), kchunk, out, ldc,
                                                                            table, m_bits);
     };
-    dispatch_tile<true>(t, run);
+    {
+        TimedLaunch tl(AMSIM_KERNEL_GEMM, st);
+        dispatch_tile<true>(t, run);
+    }
     if (launch_status() != AMSIM_OK) return AMSIM_ERR_HIP;
     if (splits > 1) {
         hipLaunchKernelGGL(reduce_splits_kernel, dim3(grid_for(m * n)), dim3(256), 0, st,
@@ -818,6 +876,7 @@ int approx_conv2d_fwd(const amsim_conv2d *desc, const float *x, const float *w, 
             hipLaunchKernelGGL((conv_fwd_kernel<TM, TN, false>), grid, dim3(kThreads), 0, st, Xd, Wd, int(p.b_ld), s,
                                y, table, entries);
     };
+    TimedLaunch tl(AMSIM_KERNEL_CONV_FWD, st);
     dispatch_tile<true>(t, run);
     return launch_status();
 }
@@ -857,6 +916,7 @@ int approx_conv2d_bwd_data(const amsim_conv2d *desc, const float *dy, const floa
             hipLaunchKernelGGL((conv_bwd_data_kernel<TM, TN, false>), grid, dim3(kThreads), 0, st, Dyd, Wtd,
                                int(p.b_ld), s, dx, table, entries);
     };
+    TimedLaunch tl(AMSIM_KERNEL_CONV_BWD_DATA, st);
     dispatch_tile<true>(t, run);
     return launch_status();
 }
@@ -898,7 +958,10 @@ int approx_conv2d_bwd_weight(const amsim_conv2d *desc, const float *x, const flo
             hipLaunchKernelGGL((conv_bwd_weight_kernel<TM, TN, false>), grid, dim3(kThreads), 0, st, Xd, Dyd,
                                int(p.b_ld), s, per, out, table, entries);
     };
-    dispatch_tile<true>(t, run);
+    {
+        TimedLaunch tl(AMSIM_KERNEL_CONV_BWD_WEIGHT, st);
+        dispatch_tile<true>(t, run);
+    }
     if (launch_status() != AMSIM_OK) return AMSIM_ERR_HIP;
     if (splits > 1) {
         hipLaunchKernelGGL(reduce_splits_kernel, dim3(grid_for(int64_t(R) * s.co)), dim3(256), 0, st,
@@ -917,6 +980,62 @@ int approx_mul_ew(int64_t n, const float *a, const float *b, float *c, const uin
     hipStream_t st = static_cast<hipStream_t>(stream);
     hipLaunchKernelGGL(mul_ew_kernel, dim3(grid_for(n)), dim3(256), 0, st, n, a, b, c, lut, m_bits);
     return launch_status();
+}
+
+int amsim_profile_start(int max_launches)
+{
+    if (max_launches < 1) return AMSIM_ERR_INVALID_ARG;
+    KernelTimer &t = timer();
+    std::lock_guard<std::mutex> g(t.mu);
+    t.active = false;
+    destroy_events(t);
+    t.used = 0;
+    for (int k = 0; k < 4; ++k) {
+        t.launches[k] = 0;
+        t.total_ms[k] = 0.0;
+    }
+    t.begin.resize(size_t(max_launches));
+    t.end.resize(size_t(max_launches));
+    t.kind.assign(size_t(max_launches), 0);
+    for (int i = 0; i < max_launches; ++i) {
+        if (hipEventCreate(&t.begin[size_t(i)]) != hipSuccess || hipEventCreate(&t.end[size_t(i)]) != hipSuccess) {
+            t.begin.resize(size_t(i));
+            t.end.resize(size_t(i));
+            destroy_events(t);
+            return AMSIM_ERR_HIP;
+        }
+    }
+    t.active = true;
+    return AMSIM_OK;
+}
+
+int amsim_profile_stop(void)
+{
+    KernelTimer &t = timer();
+    std::lock_guard<std::mutex> g(t.mu);
+    t.active = false;
+    int rc = AMSIM_OK;
+    for (size_t i = 0; i < t.used; ++i) {
+        float ms = 0.f;
+        if (hipEventSynchronize(t.end[i]) != hipSuccess || hipEventElapsedTime(&ms, t.begin[i], t.end[i]) != hipSuccess) {
+            rc = AMSIM_ERR_HIP;
+            continue;
+        }
+        t.launches[t.kind[i]] += 1;
+        t.total_ms[t.kind[i]] += double(ms);
+    }
+    t.used = 0;
+    return rc;
+}
+
+int amsim_profile_read(int kind, int *launches, double *total_ms)
+{
+    if (kind < 0 || kind > 3 || !launches || !total_ms) return AMSIM_ERR_INVALID_ARG;
+    KernelTimer &t = timer();
+    std::lock_guard<std::mutex> g(t.mu);
+    *launches = t.launches[kind];
+    *total_ms = t.total_ms[kind];
+    return AMSIM_OK;
 }
 
 }  // extern "C"
