@@ -254,6 +254,217 @@ __global__ __launch_bounds__(kThreads) void gemm_kernel(const uint32_t *__restri
     }
 }
 
+// ------------------------------------------------------------------ GEMM, per-column tables
+// For M <= 7 the fastest form keeps, per k-step and output column j, the table row selected
+// by that column's second-operand mantissa kb(k, j) -- LUT[. ][kb], indexed by the first
+// operand's mantissa -- at a fixed LDS address.  Lanes then gather with
+//   ds_read  v, (lane's first-operand mantissa * entry bytes)  offset:(fixed row address)
+// so no per-product address arithmetic is left: per product one LDS gather, one multiply
+// (pa * pb) and one fma.  Rows are copied from a transposed copy of the table in global
+// memory, slab by slab (KS k-steps), double-buffered with one barrier per slab.
+//
+// Rows are stored compressed when the table allows it without loss: 1 byte per entry when
+// every entry's low 16 mantissa bits are zero (e.g. Mitchell at M <= 7), 2 bytes when the low 8
+// are zero (e.g. the exact truncated product at M <= 7), else the 4-byte rebiased float.  A
+// 128-entry row of bytes spans exactly the 32 LDS banks once, so its gathers are conflict-free.
+// The entry width is decided on the device by the table-preparation kernel and read by the
+// GEMM kernel, which runs the matching specialisation.
+
+constexpr int kTabRowEntries = 128;  // rows padded to 2^7 entries
+
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+
+template <int EB>
+__device__ __forceinline__ float tab_value(const unsigned char *p)
+{
+    if constexpr (EB == 1)
+        return __uint_as_float((uint32_t(*p) << 16) + 0x3F800000u);
+    else if constexpr (EB == 2)
+        return __uint_as_float((uint32_t(*reinterpret_cast<const uint16_t *>(p)) << 8) + 0x3F800000u);
+    else
+        return *reinterpret_cast<const float *>(p);
+}
+
+// Transposed, width-reduced table: dst row kb (kTabRowEntries * EB bytes) holds entry
+// (ka, kb) at byte ka * EB.  One workgroup; *eb_out receives the entry width chosen.
+__global__ __launch_bounds__(1024) void prep_rows_kernel(const uint32_t *__restrict__ lut, int m,
+                                                         unsigned char *__restrict__ dst, int *__restrict__ eb_out)
+{
+    __shared__ uint32_t low_bits;
+    if (threadIdx.x == 0) low_bits = 0u;
+    __syncthreads();
+    const int n = 1 << m, total = n * n;
+    uint32_t acc = 0u;
+    for (int i = threadIdx.x; i < total; i += blockDim.x) acc |= lut[i] & 0xFFFFu;
+    atomicOr(&low_bits, acc);
+    __syncthreads();
+    const uint32_t lb = low_bits;
+    const int eb = lb == 0u ? 1 : ((lb & 0xFFu) == 0u ? 2 : 4);
+    for (int i = threadIdx.x; i < total; i += blockDim.x) {
+        const int ka = i / n, kb = i % n;
+        const uint32_t e = lut[i] & 0x00FFFFFFu;
+        unsigned char *row = dst + size_t(kb) * kTabRowEntries * eb;
+        if (eb == 1)
+            row[ka] = static_cast<unsigned char>(e >> 16);
+        else if (eb == 2)
+            reinterpret_cast<uint16_t *>(row)[ka] = static_cast<uint16_t>(e >> 8);
+        else
+            reinterpret_cast<uint32_t *>(row)[ka] = e + 0x3F800000u;
+    }
+    if (threadIdx.x == 0) *eb_out = eb;
+}
+
+// Slab staging for the per-column-table kernels: each thread copies CPT 16-byte pieces of the
+// rows selected by the second operand's mantissas (kb), plus that operand's head (pb).
+template <int TN, int EB, int CPT>
+__device__ __forceinline__ void tab_fetch(u32x4 (&stage)[CPT], float (&stage_pb)[CPT], int k0, int kend,
+                                          const uint32_t *__restrict__ Bd, int Np, int col0,
+                                          const unsigned char *__restrict__ rows)
+{
+    constexpr int ROWB = kTabRowEntries * EB;
+    constexpr int PIECES = ROWB / 16;
+#pragma unroll
+    for (int i = 0; i < CPT; ++i) {
+        const int c = threadIdx.x + i * kThreads;
+        const int slot = c / (TN * PIECES);
+        const int t = (c / PIECES) % TN;
+        const int piece = c % PIECES;
+        const int k = k0 + slot;
+        const uint32_t bw = k < kend ? Bd[int64_t(k) * Np + col0 + t] : 0u;
+        stage_pb[i] = head_value(bw);
+        stage[i] = *reinterpret_cast<const u32x4 *>(rows + (bw & kIdxMask) * ROWB + piece * 16);
+    }
+}
+
+template <int TN, int EB, int CPT>
+__device__ __forceinline__ void tab_commit(const u32x4 (&stage)[CPT], const float (&stage_pb)[CPT],
+                                           unsigned char *smem, float *pbs, int buf)
+{
+    constexpr int ROWB = kTabRowEntries * EB;
+    constexpr int KS = 8 / EB;
+    constexpr int SLAB = KS * TN * ROWB;
+    constexpr int PIECES = ROWB / 16;
+#pragma unroll
+    for (int i = 0; i < CPT; ++i) {
+        const int c = threadIdx.x + i * kThreads;
+        *reinterpret_cast<u32x4 *>(smem + buf * SLAB + c * 16) = stage[i];
+        if (c % PIECES == 0) pbs[buf * KS * TN + c / PIECES] = stage_pb[i];
+    }
+}
+
+// Ad: decoded op(A) k-major [K][Mp], idx field = ka.  Bd: decoded op(B) [K][Np], idx = kb.
+// Workgroup: 4 waves on consecutive row blocks (64*TM rows each) sharing TN columns.
+template <int TM, int TN, int EB>
+__device__ __forceinline__ void gemm_tab_body(const uint32_t *__restrict__ Ad, int Mp, const uint32_t *__restrict__ Bd,
+                                              int Np, int M, int N, int K, int kchunk, float *__restrict__ out,
+                                              int64_t ldc, const unsigned char *__restrict__ rows)
+{
+    constexpr int ROWB = kTabRowEntries * EB;
+    constexpr int KS = 8 / EB;                  // k-steps per slab: every slab is 8*TN*128 bytes
+    constexpr int SLAB = KS * TN * ROWB;
+    constexpr int PIECES = ROWB / 16;           // 16-byte pieces per row
+    constexpr int CPT = SLAB / 16 / kThreads;   // pieces per thread per slab
+    static_assert(CPT * 16 * kThreads == SLAB, "slab must split evenly over the workgroup");
+    extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
+    float *pbs = reinterpret_cast<float *>(smem + 2 * SLAB);  // [2][KS][TN] second-operand heads
+
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int row0 = blockIdx.x * (64 * TM * kWaves) + wave_id() * (64 * TM) + lane;
+    const int col0 = blockIdx.y * TN;
+    const int kbeg = blockIdx.z * kchunk;
+    const int kend = min(K, kbeg + kchunk);
+    const int nslab = (kend - kbeg + KS - 1) / KS;
+
+    u32x4 stage[CPT];
+    float stage_pb[CPT];
+    float acc[TM][TN];
+    init_acc(acc);
+    if (nslab > 0) {
+        tab_fetch<TN, EB, CPT>(stage, stage_pb, kbeg, kend, Bd, Np, col0, rows);
+        tab_commit<TN, EB, CPT>(stage, stage_pb, smem, pbs, 0);
+    }
+    __syncthreads();
+    // first-operand words of the current k-step; the next step's are loaded one step ahead
+    uint32_t acur[TM];
+#pragma unroll
+    for (int r = 0; r < TM; ++r) acur[r] = nslab > 0 ? Ad[int64_t(kbeg) * Mp + row0 + 64 * r] : 0u;
+    for (int s = 0; s < nslab; ++s) {
+        const int k0 = kbeg + s * KS;
+        if (s + 1 < nslab) tab_fetch<TN, EB, CPT>(stage, stage_pb, k0 + KS, kend, Bd, Np, col0, rows);
+        const unsigned char *tb = smem + (s & 1) * SLAB;
+        const float *pb_s = pbs + (s & 1) * KS * TN;
+#pragma unroll
+        for (int slot = 0; slot < KS; ++slot) {
+            const int k = k0 + slot;
+            if (k >= kend) break;
+            uint32_t anext[TM];
+            const bool more = k + 1 < kend;
+#pragma unroll
+            for (int r = 0; r < TM; ++r) anext[r] = more ? Ad[int64_t(k + 1) * Mp + row0 + 64 * r] : 0u;
+            const unsigned char *vaddr[TM];
+            float pa[TM];
+#pragma unroll
+            for (int r = 0; r < TM; ++r) {
+                vaddr[r] = tb + (acur[r] & kIdxMask) * EB;
+                pa[r] = head_value(acur[r]);
+            }
+#pragma unroll
+            for (int t = 0; t < TN; ++t) {
+                const float pb = pb_s[slot * TN + t];
+#pragma unroll
+                for (int r = 0; r < TM; ++r) {
+                    const float v = tab_value<EB>(vaddr[r] + (slot * TN + t) * ROWB);
+                    acc[r][t] = __builtin_fmaf(v, pa[r] * pb, acc[r][t]);
+                }
+            }
+#pragma unroll
+            for (int r = 0; r < TM; ++r) acur[r] = anext[r];
+        }
+        if (s + 1 < nslab) tab_commit<TN, EB, CPT>(stage, stage_pb, smem, pbs, (s + 1) & 1);
+        __syncthreads();
+    }
+
+    float *dst = out;
+    int64_t ld = ldc;
+    if (gridDim.z > 1) {
+        dst = out + int64_t(blockIdx.z) * M * N;
+        ld = N;
+    }
+#pragma unroll
+    for (int r = 0; r < TM; ++r) {
+        const int row = row0 + 64 * r;
+        if (row >= M) continue;
+#pragma unroll
+        for (int t = 0; t < TN; ++t) {
+            const int col = col0 + t;
+            if (col < N) dst[int64_t(row) * ld + col] = acc[r][t];
+        }
+    }
+}
+
+template <int TM, int TN>
+__global__ __launch_bounds__(kThreads) void gemm_tab_kernel(const uint32_t *__restrict__ Ad, int Mp,
+                                                            const uint32_t *__restrict__ Bd, int Np, int M, int N,
+                                                            int K, int kchunk, float *__restrict__ out, int64_t ldc,
+                                                            const unsigned char *__restrict__ rows,
+                                                            const int *__restrict__ eb_ptr)
+{
+    const int eb = __builtin_amdgcn_readfirstlane(*eb_ptr);
+    if (eb == 1)
+        gemm_tab_body<TM, TN, 1>(Ad, Mp, Bd, Np, M, N, K, kchunk, out, ldc, rows);
+    else if (eb == 2)
+        gemm_tab_body<TM, TN, 2>(Ad, Mp, Bd, Np, M, N, K, kchunk, out, ldc, rows);
+    else
+        gemm_tab_body<TM, TN, 4>(Ad, Mp, Bd, Np, M, N, K, kchunk, out, ldc, rows);
+}
+
+template <int TN>
+constexpr size_t tab_lds_bytes()
+{
+    return size_t(2) * 8 * TN * kTabRowEntries + size_t(2) * 8 * TN * 4;
+}
+
 // ------------------------------------------------------------------ convolution kernels --
 
 struct ConvShape {
@@ -509,6 +720,12 @@ void allow_big_lds(K kernel)
 
 void set_attributes()
 {
+    allow_big_lds(gemm_tab_kernel<4, 8>);
+    allow_big_lds(gemm_tab_kernel<2, 8>);
+    allow_big_lds(gemm_tab_kernel<1, 8>);
+    allow_big_lds(gemm_tab_kernel<4, 4>);
+    allow_big_lds(gemm_tab_kernel<2, 4>);
+    allow_big_lds(gemm_tab_kernel<1, 4>);
 #define X(TM, TN)                                          \
     allow_big_lds(gemm_kernel<TM, TN, true>);              \
     allow_big_lds(conv_fwd_kernel<TM, TN, true>);          \
@@ -544,16 +761,49 @@ struct Plan {
 
 bool valid_m(int m_bits) { return m_bits >= 1 && m_bits <= 11; }
 
+// Per-column-table GEMM tile: 4 waves x 64*TM rows per workgroup, TN shared columns.  Chosen
+// from measurements on MI355X (4096^3): TM = 4, TN = 8 keeps the kernel at 4 waves per SIMD
+// (~120 VGPRs) with enough register tiling; larger tiles drop occupancy and lose more to
+// latency than they save in operand loads.
+Tile choose_tab_tile(int64_t rows, int64_t cols, int64_t red)
+{
+    Tile t;
+    t.tn = cols > 4 ? 8 : 4;
+    const int64_t col_tiles = ceil_div(cols, t.tn);
+    t.tm = 1;
+    for (int tm : {4, 2}) {
+        if (ceil_div(rows, int64_t(64) * kWaves * tm) * col_tiles >= 2 * kTargetWgs) {
+            t.tm = tm;
+            break;
+        }
+    }
+    const int64_t tiles = ceil_div(rows, int64_t(64) * kWaves * t.tm) * col_tiles;
+    t.split = 1;
+    if (tiles < kTargetWgs) {
+        const int64_t max_split = std::max<int64_t>(1, red / 256);
+        t.split = int(std::min<int64_t>(std::min<int64_t>(ceil_div(kTargetWgs, tiles), max_split), 1024));
+    }
+    return t;
+}
+
+constexpr size_t kRowsBytes = size_t(kTabRowEntries) * kTabRowEntries * 4;  // widest transposed table
+
 Plan plan_gemm(int64_t m, int64_t n, int64_t k, int m_bits)
 {
     Plan p{};
-    p.tile = choose_tile(m, n, k, 1, true);
     p.lds = lds_path(m_bits);
-    p.a_ld = round_up(m, 64 * p.tile.tm);
-    p.b_ld = round_up(n, int64_t(p.tile.tn) * kWaves);
     size_t o = 0;
     p.off_table = o;
-    if (p.lds) o += align_up(table_bytes(m_bits));
+    if (p.lds) {
+        p.tile = choose_tab_tile(m, n, k);
+        p.a_ld = round_up(m, int64_t(64) * kWaves * p.tile.tm);
+        p.b_ld = round_up(n, p.tile.tn);
+        o += align_up(kRowsBytes) + kAlign;  // transposed rows + entry-width word
+    } else {
+        p.tile = choose_tile(m, n, k, 1, true);
+        p.a_ld = round_up(m, 64 * p.tile.tm);
+        p.b_ld = round_up(n, int64_t(p.tile.tn) * kWaves);
+    }
     p.off_a = o;
     o += align_up(size_t(k) * p.a_ld * 4);
     p.off_b = o;
@@ -664,6 +914,18 @@ void launch_gemm_t(dim3 grid, hipStream_t st, const uint32_t *Ad, int Mp, const 
                        out, ldc, table, entries);
 }
 
+template <typename F>
+void dispatch_tab_tile(const Tile &t, F &&f)
+{
+#define X(TM, TN)                                                                \
+    if (t.tm == TM && t.tn == TN) {                                              \
+        f(std::integral_constant<int, TM>{}, std::integral_constant<int, TN>{}); \
+        return;                                                                  \
+    }
+    X(4, 8) X(2, 8) X(1, 8) X(4, 4) X(2, 4) X(1, 4)
+#undef X
+}
+
 template <bool LDS, typename F>
 void dispatch_tile(const Tile &t, F &&f)
 {
@@ -706,7 +968,7 @@ class TimedLaunch {
         if (t.active && t.used < t.begin.size()) {
             slot_ = long(t.used++);
             t.kind[size_t(slot_)] = kind;
-            hipEventRecord(t.begin[size_t(slot_)], st_);
+            (void)hipEventRecord(t.begin[size_t(slot_)], st_);
         }
     }
     ~TimedLaunch()
@@ -714,7 +976,7 @@ class TimedLaunch {
         if (slot_ < 0) return;
         KernelTimer &t = timer();
         std::lock_guard<std::mutex> g(t.mu);
-        hipEventRecord(t.end[size_t(slot_)], st_);
+        (void)hipEventRecord(t.end[size_t(slot_)], st_);
     }
 
   private:
@@ -724,8 +986,8 @@ class TimedLaunch {
 
 void destroy_events(KernelTimer &t)
 {
-    for (hipEvent_t e : t.begin) hipEventDestroy(e);
-    for (hipEvent_t e : t.end) hipEventDestroy(e);
+    for (hipEvent_t e : t.begin) (void)hipEventDestroy(e);
+    for (hipEvent_t e : t.end) (void)hipEventDestroy(e);
     t.begin.clear();
     t.end.clear();
     t.kind.clear();
@@ -772,41 +1034,50 @@ int approx_gemm(int trans_a, int trans_b, int64_t m, int64_t n, int64_t k, const
     if (lda < (trans_a ? m : k) || ldb < (trans_b ? k : n)) return AMSIM_ERR_INVALID_ARG;
     const Plan p = plan_gemm(m, n, k, m_bits);
     if (k * p.a_ld >= lim || k * p.b_ld >= lim || int64_t(p.tile.split) * m * n >= lim ||
-        p.b_ld / (int64_t(p.tile.tn) * kWaves) > 65535)
+        p.b_ld / (int64_t(p.tile.tn) * (p.lds ? 1 : kWaves)) > 65535)
         return AMSIM_ERR_UNSUPPORTED;
     if (p.total > 0 && (!workspace || workspace_bytes < p.total)) return AMSIM_ERR_WORKSPACE;
     if (p.lds && ensure_attributes() != AMSIM_OK) return AMSIM_ERR_HIP;
     char *ws = static_cast<char *>(workspace);
-    const uint32_t *table;
-    if (prep_table(lut, m_bits, ws, p, st, &table) != AMSIM_OK) return AMSIM_ERR_HIP;
-
     uint32_t *Ad = reinterpret_cast<uint32_t *>(ws + p.off_a);
     uint32_t *Bd = reinterpret_cast<uint32_t *>(ws + p.off_b);
-    // op(A)(i, kk): row stride / column stride in A's storage
-    const int64_t a_sr = trans_a ? 1 : lda, a_sc = trans_a ? lda : 1;
-    hipLaunchKernelGGL(decode_t_kernel, dim3(unsigned(ceil_div(p.a_ld, 64)), unsigned(std::min<int64_t>(ceil_div(k, 64), 4096))), dim3(256), 0,
-                       st, A, a_sr, a_sc, int(m), int(k), Ad, int(p.a_ld), m_bits, shift_first(m_bits));
-    const int64_t b_sr = trans_b ? 1 : ldb, b_sc = trans_b ? ldb : 1;
-    hipLaunchKernelGGL(decode_kernel, dim3(grid_for(k * p.b_ld)), dim3(256), 0, st, B, int64_t(0), b_sr, b_sc, 1,
-                       int(k), int(n), Bd, int(p.b_ld), m_bits, shift_second(m_bits));
-    if (launch_status() != AMSIM_OK) return AMSIM_ERR_HIP;
-
     const Tile t = p.tile;
     const int kchunk = int(ceil_div(k, t.split));
     const int splits = int(ceil_div(k, kchunk));
-    dim3 grid(unsigned(p.a_ld / (64 * t.tm)), unsigned(p.b_ld / (int64_t(t.tn) * kWaves)), unsigned(splits));
     float *out = splits > 1 ? reinterpret_cast<float *>(ws + p.off_part) : C;
-    auto run = [&](auto tm, auto tn) {
-        if (p.lds)
-            launch_gemm_t<decltype(tm)::value, decltype(tn)::value, true>(grid, st, Ad, int(p.a_ld), Bd, int(p.b_ld),
-                                                                          int(m), int(n), int(k), kchunk, out, ldc,
-                                                                          table, m_bits);
-        else
+    // op(A)(i, kk): row stride / column stride in A's storage
+    const int64_t a_sr = trans_a ? 1 : lda, a_sc = trans_a ? lda : 1;
+    const int64_t b_sr = trans_b ? 1 : ldb, b_sc = trans_b ? ldb : 1;
+    const dim3 grid_dt(unsigned(ceil_div(p.a_ld, 64)), unsigned(std::min<int64_t>(ceil_div(k, 64), 4096)));
+    if (p.lds) {
+        unsigned char *rows = reinterpret_cast<unsigned char *>(ws + p.off_table);
+        int *eb = reinterpret_cast<int *>(ws + p.off_table + align_up(kRowsBytes));
+        hipLaunchKernelGGL(prep_rows_kernel, dim3(1), dim3(1024), 0, st, lut, m_bits, rows, eb);
+        hipLaunchKernelGGL(decode_t_kernel, grid_dt, dim3(256), 0, st, A, a_sr, a_sc, int(m), int(k), Ad, int(p.a_ld),
+                           m_bits, 0);
+        hipLaunchKernelGGL(decode_kernel, dim3(grid_for(k * p.b_ld)), dim3(256), 0, st, B, int64_t(0), b_sr, b_sc, 1,
+                           int(k), int(n), Bd, int(p.b_ld), m_bits, 0);
+        if (launch_status() != AMSIM_OK) return AMSIM_ERR_HIP;
+        dim3 grid(unsigned(p.a_ld / (int64_t(64) * kWaves * t.tm)), unsigned(p.b_ld / t.tn), unsigned(splits));
+        auto run = [&](auto tm, auto tn) {
+            constexpr int TM = decltype(tm)::value, TN = decltype(tn)::value;
+            hipLaunchKernelGGL((gemm_tab_kernel<TM, TN>), grid, dim3(kThreads), tab_lds_bytes<TN>(), st, Ad,
+                               int(p.a_ld), Bd, int(p.b_ld), int(m), int(n), int(k), kchunk, out, ldc, rows, eb);
+        };
+        TimedLaunch tl(AMSIM_KERNEL_GEMM, st);
+        dispatch_tab_tile(t, run);
+    } else {
+        hipLaunchKernelGGL(decode_t_kernel, grid_dt, dim3(256), 0, st, A, a_sr, a_sc, int(m), int(k), Ad, int(p.a_ld),
+                           m_bits, shift_first(m_bits));
+        hipLaunchKernelGGL(decode_kernel, dim3(grid_for(k * p.b_ld)), dim3(256), 0, st, B, int64_t(0), b_sr, b_sc, 1,
+                           int(k), int(n), Bd, int(p.b_ld), m_bits, shift_second(m_bits));
+        if (launch_status() != AMSIM_OK) return AMSIM_ERR_HIP;
+        dim3 grid(unsigned(p.a_ld / (64 * t.tm)), unsigned(p.b_ld / (int64_t(t.tn) * kWaves)), unsigned(splits));
+        auto run = [&](auto tm, auto tn) {
             launch_gemm_t<decltype(tm)::value, decltype(tn)::value, false>(grid, st, Ad, int(p.a_ld), Bd, int(p.b_ld),
                                                                            int(m), int(n), int(k), kchunk, out, ldc,
-                                                                           table, m_bits);
-    };
-    {
+                                                                           lut, m_bits);
+        };
         TimedLaunch tl(AMSIM_KERNEL_GEMM, st);
         dispatch_tile<true>(t, run);
     }
