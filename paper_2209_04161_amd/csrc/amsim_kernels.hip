@@ -121,17 +121,6 @@ __device__ __forceinline__ int wave_id() { return __builtin_amdgcn_readfirstlane
 
 // ------------------------------------------------------------------ pre-pass kernels -----
 
-// Transposed, rebiased copy of the table: out[j * n + k] = (lut[k * n + j] & 0xFFFFFF) + 0x3F800000.
-__global__ void prep_table_kernel(const uint32_t *__restrict__ lut, uint32_t *__restrict__ out, int m)
-{
-    const int n = 1 << m;
-    const int total = n * n;
-    for (int i = blockIdx.x * blockDim.x + threadIdx.x; i < total; i += gridDim.x * blockDim.x) {
-        const int k = i / n, j = i % n;
-        out[j * n + k] = (lut[i] & 0x00FFFFFFu) + 0x3F800000u;
-    }
-}
-
 // dst[(b * rows + r) * dld + c] = decode(src[b * sb + r * sr + c * sc]) for r < rows, c < cols;
 // padding columns c in [cols, dld) are written as decoded +0.
 __global__ void decode_kernel(const float *__restrict__ src, int64_t sb, int64_t sr, int64_t sc, int batches,
@@ -147,6 +136,46 @@ __global__ void decode_kernel(const float *__restrict__ src, int64_t sb, int64_t
         uint32_t w = 0u;
         if (c < cols) w = amsim_decode(__float_as_uint(src[b * sb + int64_t(r) * sr + int64_t(c) * sc]), m, shift);
         dst[i] = w;
+    }
+}
+
+// Decoded NHWC tensor inside a zero border: dst[n][hp][wp][c] = decode(src[n][hp-top][wp-left][c])
+// where that pixel exists, decoded +0 elsewhere.
+__global__ void decode_pad_kernel(const float *__restrict__ src, int n, int h, int w, int c, int top, int left,
+                                  int hp, int wp, uint32_t *__restrict__ dst, int m, int shift)
+{
+    const int64_t total = int64_t(n) * hp * wp * c;
+    for (int64_t i = int64_t(blockIdx.x) * blockDim.x + threadIdx.x; i < total;
+         i += int64_t(gridDim.x) * blockDim.x) {
+        const int ch = int(i % c);
+        const int64_t pix = i / c;
+        const int x = int(pix % wp), y = int((pix / wp) % hp), b = int(pix / (int64_t(wp) * hp));
+        const int ih = y - top, iw = x - left;
+        uint32_t word = 0u;
+        if (unsigned(ih) < unsigned(h) && unsigned(iw) < unsigned(w))
+            word = amsim_decode(__float_as_uint(src[((int64_t(b) * h + ih) * w + iw) * c + ch]), m, shift);
+        dst[i] = word;
+    }
+}
+
+// Decoded NHWC tensor re-laid out as [n][hp][c][wp] inside a zero border:
+// dst[n][y][ch][x] = decode(src[n][y-top][x-left][ch]) where that pixel exists, decoded +0 elsewhere.
+__global__ void decode_pad_nhcw_kernel(const float *__restrict__ src, int n, int h, int w, int c, int top, int left,
+                                       int hp, int wp, uint32_t *__restrict__ dst, int m, int shift)
+{
+    const int64_t total = int64_t(n) * hp * wp * c;
+    for (int64_t i = int64_t(blockIdx.x) * blockDim.x + threadIdx.x; i < total;
+         i += int64_t(gridDim.x) * blockDim.x) {
+        const int x = int(i % wp);
+        const int64_t rest = i / wp;
+        const int ch = int(rest % c);
+        const int64_t r2 = rest / c;
+        const int y = int(r2 % hp), b = int(r2 / hp);
+        const int ih = y - top, iw = x - left;
+        uint32_t word = 0u;
+        if (unsigned(ih) < unsigned(h) && unsigned(iw) < unsigned(w))
+            word = amsim_decode(__float_as_uint(src[((int64_t(b) * h + ih) * w + iw) * c + ch]), m, shift);
+        dst[i] = word;
     }
 }
 
@@ -314,10 +343,156 @@ __global__ __launch_bounds__(1024) void prep_rows_kernel(const uint32_t *__restr
     if (threadIdx.x == 0) *eb_out = eb;
 }
 
-// Slab staging for the per-column-table kernels: each thread copies CPT 16-byte pieces of the
-// rows selected by the second operand's mantissas (kb), plus that operand's head (pb).
+struct ConvShape {
+    int n, h, w, ci, co, kh, kw, sh, sw, pt, pl, oh, ow;
+};
+
+// Which operation the table kernel evaluates.  Every one is a sum over "taps": runs of
+// consecutive reduction steps j = 0 .. count-1 whose first-operand word sits at
+//   A[lane row base + ubase + j * ustride]
+// and whose second-operand row is Bd[bbase + j].
+//   GEMM         tap = split z: rows i, A = op(A) k-major, row base i, ubase = kbeg * Mp
+//   FWD          tap = (kh, kw): rows (n, oh, ow), A = zero-padded x stored [n][h][ci][w], j = ci
+//   BWD_DATA     tap = valid (kh, kw) of the stride phase in blockIdx.z: rows (n, hq, wq),
+//                A = zero-padded dy stored [n][h][co][w], j = co; weights read as [kh][kw][co][ci]
+//   BWD_WEIGHT   tap = output row (n, oh): rows (kh, kw, ci), A = zero-padded x (NHWC), j = ow,
+//                B = dy
+// The channel-inside-row layouts put the lanes' consecutive output pixels on consecutive words,
+// so each first-operand load of a wave touches a few cache lines instead of 64.
+enum { OP_GEMM = 0, OP_FWD = 1, OP_BWD_DATA = 2, OP_BWD_WEIGHT = 3 };
+
+struct TabArgs {
+    const uint32_t *A;   // decoded first operand
+    uint32_t a_bytes;    // its size in bytes (buffer range: reads beyond return 0)
+    const uint32_t *Bd;  // decoded second operand rows, leading dimension Np
+    int Np;
+    float *out;          // result, or split partial sums [z][R][N]
+    int64_t ldc;         // GEMM result leading dimension
+    const unsigned char *rows;
+    const int *eb;
+    int R, N;            // result rows and columns
+    int taps;            // taps in total (GEMM: number of splits)
+    int taps_per_split;  // taps per blockIdx.z (BWD_WEIGHT split reduction); phases for BWD_DATA use z
+    int Mp, K, kchunk;   // GEMM
+    ConvShape s;
+    int Hp, Wp;          // zero-padded x (FWD, BWD_WEIGHT)
+    int OHp, OWp, pad_oh, pad_ow;  // zero-padded dy (BWD_DATA)
+};
+
+struct TabTap {
+    int ubase, ustride, bbase, count;
+};
+
+// Rows of one stride phase of the backward-data pass.
+__device__ __forceinline__ void phase_dims(const ConvShape &s, int ph, int pw, int &hq_n, int &wq_n)
+{
+    hq_n = ph < s.h ? (s.h - ph + s.sh - 1) / s.sh : 0;
+    wq_n = pw < s.w ? (s.w - pw + s.sw - 1) / s.sw : 0;
+}
+
+template <int OP>
+__device__ __forceinline__ int tab_rows(const TabArgs &a)
+{
+    if constexpr (OP == OP_BWD_DATA) {
+        int hq_n, wq_n;
+        phase_dims(a.s, int(blockIdx.z) / a.s.sw, int(blockIdx.z) % a.s.sw, hq_n, wq_n);
+        return a.s.n * hq_n * wq_n;
+    } else {
+        return a.R;
+    }
+}
+
+// Lane row -> (first-operand element offset of the row, result element offset).
+template <int OP>
+__device__ __forceinline__ void tab_row(const TabArgs &a, int row, int &abase, int64_t &obase)
+{
+    const ConvShape &s = a.s;
+    if constexpr (OP == OP_GEMM) {
+        abase = row;
+        obase = int64_t(row) * a.ldc;
+    } else if constexpr (OP == OP_FWD) {
+        const int ow = row % s.ow, oh = (row / s.ow) % s.oh, n = row / (s.ow * s.oh);
+        abase = (n * a.Hp + oh * s.sh) * s.ci * a.Wp + ow * s.sw;  // x as [n][hp][ci][wp]
+        obase = int64_t(row) * s.co;
+    } else if constexpr (OP == OP_BWD_DATA) {
+        const int ph = int(blockIdx.z) / s.sw, pw = int(blockIdx.z) % s.sw;
+        int hq_n, wq_n;
+        phase_dims(s, ph, pw, hq_n, wq_n);
+        const int wq = row % wq_n, hq = (row / wq_n) % hq_n, n = row / (wq_n * hq_n);
+        abase = (n * a.OHp + hq) * s.co * a.OWp + wq;  // dy as [n][ohp][co][owp]; pads in the tap offset
+        obase = (int64_t(n * s.h + hq * s.sh + ph) * s.w + wq * s.sw + pw) * s.ci;
+    } else {
+        const int ci = row % s.ci, kw = (row / s.ci) % s.kw, kh = row / (s.ci * s.kw);
+        abase = (kh * a.Wp + kw) * s.ci + ci;
+        obase = int64_t(row) * s.co;
+    }
+}
+
+// Tap range of this workgroup.
+template <int OP>
+__device__ __forceinline__ void tab_tap_range(const TabArgs &a, int &t0, int &t1)
+{
+    if constexpr (OP == OP_GEMM) {
+        t0 = int(blockIdx.z);
+        t1 = t0 + 1;
+    } else if constexpr (OP == OP_BWD_WEIGHT) {
+        t0 = int(blockIdx.z) * a.taps_per_split;
+        t1 = min(a.taps, t0 + a.taps_per_split);
+    } else if constexpr (OP == OP_BWD_DATA) {
+        const ConvShape &s = a.s;
+        const int ph = int(blockIdx.z) / s.sw, pw = int(blockIdx.z) % s.sw;
+        const int kh0 = (ph + s.pt) % s.sh, kw0 = (pw + s.pl) % s.sw;
+        const int nvh = kh0 < s.kh ? (s.kh - kh0 + s.sh - 1) / s.sh : 0;
+        const int nvw = kw0 < s.kw ? (s.kw - kw0 + s.sw - 1) / s.sw : 0;
+        t0 = 0;
+        t1 = nvh * nvw;
+    } else {
+        t0 = 0;
+        t1 = a.s.kh * a.s.kw;
+    }
+}
+
+template <int OP>
+__device__ __forceinline__ TabTap tab_tap(const TabArgs &a, int tap)
+{
+    const ConvShape &s = a.s;
+    TabTap t;
+    if constexpr (OP == OP_GEMM) {
+        const int kbeg = tap * a.kchunk;
+        t.count = min(a.kchunk, a.K - kbeg);
+        t.ubase = kbeg * a.Mp;
+        t.ustride = a.Mp;
+        t.bbase = kbeg;
+    } else if constexpr (OP == OP_FWD) {
+        const int kh = tap / s.kw, kw = tap % s.kw;
+        t.count = s.ci;
+        t.ubase = kh * s.ci * a.Wp + kw;
+        t.ustride = a.Wp;
+        t.bbase = tap * s.ci;
+    } else if constexpr (OP == OP_BWD_DATA) {
+        const int ph = int(blockIdx.z) / s.sw, pw = int(blockIdx.z) % s.sw;
+        const int kh0 = (ph + s.pt) % s.sh, kw0 = (pw + s.pl) % s.sw;
+        const int nvw = (s.kw - kw0 + s.sw - 1) / s.sw;
+        const int kh = kh0 + (tap / nvw) * s.sh, kw = kw0 + (tap % nvw) * s.sw;
+        const int dh = (ph + s.pt - kh) / s.sh, dw = (pw + s.pl - kw) / s.sw;  // exact divisions
+        t.count = s.co;
+        t.ubase = (dh + a.pad_oh) * s.co * a.OWp + dw + a.pad_ow;  // >= 0: the padding covers every dh, dw
+        t.ustride = a.OWp;
+        t.bbase = (kh * s.kw + kw) * s.co;
+    } else {
+        const int n = tap / s.oh, oh = tap % s.oh;
+        t.count = s.ow;
+        t.ubase = (n * a.Hp + oh * s.sh) * a.Wp * s.ci;
+        t.ustride = s.sw * s.ci;
+        t.bbase = tap * s.ow;
+    }
+    return t;
+}
+
+// Slab staging: each thread copies CPT 16-byte pieces of the rows selected by the second
+// operand's mantissas (kb) for slots [0, nslots) of a slab, and that operand's head (pb).
 template <int TN, int EB, int CPT>
-__device__ __forceinline__ void tab_fetch(u32x4 (&stage)[CPT], float (&stage_pb)[CPT], int k0, int kend,
+__device__ __forceinline__ void tab_fetch(u32x4 (&stage)[CPT], float (&stage_pb)[CPT], const TabTap &tp, int c0,
                                           const uint32_t *__restrict__ Bd, int Np, int col0,
                                           const unsigned char *__restrict__ rows)
 {
@@ -329,8 +504,8 @@ __device__ __forceinline__ void tab_fetch(u32x4 (&stage)[CPT], float (&stage_pb)
         const int slot = c / (TN * PIECES);
         const int t = (c / PIECES) % TN;
         const int piece = c % PIECES;
-        const int k = k0 + slot;
-        const uint32_t bw = k < kend ? Bd[int64_t(k) * Np + col0 + t] : 0u;
+        const int j = c0 + slot;
+        const uint32_t bw = j < tp.count ? Bd[int64_t(tp.bbase + j) * Np + col0 + t] : 0u;
         stage_pb[i] = head_value(bw);
         stage[i] = *reinterpret_cast<const u32x4 *>(rows + (bw & kIdxMask) * ROWB + piece * 16);
     }
@@ -352,56 +527,91 @@ __device__ __forceinline__ void tab_commit(const u32x4 (&stage)[CPT], const floa
     }
 }
 
-// Ad: decoded op(A) k-major [K][Mp], idx field = ka.  Bd: decoded op(B) [K][Np], idx = kb.
-// Workgroup: 4 waves on consecutive row blocks (64*TM rows each) sharing TN columns.
-template <int TM, int TN, int EB>
-__device__ __forceinline__ void gemm_tab_body(const uint32_t *__restrict__ Ad, int Mp, const uint32_t *__restrict__ Bd,
-                                              int Np, int M, int N, int K, int kchunk, float *__restrict__ out,
-                                              int64_t ldc, const unsigned char *__restrict__ rows)
+// Workgroup: 4 waves on consecutive row blocks (64*TM rows each) sharing TN result columns.
+template <int OP, int TM, int TN, int EB>
+__device__ __forceinline__ void tab_body(const TabArgs &a)
 {
     constexpr int ROWB = kTabRowEntries * EB;
-    constexpr int KS = 8 / EB;                  // k-steps per slab: every slab is 8*TN*128 bytes
+    constexpr int KS = 8 / EB;                  // steps per slab: every slab is 8*TN*128 bytes
     constexpr int SLAB = KS * TN * ROWB;
-    constexpr int PIECES = ROWB / 16;           // 16-byte pieces per row
     constexpr int CPT = SLAB / 16 / kThreads;   // pieces per thread per slab
     static_assert(CPT * 16 * kThreads == SLAB, "slab must split evenly over the workgroup");
     extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
     float *pbs = reinterpret_cast<float *>(smem + 2 * SLAB);  // [2][KS][TN] second-operand heads
 
-    const int tid = threadIdx.x;
-    const int lane = tid & 63;
+    const int R = tab_rows<OP>(a);
+    if (int(blockIdx.x) * 64 * TM * kWaves >= R) return;  // uniform over the workgroup
+    const int lane = threadIdx.x & 63;
     const int row0 = blockIdx.x * (64 * TM * kWaves) + wave_id() * (64 * TM) + lane;
     const int col0 = blockIdx.y * TN;
-    const int kbeg = blockIdx.z * kchunk;
-    const int kend = min(K, kbeg + kchunk);
-    const int nslab = (kend - kbeg + KS - 1) / KS;
+    // First-operand reads are raw buffer loads: voffset = the lane row's byte offset (range-checked,
+    // reads past a_bytes return 0), soffset = the wave-uniform step offset, which every tap keeps
+    // non-negative and inside the tensor, since the hardware does not range-check it.
+    const __amdgpu_buffer_rsrc_t ares =
+        __builtin_amdgcn_make_buffer_rsrc(const_cast<uint32_t *>(a.A), 0, int(a.a_bytes), 0x00020000);
+
+    uint32_t aoff[TM];  // byte offset of each lane row's first-operand run
+    int64_t obase[TM];
+#pragma unroll
+    for (int r = 0; r < TM; ++r) {
+        const int row = row0 + 64 * r;
+        int ab = 0;
+        int64_t ob = 0;
+        if (row < R) tab_row<OP>(a, row, ab, ob);
+        aoff[r] = uint32_t(ab) * 4u;
+        obase[r] = ob;
+    }
+    int t0, t1;
+    tab_tap_range<OP>(a, t0, t1);
 
     u32x4 stage[CPT];
     float stage_pb[CPT];
     float acc[TM][TN];
     init_acc(acc);
-    if (nslab > 0) {
-        tab_fetch<TN, EB, CPT>(stage, stage_pb, kbeg, kend, Bd, Np, col0, rows);
+    uint32_t acur[TM];
+    TabTap cur{0, 0, 0, 0};
+    int c0 = 0;
+    bool have = t0 < t1;
+    if (have) {
+        cur = tab_tap<OP>(a, t0);
+        tab_fetch<TN, EB, CPT>(stage, stage_pb, cur, 0, a.Bd, a.Np, col0, a.rows);
         tab_commit<TN, EB, CPT>(stage, stage_pb, smem, pbs, 0);
+#pragma unroll
+        for (int r = 0; r < TM; ++r)
+            acur[r] = __builtin_amdgcn_raw_buffer_load_b32(ares, aoff[r], uint32_t(cur.ubase) * 4u, 0);
     }
     __syncthreads();
-    // first-operand words of the current k-step; the next step's are loaded one step ahead
-    uint32_t acur[TM];
-#pragma unroll
-    for (int r = 0; r < TM; ++r) acur[r] = nslab > 0 ? Ad[int64_t(kbeg) * Mp + row0 + 64 * r] : 0u;
-    for (int s = 0; s < nslab; ++s) {
-        const int k0 = kbeg + s * KS;
-        if (s + 1 < nslab) tab_fetch<TN, EB, CPT>(stage, stage_pb, k0 + KS, kend, Bd, Np, col0, rows);
-        const unsigned char *tb = smem + (s & 1) * SLAB;
-        const float *pb_s = pbs + (s & 1) * KS * TN;
+    int tap = t0;
+    int buf = 0;
+    while (have) {
+        // the slab after this one
+        TabTap nxt = cur;
+        int ntap = tap, nc0 = c0 + KS;
+        if (nc0 >= cur.count) {
+            ntap = tap + 1;
+            nc0 = 0;
+            if (ntap < t1) nxt = tab_tap<OP>(a, ntap);
+        }
+        const bool has_next = ntap < t1;
+        if (has_next) tab_fetch<TN, EB, CPT>(stage, stage_pb, nxt, nc0, a.Bd, a.Np, col0, a.rows);
+        const unsigned char *tb = smem + buf * SLAB;
+        const float *pb_s = pbs + buf * KS * TN;
+        const int nslots = min(KS, cur.count - c0);
 #pragma unroll
         for (int slot = 0; slot < KS; ++slot) {
-            const int k = k0 + slot;
-            if (k >= kend) break;
+            if (slot >= nslots) break;
+            // next step's first-operand words: this slab's next slot or the next slab's first
             uint32_t anext[TM];
-            const bool more = k + 1 < kend;
+            const bool in_slab = slot + 1 < nslots;
+            const uint32_t unext = in_slab ? uint32_t(cur.ubase + (c0 + slot + 1) * cur.ustride) * 4u
+                                           : uint32_t(nxt.ubase + nc0 * nxt.ustride) * 4u;
+            if (in_slab || has_next) {
 #pragma unroll
-            for (int r = 0; r < TM; ++r) anext[r] = more ? Ad[int64_t(k + 1) * Mp + row0 + 64 * r] : 0u;
+                for (int r = 0; r < TM; ++r) anext[r] = __builtin_amdgcn_raw_buffer_load_b32(ares, aoff[r], unext, 0);
+            } else {
+#pragma unroll
+                for (int r = 0; r < TM; ++r) anext[r] = 0u;
+            }
             const unsigned char *vaddr[TM];
             float pa[TM];
 #pragma unroll
@@ -421,42 +631,42 @@ __device__ __forceinline__ void gemm_tab_body(const uint32_t *__restrict__ Ad, i
 #pragma unroll
             for (int r = 0; r < TM; ++r) acur[r] = anext[r];
         }
-        if (s + 1 < nslab) tab_commit<TN, EB, CPT>(stage, stage_pb, smem, pbs, (s + 1) & 1);
+        if (has_next) tab_commit<TN, EB, CPT>(stage, stage_pb, smem, pbs, buf ^ 1);
         __syncthreads();
+        cur = nxt;
+        tap = ntap;
+        c0 = nc0;
+        buf ^= 1;
+        have = has_next;
     }
 
-    float *dst = out;
-    int64_t ld = ldc;
-    if (gridDim.z > 1) {
-        dst = out + int64_t(blockIdx.z) * M * N;
-        ld = N;
-    }
+    // results: split partial sums go to [z][R][N] (GEMM, BWD_WEIGHT with gridDim.z > 1)
+    const bool partial = (OP == OP_GEMM || OP == OP_BWD_WEIGHT) && gridDim.z > 1;
 #pragma unroll
     for (int r = 0; r < TM; ++r) {
         const int row = row0 + 64 * r;
-        if (row >= M) continue;
+        if (row >= R) continue;
+        float *dst = partial ? a.out + (int64_t(blockIdx.z) * R + row) * a.N : a.out + obase[r];
 #pragma unroll
         for (int t = 0; t < TN; ++t) {
             const int col = col0 + t;
-            if (col < N) dst[int64_t(row) * ld + col] = acc[r][t];
+            if (col < a.N) dst[col] = acc[r][t];
         }
     }
 }
 
-template <int TM, int TN>
-__global__ __launch_bounds__(kThreads) void gemm_tab_kernel(const uint32_t *__restrict__ Ad, int Mp,
-                                                            const uint32_t *__restrict__ Bd, int Np, int M, int N,
-                                                            int K, int kchunk, float *__restrict__ out, int64_t ldc,
-                                                            const unsigned char *__restrict__ rows,
-                                                            const int *__restrict__ eb_ptr)
+// Four waves per SIMD: the register budget (<= 128 VGPRs) the tiles are sized for.  Without the
+// hint the scheduler minimises registers and serialises the LDS gathers.
+template <int OP, int TM, int TN>
+__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(4, 4))) void tab_kernel(TabArgs a)
 {
-    const int eb = __builtin_amdgcn_readfirstlane(*eb_ptr);
+    const int eb = __builtin_amdgcn_readfirstlane(*a.eb);
     if (eb == 1)
-        gemm_tab_body<TM, TN, 1>(Ad, Mp, Bd, Np, M, N, K, kchunk, out, ldc, rows);
+        tab_body<OP, TM, TN, 1>(a);
     else if (eb == 2)
-        gemm_tab_body<TM, TN, 2>(Ad, Mp, Bd, Np, M, N, K, kchunk, out, ldc, rows);
+        tab_body<OP, TM, TN, 2>(a);
     else
-        gemm_tab_body<TM, TN, 4>(Ad, Mp, Bd, Np, M, N, K, kchunk, out, ldc, rows);
+        tab_body<OP, TM, TN, 4>(a);
 }
 
 template <int TN>
@@ -466,10 +676,6 @@ constexpr size_t tab_lds_bytes()
 }
 
 // ------------------------------------------------------------------ convolution kernels --
-
-struct ConvShape {
-    int n, h, w, ci, co, kh, kw, sh, sw, pt, pl, oh, ow;
-};
 
 // Forward: rows (n, oh, ow) on lanes, columns co.  Xd: decoded x (NHWC, first-operand idx),
 // Wd: decoded w as [kh*kw*ci][COp].
@@ -669,18 +875,16 @@ inline int64_t round_up(int64_t x, int64_t m) { return (x + m - 1) / m * m; }
 inline int64_t ceil_div(int64_t x, int64_t m) { return (x + m - 1) / m; }
 
 inline bool lds_path(int m_bits) { return m_bits <= kMaxLdsBits; }
-inline size_t table_bytes(int m_bits) { return size_t(4) << (2 * m_bits); }
 
-// Tile choice: TN = 16 uniform columns per wave for wide outputs, 4 for narrow ones; TM the
-// largest of 8/4/2/1 that still gives at least two workgroups per CU (or the smallest when
-// the problem is small).  Split the reduction when the tile grid is too small to fill the
-// chip and the reduction is long.
 struct Tile {
     int tm, tn, split;
 };
 
-constexpr int kTargetWgs = 512;  // 256 CUs x 2 workgroups (LDS: 2 x 64 KiB tables per CU)
+constexpr int kTargetWgs = 512;  // 256 CUs x 2 workgroups
 
+// Global-table kernels (M = 8..11): TN = 16 uniform columns per wave for wide outputs, 4 for
+// narrow ones; TM the largest of 8/4/2/1 that still gives two workgroups per CU; split the
+// reduction when the tile grid is too small to fill the chip and the reduction is long.
 Tile choose_tile(int64_t rows, int64_t cols, int64_t red, int64_t red_unit, bool allow_split)
 {
     Tile t;
@@ -704,34 +908,57 @@ Tile choose_tile(int64_t rows, int64_t cols, int64_t red, int64_t red_unit, bool
     return t;
 }
 
+// Per-column-table kernels (M <= 7): 4 waves x 64*TM rows per workgroup, TN shared columns.
+// Chosen from measurements on MI355X (GEMM 4096^3): TM = 4, TN = 8 keeps the kernel at 4 waves
+// per SIMD (~120 VGPRs) with enough register tiling; larger tiles drop occupancy and lose more
+// to latency than they save in operand loads.  `red` is the reduction length in steps and
+// `min_steps` the fewest steps a split may hold.
+Tile choose_tab_tile(int64_t rows, int64_t cols, int64_t red, int64_t min_steps, bool allow_split)
+{
+    Tile t;
+    t.tn = cols > 4 ? 8 : 4;
+    const int64_t col_tiles = ceil_div(cols, t.tn);
+    t.tm = 1;
+    for (int tm : {4, 2}) {
+        if (ceil_div(rows, int64_t(64) * kWaves * tm) * col_tiles >= 2 * kTargetWgs) {
+            t.tm = tm;
+            break;
+        }
+    }
+    const int64_t tiles = ceil_div(rows, int64_t(64) * kWaves * t.tm) * col_tiles;
+    t.split = 1;
+    if (allow_split && tiles < kTargetWgs) {
+        const int64_t max_split = std::max<int64_t>(1, red / std::max<int64_t>(1, min_steps));
+        t.split = int(std::min<int64_t>(std::min<int64_t>(ceil_div(kTargetWgs, tiles), max_split), 1024));
+    }
+    return t;
+}
+
 std::once_flag g_attr_once;
 hipError_t g_attr_err = hipSuccess;
 
 template <typename K>
-void allow_big_lds(K kernel)
+void allow_lds(K kernel, size_t bytes)
 {
     hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void *>(kernel),
-                                       hipFuncAttributeMaxDynamicSharedMemorySize, int(table_bytes(kMaxLdsBits)));
+                                       hipFuncAttributeMaxDynamicSharedMemorySize, int(bytes));
     if (e != hipSuccess) g_attr_err = e;
 }
 
-#define AMSIM_FOR_TILES(X)                                                                                   \
-    X(8, 16) X(4, 16) X(2, 16) X(1, 16) X(8, 4) X(4, 4) X(2, 4) X(1, 4)
+#define AMSIM_FOR_TAB_TILES(X) X(4, 8) X(2, 8) X(1, 8) X(4, 4) X(2, 4) X(1, 4)
+#define AMSIM_FOR_TILES(X) X(8, 16) X(4, 16) X(2, 16) X(1, 16) X(8, 4) X(4, 4) X(2, 4) X(1, 4)
+
+template <int TN>
+constexpr size_t tab_lds_bytes();
 
 void set_attributes()
 {
-    allow_big_lds(gemm_tab_kernel<4, 8>);
-    allow_big_lds(gemm_tab_kernel<2, 8>);
-    allow_big_lds(gemm_tab_kernel<1, 8>);
-    allow_big_lds(gemm_tab_kernel<4, 4>);
-    allow_big_lds(gemm_tab_kernel<2, 4>);
-    allow_big_lds(gemm_tab_kernel<1, 4>);
-#define X(TM, TN)                                          \
-    allow_big_lds(gemm_kernel<TM, TN, true>);              \
-    allow_big_lds(conv_fwd_kernel<TM, TN, true>);          \
-    allow_big_lds(conv_bwd_data_kernel<TM, TN, true>);     \
-    allow_big_lds(conv_bwd_weight_kernel<TM, TN, true>);
-    AMSIM_FOR_TILES(X)
+#define X(TM, TN)                                                          \
+    allow_lds(tab_kernel<OP_GEMM, TM, TN>, tab_lds_bytes<TN>());          \
+    allow_lds(tab_kernel<OP_FWD, TM, TN>, tab_lds_bytes<TN>());           \
+    allow_lds(tab_kernel<OP_BWD_DATA, TM, TN>, tab_lds_bytes<TN>());      \
+    allow_lds(tab_kernel<OP_BWD_WEIGHT, TM, TN>, tab_lds_bytes<TN>());
+    AMSIM_FOR_TAB_TILES(X)
 #undef X
 }
 
@@ -751,54 +978,64 @@ inline int grid_for(int64_t total, int block = 256)
     return int(std::max<int64_t>(1, std::min<int64_t>(ceil_div(total, block), 8192)));
 }
 
+template <typename F>
+void dispatch_tab_tile(const Tile &t, F &&f)
+{
+#define X(TM, TN)                                                                \
+    if (t.tm == TM && t.tn == TN) {                                              \
+        f(std::integral_constant<int, TM>{}, std::integral_constant<int, TN>{}); \
+        return;                                                                  \
+    }
+    AMSIM_FOR_TAB_TILES(X)
+#undef X
+}
+
+template <typename F>
+void dispatch_tile(const Tile &t, F &&f)
+{
+#define X(TM, TN)                                                                \
+    if (t.tm == TM && t.tn == TN) {                                              \
+        f(std::integral_constant<int, TM>{}, std::integral_constant<int, TN>{}); \
+        return;                                                                  \
+    }
+    AMSIM_FOR_TILES(X)
+#undef X
+}
+
+constexpr size_t kRowsBytes = size_t(kTabRowEntries) * kTabRowEntries * 4;  // widest transposed table
+
 // Workspace layout shared by the size queries and the launches.
+//   table path: [transposed rows][entry-width word][first operand][second operand][partials]
+//   global path:                                   [first operand][second operand][partials]
 struct Plan {
     Tile tile;
     bool lds;
-    size_t off_table, off_a, off_b, off_part, total;
-    int64_t a_ld, b_ld;  // padded leading dims of the decoded operands
+    size_t off_rows, off_eb, off_a, off_b, off_part, total;
+    int64_t a_ld, b_ld;   // GEMM: padded leading dims of the decoded operands; conv: b_ld only
+    int64_t a_elems;      // conv: elements of the decoded first operand
+    int splits, per_split;
+    int Hp, Wp, OHp, OWp, pad_oh, pad_ow;
 };
 
 bool valid_m(int m_bits) { return m_bits >= 1 && m_bits <= 11; }
 
-// Per-column-table GEMM tile: 4 waves x 64*TM rows per workgroup, TN shared columns.  Chosen
-// from measurements on MI355X (4096^3): TM = 4, TN = 8 keeps the kernel at 4 waves per SIMD
-// (~120 VGPRs) with enough register tiling; larger tiles drop occupancy and lose more to
-// latency than they save in operand loads.
-Tile choose_tab_tile(int64_t rows, int64_t cols, int64_t red)
+size_t table_area(Plan &p, size_t o)
 {
-    Tile t;
-    t.tn = cols > 4 ? 8 : 4;
-    const int64_t col_tiles = ceil_div(cols, t.tn);
-    t.tm = 1;
-    for (int tm : {4, 2}) {
-        if (ceil_div(rows, int64_t(64) * kWaves * tm) * col_tiles >= 2 * kTargetWgs) {
-            t.tm = tm;
-            break;
-        }
-    }
-    const int64_t tiles = ceil_div(rows, int64_t(64) * kWaves * t.tm) * col_tiles;
-    t.split = 1;
-    if (tiles < kTargetWgs) {
-        const int64_t max_split = std::max<int64_t>(1, red / 256);
-        t.split = int(std::min<int64_t>(std::min<int64_t>(ceil_div(kTargetWgs, tiles), max_split), 1024));
-    }
-    return t;
+    p.off_rows = o;
+    p.off_eb = o + align_up(kRowsBytes);
+    return o + align_up(kRowsBytes) + kAlign;
 }
-
-constexpr size_t kRowsBytes = size_t(kTabRowEntries) * kTabRowEntries * 4;  // widest transposed table
 
 Plan plan_gemm(int64_t m, int64_t n, int64_t k, int m_bits)
 {
     Plan p{};
     p.lds = lds_path(m_bits);
     size_t o = 0;
-    p.off_table = o;
     if (p.lds) {
-        p.tile = choose_tab_tile(m, n, k);
+        p.tile = choose_tab_tile(m, n, k, 256, true);
         p.a_ld = round_up(m, int64_t(64) * kWaves * p.tile.tm);
         p.b_ld = round_up(n, p.tile.tn);
-        o += align_up(kRowsBytes) + kAlign;  // transposed rows + entry-width word
+        o = table_area(p, o);
     } else {
         p.tile = choose_tile(m, n, k, 1, true);
         p.a_ld = round_up(m, 64 * p.tile.tm);
@@ -808,8 +1045,10 @@ Plan plan_gemm(int64_t m, int64_t n, int64_t k, int m_bits)
     o += align_up(size_t(k) * p.a_ld * 4);
     p.off_b = o;
     o += align_up(size_t(k) * p.b_ld * 4);
+    p.per_split = int(ceil_div(k, p.tile.split));
+    p.splits = int(ceil_div(k, p.per_split));
     p.off_part = o;
-    if (p.tile.split > 1) o += align_up(size_t(p.tile.split) * m * n * 4);
+    if (p.splits > 1) o += align_up(size_t(p.splits) * m * n * 4);
     p.total = o;
     return p;
 }
@@ -834,16 +1073,45 @@ int check_conv(const amsim_conv2d *d)
     const int64_t hp = int64_t(d->h) + d->pad_top + d->pad_bottom, wp = int64_t(d->w) + d->pad_left + d->pad_right;
     if (hp < d->kh || wp < d->kw) return AMSIM_ERR_INVALID_ARG;
     const int64_t oh = (hp - d->kh) / d->stride_h + 1, ow = (wp - d->kw) / d->stride_w + 1;
-    const int64_t lim = int64_t(1) << 31;
-    const int64_t x = int64_t(d->n) * d->h * d->w * d->c_in;
-    const int64_t y = int64_t(d->n) * oh * ow * d->c_out;
-    const int64_t w = int64_t(d->kh) * d->kw * d->c_in * d->c_out;
-    if (x >= lim || y >= lim || w >= lim || int64_t(d->kh) * d->kw * d->c_out * (d->c_in + 64) >= lim ||
-        int64_t(d->n) * oh * ow * (d->c_out + 64) >= lim || int64_t(d->kh) * d->kw * d->c_in * (d->c_out + 64) >= lim ||
-        d->pad_top >= d->kh + d->stride_h * 4096 || d->pad_left >= d->kw + d->stride_w * 4096 ||
-        int64_t(d->stride_h) * d->stride_w > 65535 || d->c_in > 65535 * 64 || d->c_out > 65535 * 64)
+    // every index, padded tensor and byte offset must stay below 2^31
+    const int64_t lim = int64_t(1) << 29;
+    const int64_t xp = int64_t(d->n) * hp * wp * d->c_in;
+    const int64_t yp = int64_t(d->n) * (oh + 2 * d->kh + 2) * (ow + 2 * d->kw + 2) * d->c_out;
+    const int64_t w = int64_t(d->kh) * d->kw * (d->c_in + 16) * (d->c_out + 16);
+    const int64_t y = int64_t(d->n) * oh * ow * (d->c_out + 16);
+    if (xp >= lim || yp >= lim || w >= lim || y >= lim || d->pad_top >= 65536 || d->pad_bottom >= 65536 ||
+        d->pad_left >= 65536 || d->pad_right >= 65536 || d->kh >= 65536 || d->kw >= 65536 ||
+        int64_t(d->stride_h) * d->stride_w > 65535 || d->c_in > 65535 * 16 || d->c_out > 65535 * 16)
         return AMSIM_ERR_UNSUPPORTED;
     return AMSIM_OK;
+}
+
+// Zero padding of dy for the backward-data table kernel: every phase row (hq, wq) plus every
+// valid tap offset (dh, dw) must land inside the padded tensor.
+void bwd_data_dy_pads(const ConvShape &s, int &top, int &bottom, int &left, int &right)
+{
+    top = bottom = left = right = 0;
+    for (int ph = 0; ph < s.sh && ph < s.h; ++ph) {
+        const int hq_n = (s.h - ph + s.sh - 1) / s.sh;
+        for (int kh = (ph + s.pt) % s.sh; kh < s.kh; kh += s.sh) {
+            const int dh = (ph + s.pt - kh) / s.sh;
+            top = std::max(top, -dh);
+            bottom = std::max(bottom, hq_n - 1 + dh - (s.oh - 1));
+        }
+    }
+    for (int pw = 0; pw < s.sw && pw < s.w; ++pw) {
+        const int wq_n = (s.w - pw + s.sw - 1) / s.sw;
+        for (int kw = (pw + s.pl) % s.sw; kw < s.kw; kw += s.sw) {
+            const int dw = (pw + s.pl - kw) / s.sw;
+            left = std::max(left, -dw);
+            right = std::max(right, wq_n - 1 + dw - (s.ow - 1));
+        }
+    }
+}
+
+int64_t bwd_data_rows(const ConvShape &s)
+{
+    return int64_t(s.n) * ceil_div(s.h, s.sh) * ceil_div(s.w, s.sw);  // largest phase
 }
 
 Plan plan_conv(const amsim_conv2d *d, int pass, int m_bits)
@@ -852,93 +1120,109 @@ Plan plan_conv(const amsim_conv2d *d, int pass, int m_bits)
     Plan p{};
     p.lds = lds_path(m_bits);
     size_t o = 0;
-    p.off_table = o;
-    if (p.lds) o += align_up(table_bytes(m_bits));
+    if (p.lds) o = table_area(p, o);
     const int64_t npix_in = int64_t(s.n) * s.h * s.w, npix_out = int64_t(s.n) * s.oh * s.ow;
+    p.Hp = d->h + d->pad_top + d->pad_bottom;
+    p.Wp = d->w + d->pad_left + d->pad_right;
+    p.splits = 1;
     if (pass == AMSIM_CONV_FWD) {
-        p.tile = choose_tile(npix_out, s.co, 1, 1, false);
-        p.b_ld = round_up(s.co, int64_t(p.tile.tn) * kWaves);
-        p.off_a = o;  // decoded x
-        o += align_up(size_t(npix_in) * s.ci * 4);
+        p.tile = p.lds ? choose_tab_tile(npix_out, s.co, 1, 1, false) : choose_tile(npix_out, s.co, 1, 1, false);
+        p.b_ld = p.lds ? round_up(s.co, p.tile.tn) : round_up(s.co, int64_t(p.tile.tn) * kWaves);
+        p.a_elems = p.lds ? int64_t(s.n) * p.Hp * p.Wp * s.ci : npix_in * s.ci;  // decoded x
+        p.off_a = o;
+        o += align_up(size_t(p.a_elems) * 4);
         p.off_b = o;  // decoded w [kh*kw*ci][COp]
         o += align_up(size_t(s.kh) * s.kw * s.ci * p.b_ld * 4);
     } else if (pass == AMSIM_CONV_BWD_DATA) {
-        const int64_t rows = s.n * ceil_div(s.h, s.sh) * ceil_div(s.w, s.sw);
-        p.tile = choose_tile(rows, s.ci, 1, 1, false);
-        p.b_ld = round_up(s.ci, int64_t(p.tile.tn) * kWaves);
-        p.off_a = o;  // decoded dy
-        o += align_up(size_t(npix_out) * s.co * 4);
+        const int64_t rows = bwd_data_rows(s);
+        p.tile = p.lds ? choose_tab_tile(rows, s.ci, 1, 1, false) : choose_tile(rows, s.ci, 1, 1, false);
+        p.b_ld = p.lds ? round_up(s.ci, p.tile.tn) : round_up(s.ci, int64_t(p.tile.tn) * kWaves);
+        if (p.lds) {
+            int top, bottom, left, right;
+            bwd_data_dy_pads(s, top, bottom, left, right);
+            p.pad_oh = top;
+            p.pad_ow = left;
+            p.OHp = top + s.oh + bottom;
+            p.OWp = left + s.ow + right;
+            p.a_elems = int64_t(s.n) * p.OHp * p.OWp * s.co;  // decoded, zero-padded dy
+        } else {
+            p.a_elems = npix_out * s.co;
+        }
+        p.off_a = o;
+        o += align_up(size_t(p.a_elems) * 4);
         p.off_b = o;  // decoded w^T [kh][kw][co][CIp]
         o += align_up(size_t(s.kh) * s.kw * s.co * p.b_ld * 4);
     } else {
         const int64_t R = int64_t(s.kh) * s.kw * s.ci;
-        p.tile = choose_tile(R, s.co, int64_t(s.n) * s.oh, s.ow, true);
-        p.b_ld = round_up(s.co, int64_t(p.tile.tn) * kWaves);
+        const int64_t taps = int64_t(s.n) * s.oh;
+        if (p.lds) {
+            p.tile = choose_tab_tile(R, s.co, taps, ceil_div(256, s.ow), true);
+            p.b_ld = round_up(s.co, p.tile.tn);
+            p.a_elems = int64_t(s.n) * p.Hp * p.Wp * s.ci;
+        } else {
+            p.tile = choose_tile(R, s.co, taps, s.ow, true);
+            p.b_ld = round_up(s.co, int64_t(p.tile.tn) * kWaves);
+            p.a_elems = npix_in * s.ci;
+        }
+        p.per_split = int(ceil_div(taps, p.tile.split));
+        p.splits = int(ceil_div(taps, p.per_split));
         p.off_a = o;  // decoded x
-        o += align_up(size_t(npix_in) * s.ci * 4);
+        o += align_up(size_t(p.a_elems) * 4);
         p.off_b = o;  // decoded dy [n*oh*ow][COp]
         o += align_up(size_t(npix_out) * p.b_ld * 4);
         p.off_part = o;
-        if (p.tile.split > 1) o += align_up(size_t(p.tile.split) * R * s.co * 4);
+        if (p.splits > 1) o += align_up(size_t(p.splits) * R * s.co * 4);
     }
     p.total = o;
     return p;
 }
 
-int prep_table(const uint32_t *lut, int m_bits, char *ws, const Plan &p, hipStream_t st, const uint32_t **table)
+// Decoded-index shift of each operand.  Table path: mantissa index itself (the kernels scale
+// it).  Global path: entry index into the canonical table, ka * 2^M + kb.
+inline int shift_first(int m_bits) { return lds_path(m_bits) ? 0 : m_bits; }
+inline int shift_second(int m_bits) { return lds_path(m_bits) ? 0 : 0; }
+
+// Launches the table preparation for the table path (rows + entry width into the workspace).
+int prep_rows(const uint32_t *lut, int m_bits, char *ws, const Plan &p, hipStream_t st)
 {
-    if (p.lds) {
-        uint32_t *t = reinterpret_cast<uint32_t *>(ws + p.off_table);
-        hipLaunchKernelGGL(prep_table_kernel, dim3(grid_for(int64_t(1) << (2 * m_bits))), dim3(256), 0, st, lut, t,
-                           m_bits);
-        *table = t;
-    } else {
-        *table = lut;
-    }
+    hipLaunchKernelGGL(prep_rows_kernel, dim3(1), dim3(1024), 0, st, lut, m_bits,
+                       reinterpret_cast<unsigned char *>(ws + p.off_rows), reinterpret_cast<int *>(ws + p.off_eb));
     return launch_status();
 }
 
-// Shift of the decoded index field: the lane (first) operand carries ka, the uniform (second)
-// operand kb.  LDS: byte offset into the transposed table (kb * 2^M + ka) * 4.  Global: entry
-// index into the canonical table ka * 2^M + kb.
-inline int shift_first(int m_bits) { return lds_path(m_bits) ? 2 : m_bits; }
-inline int shift_second(int m_bits) { return lds_path(m_bits) ? m_bits + 2 : 0; }
-
-template <int TM, int TN, bool LDS>
-void launch_gemm_t(dim3 grid, hipStream_t st, const uint32_t *Ad, int Mp, const uint32_t *Bd, int Np, int M, int N,
-                   int K, int kchunk, float *out, int64_t ldc, const uint32_t *table, int m_bits)
+template <int OP>
+int launch_tab(const Plan &p, const TabArgs &a, dim3 grid, hipStream_t st)
 {
-    const int entries = 1 << (2 * m_bits);
-    const size_t lds = LDS ? size_t(entries) * 4 : 0;
-    hipLaunchKernelGGL((gemm_kernel<TM, TN, LDS>), grid, dim3(kThreads), lds, st, Ad, Mp, Bd, Np, M, N, K, kchunk,
-                       out, ldc, table, entries);
+    auto run = [&](auto tm, auto tn) {
+        constexpr int TM = decltype(tm)::value, TN = decltype(tn)::value;
+        hipLaunchKernelGGL((tab_kernel<OP, TM, TN>), grid, dim3(kThreads), tab_lds_bytes<TN>(), st, a);
+    };
+    dispatch_tab_tile(p.tile, run);
+    return launch_status();
 }
 
-template <typename F>
-void dispatch_tab_tile(const Tile &t, F &&f)
+TabArgs tab_args(const Plan &p, char *ws, const uint32_t *A, int64_t a_elems, const uint32_t *Bd, float *out, int R,
+                 int N)
 {
-#define X(TM, TN)                                                                \
-    if (t.tm == TM && t.tn == TN) {                                              \
-        f(std::integral_constant<int, TM>{}, std::integral_constant<int, TN>{}); \
-        return;                                                                  \
-    }
-    X(4, 8) X(2, 8) X(1, 8) X(4, 4) X(2, 4) X(1, 4)
-#undef X
+    TabArgs a{};
+    a.A = A;
+    a.a_bytes = uint32_t(a_elems * 4);
+    a.Bd = Bd;
+    a.Np = int(p.b_ld);
+    a.out = out;
+    a.rows = reinterpret_cast<const unsigned char *>(ws + p.off_rows);
+    a.eb = reinterpret_cast<const int *>(ws + p.off_eb);
+    a.R = R;
+    a.N = N;
+    a.Hp = p.Hp;
+    a.Wp = p.Wp;
+    a.OHp = p.OHp;
+    a.OWp = p.OWp;
+    a.pad_oh = p.pad_oh;
+    a.pad_ow = p.pad_ow;
+    a.taps_per_split = p.per_split;
+    return a;
 }
-
-template <bool LDS, typename F>
-void dispatch_tile(const Tile &t, F &&f)
-{
-    // f is a generic lambda taking std::integral_constant-like tags
-#define X(TM, TN)                                                  \
-    if (t.tm == TM && t.tn == TN) {                                \
-        f(std::integral_constant<int, TM>{}, std::integral_constant<int, TN>{}); \
-        return;                                                    \
-    }
-    AMSIM_FOR_TILES(X)
-#undef X
-}
-
 
 // ------------------------------------------------------------------ kernel timer --------
 
@@ -1033,7 +1317,8 @@ int approx_gemm(int trans_a, int trans_b, int64_t m, int64_t n, int64_t k, const
     if (!A || !B || !lut) return AMSIM_ERR_INVALID_ARG;
     if (lda < (trans_a ? m : k) || ldb < (trans_b ? k : n)) return AMSIM_ERR_INVALID_ARG;
     const Plan p = plan_gemm(m, n, k, m_bits);
-    if (k * p.a_ld >= lim || k * p.b_ld >= lim || int64_t(p.tile.split) * m * n >= lim ||
+    // decoded operands are addressed with 32-bit byte offsets
+    if (k * p.a_ld >= (int64_t(1) << 29) || k * p.b_ld >= lim || int64_t(p.splits) * m * n >= lim ||
         p.b_ld / (int64_t(p.tile.tn) * (p.lds ? 1 : kWaves)) > 65535)
         return AMSIM_ERR_UNSUPPORTED;
     if (p.total > 0 && (!workspace || workspace_bytes < p.total)) return AMSIM_ERR_WORKSPACE;
@@ -1042,49 +1327,43 @@ int approx_gemm(int trans_a, int trans_b, int64_t m, int64_t n, int64_t k, const
     uint32_t *Ad = reinterpret_cast<uint32_t *>(ws + p.off_a);
     uint32_t *Bd = reinterpret_cast<uint32_t *>(ws + p.off_b);
     const Tile t = p.tile;
-    const int kchunk = int(ceil_div(k, t.split));
-    const int splits = int(ceil_div(k, kchunk));
-    float *out = splits > 1 ? reinterpret_cast<float *>(ws + p.off_part) : C;
+    float *out = p.splits > 1 ? reinterpret_cast<float *>(ws + p.off_part) : C;
     // op(A)(i, kk): row stride / column stride in A's storage
     const int64_t a_sr = trans_a ? 1 : lda, a_sc = trans_a ? lda : 1;
     const int64_t b_sr = trans_b ? 1 : ldb, b_sc = trans_b ? ldb : 1;
     const dim3 grid_dt(unsigned(ceil_div(p.a_ld, 64)), unsigned(std::min<int64_t>(ceil_div(k, 64), 4096)));
+    if (p.lds && prep_rows(lut, m_bits, ws, p, st) != AMSIM_OK) return AMSIM_ERR_HIP;
+    hipLaunchKernelGGL(decode_t_kernel, grid_dt, dim3(256), 0, st, A, a_sr, a_sc, int(m), int(k), Ad, int(p.a_ld),
+                       m_bits, shift_first(m_bits));
+    hipLaunchKernelGGL(decode_kernel, dim3(grid_for(k * p.b_ld)), dim3(256), 0, st, B, int64_t(0), b_sr, b_sc, 1,
+                       int(k), int(n), Bd, int(p.b_ld), m_bits, shift_second(m_bits));
+    if (launch_status() != AMSIM_OK) return AMSIM_ERR_HIP;
+    int rc;
     if (p.lds) {
-        unsigned char *rows = reinterpret_cast<unsigned char *>(ws + p.off_table);
-        int *eb = reinterpret_cast<int *>(ws + p.off_table + align_up(kRowsBytes));
-        hipLaunchKernelGGL(prep_rows_kernel, dim3(1), dim3(1024), 0, st, lut, m_bits, rows, eb);
-        hipLaunchKernelGGL(decode_t_kernel, grid_dt, dim3(256), 0, st, A, a_sr, a_sc, int(m), int(k), Ad, int(p.a_ld),
-                           m_bits, 0);
-        hipLaunchKernelGGL(decode_kernel, dim3(grid_for(k * p.b_ld)), dim3(256), 0, st, B, int64_t(0), b_sr, b_sc, 1,
-                           int(k), int(n), Bd, int(p.b_ld), m_bits, 0);
-        if (launch_status() != AMSIM_OK) return AMSIM_ERR_HIP;
-        dim3 grid(unsigned(p.a_ld / (int64_t(64) * kWaves * t.tm)), unsigned(p.b_ld / t.tn), unsigned(splits));
+        TabArgs a = tab_args(p, ws, Ad, k * p.a_ld, Bd, out, int(m), int(n));
+        a.ldc = ldc;
+        a.Mp = int(p.a_ld);
+        a.K = int(k);
+        a.kchunk = p.per_split;
+        a.taps = p.splits;
+        dim3 grid(unsigned(p.a_ld / (int64_t(64) * kWaves * t.tm)), unsigned(p.b_ld / t.tn), unsigned(p.splits));
+        TimedLaunch tl(AMSIM_KERNEL_GEMM, st);
+        rc = launch_tab<OP_GEMM>(p, a, grid, st);
+    } else {
+        dim3 grid(unsigned(p.a_ld / (64 * t.tm)), unsigned(p.b_ld / (int64_t(t.tn) * kWaves)), unsigned(p.splits));
         auto run = [&](auto tm, auto tn) {
             constexpr int TM = decltype(tm)::value, TN = decltype(tn)::value;
-            hipLaunchKernelGGL((gemm_tab_kernel<TM, TN>), grid, dim3(kThreads), tab_lds_bytes<TN>(), st, Ad,
-                               int(p.a_ld), Bd, int(p.b_ld), int(m), int(n), int(k), kchunk, out, ldc, rows, eb);
+            hipLaunchKernelGGL((gemm_kernel<TM, TN, false>), grid, dim3(kThreads), 0, st, Ad, int(p.a_ld), Bd,
+                               int(p.b_ld), int(m), int(n), int(k), p.per_split, out, ldc, lut, 1 << (2 * m_bits));
         };
         TimedLaunch tl(AMSIM_KERNEL_GEMM, st);
-        dispatch_tab_tile(t, run);
-    } else {
-        hipLaunchKernelGGL(decode_t_kernel, grid_dt, dim3(256), 0, st, A, a_sr, a_sc, int(m), int(k), Ad, int(p.a_ld),
-                           m_bits, shift_first(m_bits));
-        hipLaunchKernelGGL(decode_kernel, dim3(grid_for(k * p.b_ld)), dim3(256), 0, st, B, int64_t(0), b_sr, b_sc, 1,
-                           int(k), int(n), Bd, int(p.b_ld), m_bits, shift_second(m_bits));
-        if (launch_status() != AMSIM_OK) return AMSIM_ERR_HIP;
-        dim3 grid(unsigned(p.a_ld / (64 * t.tm)), unsigned(p.b_ld / (int64_t(t.tn) * kWaves)), unsigned(splits));
-        auto run = [&](auto tm, auto tn) {
-            launch_gemm_t<decltype(tm)::value, decltype(tn)::value, false>(grid, st, Ad, int(p.a_ld), Bd, int(p.b_ld),
-                                                                           int(m), int(n), int(k), kchunk, out, ldc,
-                                                                           lut, m_bits);
-        };
-        TimedLaunch tl(AMSIM_KERNEL_GEMM, st);
-        dispatch_tile<true>(t, run);
+        dispatch_tile(t, run);
+        rc = launch_status();
     }
-    if (launch_status() != AMSIM_OK) return AMSIM_ERR_HIP;
-    if (splits > 1) {
+    if (rc != AMSIM_OK) return AMSIM_ERR_HIP;
+    if (p.splits > 1) {
         hipLaunchKernelGGL(reduce_splits_kernel, dim3(grid_for(m * n)), dim3(256), 0, st,
-                           reinterpret_cast<const float *>(ws + p.off_part), splits, int(m), int(n), C, ldc);
+                           reinterpret_cast<const float *>(ws + p.off_part), p.splits, int(m), int(n), C, ldc);
         if (launch_status() != AMSIM_OK) return AMSIM_ERR_HIP;
     }
     return AMSIM_OK;
@@ -1114,6 +1393,23 @@ static int conv_common(const amsim_conv2d *desc, int pass, const void *in0, cons
     return AMSIM_OK;
 }
 
+// Decoded copy of an NHWC tensor, zero-padded (table path) or as is (global path).
+static void decode_nhwc(const float *src, int n, int h, int w, int c, int top, int left, int hp, int wp, uint32_t *dst,
+                        int m_bits, int shift, hipStream_t st)
+{
+    const int64_t total = int64_t(n) * hp * wp * c;
+    hipLaunchKernelGGL(decode_pad_kernel, dim3(grid_for(total)), dim3(256), 0, st, src, n, h, w, c, top, left, hp, wp,
+                       dst, m_bits, shift);
+}
+
+static void decode_nhcw(const float *src, int n, int h, int w, int c, int top, int left, int hp, int wp, uint32_t *dst,
+                        int m_bits, int shift, hipStream_t st)
+{
+    const int64_t total = int64_t(n) * hp * wp * c;
+    hipLaunchKernelGGL(decode_pad_nhcw_kernel, dim3(grid_for(total)), dim3(256), 0, st, src, n, h, w, c, top, left, hp,
+                       wp, dst, m_bits, shift);
+}
+
 int approx_conv2d_fwd(const amsim_conv2d *desc, const float *x, const float *w, float *y, const uint32_t *lut,
                       int m_bits, void *workspace, size_t workspace_bytes, void *stream)
 {
@@ -1123,32 +1419,33 @@ int approx_conv2d_fwd(const amsim_conv2d *desc, const float *x, const float *w, 
     hipStream_t st = static_cast<hipStream_t>(stream);
     const ConvShape s = shape_of(desc);
     char *ws = static_cast<char *>(workspace);
-    const uint32_t *table;
-    if (prep_table(lut, m_bits, ws, p, st, &table) != AMSIM_OK) return AMSIM_ERR_HIP;
     uint32_t *Xd = reinterpret_cast<uint32_t *>(ws + p.off_a);
     uint32_t *Wd = reinterpret_cast<uint32_t *>(ws + p.off_b);
-    const int64_t nx = int64_t(s.n) * s.h * s.w * s.ci;
-    hipLaunchKernelGGL(decode_kernel, dim3(grid_for(nx)), dim3(256), 0, st, x, int64_t(0), int64_t(s.ci), int64_t(1), 1,
-                       int(nx / s.ci), s.ci, Xd, s.ci, m_bits, shift_first(m_bits));
+    if (p.lds && prep_rows(lut, m_bits, ws, p, st) != AMSIM_OK) return AMSIM_ERR_HIP;
+    if (p.lds)
+        decode_nhcw(x, s.n, s.h, s.w, s.ci, s.pt, s.pl, p.Hp, p.Wp, Xd, m_bits, shift_first(m_bits), st);
+    else
+        decode_nhwc(x, s.n, s.h, s.w, s.ci, 0, 0, s.h, s.w, Xd, m_bits, shift_first(m_bits), st);
     const int kk = s.kh * s.kw * s.ci;
     hipLaunchKernelGGL(decode_kernel, dim3(grid_for(int64_t(kk) * p.b_ld)), dim3(256), 0, st, w, int64_t(0),
                        int64_t(s.co), int64_t(1), 1, kk, s.co, Wd, int(p.b_ld), m_bits, shift_second(m_bits));
     if (launch_status() != AMSIM_OK) return AMSIM_ERR_HIP;
     const Tile t = p.tile;
     const int64_t rows = int64_t(s.n) * s.oh * s.ow;
+    TimedLaunch tl(AMSIM_KERNEL_CONV_FWD, st);
+    if (p.lds) {
+        TabArgs a = tab_args(p, ws, Xd, p.a_elems, Wd, y, int(rows), s.co);
+        a.s = s;
+        dim3 grid(unsigned(ceil_div(rows, int64_t(64) * kWaves * t.tm)), unsigned(p.b_ld / t.tn), 1);
+        return launch_tab<OP_FWD>(p, a, grid, st);
+    }
     dim3 grid(unsigned(ceil_div(rows, 64 * t.tm)), unsigned(p.b_ld / (int64_t(t.tn) * kWaves)), 1);
-    const int entries = 1 << (2 * m_bits);
     auto run = [&](auto tm, auto tn) {
         constexpr int TM = decltype(tm)::value, TN = decltype(tn)::value;
-        if (p.lds)
-            hipLaunchKernelGGL((conv_fwd_kernel<TM, TN, true>), grid, dim3(kThreads), size_t(entries) * 4, st, Xd, Wd,
-                               int(p.b_ld), s, y, table, entries);
-        else
-            hipLaunchKernelGGL((conv_fwd_kernel<TM, TN, false>), grid, dim3(kThreads), 0, st, Xd, Wd, int(p.b_ld), s,
-                               y, table, entries);
+        hipLaunchKernelGGL((conv_fwd_kernel<TM, TN, false>), grid, dim3(kThreads), 0, st, Xd, Wd, int(p.b_ld), s, y,
+                           lut, 1 << (2 * m_bits));
     };
-    TimedLaunch tl(AMSIM_KERNEL_CONV_FWD, st);
-    dispatch_tile<true>(t, run);
+    dispatch_tile(t, run);
     return launch_status();
 }
 
@@ -1161,34 +1458,36 @@ int approx_conv2d_bwd_data(const amsim_conv2d *desc, const float *dy, const floa
     hipStream_t st = static_cast<hipStream_t>(stream);
     const ConvShape s = shape_of(desc);
     char *ws = static_cast<char *>(workspace);
-    const uint32_t *table;
-    if (prep_table(lut, m_bits, ws, p, st, &table) != AMSIM_OK) return AMSIM_ERR_HIP;
     uint32_t *Dyd = reinterpret_cast<uint32_t *>(ws + p.off_a);
     uint32_t *Wtd = reinterpret_cast<uint32_t *>(ws + p.off_b);
-    const int64_t ndy = int64_t(s.n) * s.oh * s.ow * s.co;
-    hipLaunchKernelGGL(decode_kernel, dim3(grid_for(ndy)), dim3(256), 0, st, dy, int64_t(0), int64_t(s.co), int64_t(1),
-                       1, int(ndy / s.co), s.co, Dyd, s.co, m_bits, shift_first(m_bits));
+    if (p.lds && prep_rows(lut, m_bits, ws, p, st) != AMSIM_OK) return AMSIM_ERR_HIP;
+    if (p.lds)
+        decode_nhcw(dy, s.n, s.oh, s.ow, s.co, p.pad_oh, p.pad_ow, p.OHp, p.OWp, Dyd, m_bits, shift_first(m_bits), st);
+    else
+        decode_nhwc(dy, s.n, s.oh, s.ow, s.co, 0, 0, s.oh, s.ow, Dyd, m_bits, shift_first(m_bits), st);
     // w[kh][kw][ci][co] -> Wt[kh][kw][co][ci]: batches (kh,kw), rows co, cols ci
     hipLaunchKernelGGL(decode_kernel, dim3(grid_for(int64_t(s.kh) * s.kw * s.co * p.b_ld)), dim3(256), 0, st, w,
                        int64_t(s.ci) * s.co, int64_t(1), int64_t(s.co), s.kh * s.kw, s.co, s.ci, Wtd, int(p.b_ld),
                        m_bits, shift_second(m_bits));
     if (launch_status() != AMSIM_OK) return AMSIM_ERR_HIP;
     const Tile t = p.tile;
-    const int64_t rows = int64_t(s.n) * ceil_div(s.h, s.sh) * ceil_div(s.w, s.sw);  // largest phase
+    const int64_t rows = bwd_data_rows(s);
+    TimedLaunch tl(AMSIM_KERNEL_CONV_BWD_DATA, st);
+    if (p.lds) {
+        TabArgs a = tab_args(p, ws, Dyd, p.a_elems, Wtd, dx, int(rows), s.ci);
+        a.s = s;
+        dim3 grid(unsigned(ceil_div(rows, int64_t(64) * kWaves * t.tm)), unsigned(p.b_ld / t.tn),
+                  unsigned(s.sh * s.sw));
+        return launch_tab<OP_BWD_DATA>(p, a, grid, st);
+    }
     dim3 grid(unsigned(ceil_div(rows, 64 * t.tm)), unsigned(p.b_ld / (int64_t(t.tn) * kWaves)),
               unsigned(s.sh * s.sw));
-    const int entries = 1 << (2 * m_bits);
     auto run = [&](auto tm, auto tn) {
         constexpr int TM = decltype(tm)::value, TN = decltype(tn)::value;
-        if (p.lds)
-            hipLaunchKernelGGL((conv_bwd_data_kernel<TM, TN, true>), grid, dim3(kThreads), size_t(entries) * 4, st,
-                               Dyd, Wtd, int(p.b_ld), s, dx, table, entries);
-        else
-            hipLaunchKernelGGL((conv_bwd_data_kernel<TM, TN, false>), grid, dim3(kThreads), 0, st, Dyd, Wtd,
-                               int(p.b_ld), s, dx, table, entries);
+        hipLaunchKernelGGL((conv_bwd_data_kernel<TM, TN, false>), grid, dim3(kThreads), 0, st, Dyd, Wtd,
+                           int(p.b_ld), s, dx, lut, 1 << (2 * m_bits));
     };
-    TimedLaunch tl(AMSIM_KERNEL_CONV_BWD_DATA, st);
-    dispatch_tile<true>(t, run);
+    dispatch_tile(t, run);
     return launch_status();
 }
 
@@ -1201,42 +1500,45 @@ int approx_conv2d_bwd_weight(const amsim_conv2d *desc, const float *x, const flo
     hipStream_t st = static_cast<hipStream_t>(stream);
     const ConvShape s = shape_of(desc);
     char *ws = static_cast<char *>(workspace);
-    const uint32_t *table;
-    if (prep_table(lut, m_bits, ws, p, st, &table) != AMSIM_OK) return AMSIM_ERR_HIP;
     uint32_t *Xd = reinterpret_cast<uint32_t *>(ws + p.off_a);
     uint32_t *Dyd = reinterpret_cast<uint32_t *>(ws + p.off_b);
-    const int64_t nx = int64_t(s.n) * s.h * s.w * s.ci;
-    hipLaunchKernelGGL(decode_kernel, dim3(grid_for(nx)), dim3(256), 0, st, x, int64_t(0), int64_t(s.ci), int64_t(1), 1,
-                       int(nx / s.ci), s.ci, Xd, s.ci, m_bits, shift_first(m_bits));
+    if (p.lds && prep_rows(lut, m_bits, ws, p, st) != AMSIM_OK) return AMSIM_ERR_HIP;
+    if (p.lds)
+        decode_nhwc(x, s.n, s.h, s.w, s.ci, s.pt, s.pl, p.Hp, p.Wp, Xd, m_bits, shift_first(m_bits), st);
+    else
+        decode_nhwc(x, s.n, s.h, s.w, s.ci, 0, 0, s.h, s.w, Xd, m_bits, shift_first(m_bits), st);
     const int64_t npo = int64_t(s.n) * s.oh * s.ow;
     hipLaunchKernelGGL(decode_kernel, dim3(grid_for(npo * p.b_ld)), dim3(256), 0, st, dy, int64_t(0), int64_t(s.co),
                        int64_t(1), 1, int(npo), s.co, Dyd, int(p.b_ld), m_bits, shift_second(m_bits));
     if (launch_status() != AMSIM_OK) return AMSIM_ERR_HIP;
     const Tile t = p.tile;
     const int R = s.kh * s.kw * s.ci;
-    const int nrows = s.n * s.oh;
-    const int per = int(ceil_div(nrows, t.split));
-    const int splits = int(ceil_div(nrows, per));
-    dim3 grid(unsigned(ceil_div(R, 64 * t.tm)), unsigned(p.b_ld / (int64_t(t.tn) * kWaves)), unsigned(splits));
-    float *out = splits > 1 ? reinterpret_cast<float *>(ws + p.off_part) : dw;
-    const int entries = 1 << (2 * m_bits);
-    auto run = [&](auto tm, auto tn) {
-        constexpr int TM = decltype(tm)::value, TN = decltype(tn)::value;
-        if (p.lds)
-            hipLaunchKernelGGL((conv_bwd_weight_kernel<TM, TN, true>), grid, dim3(kThreads), size_t(entries) * 4, st,
-                               Xd, Dyd, int(p.b_ld), s, per, out, table, entries);
-        else
-            hipLaunchKernelGGL((conv_bwd_weight_kernel<TM, TN, false>), grid, dim3(kThreads), 0, st, Xd, Dyd,
-                               int(p.b_ld), s, per, out, table, entries);
-    };
+    float *out = p.splits > 1 ? reinterpret_cast<float *>(ws + p.off_part) : dw;
     {
         TimedLaunch tl(AMSIM_KERNEL_CONV_BWD_WEIGHT, st);
-        dispatch_tile<true>(t, run);
+        if (p.lds) {
+            TabArgs a = tab_args(p, ws, Xd, p.a_elems, Dyd, out, R, s.co);
+            a.s = s;
+            a.taps = s.n * s.oh;
+            dim3 grid(unsigned(ceil_div(R, int64_t(64) * kWaves * t.tm)), unsigned(p.b_ld / t.tn),
+                      unsigned(p.splits));
+            rc = launch_tab<OP_BWD_WEIGHT>(p, a, grid, st);
+        } else {
+            dim3 grid(unsigned(ceil_div(R, 64 * t.tm)), unsigned(p.b_ld / (int64_t(t.tn) * kWaves)),
+                      unsigned(p.splits));
+            auto run = [&](auto tm, auto tn) {
+                constexpr int TM = decltype(tm)::value, TN = decltype(tn)::value;
+                hipLaunchKernelGGL((conv_bwd_weight_kernel<TM, TN, false>), grid, dim3(kThreads), 0, st, Xd, Dyd,
+                                   int(p.b_ld), s, p.per_split, out, lut, 1 << (2 * m_bits));
+            };
+            dispatch_tile(t, run);
+            rc = launch_status();
+        }
     }
-    if (launch_status() != AMSIM_OK) return AMSIM_ERR_HIP;
-    if (splits > 1) {
+    if (rc != AMSIM_OK) return AMSIM_ERR_HIP;
+    if (p.splits > 1) {
         hipLaunchKernelGGL(reduce_splits_kernel, dim3(grid_for(int64_t(R) * s.co)), dim3(256), 0, st,
-                           reinterpret_cast<const float *>(ws + p.off_part), splits, R, s.co, dw, int64_t(s.co));
+                           reinterpret_cast<const float *>(ws + p.off_part), p.splits, R, s.co, dw, int64_t(s.co));
         return launch_status();
     }
     return AMSIM_OK;

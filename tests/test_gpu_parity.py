@@ -185,6 +185,10 @@ CONV_CASES = [
     W.conv_desc(3, 10, 10, 65, 17, 3, 3, 2, 1),
     W.conv_desc(2, 9, 9, 16, 33, 1, 1, 2, 0),
     W.conv_desc(2, 28, 28, 1, 6, 5, 5, 1, 2),
+    W.conv_desc(1, 9, 9, 3, 2, 1, 1, 2, 0),
+    W.conv_desc(1, 16, 16, 3, 20, 7, 7, 2, 3),
+    W.conv_desc(1, 6, 7, 2, 2, 3, 3, 3, pads=(0, 2, 1, 0)),
+    W.conv_desc(2, 5, 4, 2, 3, 4, 4, 2, pads=(3, 3, 3, 3)),
 ]
 
 
