@@ -491,7 +491,8 @@ __device__ __forceinline__ TabTap tab_tap(const TabArgs &a, int tap)
 
 // Slab staging: each thread copies CPT 16-byte pieces of the rows selected by the second
 // operand's mantissas (kb) for slots [0, nslots) of a slab, and that operand's head (pb).
-template <int TN, int EB, int CPT>
+// TNW = result columns of the workgroup.
+template <int TNW, int EB, int CPT>
 __device__ __forceinline__ void tab_fetch(u32x4 (&stage)[CPT], float (&stage_pb)[CPT], const TabTap &tp, int c0,
                                           const uint32_t *__restrict__ Bd, int Np, int col0,
                                           const unsigned char *__restrict__ rows)
@@ -501,8 +502,8 @@ __device__ __forceinline__ void tab_fetch(u32x4 (&stage)[CPT], float (&stage_pb)
 #pragma unroll
     for (int i = 0; i < CPT; ++i) {
         const int c = threadIdx.x + i * kThreads;
-        const int slot = c / (TN * PIECES);
-        const int t = (c / PIECES) % TN;
+        const int slot = c / (TNW * PIECES);
+        const int t = (c / PIECES) % TNW;
         const int piece = c % PIECES;
         const int j = c0 + slot;
         const uint32_t bw = j < tp.count ? Bd[int64_t(tp.bbase + j) * Np + col0 + t] : 0u;
@@ -511,39 +512,45 @@ __device__ __forceinline__ void tab_fetch(u32x4 (&stage)[CPT], float (&stage_pb)
     }
 }
 
-template <int TN, int EB, int CPT>
+template <int TNW, int EB, int CPT>
 __device__ __forceinline__ void tab_commit(const u32x4 (&stage)[CPT], const float (&stage_pb)[CPT],
                                            unsigned char *smem, float *pbs, int buf)
 {
     constexpr int ROWB = kTabRowEntries * EB;
     constexpr int KS = 8 / EB;
-    constexpr int SLAB = KS * TN * ROWB;
+    constexpr int SLAB = KS * TNW * ROWB;
     constexpr int PIECES = ROWB / 16;
 #pragma unroll
     for (int i = 0; i < CPT; ++i) {
         const int c = threadIdx.x + i * kThreads;
         *reinterpret_cast<u32x4 *>(smem + buf * SLAB + c * 16) = stage[i];
-        if (c % PIECES == 0) pbs[buf * KS * TN + c / PIECES] = stage_pb[i];
+        if (c % PIECES == 0) pbs[buf * KS * TNW + c / PIECES] = stage_pb[i];
     }
 }
 
-// Workgroup: 4 waves on consecutive row blocks (64*TM rows each) sharing TN result columns.
-template <int OP, int TM, int TN, int EB>
+// Workgroup: 4 waves as a WR x (4/WR) grid -- WR row blocks of 64*TM rows, 4/WR column groups of
+// TN columns.  All waves share the LDS tables of the workgroup's TN * 4/WR columns.
+template <int OP, int TM, int TN, int WR, int EB>
 __device__ __forceinline__ void tab_body(const TabArgs &a)
 {
+    constexpr int WC = kWaves / WR;
+    constexpr int TNW = TN * WC;                // result columns of the workgroup
     constexpr int ROWB = kTabRowEntries * EB;
-    constexpr int KS = 8 / EB;                  // steps per slab: every slab is 8*TN*128 bytes
-    constexpr int SLAB = KS * TN * ROWB;
+    constexpr int KS = 8 / EB;                  // steps per slab: every slab is 8*TNW*128 bytes
+    constexpr int SLAB = KS * TNW * ROWB;
     constexpr int CPT = SLAB / 16 / kThreads;   // pieces per thread per slab
     static_assert(CPT * 16 * kThreads == SLAB, "slab must split evenly over the workgroup");
     extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
-    float *pbs = reinterpret_cast<float *>(smem + 2 * SLAB);  // [2][KS][TN] second-operand heads
+    float *pbs = reinterpret_cast<float *>(smem + 2 * SLAB);  // [2][KS][TNW] second-operand heads
 
     const int R = tab_rows<OP>(a);
-    if (int(blockIdx.x) * 64 * TM * kWaves >= R) return;  // uniform over the workgroup
+    if (int(blockIdx.x) * 64 * TM * WR >= R) return;  // uniform over the workgroup
     const int lane = threadIdx.x & 63;
-    const int row0 = blockIdx.x * (64 * TM * kWaves) + wave_id() * (64 * TM) + lane;
-    const int col0 = blockIdx.y * TN;
+    const int wave = wave_id();
+    const int rg = wave % WR, cg = wave / WR;
+    const int row0 = blockIdx.x * (64 * TM * WR) + rg * (64 * TM) + lane;
+    const int colw = blockIdx.y * TNW;  // first column of the workgroup
+    const int col0 = colw + cg * TN;    // first column of this wave
     // First-operand reads are raw buffer loads: voffset = the lane row's byte offset (range-checked,
     // reads past a_bytes return 0), soffset = the wave-uniform step offset, which every tap keeps
     // non-negative and inside the tensor, since the hardware does not range-check it.
@@ -574,8 +581,8 @@ __device__ __forceinline__ void tab_body(const TabArgs &a)
     bool have = t0 < t1;
     if (have) {
         cur = tab_tap<OP>(a, t0);
-        tab_fetch<TN, EB, CPT>(stage, stage_pb, cur, 0, a.Bd, a.Np, col0, a.rows);
-        tab_commit<TN, EB, CPT>(stage, stage_pb, smem, pbs, 0);
+        tab_fetch<TNW, EB, CPT>(stage, stage_pb, cur, 0, a.Bd, a.Np, colw, a.rows);
+        tab_commit<TNW, EB, CPT>(stage, stage_pb, smem, pbs, 0);
 #pragma unroll
         for (int r = 0; r < TM; ++r)
             acur[r] = __builtin_amdgcn_raw_buffer_load_b32(ares, aoff[r], uint32_t(cur.ubase) * 4u, 0);
@@ -593,9 +600,9 @@ __device__ __forceinline__ void tab_body(const TabArgs &a)
             if (ntap < t1) nxt = tab_tap<OP>(a, ntap);
         }
         const bool has_next = ntap < t1;
-        if (has_next) tab_fetch<TN, EB, CPT>(stage, stage_pb, nxt, nc0, a.Bd, a.Np, col0, a.rows);
-        const unsigned char *tb = smem + buf * SLAB;
-        const float *pb_s = pbs + buf * KS * TN;
+        if (has_next) tab_fetch<TNW, EB, CPT>(stage, stage_pb, nxt, nc0, a.Bd, a.Np, colw, a.rows);
+        const unsigned char *tb = smem + buf * SLAB + cg * TN * ROWB;
+        const float *pb_s = pbs + buf * KS * TNW + cg * TN;
         const int nslots = min(KS, cur.count - c0);
 #pragma unroll
         for (int slot = 0; slot < KS; ++slot) {
@@ -621,17 +628,17 @@ __device__ __forceinline__ void tab_body(const TabArgs &a)
             }
 #pragma unroll
             for (int t = 0; t < TN; ++t) {
-                const float pb = pb_s[slot * TN + t];
+                const float pb = pb_s[slot * TNW + t];
 #pragma unroll
                 for (int r = 0; r < TM; ++r) {
-                    const float v = tab_value<EB>(vaddr[r] + (slot * TN + t) * ROWB);
+                    const float v = tab_value<EB>(vaddr[r] + (slot * TNW + t) * ROWB);
                     acc[r][t] = __builtin_fmaf(v, pa[r] * pb, acc[r][t]);
                 }
             }
 #pragma unroll
             for (int r = 0; r < TM; ++r) acur[r] = anext[r];
         }
-        if (has_next) tab_commit<TN, EB, CPT>(stage, stage_pb, smem, pbs, buf ^ 1);
+        if (has_next) tab_commit<TNW, EB, CPT>(stage, stage_pb, smem, pbs, buf ^ 1);
         __syncthreads();
         cur = nxt;
         tap = ntap;
@@ -657,22 +664,23 @@ __device__ __forceinline__ void tab_body(const TabArgs &a)
 
 // Four waves per SIMD: the register budget (<= 128 VGPRs) the tiles are sized for.  Without the
 // hint the scheduler minimises registers and serialises the LDS gathers.
-template <int OP, int TM, int TN>
+template <int OP, int TM, int TN, int WR>
 __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(4, 4))) void tab_kernel(TabArgs a)
 {
     const int eb = __builtin_amdgcn_readfirstlane(*a.eb);
     if (eb == 1)
-        tab_body<OP, TM, TN, 1>(a);
+        tab_body<OP, TM, TN, WR, 1>(a);
     else if (eb == 2)
-        tab_body<OP, TM, TN, 2>(a);
+        tab_body<OP, TM, TN, WR, 2>(a);
     else
-        tab_body<OP, TM, TN, 4>(a);
+        tab_body<OP, TM, TN, WR, 4>(a);
 }
 
-template <int TN>
-constexpr size_t tab_lds_bytes()
+// Dynamic LDS of a table kernel with TNW workgroup columns: two slabs of 8*TNW*128 bytes plus
+// the second-operand heads.
+constexpr size_t tab_lds_bytes(int tnw)
 {
-    return size_t(2) * 8 * TN * kTabRowEntries + size_t(2) * 8 * TN * 4;
+    return size_t(2) * 8 * tnw * kTabRowEntries + size_t(2) * 8 * tnw * 4;
 }
 
 // ------------------------------------------------------------------ convolution kernels --
@@ -878,6 +886,7 @@ inline bool lds_path(int m_bits) { return m_bits <= kMaxLdsBits; }
 
 struct Tile {
     int tm, tn, split;
+    int wr = kWaves;  // table kernels: waves along rows (the rest take column groups)
 };
 
 constexpr int kTargetWgs = 512;  // 256 CUs x 2 workgroups
@@ -908,31 +917,52 @@ Tile choose_tile(int64_t rows, int64_t cols, int64_t red, int64_t red_unit, bool
     return t;
 }
 
-// Per-column-table kernels (M <= 7): 4 waves x 64*TM rows per workgroup, TN shared columns.
-// Chosen from measurements on MI355X (GEMM 4096^3): TM = 4, TN = 8 keeps the kernel at 4 waves
-// per SIMD (~120 VGPRs) with enough register tiling; larger tiles drop occupancy and lose more
-// to latency than they save in operand loads.  `red` is the reduction length in steps and
-// `min_steps` the fewest steps a split may hold.
+// Per-column-table kernels (M <= 7).  Candidates are the instantiated (TM, TN, WR) tiles; the
+// choice minimises an estimate of issue time: padded work x cost per product, scaled up when the
+// grid, after splitting the reduction, cannot give every CU two workgroups.  Cost per product:
+// 3 VALU ops, per-step overhead (~2.5 per row, ~4 per lane), and the table staging, whose bytes
+// per product grow with the workgroup's columns (4/WR groups) and shrink with its rows (TM) --
+// each staged table row serves the workgroup's rows once (weight fitted on MI355X: a 64 x 32
+// backward-weight tile ran 2.4x slower than a 256 x 8 one).  4096^3 GEMM picks TM = 4, TN = 8,
+// WR = 4; a 576-row backward-weight picks TM = 3, WR = 4 (one 768-row tile).  `red` is the
+// reduction length in taps and `min_steps` the fewest taps a split may hold.  (TM = 3 with
+// WR = 1 would exceed the 128-VGPR budget: its 32-column slab staging alone holds 40 registers.)
+struct TabCand {
+    int tm, tn, wr;
+};
+constexpr TabCand kTabCands[] = {{4, 8, 4}, {3, 8, 4}, {2, 8, 4}, {1, 8, 4}, {4, 4, 4}, {2, 4, 4},
+                                 {1, 4, 4}, {4, 8, 2}, {2, 8, 2}, {1, 8, 2}, {2, 8, 1}, {1, 8, 1}};
+
 Tile choose_tab_tile(int64_t rows, int64_t cols, int64_t red, int64_t min_steps, bool allow_split)
 {
-    Tile t;
-    t.tn = cols > 4 ? 8 : 4;
-    const int64_t col_tiles = ceil_div(cols, t.tn);
-    t.tm = 1;
-    for (int tm : {4, 2}) {
-        if (ceil_div(rows, int64_t(64) * kWaves * tm) * col_tiles >= 2 * kTargetWgs) {
-            t.tm = tm;
-            break;
+    Tile best{};
+    double best_cost = 0.0;
+    for (const TabCand &c : kTabCands) {
+        const int64_t rtile = int64_t(64) * c.tm * c.wr;
+        const int64_t ctile = int64_t(c.tn) * (kWaves / c.wr);
+        const int64_t tiles = ceil_div(rows, rtile) * ceil_div(cols, ctile);
+        int split = 1;
+        if (allow_split && tiles < kTargetWgs) {
+            const int64_t max_split = std::max<int64_t>(1, red / std::max<int64_t>(1, min_steps));
+            split = int(std::min<int64_t>(std::min<int64_t>(ceil_div(kTargetWgs, tiles), max_split), 1024));
+        }
+        const double work = double(ceil_div(rows, rtile) * rtile) * double(ceil_div(cols, ctile) * ctile);
+        const double per_product = 3.0 + 2.5 / c.tn + 4.0 / (c.tm * c.tn) + 2.0 * (kWaves / c.wr) / c.tm;
+        const double fill = std::min(1.0, double(tiles * split) / kTargetWgs);
+        const double cost = work * per_product / fill;
+        if (best_cost == 0.0 || cost < best_cost * 0.999) {
+            best_cost = cost;
+            best.tm = c.tm;
+            best.tn = c.tn;
+            best.wr = c.wr;
+            best.split = split;
         }
     }
-    const int64_t tiles = ceil_div(rows, int64_t(64) * kWaves * t.tm) * col_tiles;
-    t.split = 1;
-    if (allow_split && tiles < kTargetWgs) {
-        const int64_t max_split = std::max<int64_t>(1, red / std::max<int64_t>(1, min_steps));
-        t.split = int(std::min<int64_t>(std::min<int64_t>(ceil_div(kTargetWgs, tiles), max_split), 1024));
-    }
-    return t;
+    return best;
 }
+
+// Columns of a table-kernel workgroup.
+inline int64_t tab_cols(const Tile &t) { return int64_t(t.tn) * (kWaves / t.wr); }
 
 std::once_flag g_attr_once;
 hipError_t g_attr_err = hipSuccess;
@@ -945,19 +975,18 @@ void allow_lds(K kernel, size_t bytes)
     if (e != hipSuccess) g_attr_err = e;
 }
 
-#define AMSIM_FOR_TAB_TILES(X) X(4, 8) X(2, 8) X(1, 8) X(4, 4) X(2, 4) X(1, 4)
+#define AMSIM_FOR_TAB_TILES(X) \
+    X(4, 8, 4) X(3, 8, 4) X(2, 8, 4) X(1, 8, 4) X(4, 4, 4) X(2, 4, 4) X(1, 4, 4) X(4, 8, 2) X(2, 8, 2) X(1, 8, 2) \
+    X(2, 8, 1) X(1, 8, 1)
 #define AMSIM_FOR_TILES(X) X(8, 16) X(4, 16) X(2, 16) X(1, 16) X(8, 4) X(4, 4) X(2, 4) X(1, 4)
-
-template <int TN>
-constexpr size_t tab_lds_bytes();
 
 void set_attributes()
 {
-#define X(TM, TN)                                                          \
-    allow_lds(tab_kernel<OP_GEMM, TM, TN>, tab_lds_bytes<TN>());          \
-    allow_lds(tab_kernel<OP_FWD, TM, TN>, tab_lds_bytes<TN>());           \
-    allow_lds(tab_kernel<OP_BWD_DATA, TM, TN>, tab_lds_bytes<TN>());      \
-    allow_lds(tab_kernel<OP_BWD_WEIGHT, TM, TN>, tab_lds_bytes<TN>());
+#define X(TM, TN, WR)                                                                      \
+    allow_lds(tab_kernel<OP_GEMM, TM, TN, WR>, tab_lds_bytes(TN * (kWaves / WR)));        \
+    allow_lds(tab_kernel<OP_FWD, TM, TN, WR>, tab_lds_bytes(TN * (kWaves / WR)));         \
+    allow_lds(tab_kernel<OP_BWD_DATA, TM, TN, WR>, tab_lds_bytes(TN * (kWaves / WR)));    \
+    allow_lds(tab_kernel<OP_BWD_WEIGHT, TM, TN, WR>, tab_lds_bytes(TN * (kWaves / WR)));
     AMSIM_FOR_TAB_TILES(X)
 #undef X
 }
@@ -981,10 +1010,11 @@ inline int grid_for(int64_t total, int block = 256)
 template <typename F>
 void dispatch_tab_tile(const Tile &t, F &&f)
 {
-#define X(TM, TN)                                                                \
-    if (t.tm == TM && t.tn == TN) {                                              \
-        f(std::integral_constant<int, TM>{}, std::integral_constant<int, TN>{}); \
-        return;                                                                  \
+#define X(TM, TN, WR)                                                                     \
+    if (t.tm == TM && t.tn == TN && t.wr == WR) {                                         \
+        f(std::integral_constant<int, TM>{}, std::integral_constant<int, TN>{},           \
+          std::integral_constant<int, WR>{});                                             \
+        return;                                                                           \
     }
     AMSIM_FOR_TAB_TILES(X)
 #undef X
@@ -1033,8 +1063,8 @@ Plan plan_gemm(int64_t m, int64_t n, int64_t k, int m_bits)
     size_t o = 0;
     if (p.lds) {
         p.tile = choose_tab_tile(m, n, k, 256, true);
-        p.a_ld = round_up(m, int64_t(64) * kWaves * p.tile.tm);
-        p.b_ld = round_up(n, p.tile.tn);
+        p.a_ld = round_up(m, int64_t(64) * p.tile.wr * p.tile.tm);
+        p.b_ld = round_up(n, tab_cols(p.tile));
         o = table_area(p, o);
     } else {
         p.tile = choose_tile(m, n, k, 1, true);
@@ -1127,7 +1157,7 @@ Plan plan_conv(const amsim_conv2d *d, int pass, int m_bits)
     p.splits = 1;
     if (pass == AMSIM_CONV_FWD) {
         p.tile = p.lds ? choose_tab_tile(npix_out, s.co, 1, 1, false) : choose_tile(npix_out, s.co, 1, 1, false);
-        p.b_ld = p.lds ? round_up(s.co, p.tile.tn) : round_up(s.co, int64_t(p.tile.tn) * kWaves);
+        p.b_ld = p.lds ? round_up(s.co, tab_cols(p.tile)) : round_up(s.co, int64_t(p.tile.tn) * kWaves);
         p.a_elems = p.lds ? int64_t(s.n) * p.Hp * p.Wp * s.ci : npix_in * s.ci;  // decoded x
         p.off_a = o;
         o += align_up(size_t(p.a_elems) * 4);
@@ -1136,7 +1166,7 @@ Plan plan_conv(const amsim_conv2d *d, int pass, int m_bits)
     } else if (pass == AMSIM_CONV_BWD_DATA) {
         const int64_t rows = bwd_data_rows(s);
         p.tile = p.lds ? choose_tab_tile(rows, s.ci, 1, 1, false) : choose_tile(rows, s.ci, 1, 1, false);
-        p.b_ld = p.lds ? round_up(s.ci, p.tile.tn) : round_up(s.ci, int64_t(p.tile.tn) * kWaves);
+        p.b_ld = p.lds ? round_up(s.ci, tab_cols(p.tile)) : round_up(s.ci, int64_t(p.tile.tn) * kWaves);
         if (p.lds) {
             int top, bottom, left, right;
             bwd_data_dy_pads(s, top, bottom, left, right);
@@ -1157,7 +1187,7 @@ Plan plan_conv(const amsim_conv2d *d, int pass, int m_bits)
         const int64_t taps = int64_t(s.n) * s.oh;
         if (p.lds) {
             p.tile = choose_tab_tile(R, s.co, taps, ceil_div(256, s.ow), true);
-            p.b_ld = round_up(s.co, p.tile.tn);
+            p.b_ld = round_up(s.co, tab_cols(p.tile));
             p.a_elems = int64_t(s.n) * p.Hp * p.Wp * s.ci;
         } else {
             p.tile = choose_tile(R, s.co, taps, s.ow, true);
@@ -1193,9 +1223,10 @@ int prep_rows(const uint32_t *lut, int m_bits, char *ws, const Plan &p, hipStrea
 template <int OP>
 int launch_tab(const Plan &p, const TabArgs &a, dim3 grid, hipStream_t st)
 {
-    auto run = [&](auto tm, auto tn) {
-        constexpr int TM = decltype(tm)::value, TN = decltype(tn)::value;
-        hipLaunchKernelGGL((tab_kernel<OP, TM, TN>), grid, dim3(kThreads), tab_lds_bytes<TN>(), st, a);
+    auto run = [&](auto tm, auto tn, auto wr) {
+        constexpr int TM = decltype(tm)::value, TN = decltype(tn)::value, WR = decltype(wr)::value;
+        hipLaunchKernelGGL((tab_kernel<OP, TM, TN, WR>), grid, dim3(kThreads), tab_lds_bytes(TN * (kWaves / WR)), st,
+                           a);
     };
     dispatch_tab_tile(p.tile, run);
     return launch_status();
@@ -1319,7 +1350,7 @@ int approx_gemm(int trans_a, int trans_b, int64_t m, int64_t n, int64_t k, const
     const Plan p = plan_gemm(m, n, k, m_bits);
     // decoded operands are addressed with 32-bit byte offsets
     if (k * p.a_ld >= (int64_t(1) << 29) || k * p.b_ld >= lim || int64_t(p.splits) * m * n >= lim ||
-        p.b_ld / (int64_t(p.tile.tn) * (p.lds ? 1 : kWaves)) > 65535)
+        p.b_ld / (p.lds ? tab_cols(p.tile) : int64_t(p.tile.tn) * kWaves) > 65535)
         return AMSIM_ERR_UNSUPPORTED;
     if (p.total > 0 && (!workspace || workspace_bytes < p.total)) return AMSIM_ERR_WORKSPACE;
     if (p.lds && ensure_attributes() != AMSIM_OK) return AMSIM_ERR_HIP;
@@ -1346,7 +1377,7 @@ int approx_gemm(int trans_a, int trans_b, int64_t m, int64_t n, int64_t k, const
         a.K = int(k);
         a.kchunk = p.per_split;
         a.taps = p.splits;
-        dim3 grid(unsigned(p.a_ld / (int64_t(64) * kWaves * t.tm)), unsigned(p.b_ld / t.tn), unsigned(p.splits));
+        dim3 grid(unsigned(p.a_ld / (int64_t(64) * t.wr * t.tm)), unsigned(p.b_ld / tab_cols(t)), unsigned(p.splits));
         TimedLaunch tl(AMSIM_KERNEL_GEMM, st);
         rc = launch_tab<OP_GEMM>(p, a, grid, st);
     } else {
@@ -1436,7 +1467,7 @@ int approx_conv2d_fwd(const amsim_conv2d *desc, const float *x, const float *w, 
     if (p.lds) {
         TabArgs a = tab_args(p, ws, Xd, p.a_elems, Wd, y, int(rows), s.co);
         a.s = s;
-        dim3 grid(unsigned(ceil_div(rows, int64_t(64) * kWaves * t.tm)), unsigned(p.b_ld / t.tn), 1);
+        dim3 grid(unsigned(ceil_div(rows, int64_t(64) * t.wr * t.tm)), unsigned(p.b_ld / tab_cols(t)), 1);
         return launch_tab<OP_FWD>(p, a, grid, st);
     }
     dim3 grid(unsigned(ceil_div(rows, 64 * t.tm)), unsigned(p.b_ld / (int64_t(t.tn) * kWaves)), 1);
@@ -1476,7 +1507,7 @@ int approx_conv2d_bwd_data(const amsim_conv2d *desc, const float *dy, const floa
     if (p.lds) {
         TabArgs a = tab_args(p, ws, Dyd, p.a_elems, Wtd, dx, int(rows), s.ci);
         a.s = s;
-        dim3 grid(unsigned(ceil_div(rows, int64_t(64) * kWaves * t.tm)), unsigned(p.b_ld / t.tn),
+        dim3 grid(unsigned(ceil_div(rows, int64_t(64) * t.wr * t.tm)), unsigned(p.b_ld / tab_cols(t)),
                   unsigned(s.sh * s.sw));
         return launch_tab<OP_BWD_DATA>(p, a, grid, st);
     }
@@ -1520,7 +1551,7 @@ int approx_conv2d_bwd_weight(const amsim_conv2d *desc, const float *x, const flo
             TabArgs a = tab_args(p, ws, Xd, p.a_elems, Dyd, out, R, s.co);
             a.s = s;
             a.taps = s.n * s.oh;
-            dim3 grid(unsigned(ceil_div(R, int64_t(64) * kWaves * t.tm)), unsigned(p.b_ld / t.tn),
+            dim3 grid(unsigned(ceil_div(R, int64_t(64) * t.wr * t.tm)), unsigned(p.b_ld / tab_cols(t)),
                       unsigned(p.splits));
             rc = launch_tab<OP_BWD_WEIGHT>(p, a, grid, st);
         } else {
