@@ -351,7 +351,7 @@ struct ConvShape {
 // consecutive reduction steps j = 0 .. count-1 whose first-operand word sits at
 //   A[lane row base + ubase + j * ustride]
 // and whose second-operand row is Bd[bbase + j].
-//   GEMM         tap = split z: rows i, A = op(A) k-major, row base i, ubase = kbeg * Mp
+//   GEMM         one tap of K steps: rows i, A = op(A) k-major, row base i
 //   FWD          tap = (kh, kw): rows (n, oh, ow), A = zero-padded x stored [n][h][ci][w], j = ci
 //   BWD_DATA     tap = valid (kh, kw) of the stride phase in blockIdx.z: rows (n, hq, wq),
 //                A = zero-padded dy stored [n][h][co][w], j = co; weights read as [kh][kw][co][ci]
@@ -359,6 +359,9 @@ struct ConvShape {
 //                B = dy
 // The channel-inside-row layouts put the lanes' consecutive output pixels on consecutive words,
 // so each first-operand load of a wave touches a few cache lines instead of 64.
+// The reduction is cut into chunks of 8 steps (a tap of `count` steps holds ceil(count / 8));
+// split s of blockIdx.z sums chunks [s * chunks_per_split, (s + 1) * chunks_per_split) into its
+// own partial result, laid out like the final one; a fixed-order pass adds the partials.
 enum { OP_GEMM = 0, OP_FWD = 1, OP_BWD_DATA = 2, OP_BWD_WEIGHT = 3 };
 
 struct TabArgs {
@@ -371,9 +374,10 @@ struct TabArgs {
     const unsigned char *rows;
     const int *eb;
     int R, N;            // result rows and columns
-    int taps;            // taps in total (GEMM: number of splits)
-    int taps_per_split;  // taps per blockIdx.z (BWD_WEIGHT split reduction); phases for BWD_DATA use z
-    int Mp, K, kchunk;   // GEMM
+    int splits;          // reduction splits: blockIdx.z = (phase *) splits + split
+    int chunks_per_split;  // reduction chunks (8 steps each) per split
+    int64_t out_elems;   // elements of one split's partial result (splits > 1)
+    int Mp, K;           // GEMM
     ConvShape s;
     int Hp, Wp;          // zero-padded x (FWD, BWD_WEIGHT)
     int OHp, OWp, pad_oh, pad_ow;  // zero-padded dy (BWD_DATA)
@@ -390,12 +394,16 @@ __device__ __forceinline__ void phase_dims(const ConvShape &s, int ph, int pw, i
     wq_n = pw < s.w ? (s.w - pw + s.sw - 1) / s.sw : 0;
 }
 
+// blockIdx.z = phase * splits + split (phase only for BWD_DATA, else 0)
+__device__ __forceinline__ int tab_phase(const TabArgs &a) { return int(blockIdx.z) / a.splits; }
+__device__ __forceinline__ int tab_split(const TabArgs &a) { return int(blockIdx.z) % a.splits; }
+
 template <int OP>
 __device__ __forceinline__ int tab_rows(const TabArgs &a)
 {
     if constexpr (OP == OP_BWD_DATA) {
         int hq_n, wq_n;
-        phase_dims(a.s, int(blockIdx.z) / a.s.sw, int(blockIdx.z) % a.s.sw, hq_n, wq_n);
+        phase_dims(a.s, tab_phase(a) / a.s.sw, tab_phase(a) % a.s.sw, hq_n, wq_n);
         return a.s.n * hq_n * wq_n;
     } else {
         return a.R;
@@ -415,7 +423,7 @@ __device__ __forceinline__ void tab_row(const TabArgs &a, int row, int &abase, i
         abase = (n * a.Hp + oh * s.sh) * s.ci * a.Wp + ow * s.sw;  // x as [n][hp][ci][wp]
         obase = int64_t(row) * s.co;
     } else if constexpr (OP == OP_BWD_DATA) {
-        const int ph = int(blockIdx.z) / s.sw, pw = int(blockIdx.z) % s.sw;
+        const int ph = tab_phase(a) / s.sw, pw = tab_phase(a) % s.sw;
         int hq_n, wq_n;
         phase_dims(s, ph, pw, hq_n, wq_n);
         const int wq = row % wq_n, hq = (row / wq_n) % hq_n, n = row / (wq_n * hq_n);
@@ -428,28 +436,34 @@ __device__ __forceinline__ void tab_row(const TabArgs &a, int row, int &abase, i
     }
 }
 
-// Tap range of this workgroup.
+// Taps of the reduction (BWD_DATA: of this workgroup's stride phase).
 template <int OP>
-__device__ __forceinline__ void tab_tap_range(const TabArgs &a, int &t0, int &t1)
+__device__ __forceinline__ int tab_taps(const TabArgs &a)
 {
     if constexpr (OP == OP_GEMM) {
-        t0 = int(blockIdx.z);
-        t1 = t0 + 1;
+        return 1;
     } else if constexpr (OP == OP_BWD_WEIGHT) {
-        t0 = int(blockIdx.z) * a.taps_per_split;
-        t1 = min(a.taps, t0 + a.taps_per_split);
+        return a.s.n * a.s.oh;
     } else if constexpr (OP == OP_BWD_DATA) {
         const ConvShape &s = a.s;
-        const int ph = int(blockIdx.z) / s.sw, pw = int(blockIdx.z) % s.sw;
+        const int ph = tab_phase(a) / s.sw, pw = tab_phase(a) % s.sw;
         const int kh0 = (ph + s.pt) % s.sh, kw0 = (pw + s.pl) % s.sw;
         const int nvh = kh0 < s.kh ? (s.kh - kh0 + s.sh - 1) / s.sh : 0;
         const int nvw = kw0 < s.kw ? (s.kw - kw0 + s.sw - 1) / s.sw : 0;
-        t0 = 0;
-        t1 = nvh * nvw;
+        return nvh * nvw;
     } else {
-        t0 = 0;
-        t1 = a.s.kh * a.s.kw;
+        return a.s.kh * a.s.kw;
     }
+}
+
+// Steps per tap (the same for every tap of an operation).
+template <int OP>
+__device__ __forceinline__ int tab_count(const TabArgs &a)
+{
+    if constexpr (OP == OP_GEMM) return a.K;
+    else if constexpr (OP == OP_FWD) return a.s.ci;
+    else if constexpr (OP == OP_BWD_DATA) return a.s.co;
+    else return a.s.ow;
 }
 
 template <int OP>
@@ -458,11 +472,10 @@ __device__ __forceinline__ TabTap tab_tap(const TabArgs &a, int tap)
     const ConvShape &s = a.s;
     TabTap t;
     if constexpr (OP == OP_GEMM) {
-        const int kbeg = tap * a.kchunk;
-        t.count = min(a.kchunk, a.K - kbeg);
-        t.ubase = kbeg * a.Mp;
+        t.count = a.K;
+        t.ubase = 0;
         t.ustride = a.Mp;
-        t.bbase = kbeg;
+        t.bbase = 0;
     } else if constexpr (OP == OP_FWD) {
         const int kh = tap / s.kw, kw = tap % s.kw;
         t.count = s.ci;
@@ -470,7 +483,7 @@ __device__ __forceinline__ TabTap tab_tap(const TabArgs &a, int tap)
         t.ustride = a.Wp;
         t.bbase = tap * s.ci;
     } else if constexpr (OP == OP_BWD_DATA) {
-        const int ph = int(blockIdx.z) / s.sw, pw = int(blockIdx.z) % s.sw;
+        const int ph = tab_phase(a) / s.sw, pw = tab_phase(a) % s.sw;
         const int kh0 = (ph + s.pt) % s.sh, kw0 = (pw + s.pl) % s.sw;
         const int nvw = (s.kw - kw0 + s.sw - 1) / s.sw;
         const int kh = kh0 + (tap / nvw) * s.sh, kw = kw0 + (tap % nvw) * s.sw;
@@ -568,8 +581,12 @@ __device__ __forceinline__ void tab_body(const TabArgs &a)
         aoff[r] = uint32_t(ab) * 4u;
         obase[r] = ob;
     }
-    int t0, t1;
-    tab_tap_range<OP>(a, t0, t1);
+    // this split's chunks, as positions p = tap * (8 * chunks per tap) + step
+    const int count = tab_count<OP>(a);
+    const int cpt = (count + 7) / 8;  // chunks per tap
+    const int q_total = tab_taps<OP>(a) * cpt;
+    const int q0 = tab_split(a) * a.chunks_per_split;
+    const int p_end = min(q_total, q0 + a.chunks_per_split) * 8;
 
     u32x4 stage[CPT];
     float stage_pb[CPT];
@@ -577,29 +594,30 @@ __device__ __forceinline__ void tab_body(const TabArgs &a)
     init_acc(acc);
     uint32_t acur[TM];
     TabTap cur{0, 0, 0, 0};
-    int c0 = 0;
-    bool have = t0 < t1;
+    int tap = q0 / max(cpt, 1);
+    int c0 = (q0 - tap * cpt) * 8;
+    bool have = q0 * 8 < p_end;
     if (have) {
-        cur = tab_tap<OP>(a, t0);
-        tab_fetch<TNW, EB, CPT>(stage, stage_pb, cur, 0, a.Bd, a.Np, colw, a.rows);
+        cur = tab_tap<OP>(a, tap);
+        tab_fetch<TNW, EB, CPT>(stage, stage_pb, cur, c0, a.Bd, a.Np, colw, a.rows);
         tab_commit<TNW, EB, CPT>(stage, stage_pb, smem, pbs, 0);
 #pragma unroll
         for (int r = 0; r < TM; ++r)
-            acur[r] = __builtin_amdgcn_raw_buffer_load_b32(ares, aoff[r], uint32_t(cur.ubase) * 4u, 0);
+            acur[r] = __builtin_amdgcn_raw_buffer_load_b32(ares, aoff[r], uint32_t(cur.ubase + c0 * cur.ustride) * 4u,
+                                                           0);
     }
     __syncthreads();
-    int tap = t0;
     int buf = 0;
     while (have) {
         // the slab after this one
         TabTap nxt = cur;
         int ntap = tap, nc0 = c0 + KS;
-        if (nc0 >= cur.count) {
+        if (nc0 >= count) {
             ntap = tap + 1;
             nc0 = 0;
-            if (ntap < t1) nxt = tab_tap<OP>(a, ntap);
         }
-        const bool has_next = ntap < t1;
+        const bool has_next = ntap * cpt * 8 + nc0 < p_end;
+        if (has_next && ntap != tap) nxt = tab_tap<OP>(a, ntap);
         if (has_next) tab_fetch<TNW, EB, CPT>(stage, stage_pb, nxt, nc0, a.Bd, a.Np, colw, a.rows);
         const unsigned char *tb = smem + buf * SLAB + cg * TN * ROWB;
         const float *pb_s = pbs + buf * KS * TNW + cg * TN;
@@ -647,13 +665,13 @@ __device__ __forceinline__ void tab_body(const TabArgs &a)
         have = has_next;
     }
 
-    // results: split partial sums go to [z][R][N] (GEMM, BWD_WEIGHT with gridDim.z > 1)
-    const bool partial = (OP == OP_GEMM || OP == OP_BWD_WEIGHT) && gridDim.z > 1;
+    // results (with splits, each split's partial result is laid out like the final one)
+    float *out = a.out + int64_t(tab_split(a)) * a.out_elems;
 #pragma unroll
     for (int r = 0; r < TM; ++r) {
         const int row = row0 + 64 * r;
         if (row >= R) continue;
-        float *dst = partial ? a.out + (int64_t(blockIdx.z) * R + row) * a.N : a.out + obase[r];
+        float *dst = out + obase[r];
 #pragma unroll
         for (int t = 0; t < TN; ++t) {
             const int col = col0 + t;
@@ -1043,9 +1061,18 @@ struct Plan {
     size_t off_rows, off_eb, off_a, off_b, off_part, total;
     int64_t a_ld, b_ld;   // GEMM: padded leading dims of the decoded operands; conv: b_ld only
     int64_t a_elems;      // conv: elements of the decoded first operand
-    int splits, per_split;
+    int splits, per_split;  // global path: steps (GEMM) or output rows (bwd_weight) per split
+    int chunks_per_split;   // table path: 8-step reduction chunks per split
+    int64_t out_elems;      // elements of the result (partial sums hold splits of them)
     int Hp, Wp, OHp, OWp, pad_oh, pad_ow;
 };
+
+// Table path split of a reduction of q chunks (8 steps each).
+void plan_tab_split(Plan &p, int64_t q)
+{
+    p.chunks_per_split = int(std::max<int64_t>(1, ceil_div(q, p.tile.split)));
+    p.splits = int(std::max<int64_t>(1, ceil_div(q, p.chunks_per_split)));
+}
 
 bool valid_m(int m_bits) { return m_bits >= 1 && m_bits <= 11; }
 
@@ -1062,9 +1089,10 @@ Plan plan_gemm(int64_t m, int64_t n, int64_t k, int m_bits)
     p.lds = lds_path(m_bits);
     size_t o = 0;
     if (p.lds) {
-        p.tile = choose_tab_tile(m, n, k, 256, true);
+        p.tile = choose_tab_tile(m, n, ceil_div(k, 8), 32, true);
         p.a_ld = round_up(m, int64_t(64) * p.tile.wr * p.tile.tm);
         p.b_ld = round_up(n, tab_cols(p.tile));
+        plan_tab_split(p, ceil_div(k, 8));
         o = table_area(p, o);
     } else {
         p.tile = choose_tile(m, n, k, 1, true);
@@ -1075,8 +1103,11 @@ Plan plan_gemm(int64_t m, int64_t n, int64_t k, int m_bits)
     o += align_up(size_t(k) * p.a_ld * 4);
     p.off_b = o;
     o += align_up(size_t(k) * p.b_ld * 4);
-    p.per_split = int(ceil_div(k, p.tile.split));
-    p.splits = int(ceil_div(k, p.per_split));
+    if (!p.lds) {
+        p.per_split = int(ceil_div(k, p.tile.split));
+        p.splits = int(ceil_div(k, p.per_split));
+    }
+    p.out_elems = m * n;
     p.off_part = o;
     if (p.splits > 1) o += align_up(size_t(p.splits) * m * n * 4);
     p.total = o;
@@ -1111,7 +1142,7 @@ int check_conv(const amsim_conv2d *d)
     const int64_t y = int64_t(d->n) * oh * ow * (d->c_out + 16);
     if (xp >= lim || yp >= lim || w >= lim || y >= lim || d->pad_top >= 65536 || d->pad_bottom >= 65536 ||
         d->pad_left >= 65536 || d->pad_right >= 65536 || d->kh >= 65536 || d->kw >= 65536 ||
-        int64_t(d->stride_h) * d->stride_w > 65535 || d->c_in > 65535 * 16 || d->c_out > 65535 * 16)
+        int64_t(d->stride_h) * d->stride_w > 32 || d->c_in > 65535 * 16 || d->c_out > 65535 * 16)
         return AMSIM_ERR_UNSUPPORTED;
     return AMSIM_OK;
 }
@@ -1156,16 +1187,21 @@ Plan plan_conv(const amsim_conv2d *d, int pass, int m_bits)
     p.Wp = d->w + d->pad_left + d->pad_right;
     p.splits = 1;
     if (pass == AMSIM_CONV_FWD) {
-        p.tile = p.lds ? choose_tab_tile(npix_out, s.co, 1, 1, false) : choose_tile(npix_out, s.co, 1, 1, false);
+        const int64_t q = int64_t(s.kh) * s.kw * ceil_div(s.ci, 8);
+        p.tile = p.lds ? choose_tab_tile(npix_out, s.co, q, 16, true) : choose_tile(npix_out, s.co, 1, 1, false);
+        if (p.lds) plan_tab_split(p, q);
         p.b_ld = p.lds ? round_up(s.co, tab_cols(p.tile)) : round_up(s.co, int64_t(p.tile.tn) * kWaves);
         p.a_elems = p.lds ? int64_t(s.n) * p.Hp * p.Wp * s.ci : npix_in * s.ci;  // decoded x
+        p.out_elems = npix_out * s.co;
         p.off_a = o;
         o += align_up(size_t(p.a_elems) * 4);
         p.off_b = o;  // decoded w [kh*kw*ci][COp]
         o += align_up(size_t(s.kh) * s.kw * s.ci * p.b_ld * 4);
     } else if (pass == AMSIM_CONV_BWD_DATA) {
         const int64_t rows = bwd_data_rows(s);
-        p.tile = p.lds ? choose_tab_tile(rows, s.ci, 1, 1, false) : choose_tile(rows, s.ci, 1, 1, false);
+        const int64_t q = ceil_div(s.kh, s.sh) * ceil_div(s.kw, s.sw) * ceil_div(s.co, 8);  // largest phase
+        p.tile = p.lds ? choose_tab_tile(rows, s.ci, q, 16, true) : choose_tile(rows, s.ci, 1, 1, false);
+        if (p.lds) plan_tab_split(p, q);
         p.b_ld = p.lds ? round_up(s.ci, tab_cols(p.tile)) : round_up(s.ci, int64_t(p.tile.tn) * kWaves);
         if (p.lds) {
             int top, bottom, left, right;
@@ -1178,6 +1214,7 @@ Plan plan_conv(const amsim_conv2d *d, int pass, int m_bits)
         } else {
             p.a_elems = npix_out * s.co;
         }
+        p.out_elems = npix_in * s.ci;
         p.off_a = o;
         o += align_up(size_t(p.a_elems) * 4);
         p.off_b = o;  // decoded w^T [kh][kw][co][CIp]
@@ -1186,23 +1223,26 @@ Plan plan_conv(const amsim_conv2d *d, int pass, int m_bits)
         const int64_t R = int64_t(s.kh) * s.kw * s.ci;
         const int64_t taps = int64_t(s.n) * s.oh;
         if (p.lds) {
-            p.tile = choose_tab_tile(R, s.co, taps, ceil_div(256, s.ow), true);
+            const int64_t q = taps * ceil_div(s.ow, 8);
+            p.tile = choose_tab_tile(R, s.co, q, 16, true);
+            plan_tab_split(p, q);
             p.b_ld = round_up(s.co, tab_cols(p.tile));
             p.a_elems = int64_t(s.n) * p.Hp * p.Wp * s.ci;
         } else {
             p.tile = choose_tile(R, s.co, taps, s.ow, true);
             p.b_ld = round_up(s.co, int64_t(p.tile.tn) * kWaves);
             p.a_elems = npix_in * s.ci;
+            p.per_split = int(ceil_div(taps, p.tile.split));
+            p.splits = int(ceil_div(taps, p.per_split));
         }
-        p.per_split = int(ceil_div(taps, p.tile.split));
-        p.splits = int(ceil_div(taps, p.per_split));
+        p.out_elems = R * s.co;
         p.off_a = o;  // decoded x
         o += align_up(size_t(p.a_elems) * 4);
         p.off_b = o;  // decoded dy [n*oh*ow][COp]
         o += align_up(size_t(npix_out) * p.b_ld * 4);
-        p.off_part = o;
-        if (p.splits > 1) o += align_up(size_t(p.splits) * R * s.co * 4);
     }
+    p.off_part = o;
+    if (p.splits > 1) o += align_up(size_t(p.splits) * p.out_elems * 4);
     p.total = o;
     return p;
 }
@@ -1251,7 +1291,9 @@ TabArgs tab_args(const Plan &p, char *ws, const uint32_t *A, int64_t a_elems, co
     a.OWp = p.OWp;
     a.pad_oh = p.pad_oh;
     a.pad_ow = p.pad_ow;
-    a.taps_per_split = p.per_split;
+    a.splits = p.lds ? p.splits : 1;
+    a.chunks_per_split = p.chunks_per_split;
+    a.out_elems = p.out_elems;
     return a;
 }
 
@@ -1372,11 +1414,9 @@ int approx_gemm(int trans_a, int trans_b, int64_t m, int64_t n, int64_t k, const
     int rc;
     if (p.lds) {
         TabArgs a = tab_args(p, ws, Ad, k * p.a_ld, Bd, out, int(m), int(n));
-        a.ldc = ldc;
+        a.ldc = p.splits > 1 ? n : ldc;  // partial sums are dense
         a.Mp = int(p.a_ld);
         a.K = int(k);
-        a.kchunk = p.per_split;
-        a.taps = p.splits;
         dim3 grid(unsigned(p.a_ld / (int64_t(64) * t.wr * t.tm)), unsigned(p.b_ld / tab_cols(t)), unsigned(p.splits));
         TimedLaunch tl(AMSIM_KERNEL_GEMM, st);
         rc = launch_tab<OP_GEMM>(p, a, grid, st);
@@ -1463,13 +1503,23 @@ int approx_conv2d_fwd(const amsim_conv2d *desc, const float *x, const float *w, 
     if (launch_status() != AMSIM_OK) return AMSIM_ERR_HIP;
     const Tile t = p.tile;
     const int64_t rows = int64_t(s.n) * s.oh * s.ow;
-    TimedLaunch tl(AMSIM_KERNEL_CONV_FWD, st);
     if (p.lds) {
-        TabArgs a = tab_args(p, ws, Xd, p.a_elems, Wd, y, int(rows), s.co);
+        float *out = p.splits > 1 ? reinterpret_cast<float *>(ws + p.off_part) : y;
+        TabArgs a = tab_args(p, ws, Xd, p.a_elems, Wd, out, int(rows), s.co);
         a.s = s;
-        dim3 grid(unsigned(ceil_div(rows, int64_t(64) * t.wr * t.tm)), unsigned(p.b_ld / tab_cols(t)), 1);
-        return launch_tab<OP_FWD>(p, a, grid, st);
+        dim3 grid(unsigned(ceil_div(rows, int64_t(64) * t.wr * t.tm)), unsigned(p.b_ld / tab_cols(t)),
+                  unsigned(p.splits));
+        {
+            TimedLaunch tl(AMSIM_KERNEL_CONV_FWD, st);
+            rc = launch_tab<OP_FWD>(p, a, grid, st);
+        }
+        if (rc != AMSIM_OK || p.splits == 1) return rc;
+        hipLaunchKernelGGL(reduce_splits_kernel, dim3(grid_for(p.out_elems)), dim3(256), 0, st,
+                           reinterpret_cast<const float *>(ws + p.off_part), p.splits, int(rows), s.co, y,
+                           int64_t(s.co));
+        return launch_status();
     }
+    TimedLaunch tl(AMSIM_KERNEL_CONV_FWD, st);
     dim3 grid(unsigned(ceil_div(rows, 64 * t.tm)), unsigned(p.b_ld / (int64_t(t.tn) * kWaves)), 1);
     auto run = [&](auto tm, auto tn) {
         constexpr int TM = decltype(tm)::value, TN = decltype(tn)::value;
@@ -1503,14 +1553,23 @@ int approx_conv2d_bwd_data(const amsim_conv2d *desc, const float *dy, const floa
     if (launch_status() != AMSIM_OK) return AMSIM_ERR_HIP;
     const Tile t = p.tile;
     const int64_t rows = bwd_data_rows(s);
-    TimedLaunch tl(AMSIM_KERNEL_CONV_BWD_DATA, st);
     if (p.lds) {
-        TabArgs a = tab_args(p, ws, Dyd, p.a_elems, Wtd, dx, int(rows), s.ci);
+        float *out = p.splits > 1 ? reinterpret_cast<float *>(ws + p.off_part) : dx;
+        TabArgs a = tab_args(p, ws, Dyd, p.a_elems, Wtd, out, int(rows), s.ci);
         a.s = s;
         dim3 grid(unsigned(ceil_div(rows, int64_t(64) * t.wr * t.tm)), unsigned(p.b_ld / tab_cols(t)),
-                  unsigned(s.sh * s.sw));
-        return launch_tab<OP_BWD_DATA>(p, a, grid, st);
+                  unsigned(s.sh * s.sw * p.splits));
+        {
+            TimedLaunch tl(AMSIM_KERNEL_CONV_BWD_DATA, st);
+            rc = launch_tab<OP_BWD_DATA>(p, a, grid, st);
+        }
+        if (rc != AMSIM_OK || p.splits == 1) return rc;
+        hipLaunchKernelGGL(reduce_splits_kernel, dim3(grid_for(p.out_elems)), dim3(256), 0, st,
+                           reinterpret_cast<const float *>(ws + p.off_part), p.splits, s.n * s.h * s.w, s.ci, dx,
+                           int64_t(s.ci));
+        return launch_status();
     }
+    TimedLaunch tl(AMSIM_KERNEL_CONV_BWD_DATA, st);
     dim3 grid(unsigned(ceil_div(rows, 64 * t.tm)), unsigned(p.b_ld / (int64_t(t.tn) * kWaves)),
               unsigned(s.sh * s.sw));
     auto run = [&](auto tm, auto tn) {
@@ -1550,7 +1609,6 @@ int approx_conv2d_bwd_weight(const amsim_conv2d *desc, const float *x, const flo
         if (p.lds) {
             TabArgs a = tab_args(p, ws, Xd, p.a_elems, Dyd, out, R, s.co);
             a.s = s;
-            a.taps = s.n * s.oh;
             dim3 grid(unsigned(ceil_div(R, int64_t(64) * t.wr * t.tm)), unsigned(p.b_ld / tab_cols(t)),
                       unsigned(p.splits));
             rc = launch_tab<OP_BWD_WEIGHT>(p, a, grid, st);

@@ -189,6 +189,8 @@ CONV_CASES = [
     W.conv_desc(1, 16, 16, 3, 20, 7, 7, 2, 3),
     W.conv_desc(1, 6, 7, 2, 2, 3, 3, 3, pads=(0, 2, 1, 0)),
     W.conv_desc(2, 5, 4, 2, 3, 4, 4, 2, pads=(3, 3, 3, 3)),
+    W.conv_desc(2, 5, 5, 300, 20, 3, 3, 1, 1),
+    W.conv_desc(2, 6, 6, 24, 200, 3, 3, 2, 1),
 ]
 
 
