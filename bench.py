@@ -158,7 +158,8 @@ def main():
     achieved = FLOP_PER_APPROX_MAC * gemm_macs / g_avg_s / 1e12
     roofline = {"bound": "alu", "achieved": round(achieved, 3), "peak": FP32_VECTOR_PEAK_TFLOPS,
                 "unit": "TFLOP/s", "frac": round(achieved / FP32_VECTOR_PEAK_TFLOPS, 4),
-                "traffic": read_traffic(), "kernel": "gemm_kernel (approx_gemm 4096^3, Mitchell M=7, LDS table)"}
+                "traffic": read_traffic(),
+                "kernel": "tab_kernel<OP_GEMM, 4, 8, 4> (approx_gemm 4096^3, Mitchell M=7, 1-byte LDS tables)"}
 
     out = {
         "metric": METRIC,

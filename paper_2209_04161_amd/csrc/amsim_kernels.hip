@@ -40,6 +40,8 @@ constexpr int kWaves = 4;           // waves per workgroup (column groups)
 constexpr int kThreads = 64 * kWaves;
 constexpr int kMaxLdsBits = 7;      // table in LDS for M <= 7 (64 KiB)
 
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+
 // ------------------------------------------------------------------ device helpers -------
 
 __device__ __forceinline__ uint32_t amsim_decode(uint32_t u, int m, int shift)
@@ -119,88 +121,242 @@ __device__ __forceinline__ void init_acc(float (&acc)[TM][TN])
 
 __device__ __forceinline__ int wave_id() { return __builtin_amdgcn_readfirstlane(threadIdx.x >> 6); }
 
+// Exponent range of the operands a decode pass has seen, for the table kernels' bf16 path
+// (which is exact only while no product can leave the normal range).  Finite non-zero operands
+// count; zeros and denormals (read as zeros) do not.  One packed word per workgroup:
+//   bits 0..7 smallest exponent field, 8..15 largest, bit 16 set if an Inf or NaN was seen.
+constexpr int kStatSlots = 8192;  // most workgroups of a decode launch that records them
+
+struct ExpStats {
+    uint32_t lo = 255u, hi = 0u, special = 0u;
+    __device__ __forceinline__ void add(uint32_t u)
+    {
+        const uint32_t e = (u >> 23) & 0xFFu;
+        if (e == 0xFFu) {
+            special = 1u;
+        } else if (e != 0u) {
+            lo = min(lo, e);
+            hi = max(hi, e);
+        }
+    }
+};
+
+__device__ __forceinline__ uint32_t wave_min(uint32_t v)
+{
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) v = min(v, uint32_t(__shfl_xor(int(v), o)));
+    return v;
+}
+
+__device__ __forceinline__ uint32_t wave_max(uint32_t v)
+{
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) v = max(v, uint32_t(__shfl_xor(int(v), o)));
+    return v;
+}
+
+// Workgroup reduction of the threads' statistics into stats[slot] (every thread of a workgroup
+// of at most 1024 threads must call it).  Reduced within each wave first: same-address LDS
+// atomics from every thread would serialise.  Once an Inf or NaN is seen the largest exponent no
+// longer matters, so it travels with the special flag in one maximum.
+__device__ __forceinline__ void store_stats(const ExpStats &s, uint32_t *stats, int slot)
+{
+    __shared__ uint32_t s_lo[16], s_hs[16];
+    if (stats == nullptr) return;  // uniform: the whole launch records or none of it
+    const uint32_t lo = wave_min(s.lo), hs = wave_max((s.special << 8) | s.hi);
+    const int wave = int(threadIdx.x) >> 6, nwaves = int(blockDim.x + 63) >> 6;
+    if ((threadIdx.x & 63) == 0) {
+        s_lo[wave] = lo;
+        s_hs[wave] = hs;
+    }
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        uint32_t l = 255u, h = 0u;
+        for (int i = 0; i < nwaves; ++i) {
+            l = min(l, s_lo[i]);
+            h = max(h, s_hs[i]);
+        }
+        stats[slot] = l | ((h & 0xFFu) << 8) | ((h >> 8) << 16);
+    }
+}
+
 // ------------------------------------------------------------------ pre-pass kernels -----
 
 // dst[(b * rows + r) * dld + c] = decode(src[b * sb + r * sr + c * sc]) for r < rows, c < cols;
-// padding columns c in [cols, dld) are written as decoded +0.
-__global__ void decode_kernel(const float *__restrict__ src, int64_t sb, int64_t sr, int64_t sc, int batches,
-                              int rows, int cols, uint32_t *__restrict__ dst, int dld, int m, int shift)
+// padding columns c in [cols, dld) are written as decoded +0.  dld is a multiple of 4 and
+// batches * rows * dld / 4 < 2^31: each thread takes groups of 4 columns (16-byte stores), two
+// groups per iteration so that 8 loads are in flight.  vec: sc == 1 and every row start is
+// 16-byte aligned, so a full group is one 16-byte load.
+__global__ __launch_bounds__(256) void decode_kernel(const float *__restrict__ src, int64_t sb, int64_t sr, int64_t sc,
+                                                     int batches, int rows, int cols, uint32_t *__restrict__ dst,
+                                                     int dld, int m, int shift, uint32_t *__restrict__ stats, int vec)
 {
-    const int64_t per = int64_t(rows) * dld;
-    const int64_t total = per * batches;
-    for (int64_t i = int64_t(blockIdx.x) * blockDim.x + threadIdx.x; i < total;
-         i += int64_t(gridDim.x) * blockDim.x) {
-        const int b = int(i / per);
-        const int64_t rem = i - b * per;
-        const int r = int(rem / dld), c = int(rem % dld);
-        uint32_t w = 0u;
-        if (c < cols) w = amsim_decode(__float_as_uint(src[b * sb + int64_t(r) * sr + int64_t(c) * sc]), m, shift);
-        dst[i] = w;
+    const uint32_t qpr = uint32_t(dld) / 4u;
+    const uint32_t total = uint32_t(batches) * uint32_t(rows) * qpr;
+    const uint32_t step = gridDim.x * blockDim.x;
+    ExpStats st;
+    for (uint32_t q0 = blockIdx.x * blockDim.x + threadIdx.x; q0 < total; q0 += 2u * step) {
+        uint32_t w[2][4];
+        uint32_t row[2], c[2];
+        bool live[2];
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+            const uint32_t q = q0 + uint32_t(h) * step;
+            live[h] = q < total;
+            row[h] = live[h] ? q / qpr : 0u;
+            c[h] = (q - row[h] * qpr) * 4u;
+            const uint32_t b = row[h] / uint32_t(rows), r = row[h] - b * uint32_t(rows);
+            const float *base = src + int64_t(b) * sb + int64_t(r) * sr;
+            if (vec && live[h] && c[h] + 4u <= uint32_t(cols)) {
+                const u32x4 q4 = *reinterpret_cast<const u32x4 *>(base + c[h]);
+#pragma unroll
+                for (int e = 0; e < 4; ++e) w[h][e] = q4[e];
+            } else {
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    const uint32_t ce = c[h] + uint32_t(e);
+                    w[h][e] = (live[h] && ce < uint32_t(cols)) ? __float_as_uint(base[int64_t(ce) * sc]) : 0u;
+                }
+            }
+        }
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+            if (!live[h]) continue;
+            u32x4 o;
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                // padding columns and +0 operands both decode to 0 and leave the statistics alone
+                st.add(w[h][e]);
+                o[e] = amsim_decode(w[h][e], m, shift);
+            }
+            *reinterpret_cast<u32x4 *>(dst + int64_t(row[h]) * dld + c[h]) = o;
+        }
     }
+    store_stats(st, stats, blockIdx.x);
 }
 
 // Decoded NHWC tensor inside a zero border: dst[n][hp][wp][c] = decode(src[n][hp-top][wp-left][c])
-// where that pixel exists, decoded +0 elsewhere.
-__global__ void decode_pad_kernel(const float *__restrict__ src, int n, int h, int w, int c, int top, int left,
-                                  int hp, int wp, uint32_t *__restrict__ dst, int m, int shift)
+// where that pixel exists, decoded +0 elsewhere.  One padded image row (wp * c words, of which
+// the w * c in the middle come from one contiguous source row) per workgroup iteration.
+__global__ __launch_bounds__(256) void decode_pad_kernel(const float *__restrict__ src, int n, int h, int w, int c,
+                                                         int top, int left, int hp, int wp,
+                                                         uint32_t *__restrict__ dst, int m, int shift,
+                                                         uint32_t *__restrict__ stats)
 {
-    const int64_t total = int64_t(n) * hp * wp * c;
-    for (int64_t i = int64_t(blockIdx.x) * blockDim.x + threadIdx.x; i < total;
-         i += int64_t(gridDim.x) * blockDim.x) {
-        const int ch = int(i % c);
-        const int64_t pix = i / c;
-        const int x = int(pix % wp), y = int((pix / wp) % hp), b = int(pix / (int64_t(wp) * hp));
-        const int ih = y - top, iw = x - left;
-        uint32_t word = 0u;
-        if (unsigned(ih) < unsigned(h) && unsigned(iw) < unsigned(w))
-            word = amsim_decode(__float_as_uint(src[((int64_t(b) * h + ih) * w + iw) * c + ch]), m, shift);
-        dst[i] = word;
+    const int len = wp * c, lead = left * c, body = w * c;
+    ExpStats st;
+    for (int rr = blockIdx.x; rr < n * hp; rr += gridDim.x) {
+        const int b = rr / hp, y = rr - b * hp, ih = y - top;
+        const bool inside = unsigned(ih) < unsigned(h);
+        const float *srow = src + (int64_t(b) * h + ih) * body;
+        uint32_t *drow = dst + int64_t(rr) * len;
+        for (int i0 = threadIdx.x; i0 < len; i0 += 4 * 256) {
+            uint32_t v[4];
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                const int j = i0 + e * 256 - lead;
+                v[e] = (inside && i0 + e * 256 < len && unsigned(j) < unsigned(body)) ? __float_as_uint(srow[j]) : 0u;
+            }
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                if (i0 + e * 256 >= len) break;
+                st.add(v[e]);
+                drow[i0 + e * 256] = amsim_decode(v[e], m, shift);
+            }
+        }
     }
+    store_stats(st, stats, blockIdx.x);
 }
 
 // Decoded NHWC tensor re-laid out as [n][hp][c][wp] inside a zero border:
-// dst[n][y][ch][x] = decode(src[n][y-top][x-left][ch]) where that pixel exists, decoded +0 elsewhere.
-__global__ void decode_pad_nhcw_kernel(const float *__restrict__ src, int n, int h, int w, int c, int top, int left,
-                                       int hp, int wp, uint32_t *__restrict__ dst, int m, int shift)
+// dst[n][y][ch][x] = decode(src[n][y-top][x-left][ch]) where that pixel exists, decoded +0
+// elsewhere.  A workgroup takes one padded image row at a time: the source row (w pixels x cc
+// channels at a time, contiguous loads) goes through LDS as [channel][x] (row pitch w | 1, odd,
+// so the transposing stores do not collide in banks), then each wave writes whole channel rows.
+constexpr int kNhcwTile = 8192;  // words of the LDS tile: cc * (w | 1) <= kNhcwTile
+
+__global__ __launch_bounds__(256) void decode_pad_nhcw_kernel(const float *__restrict__ src, int n, int h, int w, int c,
+                                                              int top, int left, int hp, int wp,
+                                                              uint32_t *__restrict__ dst, int m, int shift,
+                                                              uint32_t *__restrict__ stats, int cc)
 {
-    const int64_t total = int64_t(n) * hp * wp * c;
-    for (int64_t i = int64_t(blockIdx.x) * blockDim.x + threadIdx.x; i < total;
-         i += int64_t(gridDim.x) * blockDim.x) {
-        const int x = int(i % wp);
-        const int64_t rest = i / wp;
-        const int ch = int(rest % c);
-        const int64_t r2 = rest / c;
-        const int y = int(r2 % hp), b = int(r2 / hp);
-        const int ih = y - top, iw = x - left;
-        uint32_t word = 0u;
-        if (unsigned(ih) < unsigned(h) && unsigned(iw) < unsigned(w))
-            word = amsim_decode(__float_as_uint(src[((int64_t(b) * h + ih) * w + iw) * c + ch]), m, shift);
-        dst[i] = word;
+    __shared__ uint32_t tile[kNhcwTile];
+    const int ws = w | 1;
+    const int wave = int(threadIdx.x) >> 6, lane = int(threadIdx.x) & 63;
+    ExpStats st;
+    for (int rr = blockIdx.x; rr < n * hp; rr += gridDim.x) {
+        const int b = rr / hp, y = rr - b * hp, ih = y - top;
+        uint32_t *dimg = dst + int64_t(rr) * c * wp;
+        if (unsigned(ih) >= unsigned(h)) {  // a padding row (uniform over the workgroup)
+            for (int i = threadIdx.x; i < c * wp; i += 256) dimg[i] = 0u;
+            continue;
+        }
+        const float *srow = src + (int64_t(b) * h + ih) * w * c;
+        for (int c0 = 0; c0 < c; c0 += cc) {
+            const int ccn = min(cc, c - c0), cnt = w * ccn;
+            __syncthreads();  // the previous chunk's stores have read the tile
+            for (int e0 = threadIdx.x; e0 < cnt; e0 += 256 * 8) {
+                uint32_t v[8];
+                int x[8], ch[8];
+#pragma unroll
+                for (int k = 0; k < 8; ++k) {
+                    const int e = e0 + 256 * k;
+                    x[k] = e / ccn;
+                    ch[k] = e - x[k] * ccn;
+                    v[k] = e < cnt ? __float_as_uint(srow[x[k] * c + c0 + ch[k]]) : 0u;
+                }
+#pragma unroll
+                for (int k = 0; k < 8; ++k) {
+                    if (e0 + 256 * k >= cnt) break;
+                    st.add(v[k]);
+                    tile[ch[k] * ws + x[k]] = amsim_decode(v[k], m, shift);
+                }
+            }
+            __syncthreads();
+            for (int ch = wave; ch < ccn; ch += 4) {
+                uint32_t *drow = dimg + int64_t(c0 + ch) * wp;
+                for (int xo = lane; xo < wp; xo += 64) {
+                    const int ix = xo - left;
+                    drow[xo] = unsigned(ix) < unsigned(w) ? tile[ch * ws + ix] : 0u;
+                }
+            }
+        }
     }
+    store_stats(st, stats, blockIdx.x);
 }
 
 // Tiled transpose-decode for the GEMM first operand: src is `rows x cols` with strides
 // (sr, sc); dst[c * dld + r] = decode(src(r, c)), rows padded to dld with decoded +0.
+// The grid strides over 64 x 64 tiles in both directions.
 __global__ __launch_bounds__(256) void decode_t_kernel(const float *__restrict__ src, int64_t sr, int64_t sc, int rows,
-                                                       int cols, uint32_t *__restrict__ dst, int dld, int m, int shift)
+                                                       int cols, uint32_t *__restrict__ dst, int dld, int m, int shift,
+                                                       uint32_t *__restrict__ stats)
 {
     __shared__ uint32_t tile[64][65];
-    const int r0 = blockIdx.x * 64;
     const int tx = threadIdx.x & 63, ty = threadIdx.x >> 6;
-    for (int c0 = blockIdx.y * 64; c0 < cols; c0 += gridDim.y * 64) {
-        for (int i = ty; i < 64; i += 4) {
-            const int r = r0 + i, c = c0 + tx;
-            uint32_t w = 0u;
-            if (r < rows && c < cols) w = amsim_decode(__float_as_uint(src[int64_t(r) * sr + int64_t(c) * sc]), m, shift);
-            tile[i][tx] = w;
+    ExpStats st;
+    for (int r0 = blockIdx.x * 64; r0 < dld; r0 += gridDim.x * 64) {
+        for (int c0 = blockIdx.y * 64; c0 < cols; c0 += gridDim.y * 64) {
+            uint32_t u[16];
+#pragma unroll
+            for (int i = 0; i < 16; ++i) {
+                const int r = r0 + ty + 4 * i, c = c0 + tx;
+                u[i] = (r < rows && c < cols) ? __float_as_uint(src[int64_t(r) * sr + int64_t(c) * sc]) : 0u;
+            }
+#pragma unroll
+            for (int i = 0; i < 16; ++i) {
+                st.add(u[i]);
+                tile[ty + 4 * i][tx] = amsim_decode(u[i], m, shift);
+            }
+            __syncthreads();
+            for (int i = ty; i < 64; i += 4) {
+                const int c = c0 + i, r = r0 + tx;
+                if (c < cols && r < dld) dst[int64_t(c) * dld + r] = tile[tx][i];
+            }
+            __syncthreads();
         }
-        __syncthreads();
-        for (int i = ty; i < 64; i += 4) {
-            const int c = c0 + i, r = r0 + tx;
-            if (c < cols && r < dld) dst[int64_t(c) * dld + r] = tile[tx][i];
-        }
-        __syncthreads();
     }
+    store_stats(st, stats, blockIdx.y * gridDim.x + blockIdx.x);
 }
 
 // C[r][c] = sum over z of part[z][r][c], z in order (deterministic).
@@ -301,8 +457,6 @@ __global__ __launch_bounds__(kThreads) void gemm_kernel(const uint32_t *__restri
 
 constexpr int kTabRowEntries = 128;  // rows padded to 2^7 entries
 
-typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
-
 template <int EB>
 __device__ __forceinline__ float tab_value(const unsigned char *p)
 {
@@ -315,32 +469,124 @@ __device__ __forceinline__ float tab_value(const unsigned char *p)
 }
 
 // Transposed, width-reduced table: dst row kb (kTabRowEntries * EB bytes) holds entry
-// (ka, kb) at byte ka * EB.  One workgroup; *eb_out receives the entry width chosen.
+// (ka, kb) at byte ka * EB.  With 1-byte entries it also writes dot_rows, the same bytes in the
+// order the bf16 path stages them: byte 4 * (ka % 32) + ka / 32 of row kb.  Then it reduces
+// the decode passes' exponent statistics (n_a words for the first operand, n_b for the second)
+// and decides whether the bf16 path is exact for this call.  One workgroup; flags[0] receives
+// the entry width, flags[1] 1 when the bf16 path may run.
 __global__ __launch_bounds__(1024) void prep_rows_kernel(const uint32_t *__restrict__ lut, int m,
-                                                         unsigned char *__restrict__ dst, int *__restrict__ eb_out)
+                                                         unsigned char *__restrict__ dst,
+                                                         unsigned char *__restrict__ dot_rows,
+                                                         const uint32_t *__restrict__ stats_a, int n_a,
+                                                         const uint32_t *__restrict__ stats_b, int n_b,
+                                                         int *__restrict__ flags)
 {
-    __shared__ uint32_t low_bits;
-    if (threadIdx.x == 0) low_bits = 0u;
-    __syncthreads();
+    __shared__ uint32_t slut[kTabRowEntries * kTabRowEntries];  // the table, canonical order
+    __shared__ uint32_t w_low[16], w_alo[16], w_ahs[16], w_blo[16], w_bhs[16];
+    __shared__ int s_eb;
     const int n = 1 << m, total = n * n;
-    uint32_t acc = 0u;
-    for (int i = threadIdx.x; i < total; i += blockDim.x) acc |= lut[i] & 0xFFFFu;
-    atomicOr(&low_bits, acc);
-    __syncthreads();
-    const uint32_t lb = low_bits;
-    const int eb = lb == 0u ? 1 : ((lb & 0xFFu) == 0u ? 2 : 4);
-    for (int i = threadIdx.x; i < total; i += blockDim.x) {
-        const int ka = i / n, kb = i % n;
-        const uint32_t e = lut[i] & 0x00FFFFFFu;
-        unsigned char *row = dst + size_t(kb) * kTabRowEntries * eb;
-        if (eb == 1)
-            row[ka] = static_cast<unsigned char>(e >> 16);
-        else if (eb == 2)
-            reinterpret_cast<uint16_t *>(row)[ka] = static_cast<uint16_t>(e >> 8);
-        else
-            reinterpret_cast<uint32_t *>(row)[ka] = e + 0x3F800000u;
+    const int wave = int(threadIdx.x) >> 6;
+    uint32_t v[16];
+#pragma unroll
+    for (int i = 0; i < 16; ++i) {
+        const int k = int(threadIdx.x) + 1024 * i;
+        v[i] = k < total ? lut[k] : 0u;
     }
-    if (threadIdx.x == 0) *eb_out = eb;
+    uint32_t sa[8], sb[8];
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+        const int k = int(threadIdx.x) + 1024 * i;
+        sa[i] = k < n_a ? stats_a[k] : 255u;
+        sb[i] = k < n_b ? stats_b[k] : 255u;
+    }
+    uint32_t low = 0u, alo = 255u, ahs = 0u, blo = 255u, bhs = 0u;
+#pragma unroll
+    for (int i = 0; i < 16; ++i) {
+        const int k = int(threadIdx.x) + 1024 * i;
+        if (k < total) slut[k] = v[i];
+        low |= v[i] & 0xFFFFu;
+    }
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+        // (special << 8 | largest exponent), as recorded by the decode passes
+        alo = min(alo, sa[i] & 0xFFu);
+        ahs = max(ahs, (sa[i] >> 8) & 0x1FFu);
+        blo = min(blo, sb[i] & 0xFFu);
+        bhs = max(bhs, (sb[i] >> 8) & 0x1FFu);
+    }
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) low |= uint32_t(__shfl_xor(int(low), o));
+    alo = wave_min(alo);
+    ahs = wave_max(ahs);
+    blo = wave_min(blo);
+    bhs = wave_max(bhs);
+    if ((threadIdx.x & 63) == 0) {
+        w_low[wave] = low;
+        w_alo[wave] = alo;
+        w_ahs[wave] = ahs;
+        w_blo[wave] = blo;
+        w_bhs[wave] = bhs;
+    }
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        uint32_t l = 0u, a_lo = 255u, a_hs = 0u, b_lo = 255u, b_hs = 0u;
+        for (int i = 0; i < int(blockDim.x) / 64; ++i) {
+            l |= w_low[i];
+            a_lo = min(a_lo, w_alo[i]);
+            a_hs = max(a_hs, w_ahs[i]);
+            b_lo = min(b_lo, w_blo[i]);
+            b_hs = max(b_hs, w_bhs[i]);
+        }
+        const int eb = l == 0u ? 1 : ((l & 0xFFu) == 0u ? 2 : 4);
+        s_eb = eb;
+        // Every product of finite non-zero operands then has exponent field
+        // Ea + Eb - 127 + carry in [1, 254], and v * pb (Eb + carry) stays below 255.
+        const uint32_t a_hi = a_hs & 0xFFu, b_hi = b_hs & 0xFFu;
+        const bool special = ((a_hs | b_hs) >> 8) != 0u;
+        const bool window = stats_a != nullptr && !special && a_lo + b_lo >= 128u && a_hi + b_hi <= 380u &&
+                            b_hi <= 253u;
+        flags[0] = eb;
+        flags[1] = (eb == 1 && window) ? 1 : 0;
+    }
+    __syncthreads();
+    const int eb = s_eb;
+    // Rows: thread -> (kb = consecutive threads, group of 4 entries), so that the LDS reads of a
+    // wave are consecutive words; each thread stores 4 entries.
+    for (int i = threadIdx.x; i < n * ((n + 3) / 4); i += blockDim.x) {
+        const int kb = i % n, k4 = (i / n) * 4;
+        if (eb == 1) {
+            uint32_t word = 0u;
+#pragma unroll
+            for (int j = 0; j < 4; ++j)
+                if (k4 + j < n) word |= ((slut[(k4 + j) * n + kb] >> 16) & 0xFFu) << (8 * j);
+            if (k4 + 4 <= n)
+                *reinterpret_cast<uint32_t *>(dst + size_t(kb) * kTabRowEntries + k4) = word;
+            else
+                for (int j = 0; k4 + j < n; ++j) dst[size_t(kb) * kTabRowEntries + k4 + j] = (word >> (8 * j)) & 0xFFu;
+        } else {
+            for (int j = 0; j < 4 && k4 + j < n; ++j) {
+                const uint32_t e = slut[(k4 + j) * n + kb] & 0x00FFFFFFu;
+                unsigned char *row = dst + size_t(kb) * kTabRowEntries * eb;
+                if (eb == 2)
+                    reinterpret_cast<uint16_t *>(row)[k4 + j] = static_cast<uint16_t>(e >> 8);
+                else
+                    reinterpret_cast<uint32_t *>(row)[k4 + j] = e + 0x3F800000u;
+            }
+        }
+    }
+    // bf16-path rows: word g of row kb holds the bytes of entries g, g + 32, g + 64, g + 96.
+    if (eb == 1) {
+        for (int i = threadIdx.x; i < n * 32; i += blockDim.x) {
+            const int kb = i % n, g = i / n;
+            uint32_t word = 0u;
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                const int ka = g + 32 * j;
+                if (ka < n) word |= ((slut[ka * n + kb] >> 16) & 0xFFu) << (8 * j);
+            }
+            *reinterpret_cast<uint32_t *>(dot_rows + size_t(kb) * kTabRowEntries + 4 * g) = word;
+        }
+    }
 }
 
 struct ConvShape {
@@ -371,8 +617,9 @@ struct TabArgs {
     int Np;
     float *out;          // result, or split partial sums [z][R][N]
     int64_t ldc;         // GEMM result leading dimension
-    const unsigned char *rows;
-    const int *eb;
+    const unsigned char *rows;      // transposed table rows (exact path)
+    const unsigned char *dot_rows;  // the same 1-byte rows in bf16-path staging order
+    const int *eb;                  // [0] entry width, [1] 1 when the bf16 path may run
     int R, N;            // result rows and columns
     int splits;          // reduction splits: blockIdx.z = (phase *) splits + split
     int chunks_per_split;  // reduction chunks (8 steps each) per split
@@ -466,8 +713,9 @@ __device__ __forceinline__ int tab_count(const TabArgs &a)
     else return a.s.ow;
 }
 
+// The tap's fields are wave-uniform (they depend on the workgroup and the tap only).
 template <int OP>
-__device__ __forceinline__ TabTap tab_tap(const TabArgs &a, int tap)
+__device__ __forceinline__ TabTap tab_tap_raw(const TabArgs &a, int tap)
 {
     const ConvShape &s = a.s;
     TabTap t;
@@ -500,6 +748,25 @@ __device__ __forceinline__ TabTap tab_tap(const TabArgs &a, int tap)
         t.bbase = tap * s.ow;
     }
     return t;
+}
+
+template <int OP>
+__device__ __forceinline__ TabTap tab_tap(const TabArgs &a, int tap)
+{
+    const TabTap t = tab_tap_raw<OP>(a, tap);
+    return TabTap{__builtin_amdgcn_readfirstlane(t.ubase), __builtin_amdgcn_readfirstlane(t.ustride),
+                  __builtin_amdgcn_readfirstlane(t.bbase), __builtin_amdgcn_readfirstlane(t.count)};
+}
+
+// The slab cursor is wave-uniform; saying so at the loop head keeps it, and the buffer loads'
+// step offsets derived from it, in scalar registers (the compiler's uniformity analysis does not
+// prove it through the backward-data phase math and would loop each load over the lanes).
+__device__ __forceinline__ void uniform_cursor(TabTap &cur, int &tap, int &c0)
+{
+    cur = TabTap{__builtin_amdgcn_readfirstlane(cur.ubase), __builtin_amdgcn_readfirstlane(cur.ustride),
+                 __builtin_amdgcn_readfirstlane(cur.bbase), __builtin_amdgcn_readfirstlane(cur.count)};
+    tap = __builtin_amdgcn_readfirstlane(tap);
+    c0 = __builtin_amdgcn_readfirstlane(c0);
 }
 
 // Slab staging: each thread copies CPT 16-byte pieces of the rows selected by the second
@@ -603,12 +870,13 @@ __device__ __forceinline__ void tab_body(const TabArgs &a)
         tab_commit<TNW, EB, CPT>(stage, stage_pb, smem, pbs, 0);
 #pragma unroll
         for (int r = 0; r < TM; ++r)
-            acur[r] = __builtin_amdgcn_raw_buffer_load_b32(ares, aoff[r], uint32_t(cur.ubase + c0 * cur.ustride) * 4u,
-                                                           0);
+            acur[r] = __builtin_amdgcn_raw_buffer_load_b32(
+                ares, aoff[r], __builtin_amdgcn_readfirstlane(uint32_t(cur.ubase + c0 * cur.ustride) * 4u), 0);
     }
     __syncthreads();
     int buf = 0;
     while (have) {
+        uniform_cursor(cur, tap, c0);
         // the slab after this one
         TabTap nxt = cur;
         int ntap = tap, nc0 = c0 + KS;
@@ -628,8 +896,9 @@ __device__ __forceinline__ void tab_body(const TabArgs &a)
             // next step's first-operand words: this slab's next slot or the next slab's first
             uint32_t anext[TM];
             const bool in_slab = slot + 1 < nslots;
-            const uint32_t unext = in_slab ? uint32_t(cur.ubase + (c0 + slot + 1) * cur.ustride) * 4u
-                                           : uint32_t(nxt.ubase + nc0 * nxt.ustride) * 4u;
+            const uint32_t unext = __builtin_amdgcn_readfirstlane(
+                in_slab ? uint32_t(cur.ubase + (c0 + slot + 1) * cur.ustride) * 4u
+                        : uint32_t(nxt.ubase + nc0 * nxt.ustride) * 4u);
             if (in_slab || has_next) {
 #pragma unroll
                 for (int r = 0; r < TM; ++r) anext[r] = __builtin_amdgcn_raw_buffer_load_b32(ares, aoff[r], unext, 0);
@@ -641,7 +910,7 @@ __device__ __forceinline__ void tab_body(const TabArgs &a)
             float pa[TM];
 #pragma unroll
             for (int r = 0; r < TM; ++r) {
-                vaddr[r] = tb + (acur[r] & kIdxMask) * EB;
+                vaddr[r] = tb + __builtin_amdgcn_ubfe(acur[r], 4, 7) * EB;  // idx = ka << 4
                 pa[r] = head_value(acur[r]);
             }
 #pragma unroll
@@ -680,12 +949,268 @@ __device__ __forceinline__ void tab_body(const TabArgs &a)
     }
 }
 
+// ---------------------------------------------------------- bf16 pair path (1-byte tables)
+// When every table entry fits 8 bits (its low 16 mantissa bits are zero) a table value v is a
+// bfloat16, and so are v * pb (the second operand's sign and exponent added to v's bits) and pa.
+// Products of such operands are exact in fp32, so two reduction steps k, k+1 can go through one
+// v_dot2_f32_bf16:  acc += t(k) * pa(k) + t(k+1) * pa(k+1),  t = v * pb.
+// The slab then holds, per step and first-operand mantissa ka, one 16-byte entry with t for the
+// workgroup's 8 columns (8 bf16); a lane reads it with one ds_read_b128 and pairs the halves of
+// two steps' entries with v_perm.
+// Exactness needs every product of finite non-zero operands to stay normal (exponent field
+// Ea + Eb - 127 + carry in [1, 254]) and v * pb not to overflow; the decode passes record the
+// operands' exponent range and the kernel takes this path only when that holds (else the exact
+// path).  Inside that range each product is the exact Algorithm 2 result; the sum is rounded
+// per pair instead of per step.  A sum that comes out exactly zero gets its sign from a second
+// pass over its products (the hardware returns +0 for zero sums; the sign of a sum of zeros is
+// -0 exactly when every product is -0).
+typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+typedef uint16_t u16x2_t __attribute__((ext_vector_type(2)));
+
+constexpr int kDotCols = 8;                          // columns per entry
+constexpr int kDotStepBytes = kTabRowEntries * 16;   // 128 entries x 16 bytes
+constexpr int kDotSlab = 8 * kDotStepBytes;          // 8 steps per slab: 16 KiB
+
+__device__ __forceinline__ float dot2_bf16(uint32_t x, uint32_t y, float c)
+{
+    return __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2_t, x), __builtin_bit_cast(bf16x2_t, y), c,
+                                           false);
+}
+
+__device__ __forceinline__ uint32_t add_u16x2(uint32_t x, uint32_t y)
+{
+    return __builtin_bit_cast(uint32_t, __builtin_bit_cast(u16x2_t, x) + __builtin_bit_cast(u16x2_t, y));
+}
+
+// Staging of one slab: thread -> step slot (tid / 32) and entry group g (tid % 32), which builds
+// the entries ka = g, g + 32, g + 64, g + 96.  Fetch: the slot's 8 second-operand words and, per
+// column, the 4 bytes of its table row that hold those entries.
+__device__ __forceinline__ void dot_fetch(u32x4 (&bw)[2], uint32_t (&rw)[kDotCols], const TabTap &tp, int c0,
+                                          const uint32_t *__restrict__ Bd, int Np, int colw,
+                                          const unsigned char *__restrict__ dot_rows)
+{
+    const int slot = threadIdx.x >> 5, g = threadIdx.x & 31;
+    const int j = c0 + slot;
+    if (j < tp.count) {
+        const u32x4 *src = reinterpret_cast<const u32x4 *>(Bd + int64_t(tp.bbase + j) * Np + colw);
+        bw[0] = src[0];
+        bw[1] = src[1];
+    } else {
+        bw[0] = u32x4{0u, 0u, 0u, 0u};  // decoded +0: a row of +0 entries
+        bw[1] = u32x4{0u, 0u, 0u, 0u};
+    }
+#pragma unroll
+    for (int c = 0; c < kDotCols; ++c) {
+        const uint32_t w = bw[c / 4][c % 4];
+        rw[c] = *reinterpret_cast<const uint32_t *>(dot_rows + (w & 0x7Fu) * kTabRowEntries + g * 4);
+    }
+}
+
+// Commit: t = v * pb as bf16 bits = table byte + (pb's bits >> 16), a zero second operand giving
+// a row of signed zeros; entry dword q = (t of column 2q, t of column 2q + 1).
+__device__ __forceinline__ void dot_commit(const u32x4 (&bw)[2], const uint32_t (&rw)[kDotCols], unsigned char *slab)
+{
+    const int slot = threadIdx.x >> 5, g = threadIdx.x & 31;
+    uint32_t w[kDotCols], hb[kDotCols / 2];
+#pragma unroll
+    for (int c = 0; c < kDotCols; ++c) w[c] = (bw[c / 4][c % 4] & 0x7F800000u) ? rw[c] : 0u;
+#pragma unroll
+    for (int q = 0; q < kDotCols / 2; ++q)
+        hb[q] = __builtin_amdgcn_perm(bw[(2 * q + 1) / 4][(2 * q + 1) % 4], bw[(2 * q) / 4][(2 * q) % 4], 0x07060302u);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        u32x4 e;
+#pragma unroll
+        for (int q = 0; q < kDotCols / 2; ++q) {
+            // low half: byte i of the even column's word, high half: byte i of the odd one's
+            const uint32_t d = __builtin_amdgcn_perm(w[2 * q + 1], w[2 * q], 0x0C000C00u | ((4u + i) << 16) | i);
+            e[q] = add_u16x2(d, hb[q]);
+        }
+        *reinterpret_cast<u32x4 *>(slab + slot * kDotStepBytes + (g + 32 * i) * 16) = e;
+    }
+}
+
+// One first-operand word per lane row and step; steps at or past `count` of the tap read as 0.
+template <int TM>
+__device__ __forceinline__ void dot_load_a(uint32_t (&dst)[TM], __amdgpu_buffer_rsrc_t ares, const uint32_t (&aoff)[TM],
+                                           const TabTap &tp, int j)
+{
+    if (j < tp.count) {
+        const uint32_t so = __builtin_amdgcn_readfirstlane(uint32_t(tp.ubase + j * tp.ustride) * 4u);
+#pragma unroll
+        for (int r = 0; r < TM; ++r) dst[r] = __builtin_amdgcn_raw_buffer_load_b32(ares, aoff[r], so, 0);
+    } else {
+#pragma unroll
+        for (int r = 0; r < TM; ++r) dst[r] = 0u;
+    }
+}
+
+// Workgroup: 4 waves along rows (64*TM rows each), all on the same 8 columns.
+template <int OP, int TM>
+__device__ __forceinline__ void tab_body_dot(const TabArgs &a)
+{
+    constexpr int KS = 8;
+    constexpr int TN = kDotCols;
+    extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
+
+    const int R = tab_rows<OP>(a);
+    if (int(blockIdx.x) * 64 * TM * kWaves >= R) return;  // uniform over the workgroup
+    const int lane = threadIdx.x & 63;
+    const int wave = wave_id();
+    const int row0 = blockIdx.x * (64 * TM * kWaves) + wave * (64 * TM) + lane;
+    const int col0 = blockIdx.y * TN;
+    const __amdgpu_buffer_rsrc_t ares =
+        __builtin_amdgcn_make_buffer_rsrc(const_cast<uint32_t *>(a.A), 0, int(a.a_bytes), 0x00020000);
+
+    uint32_t aoff[TM];
+    int64_t obase[TM];
+#pragma unroll
+    for (int r = 0; r < TM; ++r) {
+        const int row = row0 + 64 * r;
+        int ab = 0;
+        int64_t ob = 0;
+        if (row < R) tab_row<OP>(a, row, ab, ob);
+        aoff[r] = uint32_t(ab) * 4u;
+        obase[r] = ob;
+    }
+    const int count = tab_count<OP>(a);
+    const int cpt = (count + 7) / 8;
+    const int q_total = tab_taps<OP>(a) * cpt;
+    const int q0 = tab_split(a) * a.chunks_per_split;
+    const int p_end = min(q_total, q0 + a.chunks_per_split) * 8;
+
+    u32x4 sbw[2];
+    uint32_t srw[kDotCols];
+    float acc[TM][TN];
+    init_acc(acc);
+    uint32_t a0[TM], a1[TM];  // first-operand words of the current step pair
+    TabTap cur{0, 0, 0, 0};
+    int tap = q0 / max(cpt, 1);
+    int c0 = (q0 - tap * cpt) * 8;
+    bool have = q0 * 8 < p_end;
+    if (have) {
+        cur = tab_tap<OP>(a, tap);
+        dot_fetch(sbw, srw, cur, c0, a.Bd, a.Np, col0, a.dot_rows);
+        dot_commit(sbw, srw, smem);
+        dot_load_a(a0, ares, aoff, cur, c0);
+        dot_load_a(a1, ares, aoff, cur, c0 + 1);
+    }
+    __syncthreads();
+    int buf = 0;
+    while (have) {
+        uniform_cursor(cur, tap, c0);
+        TabTap nxt = cur;
+        int ntap = tap, nc0 = c0 + KS;
+        if (nc0 >= count) {
+            ntap = tap + 1;
+            nc0 = 0;
+        }
+        const bool has_next = ntap * cpt * 8 + nc0 < p_end;
+        if (has_next && ntap != tap) nxt = tab_tap<OP>(a, ntap);
+        if (has_next) dot_fetch(sbw, srw, nxt, nc0, a.Bd, a.Np, col0, a.dot_rows);
+        const unsigned char *tb = smem + buf * kDotSlab;
+        const int nslots = min(KS, cur.count - c0);
+#pragma unroll
+        for (int kp = 0; kp < KS / 2; ++kp) {
+            if (2 * kp >= nslots) break;
+            // the next pair's words: this slab's next pair or the next slab's first
+            uint32_t n0[TM], n1[TM];
+            if (2 * kp + 2 < nslots) {
+                dot_load_a(n0, ares, aoff, cur, c0 + 2 * kp + 2);
+                dot_load_a(n1, ares, aoff, cur, c0 + 2 * kp + 3);
+            } else if (has_next) {
+                dot_load_a(n0, ares, aoff, nxt, nc0);
+                dot_load_a(n1, ares, aoff, nxt, nc0 + 1);
+            } else {
+#pragma unroll
+                for (int r = 0; r < TM; ++r) n0[r] = n1[r] = 0u;
+            }
+#pragma unroll
+            for (int r = 0; r < TM; ++r) {
+                const u32x4 X = *reinterpret_cast<const u32x4 *>(tb + (a0[r] & 0x7F0u) + (2 * kp) * kDotStepBytes);
+                const u32x4 Y = *reinterpret_cast<const u32x4 *>(tb + (a1[r] & 0x7F0u) + (2 * kp + 1) * kDotStepBytes);
+                const uint32_t pa = __builtin_amdgcn_perm(a1[r], a0[r], 0x07060302u);  // (pa(k), pa(k+1))
+#pragma unroll
+                for (int q = 0; q < TN / 2; ++q) {
+                    acc[r][2 * q] = dot2_bf16(__builtin_amdgcn_perm(Y[q], X[q], 0x05040100u), pa, acc[r][2 * q]);
+                    acc[r][2 * q + 1] =
+                        dot2_bf16(__builtin_amdgcn_perm(Y[q], X[q], 0x07060302u), pa, acc[r][2 * q + 1]);
+                }
+            }
+#pragma unroll
+            for (int r = 0; r < TM; ++r) {
+                a0[r] = n0[r];
+                a1[r] = n1[r];
+            }
+        }
+        if (has_next) dot_commit(sbw, srw, smem + (buf ^ 1) * kDotSlab);
+        __syncthreads();
+        cur = nxt;
+        tap = ntap;
+        c0 = nc0;
+        buf ^= 1;
+        have = has_next;
+    }
+
+    // Signs of zero sums: -0 when every product of the split's range is -0, else +0.
+    uint32_t zero = 0u;
+#pragma unroll
+    for (int r = 0; r < TM; ++r)
+#pragma unroll
+        for (int t = 0; t < TN; ++t)
+            if (row0 + 64 * r < R && col0 + t < a.N && acc[r][t] == 0.0f) zero |= 1u << (r * TN + t);
+    if (__builtin_amdgcn_ballot_w64(zero != 0u) != 0u) {
+        uint32_t other = 0u;  // a product that is not -0 was seen
+        for (int tp_i = q0 / max(cpt, 1); tp_i * cpt * 8 < p_end; ++tp_i) {
+            const int pbase = tp_i * cpt * 8;
+            const TabTap tp = tab_tap<OP>(a, tp_i);
+            const int j1 = min(tp.count, p_end - pbase);
+            for (int j = max(q0 * 8 - pbase, 0); j < j1; ++j) {
+                uint32_t aw[TM];
+                dot_load_a(aw, ares, aoff, tp, j);
+                const uint32_t *brow = a.Bd + int64_t(tp.bbase + j) * a.Np + col0;
+#pragma unroll
+                for (int t = 0; t < TN; ++t) {
+                    const float pb = head_value(brow[t]);
+#pragma unroll
+                    for (int r = 0; r < TM; ++r)
+                        if (__float_as_uint(head_value(aw[r]) * pb) != 0x80000000u) other |= 1u << (r * TN + t);
+                }
+            }
+        }
+#pragma unroll
+        for (int r = 0; r < TM; ++r)
+#pragma unroll
+            for (int t = 0; t < TN; ++t)
+                if ((zero & ~other) & (1u << (r * TN + t))) acc[r][t] = -0.0f;
+    }
+
+    float *out = a.out + int64_t(tab_split(a)) * a.out_elems;
+#pragma unroll
+    for (int r = 0; r < TM; ++r) {
+        const int row = row0 + 64 * r;
+        if (row >= R) continue;
+        float *dst = out + obase[r];
+#pragma unroll
+        for (int t = 0; t < TN; ++t) {
+            const int col = col0 + t;
+            if (col < a.N) dst[col] = acc[r][t];
+        }
+    }
+}
+
 // Four waves per SIMD: the register budget (<= 128 VGPRs) the tiles are sized for.  Without the
 // hint the scheduler minimises registers and serialises the LDS gathers.
 template <int OP, int TM, int TN, int WR>
 __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(4, 4))) void tab_kernel(TabArgs a)
 {
-    const int eb = __builtin_amdgcn_readfirstlane(*a.eb);
+    const int eb = __builtin_amdgcn_readfirstlane(a.eb[0]);
+    if constexpr (TN == kDotCols && WR == kWaves) {
+        if (__builtin_amdgcn_readfirstlane(a.eb[1]) != 0) {
+            tab_body_dot<OP, TM>(a);
+            return;
+        }
+    }
     if (eb == 1)
         tab_body<OP, TM, TN, WR, 1>(a);
     else if (eb == 2)
@@ -694,11 +1219,14 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(4, 4))
         tab_body<OP, TM, TN, WR, 4>(a);
 }
 
-// Dynamic LDS of a table kernel with TNW workgroup columns: two slabs of 8*TNW*128 bytes plus
-// the second-operand heads.
-constexpr size_t tab_lds_bytes(int tnw)
+// Dynamic LDS of a table kernel with TN columns per wave and WR waves along rows: two slabs of
+// 8*TNW*128 bytes plus the second-operand heads, or two bf16-path slabs where that path exists.
+constexpr size_t tab_lds_bytes(int tn, int wr)
 {
-    return size_t(2) * 8 * tnw * kTabRowEntries + size_t(2) * 8 * tnw * 4;
+    const int tnw = tn * (kWaves / wr);
+    const size_t exact = size_t(2) * 8 * tnw * kTabRowEntries + size_t(2) * 8 * tnw * 4;
+    const size_t dot = (tn == kDotCols && wr == kWaves) ? size_t(2) * kDotSlab : 0;
+    return exact > dot ? exact : dot;
 }
 
 // ------------------------------------------------------------------ convolution kernels --
@@ -1001,10 +1529,10 @@ void allow_lds(K kernel, size_t bytes)
 void set_attributes()
 {
 #define X(TM, TN, WR)                                                                      \
-    allow_lds(tab_kernel<OP_GEMM, TM, TN, WR>, tab_lds_bytes(TN * (kWaves / WR)));        \
-    allow_lds(tab_kernel<OP_FWD, TM, TN, WR>, tab_lds_bytes(TN * (kWaves / WR)));         \
-    allow_lds(tab_kernel<OP_BWD_DATA, TM, TN, WR>, tab_lds_bytes(TN * (kWaves / WR)));    \
-    allow_lds(tab_kernel<OP_BWD_WEIGHT, TM, TN, WR>, tab_lds_bytes(TN * (kWaves / WR)));
+    allow_lds(tab_kernel<OP_GEMM, TM, TN, WR>, tab_lds_bytes(TN, WR));        \
+    allow_lds(tab_kernel<OP_FWD, TM, TN, WR>, tab_lds_bytes(TN, WR));         \
+    allow_lds(tab_kernel<OP_BWD_DATA, TM, TN, WR>, tab_lds_bytes(TN, WR));    \
+    allow_lds(tab_kernel<OP_BWD_WEIGHT, TM, TN, WR>, tab_lds_bytes(TN, WR));
     AMSIM_FOR_TAB_TILES(X)
 #undef X
 }
@@ -1023,6 +1551,15 @@ int launch_status()
 inline int grid_for(int64_t total, int block = 256)
 {
     return int(std::max<int64_t>(1, std::min<int64_t>(ceil_div(total, block), 8192)));
+}
+
+// Workgroups of decode_kernel for `words` output words (8 per thread and iteration).
+inline int decode_grid(int64_t words) { return grid_for(ceil_div(words, 8)); }
+
+// decode_kernel's 16-byte load path: unit column stride and 16-byte aligned rows.
+inline int decode_vec(const float *src, int64_t sb, int64_t sr, int64_t sc)
+{
+    return sc == 1 && reinterpret_cast<uintptr_t>(src) % 16 == 0 && sr % 4 == 0 && sb % 4 == 0 ? 1 : 0;
 }
 
 template <typename F>
@@ -1058,7 +1595,7 @@ constexpr size_t kRowsBytes = size_t(kTabRowEntries) * kTabRowEntries * 4;  // w
 struct Plan {
     Tile tile;
     bool lds;
-    size_t off_rows, off_eb, off_a, off_b, off_part, total;
+    size_t off_rows, off_dot_rows, off_eb, off_stats, off_a, off_b, off_part, total;
     int64_t a_ld, b_ld;   // GEMM: padded leading dims of the decoded operands; conv: b_ld only
     int64_t a_elems;      // conv: elements of the decoded first operand
     int splits, per_split;  // global path: steps (GEMM) or output rows (bwd_weight) per split
@@ -1076,11 +1613,17 @@ void plan_tab_split(Plan &p, int64_t q)
 
 bool valid_m(int m_bits) { return m_bits >= 1 && m_bits <= 11; }
 
+// Table path: transposed rows, bf16-path rows, flags, decode statistics (two operands).
+constexpr size_t kDotRowsBytes = size_t(kTabRowEntries) * kTabRowEntries;
+constexpr size_t kStatsBytes = size_t(2) * kStatSlots * 4;
+
 size_t table_area(Plan &p, size_t o)
 {
     p.off_rows = o;
-    p.off_eb = o + align_up(kRowsBytes);
-    return o + align_up(kRowsBytes) + kAlign;
+    p.off_dot_rows = p.off_rows + align_up(kRowsBytes);
+    p.off_eb = p.off_dot_rows + align_up(kDotRowsBytes);
+    p.off_stats = p.off_eb + kAlign;
+    return p.off_stats + align_up(kStatsBytes);
 }
 
 Plan plan_gemm(int64_t m, int64_t n, int64_t k, int m_bits)
@@ -1142,7 +1685,8 @@ int check_conv(const amsim_conv2d *d)
     const int64_t y = int64_t(d->n) * oh * ow * (d->c_out + 16);
     if (xp >= lim || yp >= lim || w >= lim || y >= lim || d->pad_top >= 65536 || d->pad_bottom >= 65536 ||
         d->pad_left >= 65536 || d->pad_right >= 65536 || d->kh >= 65536 || d->kw >= 65536 ||
-        int64_t(d->stride_h) * d->stride_w > 32 || d->c_in > 65535 * 16 || d->c_out > 65535 * 16)
+        int64_t(d->stride_h) * d->stride_w > 32 || d->c_in > 65535 * 16 || d->c_out > 65535 * 16 ||
+        d->w >= kNhcwTile || ow >= kNhcwTile)
         return AMSIM_ERR_UNSUPPORTED;
     return AMSIM_OK;
 }
@@ -1247,16 +1791,30 @@ Plan plan_conv(const amsim_conv2d *d, int pass, int m_bits)
     return p;
 }
 
-// Decoded-index shift of each operand.  Table path: mantissa index itself (the kernels scale
-// it).  Global path: entry index into the canonical table, ka * 2^M + kb.
-inline int shift_first(int m_bits) { return lds_path(m_bits) ? 0 : m_bits; }
+// Decoded-index shift of each operand.  Table path: the first operand's mantissa times 16 (the
+// bf16 path's entry size; the exact path extracts it), the second's as is.  Global path: entry
+// index into the canonical table, ka * 2^M + kb.
+inline int shift_first(int m_bits) { return lds_path(m_bits) ? 4 : m_bits; }
 inline int shift_second(int m_bits) { return lds_path(m_bits) ? 0 : 0; }
 
-// Launches the table preparation for the table path (rows + entry width into the workspace).
-int prep_rows(const uint32_t *lut, int m_bits, char *ws, const Plan &p, hipStream_t st)
+// Decode statistics of the table path: kStatSlots words per operand (null on the global path).
+inline uint32_t *stats_a(char *ws, const Plan &p)
+{
+    return p.lds ? reinterpret_cast<uint32_t *>(ws + p.off_stats) : nullptr;
+}
+inline uint32_t *stats_b(char *ws, const Plan &p)
+{
+    return p.lds ? reinterpret_cast<uint32_t *>(ws + p.off_stats) + kStatSlots : nullptr;
+}
+
+// Launches the table preparation for the table path, after both decode passes (rows, flags and
+// the reduction of the n_a / n_b statistics words into the workspace).
+int prep_rows(const uint32_t *lut, int m_bits, char *ws, const Plan &p, int n_a, int n_b, hipStream_t st)
 {
     hipLaunchKernelGGL(prep_rows_kernel, dim3(1), dim3(1024), 0, st, lut, m_bits,
-                       reinterpret_cast<unsigned char *>(ws + p.off_rows), reinterpret_cast<int *>(ws + p.off_eb));
+                       reinterpret_cast<unsigned char *>(ws + p.off_rows),
+                       reinterpret_cast<unsigned char *>(ws + p.off_dot_rows), stats_a(ws, p), n_a, stats_b(ws, p), n_b,
+                       reinterpret_cast<int *>(ws + p.off_eb));
     return launch_status();
 }
 
@@ -1265,7 +1823,7 @@ int launch_tab(const Plan &p, const TabArgs &a, dim3 grid, hipStream_t st)
 {
     auto run = [&](auto tm, auto tn, auto wr) {
         constexpr int TM = decltype(tm)::value, TN = decltype(tn)::value, WR = decltype(wr)::value;
-        hipLaunchKernelGGL((tab_kernel<OP, TM, TN, WR>), grid, dim3(kThreads), tab_lds_bytes(TN * (kWaves / WR)), st,
+        hipLaunchKernelGGL((tab_kernel<OP, TM, TN, WR>), grid, dim3(kThreads), tab_lds_bytes(TN, WR), st,
                            a);
     };
     dispatch_tab_tile(p.tile, run);
@@ -1282,6 +1840,7 @@ TabArgs tab_args(const Plan &p, char *ws, const uint32_t *A, int64_t a_elems, co
     a.Np = int(p.b_ld);
     a.out = out;
     a.rows = reinterpret_cast<const unsigned char *>(ws + p.off_rows);
+    a.dot_rows = reinterpret_cast<const unsigned char *>(ws + p.off_dot_rows);
     a.eb = reinterpret_cast<const int *>(ws + p.off_eb);
     a.R = R;
     a.N = N;
@@ -1404,13 +1963,16 @@ int approx_gemm(int trans_a, int trans_b, int64_t m, int64_t n, int64_t k, const
     // op(A)(i, kk): row stride / column stride in A's storage
     const int64_t a_sr = trans_a ? 1 : lda, a_sc = trans_a ? lda : 1;
     const int64_t b_sr = trans_b ? 1 : ldb, b_sc = trans_b ? ldb : 1;
-    const dim3 grid_dt(unsigned(ceil_div(p.a_ld, 64)), unsigned(std::min<int64_t>(ceil_div(k, 64), 4096)));
-    if (p.lds && prep_rows(lut, m_bits, ws, p, st) != AMSIM_OK) return AMSIM_ERR_HIP;
+    const dim3 grid_dt(unsigned(std::min<int64_t>(ceil_div(p.a_ld, 64), 128)),
+                       unsigned(std::min<int64_t>(ceil_div(k, 64), 64)));  // <= kStatSlots workgroups
+    const int grid_b = decode_grid(k * p.b_ld);
     hipLaunchKernelGGL(decode_t_kernel, grid_dt, dim3(256), 0, st, A, a_sr, a_sc, int(m), int(k), Ad, int(p.a_ld),
-                       m_bits, shift_first(m_bits));
-    hipLaunchKernelGGL(decode_kernel, dim3(grid_for(k * p.b_ld)), dim3(256), 0, st, B, int64_t(0), b_sr, b_sc, 1,
-                       int(k), int(n), Bd, int(p.b_ld), m_bits, shift_second(m_bits));
+                       m_bits, shift_first(m_bits), stats_a(ws, p));
+    hipLaunchKernelGGL(decode_kernel, dim3(grid_b), dim3(256), 0, st, B, int64_t(0), b_sr, b_sc, 1, int(k), int(n), Bd,
+                       int(p.b_ld), m_bits, shift_second(m_bits), stats_b(ws, p), decode_vec(B, 0, b_sr, b_sc));
     if (launch_status() != AMSIM_OK) return AMSIM_ERR_HIP;
+    if (p.lds && prep_rows(lut, m_bits, ws, p, int(grid_dt.x * grid_dt.y), grid_b, st) != AMSIM_OK)
+        return AMSIM_ERR_HIP;
     int rc;
     if (p.lds) {
         TabArgs a = tab_args(p, ws, Ad, k * p.a_ld, Bd, out, int(m), int(n));
@@ -1464,21 +2026,25 @@ static int conv_common(const amsim_conv2d *desc, int pass, const void *in0, cons
     return AMSIM_OK;
 }
 
-// Decoded copy of an NHWC tensor, zero-padded (table path) or as is (global path).
-static void decode_nhwc(const float *src, int n, int h, int w, int c, int top, int left, int hp, int wp, uint32_t *dst,
-                        int m_bits, int shift, hipStream_t st)
+// Decoded copy of an NHWC tensor, zero-padded (table path) or as is (global path).  Returns the
+// number of workgroups (statistics words written when stats is not null).
+static int decode_nhwc(const float *src, int n, int h, int w, int c, int top, int left, int hp, int wp, uint32_t *dst,
+                       int m_bits, int shift, uint32_t *stats, hipStream_t st)
 {
-    const int64_t total = int64_t(n) * hp * wp * c;
-    hipLaunchKernelGGL(decode_pad_kernel, dim3(grid_for(total)), dim3(256), 0, st, src, n, h, w, c, top, left, hp, wp,
-                       dst, m_bits, shift);
+    const int grid = int(std::min<int64_t>(int64_t(n) * hp, kStatSlots));  // one padded image row per workgroup
+    hipLaunchKernelGGL(decode_pad_kernel, dim3(grid), dim3(256), 0, st, src, n, h, w, c, top, left, hp, wp, dst,
+                       m_bits, shift, stats);
+    return grid;
 }
 
-static void decode_nhcw(const float *src, int n, int h, int w, int c, int top, int left, int hp, int wp, uint32_t *dst,
-                        int m_bits, int shift, hipStream_t st)
+static int decode_nhcw(const float *src, int n, int h, int w, int c, int top, int left, int hp, int wp, uint32_t *dst,
+                       int m_bits, int shift, uint32_t *stats, hipStream_t st)
 {
-    const int64_t total = int64_t(n) * hp * wp * c;
-    hipLaunchKernelGGL(decode_pad_nhcw_kernel, dim3(grid_for(total)), dim3(256), 0, st, src, n, h, w, c, top, left, hp,
-                       wp, dst, m_bits, shift);
+    const int cc = std::max(1, std::min(c, kNhcwTile / (w | 1)));  // channels per LDS tile
+    const int grid = int(std::min<int64_t>(int64_t(n) * hp, kStatSlots));  // one padded image row at a time
+    hipLaunchKernelGGL(decode_pad_nhcw_kernel, dim3(grid), dim3(256), 0, st, src, n, h, w, c, top, left, hp, wp, dst,
+                       m_bits, shift, stats, cc);
+    return grid;
 }
 
 int approx_conv2d_fwd(const amsim_conv2d *desc, const float *x, const float *w, float *y, const uint32_t *lut,
@@ -1492,15 +2058,18 @@ int approx_conv2d_fwd(const amsim_conv2d *desc, const float *x, const float *w, 
     char *ws = static_cast<char *>(workspace);
     uint32_t *Xd = reinterpret_cast<uint32_t *>(ws + p.off_a);
     uint32_t *Wd = reinterpret_cast<uint32_t *>(ws + p.off_b);
-    if (p.lds && prep_rows(lut, m_bits, ws, p, st) != AMSIM_OK) return AMSIM_ERR_HIP;
+    int n_a;
     if (p.lds)
-        decode_nhcw(x, s.n, s.h, s.w, s.ci, s.pt, s.pl, p.Hp, p.Wp, Xd, m_bits, shift_first(m_bits), st);
+        n_a = decode_nhcw(x, s.n, s.h, s.w, s.ci, s.pt, s.pl, p.Hp, p.Wp, Xd, m_bits, shift_first(m_bits),
+                          stats_a(ws, p), st);
     else
-        decode_nhwc(x, s.n, s.h, s.w, s.ci, 0, 0, s.h, s.w, Xd, m_bits, shift_first(m_bits), st);
+        n_a = decode_nhwc(x, s.n, s.h, s.w, s.ci, 0, 0, s.h, s.w, Xd, m_bits, shift_first(m_bits), nullptr, st);
     const int kk = s.kh * s.kw * s.ci;
-    hipLaunchKernelGGL(decode_kernel, dim3(grid_for(int64_t(kk) * p.b_ld)), dim3(256), 0, st, w, int64_t(0),
-                       int64_t(s.co), int64_t(1), 1, kk, s.co, Wd, int(p.b_ld), m_bits, shift_second(m_bits));
+    const int n_b = decode_grid(int64_t(kk) * p.b_ld);
+    hipLaunchKernelGGL(decode_kernel, dim3(n_b), dim3(256), 0, st, w, int64_t(0), int64_t(s.co), int64_t(1), 1, kk,
+                       s.co, Wd, int(p.b_ld), m_bits, shift_second(m_bits), stats_b(ws, p), decode_vec(w, 0, s.co, 1));
     if (launch_status() != AMSIM_OK) return AMSIM_ERR_HIP;
+    if (p.lds && prep_rows(lut, m_bits, ws, p, n_a, n_b, st) != AMSIM_OK) return AMSIM_ERR_HIP;
     const Tile t = p.tile;
     const int64_t rows = int64_t(s.n) * s.oh * s.ow;
     if (p.lds) {
@@ -1541,16 +2110,18 @@ int approx_conv2d_bwd_data(const amsim_conv2d *desc, const float *dy, const floa
     char *ws = static_cast<char *>(workspace);
     uint32_t *Dyd = reinterpret_cast<uint32_t *>(ws + p.off_a);
     uint32_t *Wtd = reinterpret_cast<uint32_t *>(ws + p.off_b);
-    if (p.lds && prep_rows(lut, m_bits, ws, p, st) != AMSIM_OK) return AMSIM_ERR_HIP;
+    int n_a;
     if (p.lds)
-        decode_nhcw(dy, s.n, s.oh, s.ow, s.co, p.pad_oh, p.pad_ow, p.OHp, p.OWp, Dyd, m_bits, shift_first(m_bits), st);
+        n_a = decode_nhcw(dy, s.n, s.oh, s.ow, s.co, p.pad_oh, p.pad_ow, p.OHp, p.OWp, Dyd, m_bits, shift_first(m_bits),
+                          stats_a(ws, p), st);
     else
-        decode_nhwc(dy, s.n, s.oh, s.ow, s.co, 0, 0, s.oh, s.ow, Dyd, m_bits, shift_first(m_bits), st);
+        n_a = decode_nhwc(dy, s.n, s.oh, s.ow, s.co, 0, 0, s.oh, s.ow, Dyd, m_bits, shift_first(m_bits), nullptr, st);
     // w[kh][kw][ci][co] -> Wt[kh][kw][co][ci]: batches (kh,kw), rows co, cols ci
-    hipLaunchKernelGGL(decode_kernel, dim3(grid_for(int64_t(s.kh) * s.kw * s.co * p.b_ld)), dim3(256), 0, st, w,
-                       int64_t(s.ci) * s.co, int64_t(1), int64_t(s.co), s.kh * s.kw, s.co, s.ci, Wtd, int(p.b_ld),
-                       m_bits, shift_second(m_bits));
+    const int n_b = decode_grid(int64_t(s.kh) * s.kw * s.co * p.b_ld);
+    hipLaunchKernelGGL(decode_kernel, dim3(n_b), dim3(256), 0, st, w, int64_t(s.ci) * s.co, int64_t(1), int64_t(s.co),
+                       s.kh * s.kw, s.co, s.ci, Wtd, int(p.b_ld), m_bits, shift_second(m_bits), stats_b(ws, p), 0);
     if (launch_status() != AMSIM_OK) return AMSIM_ERR_HIP;
+    if (p.lds && prep_rows(lut, m_bits, ws, p, n_a, n_b, st) != AMSIM_OK) return AMSIM_ERR_HIP;
     const Tile t = p.tile;
     const int64_t rows = bwd_data_rows(s);
     if (p.lds) {
@@ -1592,15 +2163,19 @@ int approx_conv2d_bwd_weight(const amsim_conv2d *desc, const float *x, const flo
     char *ws = static_cast<char *>(workspace);
     uint32_t *Xd = reinterpret_cast<uint32_t *>(ws + p.off_a);
     uint32_t *Dyd = reinterpret_cast<uint32_t *>(ws + p.off_b);
-    if (p.lds && prep_rows(lut, m_bits, ws, p, st) != AMSIM_OK) return AMSIM_ERR_HIP;
+    int n_a;
     if (p.lds)
-        decode_nhwc(x, s.n, s.h, s.w, s.ci, s.pt, s.pl, p.Hp, p.Wp, Xd, m_bits, shift_first(m_bits), st);
+        n_a = decode_nhwc(x, s.n, s.h, s.w, s.ci, s.pt, s.pl, p.Hp, p.Wp, Xd, m_bits, shift_first(m_bits),
+                          stats_a(ws, p), st);
     else
-        decode_nhwc(x, s.n, s.h, s.w, s.ci, 0, 0, s.h, s.w, Xd, m_bits, shift_first(m_bits), st);
+        n_a = decode_nhwc(x, s.n, s.h, s.w, s.ci, 0, 0, s.h, s.w, Xd, m_bits, shift_first(m_bits), nullptr, st);
     const int64_t npo = int64_t(s.n) * s.oh * s.ow;
-    hipLaunchKernelGGL(decode_kernel, dim3(grid_for(npo * p.b_ld)), dim3(256), 0, st, dy, int64_t(0), int64_t(s.co),
-                       int64_t(1), 1, int(npo), s.co, Dyd, int(p.b_ld), m_bits, shift_second(m_bits));
+    const int n_b = decode_grid(npo * p.b_ld);
+    hipLaunchKernelGGL(decode_kernel, dim3(n_b), dim3(256), 0, st, dy, int64_t(0), int64_t(s.co), int64_t(1), 1,
+                       int(npo), s.co, Dyd, int(p.b_ld), m_bits, shift_second(m_bits), stats_b(ws, p),
+                       decode_vec(dy, 0, s.co, 1));
     if (launch_status() != AMSIM_OK) return AMSIM_ERR_HIP;
+    if (p.lds && prep_rows(lut, m_bits, ws, p, n_a, n_b, st) != AMSIM_OK) return AMSIM_ERR_HIP;
     const Tile t = p.tile;
     const int R = s.kh * s.kw * s.ci;
     float *out = p.splits > 1 ? reinterpret_cast<float *>(ws + p.off_part) : dw;

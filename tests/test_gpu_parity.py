@@ -90,6 +90,55 @@ def test_gemm_k1_special_values_bit_exact(B):
         assert_bits_equal(C, want, "gemm K=1 specials M=%d" % m)
 
 
+def _window_vector(m, exps, rng):
+    """Every M-bit mantissa field at each exponent and sign, plus +-0 and two denormals (read as
+    zeros): finite non-zero values whose exponents keep every product in the normal range, the
+    operands the table kernels' bf16 pair path takes."""
+    k = np.arange(1 << m, dtype=np.uint32)
+    parts = []
+    for e in exps:
+        for s in (0, 1):
+            low = rng.integers(0, 1 << (23 - m), k.size, dtype=np.uint32)
+            parts.append((np.uint32(s) << 31) | (np.uint32(e) << 23) | (k << (23 - m)) | low)
+    parts.append(np.array([0x00000000, 0x80000000, 0x00000001, 0x80400000], np.uint32))
+    return np.concatenate(parts).view(np.float32)
+
+
+@pytest.mark.parametrize("m", [3, 7])
+def test_gemm_k1_window_products_bit_exact(B, m):
+    """K = 1 on operands inside the exponent window (Mitchell tables at M <= 7 take the bf16
+    pair path there): every product bit for bit, signed zeros included."""
+    rng = np.random.default_rng(70 + m)
+    a = _window_vector(m, [127, 100, 150], rng).reshape(-1, 1)
+    b = _window_vector(m, [127, 110, 140], rng).reshape(1, -1)
+    C = host(B.approx_gemm(cuda(a), cuda(b), dev_lut(B, "mitchell", m), m))
+    want = oracle.mul(oracle.MITCHELL, m, np.repeat(a[:, 0], b.shape[1]), np.tile(b[0], a.shape[0]))
+    assert_bits_equal(C, want, "gemm K=1 window M=%d" % m)
+
+
+@pytest.mark.parametrize("k", [2, 3, 41, 200])
+def test_gemm_zero_sums_keep_their_sign(B, k):
+    """Sums of signed zeros: -0 exactly when every product is -0 (the sum starts at -0.0), +0
+    otherwise; the bf16 pair path rebuilds the sign of such sums in a second pass."""
+    rng = np.random.default_rng(k)
+    m = 7
+    A = W.normal((70, k), 1.0, 80 + k)
+    Bm = W.normal((k, 24), 1.0, 90 + k)
+    A[:10] = 0.0                     # rows of +0
+    A[10:14] = -0.0                  # rows of -0
+    A[14, ::2] = 0.0                 # mixed row: zeros and values
+    Bm[:, :6] = -np.abs(Bm[:, :6])   # columns of negative values
+    Bm[:, 6:9] = np.abs(Bm[:, 6:9])  # columns of positive values
+    Bm[:, 9] = -0.0
+    Bm[rng.integers(0, k), 10] = 0.0
+    C = host(B.approx_gemm(cuda(A), cuda(Bm), dev_lut(B, "mitchell", m), m))
+    ref, S = oracle.gemm(oracle.MITCHELL, m, A, Bm)
+    zero = ref == 0.0
+    assert zero.sum() >= 14 * 24
+    assert_bits_equal(C[zero], ref[zero].astype(np.float32), "zero sums K=%d" % k)
+    assert_within_tolerance(C, ref, S, "gemm zero rows K=%d" % k)
+
+
 def test_conv_single_product_shapes_bit_exact(B):
     """1x1 conv with one input channel (fwd), one output position (bwd_weight) and one output
     channel with a 1x1 kernel (bwd_data): every output is a single product."""
@@ -191,6 +240,8 @@ CONV_CASES = [
     W.conv_desc(2, 5, 4, 2, 3, 4, 4, 2, pads=(3, 3, 3, 3)),
     W.conv_desc(2, 5, 5, 300, 20, 3, 3, 1, 1),
     W.conv_desc(2, 6, 6, 24, 200, 3, 3, 2, 1),
+    W.conv_desc(1, 3, 70, 130, 9, 3, 3, 1, 1),   # x rows pass through LDS in two channel chunks
+    W.conv_desc(1, 3, 70, 9, 130, 3, 3, 1, 1),   # dy rows (backward data) likewise
 ]
 
 
