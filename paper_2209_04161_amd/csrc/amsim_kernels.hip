@@ -44,13 +44,14 @@ typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
 // ------------------------------------------------------------------ device helpers -------
 
-__device__ __forceinline__ uint32_t amsim_decode(uint32_t u, int m, int shift)
+// zidx: the index field given to zeros and denormals (their mantissa bits never matter: every
+// product with a zero is a signed zero, whatever table entry it reads).
+__device__ __forceinline__ uint32_t amsim_decode(uint32_t u, int m, int shift, uint32_t zidx = 0u)
 {
     const uint32_t e = (u >> 23) & 0xFFu;
+    if (e == 0u) return (u & 0x80000000u) | zidx;                      // +-0 (denormals too)
     uint32_t head;
-    if (e == 0u)
-        head = u & 0x80000000u;                                        // +-0 (denormals too)
-    else if (e == 0xFFu)
+    if (e == 0xFFu)
         head = (u & 0xFF800000u) | ((u & 0x007FFFFFu) ? 0x00400000u : 0u);  // +-Inf / qNaN
     else
         head = u & 0xFF800000u;                                        // +-2^(E-127)
@@ -189,7 +190,8 @@ __device__ __forceinline__ void store_stats(const ExpStats &s, uint32_t *stats, 
 // 16-byte aligned, so a full group is one 16-byte load.
 __global__ __launch_bounds__(256) void decode_kernel(const float *__restrict__ src, int64_t sb, int64_t sr, int64_t sc,
                                                      int batches, int rows, int cols, uint32_t *__restrict__ dst,
-                                                     int dld, int m, int shift, uint32_t *__restrict__ stats, int vec)
+                                                     int dld, int m, int shift, uint32_t zidx,
+                                                     uint32_t *__restrict__ stats, int vec)
 {
     const uint32_t qpr = uint32_t(dld) / 4u;
     const uint32_t total = uint32_t(batches) * uint32_t(rows) * qpr;
@@ -227,7 +229,7 @@ __global__ __launch_bounds__(256) void decode_kernel(const float *__restrict__ s
             for (int e = 0; e < 4; ++e) {
                 // padding columns and +0 operands both decode to 0 and leave the statistics alone
                 st.add(w[h][e]);
-                o[e] = amsim_decode(w[h][e], m, shift);
+                o[e] = amsim_decode(w[h][e], m, shift, zidx);
             }
             *reinterpret_cast<u32x4 *>(dst + int64_t(row[h]) * dld + c[h]) = o;
         }
@@ -240,7 +242,7 @@ __global__ __launch_bounds__(256) void decode_kernel(const float *__restrict__ s
 // the w * c in the middle come from one contiguous source row) per workgroup iteration.
 __global__ __launch_bounds__(256) void decode_pad_kernel(const float *__restrict__ src, int n, int h, int w, int c,
                                                          int top, int left, int hp, int wp,
-                                                         uint32_t *__restrict__ dst, int m, int shift,
+                                                         uint32_t *__restrict__ dst, int m, int shift, uint32_t zidx,
                                                          uint32_t *__restrict__ stats)
 {
     const int len = wp * c, lead = left * c, body = w * c;
@@ -261,7 +263,7 @@ __global__ __launch_bounds__(256) void decode_pad_kernel(const float *__restrict
             for (int e = 0; e < 4; ++e) {
                 if (i0 + e * 256 >= len) break;
                 st.add(v[e]);
-                drow[i0 + e * 256] = amsim_decode(v[e], m, shift);
+                drow[i0 + e * 256] = amsim_decode(v[e], m, shift, zidx);
             }
         }
     }
@@ -277,7 +279,7 @@ constexpr int kNhcwTile = 8192;  // words of the LDS tile: cc * (w | 1) <= kNhcw
 
 __global__ __launch_bounds__(256) void decode_pad_nhcw_kernel(const float *__restrict__ src, int n, int h, int w, int c,
                                                               int top, int left, int hp, int wp,
-                                                              uint32_t *__restrict__ dst, int m, int shift,
+                                                              uint32_t *__restrict__ dst, int m, int shift, uint32_t zidx,
                                                               uint32_t *__restrict__ stats, int cc)
 {
     __shared__ uint32_t tile[kNhcwTile];
@@ -309,7 +311,7 @@ __global__ __launch_bounds__(256) void decode_pad_nhcw_kernel(const float *__res
                 for (int k = 0; k < 8; ++k) {
                     if (e0 + 256 * k >= cnt) break;
                     st.add(v[k]);
-                    tile[ch[k] * ws + x[k]] = amsim_decode(v[k], m, shift);
+                    tile[ch[k] * ws + x[k]] = amsim_decode(v[k], m, shift, zidx);
                 }
             }
             __syncthreads();
@@ -330,6 +332,7 @@ __global__ __launch_bounds__(256) void decode_pad_nhcw_kernel(const float *__res
 // The grid strides over 64 x 64 tiles in both directions.
 __global__ __launch_bounds__(256) void decode_t_kernel(const float *__restrict__ src, int64_t sr, int64_t sc, int rows,
                                                        int cols, uint32_t *__restrict__ dst, int dld, int m, int shift,
+                                                       uint32_t zidx,
                                                        uint32_t *__restrict__ stats)
 {
     __shared__ uint32_t tile[64][65];
@@ -346,7 +349,7 @@ __global__ __launch_bounds__(256) void decode_t_kernel(const float *__restrict__
 #pragma unroll
             for (int i = 0; i < 16; ++i) {
                 st.add(u[i]);
-                tile[ty + 4 * i][tx] = amsim_decode(u[i], m, shift);
+                tile[ty + 4 * i][tx] = amsim_decode(u[i], m, shift, zidx);
             }
             __syncthreads();
             for (int i = ty; i < 64; i += 4) {
@@ -456,6 +459,10 @@ __global__ __launch_bounds__(kThreads) void gemm_kernel(const uint32_t *__restri
 // GEMM kernel, which runs the matching specialisation.
 
 constexpr int kTabRowEntries = 128;  // rows padded to 2^7 entries
+// Table row kZeroRow (after the 2^M rows) holds zeros: the table path decodes second-operand
+// zeros, and names padding steps, with its index, so that a zero's row needs no test.
+constexpr int kZeroRow = kTabRowEntries;
+constexpr uint32_t kZeroRowWord = uint32_t(kZeroRow) << 7;  // decoded +0 of the second operand
 
 template <int EB>
 __device__ __forceinline__ float tab_value(const unsigned char *p)
@@ -574,6 +581,11 @@ __global__ __launch_bounds__(1024) void prep_rows_kernel(const uint32_t *__restr
             }
         }
     }
+    // the zero row
+    for (int i = threadIdx.x; i < kTabRowEntries * eb / 4; i += blockDim.x)
+        reinterpret_cast<uint32_t *>(dst + size_t(kZeroRow) * kTabRowEntries * eb)[i] = 0u;
+    if (eb == 1 && threadIdx.x < kTabRowEntries / 4)
+        reinterpret_cast<uint32_t *>(dot_rows + size_t(kZeroRow) * kTabRowEntries)[threadIdx.x] = 0u;
     // bf16-path rows: word g of row kb holds the bytes of entries g, g + 32, g + 64, g + 96.
     if (eb == 1) {
         for (int i = threadIdx.x; i < n * 32; i += blockDim.x) {
@@ -786,9 +798,9 @@ __device__ __forceinline__ void tab_fetch(u32x4 (&stage)[CPT], float (&stage_pb)
         const int t = (c / PIECES) % TNW;
         const int piece = c % PIECES;
         const int j = c0 + slot;
-        const uint32_t bw = j < tp.count ? Bd[int64_t(tp.bbase + j) * Np + col0 + t] : 0u;
+        const uint32_t bw = j < tp.count ? Bd[int64_t(tp.bbase + j) * Np + col0 + t] : kZeroRowWord;
         stage_pb[i] = head_value(bw);
-        stage[i] = *reinterpret_cast<const u32x4 *>(rows + (bw & kIdxMask) * ROWB + piece * 16);
+        stage[i] = *reinterpret_cast<const u32x4 *>(rows + (bw & kIdxMask) * EB + piece * 16);  // idx = kb * 128
     }
 }
 
@@ -987,7 +999,7 @@ __device__ __forceinline__ uint32_t add_u16x2(uint32_t x, uint32_t y)
 // column, the 4 bytes of its table row that hold those entries.
 __device__ __forceinline__ void dot_fetch(u32x4 (&bw)[2], uint32_t (&rw)[kDotCols], const TabTap &tp, int c0,
                                           const uint32_t *__restrict__ Bd, int Np, int colw,
-                                          const unsigned char *__restrict__ dot_rows)
+                                          __amdgpu_buffer_rsrc_t rres)
 {
     const int slot = threadIdx.x >> 5, g = threadIdx.x & 31;
     const int j = c0 + slot;
@@ -995,25 +1007,24 @@ __device__ __forceinline__ void dot_fetch(u32x4 (&bw)[2], uint32_t (&rw)[kDotCol
         const u32x4 *src = reinterpret_cast<const u32x4 *>(Bd + int64_t(tp.bbase + j) * Np + colw);
         bw[0] = src[0];
         bw[1] = src[1];
-    } else {
-        bw[0] = u32x4{0u, 0u, 0u, 0u};  // decoded +0: a row of +0 entries
-        bw[1] = u32x4{0u, 0u, 0u, 0u};
+    } else {  // a padding step: +0 operands, whose entries are +0
+        bw[0] = u32x4{kZeroRowWord, kZeroRowWord, kZeroRowWord, kZeroRowWord};
+        bw[1] = bw[0];
     }
 #pragma unroll
     for (int c = 0; c < kDotCols; ++c) {
-        const uint32_t w = bw[c / 4][c % 4];
-        rw[c] = *reinterpret_cast<const uint32_t *>(dot_rows + (w & 0x7Fu) * kTabRowEntries + g * 4);
+        const uint32_t w = bw[c / 4][c % 4];  // idx = kb * 128 (kZeroRow for zeros)
+        rw[c] = __builtin_amdgcn_raw_buffer_load_b32(rres, (w & 0x7F80u) | uint32_t(g * 4), 0, 0);
     }
 }
 
-// Commit: t = v * pb as bf16 bits = table byte + (pb's bits >> 16), a zero second operand giving
-// a row of signed zeros; entry dword q = (t of column 2q, t of column 2q + 1).
+// Commit: t = v * pb as bf16 bits = table byte + (pb's bits >> 16); a zero second operand reads
+// the zero row and gets signed zeros.  Entry dword q = (t of column 2q, t of column 2q + 1).
 __device__ __forceinline__ void dot_commit(const u32x4 (&bw)[2], const uint32_t (&rw)[kDotCols], unsigned char *slab)
 {
     const int slot = threadIdx.x >> 5, g = threadIdx.x & 31;
-    uint32_t w[kDotCols], hb[kDotCols / 2];
-#pragma unroll
-    for (int c = 0; c < kDotCols; ++c) w[c] = (bw[c / 4][c % 4] & 0x7F800000u) ? rw[c] : 0u;
+    const uint32_t(&w)[kDotCols] = rw;
+    uint32_t hb[kDotCols / 2];
 #pragma unroll
     for (int q = 0; q < kDotCols / 2; ++q)
         hb[q] = __builtin_amdgcn_perm(bw[(2 * q + 1) / 4][(2 * q + 1) % 4], bw[(2 * q) / 4][(2 * q) % 4], 0x07060302u);
@@ -1030,19 +1041,18 @@ __device__ __forceinline__ void dot_commit(const u32x4 (&bw)[2], const uint32_t 
     }
 }
 
-// One first-operand word per lane row and step; steps at or past `count` of the tap read as 0.
+// One first-operand word per lane row and step.  A step past the tap's end (the odd step of a
+// pair, or a slab's unused slots) reads the tap's last step again: its slot in the slab holds
+// +0 entries (staged from a +0 second operand), so it adds signed zeros only, and the load stays
+// branch-free and in bounds.
 template <int TM>
 __device__ __forceinline__ void dot_load_a(uint32_t (&dst)[TM], __amdgpu_buffer_rsrc_t ares, const uint32_t (&aoff)[TM],
                                            const TabTap &tp, int j)
 {
-    if (j < tp.count) {
-        const uint32_t so = __builtin_amdgcn_readfirstlane(uint32_t(tp.ubase + j * tp.ustride) * 4u);
+    const int jj = min(j, tp.count - 1);
+    const uint32_t so = __builtin_amdgcn_readfirstlane(uint32_t(tp.ubase + jj * tp.ustride) * 4u);
 #pragma unroll
-        for (int r = 0; r < TM; ++r) dst[r] = __builtin_amdgcn_raw_buffer_load_b32(ares, aoff[r], so, 0);
-    } else {
-#pragma unroll
-        for (int r = 0; r < TM; ++r) dst[r] = 0u;
-    }
+    for (int r = 0; r < TM; ++r) dst[r] = __builtin_amdgcn_raw_buffer_load_b32(ares, aoff[r], so, 0);
 }
 
 // Workgroup: 4 waves along rows (64*TM rows each), all on the same 8 columns.
@@ -1061,6 +1071,8 @@ __device__ __forceinline__ void tab_body_dot(const TabArgs &a)
     const int col0 = blockIdx.y * TN;
     const __amdgpu_buffer_rsrc_t ares =
         __builtin_amdgcn_make_buffer_rsrc(const_cast<uint32_t *>(a.A), 0, int(a.a_bytes), 0x00020000);
+    const __amdgpu_buffer_rsrc_t rres = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<unsigned char *>(a.dot_rows), 0, int((kZeroRow + 1) * kTabRowEntries), 0x00020000);
 
     uint32_t aoff[TM];
     int64_t obase[TM];
@@ -1090,7 +1102,7 @@ __device__ __forceinline__ void tab_body_dot(const TabArgs &a)
     bool have = q0 * 8 < p_end;
     if (have) {
         cur = tab_tap<OP>(a, tap);
-        dot_fetch(sbw, srw, cur, c0, a.Bd, a.Np, col0, a.dot_rows);
+        dot_fetch(sbw, srw, cur, c0, a.Bd, a.Np, col0, rres);
         dot_commit(sbw, srw, smem);
         dot_load_a(a0, ares, aoff, cur, c0);
         dot_load_a(a1, ares, aoff, cur, c0 + 1);
@@ -1107,8 +1119,8 @@ __device__ __forceinline__ void tab_body_dot(const TabArgs &a)
         }
         const bool has_next = ntap * cpt * 8 + nc0 < p_end;
         if (has_next && ntap != tap) nxt = tab_tap<OP>(a, ntap);
-        if (has_next) dot_fetch(sbw, srw, nxt, nc0, a.Bd, a.Np, col0, a.dot_rows);
-        const unsigned char *tb = smem + buf * kDotSlab;
+        if (has_next) dot_fetch(sbw, srw, nxt, nc0, a.Bd, a.Np, col0, rres);
+        const uint32_t boff = uint32_t(buf) * kDotSlab;
         const int nslots = min(KS, cur.count - c0);
 #pragma unroll
         for (int kp = 0; kp < KS / 2; ++kp) {
@@ -1123,12 +1135,16 @@ __device__ __forceinline__ void tab_body_dot(const TabArgs &a)
                 dot_load_a(n1, ares, aoff, nxt, nc0 + 1);
             } else {
 #pragma unroll
-                for (int r = 0; r < TM; ++r) n0[r] = n1[r] = 0u;
+                for (int r = 0; r < TM; ++r) n0[r] = n1[r] = 0u;  // past the last slab: unused
             }
 #pragma unroll
             for (int r = 0; r < TM; ++r) {
-                const u32x4 X = *reinterpret_cast<const u32x4 *>(tb + (a0[r] & 0x7F0u) + (2 * kp) * kDotStepBytes);
-                const u32x4 Y = *reinterpret_cast<const u32x4 *>(tb + (a1[r] & 0x7F0u) + (2 * kp + 1) * kDotStepBytes);
+                // entry byte offset = the word's low half (mantissa field * 16; the head is bits
+                // 22..31) plus the slab's
+                const u32x4 X =
+                    *reinterpret_cast<const u32x4 *>(smem + ((a0[r] & 0xFFFFu) + boff) + (2 * kp) * kDotStepBytes);
+                const u32x4 Y = *reinterpret_cast<const u32x4 *>(smem + ((a1[r] & 0xFFFFu) + boff) +
+                                                                 (2 * kp + 1) * kDotStepBytes);
                 const uint32_t pa = __builtin_amdgcn_perm(a1[r], a0[r], 0x07060302u);  // (pa(k), pa(k+1))
 #pragma unroll
                 for (int q = 0; q < TN / 2; ++q) {
@@ -1587,7 +1603,7 @@ void dispatch_tile(const Tile &t, F &&f)
 #undef X
 }
 
-constexpr size_t kRowsBytes = size_t(kTabRowEntries) * kTabRowEntries * 4;  // widest transposed table
+constexpr size_t kRowsBytes = size_t(kZeroRow + 1) * kTabRowEntries * 4;  // widest transposed table
 
 // Workspace layout shared by the size queries and the launches.
 //   table path: [transposed rows][entry-width word][first operand][second operand][partials]
@@ -1614,7 +1630,7 @@ void plan_tab_split(Plan &p, int64_t q)
 bool valid_m(int m_bits) { return m_bits >= 1 && m_bits <= 11; }
 
 // Table path: transposed rows, bf16-path rows, flags, decode statistics (two operands).
-constexpr size_t kDotRowsBytes = size_t(kTabRowEntries) * kTabRowEntries;
+constexpr size_t kDotRowsBytes = size_t(kZeroRow + 1) * kTabRowEntries;
 constexpr size_t kStatsBytes = size_t(2) * kStatSlots * 4;
 
 size_t table_area(Plan &p, size_t o)
@@ -1792,10 +1808,12 @@ Plan plan_conv(const amsim_conv2d *d, int pass, int m_bits)
 }
 
 // Decoded-index shift of each operand.  Table path: the first operand's mantissa times 16 (the
-// bf16 path's entry size; the exact path extracts it), the second's as is.  Global path: entry
+// bf16 path's entry size; the exact path extracts it), the second's times 128 (its row offset in
+// a table of 1-byte entries), zeros of the second operand on the zero row.  Global path: entry
 // index into the canonical table, ka * 2^M + kb.
 inline int shift_first(int m_bits) { return lds_path(m_bits) ? 4 : m_bits; }
-inline int shift_second(int m_bits) { return lds_path(m_bits) ? 0 : 0; }
+inline int shift_second(int m_bits) { return lds_path(m_bits) ? 7 : 0; }
+inline uint32_t zidx_second(const Plan &p) { return p.lds ? kZeroRowWord : 0u; }
 
 // Decode statistics of the table path: kStatSlots words per operand (null on the global path).
 inline uint32_t *stats_a(char *ws, const Plan &p)
@@ -1967,9 +1985,10 @@ int approx_gemm(int trans_a, int trans_b, int64_t m, int64_t n, int64_t k, const
                        unsigned(std::min<int64_t>(ceil_div(k, 64), 64)));  // <= kStatSlots workgroups
     const int grid_b = decode_grid(k * p.b_ld);
     hipLaunchKernelGGL(decode_t_kernel, grid_dt, dim3(256), 0, st, A, a_sr, a_sc, int(m), int(k), Ad, int(p.a_ld),
-                       m_bits, shift_first(m_bits), stats_a(ws, p));
+                       m_bits, shift_first(m_bits), 0u, stats_a(ws, p));
     hipLaunchKernelGGL(decode_kernel, dim3(grid_b), dim3(256), 0, st, B, int64_t(0), b_sr, b_sc, 1, int(k), int(n), Bd,
-                       int(p.b_ld), m_bits, shift_second(m_bits), stats_b(ws, p), decode_vec(B, 0, b_sr, b_sc));
+                       int(p.b_ld), m_bits, shift_second(m_bits), zidx_second(p), stats_b(ws, p),
+                       decode_vec(B, 0, b_sr, b_sc));
     if (launch_status() != AMSIM_OK) return AMSIM_ERR_HIP;
     if (p.lds && prep_rows(lut, m_bits, ws, p, int(grid_dt.x * grid_dt.y), grid_b, st) != AMSIM_OK)
         return AMSIM_ERR_HIP;
@@ -2033,7 +2052,7 @@ static int decode_nhwc(const float *src, int n, int h, int w, int c, int top, in
 {
     const int grid = int(std::min<int64_t>(int64_t(n) * hp, kStatSlots));  // one padded image row per workgroup
     hipLaunchKernelGGL(decode_pad_kernel, dim3(grid), dim3(256), 0, st, src, n, h, w, c, top, left, hp, wp, dst,
-                       m_bits, shift, stats);
+                       m_bits, shift, 0u, stats);
     return grid;
 }
 
@@ -2043,7 +2062,7 @@ static int decode_nhcw(const float *src, int n, int h, int w, int c, int top, in
     const int cc = std::max(1, std::min(c, kNhcwTile / (w | 1)));  // channels per LDS tile
     const int grid = int(std::min<int64_t>(int64_t(n) * hp, kStatSlots));  // one padded image row at a time
     hipLaunchKernelGGL(decode_pad_nhcw_kernel, dim3(grid), dim3(256), 0, st, src, n, h, w, c, top, left, hp, wp, dst,
-                       m_bits, shift, stats, cc);
+                       m_bits, shift, 0u, stats, cc);
     return grid;
 }
 
@@ -2067,7 +2086,8 @@ int approx_conv2d_fwd(const amsim_conv2d *desc, const float *x, const float *w, 
     const int kk = s.kh * s.kw * s.ci;
     const int n_b = decode_grid(int64_t(kk) * p.b_ld);
     hipLaunchKernelGGL(decode_kernel, dim3(n_b), dim3(256), 0, st, w, int64_t(0), int64_t(s.co), int64_t(1), 1, kk,
-                       s.co, Wd, int(p.b_ld), m_bits, shift_second(m_bits), stats_b(ws, p), decode_vec(w, 0, s.co, 1));
+                       s.co, Wd, int(p.b_ld), m_bits, shift_second(m_bits), zidx_second(p), stats_b(ws, p),
+                       decode_vec(w, 0, s.co, 1));
     if (launch_status() != AMSIM_OK) return AMSIM_ERR_HIP;
     if (p.lds && prep_rows(lut, m_bits, ws, p, n_a, n_b, st) != AMSIM_OK) return AMSIM_ERR_HIP;
     const Tile t = p.tile;
@@ -2119,7 +2139,8 @@ int approx_conv2d_bwd_data(const amsim_conv2d *desc, const float *dy, const floa
     // w[kh][kw][ci][co] -> Wt[kh][kw][co][ci]: batches (kh,kw), rows co, cols ci
     const int n_b = decode_grid(int64_t(s.kh) * s.kw * s.co * p.b_ld);
     hipLaunchKernelGGL(decode_kernel, dim3(n_b), dim3(256), 0, st, w, int64_t(s.ci) * s.co, int64_t(1), int64_t(s.co),
-                       s.kh * s.kw, s.co, s.ci, Wtd, int(p.b_ld), m_bits, shift_second(m_bits), stats_b(ws, p), 0);
+                       s.kh * s.kw, s.co, s.ci, Wtd, int(p.b_ld), m_bits, shift_second(m_bits), zidx_second(p),
+                       stats_b(ws, p), 0);
     if (launch_status() != AMSIM_OK) return AMSIM_ERR_HIP;
     if (p.lds && prep_rows(lut, m_bits, ws, p, n_a, n_b, st) != AMSIM_OK) return AMSIM_ERR_HIP;
     const Tile t = p.tile;
@@ -2172,7 +2193,7 @@ int approx_conv2d_bwd_weight(const amsim_conv2d *desc, const float *x, const flo
     const int64_t npo = int64_t(s.n) * s.oh * s.ow;
     const int n_b = decode_grid(npo * p.b_ld);
     hipLaunchKernelGGL(decode_kernel, dim3(n_b), dim3(256), 0, st, dy, int64_t(0), int64_t(s.co), int64_t(1), 1,
-                       int(npo), s.co, Dyd, int(p.b_ld), m_bits, shift_second(m_bits), stats_b(ws, p),
+                       int(npo), s.co, Dyd, int(p.b_ld), m_bits, shift_second(m_bits), zidx_second(p), stats_b(ws, p),
                        decode_vec(dy, 0, s.co, 1));
     if (launch_status() != AMSIM_OK) return AMSIM_ERR_HIP;
     if (p.lds && prep_rows(lut, m_bits, ws, p, n_a, n_b, st) != AMSIM_OK) return AMSIM_ERR_HIP;
