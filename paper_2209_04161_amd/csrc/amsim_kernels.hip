@@ -1168,16 +1168,20 @@ __device__ __forceinline__ void tab_body_dot(const TabArgs &a)
         have = has_next;
     }
 
-    // Signs of zero sums: -0 when every product of the split's range is -0, else +0.
-    uint32_t zero = 0u;
+    // Signs of zero sums: -0 when every product of the split's range is -0, else +0.  The first
+    // product that is not -0 (non-zero, or +0) settles an output as +0, so the pass stops once no
+    // output of the wave is pending -- after one step for a sum that cancelled to zero, after the
+    // whole range only for outputs whose products are all -0.
+    uint32_t pending = 0u;
 #pragma unroll
     for (int r = 0; r < TM; ++r)
 #pragma unroll
         for (int t = 0; t < TN; ++t)
-            if (row0 + 64 * r < R && col0 + t < a.N && acc[r][t] == 0.0f) zero |= 1u << (r * TN + t);
-    if (__builtin_amdgcn_ballot_w64(zero != 0u) != 0u) {
-        uint32_t other = 0u;  // a product that is not -0 was seen
-        for (int tp_i = q0 / max(cpt, 1); tp_i * cpt * 8 < p_end; ++tp_i) {
+            if (row0 + 64 * r < R && col0 + t < a.N && acc[r][t] == 0.0f) pending |= 1u << (r * TN + t);
+    const uint32_t zero = pending;
+    if (__builtin_amdgcn_ballot_w64(pending != 0u) != 0u) {
+        bool open = true;
+        for (int tp_i = q0 / max(cpt, 1); open && tp_i * cpt * 8 < p_end; ++tp_i) {
             const int pbase = tp_i * cpt * 8;
             const TabTap tp = tab_tap<OP>(a, tp_i);
             const int j1 = min(tp.count, p_end - pbase);
@@ -1190,7 +1194,11 @@ __device__ __forceinline__ void tab_body_dot(const TabArgs &a)
                     const float pb = head_value(brow[t]);
 #pragma unroll
                     for (int r = 0; r < TM; ++r)
-                        if (__float_as_uint(head_value(aw[r]) * pb) != 0x80000000u) other |= 1u << (r * TN + t);
+                        if (__float_as_uint(head_value(aw[r]) * pb) != 0x80000000u) pending &= ~(1u << (r * TN + t));
+                }
+                if (__builtin_amdgcn_ballot_w64(pending != 0u) == 0u) {
+                    open = false;
+                    break;
                 }
             }
         }
@@ -1198,7 +1206,7 @@ __device__ __forceinline__ void tab_body_dot(const TabArgs &a)
         for (int r = 0; r < TM; ++r)
 #pragma unroll
             for (int t = 0; t < TN; ++t)
-                if ((zero & ~other) & (1u << (r * TN + t))) acc[r][t] = -0.0f;
+                if (zero & (1u << (r * TN + t))) acc[r][t] = (pending & (1u << (r * TN + t))) ? -0.0f : 0.0f;
     }
 
     float *out = a.out + int64_t(tab_split(a)) * a.out_elems;

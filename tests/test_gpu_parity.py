@@ -131,6 +131,8 @@ def test_gemm_zero_sums_keep_their_sign(B, k):
     Bm[:, 6:9] = np.abs(Bm[:, 6:9])  # columns of positive values
     Bm[:, 9] = -0.0
     Bm[rng.integers(0, k), 10] = 0.0
+    Bm[:, 11] = -np.abs(Bm[:, 11])   # -0 products with the +0 rows up to the last step only
+    Bm[-1, 11] = abs(Bm[-1, 11])
     C = host(B.approx_gemm(cuda(A), cuda(Bm), dev_lut(B, "mitchell", m), m))
     ref, S = oracle.gemm(oracle.MITCHELL, m, A, Bm)
     zero = ref == 0.0
