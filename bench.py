@@ -159,7 +159,7 @@ def main():
     roofline = {"bound": "alu", "achieved": round(achieved, 3), "peak": FP32_VECTOR_PEAK_TFLOPS,
                 "unit": "TFLOP/s", "frac": round(achieved / FP32_VECTOR_PEAK_TFLOPS, 4),
                 "traffic": read_traffic(),
-                "kernel": "tab_kernel<OP_GEMM, 4, 8, 4> (approx_gemm 4096^3, Mitchell M=7, 1-byte LDS tables)"}
+                "kernel": "tab_kernel<OP_GEMM, 4, 8, 8, 8> (approx_gemm 4096^3, Mitchell M=7, bf16 pair path)"}
 
     out = {
         "metric": METRIC,

@@ -784,7 +784,7 @@ __device__ __forceinline__ void uniform_cursor(TabTap &cur, int &tap, int &c0)
 // Slab staging: each thread copies CPT 16-byte pieces of the rows selected by the second
 // operand's mantissas (kb) for slots [0, nslots) of a slab, and that operand's head (pb).
 // TNW = result columns of the workgroup.
-template <int TNW, int EB, int CPT>
+template <int TNW, int EB, int CPT, int NT>
 __device__ __forceinline__ void tab_fetch(u32x4 (&stage)[CPT], float (&stage_pb)[CPT], const TabTap &tp, int c0,
                                           const uint32_t *__restrict__ Bd, int Np, int col0,
                                           const unsigned char *__restrict__ rows)
@@ -793,7 +793,7 @@ __device__ __forceinline__ void tab_fetch(u32x4 (&stage)[CPT], float (&stage_pb)
     constexpr int PIECES = ROWB / 16;
 #pragma unroll
     for (int i = 0; i < CPT; ++i) {
-        const int c = threadIdx.x + i * kThreads;
+        const int c = threadIdx.x + i * NT;
         const int slot = c / (TNW * PIECES);
         const int t = (c / PIECES) % TNW;
         const int piece = c % PIECES;
@@ -804,7 +804,7 @@ __device__ __forceinline__ void tab_fetch(u32x4 (&stage)[CPT], float (&stage_pb)
     }
 }
 
-template <int TNW, int EB, int CPT>
+template <int TNW, int EB, int CPT, int NT>
 __device__ __forceinline__ void tab_commit(const u32x4 (&stage)[CPT], const float (&stage_pb)[CPT],
                                            unsigned char *smem, float *pbs, int buf)
 {
@@ -814,24 +814,25 @@ __device__ __forceinline__ void tab_commit(const u32x4 (&stage)[CPT], const floa
     constexpr int PIECES = ROWB / 16;
 #pragma unroll
     for (int i = 0; i < CPT; ++i) {
-        const int c = threadIdx.x + i * kThreads;
+        const int c = threadIdx.x + i * NT;
         *reinterpret_cast<u32x4 *>(smem + buf * SLAB + c * 16) = stage[i];
         if (c % PIECES == 0) pbs[buf * KS * TNW + c / PIECES] = stage_pb[i];
     }
 }
 
-// Workgroup: 4 waves as a WR x (4/WR) grid -- WR row blocks of 64*TM rows, 4/WR column groups of
-// TN columns.  All waves share the LDS tables of the workgroup's TN * 4/WR columns.
-template <int OP, int TM, int TN, int WR, int EB>
+// Workgroup: NW waves as a WR x (NW/WR) grid -- WR row blocks of 64*TM rows, NW/WR column groups
+// of TN columns.  All waves share the LDS tables of the workgroup's TN * NW/WR columns.
+template <int OP, int TM, int TN, int WR, int EB, int NW>
 __device__ __forceinline__ void tab_body(const TabArgs &a)
 {
-    constexpr int WC = kWaves / WR;
+    constexpr int NT = 64 * NW;
+    constexpr int WC = NW / WR;
     constexpr int TNW = TN * WC;                // result columns of the workgroup
     constexpr int ROWB = kTabRowEntries * EB;
     constexpr int KS = 8 / EB;                  // steps per slab: every slab is 8*TNW*128 bytes
     constexpr int SLAB = KS * TNW * ROWB;
-    constexpr int CPT = SLAB / 16 / kThreads;   // pieces per thread per slab
-    static_assert(CPT * 16 * kThreads == SLAB, "slab must split evenly over the workgroup");
+    constexpr int CPT = SLAB / 16 / NT;         // pieces per thread per slab
+    static_assert(CPT * 16 * NT == SLAB, "slab must split evenly over the workgroup");
     extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
     float *pbs = reinterpret_cast<float *>(smem + 2 * SLAB);  // [2][KS][TNW] second-operand heads
 
@@ -878,8 +879,8 @@ __device__ __forceinline__ void tab_body(const TabArgs &a)
     bool have = q0 * 8 < p_end;
     if (have) {
         cur = tab_tap<OP>(a, tap);
-        tab_fetch<TNW, EB, CPT>(stage, stage_pb, cur, c0, a.Bd, a.Np, colw, a.rows);
-        tab_commit<TNW, EB, CPT>(stage, stage_pb, smem, pbs, 0);
+        tab_fetch<TNW, EB, CPT, NT>(stage, stage_pb, cur, c0, a.Bd, a.Np, colw, a.rows);
+        tab_commit<TNW, EB, CPT, NT>(stage, stage_pb, smem, pbs, 0);
 #pragma unroll
         for (int r = 0; r < TM; ++r)
             acur[r] = __builtin_amdgcn_raw_buffer_load_b32(
@@ -898,7 +899,7 @@ __device__ __forceinline__ void tab_body(const TabArgs &a)
         }
         const bool has_next = ntap * cpt * 8 + nc0 < p_end;
         if (has_next && ntap != tap) nxt = tab_tap<OP>(a, ntap);
-        if (has_next) tab_fetch<TNW, EB, CPT>(stage, stage_pb, nxt, nc0, a.Bd, a.Np, colw, a.rows);
+        if (has_next) tab_fetch<TNW, EB, CPT, NT>(stage, stage_pb, nxt, nc0, a.Bd, a.Np, colw, a.rows);
         const unsigned char *tb = smem + buf * SLAB + cg * TN * ROWB;
         const float *pb_s = pbs + buf * KS * TNW + cg * TN;
         const int nslots = min(KS, cur.count - c0);
@@ -937,7 +938,7 @@ __device__ __forceinline__ void tab_body(const TabArgs &a)
 #pragma unroll
             for (int r = 0; r < TM; ++r) acur[r] = anext[r];
         }
-        if (has_next) tab_commit<TNW, EB, CPT>(stage, stage_pb, smem, pbs, buf ^ 1);
+        if (has_next) tab_commit<TNW, EB, CPT, NT>(stage, stage_pb, smem, pbs, buf ^ 1);
         __syncthreads();
         cur = nxt;
         tap = ntap;
@@ -1055,19 +1056,21 @@ __device__ __forceinline__ void dot_load_a(uint32_t (&dst)[TM], __amdgpu_buffer_
     for (int r = 0; r < TM; ++r) dst[r] = __builtin_amdgcn_raw_buffer_load_b32(ares, aoff[r], so, 0);
 }
 
-// Workgroup: 4 waves along rows (64*TM rows each), all on the same 8 columns.
-template <int OP, int TM>
+// Workgroup: NW waves along rows (64*TM rows each), all on the same 8 columns.  The first 256
+// threads stage the slabs (8 steps x 32 entry groups); with 8 waves the other four only compute.
+template <int OP, int TM, int NW>
 __device__ __forceinline__ void tab_body_dot(const TabArgs &a)
 {
+    const bool stager = NW == 4 || threadIdx.x < 256;  // wave-uniform
     constexpr int KS = 8;
     constexpr int TN = kDotCols;
     extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
 
     const int R = tab_rows<OP>(a);
-    if (int(blockIdx.x) * 64 * TM * kWaves >= R) return;  // uniform over the workgroup
+    if (int(blockIdx.x) * 64 * TM * NW >= R) return;  // uniform over the workgroup
     const int lane = threadIdx.x & 63;
     const int wave = wave_id();
-    const int row0 = blockIdx.x * (64 * TM * kWaves) + wave * (64 * TM) + lane;
+    const int row0 = blockIdx.x * (64 * TM * NW) + wave * (64 * TM) + lane;
     const int col0 = blockIdx.y * TN;
     const __amdgpu_buffer_rsrc_t ares =
         __builtin_amdgcn_make_buffer_rsrc(const_cast<uint32_t *>(a.A), 0, int(a.a_bytes), 0x00020000);
@@ -1102,8 +1105,10 @@ __device__ __forceinline__ void tab_body_dot(const TabArgs &a)
     bool have = q0 * 8 < p_end;
     if (have) {
         cur = tab_tap<OP>(a, tap);
-        dot_fetch(sbw, srw, cur, c0, a.Bd, a.Np, col0, rres);
-        dot_commit(sbw, srw, smem);
+        if (stager) {
+            dot_fetch(sbw, srw, cur, c0, a.Bd, a.Np, col0, rres);
+            dot_commit(sbw, srw, smem);
+        }
         dot_load_a(a0, ares, aoff, cur, c0);
         dot_load_a(a1, ares, aoff, cur, c0 + 1);
     }
@@ -1119,7 +1124,7 @@ __device__ __forceinline__ void tab_body_dot(const TabArgs &a)
         }
         const bool has_next = ntap * cpt * 8 + nc0 < p_end;
         if (has_next && ntap != tap) nxt = tab_tap<OP>(a, ntap);
-        if (has_next) dot_fetch(sbw, srw, nxt, nc0, a.Bd, a.Np, col0, rres);
+        if (has_next && stager) dot_fetch(sbw, srw, nxt, nc0, a.Bd, a.Np, col0, rres);
         const uint32_t boff = uint32_t(buf) * kDotSlab;
         const int nslots = min(KS, cur.count - c0);
 #pragma unroll
@@ -1159,7 +1164,7 @@ __device__ __forceinline__ void tab_body_dot(const TabArgs &a)
                 a1[r] = n1[r];
             }
         }
-        if (has_next) dot_commit(sbw, srw, smem + (buf ^ 1) * kDotSlab);
+        if (has_next && stager) dot_commit(sbw, srw, smem + (buf ^ 1) * kDotSlab);
         __syncthreads();
         cur = nxt;
         tap = ntap;
@@ -1225,31 +1230,31 @@ __device__ __forceinline__ void tab_body_dot(const TabArgs &a)
 
 // Four waves per SIMD: the register budget (<= 128 VGPRs) the tiles are sized for.  Without the
 // hint the scheduler minimises registers and serialises the LDS gathers.
-template <int OP, int TM, int TN, int WR>
-__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(4, 4))) void tab_kernel(TabArgs a)
+template <int OP, int TM, int TN, int WR, int NW>
+__global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(4, 4))) void tab_kernel(TabArgs a)
 {
     const int eb = __builtin_amdgcn_readfirstlane(a.eb[0]);
-    if constexpr (TN == kDotCols && WR == kWaves) {
+    if constexpr (TN == kDotCols && WR == NW) {
         if (__builtin_amdgcn_readfirstlane(a.eb[1]) != 0) {
-            tab_body_dot<OP, TM>(a);
+            tab_body_dot<OP, TM, NW>(a);
             return;
         }
     }
     if (eb == 1)
-        tab_body<OP, TM, TN, WR, 1>(a);
+        tab_body<OP, TM, TN, WR, 1, NW>(a);
     else if (eb == 2)
-        tab_body<OP, TM, TN, WR, 2>(a);
+        tab_body<OP, TM, TN, WR, 2, NW>(a);
     else
-        tab_body<OP, TM, TN, WR, 4>(a);
+        tab_body<OP, TM, TN, WR, 4, NW>(a);
 }
 
 // Dynamic LDS of a table kernel with TN columns per wave and WR waves along rows: two slabs of
 // 8*TNW*128 bytes plus the second-operand heads, or two bf16-path slabs where that path exists.
-constexpr size_t tab_lds_bytes(int tn, int wr)
+constexpr size_t tab_lds_bytes(int tn, int wr, int nw)
 {
-    const int tnw = tn * (kWaves / wr);
+    const int tnw = tn * (nw / wr);
     const size_t exact = size_t(2) * 8 * tnw * kTabRowEntries + size_t(2) * 8 * tnw * 4;
-    const size_t dot = (tn == kDotCols && wr == kWaves) ? size_t(2) * kDotSlab : 0;
+    const size_t dot = (tn == kDotCols && wr == nw) ? size_t(2) * kDotSlab : 0;
     return exact > dot ? exact : dot;
 }
 
@@ -1457,6 +1462,7 @@ inline bool lds_path(int m_bits) { return m_bits <= kMaxLdsBits; }
 struct Tile {
     int tm, tn, split;
     int wr = kWaves;  // table kernels: waves along rows (the rest take column groups)
+    int nw = kWaves;  // table kernels: waves per workgroup
 };
 
 constexpr int kTargetWgs = 512;  // 256 CUs x 2 workgroups
@@ -1487,44 +1493,50 @@ Tile choose_tile(int64_t rows, int64_t cols, int64_t red, int64_t red_unit, bool
     return t;
 }
 
-// Per-column-table kernels (M <= 7).  Candidates are the instantiated (TM, TN, WR) tiles; the
+// Per-column-table kernels (M <= 7).  Candidates are the instantiated (TM, TN, WR, NW) tiles; the
 // choice minimises an estimate of issue time: padded work x cost per product, scaled up when the
-// grid, after splitting the reduction, cannot give every CU two workgroups.  Cost per product:
-// 3 VALU ops, per-step overhead (~2.5 per row, ~4 per lane), and the table staging, whose bytes
-// per product grow with the workgroup's columns (4/WR groups) and shrink with its rows (TM) --
-// each staged table row serves the workgroup's rows once (weight fitted on MI355X: a 64 x 32
-// backward-weight tile ran 2.4x slower than a 256 x 8 one).  4096^3 GEMM picks TM = 4, TN = 8,
-// WR = 4; a 576-row backward-weight picks TM = 3, WR = 4 (one 768-row tile).  `red` is the
-// reduction length in taps and `min_steps` the fewest taps a split may hold.  (TM = 3 with
+// grid, after splitting the reduction, cannot fill the chip (2048 waves: two 4-wave workgroups or
+// one 8-wave workgroup per CU and... its LDS allows, counted in waves).  Cost per product: the
+// inner loop (~1.2 VALU ops on the bf16 pair path, which 8-column tiles with all waves on rows
+// take for 1-byte tables; 3 on the exact path), per-step overhead (~2.5 per row, ~4 per lane), and
+// the table staging, which is per workgroup and slab, so its share per product falls with the
+// workgroup's rows (64 * TM * WR; weight fitted on MI355X: a 64 x 32 backward-weight tile ran 2.4x
+// slower than a 256 x 8 one, a 768-row GEMM tile 15% slower than a 1024-row one).  `red` is the
+// reduction length in chunks and `min_steps` the fewest chunks a split may hold.  (TM = 3 with
 // WR = 1 would exceed the 128-VGPR budget: its 32-column slab staging alone holds 40 registers.)
 struct TabCand {
-    int tm, tn, wr;
+    int tm, tn, wr, nw;
 };
-constexpr TabCand kTabCands[] = {{4, 8, 4}, {3, 8, 4}, {2, 8, 4}, {1, 8, 4}, {4, 4, 4}, {2, 4, 4},
-                                 {1, 4, 4}, {4, 8, 2}, {2, 8, 2}, {1, 8, 2}, {2, 8, 1}, {1, 8, 1}};
+constexpr TabCand kTabCands[] = {{4, 8, 8, 8}, {4, 8, 4, 4}, {3, 8, 4, 4}, {2, 8, 4, 4}, {1, 8, 4, 4},
+                                 {4, 4, 4, 4}, {2, 4, 4, 4}, {1, 4, 4, 4}, {4, 8, 2, 4}, {2, 8, 2, 4},
+                                 {1, 8, 2, 4}, {2, 8, 1, 4}, {1, 8, 1, 4}};
 
 Tile choose_tab_tile(int64_t rows, int64_t cols, int64_t red, int64_t min_steps, bool allow_split)
 {
+    constexpr int64_t kTargetWaves = int64_t(kTargetWgs) * kWaves;
     Tile best{};
     double best_cost = 0.0;
     for (const TabCand &c : kTabCands) {
         const int64_t rtile = int64_t(64) * c.tm * c.wr;
-        const int64_t ctile = int64_t(c.tn) * (kWaves / c.wr);
+        const int64_t ctile = int64_t(c.tn) * (c.nw / c.wr);
         const int64_t tiles = ceil_div(rows, rtile) * ceil_div(cols, ctile);
         int split = 1;
-        if (allow_split && tiles < kTargetWgs) {
+        if (allow_split && tiles * c.nw < kTargetWaves) {
             const int64_t max_split = std::max<int64_t>(1, red / std::max<int64_t>(1, min_steps));
-            split = int(std::min<int64_t>(std::min<int64_t>(ceil_div(kTargetWgs, tiles), max_split), 1024));
+            split = int(std::min<int64_t>(std::min<int64_t>(ceil_div(kTargetWaves, tiles * c.nw), max_split), 1024));
         }
         const double work = double(ceil_div(rows, rtile) * rtile) * double(ceil_div(cols, ctile) * ctile);
-        const double per_product = 3.0 + 2.5 / c.tn + 4.0 / (c.tm * c.tn) + 2.0 * (kWaves / c.wr) / c.tm;
-        const double fill = std::min(1.0, double(tiles * split) / kTargetWgs);
+        const bool pair = c.tn == kDotCols && c.wr == c.nw;
+        const double per_product =
+            (pair ? 1.2 : 3.0) + 2.5 / c.tn + 4.0 / (c.tm * c.tn) + 8.0 / (c.wr * c.tm) * (pair ? 0.5 : 1.0);
+        const double fill = std::min(1.0, double(tiles * split * c.nw) / kTargetWaves);
         const double cost = work * per_product / fill;
         if (best_cost == 0.0 || cost < best_cost * 0.999) {
             best_cost = cost;
             best.tm = c.tm;
             best.tn = c.tn;
             best.wr = c.wr;
+            best.nw = c.nw;
             best.split = split;
         }
     }
@@ -1532,7 +1544,7 @@ Tile choose_tab_tile(int64_t rows, int64_t cols, int64_t red, int64_t min_steps,
 }
 
 // Columns of a table-kernel workgroup.
-inline int64_t tab_cols(const Tile &t) { return int64_t(t.tn) * (kWaves / t.wr); }
+inline int64_t tab_cols(const Tile &t) { return int64_t(t.tn) * (t.nw / t.wr); }
 
 std::once_flag g_attr_once;
 hipError_t g_attr_err = hipSuccess;
@@ -1545,18 +1557,18 @@ void allow_lds(K kernel, size_t bytes)
     if (e != hipSuccess) g_attr_err = e;
 }
 
-#define AMSIM_FOR_TAB_TILES(X) \
-    X(4, 8, 4) X(3, 8, 4) X(2, 8, 4) X(1, 8, 4) X(4, 4, 4) X(2, 4, 4) X(1, 4, 4) X(4, 8, 2) X(2, 8, 2) X(1, 8, 2) \
-    X(2, 8, 1) X(1, 8, 1)
+#define AMSIM_FOR_TAB_TILES(X)                                                                               \
+    X(4, 8, 8, 8) X(4, 8, 4, 4) X(3, 8, 4, 4) X(2, 8, 4, 4) X(1, 8, 4, 4) X(4, 4, 4, 4) X(2, 4, 4, 4) X(1, 4, 4, 4) \
+    X(4, 8, 2, 4) X(2, 8, 2, 4) X(1, 8, 2, 4) X(2, 8, 1, 4) X(1, 8, 1, 4)
 #define AMSIM_FOR_TILES(X) X(8, 16) X(4, 16) X(2, 16) X(1, 16) X(8, 4) X(4, 4) X(2, 4) X(1, 4)
 
 void set_attributes()
 {
-#define X(TM, TN, WR)                                                                      \
-    allow_lds(tab_kernel<OP_GEMM, TM, TN, WR>, tab_lds_bytes(TN, WR));        \
-    allow_lds(tab_kernel<OP_FWD, TM, TN, WR>, tab_lds_bytes(TN, WR));         \
-    allow_lds(tab_kernel<OP_BWD_DATA, TM, TN, WR>, tab_lds_bytes(TN, WR));    \
-    allow_lds(tab_kernel<OP_BWD_WEIGHT, TM, TN, WR>, tab_lds_bytes(TN, WR));
+#define X(TM, TN, WR, NW)                                                                  \
+    allow_lds(tab_kernel<OP_GEMM, TM, TN, WR, NW>, tab_lds_bytes(TN, WR, NW));           \
+    allow_lds(tab_kernel<OP_FWD, TM, TN, WR, NW>, tab_lds_bytes(TN, WR, NW));            \
+    allow_lds(tab_kernel<OP_BWD_DATA, TM, TN, WR, NW>, tab_lds_bytes(TN, WR, NW));       \
+    allow_lds(tab_kernel<OP_BWD_WEIGHT, TM, TN, WR, NW>, tab_lds_bytes(TN, WR, NW));
     AMSIM_FOR_TAB_TILES(X)
 #undef X
 }
@@ -1589,10 +1601,10 @@ inline int decode_vec(const float *src, int64_t sb, int64_t sr, int64_t sc)
 template <typename F>
 void dispatch_tab_tile(const Tile &t, F &&f)
 {
-#define X(TM, TN, WR)                                                                     \
-    if (t.tm == TM && t.tn == TN && t.wr == WR) {                                         \
+#define X(TM, TN, WR, NW)                                                                 \
+    if (t.tm == TM && t.tn == TN && t.wr == WR && t.nw == NW) {                           \
         f(std::integral_constant<int, TM>{}, std::integral_constant<int, TN>{},           \
-          std::integral_constant<int, WR>{});                                             \
+          std::integral_constant<int, WR>{}, std::integral_constant<int, NW>{});          \
         return;                                                                           \
     }
     AMSIM_FOR_TAB_TILES(X)
@@ -1847,10 +1859,10 @@ int prep_rows(const uint32_t *lut, int m_bits, char *ws, const Plan &p, int n_a,
 template <int OP>
 int launch_tab(const Plan &p, const TabArgs &a, dim3 grid, hipStream_t st)
 {
-    auto run = [&](auto tm, auto tn, auto wr) {
+    auto run = [&](auto tm, auto tn, auto wr, auto nw) {
         constexpr int TM = decltype(tm)::value, TN = decltype(tn)::value, WR = decltype(wr)::value;
-        hipLaunchKernelGGL((tab_kernel<OP, TM, TN, WR>), grid, dim3(kThreads), tab_lds_bytes(TN, WR), st,
-                           a);
+        constexpr int NW = decltype(nw)::value;
+        hipLaunchKernelGGL((tab_kernel<OP, TM, TN, WR, NW>), grid, dim3(64 * NW), tab_lds_bytes(TN, WR, NW), st, a);
     };
     dispatch_tab_tile(p.tile, run);
     return launch_status();
