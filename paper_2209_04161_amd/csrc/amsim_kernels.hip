@@ -1098,7 +1098,10 @@ __device__ __forceinline__ void tab_body_dot(const TabArgs &a)
     uint32_t srw[kDotCols];
     float acc[TM][TN];
     init_acc(acc);
-    uint32_t a0[TM], a1[TM];  // first-operand words of the current step pair
+    // First-operand words of the slab's four step pairs, as a ring: pair kp is in w[kp]; while it
+    // is used, pair kp + 2 (of this slab, or of the next slab for kp >= 2) is loaded into
+    // w[(kp + 2) % 4], so that after a full slab the next slab's first two pairs sit in w[0], w[1].
+    uint32_t w[4][2][TM];
     TabTap cur{0, 0, 0, 0};
     int tap = q0 / max(cpt, 1);
     int c0 = (q0 - tap * cpt) * 8;
@@ -1109,14 +1112,17 @@ __device__ __forceinline__ void tab_body_dot(const TabArgs &a)
             dot_fetch(sbw, srw, cur, c0, a.Bd, a.Np, col0, rres);
             dot_commit(sbw, srw, smem);
         }
-        dot_load_a(a0, ares, aoff, cur, c0);
-        dot_load_a(a1, ares, aoff, cur, c0 + 1);
+#pragma unroll
+        for (int k = 0; k < 2; ++k) {
+            dot_load_a(w[k][0], ares, aoff, cur, c0 + 2 * k);
+            dot_load_a(w[k][1], ares, aoff, cur, c0 + 2 * k + 1);
+        }
     }
     __syncthreads();
     int buf = 0;
     while (have) {
         uniform_cursor(cur, tap, c0);
-        TabTap nxt = cur;
+        TabTap nxt = cur;  // stays `cur` past the last slab: the loads below then stay in bounds
         int ntap = tap, nc0 = c0 + KS;
         if (nc0 >= count) {
             ntap = tap + 1;
@@ -1127,21 +1133,20 @@ __device__ __forceinline__ void tab_body_dot(const TabArgs &a)
         if (has_next && stager) dot_fetch(sbw, srw, nxt, nc0, a.Bd, a.Np, col0, rres);
         const uint32_t boff = uint32_t(buf) * kDotSlab;
         const int nslots = min(KS, cur.count - c0);
+        const int npairs = (nslots + 1) / 2;
 #pragma unroll
         for (int kp = 0; kp < KS / 2; ++kp) {
-            if (2 * kp >= nslots) break;
-            // the next pair's words: this slab's next pair or the next slab's first
-            uint32_t n0[TM], n1[TM];
-            if (2 * kp + 2 < nslots) {
-                dot_load_a(n0, ares, aoff, cur, c0 + 2 * kp + 2);
-                dot_load_a(n1, ares, aoff, cur, c0 + 2 * kp + 3);
-            } else if (has_next) {
-                dot_load_a(n0, ares, aoff, nxt, nc0);
-                dot_load_a(n1, ares, aoff, nxt, nc0 + 1);
+            if (kp >= npairs) break;
+            uint32_t(&nw)[2][TM] = w[(kp + 2) % 4];
+            if (kp < 2) {
+                dot_load_a(nw[0], ares, aoff, cur, c0 + 2 * kp + 4);
+                dot_load_a(nw[1], ares, aoff, cur, c0 + 2 * kp + 5);
             } else {
-#pragma unroll
-                for (int r = 0; r < TM; ++r) n0[r] = n1[r] = 0u;  // past the last slab: unused
+                dot_load_a(nw[0], ares, aoff, nxt, nc0 + 2 * kp - 4);
+                dot_load_a(nw[1], ares, aoff, nxt, nc0 + 2 * kp - 3);
             }
+            const uint32_t(&a0)[TM] = w[kp][0];
+            const uint32_t(&a1)[TM] = w[kp][1];
 #pragma unroll
             for (int r = 0; r < TM; ++r) {
                 // entry byte offset = the word's low half (mantissa field * 16; the head is bits
@@ -1158,10 +1163,12 @@ __device__ __forceinline__ void tab_body_dot(const TabArgs &a)
                         dot2_bf16(__builtin_amdgcn_perm(Y[q], X[q], 0x07060302u), pa, acc[r][2 * q + 1]);
                 }
             }
+        }
+        if (npairs < KS / 2 && has_next) {  // a short slab: load the next slab's first two pairs
 #pragma unroll
-            for (int r = 0; r < TM; ++r) {
-                a0[r] = n0[r];
-                a1[r] = n1[r];
+            for (int k = 0; k < 2; ++k) {
+                dot_load_a(w[k][0], ares, aoff, nxt, nc0 + 2 * k);
+                dot_load_a(w[k][1], ares, aoff, nxt, nc0 + 2 * k + 1);
             }
         }
         if (has_next && stager) dot_commit(sbw, srw, smem + (buf ^ 1) * kDotSlab);
