@@ -842,6 +842,7 @@ __device__ __forceinline__ void tab_body(const TabArgs &a)
     const int wave = wave_id();
     const int rg = wave % WR, cg = wave / WR;
     const int row0 = blockIdx.x * (64 * TM * WR) + rg * (64 * TM) + lane;
+    const bool live = row0 - lane < R;  // wave-uniform: a wave past the end only stages
     const int colw = blockIdx.y * TNW;  // first column of the workgroup
     const int col0 = colw + cg * TN;    // first column of this wave
     // First-operand reads are raw buffer loads: voffset = the lane row's byte offset (range-checked,
@@ -902,7 +903,7 @@ __device__ __forceinline__ void tab_body(const TabArgs &a)
         if (has_next) tab_fetch<TNW, EB, CPT, NT>(stage, stage_pb, nxt, nc0, a.Bd, a.Np, colw, a.rows);
         const unsigned char *tb = smem + buf * SLAB + cg * TN * ROWB;
         const float *pb_s = pbs + buf * KS * TNW + cg * TN;
-        const int nslots = min(KS, cur.count - c0);
+        const int nslots = live ? min(KS, cur.count - c0) : 0;
 #pragma unroll
         for (int slot = 0; slot < KS; ++slot) {
             if (slot >= nslots) break;
@@ -982,7 +983,9 @@ typedef uint16_t u16x2_t __attribute__((ext_vector_type(2)));
 
 constexpr int kDotCols = 8;                          // columns per entry
 constexpr int kDotStepBytes = kTabRowEntries * 16;   // 128 entries x 16 bytes
-constexpr int kDotSlab = 8 * kDotStepBytes;          // 8 steps per slab: 16 KiB
+// Steps per slab: 8 for 4-wave workgroups, 16 for 8-wave ones (each thread stages one step's
+// entry group, 32 threads per step); a slab is 2 KiB per step.
+constexpr int dot_slab_steps(int nw) { return nw * 2; }
 
 __device__ __forceinline__ float dot2_bf16(uint32_t x, uint32_t y, float c)
 {
@@ -1056,13 +1059,13 @@ __device__ __forceinline__ void dot_load_a(uint32_t (&dst)[TM], __amdgpu_buffer_
     for (int r = 0; r < TM; ++r) dst[r] = __builtin_amdgcn_raw_buffer_load_b32(ares, aoff[r], so, 0);
 }
 
-// Workgroup: NW waves along rows (64*TM rows each), all on the same 8 columns.  The first 256
-// threads stage the slabs (8 steps x 32 entry groups); with 8 waves the other four only compute.
+// Workgroup: NW waves along rows (64*TM rows each), all on the same 8 columns.  Every thread
+// stages one step's entry group per slab (KS = 2 * NW steps x 32 groups).
 template <int OP, int TM, int NW>
 __device__ __forceinline__ void tab_body_dot(const TabArgs &a)
 {
-    const bool stager = NW == 4 || threadIdx.x < 256;  // wave-uniform
-    constexpr int KS = 8;
+    constexpr int KS = dot_slab_steps(NW);
+    constexpr int kDotSlab = KS * kDotStepBytes;
     constexpr int TN = kDotCols;
     extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
 
@@ -1071,6 +1074,7 @@ __device__ __forceinline__ void tab_body_dot(const TabArgs &a)
     const int lane = threadIdx.x & 63;
     const int wave = wave_id();
     const int row0 = blockIdx.x * (64 * TM * NW) + wave * (64 * TM) + lane;
+    const bool live = row0 - lane < R;  // wave-uniform
     const int col0 = blockIdx.y * TN;
     const __amdgpu_buffer_rsrc_t ares =
         __builtin_amdgcn_make_buffer_rsrc(const_cast<uint32_t *>(a.A), 0, int(a.a_bytes), 0x00020000);
@@ -1098,9 +1102,10 @@ __device__ __forceinline__ void tab_body_dot(const TabArgs &a)
     uint32_t srw[kDotCols];
     float acc[TM][TN];
     init_acc(acc);
-    // First-operand words of the slab's four step pairs, as a ring: pair kp is in w[kp]; while it
-    // is used, pair kp + 2 (of this slab, or of the next slab for kp >= 2) is loaded into
-    // w[(kp + 2) % 4], so that after a full slab the next slab's first two pairs sit in w[0], w[1].
+    // First-operand words of four step pairs, as a ring: pair kp of a slab is in w[kp % 4]; while
+    // it is used, pair kp + 2 (of this slab, or the next slab's first two for the last two pairs)
+    // is loaded into w[(kp + 2) % 4].  A slab holds a multiple of four pairs, so after a full slab
+    // the next slab's first two pairs sit in w[0], w[1].
     uint32_t w[4][2][TM];
     TabTap cur{0, 0, 0, 0};
     int tap = q0 / max(cpt, 1);
@@ -1108,10 +1113,8 @@ __device__ __forceinline__ void tab_body_dot(const TabArgs &a)
     bool have = q0 * 8 < p_end;
     if (have) {
         cur = tab_tap<OP>(a, tap);
-        if (stager) {
-            dot_fetch(sbw, srw, cur, c0, a.Bd, a.Np, col0, rres);
-            dot_commit(sbw, srw, smem);
-        }
+        dot_fetch(sbw, srw, cur, c0, a.Bd, a.Np, col0, rres);
+        dot_commit(sbw, srw, smem);
 #pragma unroll
         for (int k = 0; k < 2; ++k) {
             dot_load_a(w[k][0], ares, aoff, cur, c0 + 2 * k);
@@ -1130,23 +1133,25 @@ __device__ __forceinline__ void tab_body_dot(const TabArgs &a)
         }
         const bool has_next = ntap * cpt * 8 + nc0 < p_end;
         if (has_next && ntap != tap) nxt = tab_tap<OP>(a, ntap);
-        if (has_next && stager) dot_fetch(sbw, srw, nxt, nc0, a.Bd, a.Np, col0, rres);
+        if (has_next) dot_fetch(sbw, srw, nxt, nc0, a.Bd, a.Np, col0, rres);
         const uint32_t boff = uint32_t(buf) * kDotSlab;
-        const int nslots = min(KS, cur.count - c0);
-        const int npairs = (nslots + 1) / 2;
+        // the slab ends at the tap's end or, 8-step chunks being the unit of splits, at the split's
+        const int nslots = min(min(KS, cur.count - c0), p_end - (tap * cpt * 8 + c0));
+        // a wave whose rows all lie past the end only stages and keeps the barriers
+        const int npairs = live ? (nslots + 1) / 2 : 0;
 #pragma unroll
         for (int kp = 0; kp < KS / 2; ++kp) {
             if (kp >= npairs) break;
-            uint32_t(&nw)[2][TM] = w[(kp + 2) % 4];
-            if (kp < 2) {
-                dot_load_a(nw[0], ares, aoff, cur, c0 + 2 * kp + 4);
-                dot_load_a(nw[1], ares, aoff, cur, c0 + 2 * kp + 5);
+            uint32_t(&ahead)[2][TM] = w[(kp + 2) % 4];
+            if (kp + 2 < KS / 2) {
+                dot_load_a(ahead[0], ares, aoff, cur, c0 + 2 * kp + 4);
+                dot_load_a(ahead[1], ares, aoff, cur, c0 + 2 * kp + 5);
             } else {
-                dot_load_a(nw[0], ares, aoff, nxt, nc0 + 2 * kp - 4);
-                dot_load_a(nw[1], ares, aoff, nxt, nc0 + 2 * kp - 3);
+                dot_load_a(ahead[0], ares, aoff, nxt, nc0 + 2 * (kp + 2 - KS / 2));
+                dot_load_a(ahead[1], ares, aoff, nxt, nc0 + 2 * (kp + 2 - KS / 2) + 1);
             }
-            const uint32_t(&a0)[TM] = w[kp][0];
-            const uint32_t(&a1)[TM] = w[kp][1];
+            const uint32_t(&a0)[TM] = w[kp % 4][0];
+            const uint32_t(&a1)[TM] = w[kp % 4][1];
 #pragma unroll
             for (int r = 0; r < TM; ++r) {
                 // entry byte offset = the word's low half (mantissa field * 16; the head is bits
@@ -1164,14 +1169,14 @@ __device__ __forceinline__ void tab_body_dot(const TabArgs &a)
                 }
             }
         }
-        if (npairs < KS / 2 && has_next) {  // a short slab: load the next slab's first two pairs
+        if (live && npairs < KS / 2 && has_next) {  // a short slab: the next slab's first two pairs
 #pragma unroll
             for (int k = 0; k < 2; ++k) {
                 dot_load_a(w[k][0], ares, aoff, nxt, nc0 + 2 * k);
                 dot_load_a(w[k][1], ares, aoff, nxt, nc0 + 2 * k + 1);
             }
         }
-        if (has_next && stager) dot_commit(sbw, srw, smem + (buf ^ 1) * kDotSlab);
+        if (has_next) dot_commit(sbw, srw, smem + (buf ^ 1) * kDotSlab);
         __syncthreads();
         cur = nxt;
         tap = ntap;
@@ -1261,7 +1266,7 @@ constexpr size_t tab_lds_bytes(int tn, int wr, int nw)
 {
     const int tnw = tn * (nw / wr);
     const size_t exact = size_t(2) * 8 * tnw * kTabRowEntries + size_t(2) * 8 * tnw * 4;
-    const size_t dot = (tn == kDotCols && wr == nw) ? size_t(2) * kDotSlab : 0;
+    const size_t dot = (tn == kDotCols && wr == nw) ? size_t(2) * dot_slab_steps(nw) * kDotStepBytes : 0;
     return exact > dot ? exact : dot;
 }
 
@@ -1524,19 +1529,23 @@ Tile choose_tab_tile(int64_t rows, int64_t cols, int64_t red, int64_t min_steps,
     Tile best{};
     double best_cost = 0.0;
     for (const TabCand &c : kTabCands) {
-        const int64_t rtile = int64_t(64) * c.tm * c.wr;
+        // Waves whose rows all lie past the end skip the work: count the waves that have rows.
+        const int64_t wrows = int64_t(64) * c.tm;  // rows per wave
+        const int64_t rtile = wrows * c.wr;
         const int64_t ctile = int64_t(c.tn) * (c.nw / c.wr);
-        const int64_t tiles = ceil_div(rows, rtile) * ceil_div(cols, ctile);
+        const int64_t col_tiles = ceil_div(cols, ctile);
+        const int64_t live_waves = ceil_div(rows, wrows) * col_tiles * (c.nw / c.wr);
+        const int64_t live_rows = std::min(rtile, ceil_div(rows, wrows) * wrows);  // of the fullest workgroup
         int split = 1;
-        if (allow_split && tiles * c.nw < kTargetWaves) {
+        if (allow_split && live_waves < kTargetWaves) {
             const int64_t max_split = std::max<int64_t>(1, red / std::max<int64_t>(1, min_steps));
-            split = int(std::min<int64_t>(std::min<int64_t>(ceil_div(kTargetWaves, tiles * c.nw), max_split), 1024));
+            split = int(std::min<int64_t>(std::min<int64_t>(ceil_div(kTargetWaves, live_waves), max_split), 1024));
         }
-        const double work = double(ceil_div(rows, rtile) * rtile) * double(ceil_div(cols, ctile) * ctile);
+        const double work = double(ceil_div(rows, wrows) * wrows) * double(col_tiles * ctile);
         const bool pair = c.tn == kDotCols && c.wr == c.nw;
         const double per_product =
-            (pair ? 1.2 : 3.0) + 2.5 / c.tn + 4.0 / (c.tm * c.tn) + 8.0 / (c.wr * c.tm) * (pair ? 0.5 : 1.0);
-        const double fill = std::min(1.0, double(tiles * split * c.nw) / kTargetWaves);
+            (pair ? 1.2 : 3.0) + 2.5 / c.tn + 4.0 / (c.tm * c.tn) + 512.0 / double(live_rows) * (pair ? 0.5 : 1.0);
+        const double fill = std::min(1.0, double(live_waves * split) / kTargetWaves);
         const double cost = work * per_product / fill;
         if (best_cost == 0.0 || cost < best_cost * 0.999) {
             best_cost = cost;
