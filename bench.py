@@ -215,6 +215,30 @@ def extras(B, W, torch, np, dev, lut7, m7, A, Bm, C):
     ms = _time_call(torch, lambda: B.approx_gemm(A, Bm, lut11, 11, out=C, workspace=ws), 2)
     ex["gemm_4096_m11_global_table"] = {"ms": round(ms, 2), "gmacs_per_s": round(M * N * K / ms / 1e6, 1)}
     log("M=11 GEMM done")
+    # the same GEMM at smaller sizes, table in LDS (M=7) and in global memory (M=11)
+    sweep = {}
+    for n in (512, 1024, 2048):
+        a, b = (torch.from_numpy(t).to(dev) for t in W.gemm_inputs(n, n, n, "normal", seed=5100 + n))
+        c = torch.empty((n, n), dtype=torch.float32, device=dev)
+        for mb, lt in ((7, lut7), (11, lut11)):
+            wsn = torch.empty(max(1, B.amsim_gemm_workspace_size(0, 0, n, n, n, mb)), dtype=torch.uint8, device=dev)
+            ms = _time_call(torch, lambda: B.approx_gemm(a, b, lt, mb, out=c, workspace=wsn), 5 if mb == 7 else 2)
+            sweep["n%d_m%d" % (n, mb)] = {"ms": round(ms, 3), "gmacs_per_s": round(n ** 3 / ms / 1e6, 1)}
+    ex["gemm_sweep_mitchell"] = sweep
+    log("GEMM size sweep done")
+    # ResNet 3x3 with post-ReLU activations (about half exact zeros) instead of |N(0,1)|
+    cv = W.RESNET_3X3["conv"]
+    x_h, w_h, dy_h = W.resnet_conv_inputs(cv, seed=4500)
+    x_h = np.maximum(W.normal(x_h.shape, 1.0, 4501), 0.0).astype(np.float32)
+    x, w, dy = (torch.from_numpy(t).to(dev) for t in (x_h, w_h, dy_h))
+    macs = W.conv_macs(cv)
+    r = {"zero_fraction": round(float((x_h == 0).mean()), 3)}
+    for name, fn in (("fwd", lambda: B.approx_conv2d_fwd(cv, x, w, lut7, m7)),
+                     ("bwd_weight", lambda: B.approx_conv2d_bwd_weight(cv, x, dy, lut7, m7))):
+        ms = _time_call(torch, fn, 5)
+        r[name] = {"ms": round(ms, 3), "gmacs_per_s": round(macs / ms / 1e6, 1)}
+    ex["resnet_3x3_relu_input"] = r
+    log("ReLU-input ResNet 3x3 done")
     for cfg in W.RESNET50_LAYERS:
         p = cfg["conv"]
         x_h, w_h, dy_h = W.resnet_conv_inputs(p, seed=4000, stem=(cfg is W.RESNET50_LAYERS[0]))

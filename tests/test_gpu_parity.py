@@ -309,8 +309,10 @@ def _sample(total, count, seed):
     return np.sort(np.concatenate([idx, [0, total - 1]]).astype(np.int64))
 
 
-def _check_conv_full(B, p, m, seed, stem=False, samples=(2048, 2048, 512)):
+def _check_conv_full(B, p, m, seed, stem=False, samples=(2048, 2048, 512), relu=False):
     x, w, dy = W.resnet_conv_inputs(p, seed=seed, stem=stem)
+    if relu:  # post-ReLU activations: about half exact zeros
+        x = np.maximum(W.normal(x.shape, 1.0, seed + 7), 0.0).astype(np.float32)
     lut = dev_lut(B, "mitchell", m)
     xd, wd, dyd = cuda(x), cuda(w), cuda(dy)
     y = host(B.approx_conv2d_fwd(p, xd, wd, lut, m)).reshape(-1)
@@ -331,6 +333,13 @@ def _check_conv_full(B, p, m, seed, stem=False, samples=(2048, 2048, 512)):
 def test_resnet_3x3_conv_full_size(B):
     cfg = W.RESNET_3X3
     _check_conv_full(B, cfg["conv"], cfg["m_bits"], seed=3000)
+
+
+def test_resnet_3x3_relu_input_full_size(B):
+    """The same layer with x = ReLU(N(0,1)): half the first operands of forward and backward-weight
+    are exact zeros."""
+    cfg = W.RESNET_3X3
+    _check_conv_full(B, cfg["conv"], cfg["m_bits"], seed=3100, relu=True)
 
 
 @pytest.mark.parametrize("li", range(len(W.RESNET50_LAYERS)))
