@@ -20,8 +20,8 @@
  *   - `lut` is a device copy of the table built by lut_build: uint32[2^(2*m_bits)], entry
  *     k * 2^M + j holds carry << 23 | mantissa(23 bits) for first-operand mantissa k and
  *     second-operand mantissa j.  Only its low 24 bits are read.
- *   - m_bits (the paper's M) must be in [1, 11]; M <= 7 keeps the table in LDS, 8..11 reads it
- *     from global memory.
+ *   - m_bits (the paper's M) must be in [1, 11].  The library stages the table rows that each
+ *     step needs into LDS: rows of 128 entries for M <= 7, of 2^M entries for M = 8..11.
  *   - Products: zero/denormal operands give a signed zero, NaN operands NaN, Inf times a
  *     zero/denormal operand NaN, Inf times anything else a signed Inf; otherwise zero if
  *     Ea + Eb - 127 <= 0 (checked before the carry), Inf if it is >= 255 or the carry lifts

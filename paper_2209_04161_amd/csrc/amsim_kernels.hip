@@ -26,6 +26,7 @@
 
 #include <algorithm>
 #include <cstdint>
+#include <iterator>
 #include <mutex>
 #include <type_traits>
 #include <vector>
@@ -38,7 +39,6 @@ constexpr uint32_t kIdxMask = 0x003FFFFFu;
 constexpr uint32_t kHeadMask = 0xFFC00000u;
 constexpr int kWaves = 4;           // waves per workgroup (column groups)
 constexpr int kThreads = 64 * kWaves;
-constexpr int kMaxLdsBits = 7;      // table in LDS for M <= 7 (64 KiB)
 
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
@@ -64,51 +64,6 @@ __device__ __forceinline__ float head_value(uint32_t w) { return __uint_as_float
 __device__ __forceinline__ float table_value(uint32_t entry)
 {
     return __uint_as_float((entry & 0x00FFFFFFu) + 0x3F800000u);
-}
-
-// One k-step of the register tile: acc[r][t] += amul(a_r, b_t) for TM lane rows and TN
-// wave-uniform columns.  `aw` are the lane's decoded first-operand words, `brow` points at
-// TN decoded second-operand words (uniform address -> scalar loads).
-template <int TM, int TN, bool LDS>
-__device__ __forceinline__ void amsim_mac(float (&acc)[TM][TN], const uint32_t (&aw)[TM],
-                                          const uint32_t *__restrict__ brow, const uint32_t *__restrict__ glut)
-{
-    extern __shared__ uint32_t lds_lut[];
-    uint32_t aoff[TM];
-    float pa[TM];
-#pragma unroll
-    for (int r = 0; r < TM; ++r) {
-        aoff[r] = aw[r] & kIdxMask;
-        pa[r] = head_value(aw[r]);
-    }
-#pragma unroll
-    for (int t = 0; t < TN; ++t) {
-        const uint32_t bw = brow[t];
-        const uint32_t boff = bw & kIdxMask;
-        const float pb = head_value(bw);
-#pragma unroll
-        for (int r = 0; r < TM; ++r) {
-            float v;
-            if constexpr (LDS)
-                v = *reinterpret_cast<const float *>(reinterpret_cast<const char *>(lds_lut) + (aoff[r] + boff));
-            else
-                v = table_value(glut[aoff[r] + boff]);
-            acc[r][t] = __builtin_fmaf(v, pa[r] * pb, acc[r][t]);
-        }
-    }
-}
-
-// Copy the prepared (transposed, rebiased) table into LDS.  entries is a multiple of 4.
-template <bool LDS>
-__device__ __forceinline__ void stage_table(const uint32_t *__restrict__ lut_t, int entries)
-{
-    if constexpr (LDS) {
-        extern __shared__ uint32_t lds_lut[];
-        const uint4 *src = reinterpret_cast<const uint4 *>(lut_t);
-        uint4 *dst = reinterpret_cast<uint4 *>(lds_lut);
-        for (int i = threadIdx.x; i < entries / 4; i += blockDim.x) dst[i] = src[i];
-        __syncthreads();
-    }
 }
 
 template <int TM, int TN>
@@ -397,51 +352,6 @@ __global__ void mul_ew_kernel(int64_t n, const float *__restrict__ a, const floa
     }
 }
 
-// ------------------------------------------------------------------ GEMM kernel ---------
-// Ad: decoded op(A) stored k-major, Ad[k * Mp + i] (Mp = rows padded to the row tile).
-// Bd: decoded op(B) row-major, Bd[k * Np + j] (Np = columns padded to the column tile).
-// Split z of gridDim.z sums k in [z * kchunk, min(K, (z+1) * kchunk)).  out is C (ldc) when
-// gridDim.z == 1, else the split's slab of the partial-sum buffer (ld = N).
-template <int TM, int TN, bool LDS>
-__global__ __launch_bounds__(kThreads) void gemm_kernel(const uint32_t *__restrict__ Ad, int Mp,
-                                                        const uint32_t *__restrict__ Bd, int Np, int M, int N, int K,
-                                                        int kchunk, float *__restrict__ out, int64_t ldc,
-                                                        const uint32_t *__restrict__ lut, int entries)
-{
-    stage_table<LDS>(lut, entries);
-    const int lane = threadIdx.x & 63;
-    const int row0 = blockIdx.x * (64 * TM) + lane;
-    const int col0 = (blockIdx.y * kWaves + wave_id()) * TN;
-    const int kbeg = blockIdx.z * kchunk;
-    const int kend = min(K, kbeg + kchunk);
-    float acc[TM][TN];
-    init_acc(acc);
-    if (col0 < Np) {
-        for (int k = kbeg; k < kend; ++k) {
-            uint32_t aw[TM];
-#pragma unroll
-            for (int r = 0; r < TM; ++r) aw[r] = Ad[int64_t(k) * Mp + row0 + 64 * r];
-            amsim_mac<TM, TN, LDS>(acc, aw, Bd + int64_t(k) * Np + col0, lut);
-        }
-    }
-    float *dst = out;
-    int64_t ld = ldc;
-    if (gridDim.z > 1) {
-        dst = out + int64_t(blockIdx.z) * M * N;
-        ld = N;
-    }
-#pragma unroll
-    for (int r = 0; r < TM; ++r) {
-        const int row = row0 + 64 * r;
-        if (row >= M) continue;
-#pragma unroll
-        for (int t = 0; t < TN; ++t) {
-            const int col = col0 + t;
-            if (col < N) dst[int64_t(row) * ld + col] = acc[r][t];
-        }
-    }
-}
-
 // ------------------------------------------------------------------ GEMM, per-column tables
 // For M <= 7 the fastest form keeps, per k-step and output column j, the table row selected
 // by that column's second-operand mantissa kb(k, j) -- LUT[. ][kb], indexed by the first
@@ -598,6 +508,63 @@ __global__ __launch_bounds__(1024) void prep_rows_kernel(const uint32_t *__restr
             }
             *reinterpret_cast<uint32_t *>(dot_rows + size_t(kb) * kTabRowEntries + 4 * g) = word;
         }
+    }
+}
+
+// Wide tables (M = 8..11, rows of 2^M entries, no bf16 path).  First pass: the OR of every entry's
+// low 16 mantissa bits, one word per workgroup.
+__global__ __launch_bounds__(256) void lut_low_bits_kernel(const uint32_t *__restrict__ lut, int total,
+                                                           uint32_t *__restrict__ part)
+{
+    __shared__ uint32_t s_low[4];
+    uint32_t low = 0u;
+    for (int i = blockIdx.x * 256 + threadIdx.x; i < total; i += gridDim.x * 256) low |= lut[i] & 0xFFFFu;
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) low |= uint32_t(__shfl_xor(int(low), o));
+    if ((threadIdx.x & 63) == 0) s_low[threadIdx.x >> 6] = low;
+    __syncthreads();
+    if (threadIdx.x == 0) part[blockIdx.x] = s_low[0] | s_low[1] | s_low[2] | s_low[3];
+}
+
+// Second pass: the entry width from the nparts partial words, then the transposed rows -- row kb
+// (2^m entries of eb bytes) holds entry (ka, kb) at byte ka * eb -- through 64 x 64 LDS tiles
+// (loads along kb, stores along ka).  Workgroup 0 writes flags[0] = eb and flags[1] = 0 (no bf16
+// path for wide rows).
+__global__ __launch_bounds__(256) void prep_rows_wide_kernel(const uint32_t *__restrict__ lut, int m,
+                                                             const uint32_t *__restrict__ part, int nparts,
+                                                             unsigned char *__restrict__ dst, int *__restrict__ flags)
+{
+    __shared__ uint32_t tile[64][65];
+    __shared__ uint32_t s_low[4];
+    uint32_t low = 0u;
+    for (int i = threadIdx.x; i < nparts; i += 256) low |= part[i];
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) low |= uint32_t(__shfl_xor(int(low), o));
+    if ((threadIdx.x & 63) == 0) s_low[threadIdx.x >> 6] = low;
+    __syncthreads();
+    const uint32_t lb = s_low[0] | s_low[1] | s_low[2] | s_low[3];
+    const int eb = lb == 0u ? 1 : ((lb & 0xFFu) == 0u ? 2 : 4);
+    if (blockIdx.x == 0 && threadIdx.x == 0) {
+        flags[0] = eb;
+        flags[1] = 0;
+    }
+    const int n = 1 << m, tiles_1d = n / 64;
+    const int tx = threadIdx.x & 63, ty = threadIdx.x >> 6;
+    for (int t = blockIdx.x; t < tiles_1d * tiles_1d; t += gridDim.x) {
+        const int ka0 = (t / tiles_1d) * 64, kb0 = (t % tiles_1d) * 64;
+        for (int i = ty; i < 64; i += 4) tile[i][tx] = lut[size_t(ka0 + i) * n + kb0 + tx];  // [ka][kb]
+        __syncthreads();
+        for (int i = ty; i < 64; i += 4) {
+            const uint32_t e = tile[tx][i] & 0x00FFFFFFu;  // entry (ka0 + tx, kb0 + i)
+            unsigned char *row = dst + size_t(kb0 + i) * n * eb;
+            if (eb == 1)
+                row[ka0 + tx] = static_cast<unsigned char>(e >> 16);
+            else if (eb == 2)
+                reinterpret_cast<uint16_t *>(row)[ka0 + tx] = static_cast<uint16_t>(e >> 8);
+            else
+                reinterpret_cast<uint32_t *>(row)[ka0 + tx] = e + 0x3F800000u;
+        }
+        __syncthreads();
     }
 }
 
@@ -781,15 +748,28 @@ __device__ __forceinline__ void uniform_cursor(TabTap &cur, int &tap, int &c0)
     c0 = __builtin_amdgcn_readfirstlane(c0);
 }
 
+// Steps per slab of the exact path, rows of 2^RL entries of EB bytes, TNW columns: 8 KiB slabs of
+// 8 / EB steps for the 128-entry rows; wider rows (M = 8..11) take up to 32 KiB slabs of 1 to 8 steps
+// (the step loop is unrolled, so it stays short).
+constexpr int tab_slab_steps(int tnw, int rl, int eb)
+{
+    return rl == 7 ? 8 / eb
+                   : (32768 / (tnw * (1 << rl) * eb) < 1 ? 1
+                                                          : (32768 / (tnw * (1 << rl) * eb) > 8
+                                                                 ? 8
+                                                                 : 32768 / (tnw * (1 << rl) * eb)));
+}
+
 // Slab staging: each thread copies CPT 16-byte pieces of the rows selected by the second
 // operand's mantissas (kb) for slots [0, nslots) of a slab, and that operand's head (pb).
 // TNW = result columns of the workgroup.
-template <int TNW, int EB, int CPT, int NT>
+template <int TNW, int EB, int CPT, int NT, int RL>
 __device__ __forceinline__ void tab_fetch(u32x4 (&stage)[CPT], float (&stage_pb)[CPT], const TabTap &tp, int c0,
                                           const uint32_t *__restrict__ Bd, int Np, int col0,
                                           const unsigned char *__restrict__ rows)
 {
-    constexpr int ROWB = kTabRowEntries * EB;
+    constexpr int ROWB = (1 << RL) * EB;
+    constexpr uint32_t kPad = RL == 7 ? kZeroRowWord : 0u;  // a padding step's second operand: +0
     constexpr int PIECES = ROWB / 16;
 #pragma unroll
     for (int i = 0; i < CPT; ++i) {
@@ -798,18 +778,18 @@ __device__ __forceinline__ void tab_fetch(u32x4 (&stage)[CPT], float (&stage_pb)
         const int t = (c / PIECES) % TNW;
         const int piece = c % PIECES;
         const int j = c0 + slot;
-        const uint32_t bw = j < tp.count ? Bd[int64_t(tp.bbase + j) * Np + col0 + t] : kZeroRowWord;
+        const uint32_t bw = j < tp.count ? Bd[int64_t(tp.bbase + j) * Np + col0 + t] : kPad;
         stage_pb[i] = head_value(bw);
-        stage[i] = *reinterpret_cast<const u32x4 *>(rows + (bw & kIdxMask) * EB + piece * 16);  // idx = kb * 128
+        stage[i] = *reinterpret_cast<const u32x4 *>(rows + (bw & kIdxMask) * EB + piece * 16);  // idx = kb << RL
     }
 }
 
-template <int TNW, int EB, int CPT, int NT>
+template <int TNW, int EB, int CPT, int NT, int RL>
 __device__ __forceinline__ void tab_commit(const u32x4 (&stage)[CPT], const float (&stage_pb)[CPT],
                                            unsigned char *smem, float *pbs, int buf)
 {
-    constexpr int ROWB = kTabRowEntries * EB;
-    constexpr int KS = 8 / EB;
+    constexpr int ROWB = (1 << RL) * EB;
+    constexpr int KS = tab_slab_steps(TNW, RL, EB);
     constexpr int SLAB = KS * TNW * ROWB;
     constexpr int PIECES = ROWB / 16;
 #pragma unroll
@@ -822,14 +802,14 @@ __device__ __forceinline__ void tab_commit(const u32x4 (&stage)[CPT], const floa
 
 // Workgroup: NW waves as a WR x (NW/WR) grid -- WR row blocks of 64*TM rows, NW/WR column groups
 // of TN columns.  All waves share the LDS tables of the workgroup's TN * NW/WR columns.
-template <int OP, int TM, int TN, int WR, int EB, int NW>
+template <int OP, int TM, int TN, int WR, int EB, int NW, int RL>
 __device__ __forceinline__ void tab_body(const TabArgs &a)
 {
     constexpr int NT = 64 * NW;
     constexpr int WC = NW / WR;
     constexpr int TNW = TN * WC;                // result columns of the workgroup
-    constexpr int ROWB = kTabRowEntries * EB;
-    constexpr int KS = 8 / EB;                  // steps per slab: every slab is 8*TNW*128 bytes
+    constexpr int ROWB = (1 << RL) * EB;        // a table row: 2^RL entries
+    constexpr int KS = tab_slab_steps(TNW, RL, EB);
     constexpr int SLAB = KS * TNW * ROWB;
     constexpr int CPT = SLAB / 16 / NT;         // pieces per thread per slab
     static_assert(CPT * 16 * NT == SLAB, "slab must split evenly over the workgroup");
@@ -852,7 +832,6 @@ __device__ __forceinline__ void tab_body(const TabArgs &a)
         __builtin_amdgcn_make_buffer_rsrc(const_cast<uint32_t *>(a.A), 0, int(a.a_bytes), 0x00020000);
 
     uint32_t aoff[TM];  // byte offset of each lane row's first-operand run
-    int64_t obase[TM];
 #pragma unroll
     for (int r = 0; r < TM; ++r) {
         const int row = row0 + 64 * r;
@@ -860,7 +839,6 @@ __device__ __forceinline__ void tab_body(const TabArgs &a)
         int64_t ob = 0;
         if (row < R) tab_row<OP>(a, row, ab, ob);
         aoff[r] = uint32_t(ab) * 4u;
-        obase[r] = ob;
     }
     // this split's chunks, as positions p = tap * (8 * chunks per tap) + step
     const int count = tab_count<OP>(a);
@@ -880,8 +858,8 @@ __device__ __forceinline__ void tab_body(const TabArgs &a)
     bool have = q0 * 8 < p_end;
     if (have) {
         cur = tab_tap<OP>(a, tap);
-        tab_fetch<TNW, EB, CPT, NT>(stage, stage_pb, cur, c0, a.Bd, a.Np, colw, a.rows);
-        tab_commit<TNW, EB, CPT, NT>(stage, stage_pb, smem, pbs, 0);
+        tab_fetch<TNW, EB, CPT, NT, RL>(stage, stage_pb, cur, c0, a.Bd, a.Np, colw, a.rows);
+        tab_commit<TNW, EB, CPT, NT, RL>(stage, stage_pb, smem, pbs, 0);
 #pragma unroll
         for (int r = 0; r < TM; ++r)
             acur[r] = __builtin_amdgcn_raw_buffer_load_b32(
@@ -900,10 +878,11 @@ __device__ __forceinline__ void tab_body(const TabArgs &a)
         }
         const bool has_next = ntap * cpt * 8 + nc0 < p_end;
         if (has_next && ntap != tap) nxt = tab_tap<OP>(a, ntap);
-        if (has_next) tab_fetch<TNW, EB, CPT, NT>(stage, stage_pb, nxt, nc0, a.Bd, a.Np, colw, a.rows);
+        if (has_next) tab_fetch<TNW, EB, CPT, NT, RL>(stage, stage_pb, nxt, nc0, a.Bd, a.Np, colw, a.rows);
         const unsigned char *tb = smem + buf * SLAB + cg * TN * ROWB;
         const float *pb_s = pbs + buf * KS * TNW + cg * TN;
-        const int nslots = live ? min(KS, cur.count - c0) : 0;
+        // the slab ends at the tap's end or, 8-step chunks being the unit of splits, at the split's
+        const int nslots = live ? min(min(KS, cur.count - c0), p_end - (tap * cpt * 8 + c0)) : 0;
 #pragma unroll
         for (int slot = 0; slot < KS; ++slot) {
             if (slot >= nslots) break;
@@ -924,7 +903,7 @@ __device__ __forceinline__ void tab_body(const TabArgs &a)
             float pa[TM];
 #pragma unroll
             for (int r = 0; r < TM; ++r) {
-                vaddr[r] = tb + __builtin_amdgcn_ubfe(acur[r], 4, 7) * EB;  // idx = ka << 4
+                vaddr[r] = tb + __builtin_amdgcn_ubfe(acur[r], 4, RL) * EB;  // idx = ka << 4
                 pa[r] = head_value(acur[r]);
             }
 #pragma unroll
@@ -939,7 +918,7 @@ __device__ __forceinline__ void tab_body(const TabArgs &a)
 #pragma unroll
             for (int r = 0; r < TM; ++r) acur[r] = anext[r];
         }
-        if (has_next) tab_commit<TNW, EB, CPT, NT>(stage, stage_pb, smem, pbs, buf ^ 1);
+        if (has_next) tab_commit<TNW, EB, CPT, NT, RL>(stage, stage_pb, smem, pbs, buf ^ 1);
         __syncthreads();
         cur = nxt;
         tap = ntap;
@@ -954,7 +933,10 @@ __device__ __forceinline__ void tab_body(const TabArgs &a)
     for (int r = 0; r < TM; ++r) {
         const int row = row0 + 64 * r;
         if (row >= R) continue;
-        float *dst = out + obase[r];
+        int ab = 0;
+        int64_t ob = 0;
+        tab_row<OP>(a, row, ab, ob);  // the output offset, recomputed rather than kept in registers
+        float *dst = out + ob;
 #pragma unroll
         for (int t = 0; t < TN; ++t) {
             const int col = col0 + t;
@@ -1082,7 +1064,6 @@ __device__ __forceinline__ void tab_body_dot(const TabArgs &a)
         const_cast<unsigned char *>(a.dot_rows), 0, int((kZeroRow + 1) * kTabRowEntries), 0x00020000);
 
     uint32_t aoff[TM];
-    int64_t obase[TM];
 #pragma unroll
     for (int r = 0; r < TM; ++r) {
         const int row = row0 + 64 * r;
@@ -1090,7 +1071,6 @@ __device__ __forceinline__ void tab_body_dot(const TabArgs &a)
         int64_t ob = 0;
         if (row < R) tab_row<OP>(a, row, ab, ob);
         aoff[r] = uint32_t(ab) * 4u;
-        obase[r] = ob;
     }
     const int count = tab_count<OP>(a);
     const int cpt = (count + 7) / 8;
@@ -1231,7 +1211,10 @@ __device__ __forceinline__ void tab_body_dot(const TabArgs &a)
     for (int r = 0; r < TM; ++r) {
         const int row = row0 + 64 * r;
         if (row >= R) continue;
-        float *dst = out + obase[r];
+        int ab = 0;
+        int64_t ob = 0;
+        tab_row<OP>(a, row, ab, ob);  // the output offset, recomputed rather than kept in registers
+        float *dst = out + ob;
 #pragma unroll
         for (int t = 0; t < TN; ++t) {
             const int col = col0 + t;
@@ -1242,223 +1225,42 @@ __device__ __forceinline__ void tab_body_dot(const TabArgs &a)
 
 // Four waves per SIMD: the register budget (<= 128 VGPRs) the tiles are sized for.  Without the
 // hint the scheduler minimises registers and serialises the LDS gathers.
-template <int OP, int TM, int TN, int WR, int NW>
+// RL: log2 of the table row length, 7 (rows padded to 128 entries) for M <= 7, else M.
+template <int OP, int TM, int TN, int WR, int NW, int RL>
 __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(4, 4))) void tab_kernel(TabArgs a)
 {
     const int eb = __builtin_amdgcn_readfirstlane(a.eb[0]);
-    if constexpr (TN == kDotCols && WR == NW) {
+    if constexpr (RL == 7 && TN == kDotCols && WR == NW) {
         if (__builtin_amdgcn_readfirstlane(a.eb[1]) != 0) {
             tab_body_dot<OP, TM, NW>(a);
             return;
         }
     }
     if (eb == 1)
-        tab_body<OP, TM, TN, WR, 1, NW>(a);
+        tab_body<OP, TM, TN, WR, 1, NW, RL>(a);
     else if (eb == 2)
-        tab_body<OP, TM, TN, WR, 2, NW>(a);
+        tab_body<OP, TM, TN, WR, 2, NW, RL>(a);
     else
-        tab_body<OP, TM, TN, WR, 4, NW>(a);
+        tab_body<OP, TM, TN, WR, 4, NW, RL>(a);
 }
 
-// Dynamic LDS of a table kernel with TN columns per wave and WR waves along rows: two slabs of
-// 8*TNW*128 bytes plus the second-operand heads, or two bf16-path slabs where that path exists.
-constexpr size_t tab_lds_bytes(int tn, int wr, int nw)
+// Dynamic LDS of a table kernel with TN columns per wave, WR of its NW waves along rows and rows
+// of 2^RL entries: two exact-path slabs (the widest entry width) plus the second-operand heads, or
+// two bf16-path slabs where that path exists.
+constexpr size_t tab_exact_lds_bytes(int tnw, int rl, int eb)
+{
+    return size_t(2) * tab_slab_steps(tnw, rl, eb) * tnw * ((size_t(1) << rl) * eb) +
+           size_t(2) * tab_slab_steps(tnw, rl, eb) * tnw * 4;
+}
+
+constexpr size_t tab_lds_bytes(int tn, int wr, int nw, int rl)
 {
     const int tnw = tn * (nw / wr);
-    const size_t exact = size_t(2) * 8 * tnw * kTabRowEntries + size_t(2) * 8 * tnw * 4;
-    const size_t dot = (tn == kDotCols && wr == nw) ? size_t(2) * dot_slab_steps(nw) * kDotStepBytes : 0;
-    return exact > dot ? exact : dot;
-}
-
-// ------------------------------------------------------------------ convolution kernels --
-
-// Forward: rows (n, oh, ow) on lanes, columns co.  Xd: decoded x (NHWC, first-operand idx),
-// Wd: decoded w as [kh*kw*ci][COp].
-template <int TM, int TN, bool LDS>
-__global__ __launch_bounds__(kThreads) void conv_fwd_kernel(const uint32_t *__restrict__ Xd,
-                                                            const uint32_t *__restrict__ Wd, int COp, ConvShape s,
-                                                            float *__restrict__ y, const uint32_t *__restrict__ lut,
-                                                            int entries)
-{
-    stage_table<LDS>(lut, entries);
-    const int lane = threadIdx.x & 63;
-    const int rows = s.n * s.oh * s.ow;
-    const int row0 = blockIdx.x * (64 * TM) + lane;
-    const int col0 = (blockIdx.y * kWaves + wave_id()) * TN;
-    int xbase[TM], ih0[TM], iw0[TM];
-#pragma unroll
-    for (int r = 0; r < TM; ++r) {
-        const int row = row0 + 64 * r;
-        const int rr = row < rows ? row : rows - 1;
-        const int ow = rr % s.ow, oh = (rr / s.ow) % s.oh, n = rr / (s.ow * s.oh);
-        xbase[r] = n * s.h * s.w * s.ci;
-        ih0[r] = oh * s.sh - s.pt;
-        iw0[r] = ow * s.sw - s.pl;
-    }
-    float acc[TM][TN];
-    init_acc(acc);
-    if (col0 < COp) {
-        for (int kh = 0; kh < s.kh; ++kh) {
-            for (int kw = 0; kw < s.kw; ++kw) {
-                int pix[TM];
-#pragma unroll
-                for (int r = 0; r < TM; ++r) {
-                    const int ih = ih0[r] + kh, iw = iw0[r] + kw;
-                    const bool ok = unsigned(ih) < unsigned(s.h) && unsigned(iw) < unsigned(s.w);
-                    pix[r] = ok ? xbase[r] + (ih * s.w + iw) * s.ci : -1;
-                }
-                const uint32_t *brow = Wd + int64_t((kh * s.kw + kw) * s.ci) * COp + col0;
-                for (int c = 0; c < s.ci; ++c) {
-                    uint32_t aw[TM];
-#pragma unroll
-                    for (int r = 0; r < TM; ++r) aw[r] = pix[r] >= 0 ? Xd[pix[r] + c] : 0u;
-                    amsim_mac<TM, TN, LDS>(acc, aw, brow + int64_t(c) * COp, lut);
-                }
-            }
-        }
-    }
-#pragma unroll
-    for (int r = 0; r < TM; ++r) {
-        const int row = row0 + 64 * r;
-        if (row >= rows) continue;
-#pragma unroll
-        for (int t = 0; t < TN; ++t) {
-            const int col = col0 + t;
-            if (col < s.co) y[int64_t(row) * s.co + col] = acc[r][t];
-        }
-    }
-}
-
-// Backward-data, one stride phase (ph, pw) per blockIdx.z: rows (n, hq, wq) with
-// h = hq*sh + ph, w = wq*sw + pw on lanes, columns ci.  Only taps kh = ph + pt (mod sh) read a
-// real error element, at oh = hq + (ph + pt - kh) / sh (likewise w); the dilation zeros of
-// the other taps are never multiplied.  Dyd: decoded dy (NHWC), Wtd: decoded weights as
-// [kh][kw][co][CIp].
-template <int TM, int TN, bool LDS>
-__global__ __launch_bounds__(kThreads) void conv_bwd_data_kernel(const uint32_t *__restrict__ Dyd,
-                                                                 const uint32_t *__restrict__ Wtd, int CIp,
-                                                                 ConvShape s, float *__restrict__ dx,
-                                                                 const uint32_t *__restrict__ lut, int entries)
-{
-    stage_table<LDS>(lut, entries);
-    const int ph = blockIdx.z / s.sw, pw = blockIdx.z % s.sw;
-    const int hq_n = ph < s.h ? (s.h - ph + s.sh - 1) / s.sh : 0;
-    const int wq_n = pw < s.w ? (s.w - pw + s.sw - 1) / s.sw : 0;
-    const int rows = s.n * hq_n * wq_n;
-    if (int(blockIdx.x) * 64 * TM >= rows) return;  // uniform over the workgroup
-    const int lane = threadIdx.x & 63;
-    const int row0 = blockIdx.x * (64 * TM) + lane;
-    const int col0 = (blockIdx.y * kWaves + wave_id()) * TN;
-    int nb[TM], hq[TM], wq[TM];
-#pragma unroll
-    for (int r = 0; r < TM; ++r) {
-        const int row = row0 + 64 * r;
-        const int rr = row < rows ? row : rows - 1;
-        wq[r] = rr % wq_n;
-        hq[r] = (rr / wq_n) % hq_n;
-        nb[r] = rr / (wq_n * hq_n);
-    }
-    float acc[TM][TN];
-    init_acc(acc);
-    const int kh0 = (ph + s.pt) % s.sh, kw0 = (pw + s.pl) % s.sw;
-    if (col0 < CIp) {
-        for (int kh = kh0; kh < s.kh; kh += s.sh) {
-            const int dh = (ph + s.pt - kh) / s.sh;  // exact division
-            for (int kw = kw0; kw < s.kw; kw += s.sw) {
-                const int dw = (pw + s.pl - kw) / s.sw;
-                int pix[TM];
-#pragma unroll
-                for (int r = 0; r < TM; ++r) {
-                    const int oh = hq[r] + dh, ow = wq[r] + dw;
-                    const bool ok = unsigned(oh) < unsigned(s.oh) && unsigned(ow) < unsigned(s.ow);
-                    pix[r] = ok ? ((nb[r] * s.oh + oh) * s.ow + ow) * s.co : -1;
-                }
-                const uint32_t *brow = Wtd + int64_t((kh * s.kw + kw) * s.co) * CIp + col0;
-                for (int c = 0; c < s.co; ++c) {
-                    uint32_t aw[TM];
-#pragma unroll
-                    for (int r = 0; r < TM; ++r) aw[r] = pix[r] >= 0 ? Dyd[pix[r] + c] : 0u;
-                    amsim_mac<TM, TN, LDS>(acc, aw, brow + int64_t(c) * CIp, lut);
-                }
-            }
-        }
-    }
-#pragma unroll
-    for (int r = 0; r < TM; ++r) {
-        const int row = row0 + 64 * r;
-        if (row >= rows) continue;
-        const int h = hq[r] * s.sh + ph, w = wq[r] * s.sw + pw;
-        const int64_t base = (int64_t(nb[r] * s.h + h) * s.w + w) * s.ci;
-#pragma unroll
-        for (int t = 0; t < TN; ++t) {
-            const int col = col0 + t;
-            if (col < s.ci) dx[base + col] = acc[r][t];
-        }
-    }
-}
-
-// Backward-weight: rows (kh, kw, ci) on lanes, columns co, reduction over (n, oh, ow) split
-// into chunks of whole output rows (n, oh) across blockIdx.z.  Xd: decoded x (NHWC),
-// Dyd: decoded dy as [n*oh*ow][COp].  out: dw (split == 1) or the split's partial slab.
-template <int TM, int TN, bool LDS>
-__global__ __launch_bounds__(kThreads) void conv_bwd_weight_kernel(const uint32_t *__restrict__ Xd,
-                                                                   const uint32_t *__restrict__ Dyd, int COp,
-                                                                   ConvShape s, int rows_per_split,
-                                                                   float *__restrict__ out,
-                                                                   const uint32_t *__restrict__ lut, int entries)
-{
-    stage_table<LDS>(lut, entries);
-    const int lane = threadIdx.x & 63;
-    const int R = s.kh * s.kw * s.ci;
-    const int row0 = blockIdx.x * (64 * TM) + lane;
-    const int col0 = (blockIdx.y * kWaves + wave_id()) * TN;
-    int tkh[TM], tkw[TM], tci[TM];
-#pragma unroll
-    for (int r = 0; r < TM; ++r) {
-        const int row = row0 + 64 * r;
-        const int rr = row < R ? row : R - 1;
-        tci[r] = rr % s.ci;
-        tkw[r] = (rr / s.ci) % s.kw;
-        tkh[r] = rr / (s.ci * s.kw);
-    }
-    float acc[TM][TN];
-    init_acc(acc);
-    const int nrows = s.n * s.oh;  // (n, oh) output rows
-    const int rbeg = blockIdx.z * rows_per_split;
-    const int rend = min(nrows, rbeg + rows_per_split);
-    if (col0 < COp) {
-        for (int orow = rbeg; orow < rend; ++orow) {
-            const int n = orow / s.oh, oh = orow % s.oh;
-            int hbase[TM];
-#pragma unroll
-            for (int r = 0; r < TM; ++r) {
-                const int ih = oh * s.sh + tkh[r] - s.pt;
-                hbase[r] = unsigned(ih) < unsigned(s.h) ? (n * s.h + ih) * s.w : -1;
-            }
-            const uint32_t *brow = Dyd + int64_t(orow) * s.ow * COp + col0;
-            for (int ow = 0; ow < s.ow; ++ow) {
-                uint32_t aw[TM];
-#pragma unroll
-                for (int r = 0; r < TM; ++r) {
-                    const int iw = ow * s.sw + tkw[r] - s.pl;
-                    const bool ok = hbase[r] >= 0 && unsigned(iw) < unsigned(s.w);
-                    aw[r] = ok ? Xd[(hbase[r] + iw) * s.ci + tci[r]] : 0u;
-                }
-                amsim_mac<TM, TN, LDS>(acc, aw, brow + int64_t(ow) * COp, lut);
-            }
-        }
-    }
-    float *dst = out + int64_t(blockIdx.z) * R * s.co;
-#pragma unroll
-    for (int r = 0; r < TM; ++r) {
-        const int row = row0 + 64 * r;
-        if (row >= R) continue;
-#pragma unroll
-        for (int t = 0; t < TN; ++t) {
-            const int col = col0 + t;
-            if (col < s.co) dst[int64_t(row) * s.co + col] = acc[r][t];
-        }
-    }
+    size_t b = tab_exact_lds_bytes(tnw, rl, 1);
+    b = tab_exact_lds_bytes(tnw, rl, 2) > b ? tab_exact_lds_bytes(tnw, rl, 2) : b;
+    b = tab_exact_lds_bytes(tnw, rl, 4) > b ? tab_exact_lds_bytes(tnw, rl, 4) : b;
+    const size_t dot = (rl == 7 && tn == kDotCols && wr == nw) ? size_t(2) * dot_slab_steps(nw) * kDotStepBytes : 0;
+    return b > dot ? b : dot;
 }
 
 // ------------------------------------------------------------------ host dispatch -------
@@ -1469,7 +1271,8 @@ inline size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
 inline int64_t round_up(int64_t x, int64_t m) { return (x + m - 1) / m * m; }
 inline int64_t ceil_div(int64_t x, int64_t m) { return (x + m - 1) / m; }
 
-inline bool lds_path(int m_bits) { return m_bits <= kMaxLdsBits; }
+// log2 of the table row length: rows are padded to 128 entries for M <= 7.
+inline int row_log(int m_bits) { return m_bits > 7 ? m_bits : 7; }
 
 struct Tile {
     int tm, tn, split;
@@ -1478,32 +1281,6 @@ struct Tile {
 };
 
 constexpr int kTargetWgs = 512;  // 256 CUs x 2 workgroups
-
-// Global-table kernels (M = 8..11): TN = 16 uniform columns per wave for wide outputs, 4 for
-// narrow ones; TM the largest of 8/4/2/1 that still gives two workgroups per CU; split the
-// reduction when the tile grid is too small to fill the chip and the reduction is long.
-Tile choose_tile(int64_t rows, int64_t cols, int64_t red, int64_t red_unit, bool allow_split)
-{
-    Tile t;
-    t.tn = cols > 8 ? 16 : 4;
-    const int64_t col_tiles = ceil_div(cols, int64_t(t.tn) * kWaves);
-    t.tm = 1;
-    for (int tm : {8, 4, 2}) {
-        if (ceil_div(rows, 64 * tm) * col_tiles >= kTargetWgs) {
-            t.tm = tm;
-            break;
-        }
-    }
-    t.split = 1;
-    if (allow_split) {
-        const int64_t tiles = ceil_div(rows, 64 * t.tm) * col_tiles;
-        // keep at least ~1024 products per lane per split
-        const int64_t max_split = std::max<int64_t>(1, red / std::max<int64_t>(1, 1024 / std::max<int64_t>(1, red_unit)));
-        if (tiles < kTargetWgs) t.split = int(std::min<int64_t>(ceil_div(kTargetWgs, tiles), max_split));
-        t.split = std::max(1, std::min(t.split, 1024));
-    }
-    return t;
-}
 
 // Per-column-table kernels (M <= 7).  Candidates are the instantiated (TM, TN, WR, NW) tiles; the
 // choice minimises an estimate of issue time: padded work x cost per product, scaled up when the
@@ -1522,13 +1299,21 @@ struct TabCand {
 constexpr TabCand kTabCands[] = {{4, 8, 8, 8}, {4, 8, 4, 4}, {3, 8, 4, 4}, {2, 8, 4, 4}, {1, 8, 4, 4},
                                  {4, 4, 4, 4}, {2, 4, 4, 4}, {1, 4, 4, 4}, {4, 8, 2, 4}, {2, 8, 2, 4},
                                  {1, 8, 2, 4}, {2, 8, 1, 4}, {1, 8, 1, 4}};
+// Wide rows (M = 8..10; 11 uses the 4-column tiles, whose 4-byte-entry slab of one step fits 32 KiB).
+constexpr TabCand kWideCands[] = {{8, 4, 8, 8}, {4, 8, 8, 8}, {2, 8, 4, 4}, {1, 8, 4, 4}, {1, 4, 4, 4}};
+constexpr TabCand kWide11Cands[] = {{8, 4, 8, 8}, {4, 4, 8, 8}, {2, 4, 4, 4}, {1, 4, 4, 4}};
 
-Tile choose_tab_tile(int64_t rows, int64_t cols, int64_t red, int64_t min_steps, bool allow_split)
+Tile choose_tab_tile(int64_t rows, int64_t cols, int64_t red, int64_t min_steps, bool allow_split, int rl,
+                     int max_tm)
 {
     constexpr int64_t kTargetWaves = int64_t(kTargetWgs) * kWaves;
     Tile best{};
     double best_cost = 0.0;
-    for (const TabCand &c : kTabCands) {
+    const TabCand *cands = rl == 7 ? kTabCands : (rl < 11 ? kWideCands : kWide11Cands);
+    const size_t ncands = rl == 7 ? std::size(kTabCands) : (rl < 11 ? std::size(kWideCands) : std::size(kWide11Cands));
+    for (size_t ci = 0; ci < ncands; ++ci) {
+        const TabCand &c = cands[ci];
+        if (c.tm > max_tm) continue;
         // Waves whose rows all lie past the end skip the work: count the waves that have rows.
         const int64_t wrows = int64_t(64) * c.tm;  // rows per wave
         const int64_t rtile = wrows * c.wr;
@@ -1542,9 +1327,12 @@ Tile choose_tab_tile(int64_t rows, int64_t cols, int64_t red, int64_t min_steps,
             split = int(std::min<int64_t>(std::min<int64_t>(ceil_div(kTargetWaves, live_waves), max_split), 1024));
         }
         const double work = double(ceil_div(rows, wrows) * wrows) * double(col_tiles * ctile);
-        const bool pair = c.tn == kDotCols && c.wr == c.nw;
+        const bool pair = rl == 7 && c.tn == kDotCols && c.wr == c.nw;
+        // staging bytes per product grow with the row length (2^rl entries; wide rows are priced
+        // at 2-byte entries)
         const double per_product =
-            (pair ? 1.2 : 3.0) + 2.5 / c.tn + 4.0 / (c.tm * c.tn) + 512.0 / double(live_rows) * (pair ? 0.5 : 1.0);
+            (pair ? 1.2 : 3.0) + 2.5 / c.tn + 4.0 / (c.tm * c.tn) +
+            512.0 * double(1 << (rl - 7)) / double(live_rows) * (pair ? 0.5 : (rl == 7 ? 1.0 : 2.0));
         const double fill = std::min(1.0, double(live_waves * split) / kTargetWaves);
         const double cost = work * per_product / fill;
         if (best_cost == 0.0 || cost < best_cost * 0.999) {
@@ -1573,18 +1361,22 @@ void allow_lds(K kernel, size_t bytes)
     if (e != hipSuccess) g_attr_err = e;
 }
 
-#define AMSIM_FOR_TAB_TILES(X)                                                                               \
-    X(4, 8, 8, 8) X(4, 8, 4, 4) X(3, 8, 4, 4) X(2, 8, 4, 4) X(1, 8, 4, 4) X(4, 4, 4, 4) X(2, 4, 4, 4) X(1, 4, 4, 4) \
-    X(4, 8, 2, 4) X(2, 8, 2, 4) X(1, 8, 2, 4) X(2, 8, 1, 4) X(1, 8, 1, 4)
-#define AMSIM_FOR_TILES(X) X(8, 16) X(4, 16) X(2, 16) X(1, 16) X(8, 4) X(4, 4) X(2, 4) X(1, 4)
+// The instantiated (TM, TN, WR, NW, RL) tiles: every candidate of the chooser above.
+#define AMSIM_FOR_TAB_TILES(X)                                                                                \
+    X(4, 8, 8, 8, 7) X(4, 8, 4, 4, 7) X(3, 8, 4, 4, 7) X(2, 8, 4, 4, 7) X(1, 8, 4, 4, 7) X(4, 4, 4, 4, 7)          \
+    X(2, 4, 4, 4, 7) X(1, 4, 4, 4, 7) X(4, 8, 2, 4, 7) X(2, 8, 2, 4, 7) X(1, 8, 2, 4, 7) X(2, 8, 1, 4, 7)          \
+    X(1, 8, 1, 4, 7) AMSIM_WIDE_TILES(X, 8) AMSIM_WIDE_TILES(X, 9) AMSIM_WIDE_TILES(X, 10) X(8, 4, 8, 8, 11)     \
+    X(4, 4, 8, 8, 11) X(2, 4, 4, 4, 11) X(1, 4, 4, 4, 11)
+#define AMSIM_WIDE_TILES(X, RL)                                                                                \
+    X(8, 4, 8, 8, RL) X(4, 8, 8, 8, RL) X(2, 8, 4, 4, RL) X(1, 8, 4, 4, RL) X(1, 4, 4, 4, RL)
 
 void set_attributes()
 {
-#define X(TM, TN, WR, NW)                                                                  \
-    allow_lds(tab_kernel<OP_GEMM, TM, TN, WR, NW>, tab_lds_bytes(TN, WR, NW));           \
-    allow_lds(tab_kernel<OP_FWD, TM, TN, WR, NW>, tab_lds_bytes(TN, WR, NW));            \
-    allow_lds(tab_kernel<OP_BWD_DATA, TM, TN, WR, NW>, tab_lds_bytes(TN, WR, NW));       \
-    allow_lds(tab_kernel<OP_BWD_WEIGHT, TM, TN, WR, NW>, tab_lds_bytes(TN, WR, NW));
+#define X(TM, TN, WR, NW, RL)                                                                  \
+    allow_lds(tab_kernel<OP_GEMM, TM, TN, WR, NW, RL>, tab_lds_bytes(TN, WR, NW, RL));       \
+    allow_lds(tab_kernel<OP_FWD, TM, TN, WR, NW, RL>, tab_lds_bytes(TN, WR, NW, RL));        \
+    allow_lds(tab_kernel<OP_BWD_DATA, TM, TN, WR, NW, RL>, tab_lds_bytes(TN, WR, NW, RL));   \
+    allow_lds(tab_kernel<OP_BWD_WEIGHT, TM, TN, WR, NW, RL>, tab_lds_bytes(TN, WR, NW, RL));
     AMSIM_FOR_TAB_TILES(X)
 #undef X
 }
@@ -1615,48 +1407,35 @@ inline int decode_vec(const float *src, int64_t sb, int64_t sr, int64_t sc)
 }
 
 template <typename F>
-void dispatch_tab_tile(const Tile &t, F &&f)
+void dispatch_tab_tile(const Tile &t, int rl, F &&f)
 {
-#define X(TM, TN, WR, NW)                                                                 \
-    if (t.tm == TM && t.tn == TN && t.wr == WR && t.nw == NW) {                           \
+#define X(TM, TN, WR, NW, RL)                                                             \
+    if (t.tm == TM && t.tn == TN && t.wr == WR && t.nw == NW && rl == RL) {               \
         f(std::integral_constant<int, TM>{}, std::integral_constant<int, TN>{},           \
-          std::integral_constant<int, WR>{}, std::integral_constant<int, NW>{});          \
+          std::integral_constant<int, WR>{}, std::integral_constant<int, NW>{},           \
+          std::integral_constant<int, RL>{});                                             \
         return;                                                                           \
     }
     AMSIM_FOR_TAB_TILES(X)
 #undef X
 }
 
-template <typename F>
-void dispatch_tile(const Tile &t, F &&f)
-{
-#define X(TM, TN)                                                                \
-    if (t.tm == TM && t.tn == TN) {                                              \
-        f(std::integral_constant<int, TM>{}, std::integral_constant<int, TN>{}); \
-        return;                                                                  \
-    }
-    AMSIM_FOR_TILES(X)
-#undef X
-}
 
-constexpr size_t kRowsBytes = size_t(kZeroRow + 1) * kTabRowEntries * 4;  // widest transposed table
-
-// Workspace layout shared by the size queries and the launches.
-//   table path: [transposed rows][entry-width word][first operand][second operand][partials]
-//   global path:                                   [first operand][second operand][partials]
+// Workspace layout shared by the size queries and the launches:
+//   [transposed rows][bf16-path rows][flags][statistics][first operand][second operand][partials]
 struct Plan {
     Tile tile;
-    bool lds;
+    int rl;  // log2 of the table row length
     size_t off_rows, off_dot_rows, off_eb, off_stats, off_a, off_b, off_part, total;
     int64_t a_ld, b_ld;   // GEMM: padded leading dims of the decoded operands; conv: b_ld only
     int64_t a_elems;      // conv: elements of the decoded first operand
-    int splits, per_split;  // global path: steps (GEMM) or output rows (bwd_weight) per split
-    int chunks_per_split;   // table path: 8-step reduction chunks per split
+    int splits;           // reduction splits
+    int chunks_per_split;   // 8-step reduction chunks per split
     int64_t out_elems;      // elements of the result (partial sums hold splits of them)
     int Hp, Wp, OHp, OWp, pad_oh, pad_ow;
 };
 
-// Table path split of a reduction of q chunks (8 steps each).
+// Split of a reduction of q chunks (8 steps each).
 void plan_tab_split(Plan &p, int64_t q)
 {
     p.chunks_per_split = int(std::max<int64_t>(1, ceil_div(q, p.tile.split)));
@@ -1665,14 +1444,17 @@ void plan_tab_split(Plan &p, int64_t q)
 
 bool valid_m(int m_bits) { return m_bits >= 1 && m_bits <= 11; }
 
-// Table path: transposed rows, bf16-path rows, flags, decode statistics (two operands).
+// Transposed rows (the widest entry width, plus the zero row for 128-entry rows), bf16-path rows,
+// flags, decode statistics (two operands; for wide rows the table-preparation partials).
 constexpr size_t kDotRowsBytes = size_t(kZeroRow + 1) * kTabRowEntries;
 constexpr size_t kStatsBytes = size_t(2) * kStatSlots * 4;
+
+inline size_t rows_bytes(int rl) { return (size_t(1) << rl) * ((size_t(1) << rl) + (rl == 7 ? 1 : 0)) * 4; }
 
 size_t table_area(Plan &p, size_t o)
 {
     p.off_rows = o;
-    p.off_dot_rows = p.off_rows + align_up(kRowsBytes);
+    p.off_dot_rows = p.off_rows + align_up(rows_bytes(p.rl));
     p.off_eb = p.off_dot_rows + align_up(kDotRowsBytes);
     p.off_stats = p.off_eb + kAlign;
     return p.off_stats + align_up(kStatsBytes);
@@ -1681,27 +1463,16 @@ size_t table_area(Plan &p, size_t o)
 Plan plan_gemm(int64_t m, int64_t n, int64_t k, int m_bits)
 {
     Plan p{};
-    p.lds = lds_path(m_bits);
-    size_t o = 0;
-    if (p.lds) {
-        p.tile = choose_tab_tile(m, n, ceil_div(k, 8), 32, true);
-        p.a_ld = round_up(m, int64_t(64) * p.tile.wr * p.tile.tm);
-        p.b_ld = round_up(n, tab_cols(p.tile));
-        plan_tab_split(p, ceil_div(k, 8));
-        o = table_area(p, o);
-    } else {
-        p.tile = choose_tile(m, n, k, 1, true);
-        p.a_ld = round_up(m, 64 * p.tile.tm);
-        p.b_ld = round_up(n, int64_t(p.tile.tn) * kWaves);
-    }
+    p.rl = row_log(m_bits);
+    p.tile = choose_tab_tile(m, n, ceil_div(k, 8), 32, true, p.rl, 8);
+    p.a_ld = round_up(m, int64_t(64) * p.tile.wr * p.tile.tm);
+    p.b_ld = round_up(n, tab_cols(p.tile));
+    plan_tab_split(p, ceil_div(k, 8));
+    size_t o = table_area(p, 0);
     p.off_a = o;
     o += align_up(size_t(k) * p.a_ld * 4);
     p.off_b = o;
     o += align_up(size_t(k) * p.b_ld * 4);
-    if (!p.lds) {
-        p.per_split = int(ceil_div(k, p.tile.split));
-        p.splits = int(ceil_div(k, p.per_split));
-    }
     p.out_elems = m * n;
     p.off_part = o;
     if (p.splits > 1) o += align_up(size_t(p.splits) * m * n * 4);
@@ -1775,19 +1546,17 @@ Plan plan_conv(const amsim_conv2d *d, int pass, int m_bits)
 {
     const ConvShape s = shape_of(d);
     Plan p{};
-    p.lds = lds_path(m_bits);
-    size_t o = 0;
-    if (p.lds) o = table_area(p, o);
+    p.rl = row_log(m_bits);
+    size_t o = table_area(p, 0);
     const int64_t npix_in = int64_t(s.n) * s.h * s.w, npix_out = int64_t(s.n) * s.oh * s.ow;
     p.Hp = d->h + d->pad_top + d->pad_bottom;
     p.Wp = d->w + d->pad_left + d->pad_right;
-    p.splits = 1;
     if (pass == AMSIM_CONV_FWD) {
         const int64_t q = int64_t(s.kh) * s.kw * ceil_div(s.ci, 8);
-        p.tile = p.lds ? choose_tab_tile(npix_out, s.co, q, 16, true) : choose_tile(npix_out, s.co, 1, 1, false);
-        if (p.lds) plan_tab_split(p, q);
-        p.b_ld = p.lds ? round_up(s.co, tab_cols(p.tile)) : round_up(s.co, int64_t(p.tile.tn) * kWaves);
-        p.a_elems = p.lds ? int64_t(s.n) * p.Hp * p.Wp * s.ci : npix_in * s.ci;  // decoded x
+        p.tile = choose_tab_tile(npix_out, s.co, q, 16, true, p.rl, 8);
+        plan_tab_split(p, q);
+        p.b_ld = round_up(s.co, tab_cols(p.tile));
+        p.a_elems = int64_t(s.n) * p.Hp * p.Wp * s.ci;  // decoded, zero-bordered x
         p.out_elems = npix_out * s.co;
         p.off_a = o;
         o += align_up(size_t(p.a_elems) * 4);
@@ -1796,20 +1565,16 @@ Plan plan_conv(const amsim_conv2d *d, int pass, int m_bits)
     } else if (pass == AMSIM_CONV_BWD_DATA) {
         const int64_t rows = bwd_data_rows(s);
         const int64_t q = ceil_div(s.kh, s.sh) * ceil_div(s.kw, s.sw) * ceil_div(s.co, 8);  // largest phase
-        p.tile = p.lds ? choose_tab_tile(rows, s.ci, q, 16, true) : choose_tile(rows, s.ci, 1, 1, false);
-        if (p.lds) plan_tab_split(p, q);
-        p.b_ld = p.lds ? round_up(s.ci, tab_cols(p.tile)) : round_up(s.ci, int64_t(p.tile.tn) * kWaves);
-        if (p.lds) {
-            int top, bottom, left, right;
-            bwd_data_dy_pads(s, top, bottom, left, right);
-            p.pad_oh = top;
-            p.pad_ow = left;
-            p.OHp = top + s.oh + bottom;
-            p.OWp = left + s.ow + right;
-            p.a_elems = int64_t(s.n) * p.OHp * p.OWp * s.co;  // decoded, zero-padded dy
-        } else {
-            p.a_elems = npix_out * s.co;
-        }
+        p.tile = choose_tab_tile(rows, s.ci, q, 16, true, p.rl, 4);  // 8-row tiles spill here
+        plan_tab_split(p, q);
+        p.b_ld = round_up(s.ci, tab_cols(p.tile));
+        int top, bottom, left, right;
+        bwd_data_dy_pads(s, top, bottom, left, right);
+        p.pad_oh = top;
+        p.pad_ow = left;
+        p.OHp = top + s.oh + bottom;
+        p.OWp = left + s.ow + right;
+        p.a_elems = int64_t(s.n) * p.OHp * p.OWp * s.co;  // decoded, zero-padded dy
         p.out_elems = npix_in * s.ci;
         p.off_a = o;
         o += align_up(size_t(p.a_elems) * 4);
@@ -1817,22 +1582,13 @@ Plan plan_conv(const amsim_conv2d *d, int pass, int m_bits)
         o += align_up(size_t(s.kh) * s.kw * s.co * p.b_ld * 4);
     } else {
         const int64_t R = int64_t(s.kh) * s.kw * s.ci;
-        const int64_t taps = int64_t(s.n) * s.oh;
-        if (p.lds) {
-            const int64_t q = taps * ceil_div(s.ow, 8);
-            p.tile = choose_tab_tile(R, s.co, q, 16, true);
-            plan_tab_split(p, q);
-            p.b_ld = round_up(s.co, tab_cols(p.tile));
-            p.a_elems = int64_t(s.n) * p.Hp * p.Wp * s.ci;
-        } else {
-            p.tile = choose_tile(R, s.co, taps, s.ow, true);
-            p.b_ld = round_up(s.co, int64_t(p.tile.tn) * kWaves);
-            p.a_elems = npix_in * s.ci;
-            p.per_split = int(ceil_div(taps, p.tile.split));
-            p.splits = int(ceil_div(taps, p.per_split));
-        }
+        const int64_t q = int64_t(s.n) * s.oh * ceil_div(s.ow, 8);
+        p.tile = choose_tab_tile(R, s.co, q, 16, true, p.rl, 8);
+        plan_tab_split(p, q);
+        p.b_ld = round_up(s.co, tab_cols(p.tile));
+        p.a_elems = int64_t(s.n) * p.Hp * p.Wp * s.ci;
         p.out_elems = R * s.co;
-        p.off_a = o;  // decoded x
+        p.off_a = o;  // decoded, zero-bordered x
         o += align_up(size_t(p.a_elems) * 4);
         p.off_b = o;  // decoded dy [n*oh*ow][COp]
         o += align_up(size_t(npix_out) * p.b_ld * 4);
@@ -1843,44 +1599,57 @@ Plan plan_conv(const amsim_conv2d *d, int pass, int m_bits)
     return p;
 }
 
-// Decoded-index shift of each operand.  Table path: the first operand's mantissa times 16 (the
-// bf16 path's entry size; the exact path extracts it), the second's times 128 (its row offset in
-// a table of 1-byte entries), zeros of the second operand on the zero row.  Global path: entry
-// index into the canonical table, ka * 2^M + kb.
-inline int shift_first(int m_bits) { return lds_path(m_bits) ? 4 : m_bits; }
-inline int shift_second(int m_bits) { return lds_path(m_bits) ? 7 : 0; }
-inline uint32_t zidx_second(const Plan &p) { return p.lds ? kZeroRowWord : 0u; }
+// Decoded-index fields: the first operand's mantissa times 16 (the bf16 path's entry size; the
+// exact path extracts it), the second's times the row length (its row offset in entries); zeros
+// of the second operand on the zero row where rows have 128 entries (any row serves on the exact
+// path, the zero head making the product a signed zero).
+inline int shift_first(int) { return 4; }
+inline int shift_second(int m_bits) { return row_log(m_bits); }
+inline uint32_t zidx_second(const Plan &p) { return p.rl == 7 ? kZeroRowWord : 0u; }
 
-// Decode statistics of the table path: kStatSlots words per operand (null on the global path).
+// Decode statistics for the bf16 path's exponent window: kStatSlots words per operand (null for
+// wide rows, which have no bf16 path).
 inline uint32_t *stats_a(char *ws, const Plan &p)
 {
-    return p.lds ? reinterpret_cast<uint32_t *>(ws + p.off_stats) : nullptr;
+    return p.rl == 7 ? reinterpret_cast<uint32_t *>(ws + p.off_stats) : nullptr;
 }
 inline uint32_t *stats_b(char *ws, const Plan &p)
 {
-    return p.lds ? reinterpret_cast<uint32_t *>(ws + p.off_stats) + kStatSlots : nullptr;
+    return p.rl == 7 ? reinterpret_cast<uint32_t *>(ws + p.off_stats) + kStatSlots : nullptr;
 }
 
-// Launches the table preparation for the table path, after both decode passes (rows, flags and
-// the reduction of the n_a / n_b statistics words into the workspace).
+// Launches the table preparation after both decode passes: rows, flags and (128-entry rows) the
+// reduction of the n_a / n_b statistics words.  Wide rows: a low-bits pass over the table, then the
+// transposed rows.
 int prep_rows(const uint32_t *lut, int m_bits, char *ws, const Plan &p, int n_a, int n_b, hipStream_t st)
 {
-    hipLaunchKernelGGL(prep_rows_kernel, dim3(1), dim3(1024), 0, st, lut, m_bits,
-                       reinterpret_cast<unsigned char *>(ws + p.off_rows),
-                       reinterpret_cast<unsigned char *>(ws + p.off_dot_rows), stats_a(ws, p), n_a, stats_b(ws, p), n_b,
-                       reinterpret_cast<int *>(ws + p.off_eb));
+    if (p.rl == 7) {
+        hipLaunchKernelGGL(prep_rows_kernel, dim3(1), dim3(1024), 0, st, lut, m_bits,
+                           reinterpret_cast<unsigned char *>(ws + p.off_rows),
+                           reinterpret_cast<unsigned char *>(ws + p.off_dot_rows), stats_a(ws, p), n_a,
+                           stats_b(ws, p), n_b, reinterpret_cast<int *>(ws + p.off_eb));
+        return launch_status();
+    }
+    const int total = 1 << (2 * m_bits);
+    const int nparts = int(std::min<int64_t>(ceil_div(total, 256 * 16), 1024));
+    uint32_t *part = reinterpret_cast<uint32_t *>(ws + p.off_stats);
+    hipLaunchKernelGGL(lut_low_bits_kernel, dim3(nparts), dim3(256), 0, st, lut, total, part);
+    const int tiles = (1 << (m_bits - 6)) * (1 << (m_bits - 6));
+    hipLaunchKernelGGL(prep_rows_wide_kernel, dim3(std::min(tiles, 2048)), dim3(256), 0, st, lut, m_bits, part,
+                       nparts, reinterpret_cast<unsigned char *>(ws + p.off_rows), reinterpret_cast<int *>(ws + p.off_eb));
     return launch_status();
 }
 
 template <int OP>
 int launch_tab(const Plan &p, const TabArgs &a, dim3 grid, hipStream_t st)
 {
-    auto run = [&](auto tm, auto tn, auto wr, auto nw) {
+    auto run = [&](auto tm, auto tn, auto wr, auto nw, auto rl) {
         constexpr int TM = decltype(tm)::value, TN = decltype(tn)::value, WR = decltype(wr)::value;
-        constexpr int NW = decltype(nw)::value;
-        hipLaunchKernelGGL((tab_kernel<OP, TM, TN, WR, NW>), grid, dim3(64 * NW), tab_lds_bytes(TN, WR, NW), st, a);
+        constexpr int NW = decltype(nw)::value, RL = decltype(rl)::value;
+        hipLaunchKernelGGL((tab_kernel<OP, TM, TN, WR, NW, RL>), grid, dim3(64 * NW), tab_lds_bytes(TN, WR, NW, RL),
+                           st, a);
     };
-    dispatch_tab_tile(p.tile, run);
+    dispatch_tab_tile(p.tile, p.rl, run);
     return launch_status();
 }
 
@@ -1904,7 +1673,7 @@ TabArgs tab_args(const Plan &p, char *ws, const uint32_t *A, int64_t a_elems, co
     a.OWp = p.OWp;
     a.pad_oh = p.pad_oh;
     a.pad_ow = p.pad_ow;
-    a.splits = p.lds ? p.splits : 1;
+    a.splits = p.splits;
     a.chunks_per_split = p.chunks_per_split;
     a.out_elems = p.out_elems;
     return a;
@@ -2005,10 +1774,10 @@ int approx_gemm(int trans_a, int trans_b, int64_t m, int64_t n, int64_t k, const
     const Plan p = plan_gemm(m, n, k, m_bits);
     // decoded operands are addressed with 32-bit byte offsets
     if (k * p.a_ld >= (int64_t(1) << 29) || k * p.b_ld >= lim || int64_t(p.splits) * m * n >= lim ||
-        p.b_ld / (p.lds ? tab_cols(p.tile) : int64_t(p.tile.tn) * kWaves) > 65535)
+        p.b_ld / tab_cols(p.tile) > 65535)
         return AMSIM_ERR_UNSUPPORTED;
     if (p.total > 0 && (!workspace || workspace_bytes < p.total)) return AMSIM_ERR_WORKSPACE;
-    if (p.lds && ensure_attributes() != AMSIM_OK) return AMSIM_ERR_HIP;
+    if (ensure_attributes() != AMSIM_OK) return AMSIM_ERR_HIP;
     char *ws = static_cast<char *>(workspace);
     uint32_t *Ad = reinterpret_cast<uint32_t *>(ws + p.off_a);
     uint32_t *Bd = reinterpret_cast<uint32_t *>(ws + p.off_b);
@@ -2026,10 +1795,9 @@ int approx_gemm(int trans_a, int trans_b, int64_t m, int64_t n, int64_t k, const
                        int(p.b_ld), m_bits, shift_second(m_bits), zidx_second(p), stats_b(ws, p),
                        decode_vec(B, 0, b_sr, b_sc));
     if (launch_status() != AMSIM_OK) return AMSIM_ERR_HIP;
-    if (p.lds && prep_rows(lut, m_bits, ws, p, int(grid_dt.x * grid_dt.y), grid_b, st) != AMSIM_OK)
-        return AMSIM_ERR_HIP;
+    if (prep_rows(lut, m_bits, ws, p, int(grid_dt.x * grid_dt.y), grid_b, st) != AMSIM_OK) return AMSIM_ERR_HIP;
     int rc;
-    if (p.lds) {
+    {
         TabArgs a = tab_args(p, ws, Ad, k * p.a_ld, Bd, out, int(m), int(n));
         a.ldc = p.splits > 1 ? n : ldc;  // partial sums are dense
         a.Mp = int(p.a_ld);
@@ -2037,16 +1805,6 @@ int approx_gemm(int trans_a, int trans_b, int64_t m, int64_t n, int64_t k, const
         dim3 grid(unsigned(p.a_ld / (int64_t(64) * t.wr * t.tm)), unsigned(p.b_ld / tab_cols(t)), unsigned(p.splits));
         TimedLaunch tl(AMSIM_KERNEL_GEMM, st);
         rc = launch_tab<OP_GEMM>(p, a, grid, st);
-    } else {
-        dim3 grid(unsigned(p.a_ld / (64 * t.tm)), unsigned(p.b_ld / (int64_t(t.tn) * kWaves)), unsigned(p.splits));
-        auto run = [&](auto tm, auto tn) {
-            constexpr int TM = decltype(tm)::value, TN = decltype(tn)::value;
-            hipLaunchKernelGGL((gemm_kernel<TM, TN, false>), grid, dim3(kThreads), 0, st, Ad, int(p.a_ld), Bd,
-                               int(p.b_ld), int(m), int(n), int(k), p.per_split, out, ldc, lut, 1 << (2 * m_bits));
-        };
-        TimedLaunch tl(AMSIM_KERNEL_GEMM, st);
-        dispatch_tile(t, run);
-        rc = launch_status();
     }
     if (rc != AMSIM_OK) return AMSIM_ERR_HIP;
     if (p.splits > 1) {
@@ -2077,7 +1835,7 @@ static int conv_common(const amsim_conv2d *desc, int pass, const void *in0, cons
     if (!in0 || !in1 || !out || !lut) return AMSIM_ERR_INVALID_ARG;
     *p = plan_conv(desc, pass, m_bits);
     if (p->total > 0 && (!workspace || workspace_bytes < p->total)) return AMSIM_ERR_WORKSPACE;
-    if (p->lds && ensure_attributes() != AMSIM_OK) return AMSIM_ERR_HIP;
+    if (ensure_attributes() != AMSIM_OK) return AMSIM_ERR_HIP;
     return AMSIM_OK;
 }
 
@@ -2113,45 +1871,29 @@ int approx_conv2d_fwd(const amsim_conv2d *desc, const float *x, const float *w, 
     char *ws = static_cast<char *>(workspace);
     uint32_t *Xd = reinterpret_cast<uint32_t *>(ws + p.off_a);
     uint32_t *Wd = reinterpret_cast<uint32_t *>(ws + p.off_b);
-    int n_a;
-    if (p.lds)
-        n_a = decode_nhcw(x, s.n, s.h, s.w, s.ci, s.pt, s.pl, p.Hp, p.Wp, Xd, m_bits, shift_first(m_bits),
-                          stats_a(ws, p), st);
-    else
-        n_a = decode_nhwc(x, s.n, s.h, s.w, s.ci, 0, 0, s.h, s.w, Xd, m_bits, shift_first(m_bits), nullptr, st);
+    const int n_a = decode_nhcw(x, s.n, s.h, s.w, s.ci, s.pt, s.pl, p.Hp, p.Wp, Xd, m_bits, shift_first(m_bits),
+                                stats_a(ws, p), st);
     const int kk = s.kh * s.kw * s.ci;
     const int n_b = decode_grid(int64_t(kk) * p.b_ld);
     hipLaunchKernelGGL(decode_kernel, dim3(n_b), dim3(256), 0, st, w, int64_t(0), int64_t(s.co), int64_t(1), 1, kk,
                        s.co, Wd, int(p.b_ld), m_bits, shift_second(m_bits), zidx_second(p), stats_b(ws, p),
                        decode_vec(w, 0, s.co, 1));
     if (launch_status() != AMSIM_OK) return AMSIM_ERR_HIP;
-    if (p.lds && prep_rows(lut, m_bits, ws, p, n_a, n_b, st) != AMSIM_OK) return AMSIM_ERR_HIP;
+    if (prep_rows(lut, m_bits, ws, p, n_a, n_b, st) != AMSIM_OK) return AMSIM_ERR_HIP;
     const Tile t = p.tile;
     const int64_t rows = int64_t(s.n) * s.oh * s.ow;
-    if (p.lds) {
-        float *out = p.splits > 1 ? reinterpret_cast<float *>(ws + p.off_part) : y;
-        TabArgs a = tab_args(p, ws, Xd, p.a_elems, Wd, out, int(rows), s.co);
-        a.s = s;
-        dim3 grid(unsigned(ceil_div(rows, int64_t(64) * t.wr * t.tm)), unsigned(p.b_ld / tab_cols(t)),
-                  unsigned(p.splits));
-        {
-            TimedLaunch tl(AMSIM_KERNEL_CONV_FWD, st);
-            rc = launch_tab<OP_FWD>(p, a, grid, st);
-        }
-        if (rc != AMSIM_OK || p.splits == 1) return rc;
-        hipLaunchKernelGGL(reduce_splits_kernel, dim3(grid_for(p.out_elems)), dim3(256), 0, st,
-                           reinterpret_cast<const float *>(ws + p.off_part), p.splits, int(rows), s.co, y,
-                           int64_t(s.co));
-        return launch_status();
+    float *out = p.splits > 1 ? reinterpret_cast<float *>(ws + p.off_part) : y;
+    TabArgs a = tab_args(p, ws, Xd, p.a_elems, Wd, out, int(rows), s.co);
+    a.s = s;
+    dim3 grid(unsigned(ceil_div(rows, int64_t(64) * t.wr * t.tm)), unsigned(p.b_ld / tab_cols(t)),
+              unsigned(p.splits));
+    {
+        TimedLaunch tl(AMSIM_KERNEL_CONV_FWD, st);
+        rc = launch_tab<OP_FWD>(p, a, grid, st);
     }
-    TimedLaunch tl(AMSIM_KERNEL_CONV_FWD, st);
-    dim3 grid(unsigned(ceil_div(rows, 64 * t.tm)), unsigned(p.b_ld / (int64_t(t.tn) * kWaves)), 1);
-    auto run = [&](auto tm, auto tn) {
-        constexpr int TM = decltype(tm)::value, TN = decltype(tn)::value;
-        hipLaunchKernelGGL((conv_fwd_kernel<TM, TN, false>), grid, dim3(kThreads), 0, st, Xd, Wd, int(p.b_ld), s, y,
-                           lut, 1 << (2 * m_bits));
-    };
-    dispatch_tile(t, run);
+    if (rc != AMSIM_OK || p.splits == 1) return rc;
+    hipLaunchKernelGGL(reduce_splits_kernel, dim3(grid_for(p.out_elems)), dim3(256), 0, st,
+                       reinterpret_cast<const float *>(ws + p.off_part), p.splits, int(rows), s.co, y, int64_t(s.co));
     return launch_status();
 }
 
@@ -2166,46 +1908,30 @@ int approx_conv2d_bwd_data(const amsim_conv2d *desc, const float *dy, const floa
     char *ws = static_cast<char *>(workspace);
     uint32_t *Dyd = reinterpret_cast<uint32_t *>(ws + p.off_a);
     uint32_t *Wtd = reinterpret_cast<uint32_t *>(ws + p.off_b);
-    int n_a;
-    if (p.lds)
-        n_a = decode_nhcw(dy, s.n, s.oh, s.ow, s.co, p.pad_oh, p.pad_ow, p.OHp, p.OWp, Dyd, m_bits, shift_first(m_bits),
-                          stats_a(ws, p), st);
-    else
-        n_a = decode_nhwc(dy, s.n, s.oh, s.ow, s.co, 0, 0, s.oh, s.ow, Dyd, m_bits, shift_first(m_bits), nullptr, st);
+    const int n_a = decode_nhcw(dy, s.n, s.oh, s.ow, s.co, p.pad_oh, p.pad_ow, p.OHp, p.OWp, Dyd, m_bits,
+                                shift_first(m_bits), stats_a(ws, p), st);
     // w[kh][kw][ci][co] -> Wt[kh][kw][co][ci]: batches (kh,kw), rows co, cols ci
     const int n_b = decode_grid(int64_t(s.kh) * s.kw * s.co * p.b_ld);
     hipLaunchKernelGGL(decode_kernel, dim3(n_b), dim3(256), 0, st, w, int64_t(s.ci) * s.co, int64_t(1), int64_t(s.co),
                        s.kh * s.kw, s.co, s.ci, Wtd, int(p.b_ld), m_bits, shift_second(m_bits), zidx_second(p),
                        stats_b(ws, p), 0);
     if (launch_status() != AMSIM_OK) return AMSIM_ERR_HIP;
-    if (p.lds && prep_rows(lut, m_bits, ws, p, n_a, n_b, st) != AMSIM_OK) return AMSIM_ERR_HIP;
+    if (prep_rows(lut, m_bits, ws, p, n_a, n_b, st) != AMSIM_OK) return AMSIM_ERR_HIP;
     const Tile t = p.tile;
     const int64_t rows = bwd_data_rows(s);
-    if (p.lds) {
-        float *out = p.splits > 1 ? reinterpret_cast<float *>(ws + p.off_part) : dx;
-        TabArgs a = tab_args(p, ws, Dyd, p.a_elems, Wtd, out, int(rows), s.ci);
-        a.s = s;
-        dim3 grid(unsigned(ceil_div(rows, int64_t(64) * t.wr * t.tm)), unsigned(p.b_ld / tab_cols(t)),
-                  unsigned(s.sh * s.sw * p.splits));
-        {
-            TimedLaunch tl(AMSIM_KERNEL_CONV_BWD_DATA, st);
-            rc = launch_tab<OP_BWD_DATA>(p, a, grid, st);
-        }
-        if (rc != AMSIM_OK || p.splits == 1) return rc;
-        hipLaunchKernelGGL(reduce_splits_kernel, dim3(grid_for(p.out_elems)), dim3(256), 0, st,
-                           reinterpret_cast<const float *>(ws + p.off_part), p.splits, s.n * s.h * s.w, s.ci, dx,
-                           int64_t(s.ci));
-        return launch_status();
+    float *out = p.splits > 1 ? reinterpret_cast<float *>(ws + p.off_part) : dx;
+    TabArgs a = tab_args(p, ws, Dyd, p.a_elems, Wtd, out, int(rows), s.ci);
+    a.s = s;
+    dim3 grid(unsigned(ceil_div(rows, int64_t(64) * t.wr * t.tm)), unsigned(p.b_ld / tab_cols(t)),
+              unsigned(s.sh * s.sw * p.splits));
+    {
+        TimedLaunch tl(AMSIM_KERNEL_CONV_BWD_DATA, st);
+        rc = launch_tab<OP_BWD_DATA>(p, a, grid, st);
     }
-    TimedLaunch tl(AMSIM_KERNEL_CONV_BWD_DATA, st);
-    dim3 grid(unsigned(ceil_div(rows, 64 * t.tm)), unsigned(p.b_ld / (int64_t(t.tn) * kWaves)),
-              unsigned(s.sh * s.sw));
-    auto run = [&](auto tm, auto tn) {
-        constexpr int TM = decltype(tm)::value, TN = decltype(tn)::value;
-        hipLaunchKernelGGL((conv_bwd_data_kernel<TM, TN, false>), grid, dim3(kThreads), 0, st, Dyd, Wtd,
-                           int(p.b_ld), s, dx, lut, 1 << (2 * m_bits));
-    };
-    dispatch_tile(t, run);
+    if (rc != AMSIM_OK || p.splits == 1) return rc;
+    hipLaunchKernelGGL(reduce_splits_kernel, dim3(grid_for(p.out_elems)), dim3(256), 0, st,
+                       reinterpret_cast<const float *>(ws + p.off_part), p.splits, s.n * s.h * s.w, s.ci, dx,
+                       int64_t(s.ci));
     return launch_status();
 }
 
@@ -2220,41 +1946,25 @@ int approx_conv2d_bwd_weight(const amsim_conv2d *desc, const float *x, const flo
     char *ws = static_cast<char *>(workspace);
     uint32_t *Xd = reinterpret_cast<uint32_t *>(ws + p.off_a);
     uint32_t *Dyd = reinterpret_cast<uint32_t *>(ws + p.off_b);
-    int n_a;
-    if (p.lds)
-        n_a = decode_nhwc(x, s.n, s.h, s.w, s.ci, s.pt, s.pl, p.Hp, p.Wp, Xd, m_bits, shift_first(m_bits),
-                          stats_a(ws, p), st);
-    else
-        n_a = decode_nhwc(x, s.n, s.h, s.w, s.ci, 0, 0, s.h, s.w, Xd, m_bits, shift_first(m_bits), nullptr, st);
+    const int n_a = decode_nhwc(x, s.n, s.h, s.w, s.ci, s.pt, s.pl, p.Hp, p.Wp, Xd, m_bits, shift_first(m_bits),
+                                stats_a(ws, p), st);
     const int64_t npo = int64_t(s.n) * s.oh * s.ow;
     const int n_b = decode_grid(npo * p.b_ld);
     hipLaunchKernelGGL(decode_kernel, dim3(n_b), dim3(256), 0, st, dy, int64_t(0), int64_t(s.co), int64_t(1), 1,
                        int(npo), s.co, Dyd, int(p.b_ld), m_bits, shift_second(m_bits), zidx_second(p), stats_b(ws, p),
                        decode_vec(dy, 0, s.co, 1));
     if (launch_status() != AMSIM_OK) return AMSIM_ERR_HIP;
-    if (p.lds && prep_rows(lut, m_bits, ws, p, n_a, n_b, st) != AMSIM_OK) return AMSIM_ERR_HIP;
+    if (prep_rows(lut, m_bits, ws, p, n_a, n_b, st) != AMSIM_OK) return AMSIM_ERR_HIP;
     const Tile t = p.tile;
     const int R = s.kh * s.kw * s.ci;
     float *out = p.splits > 1 ? reinterpret_cast<float *>(ws + p.off_part) : dw;
     {
         TimedLaunch tl(AMSIM_KERNEL_CONV_BWD_WEIGHT, st);
-        if (p.lds) {
-            TabArgs a = tab_args(p, ws, Xd, p.a_elems, Dyd, out, R, s.co);
-            a.s = s;
-            dim3 grid(unsigned(ceil_div(R, int64_t(64) * t.wr * t.tm)), unsigned(p.b_ld / tab_cols(t)),
-                      unsigned(p.splits));
-            rc = launch_tab<OP_BWD_WEIGHT>(p, a, grid, st);
-        } else {
-            dim3 grid(unsigned(ceil_div(R, 64 * t.tm)), unsigned(p.b_ld / (int64_t(t.tn) * kWaves)),
-                      unsigned(p.splits));
-            auto run = [&](auto tm, auto tn) {
-                constexpr int TM = decltype(tm)::value, TN = decltype(tn)::value;
-                hipLaunchKernelGGL((conv_bwd_weight_kernel<TM, TN, false>), grid, dim3(kThreads), 0, st, Xd, Dyd,
-                                   int(p.b_ld), s, p.per_split, out, lut, 1 << (2 * m_bits));
-            };
-            dispatch_tile(t, run);
-            rc = launch_status();
-        }
+        TabArgs a = tab_args(p, ws, Xd, p.a_elems, Dyd, out, R, s.co);
+        a.s = s;
+        dim3 grid(unsigned(ceil_div(R, int64_t(64) * t.wr * t.tm)), unsigned(p.b_ld / tab_cols(t)),
+                  unsigned(p.splits));
+        rc = launch_tab<OP_BWD_WEIGHT>(p, a, grid, st);
     }
     if (rc != AMSIM_OK) return AMSIM_ERR_HIP;
     if (p.splits > 1) {

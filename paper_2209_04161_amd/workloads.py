@@ -79,7 +79,7 @@ RESNET50_LAYERS = [
     dict(name="r50_1x1_1024to256_14", model=MITCHELL, m_bits=7, conv=conv_desc(32, 14, 14, 1024, 256, 1, 1, 1, 0)),
 ]
 
-# large approx GEMM 4096^3, normal(0,1), Mitchell with M=11 (global table) and M=7 (LDS table)
+# large approx GEMM 4096^3, normal(0,1), Mitchell with M=11 (2048-entry table rows) and M=7 (128-entry rows)
 GEMM_LARGE = dict(name="gemm_4096", model=MITCHELL, m_bits=11, M=4096, N=4096, K=4096)
 
 # LeNet-5 layer stack, batch 64, 1x28x28 in [0,1], exact bfloat16-truncation multiplier (M=7)
