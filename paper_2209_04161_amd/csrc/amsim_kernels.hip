@@ -41,6 +41,8 @@ constexpr int kWaves = 4;           // waves per workgroup (column groups)
 constexpr int kThreads = 64 * kWaves;
 
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x3 __attribute__((ext_vector_type(3)));  // buffer_load_dwordx3 results only
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 
 // ------------------------------------------------------------------ device helpers -------
 
@@ -284,11 +286,13 @@ __global__ __launch_bounds__(256) void decode_pad_nhcw_kernel(const float *__res
 
 // Tiled transpose-decode for the GEMM first operand: src is `rows x cols` with strides
 // (sr, sc); dst[c * dld + r] = decode(src(r, c)), rows padded to dld with decoded +0.
-// The grid strides over 64 x 64 tiles in both directions.
+// Pair records (records != null): records[(c / 2) * dld + r] = {index field of (r, c), head of
+// (r, c) | head of (r, c + 1) << 16 as bf16, index field of (r, c + 1)}, a column past the end
+// being a decoded +0.  The grid strides over 64 x 64 tiles in both directions.
 __global__ __launch_bounds__(256) void decode_t_kernel(const float *__restrict__ src, int64_t sr, int64_t sc, int rows,
                                                        int cols, uint32_t *__restrict__ dst, int dld, int m, int shift,
-                                                       uint32_t zidx,
-                                                       uint32_t *__restrict__ stats)
+                                                       uint32_t zidx, uint32_t *__restrict__ stats,
+                                                       uint32_t *__restrict__ records)
 {
     __shared__ uint32_t tile[64][65];
     const int tx = threadIdx.x & 63, ty = threadIdx.x >> 6;
@@ -307,9 +311,22 @@ __global__ __launch_bounds__(256) void decode_t_kernel(const float *__restrict__
                 tile[ty + 4 * i][tx] = amsim_decode(u[i], m, shift, zidx);
             }
             __syncthreads();
-            for (int i = ty; i < 64; i += 4) {
-                const int c = c0 + i, r = r0 + tx;
-                if (c < cols && r < dld) dst[int64_t(c) * dld + r] = tile[tx][i];
+            if (records == nullptr) {
+                for (int i = ty; i < 64; i += 4) {
+                    const int c = c0 + i, r = r0 + tx;
+                    if (c < cols && r < dld) dst[int64_t(c) * dld + r] = tile[tx][i];
+                }
+            } else {
+                for (int i = ty; i < 32; i += 4) {  // c0 is even: pair (c, c + 1) lies in the tile
+                    const int c = c0 + 2 * i, r = r0 + tx;
+                    if (c < cols && r < dld) {
+                        const uint32_t w0 = tile[tx][2 * i], w1 = tile[tx][2 * i + 1];
+                        uint32_t *rec = records + (int64_t(c >> 1) * dld + r) * 3;
+                        rec[0] = w0 & 0xFFFFu;
+                        rec[1] = (w0 >> 16) | (w1 & 0xFFFF0000u);
+                        rec[2] = w1 & 0xFFFFu;
+                    }
+                }
             }
             __syncthreads();
         }
@@ -590,7 +607,7 @@ struct ConvShape {
 enum { OP_GEMM = 0, OP_FWD = 1, OP_BWD_DATA = 2, OP_BWD_WEIGHT = 3 };
 
 struct TabArgs {
-    const uint32_t *A;   // decoded first operand
+    const uint32_t *A;   // decoded first operand: words, or (pair records) 12-byte step-pair records
     uint32_t a_bytes;    // its size in bytes (buffer range: reads beyond return 0)
     const uint32_t *Bd;  // decoded second operand rows, leading dimension Np
     int Np;
@@ -611,7 +628,66 @@ struct TabArgs {
 
 struct TabTap {
     int ubase, ustride, bbase, count;
+    int pbase;  // pair records: the tap's first record (records of pair j / 2 are ustride apart)
 };
+
+// The GEMM's first operand is decoded into one 12-byte record per lane row and step pair
+// (j, j + 1), j even, instead of one word per element: j's 16-bit table-index field (an LDS byte
+// offset on the bf16 path) as a word, the two mantissa-cleared operands as bf16
+// (pa(j) | pa(j+1) << 16), and j+1's index word.  The bf16 path loads a record with one
+// instruction and uses it as loaded: no masking of the indices, no pairing of the heads.  A
+// single step is one 8-byte load at record offset 0 (j even) or 4 (j odd) and one byte permute.
+template <int OP>
+constexpr bool split_a()
+{
+    return OP == OP_GEMM;
+}
+constexpr uint32_t kPairRecordBytes = 12;
+
+// First-operand buffer and the lane rows' byte offsets in it.
+template <int TM>
+struct AView {
+    __amdgpu_buffer_rsrc_t words;  // words, or pair records
+    uint32_t aoff[TM];             // per lane row: offset of its run (word or record)
+};
+
+// Byte offset of step j's word (pair records: of the record holding j) in the tap.
+template <int OP>
+__device__ __forceinline__ uint32_t a_step_offset(const TabTap &tp, int j)
+{
+    if constexpr (split_a<OP>())
+        return uint32_t(tp.pbase + (j >> 1) * tp.ustride) * kPairRecordBytes;
+    else
+        return uint32_t(tp.ubase + j * tp.ustride) * 4u;
+}
+
+// The first operand's word of step j (head | index, as the one-word layout stores it) for each
+// lane row; so = a_step_offset of j (wave-uniform).  Pair records: j's index word with j's half
+// of the head pair moved into the high half.
+template <int OP, int TM>
+__device__ __forceinline__ void load_a_words(uint32_t (&dst)[TM], const AView<TM> &av, uint32_t so, int j)
+{
+#pragma unroll
+    for (int r = 0; r < TM; ++r) {
+        if constexpr (split_a<OP>()) {
+            // j even: (index, heads) -> index | pa(j) << 16; j odd: (heads, index) -> index | pa(j+1)'s half
+            const u32x2 d = __builtin_amdgcn_raw_buffer_load_b64(av.words, av.aoff[r], so + (j & 1) * 4u, 0);
+            dst[r] = __builtin_amdgcn_perm(d.y, d.x, (j & 1) ? 0x03020504u : 0x05040100u);
+        } else {
+            dst[r] = __builtin_amdgcn_raw_buffer_load_b32(av.words, av.aoff[r], so, 0);
+        }
+    }
+}
+
+template <int OP, int TM>
+__device__ __forceinline__ AView<TM> make_aview(const TabArgs &a, const int (&abase)[TM])
+{
+    AView<TM> av;
+    av.words = __builtin_amdgcn_make_buffer_rsrc(const_cast<uint32_t *>(a.A), 0, int(a.a_bytes), 0x00020000);
+#pragma unroll
+    for (int r = 0; r < TM; ++r) av.aoff[r] = uint32_t(abase[r]) * (split_a<OP>() ? kPairRecordBytes : 4u);
+    return av;
+}
 
 // Rows of one stride phase of the backward-data pass.
 __device__ __forceinline__ void phase_dims(const ConvShape &s, int ph, int pw, int &hq_n, int &wq_n)
@@ -703,12 +779,14 @@ __device__ __forceinline__ TabTap tab_tap_raw(const TabArgs &a, int tap)
         t.ubase = 0;
         t.ustride = a.Mp;
         t.bbase = 0;
+        t.pbase = 0;
     } else if constexpr (OP == OP_FWD) {
         const int kh = tap / s.kw, kw = tap % s.kw;
         t.count = s.ci;
         t.ubase = kh * s.ci * a.Wp + kw;
         t.ustride = a.Wp;
         t.bbase = tap * s.ci;
+        t.pbase = 0;
     } else if constexpr (OP == OP_BWD_DATA) {
         const int ph = tab_phase(a) / s.sw, pw = tab_phase(a) % s.sw;
         const int kh0 = (ph + s.pt) % s.sh, kw0 = (pw + s.pl) % s.sw;
@@ -719,12 +797,14 @@ __device__ __forceinline__ TabTap tab_tap_raw(const TabArgs &a, int tap)
         t.ubase = (dh + a.pad_oh) * s.co * a.OWp + dw + a.pad_ow;  // >= 0: the padding covers every dh, dw
         t.ustride = a.OWp;
         t.bbase = (kh * s.kw + kw) * s.co;
+        t.pbase = 0;
     } else {
         const int n = tap / s.oh, oh = tap % s.oh;
         t.count = s.ow;
         t.ubase = (n * a.Hp + oh * s.sh) * a.Wp * s.ci;
         t.ustride = s.sw * s.ci;
         t.bbase = tap * s.ow;
+        t.pbase = 0;
     }
     return t;
 }
@@ -734,7 +814,8 @@ __device__ __forceinline__ TabTap tab_tap(const TabArgs &a, int tap)
 {
     const TabTap t = tab_tap_raw<OP>(a, tap);
     return TabTap{__builtin_amdgcn_readfirstlane(t.ubase), __builtin_amdgcn_readfirstlane(t.ustride),
-                  __builtin_amdgcn_readfirstlane(t.bbase), __builtin_amdgcn_readfirstlane(t.count)};
+                  __builtin_amdgcn_readfirstlane(t.bbase), __builtin_amdgcn_readfirstlane(t.count),
+                  __builtin_amdgcn_readfirstlane(t.pbase)};
 }
 
 // The slab cursor is wave-uniform; saying so at the loop head keeps it, and the buffer loads'
@@ -743,7 +824,8 @@ __device__ __forceinline__ TabTap tab_tap(const TabArgs &a, int tap)
 __device__ __forceinline__ void uniform_cursor(TabTap &cur, int &tap, int &c0)
 {
     cur = TabTap{__builtin_amdgcn_readfirstlane(cur.ubase), __builtin_amdgcn_readfirstlane(cur.ustride),
-                 __builtin_amdgcn_readfirstlane(cur.bbase), __builtin_amdgcn_readfirstlane(cur.count)};
+                 __builtin_amdgcn_readfirstlane(cur.bbase), __builtin_amdgcn_readfirstlane(cur.count),
+                 __builtin_amdgcn_readfirstlane(cur.pbase)};
     tap = __builtin_amdgcn_readfirstlane(tap);
     c0 = __builtin_amdgcn_readfirstlane(c0);
 }
@@ -826,20 +908,18 @@ __device__ __forceinline__ void tab_body(const TabArgs &a)
     const int colw = blockIdx.y * TNW;  // first column of the workgroup
     const int col0 = colw + cg * TN;    // first column of this wave
     // First-operand reads are raw buffer loads: voffset = the lane row's byte offset (range-checked,
-    // reads past a_bytes return 0), soffset = the wave-uniform step offset, which every tap keeps
+    // reads past the buffer return 0), soffset = the wave-uniform step offset, which every tap keeps
     // non-negative and inside the tensor, since the hardware does not range-check it.
-    const __amdgpu_buffer_rsrc_t ares =
-        __builtin_amdgcn_make_buffer_rsrc(const_cast<uint32_t *>(a.A), 0, int(a.a_bytes), 0x00020000);
-
-    uint32_t aoff[TM];  // byte offset of each lane row's first-operand run
+    int abase[TM];  // element offset of each lane row's first-operand run
 #pragma unroll
     for (int r = 0; r < TM; ++r) {
         const int row = row0 + 64 * r;
         int ab = 0;
         int64_t ob = 0;
         if (row < R) tab_row<OP>(a, row, ab, ob);
-        aoff[r] = uint32_t(ab) * 4u;
+        abase[r] = ab;
     }
+    const AView<TM> av = make_aview<OP, TM>(a, abase);
     // this split's chunks, as positions p = tap * (8 * chunks per tap) + step
     const int count = tab_count<OP>(a);
     const int cpt = (count + 7) / 8;  // chunks per tap
@@ -852,7 +932,7 @@ __device__ __forceinline__ void tab_body(const TabArgs &a)
     float acc[TM][TN];
     init_acc(acc);
     uint32_t acur[TM];
-    TabTap cur{0, 0, 0, 0};
+    TabTap cur{0, 0, 0, 0, 0};
     int tap = q0 / max(cpt, 1);
     int c0 = (q0 - tap * cpt) * 8;
     bool have = q0 * 8 < p_end;
@@ -860,10 +940,7 @@ __device__ __forceinline__ void tab_body(const TabArgs &a)
         cur = tab_tap<OP>(a, tap);
         tab_fetch<TNW, EB, CPT, NT, RL>(stage, stage_pb, cur, c0, a.Bd, a.Np, colw, a.rows);
         tab_commit<TNW, EB, CPT, NT, RL>(stage, stage_pb, smem, pbs, 0);
-#pragma unroll
-        for (int r = 0; r < TM; ++r)
-            acur[r] = __builtin_amdgcn_raw_buffer_load_b32(
-                ares, aoff[r], __builtin_amdgcn_readfirstlane(uint32_t(cur.ubase + c0 * cur.ustride) * 4u), 0);
+        load_a_words<OP, TM>(acur, av, __builtin_amdgcn_readfirstlane(a_step_offset<OP>(cur, c0)), c0);
     }
     __syncthreads();
     int buf = 0;
@@ -889,12 +966,11 @@ __device__ __forceinline__ void tab_body(const TabArgs &a)
             // next step's first-operand words: this slab's next slot or the next slab's first
             uint32_t anext[TM];
             const bool in_slab = slot + 1 < nslots;
-            const uint32_t unext = __builtin_amdgcn_readfirstlane(
-                in_slab ? uint32_t(cur.ubase + (c0 + slot + 1) * cur.ustride) * 4u
-                        : uint32_t(nxt.ubase + nc0 * nxt.ustride) * 4u);
+            const uint32_t unext = __builtin_amdgcn_readfirstlane(in_slab ? a_step_offset<OP>(cur, c0 + slot + 1)
+                                                                          : a_step_offset<OP>(nxt, nc0));
+            const int jnext = __builtin_amdgcn_readfirstlane(in_slab ? c0 + slot + 1 : nc0);
             if (in_slab || has_next) {
-#pragma unroll
-                for (int r = 0; r < TM; ++r) anext[r] = __builtin_amdgcn_raw_buffer_load_b32(ares, aoff[r], unext, 0);
+                load_a_words<OP, TM>(anext, av, unext, jnext);
             } else {
 #pragma unroll
                 for (int r = 0; r < TM; ++r) anext[r] = 0u;
@@ -969,6 +1045,15 @@ constexpr int kDotStepBytes = kTabRowEntries * 16;   // 128 entries x 16 bytes
 // entry group, 32 threads per step); a slab is 2 KiB per step.
 constexpr int dot_slab_steps(int nw) { return nw * 2; }
 
+// 16 bytes of LDS at byte address off + imm.  The table kernels use no static LDS, so their
+// dynamic allocation starts at LDS address 0 (checked on the host when the kernels are set up);
+// addressing it as such lets the constant part land in the instruction's offset field.
+typedef __attribute__((address_space(3))) const u32x4 lds_u32x4;
+__device__ __forceinline__ u32x4 lds_load_b128(uint32_t off, uint32_t imm)
+{
+    return reinterpret_cast<lds_u32x4 *>(uintptr_t(off))[imm / 16];
+}
+
 __device__ __forceinline__ float dot2_bf16(uint32_t x, uint32_t y, float c)
 {
     return __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2_t, x), __builtin_bit_cast(bf16x2_t, y), c,
@@ -1027,18 +1112,36 @@ __device__ __forceinline__ void dot_commit(const u32x4 (&bw)[2], const uint32_t 
     }
 }
 
-// One first-operand word per lane row and step.  A step past the tap's end (the odd step of a
-// pair, or a slab's unused slots) reads the tap's last step again: its slot in the slab holds
-// +0 entries (staged from a +0 second operand), so it adds signed zeros only, and the load stays
+// First-operand data of the step pair (j, j + 1) per lane row: the two words, or (split layout)
+// the two indices and the head pair.  A step past the tap's end (the odd step of a pair, or a
+// slab's unused slots) reads the tap's last step again: its slot in the slab holds +0 entries
+// (staged from a +0 second operand), so it adds signed zeros only, and the loads stay
 // branch-free and in bounds.
-template <int TM>
-__device__ __forceinline__ void dot_load_a(uint32_t (&dst)[TM], __amdgpu_buffer_rsrc_t ares, const uint32_t (&aoff)[TM],
-                                           const TabTap &tp, int j)
+template <int OP, int TM>
+__device__ __forceinline__ void dot_load_pair(uint32_t (&dst)[split_a<OP>() ? 3 : 2][TM], const AView<TM> &av,
+                                              const TabTap &tp, int j)
 {
-    const int jj = min(j, tp.count - 1);
-    const uint32_t so = __builtin_amdgcn_readfirstlane(uint32_t(tp.ubase + jj * tp.ustride) * 4u);
+    const int j0 = min(j, tp.count - 1), j1 = min(j + 1, tp.count - 1);
+    if constexpr (split_a<OP>()) {
+        // j even: one record holds both steps (past the end: the last record; an odd count's
+        // last record has a decoded +0 for its missing step)
+        const uint32_t so = __builtin_amdgcn_readfirstlane(a_step_offset<OP>(tp, j0));
 #pragma unroll
-    for (int r = 0; r < TM; ++r) dst[r] = __builtin_amdgcn_raw_buffer_load_b32(ares, aoff[r], so, 0);
+        for (int r = 0; r < TM; ++r) {
+            const u32x3 rec = __builtin_amdgcn_raw_buffer_load_b96(av.words, av.aoff[r], so, 0);
+            dst[0][r] = rec.x;
+            dst[1][r] = rec.z;
+            dst[2][r] = rec.y;
+        }
+    } else {
+        const uint32_t s0 = __builtin_amdgcn_readfirstlane(a_step_offset<OP>(tp, j0));
+        const uint32_t s1 = __builtin_amdgcn_readfirstlane(a_step_offset<OP>(tp, j1));
+#pragma unroll
+        for (int r = 0; r < TM; ++r) {
+            dst[0][r] = __builtin_amdgcn_raw_buffer_load_b32(av.words, av.aoff[r], s0, 0);
+            dst[1][r] = __builtin_amdgcn_raw_buffer_load_b32(av.words, av.aoff[r], s1, 0);
+        }
+    }
 }
 
 // Workgroup: NW waves along rows (64*TM rows each), all on the same 8 columns.  Every thread
@@ -1049,6 +1152,8 @@ __device__ __forceinline__ void tab_body_dot(const TabArgs &a)
     constexpr int KS = dot_slab_steps(NW);
     constexpr int kDotSlab = KS * kDotStepBytes;
     constexpr int TN = kDotCols;
+    constexpr bool SPLIT = split_a<OP>();
+    constexpr int NA = SPLIT ? 3 : 2;  // first-operand registers per step pair and lane row
     extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
 
     const int R = tab_rows<OP>(a);
@@ -1058,20 +1163,19 @@ __device__ __forceinline__ void tab_body_dot(const TabArgs &a)
     const int row0 = blockIdx.x * (64 * TM * NW) + wave * (64 * TM) + lane;
     const bool live = row0 - lane < R;  // wave-uniform
     const int col0 = blockIdx.y * TN;
-    const __amdgpu_buffer_rsrc_t ares =
-        __builtin_amdgcn_make_buffer_rsrc(const_cast<uint32_t *>(a.A), 0, int(a.a_bytes), 0x00020000);
     const __amdgpu_buffer_rsrc_t rres = __builtin_amdgcn_make_buffer_rsrc(
         const_cast<unsigned char *>(a.dot_rows), 0, int((kZeroRow + 1) * kTabRowEntries), 0x00020000);
 
-    uint32_t aoff[TM];
+    int abase[TM];
 #pragma unroll
     for (int r = 0; r < TM; ++r) {
         const int row = row0 + 64 * r;
         int ab = 0;
         int64_t ob = 0;
         if (row < R) tab_row<OP>(a, row, ab, ob);
-        aoff[r] = uint32_t(ab) * 4u;
+        abase[r] = ab;
     }
+    const AView<TM> av = make_aview<OP, TM>(a, abase);
     const int count = tab_count<OP>(a);
     const int cpt = (count + 7) / 8;
     const int q_total = tab_taps<OP>(a) * cpt;
@@ -1082,12 +1186,12 @@ __device__ __forceinline__ void tab_body_dot(const TabArgs &a)
     uint32_t srw[kDotCols];
     float acc[TM][TN];
     init_acc(acc);
-    // First-operand words of four step pairs, as a ring: pair kp of a slab is in w[kp % 4]; while
+    // First-operand data of four step pairs, as a ring: pair kp of a slab is in w[kp % 4]; while
     // it is used, pair kp + 2 (of this slab, or the next slab's first two for the last two pairs)
     // is loaded into w[(kp + 2) % 4].  A slab holds a multiple of four pairs, so after a full slab
     // the next slab's first two pairs sit in w[0], w[1].
-    uint32_t w[4][2][TM];
-    TabTap cur{0, 0, 0, 0};
+    uint32_t w[4][NA][TM];
+    TabTap cur{0, 0, 0, 0, 0};
     int tap = q0 / max(cpt, 1);
     int c0 = (q0 - tap * cpt) * 8;
     bool have = q0 * 8 < p_end;
@@ -1096,14 +1200,14 @@ __device__ __forceinline__ void tab_body_dot(const TabArgs &a)
         dot_fetch(sbw, srw, cur, c0, a.Bd, a.Np, col0, rres);
         dot_commit(sbw, srw, smem);
 #pragma unroll
-        for (int k = 0; k < 2; ++k) {
-            dot_load_a(w[k][0], ares, aoff, cur, c0 + 2 * k);
-            dot_load_a(w[k][1], ares, aoff, cur, c0 + 2 * k + 1);
-        }
+        for (int k = 0; k < 2; ++k) dot_load_pair<OP, TM>(w[k], av, cur, c0 + 2 * k);
     }
     __syncthreads();
-    int buf = 0;
-    while (have) {
+    // One slab from buffer BUF (a compile-time LDS offset, folded into the gathers' immediate
+    // offsets); the next slab is staged into the other buffer.
+    auto slab = [&](auto buf_c) __attribute__((always_inline)) {
+        constexpr uint32_t BOFF = uint32_t(decltype(buf_c)::value) * kDotSlab;
+        constexpr uint32_t NEXT = uint32_t(decltype(buf_c)::value ^ 1) * kDotSlab;
         uniform_cursor(cur, tap, c0);
         TabTap nxt = cur;  // stays `cur` past the last slab: the loads below then stay in bounds
         int ntap = tap, nc0 = c0 + KS;
@@ -1114,7 +1218,6 @@ __device__ __forceinline__ void tab_body_dot(const TabArgs &a)
         const bool has_next = ntap * cpt * 8 + nc0 < p_end;
         if (has_next && ntap != tap) nxt = tab_tap<OP>(a, ntap);
         if (has_next) dot_fetch(sbw, srw, nxt, nc0, a.Bd, a.Np, col0, rres);
-        const uint32_t boff = uint32_t(buf) * kDotSlab;
         // the slab ends at the tap's end or, 8-step chunks being the unit of splits, at the split's
         const int nslots = min(min(KS, cur.count - c0), p_end - (tap * cpt * 8 + c0));
         // a wave whose rows all lie past the end only stages and keeps the barriers
@@ -1122,25 +1225,25 @@ __device__ __forceinline__ void tab_body_dot(const TabArgs &a)
 #pragma unroll
         for (int kp = 0; kp < KS / 2; ++kp) {
             if (kp >= npairs) break;
-            uint32_t(&ahead)[2][TM] = w[(kp + 2) % 4];
-            if (kp + 2 < KS / 2) {
-                dot_load_a(ahead[0], ares, aoff, cur, c0 + 2 * kp + 4);
-                dot_load_a(ahead[1], ares, aoff, cur, c0 + 2 * kp + 5);
-            } else {
-                dot_load_a(ahead[0], ares, aoff, nxt, nc0 + 2 * (kp + 2 - KS / 2));
-                dot_load_a(ahead[1], ares, aoff, nxt, nc0 + 2 * (kp + 2 - KS / 2) + 1);
-            }
+            if (kp + 2 < KS / 2)
+                dot_load_pair<OP, TM>(w[(kp + 2) % 4], av, cur, c0 + 2 * kp + 4);
+            else
+                dot_load_pair<OP, TM>(w[(kp + 2) % 4], av, nxt, nc0 + 2 * (kp + 2 - KS / 2));
             const uint32_t(&a0)[TM] = w[kp % 4][0];
             const uint32_t(&a1)[TM] = w[kp % 4][1];
 #pragma unroll
             for (int r = 0; r < TM; ++r) {
-                // entry byte offset = the word's low half (mantissa field * 16; the head is bits
-                // 22..31) plus the slab's
-                const u32x4 X =
-                    *reinterpret_cast<const u32x4 *>(smem + ((a0[r] & 0xFFFFu) + boff) + (2 * kp) * kDotStepBytes);
-                const u32x4 Y = *reinterpret_cast<const u32x4 *>(smem + ((a1[r] & 0xFFFFu) + boff) +
-                                                                 (2 * kp + 1) * kDotStepBytes);
-                const uint32_t pa = __builtin_amdgcn_perm(a1[r], a0[r], 0x07060302u);  // (pa(k), pa(k+1))
+                // entry byte offset = the mantissa field * 16 (the index plane, or the word's low
+                // half under its head) plus the slot's, which is a constant
+                const uint32_t o0 = SPLIT ? a0[r] : (a0[r] & 0xFFFFu);
+                const uint32_t o1 = SPLIT ? a1[r] : (a1[r] & 0xFFFFu);
+                const u32x4 X = lds_load_b128(o0, BOFF + (2 * kp) * kDotStepBytes);
+                const u32x4 Y = lds_load_b128(o1, BOFF + (2 * kp + 1) * kDotStepBytes);
+                uint32_t pa;  // (pa(k), pa(k+1)) as bf16
+                if constexpr (SPLIT)
+                    pa = w[kp % 4][NA - 1][r];
+                else
+                    pa = __builtin_amdgcn_perm(a1[r], a0[r], 0x07060302u);
 #pragma unroll
                 for (int q = 0; q < TN / 2; ++q) {
                     acc[r][2 * q] = dot2_bf16(__builtin_amdgcn_perm(Y[q], X[q], 0x05040100u), pa, acc[r][2 * q]);
@@ -1151,18 +1254,19 @@ __device__ __forceinline__ void tab_body_dot(const TabArgs &a)
         }
         if (live && npairs < KS / 2 && has_next) {  // a short slab: the next slab's first two pairs
 #pragma unroll
-            for (int k = 0; k < 2; ++k) {
-                dot_load_a(w[k][0], ares, aoff, nxt, nc0 + 2 * k);
-                dot_load_a(w[k][1], ares, aoff, nxt, nc0 + 2 * k + 1);
-            }
+            for (int k = 0; k < 2; ++k) dot_load_pair<OP, TM>(w[k], av, nxt, nc0 + 2 * k);
         }
-        if (has_next) dot_commit(sbw, srw, smem + (buf ^ 1) * kDotSlab);
+        if (has_next) dot_commit(sbw, srw, smem + NEXT);
         __syncthreads();
         cur = nxt;
         tap = ntap;
         c0 = nc0;
-        buf ^= 1;
         have = has_next;
+    };
+    while (have) {
+        slab(std::integral_constant<int, 0>{});
+        if (!have) break;
+        slab(std::integral_constant<int, 1>{});
     }
 
     // Signs of zero sums: -0 when every product of the split's range is -0, else +0.  The first
@@ -1184,7 +1288,7 @@ __device__ __forceinline__ void tab_body_dot(const TabArgs &a)
             const int j1 = min(tp.count, p_end - pbase);
             for (int j = max(q0 * 8 - pbase, 0); j < j1; ++j) {
                 uint32_t aw[TM];
-                dot_load_a(aw, ares, aoff, tp, j);
+                load_a_words<OP, TM>(aw, av, __builtin_amdgcn_readfirstlane(a_step_offset<OP>(tp, j)), j);
                 const uint32_t *brow = a.Bd + int64_t(tp.bbase + j) * a.Np + col0;
 #pragma unroll
                 for (int t = 0; t < TN; ++t) {
@@ -1353,12 +1457,18 @@ inline int64_t tab_cols(const Tile &t) { return int64_t(t.tn) * (t.nw / t.wr); }
 std::once_flag g_attr_once;
 hipError_t g_attr_err = hipSuccess;
 
+// Raises the kernel's dynamic LDS limit, and checks that it has no static LDS: the bf16 path
+// addresses its slabs as LDS addresses starting at 0.
 template <typename K>
 void allow_lds(K kernel, size_t bytes)
 {
     hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void *>(kernel),
                                        hipFuncAttributeMaxDynamicSharedMemorySize, int(bytes));
     if (e != hipSuccess) g_attr_err = e;
+    hipFuncAttributes fa{};
+    e = hipFuncGetAttributes(&fa, reinterpret_cast<const void *>(kernel));
+    if (e != hipSuccess) g_attr_err = e;
+    else if (fa.sharedSizeBytes != 0) g_attr_err = hipErrorInvalidKernelFile;
 }
 
 // The instantiated (TM, TN, WR, NW, RL) tiles: every candidate of the chooser above.
@@ -1469,8 +1579,8 @@ Plan plan_gemm(int64_t m, int64_t n, int64_t k, int m_bits)
     p.b_ld = round_up(n, tab_cols(p.tile));
     plan_tab_split(p, ceil_div(k, 8));
     size_t o = table_area(p, 0);
-    p.off_a = o;
-    o += align_up(size_t(k) * p.a_ld * 4);
+    p.off_a = o;  // step-pair records
+    o += align_up(size_t((k + 1) / 2) * p.a_ld * 12);
     p.off_b = o;
     o += align_up(size_t(k) * p.b_ld * 4);
     p.out_elems = m * n;
@@ -1789,8 +1899,8 @@ int approx_gemm(int trans_a, int trans_b, int64_t m, int64_t n, int64_t k, const
     const dim3 grid_dt(unsigned(std::min<int64_t>(ceil_div(p.a_ld, 64), 128)),
                        unsigned(std::min<int64_t>(ceil_div(k, 64), 64)));  // <= kStatSlots workgroups
     const int grid_b = decode_grid(k * p.b_ld);
-    hipLaunchKernelGGL(decode_t_kernel, grid_dt, dim3(256), 0, st, A, a_sr, a_sc, int(m), int(k), Ad, int(p.a_ld),
-                       m_bits, shift_first(m_bits), 0u, stats_a(ws, p));
+    hipLaunchKernelGGL(decode_t_kernel, grid_dt, dim3(256), 0, st, A, a_sr, a_sc, int(m), int(k), nullptr,
+                       int(p.a_ld), m_bits, shift_first(m_bits), 0u, stats_a(ws, p), Ad);
     hipLaunchKernelGGL(decode_kernel, dim3(grid_b), dim3(256), 0, st, B, int64_t(0), b_sr, b_sc, 1, int(k), int(n), Bd,
                        int(p.b_ld), m_bits, shift_second(m_bits), zidx_second(p), stats_b(ws, p),
                        decode_vec(B, 0, b_sr, b_sc));
@@ -1798,7 +1908,8 @@ int approx_gemm(int trans_a, int trans_b, int64_t m, int64_t n, int64_t k, const
     if (prep_rows(lut, m_bits, ws, p, int(grid_dt.x * grid_dt.y), grid_b, st) != AMSIM_OK) return AMSIM_ERR_HIP;
     int rc;
     {
-        TabArgs a = tab_args(p, ws, Ad, k * p.a_ld, Bd, out, int(m), int(n));
+        TabArgs a = tab_args(p, ws, Ad, 0, Bd, out, int(m), int(n));
+        a.a_bytes = uint32_t((k + 1) / 2 * p.a_ld * 12);
         a.ldc = p.splits > 1 ? n : ldc;  // partial sums are dense
         a.Mp = int(p.a_ld);
         a.K = int(k);
