@@ -1066,13 +1066,12 @@ __device__ __forceinline__ uint32_t add_u16x2(uint32_t x, uint32_t y)
 }
 
 // Staging of one slab: thread -> step slot (tid / 32) and entry group g (tid % 32), which builds
-// the entries ka = g, g + 32, g + 64, g + 96.  Fetch: the slot's 8 second-operand words and, per
-// column, the 4 bytes of its table row that hold those entries.
-__device__ __forceinline__ void dot_fetch(u32x4 (&bw)[2], uint32_t (&rw)[kDotCols], const TabTap &tp, int c0,
-                                          const uint32_t *__restrict__ Bd, int Np, int colw,
-                                          __amdgpu_buffer_rsrc_t rres)
+// the entries ka = g, g + 32, g + 64, g + 96.  Fetch, in two parts: the slot's 8 second-operand
+// words, then, per column, the 4 bytes of its table row that hold those entries.
+__device__ __forceinline__ void dot_fetch_b(u32x4 (&bw)[2], const TabTap &tp, int c0, const uint32_t *__restrict__ Bd,
+                                            int Np, int colw)
 {
-    const int slot = threadIdx.x >> 5, g = threadIdx.x & 31;
+    const int slot = threadIdx.x >> 5;
     const int j = c0 + slot;
     if (j < tp.count) {
         const u32x4 *src = reinterpret_cast<const u32x4 *>(Bd + int64_t(tp.bbase + j) * Np + colw);
@@ -1082,6 +1081,12 @@ __device__ __forceinline__ void dot_fetch(u32x4 (&bw)[2], uint32_t (&rw)[kDotCol
         bw[0] = u32x4{kZeroRowWord, kZeroRowWord, kZeroRowWord, kZeroRowWord};
         bw[1] = bw[0];
     }
+}
+
+__device__ __forceinline__ void dot_fetch_rows(uint32_t (&rw)[kDotCols], const u32x4 (&bw)[2],
+                                               __amdgpu_buffer_rsrc_t rres)
+{
+    const int g = threadIdx.x & 31;
 #pragma unroll
     for (int c = 0; c < kDotCols; ++c) {
         const uint32_t w = bw[c / 4][c % 4];  // idx = kb * 128 (kZeroRow for zeros)
@@ -1182,7 +1187,12 @@ __device__ __forceinline__ void tab_body_dot(const TabArgs &a)
     const int q0 = tab_split(a) * a.chunks_per_split;
     const int p_end = min(q_total, q0 + a.chunks_per_split) * 8;
 
-    u32x4 sbw[2];
+    // Staging pipeline: while slab s is computed, the table bytes of slab s + 1 are fetched (its
+    // second-operand words `sbw` having arrived during slab s - 1) and the second-operand words
+    // of slab s + 2 are loaded into `sbw2`.  With 8-step slabs (4-wave workgroups) the words'
+    // latency would otherwise be exposed once per slab; 16-step slabs fetch both in slab s.
+    constexpr bool AHEAD2 = NW == 4;
+    u32x4 sbw[2], sbw2[2];
     uint32_t srw[kDotCols];
     float acc[TM][TN];
     init_acc(acc);
@@ -1191,16 +1201,36 @@ __device__ __forceinline__ void tab_body_dot(const TabArgs &a)
     // is loaded into w[(kp + 2) % 4].  A slab holds a multiple of four pairs, so after a full slab
     // the next slab's first two pairs sit in w[0], w[1].
     uint32_t w[4][NA][TM];
+    // The slab after (t, tp_, c): its tap, cursor and whether it is in this split's range (if not,
+    // `o` stays `t`, so that loads aimed at it stay in bounds).
+    auto advance = [&](const TabTap &t, int tp_, int c, TabTap &o, int &otap, int &oc, bool &ok)
+                       __attribute__((always_inline)) {
+        o = t;
+        otap = tp_;
+        oc = c + KS;
+        if (oc >= count) {
+            otap = tp_ + 1;
+            oc = 0;
+        }
+        ok = otap * cpt * 8 + oc < p_end;
+        if (ok && otap != tp_) o = tab_tap<OP>(a, otap);
+    };
     TabTap cur{0, 0, 0, 0, 0};
     int tap = q0 / max(cpt, 1);
     int c0 = (q0 - tap * cpt) * 8;
     bool have = q0 * 8 < p_end;
+    TabTap nxt{0, 0, 0, 0, 0};
+    int ntap = 0, nc0 = 0;
+    bool has_next = false;
     if (have) {
         cur = tab_tap<OP>(a, tap);
-        dot_fetch(sbw, srw, cur, c0, a.Bd, a.Np, col0, rres);
+        dot_fetch_b(sbw, cur, c0, a.Bd, a.Np, col0);
+        dot_fetch_rows(srw, sbw, rres);
         dot_commit(sbw, srw, smem);
 #pragma unroll
         for (int k = 0; k < 2; ++k) dot_load_pair<OP, TM>(w[k], av, cur, c0 + 2 * k);
+        advance(cur, tap, c0, nxt, ntap, nc0, has_next);
+        if (AHEAD2 && has_next) dot_fetch_b(sbw, nxt, nc0, a.Bd, a.Np, col0);
     }
     __syncthreads();
     // One slab from buffer BUF (a compile-time LDS offset, folded into the gathers' immediate
@@ -1209,15 +1239,19 @@ __device__ __forceinline__ void tab_body_dot(const TabArgs &a)
         constexpr uint32_t BOFF = uint32_t(decltype(buf_c)::value) * kDotSlab;
         constexpr uint32_t NEXT = uint32_t(decltype(buf_c)::value ^ 1) * kDotSlab;
         uniform_cursor(cur, tap, c0);
-        TabTap nxt = cur;  // stays `cur` past the last slab: the loads below then stay in bounds
-        int ntap = tap, nc0 = c0 + KS;
-        if (nc0 >= count) {
-            ntap = tap + 1;
-            nc0 = 0;
+        uniform_cursor(nxt, ntap, nc0);
+        TabTap nxt2 = nxt;
+        int ntap2 = ntap, nc02 = nc0;
+        bool has_next2 = false;
+        if constexpr (AHEAD2) {
+            advance(nxt, ntap, nc0, nxt2, ntap2, nc02, has_next2);
+            has_next2 = has_next2 && has_next;
+            if (has_next) dot_fetch_rows(srw, sbw, rres);
+            if (has_next2) dot_fetch_b(sbw2, nxt2, nc02, a.Bd, a.Np, col0);
+        } else if (has_next) {
+            dot_fetch_b(sbw, nxt, nc0, a.Bd, a.Np, col0);
+            dot_fetch_rows(srw, sbw, rres);
         }
-        const bool has_next = ntap * cpt * 8 + nc0 < p_end;
-        if (has_next && ntap != tap) nxt = tab_tap<OP>(a, ntap);
-        if (has_next) dot_fetch(sbw, srw, nxt, nc0, a.Bd, a.Np, col0, rres);
         // the slab ends at the tap's end or, 8-step chunks being the unit of splits, at the split's
         const int nslots = min(min(KS, cur.count - c0), p_end - (tap * cpt * 8 + c0));
         // a wave whose rows all lie past the end only stages and keeps the barriers
@@ -1262,6 +1296,16 @@ __device__ __forceinline__ void tab_body_dot(const TabArgs &a)
         tap = ntap;
         c0 = nc0;
         have = has_next;
+        if constexpr (AHEAD2) {
+            nxt = nxt2;
+            ntap = ntap2;
+            nc0 = nc02;
+            has_next = has_next2;
+            sbw[0] = sbw2[0];
+            sbw[1] = sbw2[1];
+        } else {
+            advance(cur, tap, c0, nxt, ntap, nc0, has_next);
+        }
     };
     while (have) {
         slab(std::integral_constant<int, 0>{});
