@@ -25,6 +25,7 @@
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
+#include <cmath>
 #include <cstdint>
 #include <iterator>
 #include <mutex>
@@ -1428,7 +1429,6 @@ struct Tile {
     int nw = kWaves;  // table kernels: waves per workgroup
 };
 
-constexpr int kTargetWgs = 512;  // 256 CUs x 2 workgroups
 
 // Per-column-table kernels (M <= 7).  Candidates are the instantiated (TM, TN, WR, NW) tiles; the
 // choice minimises an estimate of issue time: padded work x cost per product, scaled up when the
@@ -1451,10 +1451,18 @@ constexpr TabCand kTabCands[] = {{4, 8, 8, 8}, {4, 8, 4, 4}, {3, 8, 4, 4}, {2, 8
 constexpr TabCand kWideCands[] = {{8, 4, 8, 8}, {4, 8, 8, 8}, {2, 8, 4, 4}, {1, 8, 4, 4}, {1, 4, 4, 4}};
 constexpr TabCand kWide11Cands[] = {{8, 4, 8, 8}, {4, 4, 8, 8}, {2, 4, 4, 4}, {1, 4, 4, 4}};
 
-Tile choose_tab_tile(int64_t rows, int64_t cols, int64_t red, int64_t min_steps, bool allow_split, int rl,
-                     int max_tm)
+// Tile and reduction split for `rows` x `cols` outputs (times `phases` independent grids) over q
+// reduction chunks of 8 steps.  Cost = the products a tile computes (rows padded to whole waves)
+// times an issue-cost estimate per product, divided by how well the launch fills the chip: the
+// workgroups per CU that LDS and registers allow (four waves per SIMD) give the slots of one
+// round, a last round that is partly empty is lost, and a launch under one round runs its CUs
+// below full occupancy.  Only a launch under one round is split (at least min_chunks chunks per
+// split); splits add their partial sums' traffic and a reduction launch.
+Tile choose_tab_tile(int64_t rows, int64_t cols, int64_t q, int64_t min_chunks, bool allow_split, int rl,
+                     int max_tm, int64_t phases)
 {
-    constexpr int64_t kTargetWaves = int64_t(kTargetWgs) * kWaves;
+    constexpr int kCUs = 256, kWavesPerCU = 16;
+    constexpr size_t kLdsPerCU = 160 * 1024;
     Tile best{};
     double best_cost = 0.0;
     const TabCand *cands = rl == 7 ? kTabCands : (rl < 11 ? kWideCands : kWide11Cands);
@@ -1462,34 +1470,60 @@ Tile choose_tab_tile(int64_t rows, int64_t cols, int64_t red, int64_t min_steps,
     for (size_t ci = 0; ci < ncands; ++ci) {
         const TabCand &c = cands[ci];
         if (c.tm > max_tm) continue;
-        // Waves whose rows all lie past the end skip the work: count the waves that have rows.
         const int64_t wrows = int64_t(64) * c.tm;  // rows per wave
         const int64_t rtile = wrows * c.wr;
         const int64_t ctile = int64_t(c.tn) * (c.nw / c.wr);
         const int64_t col_tiles = ceil_div(cols, ctile);
-        const int64_t live_waves = ceil_div(rows, wrows) * col_tiles * (c.nw / c.wr);
-        const int64_t live_rows = std::min(rtile, ceil_div(rows, wrows) * wrows);  // of the fullest workgroup
-        int split = 1;
-        if (allow_split && live_waves < kTargetWaves) {
-            const int64_t max_split = std::max<int64_t>(1, red / std::max<int64_t>(1, min_steps));
-            split = int(std::min<int64_t>(std::min<int64_t>(ceil_div(kTargetWaves, live_waves), max_split), 1024));
-        }
-        const double work = double(ceil_div(rows, wrows) * wrows) * double(col_tiles * ctile);
+        const int64_t base = ceil_div(rows, rtile) * col_tiles * phases;  // workgroups without splits
+        // waves whose rows all lie past the end skip the work; the fullest workgroup's live rows
+        // share its staging
+        const int64_t live_rows = std::min(rtile, ceil_div(rows, wrows) * wrows);
+        const int64_t wgs_per_cu =
+            std::max<int64_t>(1, std::min<int64_t>(kWavesPerCU / c.nw, kLdsPerCU / tab_lds_bytes(c.tn, c.wr, c.nw, rl)));
+        const double slots = double(kCUs * wgs_per_cu);
+        const double work =
+            double(ceil_div(rows, wrows) * wrows) * double(col_tiles * ctile) * double(phases) * double(q * 8);
         const bool pair = rl == 7 && c.tn == kDotCols && c.wr == c.nw;
         // staging bytes per product grow with the row length (2^rl entries; wide rows are priced
         // at 2-byte entries)
         const double per_product =
             (pair ? 1.2 : 3.0) + 2.5 / c.tn + 4.0 / (c.tm * c.tn) +
             512.0 * double(1 << (rl - 7)) / double(live_rows) * (pair ? 0.5 : (rl == 7 ? 1.0 : 2.0));
-        const double fill = std::min(1.0, double(live_waves * split) / kTargetWaves);
-        const double cost = work * per_product / fill;
-        if (best_cost == 0.0 || cost < best_cost * 0.999) {
-            best_cost = cost;
-            best.tm = c.tm;
-            best.tn = c.tn;
-            best.wr = c.wr;
-            best.nw = c.nw;
-            best.split = split;
+        const double outputs = double(rows) * double(cols) * double(phases);
+        // split only a launch that cannot fill one round by itself
+        const int64_t max_split = allow_split && double(base) < slots
+                                      ? std::max<int64_t>(1, std::min<int64_t>(q / std::max<int64_t>(1, min_chunks), 4096))
+                                      : 1;
+        auto cost_of = [&](int64_t s) {
+            const int64_t cps = ceil_div(q, s);           // chunks per split
+            const int64_t s_eff = ceil_div(q, cps);       // the splits that chunking leaves
+            const double load = double(base * s_eff) / slots;  // workgroups per slot
+            const double rounds = std::ceil(load);
+            const double fill = (load / rounds) * std::pow(std::min(1.0, load), 0.6);
+            double cst = work * per_product / fill;
+            if (s_eff > 1) cst += outputs * double(s_eff) * 45.0 + 1.4e8;
+            return std::make_pair(cst, s_eff);
+        };
+        // candidate splits: none, the most allowed, and those that fill k whole rounds of slots
+        int64_t trial[18];
+        int nt = 0;
+        trial[nt++] = 1;
+        trial[nt++] = max_split;
+        for (int k = 1; k <= 8; ++k) {
+            const int64_t s0 = int64_t(std::floor(k * slots / double(base)));
+            if (s0 >= 2 && s0 <= max_split) trial[nt++] = s0;
+            if (s0 + 1 >= 2 && s0 + 1 <= max_split) trial[nt++] = s0 + 1;
+        }
+        for (int ti = 0; ti < nt; ++ti) {
+            const auto cs = cost_of(trial[ti]);
+            if (best_cost == 0.0 || cs.first < best_cost * 0.999) {
+                best_cost = cs.first;
+                best.tm = c.tm;
+                best.tn = c.tn;
+                best.wr = c.wr;
+                best.nw = c.nw;
+                best.split = int(cs.second);
+            }
         }
     }
     return best;
@@ -1618,7 +1652,7 @@ Plan plan_gemm(int64_t m, int64_t n, int64_t k, int m_bits)
 {
     Plan p{};
     p.rl = row_log(m_bits);
-    p.tile = choose_tab_tile(m, n, ceil_div(k, 8), 32, true, p.rl, 8);
+    p.tile = choose_tab_tile(m, n, ceil_div(k, 8), 32, true, p.rl, 8, 1);
     p.a_ld = round_up(m, int64_t(64) * p.tile.wr * p.tile.tm);
     p.b_ld = round_up(n, tab_cols(p.tile));
     plan_tab_split(p, ceil_div(k, 8));
@@ -1707,7 +1741,7 @@ Plan plan_conv(const amsim_conv2d *d, int pass, int m_bits)
     p.Wp = d->w + d->pad_left + d->pad_right;
     if (pass == AMSIM_CONV_FWD) {
         const int64_t q = int64_t(s.kh) * s.kw * ceil_div(s.ci, 8);
-        p.tile = choose_tab_tile(npix_out, s.co, q, 16, true, p.rl, 8);
+        p.tile = choose_tab_tile(npix_out, s.co, q, 16, true, p.rl, 8, 1);
         plan_tab_split(p, q);
         p.b_ld = round_up(s.co, tab_cols(p.tile));
         p.a_elems = int64_t(s.n) * p.Hp * p.Wp * s.ci;  // decoded, zero-bordered x
@@ -1719,7 +1753,7 @@ Plan plan_conv(const amsim_conv2d *d, int pass, int m_bits)
     } else if (pass == AMSIM_CONV_BWD_DATA) {
         const int64_t rows = bwd_data_rows(s);
         const int64_t q = ceil_div(s.kh, s.sh) * ceil_div(s.kw, s.sw) * ceil_div(s.co, 8);  // largest phase
-        p.tile = choose_tab_tile(rows, s.ci, q, 16, true, p.rl, 4);  // 8-row tiles spill here
+        p.tile = choose_tab_tile(rows, s.ci, q, 16, true, p.rl, 4, int64_t(s.sh) * s.sw);  // 8-row tiles spill here
         plan_tab_split(p, q);
         p.b_ld = round_up(s.ci, tab_cols(p.tile));
         int top, bottom, left, right;
@@ -1737,7 +1771,7 @@ Plan plan_conv(const amsim_conv2d *d, int pass, int m_bits)
     } else {
         const int64_t R = int64_t(s.kh) * s.kw * s.ci;
         const int64_t q = int64_t(s.n) * s.oh * ceil_div(s.ow, 8);
-        p.tile = choose_tab_tile(R, s.co, q, 16, true, p.rl, 8);
+        p.tile = choose_tab_tile(R, s.co, q, 16, true, p.rl, 8, 1);
         plan_tab_split(p, q);
         p.b_ld = round_up(s.co, tab_cols(p.tile));
         p.a_elems = int64_t(s.n) * p.Hp * p.Wp * s.ci;
