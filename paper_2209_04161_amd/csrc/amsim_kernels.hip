@@ -603,7 +603,7 @@ struct ConvShape {
 // The channel-inside-row layouts put the lanes' consecutive output pixels on consecutive words,
 // so each first-operand load of a wave touches a few cache lines instead of 64.
 // The reduction is cut into chunks of 8 steps (a tap of `count` steps holds ceil(count / 8));
-// split s of blockIdx.z sums chunks [s * chunks_per_split, (s + 1) * chunks_per_split) into its
+// split s (of tile z) sums chunks [s * chunks_per_split, (s + 1) * chunks_per_split) into its
 // own partial result, laid out like the final one; a fixed-order pass adds the partials.
 enum { OP_GEMM = 0, OP_FWD = 1, OP_BWD_DATA = 2, OP_BWD_WEIGHT = 3 };
 
@@ -618,14 +618,38 @@ struct TabArgs {
     const unsigned char *dot_rows;  // the same 1-byte rows in bf16-path staging order
     const int *eb;                  // [0] entry width, [1] 1 when the bf16 path may run
     int R, N;            // result rows and columns
-    int splits;          // reduction splits: blockIdx.z = (phase *) splits + split
+    int splits;          // reduction splits: tile z = (phase *) splits + split
     int chunks_per_split;  // reduction chunks (8 steps each) per split
     int64_t out_elems;   // elements of one split's partial result (splits > 1)
     int Mp, K;           // GEMM
     ConvShape s;
     int Hp, Wp;          // zero-padded x (FWD, BWD_WEIGHT)
     int OHp, OWp, pad_oh, pad_ow;  // zero-padded dy (BWD_DATA)
+    int tx, ty, tz;      // this workgroup's tile (row block, column block, phase/split); set on entry
 };
+
+// Workgroups go to the 8 XCDs in turn (linear id mod 8), and each XCD has its own L2.  The table
+// kernels give each XCD a contiguous range of tiles instead, in the order stride phase fastest
+// (phases differ in work, so each XCD gets all of them), then column blocks, row blocks, splits --
+// so that the workgroups an XCD runs together share first-operand rows and second-operand cache
+// lines in its L2.  Grids whose size is not a multiple of 8 keep the hardware order.
+__device__ __forceinline__ void tab_tile_id(int splits, int &tx, int &ty, int &tz)
+{
+    const uint32_t gx = gridDim.x, gy = gridDim.y, gz = gridDim.z, n = gx * gy * gz;
+    const uint32_t id = blockIdx.x + gx * (blockIdx.y + gy * blockIdx.z);
+    if (n % 8u != 0u) {
+        tx = int(blockIdx.x);
+        ty = int(blockIdx.y);
+        tz = int(blockIdx.z);
+        return;
+    }
+    const uint32_t lid = (id % 8u) * (n / 8u) + id / 8u;
+    const uint32_t phases = gz / uint32_t(splits);
+    const uint32_t ph = lid % phases, rest = lid / phases;
+    ty = int(rest % gy);
+    tx = int((rest / gy) % gx);
+    tz = int(ph * uint32_t(splits) + rest / (gx * gy));
+}
 
 struct TabTap {
     int ubase, ustride, bbase, count;
@@ -697,9 +721,9 @@ __device__ __forceinline__ void phase_dims(const ConvShape &s, int ph, int pw, i
     wq_n = pw < s.w ? (s.w - pw + s.sw - 1) / s.sw : 0;
 }
 
-// blockIdx.z = phase * splits + split (phase only for BWD_DATA, else 0)
-__device__ __forceinline__ int tab_phase(const TabArgs &a) { return int(blockIdx.z) / a.splits; }
-__device__ __forceinline__ int tab_split(const TabArgs &a) { return int(blockIdx.z) % a.splits; }
+// tile z = phase * splits + split (phase only for BWD_DATA, else 0)
+__device__ __forceinline__ int tab_phase(const TabArgs &a) { return a.tz / a.splits; }
+__device__ __forceinline__ int tab_split(const TabArgs &a) { return a.tz % a.splits; }
 
 template <int OP>
 __device__ __forceinline__ int tab_rows(const TabArgs &a)
@@ -900,13 +924,13 @@ __device__ __forceinline__ void tab_body(const TabArgs &a)
     float *pbs = reinterpret_cast<float *>(smem + 2 * SLAB);  // [2][KS][TNW] second-operand heads
 
     const int R = tab_rows<OP>(a);
-    if (int(blockIdx.x) * 64 * TM * WR >= R) return;  // uniform over the workgroup
+    if (a.tx * 64 * TM * WR >= R) return;  // uniform over the workgroup
     const int lane = threadIdx.x & 63;
     const int wave = wave_id();
     const int rg = wave % WR, cg = wave / WR;
-    const int row0 = blockIdx.x * (64 * TM * WR) + rg * (64 * TM) + lane;
+    const int row0 = a.tx * (64 * TM * WR) + rg * (64 * TM) + lane;
     const bool live = row0 - lane < R;  // wave-uniform: a wave past the end only stages
-    const int colw = blockIdx.y * TNW;  // first column of the workgroup
+    const int colw = a.ty * TNW;  // first column of the workgroup
     const int col0 = colw + cg * TN;    // first column of this wave
     // First-operand reads are raw buffer loads: voffset = the lane row's byte offset (range-checked,
     // reads past the buffer return 0), soffset = the wave-uniform step offset, which every tap keeps
@@ -1163,12 +1187,12 @@ __device__ __forceinline__ void tab_body_dot(const TabArgs &a)
     extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
 
     const int R = tab_rows<OP>(a);
-    if (int(blockIdx.x) * 64 * TM * NW >= R) return;  // uniform over the workgroup
+    if (a.tx * 64 * TM * NW >= R) return;  // uniform over the workgroup
     const int lane = threadIdx.x & 63;
     const int wave = wave_id();
-    const int row0 = blockIdx.x * (64 * TM * NW) + wave * (64 * TM) + lane;
+    const int row0 = a.tx * (64 * TM * NW) + wave * (64 * TM) + lane;
     const bool live = row0 - lane < R;  // wave-uniform
-    const int col0 = blockIdx.y * TN;
+    const int col0 = a.ty * TN;
     const __amdgpu_buffer_rsrc_t rres = __builtin_amdgcn_make_buffer_rsrc(
         const_cast<unsigned char *>(a.dot_rows), 0, int((kZeroRow + 1) * kTabRowEntries), 0x00020000);
 
@@ -1376,8 +1400,10 @@ __device__ __forceinline__ void tab_body_dot(const TabArgs &a)
 // hint the scheduler minimises registers and serialises the LDS gathers.
 // RL: log2 of the table row length, 7 (rows padded to 128 entries) for M <= 7, else M.
 template <int OP, int TM, int TN, int WR, int NW, int RL>
-__global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(4, 4))) void tab_kernel(TabArgs a)
+__global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(4, 4))) void tab_kernel(TabArgs args)
 {
+    TabArgs a = args;
+    tab_tile_id(a.splits, a.tx, a.ty, a.tz);
     const int eb = __builtin_amdgcn_readfirstlane(a.eb[0]);
     if constexpr (RL == 7 && TN == kDotCols && WR == NW) {
         if (__builtin_amdgcn_readfirstlane(a.eb[1]) != 0) {
