@@ -336,14 +336,23 @@ __global__ __launch_bounds__(256) void decode_t_kernel(const float *__restrict__
 }
 
 // C[r][c] = sum over z of part[z][r][c], z in order (deterministic).
-__global__ void reduce_splits_kernel(const float *__restrict__ part, int splits, int rows, int cols,
-                                     float *__restrict__ C, int64_t ldc)
+__global__ __launch_bounds__(256) void reduce_splits_kernel(const float *__restrict__ part, int splits, int rows,
+                                                            int cols, float *__restrict__ C, int64_t ldc)
 {
     const int64_t total = int64_t(rows) * cols;
     for (int64_t i = int64_t(blockIdx.x) * blockDim.x + threadIdx.x; i < total;
          i += int64_t(gridDim.x) * blockDim.x) {
-        float s = part[i];
-        for (int z = 1; z < splits; ++z) s += part[int64_t(z) * total + i];
+        // eight loads in flight, added in z order
+        float s = -0.0f;
+        int z = 0;
+        for (; z + 8 <= splits; z += 8) {
+            float v[8];
+#pragma unroll
+            for (int k = 0; k < 8; ++k) v[k] = part[int64_t(z + k) * total + i];
+#pragma unroll
+            for (int k = 0; k < 8; ++k) s += v[k];
+        }
+        for (; z < splits; ++z) s += part[int64_t(z) * total + i];
         const int64_t r = i / cols, c = i % cols;
         C[r * ldc + c] = s;
     }
@@ -387,6 +396,7 @@ __global__ void mul_ew_kernel(int64_t n, const float *__restrict__ a, const floa
 // GEMM kernel, which runs the matching specialisation.
 
 constexpr int kTabRowEntries = 128;  // rows padded to 2^7 entries
+constexpr int kPrepWorkgroups = 8;   // table preparation (M <= 7): workgroups sharing the rows
 // Table row kZeroRow (after the 2^M rows) holds zeros: the table path decodes second-operand
 // zeros, and names padding steps, with its index, so that a zero's row needs no test.
 constexpr int kZeroRow = kTabRowEntries;
@@ -407,8 +417,10 @@ __device__ __forceinline__ float tab_value(const unsigned char *p)
 // (ka, kb) at byte ka * EB.  With 1-byte entries it also writes dot_rows, the same bytes in the
 // order the bf16 path stages them: byte 4 * (ka % 32) + ka / 32 of row kb.  Then it reduces
 // the decode passes' exponent statistics (n_a words for the first operand, n_b for the second)
-// and decides whether the bf16 path is exact for this call.  One workgroup; flags[0] receives
-// the entry width, flags[1] 1 when the bf16 path may run.
+// and decides whether the bf16 path is exact for this call.  Each workgroup reads the whole table
+// (the entry width depends on all of it) and writes its share of the rows; workgroup 0 also
+// reduces the statistics and writes flags[0] = the entry width, flags[1] = 1 when the bf16 path
+// may run, and the zero rows.
 __global__ __launch_bounds__(1024) void prep_rows_kernel(const uint32_t *__restrict__ lut, int m,
                                                          unsigned char *__restrict__ dst,
                                                          unsigned char *__restrict__ dot_rows,
@@ -427,12 +439,13 @@ __global__ __launch_bounds__(1024) void prep_rows_kernel(const uint32_t *__restr
         const int k = int(threadIdx.x) + 1024 * i;
         v[i] = k < total ? lut[k] : 0u;
     }
+    const bool lead = blockIdx.x == 0;  // uniform over the workgroup
     uint32_t sa[8], sb[8];
 #pragma unroll
     for (int i = 0; i < 8; ++i) {
         const int k = int(threadIdx.x) + 1024 * i;
-        sa[i] = k < n_a ? stats_a[k] : 255u;
-        sb[i] = k < n_b ? stats_b[k] : 255u;
+        sa[i] = lead && k < n_a ? stats_a[k] : 255u;
+        sb[i] = lead && k < n_b ? stats_b[k] : 255u;
     }
     uint32_t low = 0u, alo = 255u, ahs = 0u, blo = 255u, bhs = 0u;
 #pragma unroll
@@ -480,14 +493,17 @@ __global__ __launch_bounds__(1024) void prep_rows_kernel(const uint32_t *__restr
         const bool special = ((a_hs | b_hs) >> 8) != 0u;
         const bool window = stats_a != nullptr && !special && a_lo + b_lo >= 128u && a_hi + b_hi <= 380u &&
                             b_hi <= 253u;
-        flags[0] = eb;
-        flags[1] = (eb == 1 && window) ? 1 : 0;
+        if (lead) {
+            flags[0] = eb;
+            flags[1] = (eb == 1 && window) ? 1 : 0;
+        }
     }
     __syncthreads();
     const int eb = s_eb;
     // Rows: thread -> (kb = consecutive threads, group of 4 entries), so that the LDS reads of a
     // wave are consecutive words; each thread stores 4 entries.
-    for (int i = threadIdx.x; i < n * ((n + 3) / 4); i += blockDim.x) {
+    const int tid = int(blockIdx.x * blockDim.x + threadIdx.x), nthreads = int(gridDim.x * blockDim.x);
+    for (int i = tid; i < n * ((n + 3) / 4); i += nthreads) {
         const int kb = i % n, k4 = (i / n) * 4;
         if (eb == 1) {
             uint32_t word = 0u;
@@ -510,13 +526,15 @@ __global__ __launch_bounds__(1024) void prep_rows_kernel(const uint32_t *__restr
         }
     }
     // the zero row
-    for (int i = threadIdx.x; i < kTabRowEntries * eb / 4; i += blockDim.x)
-        reinterpret_cast<uint32_t *>(dst + size_t(kZeroRow) * kTabRowEntries * eb)[i] = 0u;
-    if (eb == 1 && threadIdx.x < kTabRowEntries / 4)
-        reinterpret_cast<uint32_t *>(dot_rows + size_t(kZeroRow) * kTabRowEntries)[threadIdx.x] = 0u;
+    if (lead) {
+        for (int i = threadIdx.x; i < kTabRowEntries * eb / 4; i += blockDim.x)
+            reinterpret_cast<uint32_t *>(dst + size_t(kZeroRow) * kTabRowEntries * eb)[i] = 0u;
+        if (eb == 1 && threadIdx.x < kTabRowEntries / 4)
+            reinterpret_cast<uint32_t *>(dot_rows + size_t(kZeroRow) * kTabRowEntries)[threadIdx.x] = 0u;
+    }
     // bf16-path rows: word g of row kb holds the bytes of entries g, g + 32, g + 64, g + 96.
     if (eb == 1) {
-        for (int i = threadIdx.x; i < n * 32; i += blockDim.x) {
+        for (int i = tid; i < n * 32; i += nthreads) {
             const int kb = i % n, g = i / n;
             uint32_t word = 0u;
 #pragma unroll
@@ -1838,7 +1856,7 @@ inline uint32_t *stats_b(char *ws, const Plan &p)
 int prep_rows(const uint32_t *lut, int m_bits, char *ws, const Plan &p, int n_a, int n_b, hipStream_t st)
 {
     if (p.rl == 7) {
-        hipLaunchKernelGGL(prep_rows_kernel, dim3(1), dim3(1024), 0, st, lut, m_bits,
+        hipLaunchKernelGGL(prep_rows_kernel, dim3(kPrepWorkgroups), dim3(1024), 0, st, lut, m_bits,
                            reinterpret_cast<unsigned char *>(ws + p.off_rows),
                            reinterpret_cast<unsigned char *>(ws + p.off_dot_rows), stats_a(ws, p), n_a,
                            stats_b(ws, p), n_b, reinterpret_cast<int *>(ws + p.off_eb));
