@@ -110,8 +110,9 @@ int approx_gemm(int trans_a, int trans_b, int64_t m, int64_t n, int64_t k, const
  * NHWC activations, HWIO weights ([kh][kw][c_in][c_out]), explicit four-sided zero padding
  * (TF "SAME" is an asymmetric pad), stride >= 1, no dilation or groups (none in the paper).
  * OH = (h + pad_top + pad_bottom - kh) / stride_h + 1, OW likewise; both must be >= 1.
- * All sizes must be >= 1 (pads >= 0) and every tensor must have fewer than 2^31 elements
- * (else AMSIM_ERR_UNSUPPORTED). */
+ * All sizes must be >= 1 (pads >= 0).  AMSIM_ERR_UNSUPPORTED when a (padded) tensor reaches
+ * 2^29 elements, a pad or kernel side reaches 65536, stride_h * stride_w exceeds 32, a channel
+ * count exceeds 1048560, or w or OW reaches 4096. */
 typedef struct amsim_conv2d {
     int n, h, w, c_in, c_out, kh, kw, stride_h, stride_w, pad_top, pad_bottom, pad_left, pad_right;
 } amsim_conv2d;

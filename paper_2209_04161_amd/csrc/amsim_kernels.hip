@@ -228,11 +228,13 @@ __global__ __launch_bounds__(256) void decode_pad_kernel(const float *__restrict
     store_stats(st, stats, blockIdx.x);
 }
 
-// Decoded NHWC tensor re-laid out as [n][hp][c][wp] inside a zero border:
-// dst[n][y][ch][x] = decode(src[n][y-top][x-left][ch]) where that pixel exists, decoded +0
-// elsewhere.  A workgroup takes one padded image row at a time: the source row (w pixels x cc
-// channels at a time, contiguous loads) goes through LDS as [channel][x] (row pitch w | 1, odd,
-// so the transposing stores do not collide in banks), then each wave writes whole channel rows.
+// Decoded NHWC tensor as step-pair records [n][hp][cp][wp] (cp = ceil(c / 2)) inside a zero
+// border: record (b, y, q, x) = {index word of channel 2q, heads of channels 2q and 2q + 1 as bf16
+// (2q in the low half), index word of channel 2q + 1} of pixel (y - top, x - left) where it
+// exists, zeros elsewhere; a channel past the end is a decoded +0.  A workgroup takes one padded
+// image row at a time: the source row (w pixels x cc channels at a time, cc even, contiguous
+// loads) goes through LDS as [channel][x] (row pitch w | 1, odd, so the transposing stores do not
+// collide in banks), then each wave writes whole record rows.
 constexpr int kNhcwTile = 8192;  // words of the LDS tile: cc * (w | 1) <= kNhcwTile
 
 __global__ __launch_bounds__(256) void decode_pad_nhcw_kernel(const float *__restrict__ src, int n, int h, int w, int c,
@@ -241,14 +243,14 @@ __global__ __launch_bounds__(256) void decode_pad_nhcw_kernel(const float *__res
                                                               uint32_t *__restrict__ stats, int cc)
 {
     __shared__ uint32_t tile[kNhcwTile];
-    const int ws = w | 1;
+    const int ws = w | 1, cp = (c + 1) / 2;
     const int wave = int(threadIdx.x) >> 6, lane = int(threadIdx.x) & 63;
     ExpStats st;
     for (int rr = blockIdx.x; rr < n * hp; rr += gridDim.x) {
         const int b = rr / hp, y = rr - b * hp, ih = y - top;
-        uint32_t *dimg = dst + int64_t(rr) * c * wp;
+        uint32_t *dimg = dst + int64_t(rr) * cp * wp * 3;
         if (unsigned(ih) >= unsigned(h)) {  // a padding row (uniform over the workgroup)
-            for (int i = threadIdx.x; i < c * wp; i += 256) dimg[i] = 0u;
+            for (int i = threadIdx.x; i < cp * wp * 3; i += 256) dimg[i] = 0u;
             continue;
         }
         const float *srow = src + (int64_t(b) * h + ih) * w * c;
@@ -273,11 +275,19 @@ __global__ __launch_bounds__(256) void decode_pad_nhcw_kernel(const float *__res
                 }
             }
             __syncthreads();
-            for (int ch = wave; ch < ccn; ch += 4) {
-                uint32_t *drow = dimg + int64_t(c0 + ch) * wp;
+            for (int q = wave; q < (ccn + 1) / 2; q += 4) {
+                uint32_t *drow = dimg + (int64_t(c0 / 2 + q) * wp) * 3;
+                const bool odd = 2 * q + 1 < ccn;
                 for (int xo = lane; xo < wp; xo += 64) {
                     const int ix = xo - left;
-                    drow[xo] = unsigned(ix) < unsigned(w) ? tile[ch * ws + ix] : 0u;
+                    uint32_t w0 = 0u, w1 = 0u;
+                    if (unsigned(ix) < unsigned(w)) {
+                        w0 = tile[(2 * q) * ws + ix];
+                        w1 = odd ? tile[(2 * q + 1) * ws + ix] : 0u;
+                    }
+                    drow[xo * 3 + 0] = w0 & 0xFFFFu;
+                    drow[xo * 3 + 1] = (w0 >> 16) | (w1 & 0xFFFF0000u);
+                    drow[xo * 3 + 2] = w1 & 0xFFFFu;
                 }
             }
         }
@@ -674,8 +684,9 @@ struct TabTap {
     int pbase;  // pair records: the tap's first record (records of pair j / 2 are ustride apart)
 };
 
-// The GEMM's first operand is decoded into one 12-byte record per lane row and step pair
-// (j, j + 1), j even, instead of one word per element: j's 16-bit table-index field (an LDS byte
+// The first operand of the GEMM and of the forward and backward-data passes (whose steps are
+// channels) is decoded into one 12-byte record per lane row and step pair (j, j + 1), j even,
+// instead of one word per element: j's 16-bit table-index field (an LDS byte
 // offset on the bf16 path) as a word, the two mantissa-cleared operands as bf16
 // (pa(j) | pa(j+1) << 16), and j+1's index word.  The bf16 path loads a record with one
 // instruction and uses it as loaded: no masking of the indices, no pairing of the heads.  A
@@ -683,7 +694,7 @@ struct TabTap {
 template <int OP>
 constexpr bool split_a()
 {
-    return OP == OP_GEMM;
+    return OP == OP_GEMM || OP == OP_FWD || OP == OP_BWD_DATA;
 }
 constexpr uint32_t kPairRecordBytes = 12;
 
@@ -781,6 +792,27 @@ __device__ __forceinline__ void tab_row(const TabArgs &a, int row, int &abase, i
     }
 }
 
+// Pair records: the lane row's record offset (element offset with the step axis halved).
+template <int OP>
+__device__ __forceinline__ int tab_row_rec(const TabArgs &a, int row)
+{
+    const ConvShape &s = a.s;
+    if constexpr (OP == OP_GEMM) {
+        return row;
+    } else if constexpr (OP == OP_FWD) {
+        const int ow = row % s.ow, oh = (row / s.ow) % s.oh, n = row / (s.ow * s.oh);
+        return (n * a.Hp + oh * s.sh) * ((s.ci + 1) / 2) * a.Wp + ow * s.sw;  // records [n][hp][ci/2][wp]
+    } else if constexpr (OP == OP_BWD_DATA) {
+        const int ph = tab_phase(a) / s.sw, pw = tab_phase(a) % s.sw;
+        int hq_n, wq_n;
+        phase_dims(s, ph, pw, hq_n, wq_n);
+        const int wq = row % wq_n, hq = (row / wq_n) % hq_n, n = row / (wq_n * hq_n);
+        return (n * a.OHp + hq) * ((s.co + 1) / 2) * a.OWp + wq;  // records [n][ohp][co/2][owp]
+    } else {
+        return 0;
+    }
+}
+
 // Taps of the reduction (BWD_DATA: of this workgroup's stride phase).
 template <int OP>
 __device__ __forceinline__ int tab_taps(const TabArgs &a)
@@ -829,7 +861,7 @@ __device__ __forceinline__ TabTap tab_tap_raw(const TabArgs &a, int tap)
         t.ubase = kh * s.ci * a.Wp + kw;
         t.ustride = a.Wp;
         t.bbase = tap * s.ci;
-        t.pbase = 0;
+        t.pbase = kh * ((s.ci + 1) / 2) * a.Wp + kw;
     } else if constexpr (OP == OP_BWD_DATA) {
         const int ph = tab_phase(a) / s.sw, pw = tab_phase(a) % s.sw;
         const int kh0 = (ph + s.pt) % s.sh, kw0 = (pw + s.pl) % s.sw;
@@ -840,7 +872,7 @@ __device__ __forceinline__ TabTap tab_tap_raw(const TabArgs &a, int tap)
         t.ubase = (dh + a.pad_oh) * s.co * a.OWp + dw + a.pad_ow;  // >= 0: the padding covers every dh, dw
         t.ustride = a.OWp;
         t.bbase = (kh * s.kw + kw) * s.co;
-        t.pbase = 0;
+        t.pbase = (dh + a.pad_oh) * ((s.co + 1) / 2) * a.OWp + dw + a.pad_ow;
     } else {
         const int n = tap / s.oh, oh = tap % s.oh;
         t.count = s.ow;
@@ -959,7 +991,10 @@ __device__ __forceinline__ void tab_body(const TabArgs &a)
         const int row = row0 + 64 * r;
         int ab = 0;
         int64_t ob = 0;
-        if (row < R) tab_row<OP>(a, row, ab, ob);
+        if (row < R) {
+            tab_row<OP>(a, row, ab, ob);
+            if constexpr (split_a<OP>()) ab = tab_row_rec<OP>(a, row);
+        }
         abase[r] = ab;
     }
     const AView<TM> av = make_aview<OP, TM>(a, abase);
@@ -1220,7 +1255,10 @@ __device__ __forceinline__ void tab_body_dot(const TabArgs &a)
         const int row = row0 + 64 * r;
         int ab = 0;
         int64_t ob = 0;
-        if (row < R) tab_row<OP>(a, row, ab, ob);
+        if (row < R) {
+            tab_row<OP>(a, row, ab, ob);
+            if constexpr (split_a<OP>()) ab = tab_row_rec<OP>(a, row);
+        }
         abase[r] = ab;
     }
     const AView<TM> av = make_aview<OP, TM>(a, abase);
@@ -1741,7 +1779,7 @@ int check_conv(const amsim_conv2d *d)
     if (xp >= lim || yp >= lim || w >= lim || y >= lim || d->pad_top >= 65536 || d->pad_bottom >= 65536 ||
         d->pad_left >= 65536 || d->pad_right >= 65536 || d->kh >= 65536 || d->kw >= 65536 ||
         int64_t(d->stride_h) * d->stride_w > 32 || d->c_in > 65535 * 16 || d->c_out > 65535 * 16 ||
-        d->w >= kNhcwTile || ow >= kNhcwTile)
+        d->w >= kNhcwTile / 2 || ow >= kNhcwTile / 2)
         return AMSIM_ERR_UNSUPPORTED;
     return AMSIM_OK;
 }
@@ -1788,7 +1826,7 @@ Plan plan_conv(const amsim_conv2d *d, int pass, int m_bits)
         p.tile = choose_tab_tile(npix_out, s.co, q, 16, true, p.rl, 8, 1);
         plan_tab_split(p, q);
         p.b_ld = round_up(s.co, tab_cols(p.tile));
-        p.a_elems = int64_t(s.n) * p.Hp * p.Wp * s.ci;  // decoded, zero-bordered x
+        p.a_elems = int64_t(s.n) * p.Hp * p.Wp * ((s.ci + 1) / 2) * 3;  // zero-bordered x as step-pair records
         p.out_elems = npix_out * s.co;
         p.off_a = o;
         o += align_up(size_t(p.a_elems) * 4);
@@ -1806,7 +1844,7 @@ Plan plan_conv(const amsim_conv2d *d, int pass, int m_bits)
         p.pad_ow = left;
         p.OHp = top + s.oh + bottom;
         p.OWp = left + s.ow + right;
-        p.a_elems = int64_t(s.n) * p.OHp * p.OWp * s.co;  // decoded, zero-padded dy
+        p.a_elems = int64_t(s.n) * p.OHp * p.OWp * ((s.co + 1) / 2) * 3;  // zero-padded dy as step-pair records
         p.out_elems = npix_in * s.ci;
         p.off_a = o;
         o += align_up(size_t(p.a_elems) * 4);
@@ -2086,7 +2124,8 @@ static int decode_nhwc(const float *src, int n, int h, int w, int c, int top, in
 static int decode_nhcw(const float *src, int n, int h, int w, int c, int top, int left, int hp, int wp, uint32_t *dst,
                        int m_bits, int shift, uint32_t *stats, hipStream_t st)
 {
-    const int cc = std::max(1, std::min(c, kNhcwTile / (w | 1)));  // channels per LDS tile
+    int cc = std::max(2, std::min(c, kNhcwTile / (w | 1)));  // channels per LDS tile
+    if (cc < c) cc &= ~1;  // chunks hold whole channel pairs
     const int grid = int(std::min<int64_t>(int64_t(n) * hp, kStatSlots));  // one padded image row at a time
     hipLaunchKernelGGL(decode_pad_nhcw_kernel, dim3(grid), dim3(256), 0, st, src, n, h, w, c, top, left, hp, wp, dst,
                        m_bits, shift, 0u, stats, cc);

@@ -129,6 +129,11 @@ def test_workspace_size_queries(L):
         binding.amsim_conv2d_workspace_size(d, 3, 7)
     with pytest.raises(binding.AmsimError):
         binding.amsim_conv2d_workspace_size(dict(d, kh=11), 0, 7)   # kernel larger than padded image
+    # the width limit of the channel-inside-row decode (w and OW below 4096)
+    wide = dict(d, n=1, h=1, w=4095, c_in=1, c_out=1, kh=1, kw=1, pad_top=0, pad_bottom=0, pad_left=0, pad_right=0)
+    assert binding.amsim_conv2d_workspace_size(wide, 0, 7) > 0
+    with pytest.raises(binding.AmsimError):
+        binding.amsim_conv2d_workspace_size(dict(wide, w=4096), 0, 7)
     with pytest.raises(binding.AmsimError):
         binding.amsim_gemm_workspace_size(0, 0, 4, 4, 4, 12)
 
