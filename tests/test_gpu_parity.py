@@ -141,6 +141,55 @@ def test_gemm_zero_sums_keep_their_sign(B, k):
     assert_within_tolerance(C, ref, S, "gemm zero rows K=%d" % k)
 
 
+def test_conv_zero_sums_keep_their_sign(B):
+    """Exactly-zero conv outputs carry the sign rule of R10 through the record layout and the
+    bf16 path's sign pass, in all three passes.  No padded taps (the GPU's zero border would add
+    signed zeros there, which the oracle skips): pad 0, and a 1x1 kernel for backward-data."""
+    m = 7
+    lut = dev_lut(B, "mitchell", m)
+
+    def check(got, ref, S, what):
+        zero = ref == 0.0
+        assert zero.sum() > 0, what
+        assert_bits_equal(got[zero], ref[zero].astype(np.float32), what + " zero outputs")
+        assert_within_tolerance(got, ref, S, what)
+
+    p = W.conv_desc(2, 6, 9, 7, 12, 3, 3, 1, 0)
+    x = W.normal((2, 6, 9, 7), 1.0, 71)
+    w = W.normal((3, 3, 7, 12), 1.0, 72)
+    x[0] = 0.0                       # first image: +0 ...
+    x[0, 2:4, 3:6, :] = -0.0         # ... with a block of -0
+    w[..., :4] = -np.abs(w[..., :4])  # negative, positive and -0 output channels
+    w[..., 4:8] = np.abs(w[..., 4:8])
+    w[..., 8] = -0.0
+    y = host(B.approx_conv2d_fwd(p, cuda(x), cuda(w), lut, m))
+    ref, S = oracle.conv2d_fwd(oracle.MITCHELL, m, p, x, w)
+    check(y, ref, S, "fwd")
+
+    p = W.conv_desc(2, 5, 7, 13, 9, 1, 1, 1, 0)
+    dy = W.normal((2, 5, 7, 9), 1.0, 73)
+    w = W.normal((1, 1, 13, 9), 1.0, 74)
+    dy[1] = 0.0
+    dy[1, :, :3, :] = -0.0
+    w[0, 0, :5, :] = -np.abs(w[0, 0, :5, :])
+    w[0, 0, 5:9, :] = np.abs(w[0, 0, 5:9, :])
+    w[0, 0, 9, :] = -0.0
+    dx = host(B.approx_conv2d_bwd_data(p, cuda(dy), cuda(w), lut, m))
+    ref, S = oracle.conv2d_bwd_data(oracle.MITCHELL, m, p, dy, w)
+    check(dx, ref, S, "bwd_data")
+
+    p = W.conv_desc(2, 6, 9, 5, 11, 3, 3, 1, 0)
+    x = W.normal((2, 6, 9, 5), 1.0, 75)
+    dy = W.normal((2, 4, 7, 11), 1.0, 76)
+    x[..., 0] = 0.0                  # input channel 0: +0, channel 1: -0
+    x[..., 1] = -0.0
+    dy[..., :4] = -np.abs(dy[..., :4])
+    dy[..., 4:8] = np.abs(dy[..., 4:8])
+    dw = host(B.approx_conv2d_bwd_weight(p, cuda(x), cuda(dy), lut, m))
+    ref, S = oracle.conv2d_bwd_weight(oracle.MITCHELL, m, p, x, dy)
+    check(dw, ref, S, "bwd_weight")
+
+
 def test_conv_single_product_shapes_bit_exact(B):
     """1x1 conv with one input channel (fwd), one output position (bwd_weight) and one output
     channel with a 1x1 kernel (bwd_data): every output is a single product."""
