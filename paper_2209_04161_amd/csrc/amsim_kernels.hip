@@ -345,26 +345,44 @@ __global__ __launch_bounds__(256) void decode_t_kernel(const float *__restrict__
     store_stats(st, stats, blockIdx.y * gridDim.x + blockIdx.x);
 }
 
-// C[r][c] = sum over z of part[z][r][c], z in order (deterministic).
+// C[r][c] = sum over z of part[z][r][c] in a fixed order (deterministic): the splits are cut into
+// G consecutive groups, summed in z order within a group (eight loads in flight) and the group
+// sums then added in group order.  G > 1 gives outputs with many splits more threads.  Workgroups
+// of 256 threads: thread (g, o) for g < G, o < 256 / G.
 __global__ __launch_bounds__(256) void reduce_splits_kernel(const float *__restrict__ part, int splits, int rows,
-                                                            int cols, float *__restrict__ C, int64_t ldc)
+                                                            int cols, float *__restrict__ C, int64_t ldc, int G)
 {
+    __shared__ float s_part[256];
     const int64_t total = int64_t(rows) * cols;
-    for (int64_t i = int64_t(blockIdx.x) * blockDim.x + threadIdx.x; i < total;
-         i += int64_t(gridDim.x) * blockDim.x) {
-        // eight loads in flight, added in z order
+    const int opb = 256 / G;  // outputs per workgroup and pass
+    const int g = int(threadIdx.x) / opb, ol = int(threadIdx.x) % opb;
+    const int per = (splits + G - 1) / G, z0 = min(splits, g * per), z1 = min(splits, z0 + per);
+    for (int64_t base = int64_t(blockIdx.x) * opb; base < total; base += int64_t(gridDim.x) * opb) {
+        const int64_t i = base + ol;
         float s = -0.0f;
-        int z = 0;
-        for (; z + 8 <= splits; z += 8) {
-            float v[8];
+        if (i < total) {
+            int z = z0;
+            for (; z + 8 <= z1; z += 8) {
+                float v[8];
 #pragma unroll
-            for (int k = 0; k < 8; ++k) v[k] = part[int64_t(z + k) * total + i];
+                for (int k = 0; k < 8; ++k) v[k] = part[int64_t(z + k) * total + i];
 #pragma unroll
-            for (int k = 0; k < 8; ++k) s += v[k];
+                for (int k = 0; k < 8; ++k) s += v[k];
+            }
+            for (; z < z1; ++z) s += part[int64_t(z) * total + i];
         }
-        for (; z < splits; ++z) s += part[int64_t(z) * total + i];
-        const int64_t r = i / cols, c = i % cols;
-        C[r * ldc + c] = s;
+        if (G > 1) {
+            __syncthreads();  // the previous pass has read s_part
+            s_part[threadIdx.x] = s;
+            __syncthreads();
+            if (g == 0) {
+                for (int k = 1; k < G; ++k) s += s_part[k * opb + ol];
+            }
+        }
+        if (g == 0 && i < total) {
+            const int64_t r = i / cols, c = i % cols;
+            C[r * ldc + c] = s;
+        }
     }
 }
 
@@ -928,9 +946,11 @@ __device__ __forceinline__ void tab_fetch(u32x4 (&stage)[CPT], float (&stage_pb)
     constexpr int ROWB = (1 << RL) * EB;
     constexpr uint32_t kPad = RL == 7 ? kZeroRowWord : 0u;  // a padding step's second operand: +0
     constexpr int PIECES = ROWB / 16;
+    constexpr int TOTAL = tab_slab_steps(TNW, RL, EB) * TNW * PIECES;
 #pragma unroll
     for (int i = 0; i < CPT; ++i) {
         const int c = threadIdx.x + i * NT;
+        if (CPT * NT > TOTAL && c >= TOTAL) break;  // the workgroup size does not divide the slab
         const int slot = c / (TNW * PIECES);
         const int t = (c / PIECES) % TNW;
         const int piece = c % PIECES;
@@ -952,6 +972,7 @@ __device__ __forceinline__ void tab_commit(const u32x4 (&stage)[CPT], const floa
 #pragma unroll
     for (int i = 0; i < CPT; ++i) {
         const int c = threadIdx.x + i * NT;
+        if (CPT * NT > SLAB / 16 && c >= SLAB / 16) break;
         *reinterpret_cast<u32x4 *>(smem + buf * SLAB + c * 16) = stage[i];
         if (c % PIECES == 0) pbs[buf * KS * TNW + c / PIECES] = stage_pb[i];
     }
@@ -968,8 +989,7 @@ __device__ __forceinline__ void tab_body(const TabArgs &a)
     constexpr int ROWB = (1 << RL) * EB;        // a table row: 2^RL entries
     constexpr int KS = tab_slab_steps(TNW, RL, EB);
     constexpr int SLAB = KS * TNW * ROWB;
-    constexpr int CPT = SLAB / 16 / NT;         // pieces per thread per slab
-    static_assert(CPT * 16 * NT == SLAB, "slab must split evenly over the workgroup");
+    constexpr int CPT = (SLAB / 16 + NT - 1) / NT;  // pieces per thread per slab (the last round partial)
     extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
     float *pbs = reinterpret_cast<float *>(smem + 2 * SLAB);  // [2][KS][TNW] second-operand heads
 
@@ -1119,8 +1139,8 @@ typedef uint16_t u16x2_t __attribute__((ext_vector_type(2)));
 
 constexpr int kDotCols = 8;                          // columns per entry
 constexpr int kDotStepBytes = kTabRowEntries * 16;   // 128 entries x 16 bytes
-// Steps per slab: 8 for 4-wave workgroups, 16 for 8-wave ones (each thread stages one step's
-// entry group, 32 threads per step); a slab is 2 KiB per step.
+// Steps per slab: 2 per wave (each thread stages one step's entry group, 32 threads per step);
+// a slab is 2 KiB per step.
 constexpr int dot_slab_steps(int nw) { return nw * 2; }
 
 // 16 bytes of LDS at byte address off + imm.  The table kernels use no static LDS, so their
@@ -1272,16 +1292,18 @@ __device__ __forceinline__ void tab_body_dot(const TabArgs &a)
     // second-operand words `sbw` having arrived during slab s - 1) and the second-operand words
     // of slab s + 2 are loaded into `sbw2`.  With 8-step slabs (4-wave workgroups) the words'
     // latency would otherwise be exposed once per slab; 16-step slabs fetch both in slab s.
-    constexpr bool AHEAD2 = NW == 4;
+    constexpr bool AHEAD2 = NW <= 4;
     u32x4 sbw[2], sbw2[2];
     uint32_t srw[kDotCols];
     float acc[TM][TN];
     init_acc(acc);
-    // First-operand data of four step pairs, as a ring: pair kp of a slab is in w[kp % 4]; while
+    // First-operand data of RS step pairs, as a ring: pair kp of a slab is in w[kp % RS]; while
     // it is used, pair kp + 2 (of this slab, or the next slab's first two for the last two pairs)
-    // is loaded into w[(kp + 2) % 4].  A slab holds a multiple of four pairs, so after a full slab
+    // is loaded into w[(kp + 2) % RS].  A slab holds a multiple of RS pairs, so after a full slab
     // the next slab's first two pairs sit in w[0], w[1].
-    uint32_t w[4][NA][TM];
+    constexpr int RS = (KS / 2) % 4 == 0 ? 4 : KS / 2;
+    static_assert(RS >= 3 && (KS / 2) % RS == 0, "ring of step pairs");
+    uint32_t w[RS][NA][TM];
     // The slab after (t, tp_, c): its tap, cursor and whether it is in this split's range (if not,
     // `o` stays `t`, so that loads aimed at it stay in bounds).
     auto advance = [&](const TabTap &t, int tp_, int c, TabTap &o, int &otap, int &oc, bool &ok)
@@ -1341,11 +1363,11 @@ __device__ __forceinline__ void tab_body_dot(const TabArgs &a)
         for (int kp = 0; kp < KS / 2; ++kp) {
             if (kp >= npairs) break;
             if (kp + 2 < KS / 2)
-                dot_load_pair<OP, TM>(w[(kp + 2) % 4], av, cur, c0 + 2 * kp + 4);
+                dot_load_pair<OP, TM>(w[(kp + 2) % RS], av, cur, c0 + 2 * kp + 4);
             else
-                dot_load_pair<OP, TM>(w[(kp + 2) % 4], av, nxt, nc0 + 2 * (kp + 2 - KS / 2));
-            const uint32_t(&a0)[TM] = w[kp % 4][0];
-            const uint32_t(&a1)[TM] = w[kp % 4][1];
+                dot_load_pair<OP, TM>(w[(kp + 2) % RS], av, nxt, nc0 + 2 * (kp + 2 - KS / 2));
+            const uint32_t(&a0)[TM] = w[kp % RS][0];
+            const uint32_t(&a1)[TM] = w[kp % RS][1];
 #pragma unroll
             for (int r = 0; r < TM; ++r) {
                 // entry byte offset = the mantissa field * 16 (the index plane, or the word's low
@@ -1356,7 +1378,7 @@ __device__ __forceinline__ void tab_body_dot(const TabArgs &a)
                 const u32x4 Y = lds_load_b128(o1, BOFF + (2 * kp + 1) * kDotStepBytes);
                 uint32_t pa;  // (pa(k), pa(k+1)) as bf16
                 if constexpr (SPLIT)
-                    pa = w[kp % 4][NA - 1][r];
+                    pa = w[kp % RS][NA - 1][r];
                 else
                     pa = __builtin_amdgcn_perm(a1[r], a0[r], 0x07060302u);
 #pragma unroll
@@ -1534,12 +1556,11 @@ constexpr TabCand kWideCands[] = {{8, 4, 8, 8}, {4, 8, 8, 8}, {2, 8, 4, 4}, {1, 
 constexpr TabCand kWide11Cands[] = {{8, 4, 8, 8}, {4, 4, 8, 8}, {2, 4, 4, 4}, {1, 4, 4, 4}};
 
 // Tile and reduction split for `rows` x `cols` outputs (times `phases` independent grids) over q
-// reduction chunks of 8 steps.  Cost = the products a tile computes (rows padded to whole waves)
-// times an issue-cost estimate per product, divided by how well the launch fills the chip: the
-// workgroups per CU that LDS and registers allow (four waves per SIMD) give the slots of one
-// round, a last round that is partly empty is lost, and a launch under one round runs its CUs
-// below full occupancy.  Only a launch under one round is split (at least min_chunks chunks per
-// split); splits add their partial sums' traffic and a reduction launch.
+// reduction chunks of 8 steps.  The products a tile computes (rows padded to whole waves) times
+// an issue-cost estimate per product, spread over the workgroups; the workgroups per CU that LDS
+// and registers allow (four waves per SIMD) give the slots of one round, and a partly empty last
+// round costs a whole one.  Only a launch under one round is split (at least min_chunks chunks
+// per split).
 Tile choose_tab_tile(int64_t rows, int64_t cols, int64_t q, int64_t min_chunks, bool allow_split, int rl,
                      int max_tm, int64_t phases)
 {
@@ -1576,14 +1597,25 @@ Tile choose_tab_tile(int64_t rows, int64_t cols, int64_t q, int64_t min_chunks, 
         const int64_t max_split = allow_split && double(base) < slots
                                       ? std::max<int64_t>(1, std::min<int64_t>(q / std::max<int64_t>(1, min_chunks), 4096))
                                       : 1;
+        // steps per slab (the bf16 path's, else a 2-byte table's) and a slab's time for one wave:
+        // the staging fetch (a dependent pair of loads, ~0.7 us) plus its products at ~1.15 (bf16
+        // path) or ~3.7 (exact path) VALU instructions each, 4 clocks per instruction at 2.4 GHz
+        const double slab_steps = pair ? 2.0 * c.nw : double(tab_slab_steps(int(ctile), rl, 2));
+        const double slab_ns = 700.0 + double(c.tm * c.tn) * slab_steps * (pair ? 1.15 : 3.7) * 4.0 / 2.4;
+        // In ns, per round of workgroups: a workgroup's products at its share of the chip
+        // (~20 T products/s, 28 cost units per ps, over all slots), or the slabs it walks through
+        // one after another, whichever is longer; splits add their partial sums' traffic, a
+        // launch, and the reduction's dependent loads (up to 32 groups of 8 per output).
         auto cost_of = [&](int64_t s) {
             const int64_t cps = ceil_div(q, s);           // chunks per split
             const int64_t s_eff = ceil_div(q, cps);       // the splits that chunking leaves
-            const double load = double(base * s_eff) / slots;  // workgroups per slot
-            const double rounds = std::ceil(load);
-            const double fill = (load / rounds) * std::pow(std::min(1.0, load), 0.6);
-            double cst = work * per_product / fill;
-            if (s_eff > 1) cst += outputs * double(s_eff) * 45.0 + 1.4e8;
+            const double wgs = double(base * s_eff);
+            const double rounds = std::ceil(wgs / slots);
+            const double issue_ns = (work / wgs) * per_product * slots / 28000.0;
+            const double latency_ns = std::ceil(double(cps) * 8.0 / slab_steps) * slab_ns;
+            double cst = rounds * std::max(issue_ns, latency_ns);
+            if (s_eff > 1)
+                cst += outputs * double(s_eff) * 8.0 / 5000.0 + 5000.0 + std::ceil(double(s_eff) / 256.0) * 800.0;
             return std::make_pair(cst, s_eff);
         };
         // candidate splits: none, the most allowed, and those that fill k whole rounds of slots
@@ -1655,6 +1687,17 @@ int ensure_attributes()
 {
     std::call_once(g_attr_once, set_attributes);
     return g_attr_err == hipSuccess ? AMSIM_OK : AMSIM_ERR_HIP;
+}
+
+// Split reduction of `splits` partial results of rows x cols into C (leading dimension ldc).
+void launch_reduce(const float *part, int splits, int rows, int cols, float *C, int64_t ldc, hipStream_t st)
+{
+    const int64_t outputs = int64_t(rows) * cols;
+    int G = 1;
+    while (G < 32 && outputs * G < 65536 && splits >= 16 * G) G *= 2;
+    const int64_t blocks = std::min<int64_t>(ceil_div(outputs, 256 / G), 65536);
+    hipLaunchKernelGGL(reduce_splits_kernel, dim3(unsigned(blocks)), dim3(256), 0, st, part, splits, rows, cols, C, ldc,
+                       G);
 }
 
 int launch_status()
@@ -1734,7 +1777,7 @@ Plan plan_gemm(int64_t m, int64_t n, int64_t k, int m_bits)
 {
     Plan p{};
     p.rl = row_log(m_bits);
-    p.tile = choose_tab_tile(m, n, ceil_div(k, 8), 32, true, p.rl, 8, 1);
+    p.tile = choose_tab_tile(m, n, ceil_div(k, 8), 4, true, p.rl, 8, 1);
     p.a_ld = round_up(m, int64_t(64) * p.tile.wr * p.tile.tm);
     p.b_ld = round_up(n, tab_cols(p.tile));
     plan_tab_split(p, ceil_div(k, 8));
@@ -1823,7 +1866,7 @@ Plan plan_conv(const amsim_conv2d *d, int pass, int m_bits)
     p.Wp = d->w + d->pad_left + d->pad_right;
     if (pass == AMSIM_CONV_FWD) {
         const int64_t q = int64_t(s.kh) * s.kw * ceil_div(s.ci, 8);
-        p.tile = choose_tab_tile(npix_out, s.co, q, 16, true, p.rl, 8, 1);
+        p.tile = choose_tab_tile(npix_out, s.co, q, 4, true, p.rl, 8, 1);
         plan_tab_split(p, q);
         p.b_ld = round_up(s.co, tab_cols(p.tile));
         p.a_elems = int64_t(s.n) * p.Hp * p.Wp * ((s.ci + 1) / 2) * 3;  // zero-bordered x as step-pair records
@@ -1835,7 +1878,7 @@ Plan plan_conv(const amsim_conv2d *d, int pass, int m_bits)
     } else if (pass == AMSIM_CONV_BWD_DATA) {
         const int64_t rows = bwd_data_rows(s);
         const int64_t q = ceil_div(s.kh, s.sh) * ceil_div(s.kw, s.sw) * ceil_div(s.co, 8);  // largest phase
-        p.tile = choose_tab_tile(rows, s.ci, q, 16, true, p.rl, 4, int64_t(s.sh) * s.sw);  // 8-row tiles spill here
+        p.tile = choose_tab_tile(rows, s.ci, q, 4, true, p.rl, 4, int64_t(s.sh) * s.sw);  // 8-row tiles spill here
         plan_tab_split(p, q);
         p.b_ld = round_up(s.ci, tab_cols(p.tile));
         int top, bottom, left, right;
@@ -1853,7 +1896,7 @@ Plan plan_conv(const amsim_conv2d *d, int pass, int m_bits)
     } else {
         const int64_t R = int64_t(s.kh) * s.kw * s.ci;
         const int64_t q = int64_t(s.n) * s.oh * ceil_div(s.ow, 8);
-        p.tile = choose_tab_tile(R, s.co, q, 16, true, p.rl, 8, 1);
+        p.tile = choose_tab_tile(R, s.co, q, 4, true, p.rl, 8, 1);
         plan_tab_split(p, q);
         p.b_ld = round_up(s.co, tab_cols(p.tile));
         p.a_elems = int64_t(s.n) * p.Hp * p.Wp * s.ci;
@@ -2079,8 +2122,7 @@ int approx_gemm(int trans_a, int trans_b, int64_t m, int64_t n, int64_t k, const
     }
     if (rc != AMSIM_OK) return AMSIM_ERR_HIP;
     if (p.splits > 1) {
-        hipLaunchKernelGGL(reduce_splits_kernel, dim3(grid_for(m * n)), dim3(256), 0, st,
-                           reinterpret_cast<const float *>(ws + p.off_part), p.splits, int(m), int(n), C, ldc);
+        launch_reduce(reinterpret_cast<const float *>(ws + p.off_part), p.splits, int(m), int(n), C, ldc, st);
         if (launch_status() != AMSIM_OK) return AMSIM_ERR_HIP;
     }
     return AMSIM_OK;
@@ -2164,8 +2206,7 @@ int approx_conv2d_fwd(const amsim_conv2d *desc, const float *x, const float *w, 
         rc = launch_tab<OP_FWD>(p, a, grid, st);
     }
     if (rc != AMSIM_OK || p.splits == 1) return rc;
-    hipLaunchKernelGGL(reduce_splits_kernel, dim3(grid_for(p.out_elems)), dim3(256), 0, st,
-                       reinterpret_cast<const float *>(ws + p.off_part), p.splits, int(rows), s.co, y, int64_t(s.co));
+    launch_reduce(reinterpret_cast<const float *>(ws + p.off_part), p.splits, int(rows), s.co, y, int64_t(s.co), st);
     return launch_status();
 }
 
@@ -2201,9 +2242,8 @@ int approx_conv2d_bwd_data(const amsim_conv2d *desc, const float *dy, const floa
         rc = launch_tab<OP_BWD_DATA>(p, a, grid, st);
     }
     if (rc != AMSIM_OK || p.splits == 1) return rc;
-    hipLaunchKernelGGL(reduce_splits_kernel, dim3(grid_for(p.out_elems)), dim3(256), 0, st,
-                       reinterpret_cast<const float *>(ws + p.off_part), p.splits, s.n * s.h * s.w, s.ci, dx,
-                       int64_t(s.ci));
+    launch_reduce(reinterpret_cast<const float *>(ws + p.off_part), p.splits, s.n * s.h * s.w, s.ci, dx, int64_t(s.ci),
+                  st);
     return launch_status();
 }
 
@@ -2240,8 +2280,7 @@ int approx_conv2d_bwd_weight(const amsim_conv2d *desc, const float *x, const flo
     }
     if (rc != AMSIM_OK) return AMSIM_ERR_HIP;
     if (p.splits > 1) {
-        hipLaunchKernelGGL(reduce_splits_kernel, dim3(grid_for(int64_t(R) * s.co)), dim3(256), 0, st,
-                           reinterpret_cast<const float *>(ws + p.off_part), p.splits, R, s.co, dw, int64_t(s.co));
+        launch_reduce(reinterpret_cast<const float *>(ws + p.off_part), p.splits, R, s.co, dw, int64_t(s.co), st);
         return launch_status();
     }
     return AMSIM_OK;
