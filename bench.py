@@ -295,7 +295,65 @@ def extras(B, W, torch, np, dev, lut7, m7, A, Bm, C):
     ex["lenet5_b64_fwd_bwd"] = {"ms": round(ms, 3), "approx_macs": lenet_macs,
                                "gmacs_per_s": round(lenet_macs / ms / 1e6, 1)}
     log("LeNet-5 stack done")
+    ex["lenet5_b64_train_step_layers"] = lenet_train_step(torch, W, np, dev, lutb, mb)
+    log("LeNet-5 training step done")
+    ex["native_fp32_vendor"] = native_fp32(torch, W, dev, A, Bm, C)
+    log("native FP32 vendor kernels done")
     return ex
+
+
+def lenet_train_step(torch, W, np, dev, lut, m_bits):
+    """One training step (forward, autograd backward, SGD update) of LeNet-5 built from the
+    autograd layers, batch 64: the per-batch training time the paper tabulates, on synthetic data."""
+    from paper_2209_04161_amd import modules
+    F = torch.nn.functional
+    torch.manual_seed(0)
+    net = torch.nn.ModuleList([modules.AMConv2d(1, 6, 5, lut, m_bits, padding="same"),
+                               modules.AMConv2d(6, 16, 5, lut, m_bits),
+                               modules.AMLinear(400, 120, lut, m_bits), modules.AMLinear(120, 84, lut, m_bits),
+                               modules.AMLinear(84, 10, lut, m_bits)])
+    x = torch.from_numpy(W.uniform((64, 28, 28, 1), 0.0, 1.0, 6000)).to(dev)
+    labels = torch.from_numpy(np.random.default_rng(6010).integers(0, 10, 64)).to(dev)
+    opt = torch.optim.SGD(net.parameters(), lr=0.01)
+
+    def pool(t):
+        return F.max_pool2d(t.permute(0, 3, 1, 2), 2).permute(0, 2, 3, 1).contiguous()
+
+    def step():
+        opt.zero_grad(set_to_none=True)
+        h = pool(torch.relu(net[0](x)))
+        h = pool(torch.relu(net[1](h))).reshape(64, 400)
+        h = torch.relu(net[3](torch.relu(net[2](h))))
+        F.cross_entropy(net[4](h), labels).backward()
+        opt.step()
+
+    return {"ms": round(_time_call(torch, step, 10), 3)}
+
+
+def native_fp32(torch, W, dev, A, Bm, C):
+    """The step's GEMM and ResNet 3x3 passes with the native FP32 multiply, in the vendor
+    libraries torch calls (hipBLASLt/rocBLAS GEMM, MIOpen convolution): the paper's
+    approximate-over-native ratio on this GPU.  Context only; nothing of the path runs here."""
+    mm, cd = torch.backends.cuda.matmul.allow_tf32, torch.backends.cudnn.allow_tf32
+    torch.backends.cuda.matmul.allow_tf32 = False  # full FP32 products
+    torch.backends.cudnn.allow_tf32 = False
+    try:
+        out = {"gemm_4096_ms": round(_time_call(torch, lambda: torch.matmul(A, Bm, out=C), 5), 3)}
+        cv = W.RESNET_3X3["conv"]
+        x_h, w_h, dy_h = W.resnet_conv_inputs(cv, seed=3000)
+        # NHWC data viewed as NCHW (channels-last strides), HWIO weights as OIHW
+        x = torch.from_numpy(x_h).to(dev).permute(0, 3, 1, 2)
+        w = torch.from_numpy(w_h).to(dev).permute(3, 2, 0, 1).contiguous()
+        dy = torch.from_numpy(dy_h).to(dev).permute(0, 3, 1, 2)
+        pad = cv["pad_top"]
+        F = torch.nn.functional
+        for name, fn in (("conv3x3_fwd_ms", lambda: F.conv2d(x, w, padding=pad)),
+                         ("conv3x3_bwd_data_ms", lambda: torch.nn.grad.conv2d_input(x.shape, w, dy, padding=pad)),
+                         ("conv3x3_bwd_weight_ms", lambda: torch.nn.grad.conv2d_weight(x, w.shape, dy, padding=pad))):
+            out[name] = round(_time_call(torch, fn, 5), 3)
+        return out
+    finally:
+        torch.backends.cuda.matmul.allow_tf32, torch.backends.cudnn.allow_tf32 = mm, cd
 
 
 def cpu_baseline(frac, A_h, B_h, cv, x_h, w_h, dy_h, m_bits):
