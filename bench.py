@@ -237,6 +237,14 @@ def extras(B, W, torch, np, dev, lut7, m7, A, Bm, C):
             sweep["n%d_m%d" % (n, mb)] = {"ms": round(ms, 3), "gmacs_per_s": round(n ** 3 / ms / 1e6, 1)}
     ex["gemm_sweep_mitchell"] = sweep
     log("GEMM size sweep done")
+    # the 4096^3 GEMM without a table: Mitchell computed from the operands' bits, and the native
+    # FP32 multiply, in the same simple register-tiled kernel (the paper's AMSim-vs-direct figure)
+    d = {}
+    for mode in ("mitchell", "native"):
+        ms = _time_call(torch, lambda: B.approx_gemm_direct(A, Bm, mode, m7, out=C), 2)
+        d[mode] = {"ms": round(ms, 2), "gmacs_per_s": round(M * N * K / ms / 1e6, 1)}
+    ex["gemm_4096_direct"] = d
+    log("direct GEMM done")
     # ResNet 3x3 with post-ReLU activations (about half exact zeros) instead of |N(0,1)|
     cv = W.RESNET_3X3["conv"]
     x_h, w_h, dy_h = W.resnet_conv_inputs(cv, seed=4500)

@@ -106,6 +106,24 @@ int approx_gemm(int trans_a, int trans_b, int64_t m, int64_t n, int64_t k, const
                 const float *B, int64_t ldb, float *C, int64_t ldc, const uint32_t *lut, int m_bits,
                 void *workspace, size_t workspace_bytes, void *stream);
 
+/* Direct evaluation: the GEMM with no table, for the comparison the paper draws for AMSim
+ * (Sec. "AMSim", its figure of GEMM run time with AMSim, with a direct simulation of the
+ * multiplier and with the native multiply).
+ *   AMSIM_DIRECT_NATIVE    C = A B with the native FP32 multiply (each product rounded, then
+ *                          added); m_bits is ignored.
+ *   AMSIM_DIRECT_MITCHELL  every product Mitchell's multiplier on the top m_bits mantissa bits,
+ *                          computed from the operands' bits in the kernel -- the same products as
+ *                          approx_gemm with a Mitchell table (same zero / denormal / Inf / NaN /
+ *                          overflow rules), bit for bit.
+ * Row-major A [m][k] (lda >= k) and B [k][n] (ldb >= n), C [m][n] (ldc >= n) overwritten; device
+ * memory; sums start from -0.0 (k == 0 fills C with -0.0).  No workspace.  Returns
+ * AMSIM_ERR_INVALID_ARG for an unknown mode, AMSIM_ERR_UNSUPPORTED for m_bits outside [1, 11]
+ * (Mitchell) or sizes from 2^31 on. */
+#define AMSIM_DIRECT_NATIVE 0
+#define AMSIM_DIRECT_MITCHELL 1
+int approx_gemm_direct(int mode, int m_bits, int64_t m, int64_t n, int64_t k, const float *A, int64_t lda,
+                       const float *B, int64_t ldb, float *C, int64_t ldc, void *stream);
+
 /* ----------------------------------------------------------------- 2-D convolution ------
  * NHWC activations, HWIO weights ([kh][kw][c_in][c_out]), explicit four-sided zero padding
  * (TF "SAME" is an asymmetric pad), stride >= 1, no dilation or groups (none in the paper).

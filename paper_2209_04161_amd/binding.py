@@ -23,6 +23,8 @@ AMSIM_ERR_IO = -6
 AMSIM_CONV_FWD = 0
 AMSIM_CONV_BWD_DATA = 1
 AMSIM_CONV_BWD_WEIGHT = 2
+AMSIM_DIRECT_NATIVE = 0
+AMSIM_DIRECT_MITCHELL = 1
 
 AMSIM_KERNEL_GEMM = 0
 AMSIM_KERNEL_CONV_FWD = 1
@@ -82,6 +84,8 @@ def lib():
         "approx_conv2d_bwd_data": ([cp, vp, vp, vp, vp, ctypes.c_int, vp, sz, vp], ctypes.c_int),
         "approx_conv2d_bwd_weight": ([cp, vp, vp, vp, vp, ctypes.c_int, vp, sz, vp], ctypes.c_int),
         "approx_mul_ew": ([i64, vp, vp, vp, vp, ctypes.c_int, vp], ctypes.c_int),
+        "approx_gemm_direct": ([ctypes.c_int, ctypes.c_int, i64, i64, i64, vp, i64, vp, i64, vp, i64, vp],
+                               ctypes.c_int),
         "amsim_profile_start": ([ctypes.c_int], ctypes.c_int),
         "amsim_profile_stop": ([], ctypes.c_int),
         "amsim_profile_read": ([ctypes.c_int, ctypes.POINTER(ctypes.c_int), ctypes.POINTER(ctypes.c_double)],
@@ -220,6 +224,26 @@ def approx_gemm(A, B, lut, m_bits, trans_a=False, trans_b=False, out=None, works
     _check(lib().approx_gemm(int(trans_a), int(trans_b), m, n, k, _ptr(A), A.shape[1], _ptr(B), B.shape[1],
                              _ptr(out), ldc, _ptr(lut), int(m_bits), _ptr(workspace), workspace.numel(), _stream()),
            "approx_gemm")
+    return out
+
+
+def approx_gemm_direct(A, B, mode, m_bits=7, out=None):
+    """C = A @ B without a table: mode "native" (FP32 multiply) or "mitchell" (Mitchell's
+    multiplier on the top m_bits mantissa bits, computed from the operands' bits)."""
+    torch = _torch()
+    _check_f32(A, "A")
+    _check_f32(B, "B")
+    modes = {"native": AMSIM_DIRECT_NATIVE, "mitchell": AMSIM_DIRECT_MITCHELL}
+    if mode not in modes:
+        raise ValueError("mode must be 'native' or 'mitchell'")
+    m, k = A.shape
+    if B.shape[0] != k:
+        raise ValueError("inner dimensions differ")
+    n = B.shape[1]
+    if out is None:
+        out = torch.empty((m, n), dtype=torch.float32, device=A.device)
+    _check(lib().approx_gemm_direct(modes[mode], int(m_bits), m, n, k, _ptr(A), A.stride(0), _ptr(B), B.stride(0),
+                                    _ptr(out), out.stride(0), _stream()), "approx_gemm_direct")
     return out
 
 

@@ -345,6 +345,98 @@ __global__ __launch_bounds__(256) void decode_t_kernel(const float *__restrict__
     store_stats(st, stats, blockIdx.y * gridDim.x + blockIdx.x);
 }
 
+// Direct evaluation, the comparison the paper draws for AMSim (Sec. "AMSim", its figure of GEMM
+// run time for AMSim, direct simulation and the native multiply): the same GEMM with no table.
+//   DIRECT_NATIVE    every product the native FP32 multiply, then an FP32 add.
+//   DIRECT_MITCHELL  every product Mitchell's multiplier computed from the operands' bits.  With
+//                    ka, kb the top-M mantissa fields, its mantissa product on the truncated
+//                    fractions x = ka / 2^M, y = kb / 2^M is 1 + x + y below 2 and 2 (x + y) from
+//                    2 on -- in FP32 bits 0x3F800000 + (ka + kb) << (23 - M) in both cases (a sum
+//                    that reaches 2^M carries into the exponent field) -- then times pa * pb as
+//                    on the table path, with the same zero, overflow, Inf and NaN rules.
+// 64 x 64 outputs per workgroup of 256 threads, 4 x 4 per thread; 16-step tiles of both operands
+// go through LDS step-major, so each thread reads its 4 rows and 4 columns with 16-byte loads.
+enum { DIRECT_NATIVE = 0, DIRECT_MITCHELL = 1 };
+constexpr int kDirTile = 64, kDirK = 16;
+
+template <int MODE>
+__global__ __launch_bounds__(256) void direct_gemm_kernel(const float *__restrict__ A, int64_t lda,
+                                                          const float *__restrict__ B, int64_t ldb,
+                                                          float *__restrict__ C, int64_t ldc, int m, int n, int k,
+                                                          int mb)
+{
+    // [0]: raw operand (native) or head; [1]: Mitchell's shifted field (B's with the bias added)
+    __shared__ __attribute__((aligned(16))) uint32_t sa[2][kDirK][kDirTile];
+    __shared__ __attribute__((aligned(16))) uint32_t sb[2][kDirK][kDirTile];
+    const int tx = int(threadIdx.x) % 16, ty = int(threadIdx.x) / 16;
+    const int row0 = int(blockIdx.x) * kDirTile, col0 = int(blockIdx.y) * kDirTile;
+    const int sh = 23 - mb;
+    float acc[4][4];
+    init_acc(acc);
+    for (int k0 = 0; k0 < k; k0 += kDirK) {
+        for (int i = threadIdx.x; i < kDirTile * kDirK; i += 256) {
+            const int r = i / kDirK, kk = i % kDirK;  // A: consecutive threads along k
+            const int gr = row0 + r, gk = k0 + kk;
+            const uint32_t u = (gr < m && gk < k) ? __float_as_uint(A[int64_t(gr) * lda + gk]) : 0u;
+            if constexpr (MODE == DIRECT_NATIVE) {
+                sa[0][kk][r] = u;
+            } else {
+                const uint32_t w = amsim_decode(u, mb, 0);
+                sa[0][kk][r] = w & kHeadMask;
+                sa[1][kk][r] = (w & ((1u << mb) - 1u)) << sh;
+            }
+        }
+        for (int i = threadIdx.x; i < kDirTile * kDirK; i += 256) {
+            const int kk = i / kDirTile, c = i % kDirTile;  // B: consecutive threads along columns
+            const int gc = col0 + c, gk = k0 + kk;
+            const uint32_t u = (gc < n && gk < k) ? __float_as_uint(B[int64_t(gk) * ldb + gc]) : 0u;
+            if constexpr (MODE == DIRECT_NATIVE) {
+                sb[0][kk][c] = u;
+            } else {
+                const uint32_t w = amsim_decode(u, mb, 0);
+                sb[0][kk][c] = w & kHeadMask;
+                sb[1][kk][c] = ((w & ((1u << mb) - 1u)) << sh) + 0x3F800000u;
+            }
+        }
+        __syncthreads();
+        const int kn = min(kDirK, k - k0);
+        for (int kk = 0; kk < kn; ++kk) {
+            const u32x4 a0 = *reinterpret_cast<const u32x4 *>(&sa[0][kk][4 * ty]);
+            const u32x4 b0 = *reinterpret_cast<const u32x4 *>(&sb[0][kk][4 * tx]);
+            if constexpr (MODE == DIRECT_NATIVE) {
+#pragma unroll
+                for (int i = 0; i < 4; ++i)
+#pragma unroll
+                    for (int j = 0; j < 4; ++j) {
+                        const float p = __uint_as_float(a0[i]) * __uint_as_float(b0[j]);
+                        acc[i][j] = acc[i][j] + p;
+                    }
+            } else {
+                const u32x4 a1 = *reinterpret_cast<const u32x4 *>(&sa[1][kk][4 * ty]);
+                const u32x4 b1 = *reinterpret_cast<const u32x4 *>(&sb[1][kk][4 * tx]);
+#pragma unroll
+                for (int i = 0; i < 4; ++i)
+#pragma unroll
+                    for (int j = 0; j < 4; ++j) {
+                        const float v = __uint_as_float(a1[i] + b1[j]);
+                        acc[i][j] = __builtin_fmaf(v, __uint_as_float(a0[i]) * __uint_as_float(b0[j]), acc[i][j]);
+                    }
+            }
+        }
+        __syncthreads();
+    }
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        const int r = row0 + 4 * ty + i;
+        if (r >= m) continue;
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            const int c = col0 + 4 * tx + j;
+            if (c < n) C[int64_t(r) * ldc + c] = acc[i][j];
+        }
+    }
+}
+
 // C[r][c] = sum over z of part[z][r][c] in a fixed order (deterministic): the splits are cut into
 // G consecutive groups, summed in z order within a group (eight loads in flight) and the group
 // sums then added in group order.  G > 1 gives outputs with many splits more threads.  Workgroups
@@ -2284,6 +2376,32 @@ int approx_conv2d_bwd_weight(const amsim_conv2d *desc, const float *x, const flo
         return launch_status();
     }
     return AMSIM_OK;
+}
+
+int approx_gemm_direct(int mode, int m_bits, int64_t m, int64_t n, int64_t k, const float *A, int64_t lda,
+                       const float *B, int64_t ldb, float *C, int64_t ldc, void *stream)
+{
+    if (mode != AMSIM_DIRECT_NATIVE && mode != AMSIM_DIRECT_MITCHELL) return AMSIM_ERR_INVALID_ARG;
+    if (mode == AMSIM_DIRECT_MITCHELL && !valid_m(m_bits)) return AMSIM_ERR_UNSUPPORTED;
+    if (m < 0 || n < 0 || k < 0) return AMSIM_ERR_INVALID_ARG;
+    if (m == 0 || n == 0) return AMSIM_OK;
+    if (!C || ldc < n) return AMSIM_ERR_INVALID_ARG;
+    const int64_t lim = int64_t(1) << 31;
+    if (m >= lim || n >= lim || k >= lim || ceil_div(n, kDirTile) > 65535) return AMSIM_ERR_UNSUPPORTED;
+    hipStream_t st = static_cast<hipStream_t>(stream);
+    if (k == 0) {
+        hipLaunchKernelGGL(fill_kernel, dim3(grid_for(m * n)), dim3(256), 0, st, C, int(m), int(n), ldc, -0.0f);
+        return launch_status();
+    }
+    if (!A || !B || lda < k || ldb < n) return AMSIM_ERR_INVALID_ARG;
+    const dim3 grid(unsigned(ceil_div(m, kDirTile)), unsigned(ceil_div(n, kDirTile)));
+    if (mode == AMSIM_DIRECT_NATIVE)
+        hipLaunchKernelGGL(direct_gemm_kernel<DIRECT_NATIVE>, grid, dim3(256), 0, st, A, lda, B, ldb, C, ldc, int(m),
+                           int(n), int(k), 0);
+    else
+        hipLaunchKernelGGL(direct_gemm_kernel<DIRECT_MITCHELL>, grid, dim3(256), 0, st, A, lda, B, ldb, C, ldc,
+                           int(m), int(n), int(k), m_bits);
+    return launch_status();
 }
 
 int approx_mul_ew(int64_t n, const float *a, const float *b, float *c, const uint32_t *lut, int m_bits, void *stream)

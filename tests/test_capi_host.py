@@ -162,6 +162,13 @@ def test_device_entry_points_reject_bad_arguments_before_launching(L):
     assert L.approx_mul_ew(4, None, fake, fake, fake, 7, None) == binding.AMSIM_ERR_INVALID_ARG
     assert L.approx_mul_ew(4, fake, fake, fake, fake, 12, None) == binding.AMSIM_ERR_UNSUPPORTED
     assert L.approx_mul_ew(0, None, None, None, None, 7, None) == binding.AMSIM_OK
+    direct = L.approx_gemm_direct
+    assert direct(2, 7, 4, 4, 4, fake, 4, fake, 4, fake, 4, None) == binding.AMSIM_ERR_INVALID_ARG
+    assert direct(binding.AMSIM_DIRECT_MITCHELL, 12, 4, 4, 4, fake, 4, fake, 4, fake, 4, None) == binding.AMSIM_ERR_UNSUPPORTED
+    assert direct(binding.AMSIM_DIRECT_NATIVE, 0, 4, 4, 4, None, 4, fake, 4, fake, 4, None) == binding.AMSIM_ERR_INVALID_ARG
+    assert direct(binding.AMSIM_DIRECT_NATIVE, 0, 4, 4, 4, fake, 3, fake, 4, fake, 4, None) == binding.AMSIM_ERR_INVALID_ARG
+    assert direct(binding.AMSIM_DIRECT_NATIVE, 0, 4, 4, 4, fake, 4, fake, 4, fake, 3, None) == binding.AMSIM_ERR_INVALID_ARG
+    assert direct(binding.AMSIM_DIRECT_NATIVE, 0, 0, 4, 4, None, 4, None, 4, None, 4, None) == binding.AMSIM_OK
 
 
 def test_product_path_does_not_touch_the_oracle():
