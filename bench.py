@@ -228,7 +228,7 @@ def extras(B, W, torch, np, dev, lut7, m7, A, Bm, C):
     log("M=11 GEMM done")
     # the same GEMM at smaller sizes, 128-entry table rows (M=7) and 2048-entry rows (M=11)
     sweep = {}
-    for n in (512, 1024, 2048):
+    for n in (64, 512, 1024, 2048):
         a, b = (torch.from_numpy(t).to(dev) for t in W.gemm_inputs(n, n, n, "normal", seed=5100 + n))
         c = torch.empty((n, n), dtype=torch.float32, device=dev)
         for mb, lt in ((7, lut7), (11, lut11)):

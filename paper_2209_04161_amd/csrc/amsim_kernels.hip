@@ -17,11 +17,13 @@
 //   acc + c rounded once.
 //
 // Kernel shape: lanes of a wave own output rows (64*TM rows per wave), the wave's TN output
-// columns are wave-uniform (their operand words come through scalar loads), waves of a
-// workgroup take neighbouring column groups.  For M <= 7 the table lives in LDS, stored
-// transposed (second-operand mantissa major) so that the lanes' first-operand mantissas --
-// the varying part of the index -- fall into different banks.  For M = 8..11 the table is
-// read from global memory (L2 / MALL).  Products are never fed to MFMA: they are not IEEE.
+// columns are wave-uniform, waves of a workgroup lie along rows and/or columns.  Per slab of
+// steps the workgroup stages into LDS, for each of its columns and steps, the table row that
+// the column's second-operand mantissa selects (128 entries for M <= 7, 2^M for M = 8..11);
+// lanes gather from it with their first-operand mantissas.  For 1-byte tables and operands
+// whose exponents keep every product normal, the bf16 pair path folds the second operand into
+// the staged entries and adds two steps' products with one dot instruction.  Products are
+// never fed to MFMA: they are not IEEE.
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
@@ -38,8 +40,6 @@ namespace {
 
 constexpr uint32_t kIdxMask = 0x003FFFFFu;
 constexpr uint32_t kHeadMask = 0xFFC00000u;
-constexpr int kWaves = 4;           // waves per workgroup (column groups)
-constexpr int kThreads = 64 * kWaves;
 
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x3 __attribute__((ext_vector_type(3)));  // buffer_load_dwordx3 results only
@@ -499,21 +499,20 @@ __global__ void mul_ew_kernel(int64_t n, const float *__restrict__ a, const floa
     }
 }
 
-// ------------------------------------------------------------------ GEMM, per-column tables
-// For M <= 7 the fastest form keeps, per k-step and output column j, the table row selected
-// by that column's second-operand mantissa kb(k, j) -- LUT[. ][kb], indexed by the first
-// operand's mantissa -- at a fixed LDS address.  Lanes then gather with
+// ------------------------------------------------------------------ per-column tables
+// The exact path keeps, per step and output column j, the table row selected by that column's
+// second-operand mantissa kb(k, j) -- LUT[. ][kb], indexed by the first operand's mantissa --
+// at a fixed LDS address.  Lanes then gather with
 //   ds_read  v, (lane's first-operand mantissa * entry bytes)  offset:(fixed row address)
 // so no per-product address arithmetic is left: per product one LDS gather, one multiply
 // (pa * pb) and one fma.  Rows are copied from a transposed copy of the table in global
-// memory, slab by slab (KS k-steps), double-buffered with one barrier per slab.
+// memory, slab by slab (KS steps), double-buffered with one barrier per slab.
 //
 // Rows are stored compressed when the table allows it without loss: 1 byte per entry when
 // every entry's low 16 mantissa bits are zero (e.g. Mitchell at M <= 7), 2 bytes when the low 8
-// are zero (e.g. the exact truncated product at M <= 7), else the 4-byte rebiased float.  A
-// 128-entry row of bytes spans exactly the 32 LDS banks once, so its gathers are conflict-free.
-// The entry width is decided on the device by the table-preparation kernel and read by the
-// GEMM kernel, which runs the matching specialisation.
+// are zero (e.g. the exact truncated product at M <= 7, Mitchell at M = 8..11), else the 4-byte
+// rebiased float.  The entry width is decided on the device by the table-preparation kernels
+// and read by the table kernel, which runs the matching specialisation.
 
 constexpr int kTabRowEntries = 128;  // rows padded to 2^7 entries
 constexpr int kPrepWorkgroups = 8;   // table preparation (M <= 7): workgroups sharing the rows
@@ -731,10 +730,11 @@ struct ConvShape {
 // Which operation the table kernel evaluates.  Every one is a sum over "taps": runs of
 // consecutive reduction steps j = 0 .. count-1 whose first-operand word sits at
 //   A[lane row base + ubase + j * ustride]
-// and whose second-operand row is Bd[bbase + j].
+// (pair records: record pbase + (j / 2) * ustride from the row's record base) and whose
+// second-operand row is Bd[bbase + j].
 //   GEMM         one tap of K steps: rows i, A = op(A) k-major, row base i
 //   FWD          tap = (kh, kw): rows (n, oh, ow), A = zero-padded x stored [n][h][ci][w], j = ci
-//   BWD_DATA     tap = valid (kh, kw) of the stride phase in blockIdx.z: rows (n, hq, wq),
+//   BWD_DATA     tap = valid (kh, kw) of the stride phase in tile z: rows (n, hq, wq),
 //                A = zero-padded dy stored [n][h][co][w], j = co; weights read as [kh][kw][co][ci]
 //   BWD_WEIGHT   tap = output row (n, oh): rows (kh, kw, ci), A = zero-padded x (NHWC), j = ow,
 //                B = dy
@@ -1620,23 +1620,20 @@ inline int64_t ceil_div(int64_t x, int64_t m) { return (x + m - 1) / m; }
 inline int row_log(int m_bits) { return m_bits > 7 ? m_bits : 7; }
 
 struct Tile {
-    int tm, tn, split;
-    int wr = kWaves;  // table kernels: waves along rows (the rest take column groups)
-    int nw = kWaves;  // table kernels: waves per workgroup
+    int tm = 1, tn = 4, split = 1;
+    int wr = 4;  // waves along rows (the rest take column groups)
+    int nw = 4;  // waves per workgroup
 };
 
 
-// Per-column-table kernels (M <= 7).  Candidates are the instantiated (TM, TN, WR, NW) tiles; the
-// choice minimises an estimate of issue time: padded work x cost per product, scaled up when the
-// grid, after splitting the reduction, cannot fill the chip (2048 waves: two 4-wave workgroups or
-// one 8-wave workgroup per CU and... its LDS allows, counted in waves).  Cost per product: the
-// inner loop (~1.2 VALU ops on the bf16 pair path, which 8-column tiles with all waves on rows
-// take for 1-byte tables; 3 on the exact path), per-step overhead (~2.5 per row, ~4 per lane), and
-// the table staging, which is per workgroup and slab, so its share per product falls with the
-// workgroup's rows (64 * TM * WR; weight fitted on MI355X: a 64 x 32 backward-weight tile ran 2.4x
-// slower than a 256 x 8 one, a 768-row GEMM tile 15% slower than a 1024-row one).  `red` is the
-// reduction length in chunks and `min_steps` the fewest chunks a split may hold.  (TM = 3 with
-// WR = 1 would exceed the 128-VGPR budget: its 32-column slab staging alone holds 40 registers.)
+// Tile candidates: the instantiated (TM, TN, WR, NW) tiles, per table-row length.  The cost per
+// product used to choose among them (choose_tab_tile): the inner loop (~1.2 VALU ops on the bf16
+// pair path, which 8-column tiles with all waves on rows take for 1-byte tables; 3 on the exact
+// path), per-step overhead (~2.5 per row, ~4 per lane), and the table staging, which is per
+// workgroup and slab, so its share per product falls with the workgroup's rows (64 * TM * WR) and
+// grows with the row length (weight fitted on MI355X: a 64 x 32 backward-weight tile ran 2.4x
+// slower than a 256 x 8 one, a 768-row GEMM tile 15% slower than a 1024-row one).  Tiles whose
+// registers would spill past the 128-VGPR budget are left out.
 struct TabCand {
     int tm, tn, wr, nw;
 };
