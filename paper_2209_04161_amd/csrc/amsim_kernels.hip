@@ -1229,10 +1229,11 @@ __device__ __forceinline__ void tab_body(const TabArgs &a)
 typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
 typedef uint16_t u16x2_t __attribute__((ext_vector_type(2)));
 
-constexpr int kDotCols = 8;                          // columns per entry
-constexpr int kDotStepBytes = kTabRowEntries * 16;   // 128 entries x 16 bytes
-// Steps per slab: 2 per wave (each thread stages one step's entry group, 32 threads per step);
-// a slab is 2 KiB per step.
+// Columns per entry DC: 8, or 4 for narrow outputs.  Entries sit 16 bytes apart either way (the
+// first operand's index field is the byte offset ka * 16); a 4-column entry fills half a slot.
+constexpr bool dot_cols_ok(int dc) { return dc == 8 || dc == 4; }
+constexpr int kDotStepBytes = kTabRowEntries * 16;  // 128 entries, 16-byte slots
+// Steps per slab: 2 per wave (each thread stages one step's entry group, 32 threads per step).
 constexpr int dot_slab_steps(int nw) { return nw * 2; }
 
 // 16 bytes of LDS at byte address off + imm.  The table kernels use no static LDS, so their
@@ -1242,6 +1243,13 @@ typedef __attribute__((address_space(3))) const u32x4 lds_u32x4;
 __device__ __forceinline__ u32x4 lds_load_b128(uint32_t off, uint32_t imm)
 {
     return reinterpret_cast<lds_u32x4 *>(uintptr_t(off))[imm / 16];
+}
+
+// The same for 8 bytes (imm a multiple of 8).
+typedef __attribute__((address_space(3))) const u32x2 lds_u32x2;
+__device__ __forceinline__ u32x2 lds_load_b64(uint32_t off, uint32_t imm)
+{
+    return reinterpret_cast<lds_u32x2 *>(uintptr_t(off))[imm / 8];
 }
 
 __device__ __forceinline__ float dot2_bf16(uint32_t x, uint32_t y, float c)
@@ -1256,8 +1264,9 @@ __device__ __forceinline__ uint32_t add_u16x2(uint32_t x, uint32_t y)
 }
 
 // Staging of one slab: thread -> step slot (tid / 32) and entry group g (tid % 32), which builds
-// the entries ka = g, g + 32, g + 64, g + 96.  Fetch, in two parts: the slot's 8 second-operand
+// the entries ka = g, g + 32, g + 64, g + 96.  Fetch, in two parts: the slot's DC second-operand
 // words, then, per column, the 4 bytes of its table row that hold those entries.
+template <int DC>
 __device__ __forceinline__ void dot_fetch_b(u32x4 (&bw)[2], const TabTap &tp, int c0, const uint32_t *__restrict__ Bd,
                                             int Np, int colw)
 {
@@ -1266,19 +1275,19 @@ __device__ __forceinline__ void dot_fetch_b(u32x4 (&bw)[2], const TabTap &tp, in
     if (j < tp.count) {
         const u32x4 *src = reinterpret_cast<const u32x4 *>(Bd + int64_t(tp.bbase + j) * Np + colw);
         bw[0] = src[0];
-        bw[1] = src[1];
+        bw[1] = DC == 8 ? src[1] : bw[0];
     } else {  // a padding step: +0 operands, whose entries are +0
         bw[0] = u32x4{kZeroRowWord, kZeroRowWord, kZeroRowWord, kZeroRowWord};
         bw[1] = bw[0];
     }
 }
 
-__device__ __forceinline__ void dot_fetch_rows(uint32_t (&rw)[kDotCols], const u32x4 (&bw)[2],
-                                               __amdgpu_buffer_rsrc_t rres)
+template <int DC>
+__device__ __forceinline__ void dot_fetch_rows(uint32_t (&rw)[DC], const u32x4 (&bw)[2], __amdgpu_buffer_rsrc_t rres)
 {
     const int g = threadIdx.x & 31;
 #pragma unroll
-    for (int c = 0; c < kDotCols; ++c) {
+    for (int c = 0; c < DC; ++c) {
         const uint32_t w = bw[c / 4][c % 4];  // idx = kb * 128 (kZeroRow for zeros)
         rw[c] = __builtin_amdgcn_raw_buffer_load_b32(rres, (w & 0x7F80u) | uint32_t(g * 4), 0, 0);
     }
@@ -1286,24 +1295,29 @@ __device__ __forceinline__ void dot_fetch_rows(uint32_t (&rw)[kDotCols], const u
 
 // Commit: t = v * pb as bf16 bits = table byte + (pb's bits >> 16); a zero second operand reads
 // the zero row and gets signed zeros.  Entry dword q = (t of column 2q, t of column 2q + 1).
-__device__ __forceinline__ void dot_commit(const u32x4 (&bw)[2], const uint32_t (&rw)[kDotCols], unsigned char *slab)
+template <int DC>
+__device__ __forceinline__ void dot_commit(const u32x4 (&bw)[2], const uint32_t (&rw)[DC], unsigned char *slab)
 {
     const int slot = threadIdx.x >> 5, g = threadIdx.x & 31;
-    const uint32_t(&w)[kDotCols] = rw;
-    uint32_t hb[kDotCols / 2];
+    const uint32_t(&w)[DC] = rw;
+    uint32_t hb[DC / 2];
 #pragma unroll
-    for (int q = 0; q < kDotCols / 2; ++q)
+    for (int q = 0; q < DC / 2; ++q)
         hb[q] = __builtin_amdgcn_perm(bw[(2 * q + 1) / 4][(2 * q + 1) % 4], bw[(2 * q) / 4][(2 * q) % 4], 0x07060302u);
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
-        u32x4 e;
+        uint32_t e[DC / 2];
 #pragma unroll
-        for (int q = 0; q < kDotCols / 2; ++q) {
+        for (int q = 0; q < DC / 2; ++q) {
             // low half: byte i of the even column's word, high half: byte i of the odd one's
             const uint32_t d = __builtin_amdgcn_perm(w[2 * q + 1], w[2 * q], 0x0C000C00u | ((4u + i) << 16) | i);
             e[q] = add_u16x2(d, hb[q]);
         }
-        *reinterpret_cast<u32x4 *>(slab + slot * kDotStepBytes + (g + 32 * i) * 16) = e;
+        unsigned char *dst = slab + slot * kDotStepBytes + (g + 32 * i) * 16;
+        if constexpr (DC == 8)
+            *reinterpret_cast<u32x4 *>(dst) = u32x4{e[0], e[1], e[2], e[3]};
+        else
+            *reinterpret_cast<u32x2 *>(dst) = u32x2{e[0], e[1]};
     }
 }
 
@@ -1341,12 +1355,13 @@ __device__ __forceinline__ void dot_load_pair(uint32_t (&dst)[split_a<OP>() ? 3 
 
 // Workgroup: NW waves along rows (64*TM rows each), all on the same 8 columns.  Every thread
 // stages one step's entry group per slab (KS = 2 * NW steps x 32 groups).
-template <int OP, int TM, int NW>
+template <int OP, int TM, int NW, int DC>
 __device__ __forceinline__ void tab_body_dot(const TabArgs &a)
 {
+    static_assert(dot_cols_ok(DC), "8 or 4 columns per entry");
     constexpr int KS = dot_slab_steps(NW);
     constexpr int kDotSlab = KS * kDotStepBytes;
-    constexpr int TN = kDotCols;
+    constexpr int TN = DC;
     constexpr bool SPLIT = split_a<OP>();
     constexpr int NA = SPLIT ? 3 : 2;  // first-operand registers per step pair and lane row
     extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
@@ -1386,7 +1401,7 @@ __device__ __forceinline__ void tab_body_dot(const TabArgs &a)
     // latency would otherwise be exposed once per slab; 16-step slabs fetch both in slab s.
     constexpr bool AHEAD2 = NW <= 4;
     u32x4 sbw[2], sbw2[2];
-    uint32_t srw[kDotCols];
+    uint32_t srw[DC];
     float acc[TM][TN];
     init_acc(acc);
     // First-operand data of RS step pairs, as a ring: pair kp of a slab is in w[kp % RS]; while
@@ -1419,13 +1434,13 @@ __device__ __forceinline__ void tab_body_dot(const TabArgs &a)
     bool has_next = false;
     if (have) {
         cur = tab_tap<OP>(a, tap);
-        dot_fetch_b(sbw, cur, c0, a.Bd, a.Np, col0);
-        dot_fetch_rows(srw, sbw, rres);
-        dot_commit(sbw, srw, smem);
+        dot_fetch_b<DC>(sbw, cur, c0, a.Bd, a.Np, col0);
+        dot_fetch_rows<DC>(srw, sbw, rres);
+        dot_commit<DC>(sbw, srw, smem);
 #pragma unroll
         for (int k = 0; k < 2; ++k) dot_load_pair<OP, TM>(w[k], av, cur, c0 + 2 * k);
         advance(cur, tap, c0, nxt, ntap, nc0, has_next);
-        if (AHEAD2 && has_next) dot_fetch_b(sbw, nxt, nc0, a.Bd, a.Np, col0);
+        if (AHEAD2 && has_next) dot_fetch_b<DC>(sbw, nxt, nc0, a.Bd, a.Np, col0);
     }
     __syncthreads();
     // One slab from buffer BUF (a compile-time LDS offset, folded into the gathers' immediate
@@ -1441,11 +1456,11 @@ __device__ __forceinline__ void tab_body_dot(const TabArgs &a)
         if constexpr (AHEAD2) {
             advance(nxt, ntap, nc0, nxt2, ntap2, nc02, has_next2);
             has_next2 = has_next2 && has_next;
-            if (has_next) dot_fetch_rows(srw, sbw, rres);
-            if (has_next2) dot_fetch_b(sbw2, nxt2, nc02, a.Bd, a.Np, col0);
+            if (has_next) dot_fetch_rows<DC>(srw, sbw, rres);
+            if (has_next2) dot_fetch_b<DC>(sbw2, nxt2, nc02, a.Bd, a.Np, col0);
         } else if (has_next) {
-            dot_fetch_b(sbw, nxt, nc0, a.Bd, a.Np, col0);
-            dot_fetch_rows(srw, sbw, rres);
+            dot_fetch_b<DC>(sbw, nxt, nc0, a.Bd, a.Np, col0);
+            dot_fetch_rows<DC>(srw, sbw, rres);
         }
         // the slab ends at the tap's end or, 8-step chunks being the unit of splits, at the split's
         const int nslots = min(min(KS, cur.count - c0), p_end - (tap * cpt * 8 + c0));
@@ -1466,8 +1481,24 @@ __device__ __forceinline__ void tab_body_dot(const TabArgs &a)
                 // half under its head) plus the slot's, which is a constant
                 const uint32_t o0 = SPLIT ? a0[r] : (a0[r] & 0xFFFFu);
                 const uint32_t o1 = SPLIT ? a1[r] : (a1[r] & 0xFFFFu);
-                const u32x4 X = lds_load_b128(o0, BOFF + (2 * kp) * kDotStepBytes);
-                const u32x4 Y = lds_load_b128(o1, BOFF + (2 * kp + 1) * kDotStepBytes);
+                uint32_t X[DC / 2], Y[DC / 2];
+                if constexpr (DC == 8) {
+                    const u32x4 x4 = lds_load_b128(o0, BOFF + (2 * kp) * kDotStepBytes);
+                    const u32x4 y4 = lds_load_b128(o1, BOFF + (2 * kp + 1) * kDotStepBytes);
+#pragma unroll
+                    for (int q = 0; q < 4; ++q) {
+                        X[q] = x4[q];
+                        Y[q] = y4[q];
+                    }
+                } else {
+                    const u32x2 x2 = lds_load_b64(o0, BOFF + (2 * kp) * kDotStepBytes);
+                    const u32x2 y2 = lds_load_b64(o1, BOFF + (2 * kp + 1) * kDotStepBytes);
+#pragma unroll
+                    for (int q = 0; q < 2; ++q) {
+                        X[q] = x2[q];
+                        Y[q] = y2[q];
+                    }
+                }
                 uint32_t pa;  // (pa(k), pa(k+1)) as bf16
                 if constexpr (SPLIT)
                     pa = w[kp % RS][NA - 1][r];
@@ -1485,7 +1516,7 @@ __device__ __forceinline__ void tab_body_dot(const TabArgs &a)
 #pragma unroll
             for (int k = 0; k < 2; ++k) dot_load_pair<OP, TM>(w[k], av, nxt, nc0 + 2 * k);
         }
-        if (has_next) dot_commit(sbw, srw, smem + NEXT);
+        if (has_next) dot_commit<DC>(sbw, srw, smem + NEXT);
         __syncthreads();
         cur = nxt;
         tap = ntap;
@@ -1575,9 +1606,9 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(4, 4)))
     TabArgs a = args;
     tab_tile_id(a.splits, a.tx, a.ty, a.tz);
     const int eb = __builtin_amdgcn_readfirstlane(a.eb[0]);
-    if constexpr (RL == 7 && TN == kDotCols && WR == NW) {
+    if constexpr (RL == 7 && dot_cols_ok(TN) && WR == NW) {
         if (__builtin_amdgcn_readfirstlane(a.eb[1]) != 0) {
-            tab_body_dot<OP, TM, NW>(a);
+            tab_body_dot<OP, TM, NW, TN>(a);
             return;
         }
     }
@@ -1604,7 +1635,7 @@ constexpr size_t tab_lds_bytes(int tn, int wr, int nw, int rl)
     size_t b = tab_exact_lds_bytes(tnw, rl, 1);
     b = tab_exact_lds_bytes(tnw, rl, 2) > b ? tab_exact_lds_bytes(tnw, rl, 2) : b;
     b = tab_exact_lds_bytes(tnw, rl, 4) > b ? tab_exact_lds_bytes(tnw, rl, 4) : b;
-    const size_t dot = (rl == 7 && tn == kDotCols && wr == nw) ? size_t(2) * dot_slab_steps(nw) * kDotStepBytes : 0;
+    const size_t dot = (rl == 7 && dot_cols_ok(tn) && wr == nw) ? size_t(2) * dot_slab_steps(nw) * kDotStepBytes : 0;
     return b > dot ? b : dot;
 }
 
@@ -1638,7 +1669,7 @@ struct TabCand {
     int tm, tn, wr, nw;
 };
 constexpr TabCand kTabCands[] = {{4, 8, 8, 8}, {4, 8, 4, 4}, {3, 8, 4, 4}, {2, 8, 4, 4}, {1, 8, 4, 4},
-                                 {4, 4, 4, 4}, {2, 4, 4, 4}, {1, 4, 4, 4}, {4, 8, 2, 4}, {2, 8, 2, 4},
+                                 {4, 4, 8, 8}, {4, 4, 4, 4}, {2, 4, 4, 4}, {1, 4, 4, 4}, {4, 8, 2, 4}, {2, 8, 2, 4},
                                  {1, 8, 2, 4}, {2, 8, 1, 4}, {1, 8, 1, 4}};
 // Wide rows (M = 8..10; 11 uses the 4-column tiles, whose 4-byte-entry slab of one step fits 32 KiB).
 constexpr TabCand kWideCands[] = {{8, 4, 8, 8}, {4, 8, 8, 8}, {2, 8, 4, 4}, {1, 8, 4, 4}, {1, 4, 4, 4}};
@@ -1675,7 +1706,7 @@ Tile choose_tab_tile(int64_t rows, int64_t cols, int64_t q, int64_t min_chunks, 
         const double slots = double(kCUs * wgs_per_cu);
         const double work =
             double(ceil_div(rows, wrows) * wrows) * double(col_tiles * ctile) * double(phases) * double(q * 8);
-        const bool pair = rl == 7 && c.tn == kDotCols && c.wr == c.nw;
+        const bool pair = rl == 7 && dot_cols_ok(c.tn) && c.wr == c.nw;
         // staging bytes per product grow with the row length (2^rl entries; wide rows are priced
         // at 2-byte entries)
         const double per_product =
@@ -1754,9 +1785,9 @@ void allow_lds(K kernel, size_t bytes)
 
 // The instantiated (TM, TN, WR, NW, RL) tiles: every candidate of the chooser above.
 #define AMSIM_FOR_TAB_TILES(X)                                                                                \
-    X(4, 8, 8, 8, 7) X(4, 8, 4, 4, 7) X(3, 8, 4, 4, 7) X(2, 8, 4, 4, 7) X(1, 8, 4, 4, 7) X(4, 4, 4, 4, 7)          \
-    X(2, 4, 4, 4, 7) X(1, 4, 4, 4, 7) X(4, 8, 2, 4, 7) X(2, 8, 2, 4, 7) X(1, 8, 2, 4, 7) X(2, 8, 1, 4, 7)          \
-    X(1, 8, 1, 4, 7) AMSIM_WIDE_TILES(X, 8) AMSIM_WIDE_TILES(X, 9) AMSIM_WIDE_TILES(X, 10) X(8, 4, 8, 8, 11)     \
+    X(4, 8, 8, 8, 7) X(4, 8, 4, 4, 7) X(3, 8, 4, 4, 7) X(2, 8, 4, 4, 7) X(1, 8, 4, 4, 7) X(4, 4, 8, 8, 7)     \
+    X(4, 4, 4, 4, 7) X(2, 4, 4, 4, 7) X(1, 4, 4, 4, 7) X(4, 8, 2, 4, 7) X(2, 8, 2, 4, 7) X(1, 8, 2, 4, 7)     \
+    X(2, 8, 1, 4, 7) X(1, 8, 1, 4, 7) AMSIM_WIDE_TILES(X, 8) AMSIM_WIDE_TILES(X, 9) AMSIM_WIDE_TILES(X, 10) X(8, 4, 8, 8, 11)     \
     X(4, 4, 8, 8, 11) X(2, 4, 4, 4, 11) X(1, 4, 4, 4, 11)
 #define AMSIM_WIDE_TILES(X, RL)                                                                                \
     X(8, 4, 8, 8, RL) X(4, 8, 8, 8, RL) X(2, 8, 4, 4, RL) X(1, 8, 4, 4, RL) X(1, 4, 4, 4, RL)
