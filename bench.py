@@ -37,7 +37,9 @@ FLOP_PER_APPROX_MAC = 2           # one multiply + one add
 # reading of "% of the FP32 vector peak", reported beside the first.
 FP32_LANE_RATE_T = 256 * 64 * 2.4e9 / 1e12
 TRAFFIC_PROFILE = os.path.join(ROOT, "profiles", "gemm_4096_m7_traffic.txt")
-KERNEL_SOURCE = os.path.join(ROOT, "paper_2209_04161_amd", "csrc", "amsim_kernels.hip")
+# Device sources whose content the committed counters belong to (hashed in this order).
+KERNEL_SOURCES = [os.path.join(ROOT, "paper_2209_04161_amd", "csrc", f)
+                  for f in ("amsim_common.h", "amsim_tab.h", "amsim_tab.hip", "amsim_kernels.hip")]
 
 
 def log(msg):
@@ -45,8 +47,11 @@ def log(msg):
 
 
 def kernel_source_hash():
-    with open(KERNEL_SOURCE, "rb") as f:
-        return hashlib.sha256(f.read()).hexdigest()
+    h = hashlib.sha256()
+    for path in KERNEL_SOURCES:
+        with open(path, "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()
 
 
 def read_traffic():

@@ -10,12 +10,21 @@ Flags that matter for the numerics:
 import os
 import subprocess
 import sys
+import tempfile
 
 HERE = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(HERE)
-SOURCES = [os.path.join(HERE, "csrc", "amsim_kernels.hip"), os.path.join(HERE, "csrc", "amsim_host.cpp")]
+CSRC = os.path.join(HERE, "csrc")
+# (source, extra flags): the table kernels are compiled once per operation (0 GEMM, 1 forward,
+# 2 backward data, 3 backward weight), in parallel with the rest.
+UNITS = [("amsim_kernels.hip", []), ("amsim_host.cpp", [])] + [
+    ("amsim_tab.hip", ["-DAMSIM_TAB_OP=%d" % op]) for op in range(4)]
 LIB = os.path.join(HERE, "libamsim.so")
 ARCH = os.environ.get("AMSIM_OFFLOAD_ARCH", "gfx950")
+FLAGS = ["--offload-arch=" + ARCH, "-O3", "-std=c++17", "-fPIC",
+         "-fgpu-flush-denormals-to-zero", "-ffp-contract=off",
+         "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+         "-I", os.path.join(ROOT, "include"), "-I", CSRC]
 
 
 def hipcc():
@@ -25,21 +34,37 @@ def hipcc():
     return "hipcc"
 
 
-def build(verbose: bool = False) -> str:
-    tmp = LIB + ".tmp%d" % os.getpid()
-    cmd = [hipcc(), "--offload-arch=" + ARCH, "-O3", "-std=c++17", "-fPIC", "-shared",
-           "-fgpu-flush-denormals-to-zero", "-ffp-contract=off",
-           "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
-           "-I", os.path.join(ROOT, "include"), "-o", tmp] + SOURCES
-    if verbose:
-        print(" ".join(cmd), flush=True)
-    res = subprocess.run(cmd, stdout=subprocess.PIPE, stderr=subprocess.STDOUT, text=True)
+def _clean(text):
     # hipcc's host pass does not know the packed-fp32 target feature and says so: harmless.
-    out = "\n".join(l for l in res.stdout.splitlines() if "packed-fp32-ops" not in l)
-    if res.returncode != 0:
-        raise RuntimeError("hipcc failed:\n" + out)
-    if verbose and out.strip():
-        print(out)
+    return "\n".join(l for l in text.splitlines() if "packed-fp32-ops" not in l)
+
+
+def build(verbose: bool = False) -> str:
+    with tempfile.TemporaryDirectory(prefix="amsim_build_") as tmpdir:
+        jobs = []
+        for i, (src, extra) in enumerate(UNITS):
+            obj = os.path.join(tmpdir, "%d_%s.o" % (i, os.path.splitext(src)[0]))
+            cmd = [hipcc()] + FLAGS + extra + ["-c", os.path.join(CSRC, src), "-o", obj]
+            if verbose:
+                print(" ".join(cmd), flush=True)
+            jobs.append((cmd, obj, subprocess.Popen(cmd, stdout=subprocess.PIPE, stderr=subprocess.STDOUT,
+                                                    text=True)))
+        failed = []
+        for cmd, obj, proc in jobs:
+            out = _clean(proc.communicate()[0])
+            if proc.returncode != 0:
+                failed.append(" ".join(cmd) + "\n" + out)
+            elif verbose and out.strip():
+                print(out)
+        if failed:
+            raise RuntimeError("hipcc failed:\n" + "\n\n".join(failed))
+        tmp = LIB + ".tmp%d" % os.getpid()
+        cmd = [hipcc(), "--offload-arch=" + ARCH, "--hip-link", "-shared", "-fPIC", "-o", tmp] + [o for _, o, _ in jobs]
+        if verbose:
+            print(" ".join(cmd), flush=True)
+        res = subprocess.run(cmd, stdout=subprocess.PIPE, stderr=subprocess.STDOUT, text=True)
+        if res.returncode != 0:
+            raise RuntimeError("hipcc link failed:\n" + _clean(res.stdout))
     os.replace(tmp, LIB)
     return LIB
 

@@ -16,14 +16,9 @@
 //   fma(v, pa*pb, acc): pa*pb is rounded on its own, and v*(pa*pb) is exact, so the fma equals
 //   acc + c rounded once.
 //
-// Kernel shape: lanes of a wave own output rows (64*TM rows per wave), the wave's TN output
-// columns are wave-uniform, waves of a workgroup lie along rows and/or columns.  Per slab of
-// steps the workgroup stages into LDS, for each of its columns and steps, the table row that
-// the column's second-operand mantissa selects (128 entries for M <= 7, 2^M for M = 8..11);
-// lanes gather from it with their first-operand mantissas.  For 1-byte tables and operands
-// whose exponents keep every product normal, the bf16 pair path folds the second operand into
-// the staged entries and adds two steps' products with one dot instruction.  Products are
-// never fed to MFMA: they are not IEEE.
+// The table kernels (the hot path) live in amsim_tab.h / amsim_tab.hip; this file holds the
+// decode and table-preparation pre-passes, the split reduction, the direct-evaluation GEMM,
+// the host-side planning and the C entry points.
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
@@ -36,108 +31,11 @@
 
 #include "amsim.h"
 
+#include "amsim_tab.h"
+
 namespace {
 
-constexpr uint32_t kIdxMask = 0x003FFFFFu;
-constexpr uint32_t kHeadMask = 0xFFC00000u;
-
-typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
-typedef uint32_t u32x3 __attribute__((ext_vector_type(3)));  // buffer_load_dwordx3 results only
-typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
-
-// ------------------------------------------------------------------ device helpers -------
-
-// zidx: the index field given to zeros and denormals (their mantissa bits never matter: every
-// product with a zero is a signed zero, whatever table entry it reads).
-__device__ __forceinline__ uint32_t amsim_decode(uint32_t u, int m, int shift, uint32_t zidx = 0u)
-{
-    const uint32_t e = (u >> 23) & 0xFFu;
-    if (e == 0u) return (u & 0x80000000u) | zidx;                      // +-0 (denormals too)
-    uint32_t head;
-    if (e == 0xFFu)
-        head = (u & 0xFF800000u) | ((u & 0x007FFFFFu) ? 0x00400000u : 0u);  // +-Inf / qNaN
-    else
-        head = u & 0xFF800000u;                                        // +-2^(E-127)
-    const uint32_t idx = ((u >> (23 - m)) & ((1u << m) - 1u)) << shift;
-    return head | idx;
-}
-
-__device__ __forceinline__ float head_value(uint32_t w) { return __uint_as_float(w & kHeadMask); }
-
-__device__ __forceinline__ float table_value(uint32_t entry)
-{
-    return __uint_as_float((entry & 0x00FFFFFFu) + 0x3F800000u);
-}
-
-template <int TM, int TN>
-__device__ __forceinline__ void init_acc(float (&acc)[TM][TN])
-{
-#pragma unroll
-    for (int r = 0; r < TM; ++r)
-#pragma unroll
-        for (int t = 0; t < TN; ++t) acc[r][t] = -0.0f;
-}
-
-__device__ __forceinline__ int wave_id() { return __builtin_amdgcn_readfirstlane(threadIdx.x >> 6); }
-
-// Exponent range of the operands a decode pass has seen, for the table kernels' bf16 path
-// (which is exact only while no product can leave the normal range).  Finite non-zero operands
-// count; zeros and denormals (read as zeros) do not.  One packed word per workgroup:
-//   bits 0..7 smallest exponent field, 8..15 largest, bit 16 set if an Inf or NaN was seen.
-constexpr int kStatSlots = 8192;  // most workgroups of a decode launch that records them
-
-struct ExpStats {
-    uint32_t lo = 255u, hi = 0u, special = 0u;
-    __device__ __forceinline__ void add(uint32_t u)
-    {
-        const uint32_t e = (u >> 23) & 0xFFu;
-        if (e == 0xFFu) {
-            special = 1u;
-        } else if (e != 0u) {
-            lo = min(lo, e);
-            hi = max(hi, e);
-        }
-    }
-};
-
-__device__ __forceinline__ uint32_t wave_min(uint32_t v)
-{
-#pragma unroll
-    for (int o = 32; o > 0; o >>= 1) v = min(v, uint32_t(__shfl_xor(int(v), o)));
-    return v;
-}
-
-__device__ __forceinline__ uint32_t wave_max(uint32_t v)
-{
-#pragma unroll
-    for (int o = 32; o > 0; o >>= 1) v = max(v, uint32_t(__shfl_xor(int(v), o)));
-    return v;
-}
-
-// Workgroup reduction of the threads' statistics into stats[slot] (every thread of a workgroup
-// of at most 1024 threads must call it).  Reduced within each wave first: same-address LDS
-// atomics from every thread would serialise.  Once an Inf or NaN is seen the largest exponent no
-// longer matters, so it travels with the special flag in one maximum.
-__device__ __forceinline__ void store_stats(const ExpStats &s, uint32_t *stats, int slot)
-{
-    __shared__ uint32_t s_lo[16], s_hs[16];
-    if (stats == nullptr) return;  // uniform: the whole launch records or none of it
-    const uint32_t lo = wave_min(s.lo), hs = wave_max((s.special << 8) | s.hi);
-    const int wave = int(threadIdx.x) >> 6, nwaves = int(blockDim.x + 63) >> 6;
-    if ((threadIdx.x & 63) == 0) {
-        s_lo[wave] = lo;
-        s_hs[wave] = hs;
-    }
-    __syncthreads();
-    if (threadIdx.x == 0) {
-        uint32_t l = 255u, h = 0u;
-        for (int i = 0; i < nwaves; ++i) {
-            l = min(l, s_lo[i]);
-            h = max(h, s_hs[i]);
-        }
-        stats[slot] = l | ((h & 0xFFu) << 8) | ((h >> 8) << 16);
-    }
-}
+using namespace amsim_detail;
 
 // ------------------------------------------------------------------ pre-pass kernels -----
 
@@ -499,38 +397,9 @@ __global__ void mul_ew_kernel(int64_t n, const float *__restrict__ a, const floa
     }
 }
 
-// ------------------------------------------------------------------ per-column tables
-// The exact path keeps, per step and output column j, the table row selected by that column's
-// second-operand mantissa kb(k, j) -- LUT[. ][kb], indexed by the first operand's mantissa --
-// at a fixed LDS address.  Lanes then gather with
-//   ds_read  v, (lane's first-operand mantissa * entry bytes)  offset:(fixed row address)
-// so no per-product address arithmetic is left: per product one LDS gather, one multiply
-// (pa * pb) and one fma.  Rows are copied from a transposed copy of the table in global
-// memory, slab by slab (KS steps), double-buffered with one barrier per slab.
-//
-// Rows are stored compressed when the table allows it without loss: 1 byte per entry when
-// every entry's low 16 mantissa bits are zero (e.g. Mitchell at M <= 7), 2 bytes when the low 8
-// are zero (e.g. the exact truncated product at M <= 7, Mitchell at M = 8..11), else the 4-byte
-// rebiased float.  The entry width is decided on the device by the table-preparation kernels
-// and read by the table kernel, which runs the matching specialisation.
+// ------------------------------------------------------------------ table preparation
 
-constexpr int kTabRowEntries = 128;  // rows padded to 2^7 entries
 constexpr int kPrepWorkgroups = 8;   // table preparation (M <= 7): workgroups sharing the rows
-// Table row kZeroRow (after the 2^M rows) holds zeros: the table path decodes second-operand
-// zeros, and names padding steps, with its index, so that a zero's row needs no test.
-constexpr int kZeroRow = kTabRowEntries;
-constexpr uint32_t kZeroRowWord = uint32_t(kZeroRow) << 7;  // decoded +0 of the second operand
-
-template <int EB>
-__device__ __forceinline__ float tab_value(const unsigned char *p)
-{
-    if constexpr (EB == 1)
-        return __uint_as_float((uint32_t(*p) << 16) + 0x3F800000u);
-    else if constexpr (EB == 2)
-        return __uint_as_float((uint32_t(*reinterpret_cast<const uint16_t *>(p)) << 8) + 0x3F800000u);
-    else
-        return *reinterpret_cast<const float *>(p);
-}
 
 // Transposed, width-reduced table: dst row kb (kTabRowEntries * EB bytes) holds entry
 // (ka, kb) at byte ka * EB.  With 1-byte entries it also writes dot_rows, the same bytes in the
@@ -723,922 +592,6 @@ __global__ __launch_bounds__(256) void prep_rows_wide_kernel(const uint32_t *__r
     }
 }
 
-struct ConvShape {
-    int n, h, w, ci, co, kh, kw, sh, sw, pt, pl, oh, ow;
-};
-
-// Which operation the table kernel evaluates.  Every one is a sum over "taps": runs of
-// consecutive reduction steps j = 0 .. count-1 whose first-operand word sits at
-//   A[lane row base + ubase + j * ustride]
-// (pair records: record pbase + (j / 2) * ustride from the row's record base) and whose
-// second-operand row is Bd[bbase + j].
-//   GEMM         one tap of K steps: rows i, A = op(A) k-major, row base i
-//   FWD          tap = (kh, kw): rows (n, oh, ow), A = zero-padded x stored [n][h][ci][w], j = ci
-//   BWD_DATA     tap = valid (kh, kw) of the stride phase in tile z: rows (n, hq, wq),
-//                A = zero-padded dy stored [n][h][co][w], j = co; weights read as [kh][kw][co][ci]
-//   BWD_WEIGHT   tap = output row (n, oh): rows (kh, kw, ci), A = zero-padded x (NHWC), j = ow,
-//                B = dy
-// The channel-inside-row layouts put the lanes' consecutive output pixels on consecutive words,
-// so each first-operand load of a wave touches a few cache lines instead of 64.
-// The reduction is cut into chunks of 8 steps (a tap of `count` steps holds ceil(count / 8));
-// split s (of tile z) sums chunks [s * chunks_per_split, (s + 1) * chunks_per_split) into its
-// own partial result, laid out like the final one; a fixed-order pass adds the partials.
-enum { OP_GEMM = 0, OP_FWD = 1, OP_BWD_DATA = 2, OP_BWD_WEIGHT = 3 };
-
-struct TabArgs {
-    const uint32_t *A;   // decoded first operand: words, or (pair records) 12-byte step-pair records
-    uint32_t a_bytes;    // its size in bytes (buffer range: reads beyond return 0)
-    const uint32_t *Bd;  // decoded second operand rows, leading dimension Np
-    int Np;
-    float *out;          // result, or split partial sums [z][R][N]
-    int64_t ldc;         // GEMM result leading dimension
-    const unsigned char *rows;      // transposed table rows (exact path)
-    const unsigned char *dot_rows;  // the same 1-byte rows in bf16-path staging order
-    const int *eb;                  // [0] entry width, [1] 1 when the bf16 path may run
-    int R, N;            // result rows and columns
-    int splits;          // reduction splits: tile z = (phase *) splits + split
-    int chunks_per_split;  // reduction chunks (8 steps each) per split
-    int64_t out_elems;   // elements of one split's partial result (splits > 1)
-    int Mp, K;           // GEMM
-    ConvShape s;
-    int Hp, Wp;          // zero-padded x (FWD, BWD_WEIGHT)
-    int OHp, OWp, pad_oh, pad_ow;  // zero-padded dy (BWD_DATA)
-    int tx, ty, tz;      // this workgroup's tile (row block, column block, phase/split); set on entry
-};
-
-// Workgroups go to the 8 XCDs in turn (linear id mod 8), and each XCD has its own L2.  The table
-// kernels give each XCD a contiguous range of tiles instead, in the order stride phase fastest
-// (phases differ in work, so each XCD gets all of them), then column blocks, row blocks, splits --
-// so that the workgroups an XCD runs together share first-operand rows and second-operand cache
-// lines in its L2.  Grids whose size is not a multiple of 8 keep the hardware order.
-__device__ __forceinline__ void tab_tile_id(int splits, int &tx, int &ty, int &tz)
-{
-    const uint32_t gx = gridDim.x, gy = gridDim.y, gz = gridDim.z, n = gx * gy * gz;
-    const uint32_t id = blockIdx.x + gx * (blockIdx.y + gy * blockIdx.z);
-    if (n % 8u != 0u) {
-        tx = int(blockIdx.x);
-        ty = int(blockIdx.y);
-        tz = int(blockIdx.z);
-        return;
-    }
-    const uint32_t lid = (id % 8u) * (n / 8u) + id / 8u;
-    const uint32_t phases = gz / uint32_t(splits);
-    const uint32_t ph = lid % phases, rest = lid / phases;
-    ty = int(rest % gy);
-    tx = int((rest / gy) % gx);
-    tz = int(ph * uint32_t(splits) + rest / (gx * gy));
-}
-
-struct TabTap {
-    int ubase, ustride, bbase, count;
-    int pbase;  // pair records: the tap's first record (records of pair j / 2 are ustride apart)
-};
-
-// The first operand of the GEMM and of the forward and backward-data passes (whose steps are
-// channels) is decoded into one 12-byte record per lane row and step pair (j, j + 1), j even,
-// instead of one word per element: j's 16-bit table-index field (an LDS byte
-// offset on the bf16 path) as a word, the two mantissa-cleared operands as bf16
-// (pa(j) | pa(j+1) << 16), and j+1's index word.  The bf16 path loads a record with one
-// instruction and uses it as loaded: no masking of the indices, no pairing of the heads.  A
-// single step is one 8-byte load at record offset 0 (j even) or 4 (j odd) and one byte permute.
-template <int OP>
-constexpr bool split_a()
-{
-    return OP == OP_GEMM || OP == OP_FWD || OP == OP_BWD_DATA;
-}
-constexpr uint32_t kPairRecordBytes = 12;
-
-// First-operand buffer and the lane rows' byte offsets in it.
-template <int TM>
-struct AView {
-    __amdgpu_buffer_rsrc_t words;  // words, or pair records
-    uint32_t aoff[TM];             // per lane row: offset of its run (word or record)
-};
-
-// Byte offset of step j's word (pair records: of the record holding j) in the tap.
-template <int OP>
-__device__ __forceinline__ uint32_t a_step_offset(const TabTap &tp, int j)
-{
-    if constexpr (split_a<OP>())
-        return uint32_t(tp.pbase + (j >> 1) * tp.ustride) * kPairRecordBytes;
-    else
-        return uint32_t(tp.ubase + j * tp.ustride) * 4u;
-}
-
-// The first operand's word of step j (head | index, as the one-word layout stores it) for each
-// lane row; so = a_step_offset of j (wave-uniform).  Pair records: j's index word with j's half
-// of the head pair moved into the high half.
-template <int OP, int TM>
-__device__ __forceinline__ void load_a_words(uint32_t (&dst)[TM], const AView<TM> &av, uint32_t so, int j)
-{
-#pragma unroll
-    for (int r = 0; r < TM; ++r) {
-        if constexpr (split_a<OP>()) {
-            // j even: (index, heads) -> index | pa(j) << 16; j odd: (heads, index) -> index | pa(j+1)'s half
-            const u32x2 d = __builtin_amdgcn_raw_buffer_load_b64(av.words, av.aoff[r], so + (j & 1) * 4u, 0);
-            dst[r] = __builtin_amdgcn_perm(d.y, d.x, (j & 1) ? 0x03020504u : 0x05040100u);
-        } else {
-            dst[r] = __builtin_amdgcn_raw_buffer_load_b32(av.words, av.aoff[r], so, 0);
-        }
-    }
-}
-
-template <int OP, int TM>
-__device__ __forceinline__ AView<TM> make_aview(const TabArgs &a, const int (&abase)[TM])
-{
-    AView<TM> av;
-    av.words = __builtin_amdgcn_make_buffer_rsrc(const_cast<uint32_t *>(a.A), 0, int(a.a_bytes), 0x00020000);
-#pragma unroll
-    for (int r = 0; r < TM; ++r) av.aoff[r] = uint32_t(abase[r]) * (split_a<OP>() ? kPairRecordBytes : 4u);
-    return av;
-}
-
-// Rows of one stride phase of the backward-data pass.
-__device__ __forceinline__ void phase_dims(const ConvShape &s, int ph, int pw, int &hq_n, int &wq_n)
-{
-    hq_n = ph < s.h ? (s.h - ph + s.sh - 1) / s.sh : 0;
-    wq_n = pw < s.w ? (s.w - pw + s.sw - 1) / s.sw : 0;
-}
-
-// tile z = phase * splits + split (phase only for BWD_DATA, else 0)
-__device__ __forceinline__ int tab_phase(const TabArgs &a) { return a.tz / a.splits; }
-__device__ __forceinline__ int tab_split(const TabArgs &a) { return a.tz % a.splits; }
-
-template <int OP>
-__device__ __forceinline__ int tab_rows(const TabArgs &a)
-{
-    if constexpr (OP == OP_BWD_DATA) {
-        int hq_n, wq_n;
-        phase_dims(a.s, tab_phase(a) / a.s.sw, tab_phase(a) % a.s.sw, hq_n, wq_n);
-        return a.s.n * hq_n * wq_n;
-    } else {
-        return a.R;
-    }
-}
-
-// Lane row -> (first-operand element offset of the row, result element offset).
-template <int OP>
-__device__ __forceinline__ void tab_row(const TabArgs &a, int row, int &abase, int64_t &obase)
-{
-    const ConvShape &s = a.s;
-    if constexpr (OP == OP_GEMM) {
-        abase = row;
-        obase = int64_t(row) * a.ldc;
-    } else if constexpr (OP == OP_FWD) {
-        const int ow = row % s.ow, oh = (row / s.ow) % s.oh, n = row / (s.ow * s.oh);
-        abase = (n * a.Hp + oh * s.sh) * s.ci * a.Wp + ow * s.sw;  // x as [n][hp][ci][wp]
-        obase = int64_t(row) * s.co;
-    } else if constexpr (OP == OP_BWD_DATA) {
-        const int ph = tab_phase(a) / s.sw, pw = tab_phase(a) % s.sw;
-        int hq_n, wq_n;
-        phase_dims(s, ph, pw, hq_n, wq_n);
-        const int wq = row % wq_n, hq = (row / wq_n) % hq_n, n = row / (wq_n * hq_n);
-        abase = (n * a.OHp + hq) * s.co * a.OWp + wq;  // dy as [n][ohp][co][owp]; pads in the tap offset
-        obase = (int64_t(n * s.h + hq * s.sh + ph) * s.w + wq * s.sw + pw) * s.ci;
-    } else {
-        const int ci = row % s.ci, kw = (row / s.ci) % s.kw, kh = row / (s.ci * s.kw);
-        abase = (kh * a.Wp + kw) * s.ci + ci;
-        obase = int64_t(row) * s.co;
-    }
-}
-
-// Pair records: the lane row's record offset (element offset with the step axis halved).
-template <int OP>
-__device__ __forceinline__ int tab_row_rec(const TabArgs &a, int row)
-{
-    const ConvShape &s = a.s;
-    if constexpr (OP == OP_GEMM) {
-        return row;
-    } else if constexpr (OP == OP_FWD) {
-        const int ow = row % s.ow, oh = (row / s.ow) % s.oh, n = row / (s.ow * s.oh);
-        return (n * a.Hp + oh * s.sh) * ((s.ci + 1) / 2) * a.Wp + ow * s.sw;  // records [n][hp][ci/2][wp]
-    } else if constexpr (OP == OP_BWD_DATA) {
-        const int ph = tab_phase(a) / s.sw, pw = tab_phase(a) % s.sw;
-        int hq_n, wq_n;
-        phase_dims(s, ph, pw, hq_n, wq_n);
-        const int wq = row % wq_n, hq = (row / wq_n) % hq_n, n = row / (wq_n * hq_n);
-        return (n * a.OHp + hq) * ((s.co + 1) / 2) * a.OWp + wq;  // records [n][ohp][co/2][owp]
-    } else {
-        return 0;
-    }
-}
-
-// Taps of the reduction (BWD_DATA: of this workgroup's stride phase).
-template <int OP>
-__device__ __forceinline__ int tab_taps(const TabArgs &a)
-{
-    if constexpr (OP == OP_GEMM) {
-        return 1;
-    } else if constexpr (OP == OP_BWD_WEIGHT) {
-        return a.s.n * a.s.oh;
-    } else if constexpr (OP == OP_BWD_DATA) {
-        const ConvShape &s = a.s;
-        const int ph = tab_phase(a) / s.sw, pw = tab_phase(a) % s.sw;
-        const int kh0 = (ph + s.pt) % s.sh, kw0 = (pw + s.pl) % s.sw;
-        const int nvh = kh0 < s.kh ? (s.kh - kh0 + s.sh - 1) / s.sh : 0;
-        const int nvw = kw0 < s.kw ? (s.kw - kw0 + s.sw - 1) / s.sw : 0;
-        return nvh * nvw;
-    } else {
-        return a.s.kh * a.s.kw;
-    }
-}
-
-// Steps per tap (the same for every tap of an operation).
-template <int OP>
-__device__ __forceinline__ int tab_count(const TabArgs &a)
-{
-    if constexpr (OP == OP_GEMM) return a.K;
-    else if constexpr (OP == OP_FWD) return a.s.ci;
-    else if constexpr (OP == OP_BWD_DATA) return a.s.co;
-    else return a.s.ow;
-}
-
-// The tap's fields are wave-uniform (they depend on the workgroup and the tap only).
-template <int OP>
-__device__ __forceinline__ TabTap tab_tap_raw(const TabArgs &a, int tap)
-{
-    const ConvShape &s = a.s;
-    TabTap t;
-    if constexpr (OP == OP_GEMM) {
-        t.count = a.K;
-        t.ubase = 0;
-        t.ustride = a.Mp;
-        t.bbase = 0;
-        t.pbase = 0;
-    } else if constexpr (OP == OP_FWD) {
-        const int kh = tap / s.kw, kw = tap % s.kw;
-        t.count = s.ci;
-        t.ubase = kh * s.ci * a.Wp + kw;
-        t.ustride = a.Wp;
-        t.bbase = tap * s.ci;
-        t.pbase = kh * ((s.ci + 1) / 2) * a.Wp + kw;
-    } else if constexpr (OP == OP_BWD_DATA) {
-        const int ph = tab_phase(a) / s.sw, pw = tab_phase(a) % s.sw;
-        const int kh0 = (ph + s.pt) % s.sh, kw0 = (pw + s.pl) % s.sw;
-        const int nvw = (s.kw - kw0 + s.sw - 1) / s.sw;
-        const int kh = kh0 + (tap / nvw) * s.sh, kw = kw0 + (tap % nvw) * s.sw;
-        const int dh = (ph + s.pt - kh) / s.sh, dw = (pw + s.pl - kw) / s.sw;  // exact divisions
-        t.count = s.co;
-        t.ubase = (dh + a.pad_oh) * s.co * a.OWp + dw + a.pad_ow;  // >= 0: the padding covers every dh, dw
-        t.ustride = a.OWp;
-        t.bbase = (kh * s.kw + kw) * s.co;
-        t.pbase = (dh + a.pad_oh) * ((s.co + 1) / 2) * a.OWp + dw + a.pad_ow;
-    } else {
-        const int n = tap / s.oh, oh = tap % s.oh;
-        t.count = s.ow;
-        t.ubase = (n * a.Hp + oh * s.sh) * a.Wp * s.ci;
-        t.ustride = s.sw * s.ci;
-        t.bbase = tap * s.ow;
-        t.pbase = 0;
-    }
-    return t;
-}
-
-template <int OP>
-__device__ __forceinline__ TabTap tab_tap(const TabArgs &a, int tap)
-{
-    const TabTap t = tab_tap_raw<OP>(a, tap);
-    return TabTap{__builtin_amdgcn_readfirstlane(t.ubase), __builtin_amdgcn_readfirstlane(t.ustride),
-                  __builtin_amdgcn_readfirstlane(t.bbase), __builtin_amdgcn_readfirstlane(t.count),
-                  __builtin_amdgcn_readfirstlane(t.pbase)};
-}
-
-// The slab cursor is wave-uniform; saying so at the loop head keeps it, and the buffer loads'
-// step offsets derived from it, in scalar registers (the compiler's uniformity analysis does not
-// prove it through the backward-data phase math and would loop each load over the lanes).
-__device__ __forceinline__ void uniform_cursor(TabTap &cur, int &tap, int &c0)
-{
-    cur = TabTap{__builtin_amdgcn_readfirstlane(cur.ubase), __builtin_amdgcn_readfirstlane(cur.ustride),
-                 __builtin_amdgcn_readfirstlane(cur.bbase), __builtin_amdgcn_readfirstlane(cur.count),
-                 __builtin_amdgcn_readfirstlane(cur.pbase)};
-    tap = __builtin_amdgcn_readfirstlane(tap);
-    c0 = __builtin_amdgcn_readfirstlane(c0);
-}
-
-// Steps per slab of the exact path, rows of 2^RL entries of EB bytes, TNW columns: 8 KiB slabs of
-// 8 / EB steps for the 128-entry rows; wider rows (M = 8..11) take up to 32 KiB slabs of 1 to 8 steps
-// (the step loop is unrolled, so it stays short).
-constexpr int tab_slab_steps(int tnw, int rl, int eb)
-{
-    return rl == 7 ? 8 / eb
-                   : (32768 / (tnw * (1 << rl) * eb) < 1 ? 1
-                                                          : (32768 / (tnw * (1 << rl) * eb) > 8
-                                                                 ? 8
-                                                                 : 32768 / (tnw * (1 << rl) * eb)));
-}
-
-// Slab staging: each thread copies CPT 16-byte pieces of the rows selected by the second
-// operand's mantissas (kb) for slots [0, nslots) of a slab, and that operand's head (pb).
-// TNW = result columns of the workgroup.
-template <int TNW, int EB, int CPT, int NT, int RL>
-__device__ __forceinline__ void tab_fetch(u32x4 (&stage)[CPT], float (&stage_pb)[CPT], const TabTap &tp, int c0,
-                                          const uint32_t *__restrict__ Bd, int Np, int col0,
-                                          const unsigned char *__restrict__ rows)
-{
-    constexpr int ROWB = (1 << RL) * EB;
-    constexpr uint32_t kPad = RL == 7 ? kZeroRowWord : 0u;  // a padding step's second operand: +0
-    constexpr int PIECES = ROWB / 16;
-    constexpr int TOTAL = tab_slab_steps(TNW, RL, EB) * TNW * PIECES;
-#pragma unroll
-    for (int i = 0; i < CPT; ++i) {
-        const int c = threadIdx.x + i * NT;
-        if (CPT * NT > TOTAL && c >= TOTAL) break;  // the workgroup size does not divide the slab
-        const int slot = c / (TNW * PIECES);
-        const int t = (c / PIECES) % TNW;
-        const int piece = c % PIECES;
-        const int j = c0 + slot;
-        const uint32_t bw = j < tp.count ? Bd[int64_t(tp.bbase + j) * Np + col0 + t] : kPad;
-        stage_pb[i] = head_value(bw);
-        stage[i] = *reinterpret_cast<const u32x4 *>(rows + (bw & kIdxMask) * EB + piece * 16);  // idx = kb << RL
-    }
-}
-
-template <int TNW, int EB, int CPT, int NT, int RL>
-__device__ __forceinline__ void tab_commit(const u32x4 (&stage)[CPT], const float (&stage_pb)[CPT],
-                                           unsigned char *smem, float *pbs, int buf)
-{
-    constexpr int ROWB = (1 << RL) * EB;
-    constexpr int KS = tab_slab_steps(TNW, RL, EB);
-    constexpr int SLAB = KS * TNW * ROWB;
-    constexpr int PIECES = ROWB / 16;
-#pragma unroll
-    for (int i = 0; i < CPT; ++i) {
-        const int c = threadIdx.x + i * NT;
-        if (CPT * NT > SLAB / 16 && c >= SLAB / 16) break;
-        *reinterpret_cast<u32x4 *>(smem + buf * SLAB + c * 16) = stage[i];
-        if (c % PIECES == 0) pbs[buf * KS * TNW + c / PIECES] = stage_pb[i];
-    }
-}
-
-// Workgroup: NW waves as a WR x (NW/WR) grid -- WR row blocks of 64*TM rows, NW/WR column groups
-// of TN columns.  All waves share the LDS tables of the workgroup's TN * NW/WR columns.
-template <int OP, int TM, int TN, int WR, int EB, int NW, int RL>
-__device__ __forceinline__ void tab_body(const TabArgs &a)
-{
-    constexpr int NT = 64 * NW;
-    constexpr int WC = NW / WR;
-    constexpr int TNW = TN * WC;                // result columns of the workgroup
-    constexpr int ROWB = (1 << RL) * EB;        // a table row: 2^RL entries
-    constexpr int KS = tab_slab_steps(TNW, RL, EB);
-    constexpr int SLAB = KS * TNW * ROWB;
-    constexpr int CPT = (SLAB / 16 + NT - 1) / NT;  // pieces per thread per slab (the last round partial)
-    extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
-    float *pbs = reinterpret_cast<float *>(smem + 2 * SLAB);  // [2][KS][TNW] second-operand heads
-
-    const int R = tab_rows<OP>(a);
-    if (a.tx * 64 * TM * WR >= R) return;  // uniform over the workgroup
-    const int lane = threadIdx.x & 63;
-    const int wave = wave_id();
-    const int rg = wave % WR, cg = wave / WR;
-    const int row0 = a.tx * (64 * TM * WR) + rg * (64 * TM) + lane;
-    const bool live = row0 - lane < R;  // wave-uniform: a wave past the end only stages
-    const int colw = a.ty * TNW;  // first column of the workgroup
-    const int col0 = colw + cg * TN;    // first column of this wave
-    // First-operand reads are raw buffer loads: voffset = the lane row's byte offset (range-checked,
-    // reads past the buffer return 0), soffset = the wave-uniform step offset, which every tap keeps
-    // non-negative and inside the tensor, since the hardware does not range-check it.
-    int abase[TM];  // element offset of each lane row's first-operand run
-#pragma unroll
-    for (int r = 0; r < TM; ++r) {
-        const int row = row0 + 64 * r;
-        int ab = 0;
-        int64_t ob = 0;
-        if (row < R) {
-            tab_row<OP>(a, row, ab, ob);
-            if constexpr (split_a<OP>()) ab = tab_row_rec<OP>(a, row);
-        }
-        abase[r] = ab;
-    }
-    const AView<TM> av = make_aview<OP, TM>(a, abase);
-    // this split's chunks, as positions p = tap * (8 * chunks per tap) + step
-    const int count = tab_count<OP>(a);
-    const int cpt = (count + 7) / 8;  // chunks per tap
-    const int q_total = tab_taps<OP>(a) * cpt;
-    const int q0 = tab_split(a) * a.chunks_per_split;
-    const int p_end = min(q_total, q0 + a.chunks_per_split) * 8;
-
-    u32x4 stage[CPT];
-    float stage_pb[CPT];
-    float acc[TM][TN];
-    init_acc(acc);
-    uint32_t acur[TM];
-    TabTap cur{0, 0, 0, 0, 0};
-    int tap = q0 / max(cpt, 1);
-    int c0 = (q0 - tap * cpt) * 8;
-    bool have = q0 * 8 < p_end;
-    if (have) {
-        cur = tab_tap<OP>(a, tap);
-        tab_fetch<TNW, EB, CPT, NT, RL>(stage, stage_pb, cur, c0, a.Bd, a.Np, colw, a.rows);
-        tab_commit<TNW, EB, CPT, NT, RL>(stage, stage_pb, smem, pbs, 0);
-        load_a_words<OP, TM>(acur, av, __builtin_amdgcn_readfirstlane(a_step_offset<OP>(cur, c0)), c0);
-    }
-    __syncthreads();
-    int buf = 0;
-    while (have) {
-        uniform_cursor(cur, tap, c0);
-        // the slab after this one
-        TabTap nxt = cur;
-        int ntap = tap, nc0 = c0 + KS;
-        if (nc0 >= count) {
-            ntap = tap + 1;
-            nc0 = 0;
-        }
-        const bool has_next = ntap * cpt * 8 + nc0 < p_end;
-        if (has_next && ntap != tap) nxt = tab_tap<OP>(a, ntap);
-        if (has_next) tab_fetch<TNW, EB, CPT, NT, RL>(stage, stage_pb, nxt, nc0, a.Bd, a.Np, colw, a.rows);
-        const unsigned char *tb = smem + buf * SLAB + cg * TN * ROWB;
-        const float *pb_s = pbs + buf * KS * TNW + cg * TN;
-        // the slab ends at the tap's end or, 8-step chunks being the unit of splits, at the split's
-        const int nslots = live ? min(min(KS, cur.count - c0), p_end - (tap * cpt * 8 + c0)) : 0;
-#pragma unroll
-        for (int slot = 0; slot < KS; ++slot) {
-            if (slot >= nslots) break;
-            // next step's first-operand words: this slab's next slot or the next slab's first
-            uint32_t anext[TM];
-            const bool in_slab = slot + 1 < nslots;
-            const uint32_t unext = __builtin_amdgcn_readfirstlane(in_slab ? a_step_offset<OP>(cur, c0 + slot + 1)
-                                                                          : a_step_offset<OP>(nxt, nc0));
-            const int jnext = __builtin_amdgcn_readfirstlane(in_slab ? c0 + slot + 1 : nc0);
-            if (in_slab || has_next) {
-                load_a_words<OP, TM>(anext, av, unext, jnext);
-            } else {
-#pragma unroll
-                for (int r = 0; r < TM; ++r) anext[r] = 0u;
-            }
-            const unsigned char *vaddr[TM];
-            float pa[TM];
-#pragma unroll
-            for (int r = 0; r < TM; ++r) {
-                vaddr[r] = tb + __builtin_amdgcn_ubfe(acur[r], 4, RL) * EB;  // idx = ka << 4
-                pa[r] = head_value(acur[r]);
-            }
-#pragma unroll
-            for (int t = 0; t < TN; ++t) {
-                const float pb = pb_s[slot * TNW + t];
-#pragma unroll
-                for (int r = 0; r < TM; ++r) {
-                    const float v = tab_value<EB>(vaddr[r] + (slot * TNW + t) * ROWB);
-                    acc[r][t] = __builtin_fmaf(v, pa[r] * pb, acc[r][t]);
-                }
-            }
-#pragma unroll
-            for (int r = 0; r < TM; ++r) acur[r] = anext[r];
-        }
-        if (has_next) tab_commit<TNW, EB, CPT, NT, RL>(stage, stage_pb, smem, pbs, buf ^ 1);
-        __syncthreads();
-        cur = nxt;
-        tap = ntap;
-        c0 = nc0;
-        buf ^= 1;
-        have = has_next;
-    }
-
-    // results (with splits, each split's partial result is laid out like the final one)
-    float *out = a.out + int64_t(tab_split(a)) * a.out_elems;
-#pragma unroll
-    for (int r = 0; r < TM; ++r) {
-        const int row = row0 + 64 * r;
-        if (row >= R) continue;
-        int ab = 0;
-        int64_t ob = 0;
-        tab_row<OP>(a, row, ab, ob);  // the output offset, recomputed rather than kept in registers
-        float *dst = out + ob;
-#pragma unroll
-        for (int t = 0; t < TN; ++t) {
-            const int col = col0 + t;
-            if (col < a.N) dst[col] = acc[r][t];
-        }
-    }
-}
-
-// ---------------------------------------------------------- bf16 pair path (1-byte tables)
-// When every table entry fits 8 bits (its low 16 mantissa bits are zero) a table value v is a
-// bfloat16, and so are v * pb (the second operand's sign and exponent added to v's bits) and pa.
-// Products of such operands are exact in fp32, so two reduction steps k, k+1 can go through one
-// v_dot2_f32_bf16:  acc += t(k) * pa(k) + t(k+1) * pa(k+1),  t = v * pb.
-// The slab then holds, per step and first-operand mantissa ka, one 16-byte entry with t for the
-// workgroup's 8 columns (8 bf16); a lane reads it with one ds_read_b128 and pairs the halves of
-// two steps' entries with v_perm.
-// Exactness needs every product of finite non-zero operands to stay normal (exponent field
-// Ea + Eb - 127 + carry in [1, 254]) and v * pb not to overflow; the decode passes record the
-// operands' exponent range and the kernel takes this path only when that holds (else the exact
-// path).  Inside that range each product is the exact Algorithm 2 result; the sum is rounded
-// per pair instead of per step.  A sum that comes out exactly zero gets its sign from a second
-// pass over its products (the hardware returns +0 for zero sums; the sign of a sum of zeros is
-// -0 exactly when every product is -0).
-typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
-typedef uint16_t u16x2_t __attribute__((ext_vector_type(2)));
-
-// Columns per entry DC: 8, or 4 for narrow outputs.  Entries sit 16 bytes apart either way (the
-// first operand's index field is the byte offset ka * 16); a 4-column entry fills half a slot.
-constexpr bool dot_cols_ok(int dc) { return dc == 8 || dc == 4; }
-constexpr int kDotStepBytes = kTabRowEntries * 16;  // 128 entries, 16-byte slots
-// Steps per slab: 2 per wave (each thread stages one step's entry group, 32 threads per step).
-constexpr int dot_slab_steps(int nw) { return nw * 2; }
-
-// 16 bytes of LDS at byte address off + imm.  The table kernels use no static LDS, so their
-// dynamic allocation starts at LDS address 0 (checked on the host when the kernels are set up);
-// addressing it as such lets the constant part land in the instruction's offset field.
-typedef __attribute__((address_space(3))) const u32x4 lds_u32x4;
-__device__ __forceinline__ u32x4 lds_load_b128(uint32_t off, uint32_t imm)
-{
-    return reinterpret_cast<lds_u32x4 *>(uintptr_t(off))[imm / 16];
-}
-
-// The same for 8 bytes (imm a multiple of 8).
-typedef __attribute__((address_space(3))) const u32x2 lds_u32x2;
-__device__ __forceinline__ u32x2 lds_load_b64(uint32_t off, uint32_t imm)
-{
-    return reinterpret_cast<lds_u32x2 *>(uintptr_t(off))[imm / 8];
-}
-
-__device__ __forceinline__ float dot2_bf16(uint32_t x, uint32_t y, float c)
-{
-    return __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2_t, x), __builtin_bit_cast(bf16x2_t, y), c,
-                                           false);
-}
-
-__device__ __forceinline__ uint32_t add_u16x2(uint32_t x, uint32_t y)
-{
-    return __builtin_bit_cast(uint32_t, __builtin_bit_cast(u16x2_t, x) + __builtin_bit_cast(u16x2_t, y));
-}
-
-// Staging of one slab: thread -> step slot (tid / 32) and entry group g (tid % 32), which builds
-// the entries ka = g, g + 32, g + 64, g + 96.  Fetch, in two parts: the slot's DC second-operand
-// words, then, per column, the 4 bytes of its table row that hold those entries.
-template <int DC>
-__device__ __forceinline__ void dot_fetch_b(u32x4 (&bw)[2], const TabTap &tp, int c0, const uint32_t *__restrict__ Bd,
-                                            int Np, int colw)
-{
-    const int slot = threadIdx.x >> 5;
-    const int j = c0 + slot;
-    if (j < tp.count) {
-        const u32x4 *src = reinterpret_cast<const u32x4 *>(Bd + int64_t(tp.bbase + j) * Np + colw);
-        bw[0] = src[0];
-        bw[1] = DC == 8 ? src[1] : bw[0];
-    } else {  // a padding step: +0 operands, whose entries are +0
-        bw[0] = u32x4{kZeroRowWord, kZeroRowWord, kZeroRowWord, kZeroRowWord};
-        bw[1] = bw[0];
-    }
-}
-
-template <int DC>
-__device__ __forceinline__ void dot_fetch_rows(uint32_t (&rw)[DC], const u32x4 (&bw)[2], __amdgpu_buffer_rsrc_t rres)
-{
-    const int g = threadIdx.x & 31;
-#pragma unroll
-    for (int c = 0; c < DC; ++c) {
-        const uint32_t w = bw[c / 4][c % 4];  // idx = kb * 128 (kZeroRow for zeros)
-        rw[c] = __builtin_amdgcn_raw_buffer_load_b32(rres, (w & 0x7F80u) | uint32_t(g * 4), 0, 0);
-    }
-}
-
-// Commit: t = v * pb as bf16 bits = table byte + (pb's bits >> 16); a zero second operand reads
-// the zero row and gets signed zeros.  Entry dword q = (t of column 2q, t of column 2q + 1).
-template <int DC>
-__device__ __forceinline__ void dot_commit(const u32x4 (&bw)[2], const uint32_t (&rw)[DC], unsigned char *slab)
-{
-    const int slot = threadIdx.x >> 5, g = threadIdx.x & 31;
-    const uint32_t(&w)[DC] = rw;
-    uint32_t hb[DC / 2];
-#pragma unroll
-    for (int q = 0; q < DC / 2; ++q)
-        hb[q] = __builtin_amdgcn_perm(bw[(2 * q + 1) / 4][(2 * q + 1) % 4], bw[(2 * q) / 4][(2 * q) % 4], 0x07060302u);
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-        uint32_t e[DC / 2];
-#pragma unroll
-        for (int q = 0; q < DC / 2; ++q) {
-            // low half: byte i of the even column's word, high half: byte i of the odd one's
-            const uint32_t d = __builtin_amdgcn_perm(w[2 * q + 1], w[2 * q], 0x0C000C00u | ((4u + i) << 16) | i);
-            e[q] = add_u16x2(d, hb[q]);
-        }
-        unsigned char *dst = slab + slot * kDotStepBytes + (g + 32 * i) * 16;
-        if constexpr (DC == 8)
-            *reinterpret_cast<u32x4 *>(dst) = u32x4{e[0], e[1], e[2], e[3]};
-        else
-            *reinterpret_cast<u32x2 *>(dst) = u32x2{e[0], e[1]};
-    }
-}
-
-// First-operand data of the step pair (j, j + 1) per lane row: the two words, or (split layout)
-// the two indices and the head pair.  A step past the tap's end (the odd step of a pair, or a
-// slab's unused slots) reads the tap's last step again: its slot in the slab holds +0 entries
-// (staged from a +0 second operand), so it adds signed zeros only, and the loads stay
-// branch-free and in bounds.
-template <int OP, int TM>
-__device__ __forceinline__ void dot_load_pair(uint32_t (&dst)[split_a<OP>() ? 3 : 2][TM], const AView<TM> &av,
-                                              const TabTap &tp, int j)
-{
-    const int j0 = min(j, tp.count - 1), j1 = min(j + 1, tp.count - 1);
-    if constexpr (split_a<OP>()) {
-        // j even: one record holds both steps (past the end: the last record; an odd count's
-        // last record has a decoded +0 for its missing step)
-        const uint32_t so = __builtin_amdgcn_readfirstlane(a_step_offset<OP>(tp, j0));
-#pragma unroll
-        for (int r = 0; r < TM; ++r) {
-            const u32x3 rec = __builtin_amdgcn_raw_buffer_load_b96(av.words, av.aoff[r], so, 0);
-            dst[0][r] = rec.x;
-            dst[1][r] = rec.z;
-            dst[2][r] = rec.y;
-        }
-    } else {
-        const uint32_t s0 = __builtin_amdgcn_readfirstlane(a_step_offset<OP>(tp, j0));
-        const uint32_t s1 = __builtin_amdgcn_readfirstlane(a_step_offset<OP>(tp, j1));
-#pragma unroll
-        for (int r = 0; r < TM; ++r) {
-            dst[0][r] = __builtin_amdgcn_raw_buffer_load_b32(av.words, av.aoff[r], s0, 0);
-            dst[1][r] = __builtin_amdgcn_raw_buffer_load_b32(av.words, av.aoff[r], s1, 0);
-        }
-    }
-}
-
-// Workgroup: NW waves along rows (64*TM rows each), all on the same 8 columns.  Every thread
-// stages one step's entry group per slab (KS = 2 * NW steps x 32 groups).
-template <int OP, int TM, int NW, int DC>
-__device__ __forceinline__ void tab_body_dot(const TabArgs &a)
-{
-    static_assert(dot_cols_ok(DC), "8 or 4 columns per entry");
-    constexpr int KS = dot_slab_steps(NW);
-    constexpr int kDotSlab = KS * kDotStepBytes;
-    constexpr int TN = DC;
-    constexpr bool SPLIT = split_a<OP>();
-    constexpr int NA = SPLIT ? 3 : 2;  // first-operand registers per step pair and lane row
-    extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
-
-    const int R = tab_rows<OP>(a);
-    if (a.tx * 64 * TM * NW >= R) return;  // uniform over the workgroup
-    const int lane = threadIdx.x & 63;
-    const int wave = wave_id();
-    const int row0 = a.tx * (64 * TM * NW) + wave * (64 * TM) + lane;
-    const bool live = row0 - lane < R;  // wave-uniform
-    const int col0 = a.ty * TN;
-    const __amdgpu_buffer_rsrc_t rres = __builtin_amdgcn_make_buffer_rsrc(
-        const_cast<unsigned char *>(a.dot_rows), 0, int((kZeroRow + 1) * kTabRowEntries), 0x00020000);
-
-    int abase[TM];
-#pragma unroll
-    for (int r = 0; r < TM; ++r) {
-        const int row = row0 + 64 * r;
-        int ab = 0;
-        int64_t ob = 0;
-        if (row < R) {
-            tab_row<OP>(a, row, ab, ob);
-            if constexpr (split_a<OP>()) ab = tab_row_rec<OP>(a, row);
-        }
-        abase[r] = ab;
-    }
-    const AView<TM> av = make_aview<OP, TM>(a, abase);
-    const int count = tab_count<OP>(a);
-    const int cpt = (count + 7) / 8;
-    const int q_total = tab_taps<OP>(a) * cpt;
-    const int q0 = tab_split(a) * a.chunks_per_split;
-    const int p_end = min(q_total, q0 + a.chunks_per_split) * 8;
-
-    // Staging pipeline: while slab s is computed, the table bytes of slab s + 1 are fetched (its
-    // second-operand words `sbw` having arrived during slab s - 1) and the second-operand words
-    // of slab s + 2 are loaded into `sbw2`.  With 8-step slabs (4-wave workgroups) the words'
-    // latency would otherwise be exposed once per slab; 16-step slabs fetch both in slab s.
-    constexpr bool AHEAD2 = NW <= 4;
-    u32x4 sbw[2], sbw2[2];
-    uint32_t srw[DC];
-    float acc[TM][TN];
-    init_acc(acc);
-    // First-operand data of RS step pairs, as a ring: pair kp of a slab is in w[kp % RS]; while
-    // it is used, pair kp + 2 (of this slab, or the next slab's first two for the last two pairs)
-    // is loaded into w[(kp + 2) % RS].  A slab holds a multiple of RS pairs, so after a full slab
-    // the next slab's first two pairs sit in w[0], w[1].
-    constexpr int RS = (KS / 2) % 4 == 0 ? 4 : KS / 2;
-    static_assert(RS >= 3 && (KS / 2) % RS == 0, "ring of step pairs");
-    uint32_t w[RS][NA][TM];
-    // The slab after (t, tp_, c): its tap, cursor and whether it is in this split's range (if not,
-    // `o` stays `t`, so that loads aimed at it stay in bounds).
-    auto advance = [&](const TabTap &t, int tp_, int c, TabTap &o, int &otap, int &oc, bool &ok)
-                       __attribute__((always_inline)) {
-        o = t;
-        otap = tp_;
-        oc = c + KS;
-        if (oc >= count) {
-            otap = tp_ + 1;
-            oc = 0;
-        }
-        ok = otap * cpt * 8 + oc < p_end;
-        if (ok && otap != tp_) o = tab_tap<OP>(a, otap);
-    };
-    TabTap cur{0, 0, 0, 0, 0};
-    int tap = q0 / max(cpt, 1);
-    int c0 = (q0 - tap * cpt) * 8;
-    bool have = q0 * 8 < p_end;
-    TabTap nxt{0, 0, 0, 0, 0};
-    int ntap = 0, nc0 = 0;
-    bool has_next = false;
-    if (have) {
-        cur = tab_tap<OP>(a, tap);
-        dot_fetch_b<DC>(sbw, cur, c0, a.Bd, a.Np, col0);
-        dot_fetch_rows<DC>(srw, sbw, rres);
-        dot_commit<DC>(sbw, srw, smem);
-#pragma unroll
-        for (int k = 0; k < 2; ++k) dot_load_pair<OP, TM>(w[k], av, cur, c0 + 2 * k);
-        advance(cur, tap, c0, nxt, ntap, nc0, has_next);
-        if (AHEAD2 && has_next) dot_fetch_b<DC>(sbw, nxt, nc0, a.Bd, a.Np, col0);
-    }
-    __syncthreads();
-    // One slab from buffer BUF (a compile-time LDS offset, folded into the gathers' immediate
-    // offsets); the next slab is staged into the other buffer.
-    auto slab = [&](auto buf_c) __attribute__((always_inline)) {
-        constexpr uint32_t BOFF = uint32_t(decltype(buf_c)::value) * kDotSlab;
-        constexpr uint32_t NEXT = uint32_t(decltype(buf_c)::value ^ 1) * kDotSlab;
-        uniform_cursor(cur, tap, c0);
-        uniform_cursor(nxt, ntap, nc0);
-        TabTap nxt2 = nxt;
-        int ntap2 = ntap, nc02 = nc0;
-        bool has_next2 = false;
-        if constexpr (AHEAD2) {
-            advance(nxt, ntap, nc0, nxt2, ntap2, nc02, has_next2);
-            has_next2 = has_next2 && has_next;
-            if (has_next) dot_fetch_rows<DC>(srw, sbw, rres);
-            if (has_next2) dot_fetch_b<DC>(sbw2, nxt2, nc02, a.Bd, a.Np, col0);
-        } else if (has_next) {
-            dot_fetch_b<DC>(sbw, nxt, nc0, a.Bd, a.Np, col0);
-            dot_fetch_rows<DC>(srw, sbw, rres);
-        }
-        // the slab ends at the tap's end or, 8-step chunks being the unit of splits, at the split's
-        const int nslots = min(min(KS, cur.count - c0), p_end - (tap * cpt * 8 + c0));
-        // a wave whose rows all lie past the end only stages and keeps the barriers
-        const int npairs = live ? (nslots + 1) / 2 : 0;
-#pragma unroll
-        for (int kp = 0; kp < KS / 2; ++kp) {
-            if (kp >= npairs) break;
-            if (kp + 2 < KS / 2)
-                dot_load_pair<OP, TM>(w[(kp + 2) % RS], av, cur, c0 + 2 * kp + 4);
-            else
-                dot_load_pair<OP, TM>(w[(kp + 2) % RS], av, nxt, nc0 + 2 * (kp + 2 - KS / 2));
-            const uint32_t(&a0)[TM] = w[kp % RS][0];
-            const uint32_t(&a1)[TM] = w[kp % RS][1];
-#pragma unroll
-            for (int r = 0; r < TM; ++r) {
-                // entry byte offset = the mantissa field * 16 (the index plane, or the word's low
-                // half under its head) plus the slot's, which is a constant
-                const uint32_t o0 = SPLIT ? a0[r] : (a0[r] & 0xFFFFu);
-                const uint32_t o1 = SPLIT ? a1[r] : (a1[r] & 0xFFFFu);
-                uint32_t X[DC / 2], Y[DC / 2];
-                if constexpr (DC == 8) {
-                    const u32x4 x4 = lds_load_b128(o0, BOFF + (2 * kp) * kDotStepBytes);
-                    const u32x4 y4 = lds_load_b128(o1, BOFF + (2 * kp + 1) * kDotStepBytes);
-#pragma unroll
-                    for (int q = 0; q < 4; ++q) {
-                        X[q] = x4[q];
-                        Y[q] = y4[q];
-                    }
-                } else {
-                    const u32x2 x2 = lds_load_b64(o0, BOFF + (2 * kp) * kDotStepBytes);
-                    const u32x2 y2 = lds_load_b64(o1, BOFF + (2 * kp + 1) * kDotStepBytes);
-#pragma unroll
-                    for (int q = 0; q < 2; ++q) {
-                        X[q] = x2[q];
-                        Y[q] = y2[q];
-                    }
-                }
-                uint32_t pa;  // (pa(k), pa(k+1)) as bf16
-                if constexpr (SPLIT)
-                    pa = w[kp % RS][NA - 1][r];
-                else
-                    pa = __builtin_amdgcn_perm(a1[r], a0[r], 0x07060302u);
-#pragma unroll
-                for (int q = 0; q < TN / 2; ++q) {
-                    acc[r][2 * q] = dot2_bf16(__builtin_amdgcn_perm(Y[q], X[q], 0x05040100u), pa, acc[r][2 * q]);
-                    acc[r][2 * q + 1] =
-                        dot2_bf16(__builtin_amdgcn_perm(Y[q], X[q], 0x07060302u), pa, acc[r][2 * q + 1]);
-                }
-            }
-        }
-        if (live && npairs < KS / 2 && has_next) {  // a short slab: the next slab's first two pairs
-#pragma unroll
-            for (int k = 0; k < 2; ++k) dot_load_pair<OP, TM>(w[k], av, nxt, nc0 + 2 * k);
-        }
-        if (has_next) dot_commit<DC>(sbw, srw, smem + NEXT);
-        __syncthreads();
-        cur = nxt;
-        tap = ntap;
-        c0 = nc0;
-        have = has_next;
-        if constexpr (AHEAD2) {
-            nxt = nxt2;
-            ntap = ntap2;
-            nc0 = nc02;
-            has_next = has_next2;
-            sbw[0] = sbw2[0];
-            sbw[1] = sbw2[1];
-        } else {
-            advance(cur, tap, c0, nxt, ntap, nc0, has_next);
-        }
-    };
-    while (have) {
-        slab(std::integral_constant<int, 0>{});
-        if (!have) break;
-        slab(std::integral_constant<int, 1>{});
-    }
-
-    // Signs of zero sums: -0 when every product of the split's range is -0, else +0.  The first
-    // product that is not -0 (non-zero, or +0) settles an output as +0, so the pass stops once no
-    // output of the wave is pending -- after one step for a sum that cancelled to zero, after the
-    // whole range only for outputs whose products are all -0.
-    uint32_t pending = 0u;
-#pragma unroll
-    for (int r = 0; r < TM; ++r)
-#pragma unroll
-        for (int t = 0; t < TN; ++t)
-            if (row0 + 64 * r < R && col0 + t < a.N && acc[r][t] == 0.0f) pending |= 1u << (r * TN + t);
-    const uint32_t zero = pending;
-    if (__builtin_amdgcn_ballot_w64(pending != 0u) != 0u) {
-        bool open = true;
-        for (int tp_i = q0 / max(cpt, 1); open && tp_i * cpt * 8 < p_end; ++tp_i) {
-            const int pbase = tp_i * cpt * 8;
-            const TabTap tp = tab_tap<OP>(a, tp_i);
-            const int j1 = min(tp.count, p_end - pbase);
-            for (int j = max(q0 * 8 - pbase, 0); j < j1; ++j) {
-                uint32_t aw[TM];
-                load_a_words<OP, TM>(aw, av, __builtin_amdgcn_readfirstlane(a_step_offset<OP>(tp, j)), j);
-                const uint32_t *brow = a.Bd + int64_t(tp.bbase + j) * a.Np + col0;
-#pragma unroll
-                for (int t = 0; t < TN; ++t) {
-                    const float pb = head_value(brow[t]);
-#pragma unroll
-                    for (int r = 0; r < TM; ++r)
-                        if (__float_as_uint(head_value(aw[r]) * pb) != 0x80000000u) pending &= ~(1u << (r * TN + t));
-                }
-                if (__builtin_amdgcn_ballot_w64(pending != 0u) == 0u) {
-                    open = false;
-                    break;
-                }
-            }
-        }
-#pragma unroll
-        for (int r = 0; r < TM; ++r)
-#pragma unroll
-            for (int t = 0; t < TN; ++t)
-                if (zero & (1u << (r * TN + t))) acc[r][t] = (pending & (1u << (r * TN + t))) ? -0.0f : 0.0f;
-    }
-
-    float *out = a.out + int64_t(tab_split(a)) * a.out_elems;
-#pragma unroll
-    for (int r = 0; r < TM; ++r) {
-        const int row = row0 + 64 * r;
-        if (row >= R) continue;
-        int ab = 0;
-        int64_t ob = 0;
-        tab_row<OP>(a, row, ab, ob);  // the output offset, recomputed rather than kept in registers
-        float *dst = out + ob;
-#pragma unroll
-        for (int t = 0; t < TN; ++t) {
-            const int col = col0 + t;
-            if (col < a.N) dst[col] = acc[r][t];
-        }
-    }
-}
-
-// Four waves per SIMD: the register budget (<= 128 VGPRs) the tiles are sized for.  Without the
-// hint the scheduler minimises registers and serialises the LDS gathers.
-// RL: log2 of the table row length, 7 (rows padded to 128 entries) for M <= 7, else M.
-template <int OP, int TM, int TN, int WR, int NW, int RL>
-__global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(4, 4))) void tab_kernel(TabArgs args)
-{
-    TabArgs a = args;
-    tab_tile_id(a.splits, a.tx, a.ty, a.tz);
-    const int eb = __builtin_amdgcn_readfirstlane(a.eb[0]);
-    if constexpr (RL == 7 && dot_cols_ok(TN) && WR == NW) {
-        if (__builtin_amdgcn_readfirstlane(a.eb[1]) != 0) {
-            tab_body_dot<OP, TM, NW, TN>(a);
-            return;
-        }
-    }
-    if (eb == 1)
-        tab_body<OP, TM, TN, WR, 1, NW, RL>(a);
-    else if (eb == 2)
-        tab_body<OP, TM, TN, WR, 2, NW, RL>(a);
-    else
-        tab_body<OP, TM, TN, WR, 4, NW, RL>(a);
-}
-
-// Dynamic LDS of a table kernel with TN columns per wave, WR of its NW waves along rows and rows
-// of 2^RL entries: two exact-path slabs (the widest entry width) plus the second-operand heads, or
-// two bf16-path slabs where that path exists.
-constexpr size_t tab_exact_lds_bytes(int tnw, int rl, int eb)
-{
-    return size_t(2) * tab_slab_steps(tnw, rl, eb) * tnw * ((size_t(1) << rl) * eb) +
-           size_t(2) * tab_slab_steps(tnw, rl, eb) * tnw * 4;
-}
-
-constexpr size_t tab_lds_bytes(int tn, int wr, int nw, int rl)
-{
-    const int tnw = tn * (nw / wr);
-    size_t b = tab_exact_lds_bytes(tnw, rl, 1);
-    b = tab_exact_lds_bytes(tnw, rl, 2) > b ? tab_exact_lds_bytes(tnw, rl, 2) : b;
-    b = tab_exact_lds_bytes(tnw, rl, 4) > b ? tab_exact_lds_bytes(tnw, rl, 4) : b;
-    const size_t dot = (rl == 7 && dot_cols_ok(tn) && wr == nw) ? size_t(2) * dot_slab_steps(nw) * kDotStepBytes : 0;
-    return b > dot ? b : dot;
-}
-
 // ------------------------------------------------------------------ host dispatch -------
 
 constexpr size_t kAlign = 256;
@@ -1650,31 +603,14 @@ inline int64_t ceil_div(int64_t x, int64_t m) { return (x + m - 1) / m; }
 // log2 of the table row length: rows are padded to 128 entries for M <= 7.
 inline int row_log(int m_bits) { return m_bits > 7 ? m_bits : 7; }
 
-struct Tile {
-    int tm = 1, tn = 4, split = 1;
-    int wr = 4;  // waves along rows (the rest take column groups)
-    int nw = 4;  // waves per workgroup
-};
-
-
-// Tile candidates: the instantiated (TM, TN, WR, NW) tiles, per table-row length.  The cost per
-// product used to choose among them (choose_tab_tile): the inner loop (~1.2 VALU ops on the bf16
-// pair path, which 8-column tiles with all waves on rows take for 1-byte tables; 3 on the exact
-// path), per-step overhead (~2.5 per row, ~4 per lane), and the table staging, which is per
-// workgroup and slab, so its share per product falls with the workgroup's rows (64 * TM * WR) and
-// grows with the row length (weight fitted on MI355X: a 64 x 32 backward-weight tile ran 2.4x
-// slower than a 256 x 8 one, a 768-row GEMM tile 15% slower than a 1024-row one).  Tiles whose
-// registers would spill past the 128-VGPR budget are left out.
-struct TabCand {
-    int tm, tn, wr, nw;
-};
-constexpr TabCand kTabCands[] = {{4, 8, 8, 8}, {4, 8, 4, 4}, {3, 8, 4, 4}, {2, 8, 4, 4}, {1, 8, 4, 4},
-                                 {4, 4, 8, 8}, {4, 4, 4, 4}, {2, 4, 4, 4}, {1, 4, 4, 4}, {4, 8, 2, 4}, {2, 8, 2, 4},
-                                 {1, 8, 2, 4}, {2, 8, 1, 4}, {1, 8, 1, 4}};
-// Wide rows (M = 8..10; 11 uses the 4-column tiles, whose 4-byte-entry slab of one step fits 32 KiB).
-constexpr TabCand kWideCands[] = {{8, 4, 8, 8}, {4, 8, 8, 8}, {2, 8, 4, 4}, {1, 8, 4, 4}, {1, 4, 4, 4}};
-constexpr TabCand kWide11Cands[] = {{8, 4, 8, 8}, {4, 4, 8, 8}, {2, 4, 4, 4}, {1, 4, 4, 4}};
-
+// Cost per product used to choose among the candidate tiles (kTabCands and the wide-row lists):
+// the inner loop (~1.2 VALU ops on the bf16 pair path, which 8-column tiles with all waves on
+// rows take for 1-byte tables; 3 on the exact path), per-step overhead (~2.5 per row, ~4 per
+// lane), and the table staging, which is per workgroup and slab, so its share per product falls
+// with the workgroup's rows (64 * TM * WR) and grows with the row length (weight fitted on
+// MI355X: a 64 x 32 backward-weight tile ran 2.4x slower than a 256 x 8 one, a 768-row GEMM tile
+// 15% slower than a 1024-row one).
+//
 // Tile and reduction split for `rows` x `cols` outputs (times `phases` independent grids) over q
 // reduction chunks of 8 steps.  The products a tile computes (rows padded to whole waves) times
 // an issue-cost estimate per product, spread over the workgroups; the workgroups per CU that LDS
@@ -1769,38 +705,11 @@ inline int64_t tab_cols(const Tile &t) { return int64_t(t.tn) * (t.nw / t.wr); }
 std::once_flag g_attr_once;
 hipError_t g_attr_err = hipSuccess;
 
-// Raises the kernel's dynamic LDS limit, and checks that it has no static LDS: the bf16 path
-// addresses its slabs as LDS addresses starting at 0.
-template <typename K>
-void allow_lds(K kernel, size_t bytes)
-{
-    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void *>(kernel),
-                                       hipFuncAttributeMaxDynamicSharedMemorySize, int(bytes));
-    if (e != hipSuccess) g_attr_err = e;
-    hipFuncAttributes fa{};
-    e = hipFuncGetAttributes(&fa, reinterpret_cast<const void *>(kernel));
-    if (e != hipSuccess) g_attr_err = e;
-    else if (fa.sharedSizeBytes != 0) g_attr_err = hipErrorInvalidKernelFile;
-}
-
-// The instantiated (TM, TN, WR, NW, RL) tiles: every candidate of the chooser above.
-#define AMSIM_FOR_TAB_TILES(X)                                                                                \
-    X(4, 8, 8, 8, 7) X(4, 8, 4, 4, 7) X(3, 8, 4, 4, 7) X(2, 8, 4, 4, 7) X(1, 8, 4, 4, 7) X(4, 4, 8, 8, 7)     \
-    X(4, 4, 4, 4, 7) X(2, 4, 4, 4, 7) X(1, 4, 4, 4, 7) X(4, 8, 2, 4, 7) X(2, 8, 2, 4, 7) X(1, 8, 2, 4, 7)     \
-    X(2, 8, 1, 4, 7) X(1, 8, 1, 4, 7) AMSIM_WIDE_TILES(X, 8) AMSIM_WIDE_TILES(X, 9) AMSIM_WIDE_TILES(X, 10) X(8, 4, 8, 8, 11)     \
-    X(4, 4, 8, 8, 11) X(2, 4, 4, 4, 11) X(1, 4, 4, 4, 11)
-#define AMSIM_WIDE_TILES(X, RL)                                                                                \
-    X(8, 4, 8, 8, RL) X(4, 8, 8, 8, RL) X(2, 8, 4, 4, RL) X(1, 8, 4, 4, RL) X(1, 4, 4, 4, RL)
-
 void set_attributes()
 {
-#define X(TM, TN, WR, NW, RL)                                                                  \
-    allow_lds(tab_kernel<OP_GEMM, TM, TN, WR, NW, RL>, tab_lds_bytes(TN, WR, NW, RL));       \
-    allow_lds(tab_kernel<OP_FWD, TM, TN, WR, NW, RL>, tab_lds_bytes(TN, WR, NW, RL));        \
-    allow_lds(tab_kernel<OP_BWD_DATA, TM, TN, WR, NW, RL>, tab_lds_bytes(TN, WR, NW, RL));   \
-    allow_lds(tab_kernel<OP_BWD_WEIGHT, TM, TN, WR, NW, RL>, tab_lds_bytes(TN, WR, NW, RL));
-    AMSIM_FOR_TAB_TILES(X)
-#undef X
+    for (hipError_t e : {tab_attributes<OP_GEMM>(), tab_attributes<OP_FWD>(), tab_attributes<OP_BWD_DATA>(),
+                         tab_attributes<OP_BWD_WEIGHT>()})
+        if (e != hipSuccess && g_attr_err == hipSuccess) g_attr_err = e;
 }
 
 int ensure_attributes()
@@ -1838,21 +747,6 @@ inline int decode_vec(const float *src, int64_t sb, int64_t sr, int64_t sc)
 {
     return sc == 1 && reinterpret_cast<uintptr_t>(src) % 16 == 0 && sr % 4 == 0 && sb % 4 == 0 ? 1 : 0;
 }
-
-template <typename F>
-void dispatch_tab_tile(const Tile &t, int rl, F &&f)
-{
-#define X(TM, TN, WR, NW, RL)                                                             \
-    if (t.tm == TM && t.tn == TN && t.wr == WR && t.nw == NW && rl == RL) {               \
-        f(std::integral_constant<int, TM>{}, std::integral_constant<int, TN>{},           \
-          std::integral_constant<int, WR>{}, std::integral_constant<int, NW>{},           \
-          std::integral_constant<int, RL>{});                                             \
-        return;                                                                           \
-    }
-    AMSIM_FOR_TAB_TILES(X)
-#undef X
-}
-
 
 // Workspace layout shared by the size queries and the launches:
 //   [transposed rows][bf16-path rows][flags][statistics][first operand][second operand][partials]
@@ -2076,14 +970,7 @@ int prep_rows(const uint32_t *lut, int m_bits, char *ws, const Plan &p, int n_a,
 template <int OP>
 int launch_tab(const Plan &p, const TabArgs &a, dim3 grid, hipStream_t st)
 {
-    auto run = [&](auto tm, auto tn, auto wr, auto nw, auto rl) {
-        constexpr int TM = decltype(tm)::value, TN = decltype(tn)::value, WR = decltype(wr)::value;
-        constexpr int NW = decltype(nw)::value, RL = decltype(rl)::value;
-        hipLaunchKernelGGL((tab_kernel<OP, TM, TN, WR, NW, RL>), grid, dim3(64 * NW), tab_lds_bytes(TN, WR, NW, RL),
-                           st, a);
-    };
-    dispatch_tab_tile(p.tile, p.rl, run);
-    return launch_status();
+    return tab_launch<OP>(p.tile, p.rl, a, grid, st) == hipSuccess ? AMSIM_OK : AMSIM_ERR_HIP;
 }
 
 TabArgs tab_args(const Plan &p, char *ws, const uint32_t *A, int64_t a_elems, const uint32_t *Bd, float *out, int R,
