@@ -33,7 +33,6 @@ namespace amsim_detail __attribute__((visibility("hidden"))) {
 // rebiased float.  The entry width is decided on the device by the table-preparation kernels
 // and read by the table kernel, which runs the matching specialisation.
 
-
 // Which operation the table kernel evaluates.  Every one is a sum over "taps": runs of
 // consecutive reduction steps j = 0 .. count-1 whose first-operand word sits at
 //   A[lane row base + ubase + j * ustride]
@@ -977,6 +976,27 @@ constexpr TabCand kWide11Cands[] = {{8, 4, 8, 8}, {4, 4, 8, 8}, {2, 4, 4, 4}, {1
     X(4, 4, 8, 8, 11) X(2, 4, 4, 4, 11) X(1, 4, 4, 4, 11)
 #define AMSIM_WIDE_TILES(X, RL)                                                                                \
     X(8, 4, 8, 8, RL) X(4, 8, 8, 8, RL) X(2, 8, 4, 4, RL) X(1, 8, 4, 4, RL) X(1, 4, 4, 4, RL)
+
+// Every candidate the chooser can return is instantiated (checked at compile time).
+constexpr bool tab_tile_listed(const TabCand &c, int rl)
+{
+#define X(TM, TN, WR, NW, RL) \
+    if (c.tm == TM && c.tn == TN && c.wr == WR && c.nw == NW && rl == RL) return true;
+    AMSIM_FOR_TAB_TILES(X)
+#undef X
+    return false;
+}
+template <size_t N>
+constexpr bool tab_cands_listed(const TabCand (&cands)[N], int rl_lo, int rl_hi)
+{
+    for (size_t i = 0; i < N; ++i)
+        for (int rl = rl_lo; rl <= rl_hi; ++rl)
+            if (!tab_tile_listed(cands[i], rl)) return false;
+    return true;
+}
+static_assert(tab_cands_listed(kTabCands, 7, 7) && tab_cands_listed(kWideCands, 8, 10) &&
+                  tab_cands_listed(kWide11Cands, 11, 11),
+              "a tile candidate is missing from AMSIM_FOR_TAB_TILES");
 
 // Per operation (defined in amsim_tab.hip, one instantiation per operation): raise the dynamic
 // LDS limit of every instantiated tile's kernel and check that none uses static LDS; launch the
