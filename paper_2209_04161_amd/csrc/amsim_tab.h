@@ -703,18 +703,22 @@ __device__ __forceinline__ void tab_body_dot(const TabArgs &a)
 
     // Staging pipeline: while slab s is computed, the table bytes of slab s + 1 are fetched (its
     // second-operand words `sbw` having arrived during slab s - 1) and the second-operand words
-    // of slab s + 2 are loaded into `sbw2`.  With 8-step slabs (4-wave workgroups) the words'
-    // latency would otherwise be exposed once per slab; 16-step slabs fetch both in slab s.
-    constexpr bool AHEAD2 = NW <= 4;
+    // of slab s + 2 are loaded into `sbw2`, so that the words' latency is not exposed once per
+    // slab (8-step slabs lose most, 16-step slabs ~1%).  The backward-data pass of 16-step slabs
+    // fetches both in slab s: its tap arithmetic leaves no registers for `sbw2`.
+    constexpr bool AHEAD2 = NW <= 4 || OP != OP_BWD_DATA;
     u32x4 sbw[2], sbw2[2];
     uint32_t srw[DC];
     float acc[TM][TN];
     init_acc(acc);
     // First-operand data of RS step pairs, as a ring: pair kp of a slab is in w[kp % RS]; while
-    // it is used, pair kp + 2 (of this slab, or the next slab's first two for the last two pairs)
-    // is loaded into w[(kp + 2) % RS].  A slab holds a multiple of RS pairs, so after a full slab
-    // the next slab's first two pairs sit in w[0], w[1].
+    // it is used, pair kp + LA (of this slab, or one of the next slab's first LA pairs for the
+    // last LA pairs) is loaded into w[(kp + LA) % RS].  A slab holds a multiple of RS pairs, so
+    // after a full slab the next slab's first LA pairs sit in w[0] .. w[LA - 1].
     constexpr int RS = (KS / 2) % 4 == 0 ? 4 : KS / 2;
+    // pairs loaded ahead: all of the ring but the pair in use, except in the backward-data pass,
+    // whose tap arithmetic leaves registers for one pair less (with three its kernel spills)
+    constexpr int LA = OP == OP_BWD_DATA ? RS - 2 : RS - 1;
     static_assert(RS >= 3 && (KS / 2) % RS == 0, "ring of step pairs");
     uint32_t w[RS][NA][TM];
     // The slab after (t, tp_, c): its tap, cursor and whether it is in this split's range (if not,
@@ -744,7 +748,7 @@ __device__ __forceinline__ void tab_body_dot(const TabArgs &a)
         dot_fetch_rows<DC>(srw, sbw, rres);
         dot_commit<DC>(sbw, srw, smem);
 #pragma unroll
-        for (int k = 0; k < 2; ++k) dot_load_pair<OP, TM>(w[k], av, cur, c0 + 2 * k);
+        for (int k = 0; k < LA; ++k) dot_load_pair<OP, TM>(w[k], av, cur, c0 + 2 * k);
         advance(cur, tap, c0, nxt, ntap, nc0, has_next);
         if (AHEAD2 && has_next) dot_fetch_b<DC>(sbw, nxt, nc0, a.Bd, a.Np, col0);
     }
@@ -775,10 +779,10 @@ __device__ __forceinline__ void tab_body_dot(const TabArgs &a)
 #pragma unroll
         for (int kp = 0; kp < KS / 2; ++kp) {
             if (kp >= npairs) break;
-            if (kp + 2 < KS / 2)
-                dot_load_pair<OP, TM>(w[(kp + 2) % RS], av, cur, c0 + 2 * kp + 4);
+            if (kp + LA < KS / 2)
+                dot_load_pair<OP, TM>(w[(kp + LA) % RS], av, cur, c0 + 2 * (kp + LA));
             else
-                dot_load_pair<OP, TM>(w[(kp + 2) % RS], av, nxt, nc0 + 2 * (kp + 2 - KS / 2));
+                dot_load_pair<OP, TM>(w[(kp + LA) % RS], av, nxt, nc0 + 2 * (kp + LA - KS / 2));
             const uint32_t(&a0)[TM] = w[kp % RS][0];
             const uint32_t(&a1)[TM] = w[kp % RS][1];
 #pragma unroll
@@ -818,9 +822,9 @@ __device__ __forceinline__ void tab_body_dot(const TabArgs &a)
                 }
             }
         }
-        if (live && npairs < KS / 2 && has_next) {  // a short slab: the next slab's first two pairs
+        if (live && npairs < KS / 2 && has_next) {  // a short slab: the next slab's first LA pairs
 #pragma unroll
-            for (int k = 0; k < 2; ++k) dot_load_pair<OP, TM>(w[k], av, nxt, nc0 + 2 * k);
+            for (int k = 0; k < LA; ++k) dot_load_pair<OP, TM>(w[k], av, nxt, nc0 + 2 * k);
         }
         if (has_next) dot_commit<DC>(sbw, srw, smem + NEXT);
         __syncthreads();
