@@ -129,7 +129,8 @@ int approx_gemm_direct(int mode, int m_bits, int64_t m, int64_t n, int64_t k, co
  * (TF "SAME" is an asymmetric pad), stride >= 1, no dilation or groups (none in the paper).
  * OH = (h + pad_top + pad_bottom - kh) / stride_h + 1, OW likewise; both must be >= 1.
  * All sizes must be >= 1 (pads >= 0).  AMSIM_ERR_UNSUPPORTED when a (padded) tensor reaches
- * 2^29 elements, a pad or kernel side reaches 65536, stride_h * stride_w exceeds 32, a channel
+ * 2^29 elements, the zero-padded x or dy stored as 12 bytes per pixel and channel pair reaches
+ * 2^31 bytes, a pad or kernel side reaches 65536, stride_h * stride_w exceeds 32, a channel
  * count exceeds 1048560, or w or OW reaches 4096. */
 typedef struct amsim_conv2d {
     int n, h, w, c_in, c_out, kh, kw, stride_h, stride_w, pad_top, pad_bottom, pad_left, pad_right;

@@ -39,13 +39,15 @@ using namespace amsim_detail;
 
 // ------------------------------------------------------------------ pre-pass kernels -----
 
-// dst[(b * rows + r) * dld + c] = decode(src[b * sb + r * sr + c * sc]) for r < rows, c < cols;
-// padding columns c in [cols, dld) are written as decoded +0.  dld is a multiple of 4 and
+// dst[(b * rows + r) * dld + c] = decode(src[b * sb + r * sr + c * sc]) for r < vrows, c < cols;
+// padding columns c in [cols, dld) and padding rows r in [vrows, rows) (whose source is not read)
+// are written as decoded +0.  dld is a multiple of 4 and
 // batches * rows * dld / 4 < 2^31: each thread takes groups of 4 columns (16-byte stores), two
 // groups per iteration so that 8 loads are in flight.  vec: sc == 1 and every row start is
 // 16-byte aligned, so a full group is one 16-byte load.
 __global__ __launch_bounds__(256) void decode_kernel(const float *__restrict__ src, int64_t sb, int64_t sr, int64_t sc,
-                                                     int batches, int rows, int cols, uint32_t *__restrict__ dst,
+                                                     int batches, int rows, int vrows, int cols,
+                                                     uint32_t *__restrict__ dst,
                                                      int dld, int m, int shift, uint32_t zidx,
                                                      uint32_t *__restrict__ stats, int vec)
 {
@@ -65,7 +67,8 @@ __global__ __launch_bounds__(256) void decode_kernel(const float *__restrict__ s
             c[h] = (q - row[h] * qpr) * 4u;
             const uint32_t b = row[h] / uint32_t(rows), r = row[h] - b * uint32_t(rows);
             const float *base = src + int64_t(b) * sb + int64_t(r) * sr;
-            if (vec && live[h] && c[h] + 4u <= uint32_t(cols)) {
+            const uint32_t ncols = r < uint32_t(vrows) ? uint32_t(cols) : 0u;
+            if (vec && live[h] && c[h] + 4u <= ncols) {
                 const u32x4 q4 = *reinterpret_cast<const u32x4 *>(base + c[h]);
 #pragma unroll
                 for (int e = 0; e < 4; ++e) w[h][e] = q4[e];
@@ -73,7 +76,7 @@ __global__ __launch_bounds__(256) void decode_kernel(const float *__restrict__ s
 #pragma unroll
                 for (int e = 0; e < 4; ++e) {
                     const uint32_t ce = c[h] + uint32_t(e);
-                    w[h][e] = (live[h] && ce < uint32_t(cols)) ? __float_as_uint(base[int64_t(ce) * sc]) : 0u;
+                    w[h][e] = (live[h] && ce < ncols) ? __float_as_uint(base[int64_t(ce) * sc]) : 0u;
                 }
             }
         }
@@ -188,6 +191,57 @@ __global__ __launch_bounds__(256) void decode_pad_nhcw_kernel(const float *__res
                     drow[xo * 3 + 2] = w1 & 0xFFFFu;
                 }
             }
+        }
+    }
+    store_stats(st, stats, blockIdx.x);
+}
+
+// Forward pass with few input channels: x unfolded along w into the step-pair records of a
+// virtual input x'[n][y][ow][kw * c + ci] = x[n][y - top][ow * sw + kw - left][ci] (zero outside
+// x), laid out [n][hp][cp'][ow_n] (cp' = ceil(kw_n * c / 2)) like decode_pad_nhcw_kernel's
+// records; an odd kw_n * c leaves a padding channel, written as -0.  The forward pass of a
+// kh x kw kernel over x is then a sum over (kh, kw * c) steps whose records lie at one stride
+// (the host's unfolded_shape).  A workgroup takes one padded image row at a time and stages the
+// decoded source row (w * c <= kNhcwTile words) in LDS.
+__global__ __launch_bounds__(256) void decode_unfold_w_kernel(const float *__restrict__ src, int n, int h, int w, int c,
+                                                              int top, int left, int hp, int kw_n, int sw, int ow_n,
+                                                              uint32_t *__restrict__ dst, int m, int shift,
+                                                              uint32_t *__restrict__ stats)
+{
+    __shared__ uint32_t tile[kNhcwTile];
+    const int cu = kw_n * c, cp = (cu + 1) / 2;
+    ExpStats st;
+    for (int rr = blockIdx.x; rr < n * hp; rr += gridDim.x) {
+        const int b = rr / hp, y = rr - b * hp, ih = y - top;
+        uint32_t *dimg = dst + int64_t(rr) * cp * ow_n * 3;
+        if (unsigned(ih) >= unsigned(h)) {  // a padding row (uniform over the workgroup)
+            for (int i = threadIdx.x; i < cp * ow_n * 3; i += 256) dimg[i] = 0u;
+            continue;
+        }
+        const float *srow = src + (int64_t(b) * h + ih) * w * c;
+        __syncthreads();  // the previous row's record stores have read the tile
+        for (int e = threadIdx.x; e < w * c; e += 256) {
+            const uint32_t v = __float_as_uint(srow[e]);
+            st.add(v);
+            tile[e] = amsim_decode(v, m, shift, 0u);
+        }
+        __syncthreads();
+        for (int i = threadIdx.x; i < cp * ow_n; i += 256) {  // record (q, xo) is record i of the row
+            const int q = i / ow_n, xo = i - q * ow_n;
+            uint32_t wd[2] = {0u, 0u};
+#pragma unroll
+            for (int t = 0; t < 2; ++t) {
+                const int j = 2 * q + t;  // = kw * c + ci
+                const int k = j / c, ix = xo * sw + k - left;
+                if (j >= cu)
+                    wd[t] = 0x80000000u;  // the padding channel: a decoded -0
+                else if (unsigned(ix) < unsigned(w))
+                    wd[t] = tile[ix * c + (j - k * c)];
+            }
+            uint32_t *d = dimg + int64_t(i) * 3;
+            d[0] = wd[0] & 0xFFFFu;
+            d[1] = (wd[0] >> 16) | (wd[1] & 0xFFFF0000u);
+            d[2] = wd[1] & 0xFFFFu;
         }
     }
     store_stats(st, stats, blockIdx.x);
@@ -760,6 +814,7 @@ struct Plan {
     int chunks_per_split;   // 8-step reduction chunks per split
     int64_t out_elems;      // elements of the result (partial sums hold splits of them)
     int Hp, Wp, OHp, OWp, pad_oh, pad_ow;
+    bool unfold_w;          // forward pass over x unfolded along w (decode_unfold_w_kernel)
 };
 
 // Split of a reduction of q chunks (8 steps each).
@@ -833,6 +888,11 @@ int check_conv(const amsim_conv2d *d)
     const int64_t yp = int64_t(d->n) * (oh + 2 * d->kh + 2) * (ow + 2 * d->kw + 2) * d->c_out;
     const int64_t w = int64_t(d->kh) * d->kw * (d->c_in + 16) * (d->c_out + 16);
     const int64_t y = int64_t(d->n) * oh * ow * (d->c_out + 16);
+    // the step-pair records of zero-padded x and dy (12 bytes per pixel and channel pair) stay
+    // below 2^31 bytes: the table kernels address them with 32-bit byte offsets
+    const int64_t xr = int64_t(d->n) * hp * wp * ((d->c_in + 1) / 2) * 12;
+    const int64_t yr = int64_t(d->n) * (oh + 2 * d->kh + 2) * (ow + 2 * d->kw + 2) * ((d->c_out + 1) / 2) * 12;
+    if (xr >= (lim << 2) || yr >= (lim << 2)) return AMSIM_ERR_UNSUPPORTED;
     if (xp >= lim || yp >= lim || w >= lim || y >= lim || d->pad_top >= 65536 || d->pad_bottom >= 65536 ||
         d->pad_left >= 65536 || d->pad_right >= 65536 || d->kh >= 65536 || d->kw >= 65536 ||
         int64_t(d->stride_h) * d->stride_w > 32 || d->c_in > 65535 * 16 || d->c_out > 65535 * 16 ||
@@ -869,6 +929,38 @@ int64_t bwd_data_rows(const ConvShape &s)
     return int64_t(s.n) * ceil_div(s.h, s.sh) * ceil_div(s.w, s.sw);  // largest phase
 }
 
+// The forward pass unfolds x along w (decode_unfold_w_kernel) when its taps are shorter than
+// a slab of the widest tiles (c < 16 steps per (kh, kw) tap), the kernel is wider than one
+// column, a source row fits the decode's LDS tile and the unfolded records stay below 2^31 bytes.
+bool fwd_unfolds(const ConvShape &s, int hp)
+{
+    if (s.ci >= 16 || s.kw < 2 || int64_t(s.w) * s.ci > kNhcwTile) return false;
+    const int64_t bytes = int64_t(s.n) * hp * s.ow * ((int64_t(s.kw) * s.ci + 1) / 2) * 12;
+    return bytes < (int64_t(1) << 31);
+}
+
+// Channels of the unfolded x, kw * c, rounded up to whole step pairs.
+inline int unfolded_channels(const ConvShape &s) { return (s.kw * s.ci + 1) / 2 * 2; }
+
+// The forward pass over the unfolded x as one tap: step kh * cu + j (cu = unfolded_channels) is
+// channel j of image row oh * sh + kh, whose records follow those of row oh * sh + kh - 1 with the
+// same stride (the rows' record blocks are cu / 2 records of ow apart), so the kernel sees a
+// 1 x 1 "kernel" with kh * cu channels over a width-ow input; the table kernel's row records keep
+// the real layout through TabArgs::rec_c = cu.  The output shape is unchanged.  A channel
+// j >= kw * c of a row is padding: -0 in the records and +0 in the decoded weights, a -0 product
+// that leaves every sum, and the sign of a zero sum, as it is.
+ConvShape unfolded_shape(const ConvShape &s)
+{
+    ConvShape v = s;
+    v.w = s.ow;
+    v.ci = s.kh * unfolded_channels(s);
+    v.kh = 1;
+    v.kw = 1;
+    v.sw = 1;
+    v.pl = 0;
+    return v;
+}
+
 Plan plan_conv(const amsim_conv2d *d, int pass, int m_bits)
 {
     const ConvShape s = shape_of(d);
@@ -879,16 +971,20 @@ Plan plan_conv(const amsim_conv2d *d, int pass, int m_bits)
     p.Hp = d->h + d->pad_top + d->pad_bottom;
     p.Wp = d->w + d->pad_left + d->pad_right;
     if (pass == AMSIM_CONV_FWD) {
-        const int64_t q = int64_t(s.kh) * s.kw * ceil_div(s.ci, 8);
+        p.unfold_w = fwd_unfolds(s, p.Hp);
+        const ConvShape v = p.unfold_w ? unfolded_shape(s) : s;
+        const int rec_c = p.unfold_w ? unfolded_channels(s) : s.ci;  // channels per record row block
+        if (p.unfold_w) p.Wp = s.ow;  // the unfolded x has no w border
+        const int64_t q = int64_t(v.kh) * v.kw * ceil_div(v.ci, 8);
         p.tile = choose_tab_tile(npix_out, s.co, q, 4, true, p.rl, 8, 1);
         plan_tab_split(p, q);
         p.b_ld = round_up(s.co, tab_cols(p.tile));
-        p.a_elems = int64_t(s.n) * p.Hp * p.Wp * ((s.ci + 1) / 2) * 3;  // zero-bordered x as step-pair records
+        p.a_elems = int64_t(s.n) * p.Hp * p.Wp * ((rec_c + 1) / 2) * 3;  // zero-bordered x as step-pair records
         p.out_elems = npix_out * s.co;
         p.off_a = o;
         o += align_up(size_t(p.a_elems) * 4);
-        p.off_b = o;  // decoded w [kh*kw*ci][COp]
-        o += align_up(size_t(s.kh) * s.kw * s.ci * p.b_ld * 4);
+        p.off_b = o;  // decoded w [kh*kw*ci][COp] (unfolded: [kh][cu][COp])
+        o += align_up(size_t(v.kh) * v.kw * v.ci * p.b_ld * 4);
     } else if (pass == AMSIM_CONV_BWD_DATA) {
         const int64_t rows = bwd_data_rows(s);
         const int64_t q = ceil_div(s.kh, s.sh) * ceil_div(s.kw, s.sw) * ceil_div(s.co, 8);  // largest phase
@@ -1111,8 +1207,8 @@ int approx_gemm(int trans_a, int trans_b, int64_t m, int64_t n, int64_t k, const
     const int grid_b = decode_grid(k * p.b_ld);
     hipLaunchKernelGGL(decode_t_kernel, grid_dt, dim3(256), 0, st, A, a_sr, a_sc, int(m), int(k), nullptr,
                        int(p.a_ld), m_bits, shift_first(m_bits), 0u, stats_a(ws, p), Ad);
-    hipLaunchKernelGGL(decode_kernel, dim3(grid_b), dim3(256), 0, st, B, int64_t(0), b_sr, b_sc, 1, int(k), int(n), Bd,
-                       int(p.b_ld), m_bits, shift_second(m_bits), zidx_second(p), stats_b(ws, p),
+    hipLaunchKernelGGL(decode_kernel, dim3(grid_b), dim3(256), 0, st, B, int64_t(0), b_sr, b_sc, 1, int(k), int(k),
+                       int(n), Bd, int(p.b_ld), m_bits, shift_second(m_bits), zidx_second(p), stats_b(ws, p),
                        decode_vec(B, 0, b_sr, b_sc));
     if (launch_status() != AMSIM_OK) return AMSIM_ERR_HIP;
     if (prep_rows(lut, m_bits, ws, p, int(grid_dt.x * grid_dt.y), grid_b, st) != AMSIM_OK) return AMSIM_ERR_HIP;
@@ -1192,20 +1288,29 @@ int approx_conv2d_fwd(const amsim_conv2d *desc, const float *x, const float *w, 
     char *ws = static_cast<char *>(workspace);
     uint32_t *Xd = reinterpret_cast<uint32_t *>(ws + p.off_a);
     uint32_t *Wd = reinterpret_cast<uint32_t *>(ws + p.off_b);
-    const int n_a = decode_nhcw(x, s.n, s.h, s.w, s.ci, s.pt, s.pl, p.Hp, p.Wp, Xd, m_bits, shift_first(m_bits),
-                                stats_a(ws, p), st);
-    const int kk = s.kh * s.kw * s.ci;
-    const int n_b = decode_grid(int64_t(kk) * p.b_ld);
-    hipLaunchKernelGGL(decode_kernel, dim3(n_b), dim3(256), 0, st, w, int64_t(0), int64_t(s.co), int64_t(1), 1, kk,
-                       s.co, Wd, int(p.b_ld), m_bits, shift_second(m_bits), zidx_second(p), stats_b(ws, p),
-                       decode_vec(w, 0, s.co, 1));
+    int n_a;
+    if (p.unfold_w) {
+        n_a = int(std::min<int64_t>(int64_t(s.n) * p.Hp, kStatSlots));  // one padded image row at a time
+        hipLaunchKernelGGL(decode_unfold_w_kernel, dim3(n_a), dim3(256), 0, st, x, s.n, s.h, s.w, s.ci, s.pt, s.pl,
+                           p.Hp, s.kw, s.sw, s.ow, Xd, m_bits, shift_first(m_bits), stats_a(ws, p));
+    } else {
+        n_a = decode_nhcw(x, s.n, s.h, s.w, s.ci, s.pt, s.pl, p.Hp, p.Wp, Xd, m_bits, shift_first(m_bits),
+                          stats_a(ws, p), st);
+    }
+    // w [kh][kw * ci][co] as batches kh of kw * ci rows (unfolded: padded to cu rows with +0)
+    const int kwc = s.kw * s.ci, wrows = p.unfold_w ? unfolded_channels(s) : kwc;
+    const int n_b = decode_grid(int64_t(s.kh) * wrows * p.b_ld);
+    hipLaunchKernelGGL(decode_kernel, dim3(n_b), dim3(256), 0, st, w, int64_t(kwc) * s.co, int64_t(s.co), int64_t(1),
+                       s.kh, wrows, kwc, s.co, Wd, int(p.b_ld), m_bits, shift_second(m_bits), zidx_second(p),
+                       stats_b(ws, p), decode_vec(w, int64_t(kwc) * s.co, s.co, 1));
     if (launch_status() != AMSIM_OK) return AMSIM_ERR_HIP;
     if (prep_rows(lut, m_bits, ws, p, n_a, n_b, st) != AMSIM_OK) return AMSIM_ERR_HIP;
     const Tile t = p.tile;
     const int64_t rows = int64_t(s.n) * s.oh * s.ow;
     float *out = p.splits > 1 ? reinterpret_cast<float *>(ws + p.off_part) : y;
     TabArgs a = tab_args(p, ws, Xd, p.a_elems, Wd, out, int(rows), s.co);
-    a.s = s;
+    a.s = p.unfold_w ? unfolded_shape(s) : s;
+    a.rec_c = p.unfold_w ? unfolded_channels(s) : s.ci;
     dim3 grid(unsigned(ceil_div(rows, int64_t(64) * t.wr * t.tm)), unsigned(p.b_ld / tab_cols(t)),
               unsigned(p.splits));
     {
@@ -1233,7 +1338,7 @@ int approx_conv2d_bwd_data(const amsim_conv2d *desc, const float *dy, const floa
     // w[kh][kw][ci][co] -> Wt[kh][kw][co][ci]: batches (kh,kw), rows co, cols ci
     const int n_b = decode_grid(int64_t(s.kh) * s.kw * s.co * p.b_ld);
     hipLaunchKernelGGL(decode_kernel, dim3(n_b), dim3(256), 0, st, w, int64_t(s.ci) * s.co, int64_t(1), int64_t(s.co),
-                       s.kh * s.kw, s.co, s.ci, Wtd, int(p.b_ld), m_bits, shift_second(m_bits), zidx_second(p),
+                       s.kh * s.kw, s.co, s.co, s.ci, Wtd, int(p.b_ld), m_bits, shift_second(m_bits), zidx_second(p),
                        stats_b(ws, p), 0);
     if (launch_status() != AMSIM_OK) return AMSIM_ERR_HIP;
     if (prep_rows(lut, m_bits, ws, p, n_a, n_b, st) != AMSIM_OK) return AMSIM_ERR_HIP;
@@ -1270,8 +1375,8 @@ int approx_conv2d_bwd_weight(const amsim_conv2d *desc, const float *x, const flo
     const int64_t npo = int64_t(s.n) * s.oh * s.ow;
     const int n_b = decode_grid(npo * p.b_ld);
     hipLaunchKernelGGL(decode_kernel, dim3(n_b), dim3(256), 0, st, dy, int64_t(0), int64_t(s.co), int64_t(1), 1,
-                       int(npo), s.co, Dyd, int(p.b_ld), m_bits, shift_second(m_bits), zidx_second(p), stats_b(ws, p),
-                       decode_vec(dy, 0, s.co, 1));
+                       int(npo), int(npo), s.co, Dyd, int(p.b_ld), m_bits, shift_second(m_bits), zidx_second(p),
+                       stats_b(ws, p), decode_vec(dy, 0, s.co, 1));
     if (launch_status() != AMSIM_OK) return AMSIM_ERR_HIP;
     if (prep_rows(lut, m_bits, ws, p, n_a, n_b, st) != AMSIM_OK) return AMSIM_ERR_HIP;
     const Tile t = p.tile;

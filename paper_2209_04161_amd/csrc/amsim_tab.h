@@ -68,6 +68,7 @@ struct TabArgs {
     int Mp, K;           // GEMM
     ConvShape s;
     int Hp, Wp;          // zero-padded x (FWD, BWD_WEIGHT)
+    int rec_c;           // FWD: channels of x's record layout [n][hp][rec_c / 2][wp] (s.ci unless unfolded)
     int OHp, OWp, pad_oh, pad_ow;  // zero-padded dy (BWD_DATA)
     int tx, ty, tz;      // this workgroup's tile (row block, column block, phase/split); set on entry
 };
@@ -217,7 +218,7 @@ __device__ __forceinline__ int tab_row_rec(const TabArgs &a, int row)
         return row;
     } else if constexpr (OP == OP_FWD) {
         const int ow = row % s.ow, oh = (row / s.ow) % s.oh, n = row / (s.ow * s.oh);
-        return (n * a.Hp + oh * s.sh) * ((s.ci + 1) / 2) * a.Wp + ow * s.sw;  // records [n][hp][ci/2][wp]
+        return (n * a.Hp + oh * s.sh) * ((a.rec_c + 1) / 2) * a.Wp + ow * s.sw;  // records [n][hp][ci/2][wp]
     } else if constexpr (OP == OP_BWD_DATA) {
         const int ph = tab_phase(a) / s.sw, pw = tab_phase(a) % s.sw;
         int hq_n, wq_n;
@@ -277,7 +278,7 @@ __device__ __forceinline__ TabTap tab_tap_raw(const TabArgs &a, int tap)
         t.ubase = kh * s.ci * a.Wp + kw;
         t.ustride = a.Wp;
         t.bbase = tap * s.ci;
-        t.pbase = kh * ((s.ci + 1) / 2) * a.Wp + kw;
+        t.pbase = kh * ((a.rec_c + 1) / 2) * a.Wp + kw;
     } else if constexpr (OP == OP_BWD_DATA) {
         const int ph = tab_phase(a) / s.sw, pw = tab_phase(a) % s.sw;
         const int kh0 = (ph + s.pt) % s.sh, kw0 = (pw + s.pl) % s.sw;

@@ -134,6 +134,12 @@ def test_workspace_size_queries(L):
     assert binding.amsim_conv2d_workspace_size(wide, 0, 7) > 0
     with pytest.raises(binding.AmsimError):
         binding.amsim_conv2d_workspace_size(dict(wide, w=4096), 0, 7)
+    # single-channel x: its 12-byte step-pair records (one per pixel) must stay below 2^31 bytes,
+    # though the tensor itself is under 2^29 elements
+    one = dict(wide, n=16, h=2048, w=2047, stride_h=4, stride_w=4)
+    assert binding.amsim_conv2d_workspace_size(one, 0, 7) > 16 * 2048 * 2047 * 12
+    with pytest.raises(binding.AmsimError):
+        binding.amsim_conv2d_workspace_size(dict(one, n=90), 0, 7)   # 4.5 GB of records
     with pytest.raises(binding.AmsimError):
         binding.amsim_gemm_workspace_size(0, 0, 4, 4, 4, 12)
 
