@@ -247,6 +247,32 @@ __global__ __launch_bounds__(256) void decode_unfold_w_kernel(const float *__res
     store_stats(st, stats, blockIdx.x);
 }
 
+// Backward-data pass with few input channels, second half: the gradient of the w-unfolded input
+// (see decode_unfold_w_kernel), dxu[n][ih][ow][kw * c + ci], folded back onto x's pixels:
+// dx[n][ih][iw][ci] = the sum, in ascending kw, of dxu[n][ih][ow][kw * c + ci] over the (kw, ow)
+// with ow * sw + kw - left = iw, 0 <= ow < ow_n; -0 (the empty sum) where there is none.
+__global__ __launch_bounds__(256) void fold_w_kernel(const float *__restrict__ dxu, int n, int h, int w, int c,
+                                                     int kw_n, int sw, int left, int ow_n, float *__restrict__ dx)
+{
+    const int64_t total = int64_t(n) * h * w * c;
+    const int cu = kw_n * c;
+    for (int64_t i = int64_t(blockIdx.x) * blockDim.x + threadIdx.x; i < total; i += int64_t(gridDim.x) * blockDim.x) {
+        const int ci = int(i % c);
+        const int64_t t = i / c;
+        const int iw = int(t % w);
+        const int64_t row = t / w;  // n * h + ih
+        float acc = -0.0f;
+        for (int k = 0; k < kw_n; ++k) {
+            const int num = iw + left - k;
+            if (num < 0) break;  // and for every larger k
+            const int ow = num / sw;
+            if (ow * sw != num || ow >= ow_n) continue;
+            acc += dxu[(row * ow_n + ow) * cu + k * c + ci];
+        }
+        dx[i] = acc;
+    }
+}
+
 // Tiled transpose-decode for the GEMM first operand: src is `rows x cols` with strides
 // (sr, sc); dst[c * dld + r] = decode(src(r, c)), rows padded to dld with decoded +0.
 // Pair records (records != null): records[(c / 2) * dld + r] = {index field of (r, c), head of
@@ -814,7 +840,8 @@ struct Plan {
     int chunks_per_split;   // 8-step reduction chunks per split
     int64_t out_elems;      // elements of the result (partial sums hold splits of them)
     int Hp, Wp, OHp, OWp, pad_oh, pad_ow;
-    bool unfold_w;          // forward pass over x unfolded along w (decode_unfold_w_kernel)
+    bool unfold_w;          // forward / backward-data pass over x unfolded along w
+    size_t off_unf;         // backward data, unfolded: the unfolded input's gradient
 };
 
 // Split of a reduction of q chunks (8 steps each).
@@ -961,8 +988,40 @@ ConvShape unfolded_shape(const ConvShape &s)
     return v;
 }
 
+// The backward-data pass unfolds along w in the same way when x has few channels (c < 8, which
+// leaves most of an 8- or 4-column tile empty): it computes the gradient of the unfolded input,
+// kw * c columns, as the backward-data pass of the virtual kh x 1 convolution below, then folds
+// it back onto x (fold_w_kernel).  Not when the virtual pass or the unfolded gradient would
+// exceed the limits.
+amsim_conv2d unfolded_desc(const amsim_conv2d *d)
+{
+    amsim_conv2d v = *d;
+    const int ow = (d->w + d->pad_left + d->pad_right - d->kw) / d->stride_w + 1;
+    v.w = ow;
+    v.c_in = d->kw * d->c_in;
+    v.kw = 1;
+    v.stride_w = 1;
+    v.pad_left = v.pad_right = 0;
+    return v;
+}
+
+bool bwd_data_unfolds(const amsim_conv2d *d)
+{
+    if (d->c_in >= 8 || d->kw < 2) return false;
+    const amsim_conv2d v = unfolded_desc(d);
+    return check_conv(&v) == AMSIM_OK && int64_t(v.n) * v.h * v.w * v.c_in < (int64_t(1) << 29);
+}
+
 Plan plan_conv(const amsim_conv2d *d, int pass, int m_bits)
 {
+    if (pass == AMSIM_CONV_BWD_DATA && bwd_data_unfolds(d)) {
+        const amsim_conv2d v = unfolded_desc(d);
+        Plan p = plan_conv(&v, pass, m_bits);  // the virtual pass (kw = 1: it does not unfold again)
+        p.unfold_w = true;
+        p.off_unf = align_up(p.total);  // the unfolded gradient [n][h][ow][kw * c]
+        p.total = p.off_unf + align_up(size_t(v.n) * v.h * v.w * v.c_in * 4);
+        return p;
+    }
     const ConvShape s = shape_of(d);
     Plan p{};
     p.rl = row_log(m_bits);
@@ -1322,13 +1381,11 @@ int approx_conv2d_fwd(const amsim_conv2d *desc, const float *x, const float *w, 
     return launch_status();
 }
 
-int approx_conv2d_bwd_data(const amsim_conv2d *desc, const float *dy, const float *w, float *dx,
-                           const uint32_t *lut, int m_bits, void *workspace, size_t workspace_bytes, void *stream)
+// The backward-data pass of `desc` (the caller's, or the virtual unfolded one) under plan p, into dx.
+static int bwd_data_run(const amsim_conv2d *desc, const Plan &p, const float *dy, const float *w, float *dx,
+                        const uint32_t *lut, int m_bits, void *workspace, hipStream_t st)
 {
-    Plan p;
-    int rc = conv_common(desc, AMSIM_CONV_BWD_DATA, dy, w, dx, lut, m_bits, workspace, workspace_bytes, &p);
-    if (rc != AMSIM_OK) return rc;
-    hipStream_t st = static_cast<hipStream_t>(stream);
+    int rc;
     const ConvShape s = shape_of(desc);
     char *ws = static_cast<char *>(workspace);
     uint32_t *Dyd = reinterpret_cast<uint32_t *>(ws + p.off_a);
@@ -1356,6 +1413,25 @@ int approx_conv2d_bwd_data(const amsim_conv2d *desc, const float *dy, const floa
     if (rc != AMSIM_OK || p.splits == 1) return rc;
     launch_reduce(reinterpret_cast<const float *>(ws + p.off_part), p.splits, s.n * s.h * s.w, s.ci, dx, int64_t(s.ci),
                   st);
+    return launch_status();
+}
+
+int approx_conv2d_bwd_data(const amsim_conv2d *desc, const float *dy, const float *w, float *dx,
+                           const uint32_t *lut, int m_bits, void *workspace, size_t workspace_bytes, void *stream)
+{
+    Plan p;
+    int rc = conv_common(desc, AMSIM_CONV_BWD_DATA, dy, w, dx, lut, m_bits, workspace, workspace_bytes, &p);
+    if (rc != AMSIM_OK) return rc;
+    hipStream_t st = static_cast<hipStream_t>(stream);
+    if (!p.unfold_w) return bwd_data_run(desc, p, dy, w, dx, lut, m_bits, workspace, st);
+    // the unfolded input's gradient, then folded back onto x's pixels
+    const amsim_conv2d v = unfolded_desc(desc);
+    float *dxu = reinterpret_cast<float *>(static_cast<char *>(workspace) + p.off_unf);
+    rc = bwd_data_run(&v, p, dy, w, dxu, lut, m_bits, workspace, st);
+    if (rc != AMSIM_OK) return rc;
+    const int64_t total = int64_t(desc->n) * desc->h * desc->w * desc->c_in;
+    hipLaunchKernelGGL(fold_w_kernel, dim3(grid_for(total)), dim3(256), 0, st, dxu, desc->n, desc->h, desc->w,
+                       desc->c_in, desc->kw, desc->stride_w, desc->pad_left, v.w, dx);
     return launch_status();
 }
 

@@ -178,6 +178,20 @@ def test_conv_zero_sums_keep_their_sign(B):
     ref, S = oracle.conv2d_bwd_data(oracle.MITCHELL, m, p, dy, w)
     check(dx, ref, S, "bwd_data")
 
+    # few input channels and a 1 x 3 kernel: the pass runs unfolded along w and folds the sums
+    # back (no padded taps either way)
+    p = W.conv_desc(2, 5, 9, 3, 6, 1, 3, 1, 0)
+    dy = W.normal((2, 5, 7, 6), 1.0, 77)
+    w = W.normal((1, 3, 3, 6), 1.0, 78)
+    dy[1] = 0.0
+    dy[1, :, :2, :] = -0.0
+    w[0, :, 0, :] = -np.abs(w[0, :, 0, :])
+    w[0, :, 1, :] = np.abs(w[0, :, 1, :])
+    w[0, 1:, 2, :] = -0.0
+    dx = host(B.approx_conv2d_bwd_data(p, cuda(dy), cuda(w), lut, m))
+    ref, S = oracle.conv2d_bwd_data(oracle.MITCHELL, m, p, dy, w)
+    check(dx, ref, S, "bwd_data unfolded")
+
     p = W.conv_desc(2, 6, 9, 5, 11, 3, 3, 1, 0)
     x = W.normal((2, 6, 9, 5), 1.0, 75)
     dy = W.normal((2, 4, 7, 11), 1.0, 76)
