@@ -39,6 +39,21 @@ using namespace amsim_detail;
 
 // ------------------------------------------------------------------ pre-pass kernels -----
 
+// r / d for 0 <= r and 1 <= d, given inv_d = 1.0f / d.  Below 2^24 (small, uniform) the float
+// quotient is within one of the true one, which a remainder test corrects; above, the integer
+// division.
+__device__ __forceinline__ int div_small(int r, int d, float inv_d, bool small)
+{
+    if (!small) return r / d;
+    int q = int(float(r) * inv_d);
+    const int rem = r - q * d;
+    if (rem < 0)
+        --q;
+    else if (rem >= d)
+        ++q;
+    return q;
+}
+
 // dst[(b * rows + r) * dld + c] = decode(src[b * sb + r * sr + c * sc]) for r < vrows, c < cols;
 // padding columns c in [cols, dld) and padding rows r in [vrows, rows) (whose source is not read)
 // are written as decoded +0.  dld is a multiple of 4 and
@@ -135,7 +150,7 @@ __global__ __launch_bounds__(256) void decode_pad_kernel(const float *__restrict
 // exists, zeros elsewhere; a channel past the end is a decoded +0.  A workgroup takes one padded
 // image row at a time: the source row (w pixels x cc channels at a time, cc even, contiguous
 // loads) goes through LDS as [channel][x] (row pitch w | 1, odd, so the transposing stores do not
-// collide in banks), then each wave writes whole record rows.
+// collide in banks), then the workgroup writes the chunk's records, one per thread.
 constexpr int kNhcwTile = 8192;  // words of the LDS tile: cc * (w | 1) <= kNhcwTile
 
 __global__ __launch_bounds__(256) void decode_pad_nhcw_kernel(const float *__restrict__ src, int n, int h, int w, int c,
@@ -145,7 +160,6 @@ __global__ __launch_bounds__(256) void decode_pad_nhcw_kernel(const float *__res
 {
     __shared__ uint32_t tile[kNhcwTile];
     const int ws = w | 1, cp = (c + 1) / 2;
-    const int wave = int(threadIdx.x) >> 6, lane = int(threadIdx.x) & 63;
     ExpStats st;
     for (int rr = blockIdx.x; rr < n * hp; rr += gridDim.x) {
         const int b = rr / hp, y = rr - b * hp, ih = y - top;
@@ -176,20 +190,23 @@ __global__ __launch_bounds__(256) void decode_pad_nhcw_kernel(const float *__res
                 }
             }
             __syncthreads();
-            for (int q = wave; q < (ccn + 1) / 2; q += 4) {
-                uint32_t *drow = dimg + (int64_t(c0 / 2 + q) * wp) * 3;
-                const bool odd = 2 * q + 1 < ccn;
-                for (int xo = lane; xo < wp; xo += 64) {
-                    const int ix = xo - left;
-                    uint32_t w0 = 0u, w1 = 0u;
-                    if (unsigned(ix) < unsigned(w)) {
-                        w0 = tile[(2 * q) * ws + ix];
-                        w1 = odd ? tile[(2 * q + 1) * ws + ix] : 0u;
-                    }
-                    drow[xo * 3 + 0] = w0 & 0xFFFFu;
-                    drow[xo * 3 + 1] = (w0 >> 16) | (w1 & 0xFFFF0000u);
-                    drow[xo * 3 + 2] = w1 & 0xFFFFu;
+            // the chunk's records are one contiguous block [q][x]: consecutive threads write
+            // consecutive records
+            const int qn = (ccn + 1) / 2;
+            uint32_t *dblk = dimg + int64_t(c0 / 2) * wp * 3;
+            const float inv_wp = 1.0f / float(wp);
+            const bool small = qn * wp < (1 << 24);
+            for (int rec = threadIdx.x; rec < qn * wp; rec += 256) {
+                const int q = div_small(rec, wp, inv_wp, small), ix = rec - q * wp - left;
+                uint32_t w0 = 0u, w1 = 0u;
+                if (unsigned(ix) < unsigned(w)) {
+                    w0 = tile[(2 * q) * ws + ix];
+                    w1 = 2 * q + 1 < ccn ? tile[(2 * q + 1) * ws + ix] : 0u;
                 }
+                uint32_t *d = dblk + int64_t(rec) * 3;
+                d[0] = w0 & 0xFFFFu;
+                d[1] = (w0 >> 16) | (w1 & 0xFFFF0000u);
+                d[2] = w1 & 0xFFFFu;
             }
         }
     }
@@ -226,8 +243,10 @@ __global__ __launch_bounds__(256) void decode_unfold_w_kernel(const float *__res
             tile[e] = amsim_decode(v, m, shift, 0u);
         }
         __syncthreads();
-        for (int i = threadIdx.x; i < cp * ow_n; i += 256) {  // record (q, xo) is record i of the row
-            const int q = i / ow_n, xo = i - q * ow_n;
+        const float inv_own = 1.0f / float(ow_n);
+        const bool small = cp * ow_n < (1 << 24);
+        for (int rec = threadIdx.x; rec < cp * ow_n; rec += 256) {  // record (q, xo), consecutive per thread
+            const int q = div_small(rec, ow_n, inv_own, small), xo = rec - q * ow_n;
             uint32_t wd[2] = {0u, 0u};
 #pragma unroll
             for (int t = 0; t < 2; ++t) {
@@ -238,7 +257,7 @@ __global__ __launch_bounds__(256) void decode_unfold_w_kernel(const float *__res
                 else if (unsigned(ix) < unsigned(w))
                     wd[t] = tile[ix * c + (j - k * c)];
             }
-            uint32_t *d = dimg + int64_t(i) * 3;
+            uint32_t *d = dimg + int64_t(rec) * 3;
             d[0] = wd[0] & 0xFFFFu;
             d[1] = (wd[0] >> 16) | (wd[1] & 0xFFFF0000u);
             d[2] = wd[1] & 0xFFFFu;
