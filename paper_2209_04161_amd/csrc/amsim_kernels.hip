@@ -714,8 +714,11 @@ inline int row_log(int m_bits) { return m_bits > 7 ? m_bits : 7; }
 // reduction chunks of 8 steps.  The products a tile computes (rows padded to whole waves) times
 // an issue-cost estimate per product, spread over the workgroups; the workgroups per CU that LDS
 // and registers allow (four waves per SIMD) give the slots of one round, and a partly empty last
-// round costs a whole one.  Only a launch under one round is split (at least min_chunks chunks
-// per split).
+// round costs a whole one.  Tiles whose workgroups have few waves with rows in them (a 3 x 64-row
+// wave tile over 147 rows) leave the SIMDs idle, which scales their issue rate down (measured on
+// MI355X: the ResNet-50 stem's backward-weight 6%, the LeNet-5 stack 11% and an M = 11 1024^3
+// GEMM 17% faster than without the scaling).  Only a launch under one round is split (at least
+// min_chunks chunks per split).
 Tile choose_tab_tile(int64_t rows, int64_t cols, int64_t q, int64_t min_chunks, bool allow_split, int rl,
                      int max_tm, int64_t phases)
 {
@@ -739,6 +742,11 @@ Tile choose_tab_tile(int64_t rows, int64_t cols, int64_t q, int64_t min_chunks, 
         const int64_t wgs_per_cu =
             std::max<int64_t>(1, std::min<int64_t>(kWavesPerCU / c.nw, kLdsPerCU / tab_lds_bytes(c.tn, c.wr, c.nw, rl)));
         const double slots = double(kCUs * wgs_per_cu);
+        // fewer than two waves with rows per SIMD cannot keep the vector ALU and LDS busy: the
+        // issue rate scales down with the live waves per CU below 8
+        const double live_waves = double(live_rows / wrows) * double(c.nw / c.wr) * double(wgs_per_cu);
+        const double occ = std::min(1.0, live_waves / 8.0);
+
         const double work =
             double(ceil_div(rows, wrows) * wrows) * double(col_tiles * ctile) * double(phases) * double(q * 8);
         const bool pair = rl == 7 && dot_cols_ok(c.tn) && c.wr == c.nw;
@@ -766,7 +774,7 @@ Tile choose_tab_tile(int64_t rows, int64_t cols, int64_t q, int64_t min_chunks, 
             const int64_t s_eff = ceil_div(q, cps);       // the splits that chunking leaves
             const double wgs = double(base * s_eff);
             const double rounds = std::ceil(wgs / slots);
-            const double issue_ns = (work / wgs) * per_product * slots / 28000.0;
+            const double issue_ns = (work / wgs) * per_product * slots / 28000.0 / occ;
             const double latency_ns = std::ceil(double(cps) * 8.0 / slab_steps) * slab_ns;
             double cst = rounds * std::max(issue_ns, latency_ns);
             if (s_eff > 1)
