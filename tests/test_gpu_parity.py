@@ -338,6 +338,45 @@ def test_conv_passes_match_oracle(B, ci, m):
     assert_within_tolerance(dw, ref, S, "bwd_weight %d" % ci)
 
 
+def _random_conv_cases(count, seed):
+    """Seeded random conv shapes: kernels 1..7, strides 1..3 (different in h and w), asymmetric pads
+    0..3, channel counts on both sides of the w-unfolding thresholds, M in {3, 5, 7, 9}, both models."""
+    rng = np.random.default_rng(seed)
+    cases = []
+    while len(cases) < count:
+        kh, kw = int(rng.integers(1, 8)), int(rng.integers(1, 8))
+        sh, sw = int(rng.integers(1, 4)), int(rng.integers(1, 4))
+        pads = [int(rng.integers(0, 4)) for _ in range(4)]
+        h, w = int(rng.integers(1, 14)), int(rng.integers(1, 14))
+        if h + pads[0] + pads[1] < kh or w + pads[2] + pads[3] < kw:
+            continue
+        p = dict(n=int(rng.integers(1, 4)), h=h, w=w, c_in=int(rng.choice([1, 2, 3, 5, 7, 9, 15, 17, 33])),
+                 c_out=int(rng.choice([1, 2, 3, 5, 8, 9, 16, 20, 40])), kh=kh, kw=kw, stride_h=sh, stride_w=sw,
+                 pad_top=pads[0], pad_bottom=pads[1], pad_left=pads[2], pad_right=pads[3])
+        cases.append((p, str(rng.choice(["mitchell", "exact_trunc"])), int(rng.choice([3, 5, 7, 9]))))
+    return cases
+
+
+RANDOM_CONV_CASES = _random_conv_cases(40, 20261202)
+
+
+@pytest.mark.parametrize("ci", range(len(RANDOM_CONV_CASES)))
+def test_conv_random_shapes_match_oracle(B, ci):
+    p, model, m = RANDOM_CONV_CASES[ci]
+    x, w, dy = _conv_inputs(p, 5000 + 3 * ci)
+    lut = dev_lut(B, model, m)
+    om = MODELS[model]
+    y = host(B.approx_conv2d_fwd(p, cuda(x), cuda(w), lut, m))
+    ref, S = oracle.conv2d_fwd(om, m, p, x, w)
+    assert_within_tolerance(y, ref, S, "fwd %s" % p)
+    dx = host(B.approx_conv2d_bwd_data(p, cuda(dy), cuda(w), lut, m))
+    ref, S = oracle.conv2d_bwd_data(om, m, p, dy, w)
+    assert_within_tolerance(dx, ref, S, "bwd_data %s" % p)
+    dw = host(B.approx_conv2d_bwd_weight(p, cuda(x), cuda(dy), lut, m))
+    ref, S = oracle.conv2d_bwd_weight(om, m, p, x, dy)
+    assert_within_tolerance(dw, ref, S, "bwd_weight %s" % p)
+
+
 def test_operand_order_with_asymmetric_table(B):
     """A table from an asymmetric model (first operand truncated to M bits, second to M-1) pins
     the first operand of GEMM and of every convolution pass."""
