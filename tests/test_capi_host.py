@@ -144,6 +144,17 @@ def test_workspace_size_queries(L):
         binding.amsim_gemm_workspace_size(0, 0, 4, 4, 4, 12)
 
 
+def test_workspace_covers_the_unfolded_conv_paths(L):
+    """Few input channels: the forward pass's workspace holds x unfolded along w as step-pair
+    records (12 bytes per output column and channel pair of kw * c), the backward-data pass's the
+    unfolded input's gradient (4 bytes per output column and kw * c channel)."""
+    stem = dict(n=32, h=224, w=224, c_in=3, c_out=64, kh=7, kw=7, stride_h=2, stride_w=2,
+                pad_top=3, pad_bottom=3, pad_left=3, pad_right=3)
+    hp, ow = 224 + 6, (224 + 6 - 7) // 2 + 1
+    assert binding.amsim_conv2d_workspace_size(stem, 0, 7) >= 32 * hp * ow * ((7 * 3 + 1) // 2) * 12
+    assert binding.amsim_conv2d_workspace_size(stem, 1, 7) >= 32 * 224 * ow * 7 * 3 * 4
+
+
 def test_device_entry_points_reject_bad_arguments_before_launching(L):
     """Argument checks return before any HIP call, so these run without a GPU."""
     vp = ctypes.c_void_p
