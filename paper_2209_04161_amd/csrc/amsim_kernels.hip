@@ -158,7 +158,7 @@ __global__ __launch_bounds__(256) void decode_pad_nhcw_kernel(const float *__res
                                                               uint32_t *__restrict__ dst, int m, int shift, uint32_t zidx,
                                                               uint32_t *__restrict__ stats, int cc)
 {
-    __shared__ uint32_t tile[kNhcwTile];
+    extern __shared__ uint32_t tile[];  // cc * (w | 1) words (the launch sizes it)
     const int ws = w | 1, cp = (c + 1) / 2;
     ExpStats st;
     for (int rr = blockIdx.x; rr < n * hp; rr += gridDim.x) {
@@ -225,7 +225,7 @@ __global__ __launch_bounds__(256) void decode_unfold_w_kernel(const float *__res
                                                               uint32_t *__restrict__ dst, int m, int shift,
                                                               uint32_t *__restrict__ stats)
 {
-    __shared__ uint32_t tile[kNhcwTile];
+    extern __shared__ uint32_t tile[];  // w * c words (the launch sizes it)
     const int cu = kw_n * c, cp = (cu + 1) / 2;
     ExpStats st;
     for (int rr = blockIdx.x; rr < n * hp; rr += gridDim.x) {
@@ -1358,8 +1358,8 @@ static int decode_nhcw(const float *src, int n, int h, int w, int c, int top, in
     int cc = std::max(2, std::min(c, kNhcwTile / (w | 1)));  // channels per LDS tile
     if (cc < c) cc &= ~1;  // chunks hold whole channel pairs
     const int grid = int(std::min<int64_t>(int64_t(n) * hp, kStatSlots));  // one padded image row at a time
-    hipLaunchKernelGGL(decode_pad_nhcw_kernel, dim3(grid), dim3(256), 0, st, src, n, h, w, c, top, left, hp, wp, dst,
-                       m_bits, shift, 0u, stats, cc);
+    hipLaunchKernelGGL(decode_pad_nhcw_kernel, dim3(grid), dim3(256), size_t(cc) * (w | 1) * 4, st, src, n, h, w, c,
+                       top, left, hp, wp, dst, m_bits, shift, 0u, stats, cc);
     return grid;
 }
 
@@ -1377,8 +1377,9 @@ int approx_conv2d_fwd(const amsim_conv2d *desc, const float *x, const float *w, 
     int n_a;
     if (p.unfold_w) {
         n_a = int(std::min<int64_t>(int64_t(s.n) * p.Hp, kStatSlots));  // one padded image row at a time
-        hipLaunchKernelGGL(decode_unfold_w_kernel, dim3(n_a), dim3(256), 0, st, x, s.n, s.h, s.w, s.ci, s.pt, s.pl,
-                           p.Hp, s.kw, s.sw, s.ow, Xd, m_bits, shift_first(m_bits), stats_a(ws, p));
+        hipLaunchKernelGGL(decode_unfold_w_kernel, dim3(n_a), dim3(256), size_t(s.w) * s.ci * 4, st, x, s.n, s.h,
+                           s.w, s.ci, s.pt, s.pl, p.Hp, s.kw, s.sw, s.ow, Xd, m_bits, shift_first(m_bits),
+                           stats_a(ws, p));
     } else {
         n_a = decode_nhcw(x, s.n, s.h, s.w, s.ci, s.pt, s.pl, p.Hp, p.Wp, Xd, m_bits, shift_first(m_bits),
                           stats_a(ws, p), st);
