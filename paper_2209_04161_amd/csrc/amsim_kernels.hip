@@ -231,8 +231,10 @@ __global__ __launch_bounds__(256) void decode_unfold_w_kernel(const float *__res
     for (int rr = blockIdx.x; rr < n * hp; rr += gridDim.x) {
         const int b = rr / hp, y = rr - b * hp, ih = y - top;
         uint32_t *dimg = dst + int64_t(rr) * cp * ow_n * 3;
-        if (unsigned(ih) >= unsigned(h)) {  // a padding row (uniform over the workgroup)
-            for (int i = threadIdx.x; i < cp * ow_n * 3; i += 256) dimg[i] = 0u;
+        if (unsigned(ih) >= unsigned(h)) {  // a padding row (uniform over the workgroup): +0, and the
+            // padding channel's -0 in the head word of the last channel pair
+            for (int i = threadIdx.x; i < cp * ow_n * 3; i += 256)
+                dimg[i] = (cu & 1) && i % 3 == 1 && i / 3 >= (cp - 1) * ow_n ? 0x80000000u : 0u;
             continue;
         }
         const float *srow = src + (int64_t(b) * h + ih) * w * c;

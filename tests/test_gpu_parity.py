@@ -204,6 +204,21 @@ def test_conv_zero_sums_keep_their_sign(B):
     check(dw, ref, S, "bwd_weight")
 
 
+def test_conv_unfolded_padding_channel_is_neutral(B):
+    """The w-unfolded forward pass pads an odd kw * c to whole channel pairs; the padding channel
+    must add nothing, not even a zero sign, also in zero-padded image rows.  With x = +0 and
+    negative weights every product, padded taps included, is -0, so every output is -0."""
+    m = 7
+    lut = dev_lut(B, "mitchell", m)
+    p = W.conv_desc(2, 5, 7, 3, 4, 3, 3, 1, pads=(2, 1, 1, 1))   # kw * c = 9: one padding channel
+    x = np.zeros((2, 5, 7, 3), dtype=np.float32)
+    w = -np.abs(W.normal((3, 3, 3, 4), 1.0, 79))
+    y = host(B.approx_conv2d_fwd(p, cuda(x), cuda(w), lut, m))
+    ref, S = oracle.conv2d_fwd(oracle.MITCHELL, m, p, x, w)
+    assert (ref == 0.0).all() and np.signbit(ref).all()
+    assert_bits_equal(y, ref.astype(np.float32), "unfolded forward, zero products")
+
+
 def test_conv_single_product_shapes_bit_exact(B):
     """1x1 conv with one input channel (fwd), one output position (bwd_weight) and one output
     channel with a 1x1 kernel (bwd_data): every output is a single product."""
