@@ -513,6 +513,7 @@ constexpr int kPrepWorkgroups = 8;   // table preparation (M <= 7): workgroups s
 __global__ __launch_bounds__(1024) void prep_rows_kernel(const uint32_t *__restrict__ lut, int m,
                                                          unsigned char *__restrict__ dst,
                                                          unsigned char *__restrict__ dot_rows,
+                                                         uint32_t *__restrict__ hl_rows,
                                                          const uint32_t *__restrict__ stats_a, int n_a,
                                                          const uint32_t *__restrict__ stats_b, int n_b,
                                                          int *__restrict__ flags)
@@ -582,9 +583,12 @@ __global__ __launch_bounds__(1024) void prep_rows_kernel(const uint32_t *__restr
         const bool special = ((a_hs | b_hs) >> 8) != 0u;
         const bool window = stats_a != nullptr && !special && a_lo + b_lo >= 128u && a_hi + b_hi <= 380u &&
                             b_hi <= 253u;
+        // The hi/lo path (2-byte entries) also needs its low halves' products normal: v_lo >= 2^-15
+        // times pb normal as a bf16 (Eb >= 16) and times pa normal (Ea + Eb - 127 - 15 >= 1).
+        const bool window_hl = window && b_lo >= 16u && a_lo + b_lo >= 143u;
         if (lead) {
             flags[0] = eb;
-            flags[1] = (eb == 1 && window) ? 1 : 0;
+            flags[1] = (eb == 1 && window) ? 1 : ((eb == 2 && window_hl) ? 2 : 0);
         }
     }
     __syncthreads();
@@ -620,6 +624,32 @@ __global__ __launch_bounds__(1024) void prep_rows_kernel(const uint32_t *__restr
             reinterpret_cast<uint32_t *>(dst + size_t(kZeroRow) * kTabRowEntries * eb)[i] = 0u;
         if (eb == 1 && threadIdx.x < kTabRowEntries / 4)
             reinterpret_cast<uint32_t *>(dot_rows + size_t(kZeroRow) * kTabRowEntries)[threadIdx.x] = 0u;
+    }
+    // hi/lo rows (2-byte entries): words 2 g + i of row kb hold entry ka = g + 64 i as
+    // (v_hi - 0x3F80) | (v_lo - 0x3F80) << 16 in bf16 bits; v_lo is never zero (see tab_body_hl).
+    if (eb == 2) {
+        for (int i = tid; i < (n + 1) * 64; i += nthreads) {
+            const int kb = i / 64, g = i % 64;  // kb = n: the zero row
+            uint32_t word[2] = {0u, 0u};
+#pragma unroll
+            for (int j = 0; j < 2; ++j) {
+                const int ka = g + 64 * j;
+                if (kb < n && ka < n) {
+                    const float v = __uint_as_float((slut[ka * n + kb] & 0x00FFFFFFu) + 0x3F800000u);
+                    float hi = __uint_as_float(__float_as_uint(v) & 0xFFFF0000u);
+                    float lo = v - hi;  // exact: the low 8 of v's 16 significant bits
+                    if (lo == 0.0f) {   // one bf16 unit of v moves to the low half
+                        lo = __uint_as_float((__float_as_uint(v) & 0x7F800000u) - (7u << 23));
+                        hi = v - lo;
+                    }
+                    word[j] = ((__float_as_uint(hi) >> 16) - 0x3F80u) & 0xFFFFu;
+                    word[j] |= (((__float_as_uint(lo) >> 16) - 0x3F80u) & 0xFFFFu) << 16;
+                }
+            }
+            const int row = kb < n ? kb : kZeroRow;
+            hl_rows[(row * 64 + g) * 2 + 0] = word[0];
+            hl_rows[(row * 64 + g) * 2 + 1] = word[1];
+        }
     }
     // bf16-path rows: word g of row kb holds the bytes of entries g, g + 32, g + 64, g + 96.
     if (eb == 1) {
@@ -858,11 +888,12 @@ inline int decode_vec(const float *src, int64_t sb, int64_t sr, int64_t sc)
 }
 
 // Workspace layout shared by the size queries and the launches:
-//   [transposed rows][bf16-path rows][flags][statistics][first operand][second operand][partials]
+//   [transposed rows][bf16-path rows][hi/lo rows][flags][statistics][first operand][second operand]
+//   [partials]
 struct Plan {
     Tile tile;
     int rl;  // log2 of the table row length
-    size_t off_rows, off_dot_rows, off_eb, off_stats, off_a, off_b, off_part, total;
+    size_t off_rows, off_dot_rows, off_hl_rows, off_eb, off_stats, off_a, off_b, off_part, total;
     int64_t a_ld, b_ld;   // GEMM: padded leading dims of the decoded operands; conv: b_ld only
     int64_t a_elems;      // conv: elements of the decoded first operand
     int splits;           // reduction splits
@@ -883,8 +914,10 @@ void plan_tab_split(Plan &p, int64_t q)
 bool valid_m(int m_bits) { return m_bits >= 1 && m_bits <= 11; }
 
 // Transposed rows (the widest entry width, plus the zero row for 128-entry rows), bf16-path rows,
-// flags, decode statistics (two operands; for wide rows the table-preparation partials).
+// hi/lo rows (128-entry rows only), flags, decode statistics (two operands; for wide rows the
+// table-preparation partials).
 constexpr size_t kDotRowsBytes = size_t(kZeroRow + 1) * kTabRowEntries;
+constexpr size_t kHlRowsBytes = size_t(kZeroRow + 1) * kHlRowBytes;  // 2-byte tables, hi/lo path
 constexpr size_t kStatsBytes = size_t(2) * kStatSlots * 4;
 
 inline size_t rows_bytes(int rl) { return (size_t(1) << rl) * ((size_t(1) << rl) + (rl == 7 ? 1 : 0)) * 4; }
@@ -893,7 +926,8 @@ size_t table_area(Plan &p, size_t o)
 {
     p.off_rows = o;
     p.off_dot_rows = p.off_rows + align_up(rows_bytes(p.rl));
-    p.off_eb = p.off_dot_rows + align_up(kDotRowsBytes);
+    p.off_hl_rows = p.off_dot_rows + align_up(kDotRowsBytes);
+    p.off_eb = p.off_hl_rows + (p.rl == 7 ? align_up(kHlRowsBytes) : 0);
     p.off_stats = p.off_eb + kAlign;
     return p.off_stats + align_up(kStatsBytes);
 }
@@ -1137,8 +1171,9 @@ int prep_rows(const uint32_t *lut, int m_bits, char *ws, const Plan &p, int n_a,
     if (p.rl == 7) {
         hipLaunchKernelGGL(prep_rows_kernel, dim3(kPrepWorkgroups), dim3(1024), 0, st, lut, m_bits,
                            reinterpret_cast<unsigned char *>(ws + p.off_rows),
-                           reinterpret_cast<unsigned char *>(ws + p.off_dot_rows), stats_a(ws, p), n_a,
-                           stats_b(ws, p), n_b, reinterpret_cast<int *>(ws + p.off_eb));
+                           reinterpret_cast<unsigned char *>(ws + p.off_dot_rows),
+                           reinterpret_cast<uint32_t *>(ws + p.off_hl_rows), stats_a(ws, p), n_a, stats_b(ws, p), n_b,
+                           reinterpret_cast<int *>(ws + p.off_eb));
         return launch_status();
     }
     const int total = 1 << (2 * m_bits);
@@ -1168,6 +1203,7 @@ TabArgs tab_args(const Plan &p, char *ws, const uint32_t *A, int64_t a_elems, co
     a.out = out;
     a.rows = reinterpret_cast<const unsigned char *>(ws + p.off_rows);
     a.dot_rows = reinterpret_cast<const unsigned char *>(ws + p.off_dot_rows);
+    a.hl_rows = reinterpret_cast<const unsigned char *>(ws + p.off_hl_rows);
     a.eb = reinterpret_cast<const int *>(ws + p.off_eb);
     a.R = R;
     a.N = N;

@@ -60,7 +60,8 @@ struct TabArgs {
     int64_t ldc;         // GEMM result leading dimension
     const unsigned char *rows;      // transposed table rows (exact path)
     const unsigned char *dot_rows;  // the same 1-byte rows in bf16-path staging order
-    const int *eb;                  // [0] entry width, [1] 1 when the bf16 path may run
+    const unsigned char *hl_rows;   // 2-byte tables: entries split into bf16 halves (hi/lo path)
+    const int *eb;                  // [0] entry width, [1] 1 (2) when the bf16 (hi/lo) path may run
     int R, N;            // result rows and columns
     int splits;          // reduction splits: tile z = (phase *) splits + split
     int chunks_per_split;  // reduction chunks (8 steps each) per split
@@ -662,6 +663,70 @@ __device__ __forceinline__ void dot_load_pair(uint32_t (&dst)[split_a<OP>() ? 3 
     }
 }
 
+// The end of a pair-path body: the signs of exactly-zero sums, then the stores of the TM x TN
+// outputs (or of the split's partial sums).
+template <int OP, int TM, int TN>
+__device__ __forceinline__ void dot_finish(const TabArgs &a, float (&acc)[TM][TN], const AView<TM> &av, int row0,
+                                           int col0, int R, int q0, int cpt, int p_end)
+{
+    // Signs of zero sums: -0 when every product of the split's range is -0, else +0.  The first
+    // product that is not -0 (non-zero, or +0) settles an output as +0, so the pass stops once no
+    // output of the wave is pending -- after one step for a sum that cancelled to zero, after the
+    // whole range only for outputs whose products are all -0.
+    uint32_t pending = 0u;
+#pragma unroll
+    for (int r = 0; r < TM; ++r)
+#pragma unroll
+        for (int t = 0; t < TN; ++t)
+            if (row0 + 64 * r < R && col0 + t < a.N && acc[r][t] == 0.0f) pending |= 1u << (r * TN + t);
+    const uint32_t zero = pending;
+    if (__builtin_amdgcn_ballot_w64(pending != 0u) != 0u) {
+        bool open = true;
+        for (int tp_i = q0 / max(cpt, 1); open && tp_i * cpt * 8 < p_end; ++tp_i) {
+            const int pbase = tp_i * cpt * 8;
+            const TabTap tp = tab_tap<OP>(a, tp_i);
+            const int j1 = min(tp.count, p_end - pbase);
+            for (int j = max(q0 * 8 - pbase, 0); j < j1; ++j) {
+                uint32_t aw[TM];
+                load_a_words<OP, TM>(aw, av, __builtin_amdgcn_readfirstlane(a_step_offset<OP>(tp, j)), j);
+                const uint32_t *brow = a.Bd + int64_t(tp.bbase + j) * a.Np + col0;
+#pragma unroll
+                for (int t = 0; t < TN; ++t) {
+                    const float pb = head_value(brow[t]);
+#pragma unroll
+                    for (int r = 0; r < TM; ++r)
+                        if (__float_as_uint(head_value(aw[r]) * pb) != 0x80000000u) pending &= ~(1u << (r * TN + t));
+                }
+                if (__builtin_amdgcn_ballot_w64(pending != 0u) == 0u) {
+                    open = false;
+                    break;
+                }
+            }
+        }
+#pragma unroll
+        for (int r = 0; r < TM; ++r)
+#pragma unroll
+            for (int t = 0; t < TN; ++t)
+                if (zero & (1u << (r * TN + t))) acc[r][t] = (pending & (1u << (r * TN + t))) ? -0.0f : 0.0f;
+    }
+
+    float *out = a.out + int64_t(tab_split(a)) * a.out_elems;
+#pragma unroll
+    for (int r = 0; r < TM; ++r) {
+        const int row = row0 + 64 * r;
+        if (row >= R) continue;
+        int ab = 0;
+        int64_t ob = 0;
+        tab_row<OP>(a, row, ab, ob);  // the output offset, recomputed rather than kept in registers
+        float *dst = out + ob;
+#pragma unroll
+        for (int t = 0; t < TN; ++t) {
+            const int col = col0 + t;
+            if (col < a.N) dst[col] = acc[r][t];
+        }
+    }
+}
+
 // Workgroup: NW waves along rows (64*TM rows each), all on the same 8 columns.  Every thread
 // stages one step's entry group per slab (KS = 2 * NW steps x 32 groups).
 template <int OP, int TM, int NW, int DC>
@@ -858,62 +923,217 @@ __device__ __forceinline__ void tab_body_dot(const TabArgs &a)
         slab(std::integral_constant<int, 1>{});
     }
 
-    // Signs of zero sums: -0 when every product of the split's range is -0, else +0.  The first
-    // product that is not -0 (non-zero, or +0) settles an output as +0, so the pass stops once no
-    // output of the wave is pending -- after one step for a sum that cancelled to zero, after the
-    // whole range only for outputs whose products are all -0.
-    uint32_t pending = 0u;
-#pragma unroll
-    for (int r = 0; r < TM; ++r)
-#pragma unroll
-        for (int t = 0; t < TN; ++t)
-            if (row0 + 64 * r < R && col0 + t < a.N && acc[r][t] == 0.0f) pending |= 1u << (r * TN + t);
-    const uint32_t zero = pending;
-    if (__builtin_amdgcn_ballot_w64(pending != 0u) != 0u) {
-        bool open = true;
-        for (int tp_i = q0 / max(cpt, 1); open && tp_i * cpt * 8 < p_end; ++tp_i) {
-            const int pbase = tp_i * cpt * 8;
-            const TabTap tp = tab_tap<OP>(a, tp_i);
-            const int j1 = min(tp.count, p_end - pbase);
-            for (int j = max(q0 * 8 - pbase, 0); j < j1; ++j) {
-                uint32_t aw[TM];
-                load_a_words<OP, TM>(aw, av, __builtin_amdgcn_readfirstlane(a_step_offset<OP>(tp, j)), j);
-                const uint32_t *brow = a.Bd + int64_t(tp.bbase + j) * a.Np + col0;
-#pragma unroll
-                for (int t = 0; t < TN; ++t) {
-                    const float pb = head_value(brow[t]);
-#pragma unroll
-                    for (int r = 0; r < TM; ++r)
-                        if (__float_as_uint(head_value(aw[r]) * pb) != 0x80000000u) pending &= ~(1u << (r * TN + t));
-                }
-                if (__builtin_amdgcn_ballot_w64(pending != 0u) == 0u) {
-                    open = false;
-                    break;
-                }
-            }
-        }
-#pragma unroll
-        for (int r = 0; r < TM; ++r)
-#pragma unroll
-            for (int t = 0; t < TN; ++t)
-                if (zero & (1u << (r * TN + t))) acc[r][t] = (pending & (1u << (r * TN + t))) ? -0.0f : 0.0f;
-    }
+    dot_finish<OP, TM, TN>(a, acc, av, row0, col0, R, q0, cpt, p_end);
+}
 
-    float *out = a.out + int64_t(tab_split(a)) * a.out_elems;
+// ------------------------------------------------------- bf16 hi/lo path (2-byte tables)
+// A 2-byte entry's value v has up to 16 significant bits: too many for one bf16, but v is the sum
+// of two bf16 values v_hi (its top 8 bits) and v_lo (the rest; where that is zero, v_hi is
+// lowered by one bf16 unit and v_lo is that unit, so that neither half is ever zero).  The
+// table-preparation kernel stores, per row kb and first-operand mantissa ka, both halves (less
+// the bias 0x3F80) in one word; the staging adds the column's pb bits to each half, giving
+// (t_hi, t_lo) = (v_hi * pb, v_lo * pb) as a bf16 pair, and one v_dot2_f32_bf16 against
+// (pa, pa) adds t_hi * pa + t_lo * pa = v * pb * pa, exact, to the sum: one instruction per
+// product and 4 bytes of LDS per product.  Exactness needs every half-product normal: pb's
+// exponent field >= 16 and Ea + Eb >= 143 (v_lo >= 2^-15), besides the bf16 path's upper bounds;
+// the table preparation checks it against the decode statistics.  8-wave, 8-column tiles only:
+// an 8-column entry is two 16-byte halves, each in a 2 KiB region of the step (so that the index
+// word, ka * 16, addresses both), and a slab holds NW steps.
+constexpr int kHlStepBytes = 2 * kDotStepBytes;        // two 8-column halves of 128 x 16 bytes
+constexpr int kHlRowBytes = 64 * 2 * 4;                // per row kb: 64 groups x 2 entries x 4 bytes
+
+// Staging of one hi/lo slab: thread -> step slot (tid / 64) and entry group g (tid % 64), which
+// builds the entries ka = g and g + 64.
+__device__ __forceinline__ void hl_fetch_b(u32x4 (&bw)[2], const TabTap &tp, int c0, const uint32_t *__restrict__ Bd,
+                                           int Np, int colw)
+{
+    const int j = c0 + (threadIdx.x >> 6);
+    if (j < tp.count) {
+        const u32x4 *src = reinterpret_cast<const u32x4 *>(Bd + int64_t(tp.bbase + j) * Np + colw);
+        bw[0] = src[0];
+        bw[1] = src[1];
+    } else {  // a padding step: +0 operands, whose entries are +0
+        bw[0] = u32x4{kZeroRowWord, kZeroRowWord, kZeroRowWord, kZeroRowWord};
+        bw[1] = bw[0];
+    }
+}
+
+// Per column, the 8 bytes of its row kb (idx = kb * 128) that hold the group's two entries.
+__device__ __forceinline__ void hl_fetch_rows(u32x2 (&rw)[8], const u32x4 (&bw)[2], __amdgpu_buffer_rsrc_t rres)
+{
+    const uint32_t g = threadIdx.x & 63;
+#pragma unroll
+    for (int c = 0; c < 8; ++c) {
+        const uint32_t w = bw[c / 4][c % 4];
+        rw[c] = __builtin_amdgcn_raw_buffer_load_b64(rres, ((w & 0x7F80u) << 2) | (g * 8u), 0, 0);
+    }
+}
+
+// Commit: (t_hi, t_lo) = each stored half + pb's bf16 bits (the word's high half, which is pb with
+// its mantissa cleared); a zero second operand reads the all-zero row and gets +-0 halves.
+__device__ __forceinline__ void hl_commit(const u32x4 (&bw)[2], const u32x2 (&rw)[8], unsigned char *slab)
+{
+    const int slot = threadIdx.x >> 6, g = threadIdx.x & 63;
+    uint32_t hb[8];
+#pragma unroll
+    for (int c = 0; c < 8; ++c) hb[c] = __builtin_amdgcn_perm(bw[c / 4][c % 4], bw[c / 4][c % 4], 0x03020302u);
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+        uint32_t t[8];
+#pragma unroll
+        for (int c = 0; c < 8; ++c) t[c] = add_u16x2(rw[c][i], hb[c]);
+        unsigned char *dst = slab + slot * kHlStepBytes + (g + 64 * i) * 16;
+        *reinterpret_cast<u32x4 *>(dst) = u32x4{t[0], t[1], t[2], t[3]};
+        *reinterpret_cast<u32x4 *>(dst + kDotStepBytes) = u32x4{t[4], t[5], t[6], t[7]};
+    }
+}
+
+// Workgroup: 8 waves along rows (64*TM rows each), all on the same 8 columns; slabs of 8 steps.
+template <int OP, int TM>
+__device__ __forceinline__ void tab_body_hl(const TabArgs &a)
+{
+    constexpr int NW = 8, TN = 8, KS = NW;
+    constexpr int kSlab = KS * kHlStepBytes;
+    constexpr bool SPLIT = split_a<OP>();
+    constexpr int NA = SPLIT ? 3 : 2;  // first-operand registers per step pair and lane row
+    extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
+
+    const int R = tab_rows<OP>(a);
+    if (a.tx * 64 * TM * NW >= R) return;  // uniform over the workgroup
+    const int lane = threadIdx.x & 63;
+    const int wave = wave_id();
+    const int row0 = a.tx * (64 * TM * NW) + wave * (64 * TM) + lane;
+    const bool live = row0 - lane < R;  // wave-uniform
+    const int col0 = a.ty * TN;
+    const __amdgpu_buffer_rsrc_t rres = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<unsigned char *>(a.hl_rows), 0, int((kZeroRow + 1) * kHlRowBytes), 0x00020000);
+
+    int abase[TM];
 #pragma unroll
     for (int r = 0; r < TM; ++r) {
         const int row = row0 + 64 * r;
-        if (row >= R) continue;
         int ab = 0;
         int64_t ob = 0;
-        tab_row<OP>(a, row, ab, ob);  // the output offset, recomputed rather than kept in registers
-        float *dst = out + ob;
-#pragma unroll
-        for (int t = 0; t < TN; ++t) {
-            const int col = col0 + t;
-            if (col < a.N) dst[col] = acc[r][t];
+        if (row < R) {
+            tab_row<OP>(a, row, ab, ob);
+            if constexpr (split_a<OP>()) ab = tab_row_rec<OP>(a, row);
         }
+        abase[r] = ab;
     }
+    const AView<TM> av = make_aview<OP, TM>(a, abase);
+    const int count = tab_count<OP>(a);
+    const int cpt = (count + 7) / 8;
+    const int q_total = tab_taps<OP>(a) * cpt;
+    const int q0 = tab_split(a) * a.chunks_per_split;
+    const int p_end = min(q_total, q0 + a.chunks_per_split) * 8;
+
+    // while slab s is computed, slab s + 1's second-operand words and row halves are fetched
+    u32x4 sbw[2];
+    u32x2 srw[8];
+    float acc[TM][TN];
+    init_acc(acc);
+    // the first operand's step pairs as a ring of four (pair kp in w[kp % 4]), loaded LA ahead
+    constexpr int RS = 4;
+    constexpr int LA = OP == OP_BWD_DATA ? 2 : 3;
+    static_assert((KS / 2) % RS == 0, "ring of step pairs");
+    uint32_t w[RS][NA][TM];
+    auto advance = [&](const TabTap &t, int tp_, int c, TabTap &o, int &otap, int &oc, bool &ok)
+                       __attribute__((always_inline)) {
+        o = t;
+        otap = tp_;
+        oc = c + KS;
+        if (oc >= count) {
+            otap = tp_ + 1;
+            oc = 0;
+        }
+        ok = otap * cpt * 8 + oc < p_end;
+        if (ok && otap != tp_) o = tab_tap<OP>(a, otap);
+    };
+    TabTap cur{0, 0, 0, 0, 0};
+    int tap = q0 / max(cpt, 1);
+    int c0 = (q0 - tap * cpt) * 8;
+    bool have = q0 * 8 < p_end;
+    TabTap nxt{0, 0, 0, 0, 0};
+    int ntap = 0, nc0 = 0;
+    bool has_next = false;
+    if (have) {
+        cur = tab_tap<OP>(a, tap);
+        hl_fetch_b(sbw, cur, c0, a.Bd, a.Np, col0);
+        hl_fetch_rows(srw, sbw, rres);
+        hl_commit(sbw, srw, smem);
+#pragma unroll
+        for (int k = 0; k < LA; ++k) dot_load_pair<OP, TM>(w[k], av, cur, c0 + 2 * k);
+        advance(cur, tap, c0, nxt, ntap, nc0, has_next);
+    }
+    __syncthreads();
+    auto slab = [&](auto buf_c) __attribute__((always_inline)) {
+        constexpr uint32_t BOFF = uint32_t(decltype(buf_c)::value) * kSlab;
+        constexpr uint32_t NEXT = uint32_t(decltype(buf_c)::value ^ 1) * kSlab;
+        uniform_cursor(cur, tap, c0);
+        uniform_cursor(nxt, ntap, nc0);
+        if (has_next) {
+            hl_fetch_b(sbw, nxt, nc0, a.Bd, a.Np, col0);
+            hl_fetch_rows(srw, sbw, rres);
+        }
+        const int nslots = min(min(KS, cur.count - c0), p_end - (tap * cpt * 8 + c0));
+        const int npairs = live ? (nslots + 1) / 2 : 0;
+        __builtin_amdgcn_s_setprio(3);  // computing waves first, as on the bf16 path
+#pragma unroll
+        for (int kp = 0; kp < KS / 2; ++kp) {
+            if (kp >= npairs) break;
+            if (kp + LA < KS / 2)
+                dot_load_pair<OP, TM>(w[(kp + LA) % RS], av, cur, c0 + 2 * (kp + LA));
+            else
+                dot_load_pair<OP, TM>(w[(kp + LA) % RS], av, nxt, nc0 + 2 * (kp + LA - KS / 2));
+            const uint32_t(&a0)[TM] = w[kp % RS][0];
+            const uint32_t(&a1)[TM] = w[kp % RS][1];
+#pragma unroll
+            for (int r = 0; r < TM; ++r) {
+                const uint32_t o0 = SPLIT ? a0[r] : (a0[r] & 0xFFFFu);
+                const uint32_t o1 = SPLIT ? a1[r] : (a1[r] & 0xFFFFu);
+                uint32_t pp;  // (pa(k), pa(k+1)) as bf16
+                if constexpr (SPLIT)
+                    pp = w[kp % RS][NA - 1][r];
+                else
+                    pp = __builtin_amdgcn_perm(a1[r], a0[r], 0x07060302u);
+                const uint32_t pk0 = __builtin_amdgcn_perm(pp, pp, 0x01000100u);  // (pa(k), pa(k))
+                const uint32_t pk1 = __builtin_amdgcn_perm(pp, pp, 0x03020302u);  // (pa(k+1), pa(k+1))
+                const u32x4 x0 = lds_load_b128(o0, BOFF + (2 * kp) * kHlStepBytes);
+                const u32x4 x1 = lds_load_b128(o0, BOFF + (2 * kp) * kHlStepBytes + kDotStepBytes);
+#pragma unroll
+                for (int q = 0; q < 4; ++q) {
+                    acc[r][q] = dot2_bf16(x0[q], pk0, acc[r][q]);
+                    acc[r][4 + q] = dot2_bf16(x1[q], pk0, acc[r][4 + q]);
+                }
+                const u32x4 y0 = lds_load_b128(o1, BOFF + (2 * kp + 1) * kHlStepBytes);
+                const u32x4 y1 = lds_load_b128(o1, BOFF + (2 * kp + 1) * kHlStepBytes + kDotStepBytes);
+#pragma unroll
+                for (int q = 0; q < 4; ++q) {
+                    acc[r][q] = dot2_bf16(y0[q], pk1, acc[r][q]);
+                    acc[r][4 + q] = dot2_bf16(y1[q], pk1, acc[r][4 + q]);
+                }
+            }
+        }
+        if (live && npairs < KS / 2 && has_next) {  // a short slab: the next slab's first LA pairs
+#pragma unroll
+            for (int k = 0; k < LA; ++k) dot_load_pair<OP, TM>(w[k], av, nxt, nc0 + 2 * k);
+        }
+        __builtin_amdgcn_s_setprio(0);
+        if (has_next) hl_commit(sbw, srw, smem + NEXT);
+        __syncthreads();
+        cur = nxt;
+        tap = ntap;
+        c0 = nc0;
+        have = has_next;
+        advance(cur, tap, c0, nxt, ntap, nc0, has_next);
+    };
+    while (have) {
+        slab(std::integral_constant<int, 0>{});
+        if (!have) break;
+        slab(std::integral_constant<int, 1>{});
+    }
+
+    dot_finish<OP, TM, TN>(a, acc, av, row0, col0, R, q0, cpt, p_end);
 }
 
 // Four waves per SIMD: the register budget (<= 128 VGPRs) the tiles are sized for.  Without the
@@ -926,9 +1146,16 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(4, 4)))
     tab_tile_id(a.splits, a.tx, a.ty, a.tz);
     const int eb = __builtin_amdgcn_readfirstlane(a.eb[0]);
     if constexpr (RL == 7 && dot_cols_ok(TN) && WR == NW) {
-        if (__builtin_amdgcn_readfirstlane(a.eb[1]) != 0) {
+        const int path = __builtin_amdgcn_readfirstlane(a.eb[1]);
+        if (path == 1) {
             tab_body_dot<OP, TM, NW, TN>(a);
             return;
+        }
+        if constexpr (TN == 8 && NW == 8) {
+            if (path == 2) {
+                tab_body_hl<OP, TM>(a);
+                return;
+            }
         }
     }
     if (eb == 1)
@@ -955,7 +1182,9 @@ constexpr size_t tab_lds_bytes(int tn, int wr, int nw, int rl)
     b = tab_exact_lds_bytes(tnw, rl, 2) > b ? tab_exact_lds_bytes(tnw, rl, 2) : b;
     b = tab_exact_lds_bytes(tnw, rl, 4) > b ? tab_exact_lds_bytes(tnw, rl, 4) : b;
     const size_t dot = (rl == 7 && dot_cols_ok(tn) && wr == nw) ? size_t(2) * dot_slab_steps(nw) * kDotStepBytes : 0;
-    return b > dot ? b : dot;
+    const size_t hl = (rl == 7 && tn == 8 && nw == 8 && wr == nw) ? size_t(2) * nw * kHlStepBytes : 0;
+    b = b > dot ? b : dot;
+    return b > hl ? b : hl;
 }
 
 // ------------------------------------------------------------------ instantiated tiles -----

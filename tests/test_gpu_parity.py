@@ -116,6 +116,30 @@ def test_gemm_k1_window_products_bit_exact(B, m):
     assert_bits_equal(C, want, "gemm K=1 window M=%d" % m)
 
 
+@pytest.mark.parametrize("model", ["mitchell", "exact_trunc"])
+def test_gemm_large_tile_k1_window_products_bit_exact(B, model):
+    """K = 1 at 4096 x 4096 inside the exponent window, a shape that takes the 8-wave 8-column
+    tile: its bf16 pair path (Mitchell: 1-byte table) and its hi/lo path (exact truncation: 2-byte
+    table), every product bit for bit, signed zeros included."""
+    m = 7
+    rng = np.random.default_rng(91)
+    a = _window_vector(m, list(range(100, 148, 3)), rng)[-4096:].reshape(-1, 1)
+    b = _window_vector(m, list(range(110, 142, 2)), rng)[-4096:].reshape(1, -1)
+    C = host(B.approx_gemm(cuda(a), cuda(b), dev_lut(B, model, m), m))
+    want = oracle.mul(MODELS[model], m, np.repeat(a[:, 0], b.shape[1]), np.tile(b[0], a.shape[0]))
+    assert_bits_equal(C, want, "gemm 4096 x 4096 K=1 window %s" % model)
+
+
+def test_gemm_large_tile_two_byte_table_sums(B):
+    """The hi/lo path's sums (exact-truncation table, normal(0,1) operands) on the 8-wave
+    8-column tile, every output against the oracle."""
+    m = 7
+    A, Bm = W.gemm_inputs(4096, 2048, 8, "normal", seed=5100)
+    C = host(B.approx_gemm(cuda(A), cuda(Bm), dev_lut(B, "exact_trunc", m), m))
+    ref, S = oracle.gemm(oracle.EXACT_TRUNC, m, A, Bm)
+    assert_within_tolerance(C, ref, S, "gemm 4096 x 2048 x 8 exact_trunc")
+
+
 @pytest.mark.parametrize("k", [2, 3, 41, 200])
 def test_gemm_zero_sums_keep_their_sign(B, k):
     """Sums of signed zeros: -0 exactly when every product is -0 (the sum starts at -0.0), +0
@@ -429,23 +453,24 @@ def _sample(total, count, seed):
     return np.sort(np.concatenate([idx, [0, total - 1]]).astype(np.int64))
 
 
-def _check_conv_full(B, p, m, seed, stem=False, samples=(2048, 2048, 512), relu=False):
+def _check_conv_full(B, p, m, seed, stem=False, samples=(2048, 2048, 512), relu=False, model="mitchell"):
     x, w, dy = W.resnet_conv_inputs(p, seed=seed, stem=stem)
     if relu:  # post-ReLU activations: about half exact zeros
         x = np.maximum(W.normal(x.shape, 1.0, seed + 7), 0.0).astype(np.float32)
-    lut = dev_lut(B, "mitchell", m)
+    lut = dev_lut(B, model, m)
+    om = MODELS[model]
     xd, wd, dyd = cuda(x), cuda(w), cuda(dy)
     y = host(B.approx_conv2d_fwd(p, xd, wd, lut, m)).reshape(-1)
     idx = _sample(y.size, samples[0], seed)
-    ref, S = oracle.conv2d_fwd(oracle.MITCHELL, m, p, x, w, idx=idx)
+    ref, S = oracle.conv2d_fwd(om, m, p, x, w, idx=idx)
     assert_within_tolerance(y[idx], ref, S, "fwd")
     dx = host(B.approx_conv2d_bwd_data(p, dyd, wd, lut, m)).reshape(-1)
     idx = _sample(dx.size, samples[1], seed + 1)
-    ref, S = oracle.conv2d_bwd_data(oracle.MITCHELL, m, p, dy, w, idx=idx)
+    ref, S = oracle.conv2d_bwd_data(om, m, p, dy, w, idx=idx)
     assert_within_tolerance(dx[idx], ref, S, "bwd_data")
     dw = host(B.approx_conv2d_bwd_weight(p, xd, dyd, lut, m)).reshape(-1)
     idx = _sample(dw.size, samples[2], seed + 2)
-    ref, S = oracle.conv2d_bwd_weight(oracle.MITCHELL, m, p, x, dy, idx=idx)
+    ref, S = oracle.conv2d_bwd_weight(om, m, p, x, dy, idx=idx)
     assert_within_tolerance(dw[idx], ref, S, "bwd_weight")
     return y
 
@@ -453,6 +478,13 @@ def _check_conv_full(B, p, m, seed, stem=False, samples=(2048, 2048, 512), relu=
 def test_resnet_3x3_conv_full_size(B):
     cfg = W.RESNET_3X3
     _check_conv_full(B, cfg["conv"], cfg["m_bits"], seed=3000)
+
+
+def test_resnet_3x3_conv_full_size_two_byte_table(B):
+    """ResNet 3x3 at full size with the exact-truncation table (2-byte entries): the forward and
+    backward-data passes take the hi/lo path, backward-weight the exact path."""
+    cfg = W.RESNET_3X3
+    _check_conv_full(B, cfg["conv"], cfg["m_bits"], seed=3200, model="exact_trunc")
 
 
 def test_resnet_3x3_relu_input_full_size(B):
