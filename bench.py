@@ -263,6 +263,20 @@ def extras(B, W, torch, np, dev, lut7, m7, A, Bm, C):
         r[name] = {"ms": round(ms, 3), "gmacs_per_s": round(macs / ms / 1e6, 1)}
     ex["resnet_3x3_relu_input"] = r
     log("ReLU-input ResNet 3x3 done")
+    # the step's GEMM and ResNet 3x3 passes with the exact bfloat16-truncation table (2-byte
+    # entries: the hi/lo path on the 8-wave 8-column tiles, the exact path elsewhere)
+    lut_et = B.device_lut(B.lut_build(7, "exact_trunc"), dev)
+    x_h, w_h, dy_h = W.resnet_conv_inputs(cv, seed=3000)
+    x, w, dy = (torch.from_numpy(t).to(dev) for t in (x_h, w_h, dy_h))
+    ms = _time_call(torch, lambda: B.approx_gemm(A, Bm, lut_et, 7, out=C), 2)
+    r = {"gemm_4096": {"ms": round(ms, 2), "gmacs_per_s": round(M * N * K / ms / 1e6, 1)}}
+    for name, fn in (("fwd", lambda: B.approx_conv2d_fwd(cv, x, w, lut_et, 7)),
+                     ("bwd_data", lambda: B.approx_conv2d_bwd_data(cv, dy, w, lut_et, 7)),
+                     ("bwd_weight", lambda: B.approx_conv2d_bwd_weight(cv, x, dy, lut_et, 7))):
+        ms = _time_call(torch, fn, 5)
+        r["resnet_3x3_" + name] = {"ms": round(ms, 3), "gmacs_per_s": round(macs / ms / 1e6, 1)}
+    ex["exact_trunc_two_byte_table"] = r
+    log("exact-truncation table done")
     for cfg in W.RESNET50_LAYERS:
         p = cfg["conv"]
         x_h, w_h, dy_h = W.resnet_conv_inputs(p, seed=4000, stem=(cfg is W.RESNET50_LAYERS[0]))
