@@ -116,15 +116,14 @@ def test_gemm_k1_window_products_bit_exact(B, m):
     assert_bits_equal(C, want, "gemm K=1 window M=%d" % m)
 
 
-@pytest.mark.parametrize("model", ["mitchell", "exact_trunc"])
-def test_gemm_large_tile_k1_window_products_bit_exact(B, model):
+@pytest.mark.parametrize("model,m", [("mitchell", 7), ("exact_trunc", 7), ("exact_trunc", 5)])
+def test_gemm_large_tile_k1_window_products_bit_exact(B, model, m):
     """K = 1 at 4096 x 4096 inside the exponent window, a shape that takes the 8-wave 8-column
     tile: its bf16 pair path (Mitchell: 1-byte table) and its hi/lo path (exact truncation: 2-byte
-    table), every product bit for bit, signed zeros included."""
-    m = 7
-    rng = np.random.default_rng(91)
-    a = _window_vector(m, list(range(100, 148, 3)), rng)[-4096:].reshape(-1, 1)
-    b = _window_vector(m, list(range(110, 142, 2)), rng)[-4096:].reshape(1, -1)
+    table; at M = 5 its rows hold 32 entries), every product bit for bit, signed zeros included."""
+    rng = np.random.default_rng(91 + m)
+    a = np.resize(_window_vector(m, list(range(100, 148, 3)), rng)[::-1], 4096).reshape(-1, 1)
+    b = np.resize(_window_vector(m, list(range(110, 142, 2)), rng)[::-1], 4096).reshape(1, -1)
     C = host(B.approx_gemm(cuda(a), cuda(b), dev_lut(B, model, m), m))
     want = oracle.mul(MODELS[model], m, np.repeat(a[:, 0], b.shape[1]), np.tile(b[0], a.shape[0]))
     assert_bits_equal(C, want, "gemm 4096 x 4096 K=1 window %s" % model)
