@@ -939,7 +939,7 @@ __device__ __forceinline__ void tab_body_dot(const TabArgs &a)
 // the table preparation checks it against the decode statistics.  8-wave, 8-column tiles only:
 // an 8-column entry is two 16-byte halves, each in a 2 KiB region of the step (so that the index
 // word, ka * 16, addresses both), and a slab holds NW steps.
-constexpr int kHlStepBytes = 2 * kDotStepBytes;        // two 8-column halves of 128 x 16 bytes
+constexpr int kHlStepBytes = 2 * kDotStepBytes;        // two 4-column halves of 128 entries x 16 bytes
 constexpr int kHlRowBytes = 64 * 2 * 4;                // per row kb: 64 groups x 2 entries x 4 bytes
 
 // Staging of one hi/lo slab: thread -> step slot (tid / 64) and entry group g (tid % 64), which
