@@ -901,6 +901,7 @@ struct Plan {
     int64_t out_elems;      // elements of the result (partial sums hold splits of them)
     int Hp, Wp, OHp, OWp, pad_oh, pad_ow;
     bool unfold_w;          // forward / backward-data pass over x unfolded along w
+    int csplit;             // forward: channel chunks per kernel position (TabArgs::csplit)
     size_t off_unf;         // backward data, unfolded: the unfolded input's gradient
 };
 
@@ -1029,6 +1030,20 @@ bool fwd_unfolds(const ConvShape &s, int hp)
     return bytes < (int64_t(1) << 31);
 }
 
+// Channel chunks of the forward pass's taps (TabArgs::csplit): the taps run chunk-major, so that
+// kernel positions one after another read the same chunk's input records.  With all channels in
+// one tap, the records the rows in flight read per tap are the whole input (ResNet 3x3 64->64 at
+// 32x32, batch 128: 57 MB, against 8 x 4 MB of L2), and each tap re-reads them from beyond L2.  Up
+// to 4 chunks of a multiple of 16 channels (whole slabs; 8-step reduction chunks stay whole, so
+// splits are unchanged); measured 2-3% faster on 3x3 layers.  Unfolded inputs have one tap.
+int fwd_channel_chunks(const ConvShape &s, bool unfold)
+{
+    if (unfold) return 1;
+    for (int c = 4; c > 1; c /= 2)
+        if (s.ci % (16 * c) == 0) return c;
+    return 1;
+}
+
 // Channels of the unfolded x, kw * c, rounded up to whole step pairs.
 inline int unfolded_channels(const ConvShape &s) { return (s.kw * s.ci + 1) / 2 * 2; }
 
@@ -1100,6 +1115,7 @@ Plan plan_conv(const amsim_conv2d *d, int pass, int m_bits)
         const int64_t q = int64_t(v.kh) * v.kw * ceil_div(v.ci, 8);
         p.tile = choose_tab_tile(npix_out, s.co, q, 4, true, p.rl, 8, 1);
         plan_tab_split(p, q);
+        p.csplit = fwd_channel_chunks(s, p.unfold_w);
         p.b_ld = round_up(s.co, tab_cols(p.tile));
         p.a_elems = int64_t(s.n) * p.Hp * p.Wp * ((rec_c + 1) / 2) * 3;  // zero-bordered x as step-pair records
         p.out_elems = npix_out * s.co;
@@ -1216,6 +1232,7 @@ TabArgs tab_args(const Plan &p, char *ws, const uint32_t *A, int64_t a_elems, co
     a.splits = p.splits;
     a.chunks_per_split = p.chunks_per_split;
     a.out_elems = p.out_elems;
+    a.csplit = 1;
     return a;
 }
 
@@ -1436,6 +1453,7 @@ int approx_conv2d_fwd(const amsim_conv2d *desc, const float *x, const float *w, 
     TabArgs a = tab_args(p, ws, Xd, p.a_elems, Wd, out, int(rows), s.co);
     a.s = p.unfold_w ? unfolded_shape(s) : s;
     a.rec_c = p.unfold_w ? unfolded_channels(s) : s.ci;
+    a.csplit = p.csplit;
     dim3 grid(unsigned(ceil_div(rows, int64_t(64) * t.wr * t.tm)), unsigned(p.b_ld / tab_cols(t)),
               unsigned(p.splits));
     {

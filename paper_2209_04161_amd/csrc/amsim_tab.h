@@ -70,6 +70,7 @@ struct TabArgs {
     ConvShape s;
     int Hp, Wp;          // zero-padded x (FWD, BWD_WEIGHT)
     int rec_c;           // FWD: channels of x's record layout [n][hp][rec_c / 2][wp] (s.ci unless unfolded)
+    int csplit;          // FWD: channel chunks; taps run chunk-major (csplit divides s.ci into multiples of 8)
     int OHp, OWp, pad_oh, pad_ow;  // zero-padded dy (BWD_DATA)
     int tx, ty, tz;      // this workgroup's tile (row block, column block, phase/split); set on entry
 };
@@ -247,7 +248,7 @@ __device__ __forceinline__ int tab_taps(const TabArgs &a)
         const int nvw = kw0 < s.kw ? (s.kw - kw0 + s.sw - 1) / s.sw : 0;
         return nvh * nvw;
     } else {
-        return a.s.kh * a.s.kw;
+        return a.s.kh * a.s.kw * a.csplit;
     }
 }
 
@@ -256,7 +257,7 @@ template <int OP>
 __device__ __forceinline__ int tab_count(const TabArgs &a)
 {
     if constexpr (OP == OP_GEMM) return a.K;
-    else if constexpr (OP == OP_FWD) return a.s.ci;
+    else if constexpr (OP == OP_FWD) return a.s.ci / a.csplit;
     else if constexpr (OP == OP_BWD_DATA) return a.s.co;
     else return a.s.ow;
 }
@@ -274,12 +275,15 @@ __device__ __forceinline__ TabTap tab_tap_raw(const TabArgs &a, int tap)
         t.bbase = 0;
         t.pbase = 0;
     } else if constexpr (OP == OP_FWD) {
-        const int kh = tap / s.kw, kw = tap % s.kw;
-        t.count = s.ci;
-        t.ubase = kh * s.ci * a.Wp + kw;
+        // chunk-major: every kernel position over one chunk of channels, then the next chunk, so
+        // that the records one tap reads are read again by the next taps while still in L2
+        const int kk = tap % (s.kh * s.kw), chunk = tap / (s.kh * s.kw);
+        const int kh = kk / s.kw, kw = kk % s.kw, cnt = s.ci / a.csplit, c0 = chunk * cnt;
+        t.count = cnt;
+        t.ubase = (kh * s.ci + c0) * a.Wp + kw;
         t.ustride = a.Wp;
-        t.bbase = tap * s.ci;
-        t.pbase = kh * ((a.rec_c + 1) / 2) * a.Wp + kw;
+        t.bbase = kk * s.ci + c0;
+        t.pbase = (kh * ((a.rec_c + 1) / 2) + c0 / 2) * a.Wp + kw;
     } else if constexpr (OP == OP_BWD_DATA) {
         const int ph = tab_phase(a) / s.sw, pw = tab_phase(a) % s.sw;
         const int kh0 = (ph + s.pt) % s.sh, kw0 = (pw + s.pl) % s.sw;

@@ -348,6 +348,9 @@ CONV_CASES = [
     W.conv_desc(1, 3, 1100, 8, 5, 3, 3, 1, 1),   # few channels, but a row too long to unfold along w
     W.conv_desc(2, 7, 9, 5, 6, 1, 4, 1, 3, pads=(0, 0, 2, 1)),  # 1 x 4 kernel, unfolded into 20 channels
     dict(W.conv_desc(2, 8, 11, 3, 4, 3, 5, 1, 2), stride_w=2),   # unfolded with different strides
+    W.conv_desc(2, 9, 7, 32, 10, 3, 3, 1, 1),    # forward taps in 2 channel chunks
+    W.conv_desc(1, 6, 5, 64, 12, 3, 2, 2, pads=(1, 0, 0, 1)),   # 4 chunks, stride 2, asymmetric pads
+    W.conv_desc(1, 3, 3, 256, 8, 3, 3, 1, 1),    # 4 chunks of 64 with a split reduction (9 rows)
 ]
 
 
