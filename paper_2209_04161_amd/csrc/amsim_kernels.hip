@@ -901,7 +901,7 @@ struct Plan {
     int64_t out_elems;      // elements of the result (partial sums hold splits of them)
     int Hp, Wp, OHp, OWp, pad_oh, pad_ow;
     bool unfold_w;          // forward / backward-data pass over x unfolded along w
-    int csplit;             // forward: channel chunks per kernel position (TabArgs::csplit)
+    int csplit;             // forward / backward data: channel chunks per kernel position (TabArgs::csplit)
     size_t off_unf;         // backward data, unfolded: the unfolded input's gradient
 };
 
@@ -1044,6 +1044,16 @@ int fwd_channel_chunks(const ConvShape &s, bool unfold)
     return 1;
 }
 
+// Channel chunks of the backward-data pass's taps, over its output-gradient channels, for the same
+// reason as the forward pass's: up to 8 chunks of a multiple of 16 channels (measured: ResNet 3x3
+// 3.5% and ResNet-50 3x3 256->256 3% faster).
+int bwd_data_channel_chunks(const ConvShape &s)
+{
+    for (int c = 8; c > 1; c /= 2)
+        if (s.co % (16 * c) == 0) return c;
+    return 1;
+}
+
 // Channels of the unfolded x, kw * c, rounded up to whole step pairs.
 inline int unfolded_channels(const ConvShape &s) { return (s.kw * s.ci + 1) / 2 * 2; }
 
@@ -1128,6 +1138,7 @@ Plan plan_conv(const amsim_conv2d *d, int pass, int m_bits)
         const int64_t q = ceil_div(s.kh, s.sh) * ceil_div(s.kw, s.sw) * ceil_div(s.co, 8);  // largest phase
         p.tile = choose_tab_tile(rows, s.ci, q, 4, true, p.rl, 4, int64_t(s.sh) * s.sw);  // 8-row tiles spill here
         plan_tab_split(p, q);
+        p.csplit = bwd_data_channel_chunks(s);
         p.b_ld = round_up(s.ci, tab_cols(p.tile));
         int top, bottom, left, right;
         bwd_data_dy_pads(s, top, bottom, left, right);
@@ -1488,6 +1499,7 @@ static int bwd_data_run(const amsim_conv2d *desc, const Plan &p, const float *dy
     float *out = p.splits > 1 ? reinterpret_cast<float *>(ws + p.off_part) : dx;
     TabArgs a = tab_args(p, ws, Dyd, p.a_elems, Wtd, out, int(rows), s.ci);
     a.s = s;
+    a.csplit = p.csplit;
     dim3 grid(unsigned(ceil_div(rows, int64_t(64) * t.wr * t.tm)), unsigned(p.b_ld / tab_cols(t)),
               unsigned(s.sh * s.sw * p.splits));
     {

@@ -70,7 +70,8 @@ struct TabArgs {
     ConvShape s;
     int Hp, Wp;          // zero-padded x (FWD, BWD_WEIGHT)
     int rec_c;           // FWD: channels of x's record layout [n][hp][rec_c / 2][wp] (s.ci unless unfolded)
-    int csplit;          // FWD: channel chunks; taps run chunk-major (csplit divides s.ci into multiples of 8)
+    int csplit;          // FWD / BWD_DATA: channel chunks; taps run chunk-major (csplit divides s.ci / s.co
+                         // into multiples of 8)
     int OHp, OWp, pad_oh, pad_ow;  // zero-padded dy (BWD_DATA)
     int tx, ty, tz;      // this workgroup's tile (row block, column block, phase/split); set on entry
 };
@@ -246,7 +247,7 @@ __device__ __forceinline__ int tab_taps(const TabArgs &a)
         const int kh0 = (ph + s.pt) % s.sh, kw0 = (pw + s.pl) % s.sw;
         const int nvh = kh0 < s.kh ? (s.kh - kh0 + s.sh - 1) / s.sh : 0;
         const int nvw = kw0 < s.kw ? (s.kw - kw0 + s.sw - 1) / s.sw : 0;
-        return nvh * nvw;
+        return nvh * nvw * a.csplit;
     } else {
         return a.s.kh * a.s.kw * a.csplit;
     }
@@ -258,7 +259,7 @@ __device__ __forceinline__ int tab_count(const TabArgs &a)
 {
     if constexpr (OP == OP_GEMM) return a.K;
     else if constexpr (OP == OP_FWD) return a.s.ci / a.csplit;
-    else if constexpr (OP == OP_BWD_DATA) return a.s.co;
+    else if constexpr (OP == OP_BWD_DATA) return a.s.co / a.csplit;
     else return a.s.ow;
 }
 
@@ -287,14 +288,16 @@ __device__ __forceinline__ TabTap tab_tap_raw(const TabArgs &a, int tap)
     } else if constexpr (OP == OP_BWD_DATA) {
         const int ph = tab_phase(a) / s.sw, pw = tab_phase(a) % s.sw;
         const int kh0 = (ph + s.pt) % s.sh, kw0 = (pw + s.pl) % s.sw;
-        const int nvw = (s.kw - kw0 + s.sw - 1) / s.sw;
-        const int kh = kh0 + (tap / nvw) * s.sh, kw = kw0 + (tap % nvw) * s.sw;
+        const int nvh = (s.kh - kh0 + s.sh - 1) / s.sh, nvw = (s.kw - kw0 + s.sw - 1) / s.sw;
+        const int kk = tap % (nvh * nvw), chunk = tap / (nvh * nvw);  // chunk-major, as FWD
+        const int kh = kh0 + (kk / nvw) * s.sh, kw = kw0 + (kk % nvw) * s.sw;
         const int dh = (ph + s.pt - kh) / s.sh, dw = (pw + s.pl - kw) / s.sw;  // exact divisions
-        t.count = s.co;
-        t.ubase = (dh + a.pad_oh) * s.co * a.OWp + dw + a.pad_ow;  // >= 0: the padding covers every dh, dw
+        const int cnt = s.co / a.csplit, c0 = chunk * cnt;
+        t.count = cnt;
+        t.ubase = ((dh + a.pad_oh) * s.co + c0) * a.OWp + dw + a.pad_ow;  // >= 0: the padding covers every dh, dw
         t.ustride = a.OWp;
-        t.bbase = (kh * s.kw + kw) * s.co;
-        t.pbase = (dh + a.pad_oh) * ((s.co + 1) / 2) * a.OWp + dw + a.pad_ow;
+        t.bbase = (kh * s.kw + kw) * s.co + c0;
+        t.pbase = ((dh + a.pad_oh) * ((s.co + 1) / 2) + c0 / 2) * a.OWp + dw + a.pad_ow;
     } else {
         const int n = tap / s.oh, oh = tap % s.oh;
         t.count = s.ow;

@@ -351,6 +351,10 @@ CONV_CASES = [
     W.conv_desc(2, 9, 7, 32, 10, 3, 3, 1, 1),    # forward taps in 2 channel chunks
     W.conv_desc(1, 6, 5, 64, 12, 3, 2, 2, pads=(1, 0, 0, 1)),   # 4 chunks, stride 2, asymmetric pads
     W.conv_desc(1, 3, 3, 256, 8, 3, 3, 1, 1),    # 4 chunks of 64 with a split reduction (9 rows)
+    W.conv_desc(2, 7, 6, 10, 32, 3, 3, 1, 1),    # backward-data taps in 2 output-channel chunks
+    W.conv_desc(1, 6, 5, 12, 64, 3, 2, 2, pads=(1, 0, 0, 1)),   # 4 chunks over stride phases
+    W.conv_desc(1, 4, 4, 8, 256, 3, 3, 1, 1),    # 8 chunks of 32 with a split reduction (16 rows)
+    W.conv_desc(2, 6, 9, 3, 32, 3, 3, 1, 1),     # unfolded backward data in 2 chunks
 ]
 
 
