@@ -226,6 +226,32 @@ def test_conv_zero_sums_keep_their_sign(B):
     ref, S = oracle.conv2d_bwd_weight(oracle.MITCHELL, m, p, x, dy)
     check(dw, ref, S, "bwd_weight")
 
+    # forward taps in 2 channel chunks (32 channels): the sign pass walks every chunk
+    p = W.conv_desc(1, 5, 6, 32, 10, 3, 3, 1, 0)
+    x = W.normal((1, 5, 6, 32), 1.0, 79)
+    w = W.normal((3, 3, 32, 10), 1.0, 80)
+    x[0, :, :4, :] = -0.0            # windows of output columns 0, 1 see -0 only
+    w[..., :4] = np.abs(w[..., :4])
+    w[..., 4:8] = -np.abs(w[..., 4:8])
+    w[..., 8] = -0.0
+    y = host(B.approx_conv2d_fwd(p, cuda(x), cuda(w), lut, m))
+    ref, S = oracle.conv2d_fwd(oracle.MITCHELL, m, p, x, w)
+    check(y, ref, S, "fwd in channel chunks")
+
+    # backward-data taps in 4 output-channel chunks (64 channels), 1 x 1 kernel
+    p = W.conv_desc(1, 4, 5, 6, 64, 1, 1, 1, 0)
+    dy = W.normal((1, 4, 5, 64), 1.0, 81)
+    w = W.normal((1, 1, 6, 64), 1.0, 82)
+    dy[0, :2] = -0.0
+    dy[0, 2, :2] = 0.0
+    w[0, 0, :2, :] = np.abs(w[0, 0, :2, :])
+    w[0, 0, 2:4, :] = -np.abs(w[0, 0, 2:4, :])
+    w[0, 0, 4, :] = -0.0
+    dx = host(B.approx_conv2d_bwd_data(p, cuda(dy), cuda(w), lut, m))
+    ref, S = oracle.conv2d_bwd_data(oracle.MITCHELL, m, p, dy, w)
+    check(dx, ref, S, "bwd_data in channel chunks")
+    assert np.signbit(ref[0, 0, 0, 0]) and not np.signbit(ref[0, 2, 0, 0])  # both zero signs occur
+
 
 def test_conv_unfolded_padding_channel_is_neutral(B):
     """The w-unfolded forward pass pads an odd kw * c to whole channel pairs; the padding channel
