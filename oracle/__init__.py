@@ -18,6 +18,14 @@ ASYM = 2          # test model: first operand truncated to M bits, second to M-1
 _lib = None
 
 
+class OrcOpts(ctypes.Structure):
+    _fields_ = [(name, ctypes.c_int) for name in ("model", "m_bits", "e_bits", "sat", "native")]
+
+
+def _opts(model_id, m_bits, e_bits=8, sat=False, native=False):
+    return OrcOpts(int(model_id), int(m_bits), int(e_bits), int(bool(sat)), int(bool(native)))
+
+
 class OrcConv(ctypes.Structure):
     _fields_ = [(name, ctypes.c_int) for name in (
         "n", "h", "w", "c_in", "c_out", "kh", "kw", "stride_h", "stride_w",
@@ -51,6 +59,22 @@ def lib():
     L.orc_conv2d.argtypes = [ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.POINTER(OrcConv),
                              f32p, f32p, i64p, i64, f32p, f64p]
     L.orc_conv2d.restype = ctypes.c_int
+    op = ctypes.POINTER(OrcOpts)
+    L.orc_mul_native.argtypes = [ctypes.c_float, ctypes.c_float]
+    L.orc_mul_native.restype = ctypes.c_float
+    L.orc_cast.argtypes = [ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_float]
+    L.orc_cast.restype = ctypes.c_float
+    L.orc_mul_fmt.argtypes = [ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_float, ctypes.c_float]
+    L.orc_mul_fmt.restype = ctypes.c_float
+    L.orc_mul_ex_array.argtypes = [op, i64, f32p, f32p, f32p]
+    L.orc_mul_ex_array.restype = None
+    L.orc_cast_array.argtypes = [ctypes.c_int, ctypes.c_int, ctypes.c_int, i64, f32p, f32p]
+    L.orc_cast_array.restype = None
+    L.orc_gemm_ex.argtypes = [op, ctypes.c_int, ctypes.c_int, i64, i64, i64, f32p, i64, f32p, i64, i64p, i64, f32p,
+                              f64p]
+    L.orc_gemm_ex.restype = None
+    L.orc_conv2d_ex.argtypes = [op, ctypes.c_int, ctypes.POINTER(OrcConv), f32p, f32p, i64p, i64, f32p, f64p]
+    L.orc_conv2d_ex.restype = ctypes.c_int
     L.orc_num_threads.argtypes = []
     L.orc_num_threads.restype = ctypes.c_int
     _lib = L
@@ -80,6 +104,32 @@ def mul(model: int, m_bits: int, a, b) -> np.ndarray:
     return c
 
 
+def mul_ex(model_id: int, m_bits: int, a, b, e_bits=8, sat=False, native=False) -> np.ndarray:
+    """Element-wise product of another multiplier: the table model through Algorithm 2 in a
+    (1, e_bits, m) format (e_bits = 8: mul), or the native FP32 multiply (model ignored)."""
+    a = _f32(a)
+    b = _f32(b)
+    assert a.shape == b.shape
+    c = np.empty_like(a)
+    o = _opts(model_id, m_bits, e_bits, sat, native)
+    lib().orc_mul_ex_array(ctypes.byref(o), a.size, _p(a, ctypes.c_float), _p(b, ctypes.c_float),
+                           _p(c, ctypes.c_float))
+    return c
+
+
+def cast(e_bits: int, x, sat=False, m_bits=7) -> np.ndarray:
+    """The exponent-casting function of a (1, e_bits, m_bits) format, element-wise."""
+    x = _f32(x)
+    y = np.empty_like(x)
+    lib().orc_cast_array(int(e_bits), int(bool(sat)), int(m_bits), x.size, _p(x, ctypes.c_float),
+                         _p(y, ctypes.c_float))
+    return y
+
+
+def mul_native(a: float, b: float) -> float:
+    return float(lib().orc_mul_native(a, b))
+
+
 def model(model_id: int, m_bits: int, a: float, b: float) -> float:
     return float(lib().orc_model(model_id, m_bits, a, b))
 
@@ -93,7 +143,7 @@ def lut(model_id: int, m_bits: int) -> np.ndarray:
     return out
 
 
-def gemm(model_id, m_bits, A, B, transa=False, transb=False, idx=None):
+def gemm(model_id, m_bits, A, B, transa=False, transb=False, idx=None, e_bits=8, sat=False, native=False):
     """C = op(A) @ op(B) with approximate products; returns (C float32, S float64 = sum |p|).
 
     A and B are 2-D float32 arrays as stored (op = transpose when the flag is set).  With
@@ -115,8 +165,9 @@ def gemm(model_id, m_bits, A, B, transa=False, transb=False, idx=None):
         C = np.empty(idx.size, np.float32)
         S = np.empty(idx.size, np.float64)
         ip, n = _p(idx, ctypes.c_int64), idx.size
-    lib().orc_gemm(model_id, m_bits, int(transa), int(transb), M, N, K, _p(A, ctypes.c_float), A.shape[1],
-                   _p(B, ctypes.c_float), B.shape[1], ip, n, _p(C, ctypes.c_float), _p(S, ctypes.c_double))
+    o = _opts(model_id, m_bits, e_bits, sat, native)
+    lib().orc_gemm_ex(ctypes.byref(o), int(transa), int(transb), M, N, K, _p(A, ctypes.c_float), A.shape[1],
+                      _p(B, ctypes.c_float), B.shape[1], ip, n, _p(C, ctypes.c_float), _p(S, ctypes.c_double))
     return C, S
 
 
@@ -126,7 +177,7 @@ def conv_out_hw(p: dict):
     return oh, ow
 
 
-def _conv(model_id, m_bits, pass_id, p, in0, in1, out_shape, idx):
+def _conv(model_id, m_bits, pass_id, p, in0, in1, out_shape, idx, e_bits=8, sat=False, native=False):
     d = OrcConv(**{k: int(p[k]) for k, _ in OrcConv._fields_})
     in0 = _f32(in0)
     in1 = _f32(in1)
@@ -139,23 +190,25 @@ def _conv(model_id, m_bits, pass_id, p, in0, in1, out_shape, idx):
         out = np.empty(idx.size, np.float32)
         S = np.empty(idx.size, np.float64)
         ip, n = _p(idx, ctypes.c_int64), idx.size
-    rc = lib().orc_conv2d(model_id, m_bits, pass_id, ctypes.byref(d), _p(in0, ctypes.c_float),
-                          _p(in1, ctypes.c_float), ip, n, _p(out, ctypes.c_float), _p(S, ctypes.c_double))
+    o = _opts(model_id, m_bits, e_bits, sat, native)
+    rc = lib().orc_conv2d_ex(ctypes.byref(o), pass_id, ctypes.byref(d), _p(in0, ctypes.c_float),
+                             _p(in1, ctypes.c_float), ip, n, _p(out, ctypes.c_float), _p(S, ctypes.c_double))
     assert rc == 0
     return out, S
 
 
-def conv2d_fwd(model_id, m_bits, p, x, w, idx=None):
-    """y[n,oh,ow,co] (NHWC) from x (NHWC) and w (HWIO); products amul(x, w)."""
+def conv2d_fwd(model_id, m_bits, p, x, w, idx=None, **mult):
+    """y[n,oh,ow,co] (NHWC) from x (NHWC) and w (HWIO); products amul(x, w).  mult: e_bits, sat,
+    native, as for gemm."""
     oh, ow = conv_out_hw(p)
-    return _conv(model_id, m_bits, 0, p, x, w, (p["n"], oh, ow, p["c_out"]), idx)
+    return _conv(model_id, m_bits, 0, p, x, w, (p["n"], oh, ow, p["c_out"]), idx, **mult)
 
 
-def conv2d_bwd_data(model_id, m_bits, p, dy, w, idx=None):
+def conv2d_bwd_data(model_id, m_bits, p, dy, w, idx=None, **mult):
     """dx[n,h,w,ci] from dy (NHWC) and w (HWIO); products amul(dy, w)."""
-    return _conv(model_id, m_bits, 1, p, dy, w, (p["n"], p["h"], p["w"], p["c_in"]), idx)
+    return _conv(model_id, m_bits, 1, p, dy, w, (p["n"], p["h"], p["w"], p["c_in"]), idx, **mult)
 
 
-def conv2d_bwd_weight(model_id, m_bits, p, x, dy, idx=None):
+def conv2d_bwd_weight(model_id, m_bits, p, x, dy, idx=None, **mult):
     """dw[kh,kw,ci,co] (HWIO) from x and dy; products amul(x, dy)."""
-    return _conv(model_id, m_bits, 2, p, x, dy, (p["kh"], p["kw"], p["c_in"], p["c_out"]), idx)
+    return _conv(model_id, m_bits, 2, p, x, dy, (p["kh"], p["kw"], p["c_in"], p["c_out"]), idx, **mult)

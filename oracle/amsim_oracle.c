@@ -38,6 +38,16 @@
  *   R6 The first operand of every product supplies the table's high index: forward
  *      amul(x, w), backward-data amul(dy, w), backward-weight amul(x, dy), GEMM amul(A, B).
  *
+ *   R11 Padding and dilation zeros are operands: Algorithm 3 and 4 build their column matrices
+ *       (IM2COL with the zero border; the error padded and dilated by the strides for the
+ *       preceding-layer gradient) and multiply every element, zeros included, so every tap of the
+ *       kernel window contributes amul(+0, weight) where the column matrix holds a zero -- a
+ *       signed zero for a finite weight, NaN for an Inf or NaN one.
+ *   R16 A (1, e, m) format with e < 8: orc_cast maps each operand into its range (see there), and
+ *       Algorithm 2 runs with the format's bias and top exponent field (orc_mul_fmt).
+ *   R17 The native multiply: IEEE FP32 products with denormals read and written as zero
+ *       (orc_mul_native).
+ *
  * Build: gcc -O2 -fopenmp -ffp-contract=off -fPIC -shared (no fast-math).
  */
 #include <math.h>
@@ -147,11 +157,128 @@ float orc_mul(int model, int m_bits, float a, float b)
     return orc_model(model, m_bits, a, b);
 }
 
+/* ---------------------------------------------------------------- other multipliers ------ */
+
+/*
+ * The native FP32 multiply (the paper's runs "with native multiply"): the IEEE product rounded to
+ * nearest-even, with denormal operands read as zero and a denormal result flushed to a signed
+ * zero, as the GPU's FP32 arithmetic does with denormals off.  (double)a * (double)b is exact for
+ * float operands, so one rounding to float gives the IEEE result; values from the largest float
+ * plus half an ulp on round to infinity.
+ */
+float orc_mul_native(float a, float b)
+{
+    if (orc_is_zero_field(a))
+        a = signbit(a) ? -0.0f : 0.0f;
+    if (orc_is_zero_field(b))
+        b = signbit(b) ? -0.0f : 0.0f;
+    double d = (double)a * (double)b;
+    if (isnan(d))
+        return NAN;
+    if (fabs(d) >= 0x1.ffffffp127)
+        return (d < 0) ? -INFINITY : INFINITY;
+    float r = (float)d;
+    if (r != 0.0f && fabsf(r) < 0x1p-126f)
+        r = signbit(r) ? -0.0f : 0.0f;
+    return r;
+}
+
+/*
+ * The exponent-casting function of a (1, e, m) format (Sec. "AMSim": e can range up to 8 given a
+ * casting function), reading taken here: bias beta = 2^(e-1) - 1, normal unbiased exponents
+ * 1 - beta .. beta (the top field reserved for Inf/NaN, as in FP32); a finite value above that
+ * range becomes a signed Inf, or with `sat` the largest finite value (2 - 2^-m) * 2^beta; a value
+ * below it (the format's denormals included) a signed zero; NaN, Inf and in-range values stay as
+ * they are (their mantissa is read through its top m bits by the multiplier).
+ */
+float orc_cast(int e_bits, int sat, int m_bits, float x)
+{
+    if (isnan(x) || isinf(x))
+        return x;
+    int neg = signbit(x) != 0;
+    if (orc_is_zero_field(x))
+        return neg ? -0.0f : 0.0f;
+    int beta = (1 << (e_bits - 1)) - 1;
+    int u = ilogbf(x);
+    if (u > beta) {
+        float big = sat ? (float)ldexp(2.0 - ldexp(1.0, -m_bits), beta) : INFINITY;
+        return neg ? -big : big;
+    }
+    if (u < 1 - beta)
+        return neg ? -0.0f : 0.0f;
+    return x;
+}
+
+/*
+ * Algorithm 2 for a (1, e, m) multiplier: both operands cast to the format, then the zero and
+ * infinity rules in the format's constants -- with Ea', Eb' the operands' e-bit exponent fields
+ * (unbiased exponent + beta), the un-normalised exponent Ea' + Eb' - beta <= 0 gives a signed zero
+ * (before the carry, as Algorithm 2 orders it), >= 2^e - 1 a signed infinity, and so does a carry
+ * that lifts it to 2^e - 1; otherwise the model's product, an FP32 value.  e = 8 is Algorithm 2
+ * itself (orc_mul).
+ */
+float orc_mul_fmt(int model, int m_bits, int e_bits, int sat, float a, float b)
+{
+    if (e_bits == 8)
+        return orc_mul(model, m_bits, a, b);
+    float ca = orc_cast(e_bits, sat, m_bits, a), cb = orc_cast(e_bits, sat, m_bits, b);
+    int neg = signbit(ca) != signbit(cb);
+    if (isnan(ca) || isnan(cb))
+        return NAN;
+    int za = orc_is_zero_field(ca), zb = orc_is_zero_field(cb);
+    int ia = isinf(ca) != 0, ib = isinf(cb) != 0;
+    if ((ia && zb) || (za && ib))
+        return NAN;
+    if (ia || ib)
+        return neg ? -INFINITY : INFINITY;
+    if (za || zb)
+        return neg ? -0.0f : 0.0f;
+    int beta = (1 << (e_bits - 1)) - 1, top = (1 << e_bits) - 1;
+    int ua = ilogbf(ca), ub = ilogbf(cb);
+    int un_normalized_exp = (ua + beta) + (ub + beta) - beta;
+    if (un_normalized_exp <= 0)
+        return neg ? -0.0f : 0.0f;
+    if (un_normalized_exp >= top)
+        return neg ? -INFINITY : INFINITY;
+    float c = orc_model(model, m_bits, ca, cb);
+    int carry = ilogbf(c) - (ua + ub);
+    if (un_normalized_exp + carry >= top)
+        return neg ? -INFINITY : INFINITY;
+    return c;
+}
+
+/* The multiplier of one call: the table's model through Algorithm 2 in a (1, e, m) format, or the
+ * native multiply. */
+typedef struct {
+    int model, m_bits, e_bits, sat, native;
+} orc_opts;
+
+static float orc_product(const orc_opts *o, float a, float b)
+{
+    if (o->native)
+        return orc_mul_native(a, b);
+    return orc_mul_fmt(o->model, o->m_bits, o->e_bits, o->sat, a, b);
+}
+
 void orc_mul_array(int model, int m_bits, int64_t n, const float *a, const float *b, float *c)
 {
 #pragma omp parallel for schedule(static)
     for (int64_t i = 0; i < n; ++i)
         c[i] = orc_mul(model, m_bits, a[i], b[i]);
+}
+
+void orc_mul_ex_array(const orc_opts *o, int64_t n, const float *a, const float *b, float *c)
+{
+#pragma omp parallel for schedule(static)
+    for (int64_t i = 0; i < n; ++i)
+        c[i] = orc_product(o, a[i], b[i]);
+}
+
+void orc_cast_array(int e_bits, int sat, int m_bits, int64_t n, const float *x, float *y)
+{
+#pragma omp parallel for schedule(static)
+    for (int64_t i = 0; i < n; ++i)
+        y[i] = orc_cast(e_bits, sat, m_bits, x[i]);
 }
 
 /*
@@ -191,14 +318,14 @@ int orc_lut(int model, int m_bits, uint32_t *out)
 /* ---------------------------------------------------------------- GEMM ------------------- */
 
 /* C = op(A) * op(B), row-major, product amul(A_ik, B_kj) (R6). */
-static float orc_gemm_one(int model, int m_bits, int transa, int transb, int64_t K, const float *A,
+static float orc_gemm_one(const orc_opts *o, int transa, int transb, int64_t K, const float *A,
                           int64_t lda, const float *B, int64_t ldb, int64_t i, int64_t j, double *sabs)
 {
     double acc = -0.0, s = 0.0;
     for (int64_t k = 0; k < K; ++k) {
         float a = transa ? A[k * lda + i] : A[i * lda + k];
         float b = transb ? B[j * ldb + k] : B[k * ldb + j];
-        float p = orc_mul(model, m_bits, a, b);
+        float p = orc_product(o, a, b);
         acc += (double)p;
         s += fabs((double)p);
     }
@@ -210,16 +337,23 @@ static float orc_gemm_one(int model, int m_bits, int transa, int transb, int64_t
  * If idx is NULL, computes all M*N outputs into C[i*N + j]; otherwise computes the outputs at
  * the flat indices idx[t] = i*N + j into C[t].  S receives the matching sums of |products|.
  */
-void orc_gemm(int model, int m_bits, int transa, int transb, int64_t M, int64_t N, int64_t K, const float *A,
-              int64_t lda, const float *B, int64_t ldb, const int64_t *idx, int64_t nidx, float *C, double *S)
+void orc_gemm_ex(const orc_opts *o, int transa, int transb, int64_t M, int64_t N, int64_t K, const float *A,
+                 int64_t lda, const float *B, int64_t ldb, const int64_t *idx, int64_t nidx, float *C, double *S)
 {
     int64_t total = idx ? nidx : M * N;
 #pragma omp parallel for schedule(dynamic, 16)
     for (int64_t t = 0; t < total; ++t) {
         int64_t flat = idx ? idx[t] : t;
         int64_t i = flat / N, j = flat % N;
-        C[t] = orc_gemm_one(model, m_bits, transa, transb, K, A, lda, B, ldb, i, j, &S[t]);
+        C[t] = orc_gemm_one(o, transa, transb, K, A, lda, B, ldb, i, j, &S[t]);
     }
+}
+
+void orc_gemm(int model, int m_bits, int transa, int transb, int64_t M, int64_t N, int64_t K, const float *A,
+              int64_t lda, const float *B, int64_t ldb, const int64_t *idx, int64_t nidx, float *C, double *S)
+{
+    orc_opts o = {model, m_bits, 8, 0, 0};
+    orc_gemm_ex(&o, transa, transb, M, N, K, A, lda, B, ldb, idx, nidx, C, S);
 }
 
 /* ---------------------------------------------------------------- convolution ----------- */
@@ -232,8 +366,9 @@ typedef struct {
 static int64_t orc_out_h(const orc_conv *p) { return (p->h + p->pad_top + p->pad_bottom - p->kh) / p->stride_h + 1; }
 static int64_t orc_out_w(const orc_conv *p) { return (p->w + p->pad_left + p->pad_right - p->kw) / p->stride_w + 1; }
 
-/* y[n,oh,ow,co] = sum_{kh,kw,ci} amul(x[n, oh*S+kh-Pt, ow*S+kw-Pl, ci], w[kh,kw,ci,co]) */
-static float orc_fwd_one(int model, int m_bits, const orc_conv *p, const float *x, const float *w, int64_t flat,
+/* y[n,oh,ow,co] = sum_{kh,kw,ci} amul(xpad[n, oh*S+kh-Pt, ow*S+kw-Pl, ci], w[kh,kw,ci,co]), xpad = x with
+ * its zero border (R11) */
+static float orc_fwd_one(const orc_opts *o, const orc_conv *p, const float *x, const float *w, int64_t flat,
                          double *sabs)
 {
     int64_t OH = orc_out_h(p), OW = orc_out_w(p);
@@ -246,12 +381,12 @@ static float orc_fwd_one(int model, int m_bits, const orc_conv *p, const float *
         for (int64_t kw = 0; kw < p->kw; ++kw) {
             int64_t ih = oh * p->stride_h + kh - p->pad_top;
             int64_t iw = ow * p->stride_w + kw - p->pad_left;
-            if (ih < 0 || ih >= p->h || iw < 0 || iw >= p->w)
-                continue; /* padded tap: the operand is zero, its product contributes +-0 */
+            int inside = ih >= 0 && ih < p->h && iw >= 0 && iw < p->w;
             for (int64_t ci = 0; ci < p->c_in; ++ci) {
-                float a = x[((n * p->h + ih) * p->w + iw) * p->c_in + ci];
+                /* a padded tap multiplies the zero the column matrix holds there (R11) */
+                float a = inside ? x[((n * p->h + ih) * p->w + iw) * p->c_in + ci] : 0.0f;
                 float b = w[((kh * p->kw + kw) * p->c_in + ci) * p->c_out + co];
-                float q = orc_mul(model, m_bits, a, b);
+                float q = orc_product(o, a, b);
                 acc += (double)q;
                 s += fabs((double)q);
             }
@@ -261,9 +396,11 @@ static float orc_fwd_one(int model, int m_bits, const orc_conv *p, const float *
     return (float)acc;
 }
 
-/* dx[n,h,w,ci] = sum over (kh,kw,co) and output positions (oh,ow) that read (h,w) in the
- * forward pass, i.e. oh*S+kh-Pt == h and ow*S+kw-Pl == w, of amul(dy[n,oh,ow,co], w[kh,kw,ci,co]) */
-static float orc_bwd_data_one(int model, int m_bits, const orc_conv *p, const float *dy, const float *w,
+/* dx[n,h,w,ci] = sum over every (kh,kw,co) of amul(E[n, h+Pt-kh, w+Pl-kw, co], w[kh,kw,ci,co]), E the
+ * error dilated by the strides and zero-padded (Algorithm 4's PaddedDilatedErrors, R11):
+ * E[n,p,q,co] = dy[n,p/Sh,q/Sw,co] where p, q are multiples of the strides and p/Sh < OH, q/Sw < OW
+ * (the output positions that read (h,w) in the forward pass), +0 elsewhere. */
+static float orc_bwd_data_one(const orc_opts *o, const orc_conv *p, const float *dy, const float *w,
                               int64_t flat, double *sabs)
 {
     int64_t OH = orc_out_h(p), OW = orc_out_w(p);
@@ -274,20 +411,15 @@ static float orc_bwd_data_one(int model, int m_bits, const orc_conv *p, const fl
     double acc = -0.0, s = 0.0;
     for (int64_t kh = 0; kh < p->kh; ++kh) {
         for (int64_t kw = 0; kw < p->kw; ++kw) {
-            for (int64_t oh = 0; oh < OH; ++oh) {
-                if (oh * p->stride_h + kh - p->pad_top != ih)
-                    continue;
-                for (int64_t ow = 0; ow < OW; ++ow) {
-                    if (ow * p->stride_w + kw - p->pad_left != iw)
-                        continue;
-                    for (int64_t co = 0; co < p->c_out; ++co) {
-                        float a = dy[((n * OH + oh) * OW + ow) * p->c_out + co];
-                        float b = w[((kh * p->kw + kw) * p->c_in + ci) * p->c_out + co];
-                        float q = orc_mul(model, m_bits, a, b);
-                        acc += (double)q;
-                        s += fabs((double)q);
-                    }
-                }
+            int64_t ph = ih + p->pad_top - kh, pw = iw + p->pad_left - kw;
+            int64_t oh = ph >= 0 ? ph / p->stride_h : -1, ow = pw >= 0 ? pw / p->stride_w : -1;
+            int real = ph >= 0 && pw >= 0 && ph % p->stride_h == 0 && pw % p->stride_w == 0 && oh < OH && ow < OW;
+            for (int64_t co = 0; co < p->c_out; ++co) {
+                float a = real ? dy[((n * OH + oh) * OW + ow) * p->c_out + co] : 0.0f;
+                float b = w[((kh * p->kw + kw) * p->c_in + ci) * p->c_out + co];
+                float q = orc_product(o, a, b);
+                acc += (double)q;
+                s += fabs((double)q);
             }
         }
     }
@@ -295,8 +427,9 @@ static float orc_bwd_data_one(int model, int m_bits, const orc_conv *p, const fl
     return (float)acc;
 }
 
-/* dw[kh,kw,ci,co] = sum_{n,oh,ow, tap inside the image} amul(x[n, oh*S+kh-Pt, ow*S+kw-Pl, ci], dy[n,oh,ow,co]) */
-static float orc_bwd_weight_one(int model, int m_bits, const orc_conv *p, const float *x, const float *dy,
+/* dw[kh,kw,ci,co] = sum over every (n,oh,ow) of amul(xpad[n, oh*S+kh-Pt, ow*S+kw-Pl, ci], dy[n,oh,ow,co]),
+ * xpad = x with its zero border (R11) */
+static float orc_bwd_weight_one(const orc_opts *o, const orc_conv *p, const float *x, const float *dy,
                                 int64_t flat, double *sabs)
 {
     int64_t OH = orc_out_h(p), OW = orc_out_w(p);
@@ -310,11 +443,10 @@ static float orc_bwd_weight_one(int model, int m_bits, const orc_conv *p, const 
             for (int64_t ow = 0; ow < OW; ++ow) {
                 int64_t ih = oh * p->stride_h + kh - p->pad_top;
                 int64_t iw = ow * p->stride_w + kw - p->pad_left;
-                if (ih < 0 || ih >= p->h || iw < 0 || iw >= p->w)
-                    continue;
-                float a = x[((n * p->h + ih) * p->w + iw) * p->c_in + ci];
+                int inside = ih >= 0 && ih < p->h && iw >= 0 && iw < p->w;
+                float a = inside ? x[((n * p->h + ih) * p->w + iw) * p->c_in + ci] : 0.0f;
                 float b = dy[((n * OH + oh) * OW + ow) * p->c_out + co];
-                float q = orc_mul(model, m_bits, a, b);
+                float q = orc_product(o, a, b);
                 acc += (double)q;
                 s += fabs((double)q);
             }
@@ -327,8 +459,8 @@ static float orc_bwd_weight_one(int model, int m_bits, const orc_conv *p, const 
 /* pass: 0 forward (in0 = x, in1 = w, out = y), 1 backward-data (in0 = dy, in1 = w, out = dx),
  * 2 backward-weight (in0 = x, in1 = dy, out = dw).  idx/nidx select output elements by flat
  * index as in orc_gemm; NULL computes the whole output tensor. */
-int orc_conv2d(int model, int m_bits, int pass, const orc_conv *p, const float *in0, const float *in1,
-               const int64_t *idx, int64_t nidx, float *out, double *S)
+int orc_conv2d_ex(const orc_opts *o, int pass, const orc_conv *p, const float *in0, const float *in1,
+                  const int64_t *idx, int64_t nidx, float *out, double *S)
 {
     int64_t OH = orc_out_h(p), OW = orc_out_w(p);
     int64_t total;
@@ -346,13 +478,20 @@ int orc_conv2d(int model, int m_bits, int pass, const orc_conv *p, const float *
     for (int64_t t = 0; t < total; ++t) {
         int64_t flat = idx ? idx[t] : t;
         if (pass == 0)
-            out[t] = orc_fwd_one(model, m_bits, p, in0, in1, flat, &S[t]);
+            out[t] = orc_fwd_one(o, p, in0, in1, flat, &S[t]);
         else if (pass == 1)
-            out[t] = orc_bwd_data_one(model, m_bits, p, in0, in1, flat, &S[t]);
+            out[t] = orc_bwd_data_one(o, p, in0, in1, flat, &S[t]);
         else
-            out[t] = orc_bwd_weight_one(model, m_bits, p, in0, in1, flat, &S[t]);
+            out[t] = orc_bwd_weight_one(o, p, in0, in1, flat, &S[t]);
     }
     return 0;
+}
+
+int orc_conv2d(int model, int m_bits, int pass, const orc_conv *p, const float *in0, const float *in1,
+               const int64_t *idx, int64_t nidx, float *out, double *S)
+{
+    orc_opts o = {model, m_bits, 8, 0, 0};
+    return orc_conv2d_ex(&o, pass, p, in0, in1, idx, nidx, out, S);
 }
 
 int orc_num_threads(void)

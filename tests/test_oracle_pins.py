@@ -288,12 +288,13 @@ def test_conv_equals_torch_float64_for_exact_model(ci):
     m = 7
     x, w, dy = _conv_inputs(p, 20 + ci, m, m, m)
     y_ref, dx_ref, dw_ref = _torch_conv_passes(p, x, w, dy)
-    y, _ = oracle.conv2d_fwd(oracle.EXACT_TRUNC, m, p, x, w)
-    dx, _ = oracle.conv2d_bwd_data(oracle.EXACT_TRUNC, m, p, dy, w)
-    dw, _ = oracle.conv2d_bwd_weight(oracle.EXACT_TRUNC, m, p, x, dy)
-    for got, ref in ((y, y_ref), (dx, dx_ref), (dw, dw_ref)):
+    y, Sy = oracle.conv2d_fwd(oracle.EXACT_TRUNC, m, p, x, w)
+    dx, Sdx = oracle.conv2d_bwd_data(oracle.EXACT_TRUNC, m, p, dy, w)
+    dw, Sdw = oracle.conv2d_bwd_weight(oracle.EXACT_TRUNC, m, p, x, dy)
+    for got, ref, S in ((y, y_ref, Sy), (dx, dx_ref, Sdx), (dw, dw_ref, Sdw)):
         assert got.shape == ref.shape
-        assert np.allclose(got, ref, rtol=1e-6, atol=1e-6)
+        # exact products summed in double, rounded once to float32 (as the GEMM pin)
+        assert np.all(np.abs(got - ref) <= 1e-12 * S + np.abs(ref) * 2.0 ** -24)
 
 
 @pytest.mark.parametrize("ci", [1, 2])
@@ -328,3 +329,89 @@ def test_conv_sampled_indices_match_full():
     idx = np.array([1, dw.size - 1])
     dws, _ = oracle.conv2d_bwd_weight(oracle.MITCHELL, 7, p, x, dy, idx=idx)
     assert np.array_equal(dws, dw.reshape(-1)[idx])
+
+
+# ------------------------------------------------ the column-matrix formulation (Alg. 3 / 4)
+
+def _im2col(xpad, kh, kw, sh, sw, oh, ow):
+    """Column matrix [n * oh * ow][kh * kw * c] of a zero-bordered NHWC tensor (numpy)."""
+    n, _, _, c = xpad.shape
+    cols = np.empty((n, oh, ow, kh, kw, c), np.float32)
+    for i in range(kh):
+        for j in range(kw):
+            cols[:, :, :, i, j, :] = xpad[:, i:i + sh * (oh - 1) + 1:sh, j:j + sw * (ow - 1) + 1:sw, :]
+    return cols.reshape(n * oh * ow, kh * kw * c)
+
+
+def _pad(x, p):
+    return np.pad(x, ((0, 0), (p["pad_top"], p["pad_bottom"]), (p["pad_left"], p["pad_right"]), (0, 0)))
+
+
+def _specials(x, w, dy, rng):
+    """Inf/NaN weights and zero blocks, so that padded and dilated zeros decide NaN and zero signs."""
+    w = w.copy()
+    w.reshape(-1)[rng.choice(w.size, 2, replace=False)] = [np.inf, np.nan]
+    x = x.copy()
+    x[:, : x.shape[1] // 2] = -0.0
+    dy = dy.copy()
+    dy[:, :, : dy.shape[2] // 2] = 0.0
+    return x, w, dy
+
+
+def _bits_equal(a, b):
+    a = np.asarray(a, np.float32).reshape(-1)
+    b = np.asarray(b, np.float32).reshape(-1)
+    return np.all((a.view(np.uint32) == b.view(np.uint32)) | (np.isnan(a) & np.isnan(b)))
+
+
+@pytest.mark.parametrize("ci", range(len(CONV_CASES)))
+@pytest.mark.parametrize("special", [False, True])
+def test_conv_fwd_and_bwd_weight_are_gemms_over_the_column_matrix(ci, special):
+    """Algorithm 3 (forward = IM2COL(x) times the weights) and the first half of Algorithm 4
+    (weights gradient = IM2COL(x) transposed times the error), with the column matrix built by
+    numpy from the zero-bordered input: the oracle's direct loops give the same sums bit for bit
+    (same summation order), including NaN from Inf weights at padded taps and zero signs."""
+    p = CONV_CASES[ci]
+    x, w, dy = _conv_inputs(p, 70 + ci, 23, 23, 23)
+    if special:
+        x, w, dy = _specials(x, w, dy, np.random.default_rng(ci))
+    oh, ow = W.conv_out_hw(p)
+    cols = _im2col(_pad(x, p), p["kh"], p["kw"], p["stride_h"], p["stride_w"], oh, ow)
+    y, _ = oracle.conv2d_fwd(oracle.MITCHELL, 7, p, x, w)
+    y_g, _ = oracle.gemm(oracle.MITCHELL, 7, cols, w.reshape(-1, p["c_out"]))
+    assert _bits_equal(y, y_g)
+    dw, _ = oracle.conv2d_bwd_weight(oracle.MITCHELL, 7, p, x, dy)
+    dw_g, _ = oracle.gemm(oracle.MITCHELL, 7, cols, dy.reshape(-1, p["c_out"]), transa=True)
+    assert _bits_equal(dw, dw_g)
+
+
+@pytest.mark.parametrize("ci", range(len(CONV_CASES)))
+@pytest.mark.parametrize("special", [False, True])
+def test_conv_bwd_data_is_a_gemm_over_the_padded_dilated_error(ci, special):
+    """The second half of Algorithm 4: the error dilated by the strides (zeros between its
+    elements) and zero-padded, its column matrix built by numpy, times the weights transposed
+    (ci <-> co) -- summed over (kh, kw, co) in the oracle's order, so bit for bit equal."""
+    p = CONV_CASES[ci]
+    x, w, dy = _conv_inputs(p, 90 + ci, 23, 23, 23)
+    if special:
+        x, w, dy = _specials(x, w, dy, np.random.default_rng(10 + ci))
+    n, h, wd, c_in, c_out = p["n"], p["h"], p["w"], p["c_in"], p["c_out"]
+    kh, kw, sh, sw = p["kh"], p["kw"], p["stride_h"], p["stride_w"]
+    oh, ow = W.conv_out_hw(p)
+    # E[n, q, r, co]: the dilated error on a grid that every tap h + pt - kh (0 <= h < H) reaches
+    lo_h, lo_w = kh - 1, kw - 1
+    E = np.zeros((n, lo_h + h + p["pad_top"], lo_w + wd + p["pad_left"], c_out), np.float32)
+    for a in range(oh):
+        for b in range(ow):
+            if a * sh < h + p["pad_top"] and b * sw < wd + p["pad_left"]:
+                E[:, lo_h + a * sh, lo_w + b * sw, :] = dy[:, a, b, :]
+    cols = np.empty((n, h, wd, kh, kw, c_out), np.float32)
+    for i in range(kh):
+        for j in range(kw):
+            # element (h, w) of tap (i, j) is E at h + pt - i, w + pl - j
+            cols[:, :, :, i, j, :] = E[:, lo_h + p["pad_top"] - i:lo_h + p["pad_top"] - i + h,
+                                       lo_w + p["pad_left"] - j:lo_w + p["pad_left"] - j + wd, :]
+    wt = np.ascontiguousarray(w.transpose(0, 1, 3, 2)).reshape(kh * kw * c_out, c_in)
+    dx, _ = oracle.conv2d_bwd_data(oracle.MITCHELL, 7, p, dy, w)
+    dx_g, _ = oracle.gemm(oracle.MITCHELL, 7, cols.reshape(n * h * wd, -1), wt)
+    assert _bits_equal(dx, dx_g)
