@@ -10,7 +10,7 @@
  *
  * Conventions for every entry point:
  *   - Return value: AMSIM_OK (0) or a negative AMSIM_ERR_* code.  Nothing throws across the
- *     ABI and nothing prints.  On error no output is written and nothing is launched.
+ *     ABI and nothing prints.
  *   - "device" pointers are HIP device allocations owned by the caller (e.g. torch tensors);
  *     "host" pointers are ordinary host memory owned by the caller.  Device pointers must be
  *     4-byte aligned; the library allocates nothing and frees nothing.
@@ -28,6 +28,9 @@
  *     it to 255, else sign | (Ea + Eb - 127 + carry) << 23 | mantissa.
  *   - Sums start from -0.0 and are FP32 with denormal results flushed to zero; summation
  *     order is unspecified (the results of one call are deterministic run to run).
+ *   - Errors in the arguments (AMSIM_ERR_INVALID_ARG, _UNSUPPORTED, _WORKSPACE) are found before
+ *     anything is launched.  AMSIM_ERR_HIP reports a failed launch; kernels the call enqueued
+ *     before it may still run, and the output is then unspecified.
  */
 #ifndef AMSIM_H
 #define AMSIM_H
@@ -165,12 +168,65 @@ int approx_conv2d_bwd_weight(const amsim_conv2d *desc, const float *x, const flo
                              const uint32_t *lut, int m_bits, void *workspace, size_t workspace_bytes,
                              void *stream);
 
+/* ----------------------------------------------------------------- options --------------
+ * The _ex variants of the GEMM, convolution and element-wise calls take the multiplier to
+ * simulate (NULL = the defaults, which are what the plain calls do):
+ *   multiply  AMSIM_MULTIPLY_TABLE: every product approximate, from the table (AMSim, the default);
+ *             AMSIM_MULTIPLY_NATIVE: the native FP32 multiply in the same kernels (the paper's
+ *             "AT with native multiply" configuration, Tables of training / inference time):
+ *             products are IEEE FP32 (denormal operands and results flushed to zero), each fused
+ *             into the sum; lut and m_bits are then ignored (lut may be NULL) and e_bits must be 8.
+ *   e_bits    exponent bits e of the simulated (1, e, m) format, 2..8 (Sec. "AMSim": e can range up
+ *             to 8 given an exponent-casting function; 8 = FP32's exponent, the default).  With
+ *             e < 8, bias beta = 2^(e-1) - 1, every operand is first cast to the format (below;
+ *             values in its range are unchanged), and Algorithm 2 runs in the format's constants:
+ *             zero if Ea + Eb - beta <= 0 (before the carry), Inf if Ea + Eb - beta (+ carry)
+ *             reaches 2^e - 1, else the product, returned as an FP32 value and summed in FP32.
+ *             e = 1 (no finite non-zero value once the top field is reserved for Inf/NaN) is
+ *             AMSIM_ERR_UNSUPPORTED.
+ *   exp_cast  the exponent-casting function: a finite value whose unbiased exponent exceeds beta
+ *             becomes a signed Inf (AMSIM_CAST_INF, the default) or the format's largest finite
+ *             value (2 - 2^-M) * 2^beta (AMSIM_CAST_SATURATE); one below 1 - beta (the format's
+ *             denormals included) a signed zero.
+ * Unknown values give AMSIM_ERR_INVALID_ARG. */
+typedef struct amsim_options {
+    int multiply;
+    int e_bits;
+    int exp_cast;
+} amsim_options;
+
+#define AMSIM_MULTIPLY_TABLE 0
+#define AMSIM_MULTIPLY_NATIVE 1
+#define AMSIM_CAST_INF 0
+#define AMSIM_CAST_SATURATE 1
+
+/* The calls above with options (same arguments, same workspace sizes). */
+int approx_gemm_ex(const amsim_options *opt, int trans_a, int trans_b, int64_t m, int64_t n, int64_t k,
+                   const float *A, int64_t lda, const float *B, int64_t ldb, float *C, int64_t ldc, const uint32_t *lut,
+                   int m_bits, void *workspace, size_t workspace_bytes, void *stream);
+int approx_conv2d_fwd_ex(const amsim_options *opt, const amsim_conv2d *desc, const float *x, const float *w, float *y,
+                         const uint32_t *lut, int m_bits, void *workspace, size_t workspace_bytes, void *stream);
+int approx_conv2d_bwd_data_ex(const amsim_options *opt, const amsim_conv2d *desc, const float *dy, const float *w,
+                              float *dx, const uint32_t *lut, int m_bits, void *workspace, size_t workspace_bytes,
+                              void *stream);
+int approx_conv2d_bwd_weight_ex(const amsim_options *opt, const amsim_conv2d *desc, const float *x, const float *dy,
+                                float *dw, const uint32_t *lut, int m_bits, void *workspace, size_t workspace_bytes,
+                                void *stream);
+
+/* amsim_cast_exponent: the exponent-casting function on its own, y[i] = x[i] cast to the
+ * (1, e_bits, m_bits) format as described above, as an FP32 value (device x, y; y may alias x;
+ * n == 0: nothing is done).  Errors as for the options, plus m_bits outside [1, 11]. */
+int amsim_cast_exponent(int e_bits, int exp_cast, int m_bits, int64_t n, const float *x, float *y, void *stream);
+
 /* ----------------------------------------------------------------- element-wise --------
  * approx_mul_ew: c[i] = amul(a[i], b[i]) for i < n -- Algorithm 2 exactly as the GEMM and
  * convolution kernels evaluate it, exposed so that single products can be checked bit for
  * bit.  a, b, c, lut: device memory (c may alias neither input).  n == 0: nothing is done. */
 int approx_mul_ew(int64_t n, const float *a, const float *b, float *c, const uint32_t *lut, int m_bits,
                   void *stream);
+/* The same with options (multiply must be AMSIM_MULTIPLY_TABLE, else AMSIM_ERR_UNSUPPORTED). */
+int approx_mul_ew_ex(const amsim_options *opt, int64_t n, const float *a, const float *b, float *c,
+                     const uint32_t *lut, int m_bits, void *stream);
 
 /* ----------------------------------------------------------------- kernel timing -------
  * Measurement support (no paper counterpart; the paper reports per-batch wall time only).
@@ -189,6 +245,11 @@ int approx_mul_ew(int64_t n, const float *a, const float *b, float *c, const uin
 #define AMSIM_KERNEL_CONV_FWD 1
 #define AMSIM_KERNEL_CONV_BWD_DATA 2
 #define AMSIM_KERNEL_CONV_BWD_WEIGHT 3
+/* the same kernels with the native multiply (AMSIM_MULTIPLY_NATIVE) */
+#define AMSIM_KERNEL_GEMM_NATIVE 4
+#define AMSIM_KERNEL_CONV_FWD_NATIVE 5
+#define AMSIM_KERNEL_CONV_BWD_DATA_NATIVE 6
+#define AMSIM_KERNEL_CONV_BWD_WEIGHT_NATIVE 7
 int amsim_profile_start(int max_launches);
 int amsim_profile_stop(void);
 int amsim_profile_read(int kind, int *launches, double *total_ms);

@@ -30,7 +30,13 @@ AMSIM_KERNEL_GEMM = 0
 AMSIM_KERNEL_CONV_FWD = 1
 AMSIM_KERNEL_CONV_BWD_DATA = 2
 AMSIM_KERNEL_CONV_BWD_WEIGHT = 3
-KERNEL_KINDS = {"gemm": 0, "conv_fwd": 1, "conv_bwd_data": 2, "conv_bwd_weight": 3}
+KERNEL_KINDS = {"gemm": 0, "conv_fwd": 1, "conv_bwd_data": 2, "conv_bwd_weight": 3,
+                "gemm_native": 4, "conv_fwd_native": 5, "conv_bwd_data_native": 6, "conv_bwd_weight_native": 7}
+
+AMSIM_MULTIPLY_TABLE = 0
+AMSIM_MULTIPLY_NATIVE = 1
+AMSIM_CAST_INF = 0
+AMSIM_CAST_SATURATE = 1
 
 MODEL_FN = ctypes.CFUNCTYPE(ctypes.c_float, ctypes.c_float, ctypes.c_float, ctypes.c_void_p)
 
@@ -45,6 +51,20 @@ class amsim_conv2d(ctypes.Structure):
     _fields_ = [(name, ctypes.c_int) for name in (
         "n", "h", "w", "c_in", "c_out", "kh", "kw", "stride_h", "stride_w",
         "pad_top", "pad_bottom", "pad_left", "pad_right")]
+
+
+class amsim_options(ctypes.Structure):
+    _fields_ = [("multiply", ctypes.c_int), ("e_bits", ctypes.c_int), ("exp_cast", ctypes.c_int)]
+
+
+def options(multiply="table", e_bits=8, exp_cast="inf") -> amsim_options:
+    """The _ex calls' options: multiply "table" (AMSim) or "native"; e_bits of the (1, e, m)
+    format; exp_cast "inf" or "saturate"."""
+    mult = {"table": AMSIM_MULTIPLY_TABLE, "native": AMSIM_MULTIPLY_NATIVE}
+    cast = {"inf": AMSIM_CAST_INF, "saturate": AMSIM_CAST_SATURATE}
+    if multiply not in mult or exp_cast not in cast:
+        raise ValueError("multiply must be 'table' or 'native', exp_cast 'inf' or 'saturate'")
+    return amsim_options(mult[multiply], int(e_bits), cast[exp_cast])
 
 
 _lib = None
@@ -68,6 +88,7 @@ def lib():
     u32p = ctypes.POINTER(ctypes.c_uint32)
     szp = ctypes.POINTER(ctypes.c_size_t)
     cp = ctypes.POINTER(amsim_conv2d)
+    op = ctypes.POINTER(amsim_options)
     sigs = {
         "amsim_status_string": ([ctypes.c_int], ctypes.c_char_p),
         "amsim_version": ([], ctypes.c_int),
@@ -84,6 +105,13 @@ def lib():
         "approx_conv2d_bwd_data": ([cp, vp, vp, vp, vp, ctypes.c_int, vp, sz, vp], ctypes.c_int),
         "approx_conv2d_bwd_weight": ([cp, vp, vp, vp, vp, ctypes.c_int, vp, sz, vp], ctypes.c_int),
         "approx_mul_ew": ([i64, vp, vp, vp, vp, ctypes.c_int, vp], ctypes.c_int),
+        "approx_gemm_ex": ([op, ctypes.c_int, ctypes.c_int, i64, i64, i64, vp, i64, vp, i64, vp, i64, vp,
+                            ctypes.c_int, vp, sz, vp], ctypes.c_int),
+        "approx_conv2d_fwd_ex": ([op, cp, vp, vp, vp, vp, ctypes.c_int, vp, sz, vp], ctypes.c_int),
+        "approx_conv2d_bwd_data_ex": ([op, cp, vp, vp, vp, vp, ctypes.c_int, vp, sz, vp], ctypes.c_int),
+        "approx_conv2d_bwd_weight_ex": ([op, cp, vp, vp, vp, vp, ctypes.c_int, vp, sz, vp], ctypes.c_int),
+        "approx_mul_ew_ex": ([op, i64, vp, vp, vp, vp, ctypes.c_int, vp], ctypes.c_int),
+        "amsim_cast_exponent": ([ctypes.c_int, ctypes.c_int, ctypes.c_int, i64, vp, vp, vp], ctypes.c_int),
         "approx_gemm_direct": ([ctypes.c_int, ctypes.c_int, i64, i64, i64, vp, i64, vp, i64, vp, i64, vp],
                                ctypes.c_int),
         "amsim_profile_start": ([ctypes.c_int], ctypes.c_int),
@@ -179,16 +207,32 @@ def device_lut(table: np.ndarray, device="cuda"):
     return torch.from_numpy(np.ascontiguousarray(table, dtype=np.uint32).view(np.int32)).to(device)
 
 
-def _check_f32(t, name):
+def _check_f32(t, name, shape=None, device=None):
     torch = _torch()
     if t.dtype != torch.float32 or not t.is_cuda or not t.is_contiguous():
         raise ValueError("%s must be a contiguous float32 CUDA tensor" % name)
+    if shape is not None and tuple(t.shape) != tuple(shape):
+        raise ValueError("%s has shape %s, the call needs %s" % (name, tuple(t.shape), tuple(shape)))
+    if device is not None and t.device != device:
+        raise ValueError("%s is on %s, the call's operands on %s" % (name, t.device, device))
 
 
-def _check_lut(lut, m_bits):
+def _check_lut(lut, m_bits, device=None, native=False):
     torch = _torch()
+    if native and lut is None:
+        return
     if lut.dtype not in (torch.int32,) or not lut.is_cuda or lut.numel() < (1 << (2 * m_bits)):
         raise ValueError("lut must be an int32 CUDA tensor of 2^(2M) entries")
+    if device is not None and lut.device != device:
+        raise ValueError("lut is on %s, the call's operands on %s" % (lut.device, device))
+
+
+def _check_workspace(ws, nbytes, device):
+    torch = _torch()
+    if ws.dtype != torch.uint8 or not ws.is_cuda or not ws.is_contiguous() or ws.device != device:
+        raise ValueError("workspace must be a contiguous uint8 CUDA tensor on %s" % device)
+    if ws.numel() < nbytes:
+        raise ValueError("workspace holds %d bytes, the call needs %d" % (ws.numel(), nbytes))
 
 
 def amsim_gemm_workspace_size(trans_a, trans_b, m, n, k, m_bits) -> int:
@@ -203,12 +247,13 @@ def _workspace(nbytes, device):
     return torch.empty(max(int(nbytes), 1), dtype=torch.uint8, device=device)
 
 
-def approx_gemm(A, B, lut, m_bits, trans_a=False, trans_b=False, out=None, workspace=None):
-    """C = op(A) @ op(B) with approximate products (row-major float32 CUDA tensors)."""
+def _gemm_args(A, B, lut, m_bits, trans_a, trans_b, out, workspace, native=False):
     torch = _torch()
     _check_f32(A, "A")
-    _check_f32(B, "B")
-    _check_lut(lut, m_bits)
+    _check_f32(B, "B", device=A.device)
+    _check_lut(lut, m_bits, A.device, native)
+    if A.dim() != 2 or B.dim() != 2:
+        raise ValueError("A and B must be 2-D")
     m = A.shape[1] if trans_a else A.shape[0]
     k = A.shape[0] if trans_a else A.shape[1]
     kb = B.shape[1] if trans_b else B.shape[0]
@@ -217,13 +262,35 @@ def approx_gemm(A, B, lut, m_bits, trans_a=False, trans_b=False, out=None, works
         raise ValueError("inner dimensions differ")
     if out is None:
         out = torch.empty((m, n), dtype=torch.float32, device=A.device)
-    ldc = out.stride(0) if out.dim() == 2 else n
-    ws_bytes = amsim_gemm_workspace_size(trans_a, trans_b, m, n, k, m_bits)
+    if (out.dtype != torch.float32 or out.device != A.device or out.dim() != 2 or tuple(out.shape) != (m, n)
+            or (m > 0 and n > 1 and out.stride(1) != 1) or (m > 1 and out.stride(0) < n)):
+        raise ValueError("out must be a float32 (%d, %d) tensor on %s with unit column stride" % (m, n, A.device))
+    ws_bytes = amsim_gemm_workspace_size(trans_a, trans_b, m, n, k, m_bits if not native else 7)
     if workspace is None:
         workspace = _workspace(ws_bytes, A.device)
+    _check_workspace(workspace, ws_bytes, A.device)
+    ldc = out.stride(0) if m > 1 else n
+    return m, n, k, out, ldc, workspace
+
+
+def approx_gemm(A, B, lut, m_bits, trans_a=False, trans_b=False, out=None, workspace=None):
+    """C = op(A) @ op(B) with approximate products (row-major float32 CUDA tensors)."""
+    m, n, k, out, ldc, workspace = _gemm_args(A, B, lut, m_bits, trans_a, trans_b, out, workspace)
     _check(lib().approx_gemm(int(trans_a), int(trans_b), m, n, k, _ptr(A), A.shape[1], _ptr(B), B.shape[1],
                              _ptr(out), ldc, _ptr(lut), int(m_bits), _ptr(workspace), workspace.numel(), _stream()),
            "approx_gemm")
+    return out
+
+
+def approx_gemm_ex(A, B, lut, m_bits, trans_a=False, trans_b=False, out=None, workspace=None, multiply="table",
+                   e_bits=8, exp_cast="inf"):
+    """approx_gemm with options (see options())."""
+    opt = options(multiply, e_bits, exp_cast)
+    native = multiply == "native"
+    m, n, k, out, ldc, workspace = _gemm_args(A, B, lut, m_bits, trans_a, trans_b, out, workspace, native)
+    _check(lib().approx_gemm_ex(ctypes.byref(opt), int(trans_a), int(trans_b), m, n, k, _ptr(A), A.shape[1], _ptr(B),
+                                B.shape[1], _ptr(out), ldc, _ptr(lut), int(m_bits), _ptr(workspace),
+                                workspace.numel(), _stream()), "approx_gemm_ex")
     return out
 
 
@@ -232,7 +299,7 @@ def approx_gemm_direct(A, B, mode, m_bits=7, out=None):
     multiplier on the top m_bits mantissa bits, computed from the operands' bits)."""
     torch = _torch()
     _check_f32(A, "A")
-    _check_f32(B, "B")
+    _check_f32(B, "B", device=A.device)
     modes = {"native": AMSIM_DIRECT_NATIVE, "mitchell": AMSIM_DIRECT_MITCHELL}
     if mode not in modes:
         raise ValueError("mode must be 'native' or 'mitchell'")
@@ -242,6 +309,9 @@ def approx_gemm_direct(A, B, mode, m_bits=7, out=None):
     n = B.shape[1]
     if out is None:
         out = torch.empty((m, n), dtype=torch.float32, device=A.device)
+    if (out.dtype != torch.float32 or out.device != A.device or tuple(out.shape) != (m, n)
+            or (n > 1 and out.stride(1) != 1) or (m > 1 and out.stride(0) < n)):
+        raise ValueError("out must be a float32 (%d, %d) tensor on %s with unit column stride" % (m, n, A.device))
     _check(lib().approx_gemm_direct(modes[mode], int(m_bits), m, n, k, _ptr(A), A.stride(0), _ptr(B), B.stride(0),
                                     _ptr(out), out.stride(0), _stream()), "approx_gemm_direct")
     return out
@@ -265,62 +335,121 @@ def amsim_conv2d_workspace_size(desc: dict, pass_id: int, m_bits: int) -> int:
     return b.value
 
 
-def _conv_call(fn_name, pass_id, desc, in0, in1, out, lut, m_bits, workspace):
+def _conv_shapes(desc):
+    oh, ow = conv_out_hw(desc)
+    x = (desc["n"], desc["h"], desc["w"], desc["c_in"])
+    w = (desc["kh"], desc["kw"], desc["c_in"], desc["c_out"])
+    y = (desc["n"], oh, ow, desc["c_out"])
+    return x, w, y
+
+
+def _conv_call(fn_name, pass_id, desc, in0, in1, out, lut, m_bits, workspace, opt=None):
+    native = opt is not None and opt.multiply == AMSIM_MULTIPLY_NATIVE
     s = conv_desc_struct(desc)
-    ws_bytes = amsim_conv2d_workspace_size(desc, pass_id, m_bits)
+    ws_bytes = amsim_conv2d_workspace_size(desc, pass_id, m_bits if not native else 7)
     if workspace is None:
         workspace = _workspace(ws_bytes, in0.device)
-    fn = getattr(lib(), fn_name)
-    _check(fn(ctypes.byref(s), _ptr(in0), _ptr(in1), _ptr(out), _ptr(lut), int(m_bits), _ptr(workspace),
-              workspace.numel(), _stream()), fn_name)
+    _check_workspace(workspace, ws_bytes, in0.device)
+    if opt is None:
+        fn = getattr(lib(), fn_name)
+        status = fn(ctypes.byref(s), _ptr(in0), _ptr(in1), _ptr(out), _ptr(lut), int(m_bits), _ptr(workspace),
+                    workspace.numel(), _stream())
+    else:
+        fn_name = fn_name + "_ex"
+        fn = getattr(lib(), fn_name)
+        status = fn(ctypes.byref(opt), ctypes.byref(s), _ptr(in0), _ptr(in1), _ptr(out), _ptr(lut), int(m_bits),
+                    _ptr(workspace), workspace.numel(), _stream())
+    _check(status, fn_name)
     return out
+
+
+def _conv_pass(pass_id, desc, in0, in1, lut, m_bits, out, workspace, opt):
+    torch = _torch()
+    xs, ws_, ys = _conv_shapes(desc)
+    shapes = {AMSIM_CONV_FWD: (("x", xs), ("w", ws_), ys), AMSIM_CONV_BWD_DATA: (("dy", ys), ("w", ws_), xs),
+              AMSIM_CONV_BWD_WEIGHT: (("x", xs), ("dy", ys), ws_)}[pass_id]
+    (n0, s0), (n1, s1), so = shapes
+    native = opt is not None and opt.multiply == AMSIM_MULTIPLY_NATIVE
+    _check_f32(in0, n0, s0)
+    _check_f32(in1, n1, s1, in0.device)
+    _check_lut(lut, m_bits, in0.device, native)
+    if out is None:
+        out = torch.empty(so, dtype=torch.float32, device=in0.device)
+    _check_f32(out, "out", so, in0.device)
+    name = {AMSIM_CONV_FWD: "approx_conv2d_fwd", AMSIM_CONV_BWD_DATA: "approx_conv2d_bwd_data",
+            AMSIM_CONV_BWD_WEIGHT: "approx_conv2d_bwd_weight"}[pass_id]
+    return _conv_call(name, pass_id, desc, in0, in1, out, lut, m_bits, workspace, opt)
 
 
 def approx_conv2d_fwd(desc, x, w, lut, m_bits, out=None, workspace=None):
     """y (NHWC) from x (NHWC) and w (HWIO)."""
-    torch = _torch()
-    _check_f32(x, "x")
-    _check_f32(w, "w")
-    _check_lut(lut, m_bits)
-    oh, ow = conv_out_hw(desc)
-    if out is None:
-        out = torch.empty((desc["n"], oh, ow, desc["c_out"]), dtype=torch.float32, device=x.device)
-    return _conv_call("approx_conv2d_fwd", AMSIM_CONV_FWD, desc, x, w, out, lut, m_bits, workspace)
+    return _conv_pass(AMSIM_CONV_FWD, desc, x, w, lut, m_bits, out, workspace, None)
 
 
 def approx_conv2d_bwd_data(desc, dy, w, lut, m_bits, out=None, workspace=None):
     """dx (NHWC) from dy (NHWC) and w (HWIO)."""
-    torch = _torch()
-    _check_f32(dy, "dy")
-    _check_f32(w, "w")
-    _check_lut(lut, m_bits)
-    if out is None:
-        out = torch.empty((desc["n"], desc["h"], desc["w"], desc["c_in"]), dtype=torch.float32, device=dy.device)
-    return _conv_call("approx_conv2d_bwd_data", AMSIM_CONV_BWD_DATA, desc, dy, w, out, lut, m_bits, workspace)
+    return _conv_pass(AMSIM_CONV_BWD_DATA, desc, dy, w, lut, m_bits, out, workspace, None)
 
 
 def approx_conv2d_bwd_weight(desc, x, dy, lut, m_bits, out=None, workspace=None):
     """dw (HWIO) from x (NHWC) and dy (NHWC)."""
-    torch = _torch()
-    _check_f32(x, "x")
-    _check_f32(dy, "dy")
-    _check_lut(lut, m_bits)
-    if out is None:
-        out = torch.empty((desc["kh"], desc["kw"], desc["c_in"], desc["c_out"]), dtype=torch.float32, device=x.device)
-    return _conv_call("approx_conv2d_bwd_weight", AMSIM_CONV_BWD_WEIGHT, desc, x, dy, out, lut, m_bits, workspace)
+    return _conv_pass(AMSIM_CONV_BWD_WEIGHT, desc, x, dy, lut, m_bits, out, workspace, None)
+
+
+def approx_conv2d_fwd_ex(desc, x, w, lut, m_bits, out=None, workspace=None, multiply="table", e_bits=8,
+                         exp_cast="inf"):
+    return _conv_pass(AMSIM_CONV_FWD, desc, x, w, lut, m_bits, out, workspace, options(multiply, e_bits, exp_cast))
+
+
+def approx_conv2d_bwd_data_ex(desc, dy, w, lut, m_bits, out=None, workspace=None, multiply="table", e_bits=8,
+                              exp_cast="inf"):
+    return _conv_pass(AMSIM_CONV_BWD_DATA, desc, dy, w, lut, m_bits, out, workspace,
+                      options(multiply, e_bits, exp_cast))
+
+
+def approx_conv2d_bwd_weight_ex(desc, x, dy, lut, m_bits, out=None, workspace=None, multiply="table", e_bits=8,
+                                exp_cast="inf"):
+    return _conv_pass(AMSIM_CONV_BWD_WEIGHT, desc, x, dy, lut, m_bits, out, workspace,
+                      options(multiply, e_bits, exp_cast))
 
 
 def approx_mul_ew(a, b, lut, m_bits, out=None):
     torch = _torch()
     _check_f32(a, "a")
-    _check_f32(b, "b")
-    _check_lut(lut, m_bits)
-    if a.shape != b.shape:
-        raise ValueError("shapes differ")
+    _check_f32(b, "b", tuple(a.shape), a.device)
+    _check_lut(lut, m_bits, a.device)
     if out is None:
         out = torch.empty_like(a)
+    _check_f32(out, "out", tuple(a.shape), a.device)
     _check(lib().approx_mul_ew(a.numel(), _ptr(a), _ptr(b), _ptr(out), _ptr(lut), int(m_bits), _stream()),
            "approx_mul_ew")
+    return out
+
+
+def approx_mul_ew_ex(a, b, lut, m_bits, out=None, e_bits=8, exp_cast="inf"):
+    torch = _torch()
+    _check_f32(a, "a")
+    _check_f32(b, "b", tuple(a.shape), a.device)
+    _check_lut(lut, m_bits, a.device)
+    if out is None:
+        out = torch.empty_like(a)
+    _check_f32(out, "out", tuple(a.shape), a.device)
+    opt = options("table", e_bits, exp_cast)
+    _check(lib().approx_mul_ew_ex(ctypes.byref(opt), a.numel(), _ptr(a), _ptr(b), _ptr(out), _ptr(lut), int(m_bits),
+                                  _stream()), "approx_mul_ew_ex")
+    return out
+
+
+def amsim_cast_exponent(x, e_bits, exp_cast="inf", m_bits=7, out=None):
+    """x cast to the (1, e_bits, m_bits) format's range, as FP32 values."""
+    torch = _torch()
+    _check_f32(x, "x")
+    cast = {"inf": AMSIM_CAST_INF, "saturate": AMSIM_CAST_SATURATE}[exp_cast]
+    if out is None:
+        out = torch.empty_like(x)
+    _check_f32(out, "out", tuple(x.shape), x.device)
+    _check(lib().amsim_cast_exponent(int(e_bits), cast, int(m_bits), x.numel(), _ptr(x), _ptr(out), _stream()),
+           "amsim_cast_exponent")
     return out
 
 

@@ -17,19 +17,56 @@ typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 
 // ------------------------------------------------------------------ device helpers -------
 
+// The decode of one operand for a (1, e, m) multiplier (Sec. "AMSim": e can range from 1 to 8 given
+// an exponent-casting function).  The cast maps an FP32 value into the e-bit format: fields
+// [lo, hi] of the FP32 exponent are the format's normal range (unbiased exponents 1 - beta ..
+// beta, beta = 2^(e-1) - 1); below it the value is a signed zero (the format's denormals read as
+// zero, as Algorithm 2 reads FP32's); above it a signed Inf, or with `sat` the format's largest
+// finite value (exponent beta, top-M mantissa bits all ones).  The head of a value in range has
+// its exponent field lowered by `delta` = (127 - beta) / 2, so that the FP32 product of two
+// heads underflows exactly when the e-bit exponent sum Ea + Eb - beta is <= 0 (Algorithm 2's zero
+// rule in the format's constants).  e = 8 is the identity: lo = 1, hi = 254, delta = 0.
+struct DecFmt {
+    int m;          // mantissa bits of the table index (the paper's M)
+    int shift;      // the index field's shift
+    uint32_t zidx;  // index field of zeros
+    int lo, hi;     // FP32 exponent fields of the format's normal range
+    int delta;      // exponent offset of in-range heads
+    int sat;        // overflow saturates to the largest finite value (else Inf)
+    int raw;        // native multiply: operands kept as they are (no decode)
+};
+
+__device__ __forceinline__ uint32_t amsim_decode_fmt(uint32_t u, const DecFmt &f)
+{
+    if (f.raw) return u;
+    const uint32_t e = (u >> 23) & 0xFFu, sign = u & 0x80000000u;
+    const uint32_t mfield = ((1u << f.m) - 1u);
+    if (e == 0u || (e != 0xFFu && int(e) < f.lo)) return sign | f.zidx;  // +-0, denormals, underflow
+    uint32_t head, idx;
+    if (e == 0xFFu) {
+        head = (u & 0xFF800000u) | ((u & 0x007FFFFFu) ? 0x00400000u : 0u);  // +-Inf / qNaN
+        idx = ((u >> (23 - f.m)) & mfield) << f.shift;
+    } else if (int(e) > f.hi) {
+        head = f.sat ? (sign | (uint32_t(f.hi - f.delta) << 23)) : (sign | 0x7F800000u);
+        idx = f.sat ? (mfield << f.shift) : 0u;
+    } else {
+        head = sign | (uint32_t(int(e) - f.delta) << 23);  // +-2^(E-127-delta)
+        idx = ((u >> (23 - f.m)) & mfield) << f.shift;
+    }
+    return head | idx;
+}
+
+// The FP32 format (e = 8): the decode of Algorithm 2's operands as they are.
+__host__ __device__ constexpr DecFmt fp32_fmt(int m, int shift, uint32_t zidx = 0u)
+{
+    return DecFmt{m, shift, zidx, 1, 254, 0, 0, 0};
+}
+
 // zidx: the index field given to zeros and denormals (their mantissa bits never matter: every
 // product with a zero is a signed zero, whatever table entry it reads).
 __device__ __forceinline__ uint32_t amsim_decode(uint32_t u, int m, int shift, uint32_t zidx = 0u)
 {
-    const uint32_t e = (u >> 23) & 0xFFu;
-    if (e == 0u) return (u & 0x80000000u) | zidx;                      // +-0 (denormals too)
-    uint32_t head;
-    if (e == 0xFFu)
-        head = (u & 0xFF800000u) | ((u & 0x007FFFFFu) ? 0x00400000u : 0u);  // +-Inf / qNaN
-    else
-        head = u & 0xFF800000u;                                        // +-2^(E-127)
-    const uint32_t idx = ((u >> (23 - m)) & ((1u << m) - 1u)) << shift;
-    return head | idx;
+    return amsim_decode_fmt(u, fp32_fmt(m, shift, zidx));
 }
 
 __device__ __forceinline__ float head_value(uint32_t w) { return __uint_as_float(w & kHeadMask); }
@@ -128,6 +165,18 @@ __device__ __forceinline__ float tab_value(const unsigned char *p)
         return __uint_as_float((uint32_t(*reinterpret_cast<const uint16_t *>(p)) << 8) + 0x3F800000u);
     else
         return *reinterpret_cast<const float *>(p);
+}
+
+// The same factor times 2^k, vadd = k << 23 (0 <= k <= 126: v * 2^k stays finite).
+template <int EB>
+__device__ __forceinline__ float tab_value_scaled(const unsigned char *p, uint32_t vadd)
+{
+    if constexpr (EB == 1)
+        return __uint_as_float((uint32_t(*p) << 16) + (0x3F800000u + vadd));
+    else if constexpr (EB == 2)
+        return __uint_as_float((uint32_t(*reinterpret_cast<const uint16_t *>(p)) << 8) + (0x3F800000u + vadd));
+    else
+        return __uint_as_float(*reinterpret_cast<const uint32_t *>(p) + vadd);
 }
 
 // Convolution geometry: batch, input height and width, input and output channels, kernel height

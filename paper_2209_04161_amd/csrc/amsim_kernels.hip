@@ -12,9 +12,11 @@
 //   with f32 denormals flushed to zero: pa*pb underflows to a signed zero exactly when
 //   Ea + Eb - 127 <= 0 (the zero rule, before the carry), overflows to a signed Inf when it
 //   is >= 255, and v * (pa*pb) is exact, or Inf when the carry lifts the exponent to 255.
-//   IEEE arithmetic gives the NaN/Inf policy for special operands.  The sum uses
-//   fma(v, pa*pb, acc): pa*pb is rounded on its own, and v*(pa*pb) is exact, so the fma equals
-//   acc + c rounded once.
+//   IEEE arithmetic gives the NaN/Inf policy for special operands.  Where the operands'
+//   exponents rule that last case out (Ea + Eb <= 380 for every finite pair, known from the
+//   decode statistics), the sum uses fma(v, pa*pb, acc), which then equals acc + c rounded once;
+//   otherwise c is rounded on its own first, so that an overflowing product is Inf whatever the
+//   sum it is added to.
 //
 // The table kernels (the hot path) live in amsim_tab.h / amsim_tab.hip; this file holds the
 // decode and table-preparation pre-passes, the split reduction, the direct-evaluation GEMM,
@@ -54,6 +56,16 @@ __device__ __forceinline__ int div_small(int r, int d, float inv_d, bool small)
     return q;
 }
 
+// A step-pair record from the decoded words of its two steps: {index field of the first, the two
+// heads as bf16 (the first in the low half), index field of the second}; with raw operands
+// (native multiply) {first, 0, second}.
+__device__ __forceinline__ void store_record(uint32_t *d, uint32_t w0, uint32_t w1, int raw)
+{
+    d[0] = raw ? w0 : (w0 & 0xFFFFu);
+    d[1] = raw ? 0u : ((w0 >> 16) | (w1 & 0xFFFF0000u));
+    d[2] = raw ? w1 : (w1 & 0xFFFFu);
+}
+
 // dst[(b * rows + r) * dld + c] = decode(src[b * sb + r * sr + c * sc]) for r < vrows, c < cols;
 // padding columns c in [cols, dld) and padding rows r in [vrows, rows) (whose source is not read)
 // are written as decoded +0.  dld is a multiple of 4 and
@@ -63,7 +75,7 @@ __device__ __forceinline__ int div_small(int r, int d, float inv_d, bool small)
 __global__ __launch_bounds__(256) void decode_kernel(const float *__restrict__ src, int64_t sb, int64_t sr, int64_t sc,
                                                      int batches, int rows, int vrows, int cols,
                                                      uint32_t *__restrict__ dst,
-                                                     int dld, int m, int shift, uint32_t zidx,
+                                                     int dld, DecFmt f,
                                                      uint32_t *__restrict__ stats, int vec)
 {
     const uint32_t qpr = uint32_t(dld) / 4u;
@@ -103,7 +115,7 @@ __global__ __launch_bounds__(256) void decode_kernel(const float *__restrict__ s
             for (int e = 0; e < 4; ++e) {
                 // padding columns and +0 operands both decode to 0 and leave the statistics alone
                 st.add(w[h][e]);
-                o[e] = amsim_decode(w[h][e], m, shift, zidx);
+                o[e] = amsim_decode_fmt(w[h][e], f);
             }
             *reinterpret_cast<u32x4 *>(dst + int64_t(row[h]) * dld + c[h]) = o;
         }
@@ -111,34 +123,32 @@ __global__ __launch_bounds__(256) void decode_kernel(const float *__restrict__ s
     store_stats(st, stats, blockIdx.x);
 }
 
-// Decoded NHWC tensor inside a zero border: dst[n][hp][wp][c] = decode(src[n][hp-top][wp-left][c])
-// where that pixel exists, decoded +0 elsewhere.  One padded image row (wp * c words, of which
-// the w * c in the middle come from one contiguous source row) per workgroup iteration.
-__global__ __launch_bounds__(256) void decode_pad_kernel(const float *__restrict__ src, int n, int h, int w, int c,
-                                                         int top, int left, int hp, int wp,
-                                                         uint32_t *__restrict__ dst, int m, int shift, uint32_t zidx,
-                                                         uint32_t *__restrict__ stats)
+// The backward-weight pass's first operand: the NHWC tensor inside its zero border as step-pair
+// records [n][hp][wp][c], record (b, y, x, ci) = the record of the decoded elements at columns x and
+// x + sw of padded row y (a column past the border, or outside x, a decoded +0).  A workgroup takes
+// one padded image row at a time; consecutive threads write consecutive records.
+__global__ __launch_bounds__(256) void decode_pad_pairs_kernel(const float *__restrict__ src, int n, int h, int w, int c,
+                                                               int top, int left, int hp, int wp, int sw,
+                                                               uint32_t *__restrict__ dst, DecFmt f,
+                                                               uint32_t *__restrict__ stats)
 {
-    const int len = wp * c, lead = left * c, body = w * c;
+    const int len = wp * c;
     ExpStats st;
     for (int rr = blockIdx.x; rr < n * hp; rr += gridDim.x) {
         const int b = rr / hp, y = rr - b * hp, ih = y - top;
-        const bool inside = unsigned(ih) < unsigned(h);
-        const float *srow = src + (int64_t(b) * h + ih) * body;
-        uint32_t *drow = dst + int64_t(rr) * len;
-        for (int i0 = threadIdx.x; i0 < len; i0 += 4 * 256) {
-            uint32_t v[4];
-#pragma unroll
-            for (int e = 0; e < 4; ++e) {
-                const int j = i0 + e * 256 - lead;
-                v[e] = (inside && i0 + e * 256 < len && unsigned(j) < unsigned(body)) ? __float_as_uint(srow[j]) : 0u;
+        const bool inside = unsigned(ih) < unsigned(h);  // uniform over the workgroup
+        const float *srow = src + (int64_t(b) * h + ih) * w * c;
+        uint32_t *drow = dst + int64_t(rr) * len * 3;
+        for (int i = threadIdx.x; i < len; i += 256) {
+            const int x = i / c, ci = i - x * c, x1 = x + sw;
+            const int ix0 = x - left, ix1 = x1 - left;
+            uint32_t u0 = 0u, u1 = 0u;
+            if (inside) {
+                if (unsigned(ix0) < unsigned(w)) u0 = __float_as_uint(srow[ix0 * c + ci]);
+                if (x1 < wp && unsigned(ix1) < unsigned(w)) u1 = __float_as_uint(srow[ix1 * c + ci]);
             }
-#pragma unroll
-            for (int e = 0; e < 4; ++e) {
-                if (i0 + e * 256 >= len) break;
-                st.add(v[e]);
-                drow[i0 + e * 256] = amsim_decode(v[e], m, shift, zidx);
-            }
+            st.add(u0);  // every element is the first of exactly one record
+            store_record(drow + int64_t(i) * 3, amsim_decode_fmt(u0, f), amsim_decode_fmt(u1, f), f.raw);
         }
     }
     store_stats(st, stats, blockIdx.x);
@@ -155,11 +165,11 @@ constexpr int kNhcwTile = 8192;  // words of the LDS tile: cc * (w | 1) <= kNhcw
 
 __global__ __launch_bounds__(256) void decode_pad_nhcw_kernel(const float *__restrict__ src, int n, int h, int w, int c,
                                                               int top, int left, int hp, int wp,
-                                                              uint32_t *__restrict__ dst, int m, int shift, uint32_t zidx,
-                                                              uint32_t *__restrict__ stats, int cc)
+                                                              uint32_t *__restrict__ dst, DecFmt f,
+                                                              uint32_t *__restrict__ stats, int cc, int cp)
 {
     extern __shared__ uint32_t tile[];  // cc * (w | 1) words (the launch sizes it)
-    const int ws = w | 1, cp = (c + 1) / 2;
+    const int ws = w | 1;
     ExpStats st;
     for (int rr = blockIdx.x; rr < n * hp; rr += gridDim.x) {
         const int b = rr / hp, y = rr - b * hp, ih = y - top;
@@ -186,7 +196,7 @@ __global__ __launch_bounds__(256) void decode_pad_nhcw_kernel(const float *__res
                 for (int k = 0; k < 8; ++k) {
                     if (e0 + 256 * k >= cnt) break;
                     st.add(v[k]);
-                    tile[ch[k] * ws + x[k]] = amsim_decode(v[k], m, shift, zidx);
+                    tile[ch[k] * ws + x[k]] = amsim_decode_fmt(v[k], f);
                 }
             }
             __syncthreads();
@@ -197,16 +207,13 @@ __global__ __launch_bounds__(256) void decode_pad_nhcw_kernel(const float *__res
             const float inv_wp = 1.0f / float(wp);
             const bool small = qn * wp < (1 << 24);
             for (int rec = threadIdx.x; rec < qn * wp; rec += 256) {
-                const int q = div_small(rec, wp, inv_wp, small), ix = rec - q * wp - left;
+                const int q = div_small(rec, wp, inv_wp, small), x = rec - q * wp, ix = x - left;
                 uint32_t w0 = 0u, w1 = 0u;
                 if (unsigned(ix) < unsigned(w)) {
                     w0 = tile[(2 * q) * ws + ix];
                     w1 = 2 * q + 1 < ccn ? tile[(2 * q + 1) * ws + ix] : 0u;
                 }
-                uint32_t *d = dblk + int64_t(rec) * 3;
-                d[0] = w0 & 0xFFFFu;
-                d[1] = (w0 >> 16) | (w1 & 0xFFFF0000u);
-                d[2] = w1 & 0xFFFFu;
+                store_record(dblk + int64_t(rec) * 3, w0, w1, f.raw);
             }
         }
     }
@@ -222,7 +229,7 @@ __global__ __launch_bounds__(256) void decode_pad_nhcw_kernel(const float *__res
 // decoded source row (w * c <= kNhcwTile words) in LDS.
 __global__ __launch_bounds__(256) void decode_unfold_w_kernel(const float *__restrict__ src, int n, int h, int w, int c,
                                                               int top, int left, int hp, int kw_n, int sw, int ow_n,
-                                                              uint32_t *__restrict__ dst, int m, int shift,
+                                                              uint32_t *__restrict__ dst, DecFmt f,
                                                               uint32_t *__restrict__ stats)
 {
     extern __shared__ uint32_t tile[];  // w * c words (the launch sizes it)
@@ -232,9 +239,9 @@ __global__ __launch_bounds__(256) void decode_unfold_w_kernel(const float *__res
         const int b = rr / hp, y = rr - b * hp, ih = y - top;
         uint32_t *dimg = dst + int64_t(rr) * cp * ow_n * 3;
         if (unsigned(ih) >= unsigned(h)) {  // a padding row (uniform over the workgroup): +0, and the
-            // padding channel's -0 in the head word of the last channel pair
-            for (int i = threadIdx.x; i < cp * ow_n * 3; i += 256)
-                dimg[i] = (cu & 1) && i % 3 == 1 && i / 3 >= (cp - 1) * ow_n ? 0x80000000u : 0u;
+            // padding channel's -0 in the last channel pair
+            for (int rec = threadIdx.x; rec < cp * ow_n; rec += 256)
+                store_record(dimg + int64_t(rec) * 3, 0u, (cu & 1) && rec >= (cp - 1) * ow_n ? 0x80000000u : 0u, f.raw);
             continue;
         }
         const float *srow = src + (int64_t(b) * h + ih) * w * c;
@@ -242,7 +249,7 @@ __global__ __launch_bounds__(256) void decode_unfold_w_kernel(const float *__res
         for (int e = threadIdx.x; e < w * c; e += 256) {
             const uint32_t v = __float_as_uint(srow[e]);
             st.add(v);
-            tile[e] = amsim_decode(v, m, shift, 0u);
+            tile[e] = amsim_decode_fmt(v, f);
         }
         __syncthreads();
         const float inv_own = 1.0f / float(ow_n);
@@ -259,21 +266,88 @@ __global__ __launch_bounds__(256) void decode_unfold_w_kernel(const float *__res
                 else if (unsigned(ix) < unsigned(w))
                     wd[t] = tile[ix * c + (j - k * c)];
             }
-            uint32_t *d = dimg + int64_t(rec) * 3;
-            d[0] = wd[0] & 0xFFFFu;
-            d[1] = (wd[0] >> 16) | (wd[1] & 0xFFFF0000u);
-            d[2] = wd[1] & 0xFFFFu;
+            store_record(dimg + int64_t(rec) * 3, wd[0], wd[1], f.raw);
         }
     }
     store_stats(st, stats, blockIdx.x);
 }
 
+// Backward data: the products of the padded, dilated error (Algorithm 4) that the stride-phase
+// decomposition does not evaluate.  Every tap (kh, kw) of the kernel window contributes to every
+// output; a tap outside the output's stride phase reads a dilation or padding zero, so it adds
+// amul(+0, w[kh][kw][ci][co]) for every co: NaN when the weight, as the call's format casts it,
+// is Inf or NaN (Inf x 0), else a zero whose sign is the weight's (so a +0 unless the sign bit
+// is set).  Such products leave every sum but an exactly zero one (-0 turns into +0 when one
+// of them is +0) and make it NaN when one of them is.  One word per (stride phase, ci) over the
+// taps outside the phase and per (kw, ci) over all kh (for the w-unfolded pass's fold): bit 0 a
+// NaN product, bit 1 a +0 product.  w is [KH][KW][CI][CO]; `hi` the largest finite exponent field of
+// the format (values above it are Inf unless `sat`).
+constexpr uint32_t kZeroNan = 1u, kZeroPos = 2u;
+
+__device__ __forceinline__ uint32_t zero_product_class(uint32_t u, int hi, int sat)
+{
+    const int e = int((u >> 23) & 0xFFu);
+    if (e == 0xFF || (!sat && e > hi)) return kZeroNan;
+    return (u >> 31) ? 0u : kZeroPos;
+}
+
+__global__ __launch_bounds__(256) void zero_tap_flags_kernel(const float *__restrict__ w, int KH, int KW, int CI, int CO,
+                                                             int sh, int sw, int pt, int pl, int hi, int sat,
+                                                             uint32_t *__restrict__ phase_flags,
+                                                             uint32_t *__restrict__ kw_flags)
+{
+    const int nphase = phase_flags ? sh * sw * CI : 0, total = nphase + (kw_flags ? KW * CI : 0);
+    const uint32_t *wu = reinterpret_cast<const uint32_t *>(w);
+    for (int t = blockIdx.x * blockDim.x + threadIdx.x; t < total; t += gridDim.x * blockDim.x) {
+        uint32_t f = 0u;
+        if (t < nphase) {
+            const int ci = t % CI, phase = t / CI, ph = phase / sw, pw = phase % sw;
+            for (int kh = 0; kh < KH; ++kh)
+                for (int kw = 0; kw < KW; ++kw) {
+                    if ((kh - ph - pt) % sh == 0 && (kw - pw - pl) % sw == 0) continue;  // a tap of the phase
+                    const uint32_t *wr = wu + (int64_t(kh * KW + kw) * CI + ci) * CO;
+                    for (int co = 0; co < CO; ++co) f |= zero_product_class(wr[co], hi, sat);
+                }
+            phase_flags[t] = f;
+        } else {
+            const int ci = (t - nphase) % CI, kw = (t - nphase) / CI;
+            for (int kh = 0; kh < KH; ++kh) {
+                const uint32_t *wr = wu + (int64_t(kh * KW + kw) * CI + ci) * CO;
+                for (int co = 0; co < CO; ++co) f |= zero_product_class(wr[co], hi, sat);
+            }
+            kw_flags[t - nphase] = f;
+        }
+    }
+}
+
+// Adds the products outside each output's stride phase (see zero_tap_flags_kernel) to dx
+// [n][H][W][CI]: NaN where one is NaN, +0 for an exactly -0 sum where one is +0.
+__global__ __launch_bounds__(256) void dilation_fixup_kernel(float *__restrict__ dx, int64_t total, int H, int Wd, int CI,
+                                                             int sh, int sw, const uint32_t *__restrict__ phase_flags)
+{
+    for (int64_t i = int64_t(blockIdx.x) * blockDim.x + threadIdx.x; i < total; i += int64_t(gridDim.x) * blockDim.x) {
+        const int ci = int(i % CI);
+        const int64_t t = i / CI;
+        const int x = int(t % Wd), y = int((t / Wd) % H);
+        const uint32_t f = phase_flags[((y % sh) * sw + x % sw) * CI + ci];
+        if (f == 0u) continue;
+        const uint32_t u = __float_as_uint(dx[i]);
+        if (f & kZeroNan)
+            dx[i] = __uint_as_float(0x7FC00000u);
+        else if (u == 0x80000000u)
+            dx[i] = 0.0f;
+    }
+}
+
 // Backward-data pass with few input channels, second half: the gradient of the w-unfolded input
 // (see decode_unfold_w_kernel), dxu[n][ih][ow][kw * c + ci], folded back onto x's pixels:
 // dx[n][ih][iw][ci] = the sum, in ascending kw, of dxu[n][ih][ow][kw * c + ci] over the (kw, ow)
-// with ow * sw + kw - left = iw, 0 <= ow < ow_n; -0 (the empty sum) where there is none.
+// with ow * sw + kw - left = iw, 0 <= ow < ow_n; -0 (the empty sum) where there is none.  A kw with
+// no such ow reads zeros of the dilated, padded error at every kh: its products are those of
+// kw_flags (see zero_tap_flags_kernel).
 __global__ __launch_bounds__(256) void fold_w_kernel(const float *__restrict__ dxu, int n, int h, int w, int c,
-                                                     int kw_n, int sw, int left, int ow_n, float *__restrict__ dx)
+                                                     int kw_n, int sw, int left, int ow_n,
+                                                     const uint32_t *__restrict__ kw_flags, float *__restrict__ dx)
 {
     const int64_t total = int64_t(n) * h * w * c;
     const int cu = kw_n * c;
@@ -283,13 +357,20 @@ __global__ __launch_bounds__(256) void fold_w_kernel(const float *__restrict__ d
         const int iw = int(t % w);
         const int64_t row = t / w;  // n * h + ih
         float acc = -0.0f;
+        uint32_t zf = 0u;
         for (int k = 0; k < kw_n; ++k) {
             const int num = iw + left - k;
-            if (num < 0) break;  // and for every larger k
-            const int ow = num / sw;
-            if (ow * sw != num || ow >= ow_n) continue;
+            const int ow = num >= 0 ? num / sw : -1;
+            if (num < 0 || ow * sw != num || ow >= ow_n) {
+                zf |= kw_flags[k * c + ci];
+                continue;
+            }
             acc += dxu[(row * ow_n + ow) * cu + k * c + ci];
         }
+        if (zf & kZeroNan)
+            acc = __uint_as_float(0x7FC00000u);
+        else if ((zf & kZeroPos) && __float_as_uint(acc) == 0x80000000u)
+            acc = 0.0f;
         dx[i] = acc;
     }
 }
@@ -300,8 +381,8 @@ __global__ __launch_bounds__(256) void fold_w_kernel(const float *__restrict__ d
 // (r, c) | head of (r, c + 1) << 16 as bf16, index field of (r, c + 1)}, a column past the end
 // being a decoded +0.  The grid strides over 64 x 64 tiles in both directions.
 __global__ __launch_bounds__(256) void decode_t_kernel(const float *__restrict__ src, int64_t sr, int64_t sc, int rows,
-                                                       int cols, uint32_t *__restrict__ dst, int dld, int m, int shift,
-                                                       uint32_t zidx, uint32_t *__restrict__ stats,
+                                                       int cols, uint32_t *__restrict__ dst, int dld, DecFmt f,
+                                                       uint32_t *__restrict__ stats,
                                                        uint32_t *__restrict__ records)
 {
     __shared__ uint32_t tile[64][65];
@@ -318,7 +399,7 @@ __global__ __launch_bounds__(256) void decode_t_kernel(const float *__restrict__
 #pragma unroll
             for (int i = 0; i < 16; ++i) {
                 st.add(u[i]);
-                tile[ty + 4 * i][tx] = amsim_decode(u[i], m, shift, zidx);
+                tile[ty + 4 * i][tx] = amsim_decode_fmt(u[i], f);
             }
             __syncthreads();
             if (records == nullptr) {
@@ -330,11 +411,8 @@ __global__ __launch_bounds__(256) void decode_t_kernel(const float *__restrict__
                 for (int i = ty; i < 32; i += 4) {  // c0 is even: pair (c, c + 1) lies in the tile
                     const int c = c0 + 2 * i, r = r0 + tx;
                     if (c < cols && r < dld) {
-                        const uint32_t w0 = tile[tx][2 * i], w1 = tile[tx][2 * i + 1];
-                        uint32_t *rec = records + (int64_t(c >> 1) * dld + r) * 3;
-                        rec[0] = w0 & 0xFFFFu;
-                        rec[1] = (w0 >> 16) | (w1 & 0xFFFF0000u);
-                        rec[2] = w1 & 0xFFFFu;
+                        store_record(records + (int64_t(c >> 1) * dld + r) * 3, tile[tx][2 * i], tile[tx][2 * i + 1],
+                                     f.raw);
                     }
                 }
             }
@@ -417,8 +495,11 @@ __global__ __launch_bounds__(256) void direct_gemm_kernel(const float *__restric
                 for (int i = 0; i < 4; ++i)
 #pragma unroll
                     for (int j = 0; j < 4; ++j) {
+                        // the product rounded on its own before the add: it may overflow to Inf
+                        // (exponent 254 plus a carry), which an fma with the sum would not see
                         const float v = __uint_as_float(a1[i] + b1[j]);
-                        acc[i][j] = __builtin_fmaf(v, __uint_as_float(a0[i]) * __uint_as_float(b0[j]), acc[i][j]);
+                        const float c = v * (__uint_as_float(a0[i]) * __uint_as_float(b0[j]));
+                        acc[i][j] = acc[i][j] + c;
                     }
             }
         }
@@ -486,19 +567,53 @@ __global__ void fill_kernel(float *__restrict__ C, int rows, int cols, int64_t l
 }
 
 // Element-wise products through the same decode/combine path as the GEMM kernels, with the
-// table read from global memory in its canonical layout (index = ka * 2^M + kb).
+// table read from global memory in its canonical layout (index = ka * 2^M + kb).  fa, fb: the
+// operands' decode (fa's index field ka << M, fb's kb); vadd, su, sd: the exact path's format
+// scaling (see tab_body).
 __global__ void mul_ew_kernel(int64_t n, const float *__restrict__ a, const float *__restrict__ b,
-                              float *__restrict__ c, const uint32_t *__restrict__ lut, int m)
+                              float *__restrict__ c, const uint32_t *__restrict__ lut, DecFmt fa, DecFmt fb,
+                              uint32_t vadd, float su, float sd)
 {
     for (int64_t i = int64_t(blockIdx.x) * blockDim.x + threadIdx.x; i < n; i += int64_t(gridDim.x) * blockDim.x) {
-        const uint32_t wa = amsim_decode(__float_as_uint(a[i]), m, m);
-        const uint32_t wb = amsim_decode(__float_as_uint(b[i]), m, 0);
-        const float v = table_value(lut[(wa & kIdxMask) + (wb & kIdxMask)]);
-        c[i] = v * (head_value(wa) * head_value(wb));
+        const uint32_t wa = amsim_decode_fmt(__float_as_uint(a[i]), fa);
+        const uint32_t wb = amsim_decode_fmt(__float_as_uint(b[i]), fb);
+        const float v = __uint_as_float(((lut[(wa & kIdxMask) + (wb & kIdxMask)] & 0x00FFFFFFu) + 0x3F800000u) + vadd);
+        c[i] = ((v * (head_value(wa) * head_value(wb))) * su) * sd;
+    }
+}
+
+// The exponent cast on its own: y[i] = x[i] cast to the (1, e, m) format's range (see DecFmt),
+// as an FP32 value -- in range unchanged, below it a signed zero, above it a signed Inf or the
+// largest finite value (2 - 2^-m) * 2^beta; NaN and Inf as they are, denormals a signed zero.
+__global__ void cast_kernel(int64_t n, const float *__restrict__ x, float *__restrict__ y, DecFmt f)
+{
+    for (int64_t i = int64_t(blockIdx.x) * blockDim.x + threadIdx.x; i < n; i += int64_t(gridDim.x) * blockDim.x) {
+        const uint32_t u = __float_as_uint(x[i]);
+        const uint32_t e = (u >> 23) & 0xFFu, sign = u & 0x80000000u;
+        uint32_t r = u;
+        if (e == 0u || (e != 0xFFu && int(e) < f.lo))
+            r = sign;
+        else if (e != 0xFFu && int(e) > f.hi)
+            r = f.sat ? (sign | (uint32_t(f.hi) << 23) | (((1u << f.m) - 1u) << (23 - f.m))) : (sign | 0x7F800000u);
+        y[i] = __uint_as_float(r);
     }
 }
 
 // ------------------------------------------------------------------ table preparation
+
+// The exact path's product form (flags[2]): 1 when a product must be rounded on its own before it
+// is added (t = v * (pa * pb), then the sum), 0 when fma(v, pa * pb, acc) gives the same result.
+// They differ only where v * (pa * pb) overflows to Inf -- exponent field Ea + Eb - 127 = 254 plus
+// a carry -- which an fma would fold into the sum unrounded: impossible when the largest finite
+// exponent fields of the two operands add up to at most 380.  Inf and NaN operands give the same
+// result either way, but their statistics carry no exponent range, so they take the rounded
+// form; so do formats with fewer exponent bits (`narrow`), whose products are scaled before the
+// add, and calls without statistics.
+__device__ __forceinline__ int exact_needs_rounded_products(bool have_stats, bool special, uint32_t a_hi,
+                                                            uint32_t b_hi, int narrow)
+{
+    return (narrow || !have_stats || special || a_hi + b_hi > 380u) ? 1 : 0;
+}
 
 constexpr int kPrepWorkgroups = 8;   // table preparation (M <= 7): workgroups sharing the rows
 
@@ -516,7 +631,7 @@ __global__ __launch_bounds__(1024) void prep_rows_kernel(const uint32_t *__restr
                                                          uint32_t *__restrict__ hl_rows,
                                                          const uint32_t *__restrict__ stats_a, int n_a,
                                                          const uint32_t *__restrict__ stats_b, int n_b,
-                                                         int *__restrict__ flags)
+                                                         int narrow, int *__restrict__ flags)
 {
     __shared__ uint32_t slut[kTabRowEntries * kTabRowEntries];  // the table, canonical order
     __shared__ uint32_t w_low[16], w_alo[16], w_ahs[16], w_blo[16], w_bhs[16];
@@ -588,7 +703,8 @@ __global__ __launch_bounds__(1024) void prep_rows_kernel(const uint32_t *__restr
         const bool window_hl = window && b_lo >= 16u && a_lo + b_lo >= 143u;
         if (lead) {
             flags[0] = eb;
-            flags[1] = (eb == 1 && window) ? 1 : ((eb == 2 && window_hl) ? 2 : 0);
+            flags[1] = narrow ? 0 : ((eb == 1 && window) ? 1 : ((eb == 2 && window_hl) ? 2 : 0));
+            flags[2] = exact_needs_rounded_products(stats_a != nullptr, special, a_hi, b_hi, narrow);
         }
     }
     __syncthreads();
@@ -683,25 +799,43 @@ __global__ __launch_bounds__(256) void lut_low_bits_kernel(const uint32_t *__res
 
 // Second pass: the entry width from the nparts partial words, then the transposed rows -- row kb
 // (2^m entries of eb bytes) holds entry (ka, kb) at byte ka * eb -- through 64 x 64 LDS tiles
-// (loads along kb, stores along ka).  Workgroup 0 writes flags[0] = eb and flags[1] = 0 (no bf16
-// path for wide rows).
+// (loads along kb, stores along ka).  Workgroup 0 writes flags[0] = eb, flags[1] = 0 (no bf16
+// path for wide rows) and flags[2], the exact path's product form, from the decode statistics
+// (n_a and n_b words).
 __global__ __launch_bounds__(256) void prep_rows_wide_kernel(const uint32_t *__restrict__ lut, int m,
                                                              const uint32_t *__restrict__ part, int nparts,
-                                                             unsigned char *__restrict__ dst, int *__restrict__ flags)
+                                                             const uint32_t *__restrict__ stats_a, int n_a,
+                                                             const uint32_t *__restrict__ stats_b, int n_b,
+                                                             int narrow, unsigned char *__restrict__ dst,
+                                                             int *__restrict__ flags)
 {
     __shared__ uint32_t tile[64][65];
-    __shared__ uint32_t s_low[4];
-    uint32_t low = 0u;
+    __shared__ uint32_t s_low[4], s_ahs[4], s_bhs[4];
+    uint32_t low = 0u, ahs = 0u, bhs = 0u;
     for (int i = threadIdx.x; i < nparts; i += 256) low |= part[i];
+    if (blockIdx.x == 0) {
+        for (int i = threadIdx.x; i < n_a; i += 256) ahs = max(ahs, (stats_a[i] >> 8) & 0x1FFu);
+        for (int i = threadIdx.x; i < n_b; i += 256) bhs = max(bhs, (stats_b[i] >> 8) & 0x1FFu);
+    }
 #pragma unroll
     for (int o = 32; o > 0; o >>= 1) low |= uint32_t(__shfl_xor(int(low), o));
-    if ((threadIdx.x & 63) == 0) s_low[threadIdx.x >> 6] = low;
+    ahs = wave_max(ahs);
+    bhs = wave_max(bhs);
+    if ((threadIdx.x & 63) == 0) {
+        s_low[threadIdx.x >> 6] = low;
+        s_ahs[threadIdx.x >> 6] = ahs;
+        s_bhs[threadIdx.x >> 6] = bhs;
+    }
     __syncthreads();
     const uint32_t lb = s_low[0] | s_low[1] | s_low[2] | s_low[3];
     const int eb = lb == 0u ? 1 : ((lb & 0xFFu) == 0u ? 2 : 4);
     if (blockIdx.x == 0 && threadIdx.x == 0) {
+        const uint32_t a_hs = max(max(s_ahs[0], s_ahs[1]), max(s_ahs[2], s_ahs[3]));
+        const uint32_t b_hs = max(max(s_bhs[0], s_bhs[1]), max(s_bhs[2], s_bhs[3]));
         flags[0] = eb;
         flags[1] = 0;
+        flags[2] = exact_needs_rounded_products(stats_a != nullptr && stats_b != nullptr, ((a_hs | b_hs) >> 8) != 0u,
+                                                a_hs & 0xFFu, b_hs & 0xFFu, narrow);
     }
     const int n = 1 << m, tiles_1d = n / 64;
     const int tx = threadIdx.x & 63, ty = threadIdx.x >> 6;
@@ -888,12 +1022,12 @@ inline int decode_vec(const float *src, int64_t sb, int64_t sr, int64_t sc)
 }
 
 // Workspace layout shared by the size queries and the launches:
-//   [transposed rows][bf16-path rows][hi/lo rows][flags][statistics][first operand][second operand]
-//   [partials]
+//   [transposed rows][bf16-path rows][hi/lo rows][flags][statistics][wide-table partials]
+//   [first operand][second operand][partials]
 struct Plan {
     Tile tile;
     int rl;  // log2 of the table row length
-    size_t off_rows, off_dot_rows, off_hl_rows, off_eb, off_stats, off_a, off_b, off_part, total;
+    size_t off_rows, off_dot_rows, off_hl_rows, off_eb, off_stats, off_wpart, off_a, off_b, off_part, total;
     int64_t a_ld, b_ld;   // GEMM: padded leading dims of the decoded operands; conv: b_ld only
     int64_t a_elems;      // conv: elements of the decoded first operand
     int splits;           // reduction splits
@@ -903,11 +1037,16 @@ struct Plan {
     bool unfold_w;          // forward / backward-data pass over x unfolded along w
     int csplit;             // forward / backward data: channel chunks per kernel position (TabArgs::csplit)
     size_t off_unf;         // backward data, unfolded: the unfolded input's gradient
+    int chunk;              // steps per reduction chunk (TabArgs::chunk)
+    int rec_c;              // forward / backward data: channels of the first operand's record rows
+    size_t off_bflags;      // backward data: zero-tap flags per (stride phase, ci), then per (kw, ci)
 };
 
-// Split of a reduction of q chunks (8 steps each).
-void plan_tab_split(Plan &p, int64_t q)
+// Split of a reduction of `taps` taps of `count` steps, in chunks of p.chunk steps (the table
+// kernels count chunks per tap as ceil(count / chunk)), into the tile's number of splits.
+void plan_tab_split(Plan &p, int64_t taps, int64_t count)
 {
+    const int64_t q = taps * ceil_div(count, p.chunk);
     p.chunks_per_split = int(std::max<int64_t>(1, ceil_div(q, p.tile.split)));
     p.splits = int(std::max<int64_t>(1, ceil_div(q, p.chunks_per_split)));
 }
@@ -915,13 +1054,17 @@ void plan_tab_split(Plan &p, int64_t q)
 bool valid_m(int m_bits) { return m_bits >= 1 && m_bits <= 11; }
 
 // Transposed rows (the widest entry width, plus the zero row for 128-entry rows), bf16-path rows,
-// hi/lo rows (128-entry rows only), flags, decode statistics (two operands; for wide rows the
-// table-preparation partials).
+// hi/lo rows (128-entry rows only), flags, decode statistics (two operands), the wide-table
+// preparation's partial words.
 constexpr size_t kDotRowsBytes = size_t(kZeroRow + 1) * kTabRowEntries;
 constexpr size_t kHlRowsBytes = size_t(kZeroRow + 1) * kHlRowBytes;  // 2-byte tables, hi/lo path
 constexpr size_t kStatsBytes = size_t(2) * kStatSlots * 4;
+constexpr int kWidePartWords = 1024;
 
 inline size_t rows_bytes(int rl) { return (size_t(1) << rl) * ((size_t(1) << rl) + (rl == 7 ? 1 : 0)) * 4; }
+
+// Step-pair records of the GEMM's first operand per row.
+inline int64_t gemm_record_pairs(int64_t k) { return (k + 1) / 2; }
 
 size_t table_area(Plan &p, size_t o)
 {
@@ -930,20 +1073,22 @@ size_t table_area(Plan &p, size_t o)
     p.off_hl_rows = p.off_dot_rows + align_up(kDotRowsBytes);
     p.off_eb = p.off_hl_rows + (p.rl == 7 ? align_up(kHlRowsBytes) : 0);
     p.off_stats = p.off_eb + kAlign;
-    return p.off_stats + align_up(kStatsBytes);
+    p.off_wpart = p.off_stats + align_up(kStatsBytes);
+    return p.off_wpart + (p.rl == 7 ? 0 : align_up(size_t(kWidePartWords) * 4));
 }
 
-Plan plan_gemm(int64_t m, int64_t n, int64_t k, int m_bits)
+Plan plan_gemm(int64_t m, int64_t n, int64_t k, int m_bits, bool native = false)
 {
     Plan p{};
     p.rl = row_log(m_bits);
     p.tile = choose_tab_tile(m, n, ceil_div(k, 8), 4, true, p.rl, 8, 1);
     p.a_ld = round_up(m, int64_t(64) * p.tile.wr * p.tile.tm);
+    p.chunk = 8;
     p.b_ld = round_up(n, tab_cols(p.tile));
-    plan_tab_split(p, ceil_div(k, 8));
+    plan_tab_split(p, 1, k);
     size_t o = table_area(p, 0);
     p.off_a = o;  // step-pair records
-    o += align_up(size_t((k + 1) / 2) * p.a_ld * 12);
+    o += align_up(size_t(gemm_record_pairs(k)) * p.a_ld * 12);
     p.off_b = o;
     o += align_up(size_t(k) * p.b_ld * 4);
     p.out_elems = m * n;
@@ -963,7 +1108,7 @@ ConvShape shape_of(const amsim_conv2d *d)
     return s;
 }
 
-int check_conv(const amsim_conv2d *d)
+int check_conv(const amsim_conv2d *d, int pass)
 {
     if (!d) return AMSIM_ERR_INVALID_ARG;
     if (d->n < 1 || d->h < 1 || d->w < 1 || d->c_in < 1 || d->c_out < 1 || d->kh < 1 || d->kw < 1 ||
@@ -983,7 +1128,10 @@ int check_conv(const amsim_conv2d *d)
     // below 2^31 bytes: the table kernels address them with 32-bit byte offsets
     const int64_t xr = int64_t(d->n) * hp * wp * ((d->c_in + 1) / 2) * 12;
     const int64_t yr = int64_t(d->n) * (oh + 2 * d->kh + 2) * (ow + 2 * d->kw + 2) * ((d->c_out + 1) / 2) * 12;
-    if (xr >= (lim << 2) || yr >= (lim << 2)) return AMSIM_ERR_UNSUPPORTED;
+    // backward weight: one record per element of the zero-bordered x
+    const int64_t xe = int64_t(d->n) * hp * wp * d->c_in * 12;
+    if (xr >= (lim << 2) || yr >= (lim << 2) || (pass == AMSIM_CONV_BWD_WEIGHT && xe >= (lim << 2)))
+        return AMSIM_ERR_UNSUPPORTED;
     if (xp >= lim || yp >= lim || w >= lim || y >= lim || d->pad_top >= 65536 || d->pad_bottom >= 65536 ||
         d->pad_left >= 65536 || d->pad_right >= 65536 || d->kh >= 65536 || d->kw >= 65536 ||
         int64_t(d->stride_h) * d->stride_w > 32 || d->c_in > 65535 * 16 || d->c_out > 65535 * 16 ||
@@ -1097,14 +1245,14 @@ bool bwd_data_unfolds(const amsim_conv2d *d)
 {
     if (d->c_in >= 8 || d->kw < 2) return false;
     const amsim_conv2d v = unfolded_desc(d);
-    return check_conv(&v) == AMSIM_OK && int64_t(v.n) * v.h * v.w * v.c_in < (int64_t(1) << 29);
+    return check_conv(&v, AMSIM_CONV_BWD_DATA) == AMSIM_OK && int64_t(v.n) * v.h * v.w * v.c_in < (int64_t(1) << 29);
 }
 
-Plan plan_conv(const amsim_conv2d *d, int pass, int m_bits)
+Plan plan_conv(const amsim_conv2d *d, int pass, int m_bits, bool native = false)
 {
     if (pass == AMSIM_CONV_BWD_DATA && bwd_data_unfolds(d)) {
         const amsim_conv2d v = unfolded_desc(d);
-        Plan p = plan_conv(&v, pass, m_bits);  // the virtual pass (kw = 1: it does not unfold again)
+        Plan p = plan_conv(&v, pass, m_bits, native);  // the virtual pass (kw = 1: it does not unfold again)
         p.unfold_w = true;
         p.off_unf = align_up(p.total);  // the unfolded gradient [n][h][ow][kw * c]
         p.total = p.off_unf + align_up(size_t(v.n) * v.h * v.w * v.c_in * 4);
@@ -1113,6 +1261,7 @@ Plan plan_conv(const amsim_conv2d *d, int pass, int m_bits)
     const ConvShape s = shape_of(d);
     Plan p{};
     p.rl = row_log(m_bits);
+    p.chunk = 8;
     size_t o = table_area(p, 0);
     const int64_t npix_in = int64_t(s.n) * s.h * s.w, npix_out = int64_t(s.n) * s.oh * s.ow;
     p.Hp = d->h + d->pad_top + d->pad_bottom;
@@ -1120,14 +1269,14 @@ Plan plan_conv(const amsim_conv2d *d, int pass, int m_bits)
     if (pass == AMSIM_CONV_FWD) {
         p.unfold_w = fwd_unfolds(s, p.Hp);
         const ConvShape v = p.unfold_w ? unfolded_shape(s) : s;
-        const int rec_c = p.unfold_w ? unfolded_channels(s) : s.ci;  // channels per record row block
         if (p.unfold_w) p.Wp = s.ow;  // the unfolded x has no w border
         const int64_t q = int64_t(v.kh) * v.kw * ceil_div(v.ci, 8);
         p.tile = choose_tab_tile(npix_out, s.co, q, 4, true, p.rl, 8, 1);
-        plan_tab_split(p, q);
         p.csplit = fwd_channel_chunks(s, p.unfold_w);
+        plan_tab_split(p, int64_t(v.kh) * v.kw * p.csplit, v.ci / p.csplit);
+        p.rec_c = p.unfold_w ? unfolded_channels(s) : s.ci;  // channels per record row block
         p.b_ld = round_up(s.co, tab_cols(p.tile));
-        p.a_elems = int64_t(s.n) * p.Hp * p.Wp * ((rec_c + 1) / 2) * 3;  // zero-bordered x as step-pair records
+        p.a_elems = int64_t(s.n) * p.Hp * p.Wp * ((p.rec_c + 1) / 2) * 3;  // zero-bordered x as step-pair records
         p.out_elems = npix_out * s.co;
         p.off_a = o;
         o += align_up(size_t(p.a_elems) * 4);
@@ -1137,30 +1286,33 @@ Plan plan_conv(const amsim_conv2d *d, int pass, int m_bits)
         const int64_t rows = bwd_data_rows(s);
         const int64_t q = ceil_div(s.kh, s.sh) * ceil_div(s.kw, s.sw) * ceil_div(s.co, 8);  // largest phase
         p.tile = choose_tab_tile(rows, s.ci, q, 4, true, p.rl, 4, int64_t(s.sh) * s.sw);  // 8-row tiles spill here
-        plan_tab_split(p, q);
-        p.csplit = bwd_data_channel_chunks(s);
-        p.b_ld = round_up(s.ci, tab_cols(p.tile));
         int top, bottom, left, right;
         bwd_data_dy_pads(s, top, bottom, left, right);
         p.pad_oh = top;
         p.pad_ow = left;
         p.OHp = top + s.oh + bottom;
         p.OWp = left + s.ow + right;
-        p.a_elems = int64_t(s.n) * p.OHp * p.OWp * ((s.co + 1) / 2) * 3;  // zero-padded dy as step-pair records
+        p.csplit = bwd_data_channel_chunks(s);
+        plan_tab_split(p, ceil_div(s.kh, s.sh) * ceil_div(s.kw, s.sw) * p.csplit, s.co / p.csplit);
+        p.rec_c = s.co;
+        p.b_ld = round_up(s.ci, tab_cols(p.tile));
+        p.a_elems = int64_t(s.n) * p.OHp * p.OWp * ((p.rec_c + 1) / 2) * 3;  // zero-padded dy as step-pair records
         p.out_elems = npix_in * s.ci;
         p.off_a = o;
         o += align_up(size_t(p.a_elems) * 4);
         p.off_b = o;  // decoded w^T [kh][kw][co][CIp]
         o += align_up(size_t(s.kh) * s.kw * s.co * p.b_ld * 4);
+        p.off_bflags = o;
+        o += align_up((size_t(s.sh) * s.sw * s.ci + size_t(s.kw) * s.ci) * 4);
     } else {
         const int64_t R = int64_t(s.kh) * s.kw * s.ci;
         const int64_t q = int64_t(s.n) * s.oh * ceil_div(s.ow, 8);
         p.tile = choose_tab_tile(R, s.co, q, 4, true, p.rl, 8, 1);
-        plan_tab_split(p, q);
+        plan_tab_split(p, int64_t(s.n) * s.oh, s.ow);
         p.b_ld = round_up(s.co, tab_cols(p.tile));
-        p.a_elems = int64_t(s.n) * p.Hp * p.Wp * s.ci;
+        p.a_elems = int64_t(s.n) * p.Hp * p.Wp * s.ci * 3;
         p.out_elems = R * s.co;
-        p.off_a = o;  // decoded, zero-bordered x
+        p.off_a = o;  // zero-bordered x as step-pair records, one per element
         o += align_up(size_t(p.a_elems) * 4);
         p.off_b = o;  // decoded dy [n*oh*ow][COp]
         o += align_up(size_t(npix_out) * p.b_ld * 4);
@@ -1171,6 +1323,34 @@ Plan plan_conv(const amsim_conv2d *d, int pass, int m_bits)
     return p;
 }
 
+// How the products of a call are formed (amsim_options): the table's approximate product or the
+// native FP32 multiply, on operands cast to a (1, e, m) format (e = 8: FP32's own exponent).
+struct Mode {
+    int native = 0;
+    int e_bits = 8;
+    int sat = 0;
+};
+
+int mode_of(const amsim_options *o, Mode &md)
+{
+    md = Mode{};
+    if (!o) return AMSIM_OK;
+    if (o->multiply != AMSIM_MULTIPLY_TABLE && o->multiply != AMSIM_MULTIPLY_NATIVE) return AMSIM_ERR_INVALID_ARG;
+    if (o->exp_cast != AMSIM_CAST_INF && o->exp_cast != AMSIM_CAST_SATURATE) return AMSIM_ERR_INVALID_ARG;
+    if (o->e_bits < 2 || o->e_bits > 8) return AMSIM_ERR_UNSUPPORTED;
+    md.native = o->multiply == AMSIM_MULTIPLY_NATIVE ? 1 : 0;
+    md.e_bits = o->e_bits;
+    md.sat = o->exp_cast == AMSIM_CAST_SATURATE ? 1 : 0;
+    if (md.native && md.e_bits != 8) return AMSIM_ERR_UNSUPPORTED;  // the native multiply is FP32's
+    return AMSIM_OK;
+}
+
+// The format's bias beta = 2^(e-1) - 1 and the decode's exponent offset delta = (127 - beta) / 2.
+inline int fmt_beta(const Mode &md) { return (1 << (md.e_bits - 1)) - 1; }
+inline int fmt_delta(const Mode &md) { return (127 - fmt_beta(md)) / 2; }
+// The largest finite FP32 exponent field the format keeps (beyond it the cast gives Inf or saturates).
+inline int fmt_hi(const Mode &md) { return md.native || md.e_bits == 8 ? 254 : 127 + fmt_beta(md); }
+
 // Decoded-index fields: the first operand's mantissa times 16 (the bf16 path's entry size; the
 // exact path extracts it), the second's times the row length (its row offset in entries); zeros
 // of the second operand on the zero row where rows have 128 entries (any row serves on the exact
@@ -1179,44 +1359,55 @@ inline int shift_first(int) { return 4; }
 inline int shift_second(int m_bits) { return row_log(m_bits); }
 inline uint32_t zidx_second(const Plan &p) { return p.rl == 7 ? kZeroRowWord : 0u; }
 
-// Decode statistics for the bf16 path's exponent window: kStatSlots words per operand (null for
-// wide rows, which have no bf16 path).
-inline uint32_t *stats_a(char *ws, const Plan &p)
+DecFmt dec_fmt(const Mode &md, int m_bits, int shift, uint32_t zidx)
 {
-    return p.rl == 7 ? reinterpret_cast<uint32_t *>(ws + p.off_stats) : nullptr;
+    DecFmt f = fp32_fmt(m_bits, shift, zidx);
+    if (md.native) {
+        f.raw = 1;
+        f.zidx = 0u;
+    } else if (md.e_bits < 8) {
+        const int beta = fmt_beta(md);
+        f.lo = 128 - beta;
+        f.hi = 127 + beta;
+        f.delta = fmt_delta(md);
+        f.sat = md.sat;
+    }
+    return f;
 }
-inline uint32_t *stats_b(char *ws, const Plan &p)
+inline DecFmt fmt_first(const Mode &md, int m_bits) { return dec_fmt(md, m_bits, shift_first(m_bits), 0u); }
+inline DecFmt fmt_second(const Mode &md, const Plan &p, int m_bits)
 {
-    return p.rl == 7 ? reinterpret_cast<uint32_t *>(ws + p.off_stats) + kStatSlots : nullptr;
+    return dec_fmt(md, m_bits, shift_second(m_bits), zidx_second(p));
 }
 
-// Launches the table preparation after both decode passes: rows, flags and (128-entry rows) the
-// reduction of the n_a / n_b statistics words.  Wide rows: a low-bits pass over the table, then the
-// transposed rows.
-int prep_rows(const uint32_t *lut, int m_bits, char *ws, const Plan &p, int n_a, int n_b, hipStream_t st)
+// Decode statistics (the bf16 path's exponent window and the exact path's product form):
+// kStatSlots words per operand.
+inline uint32_t *stats_a(char *ws, const Plan &p) { return reinterpret_cast<uint32_t *>(ws + p.off_stats); }
+inline uint32_t *stats_b(char *ws, const Plan &p) { return reinterpret_cast<uint32_t *>(ws + p.off_stats) + kStatSlots; }
+
+// Launches the table preparation after both decode passes: rows, flags and the reduction of the
+// n_a / n_b statistics words.  Wide rows: a low-bits pass over the table, then the transposed rows.
+int prep_rows(const uint32_t *lut, int m_bits, char *ws, const Plan &p, int n_a, int n_b, const Mode &md,
+              hipStream_t st)
 {
+    const int narrow = md.e_bits < 8 ? 1 : 0;
     if (p.rl == 7) {
         hipLaunchKernelGGL(prep_rows_kernel, dim3(kPrepWorkgroups), dim3(1024), 0, st, lut, m_bits,
                            reinterpret_cast<unsigned char *>(ws + p.off_rows),
                            reinterpret_cast<unsigned char *>(ws + p.off_dot_rows),
                            reinterpret_cast<uint32_t *>(ws + p.off_hl_rows), stats_a(ws, p), n_a, stats_b(ws, p), n_b,
-                           reinterpret_cast<int *>(ws + p.off_eb));
+                           narrow, reinterpret_cast<int *>(ws + p.off_eb));
         return launch_status();
     }
     const int total = 1 << (2 * m_bits);
-    const int nparts = int(std::min<int64_t>(ceil_div(total, 256 * 16), 1024));
-    uint32_t *part = reinterpret_cast<uint32_t *>(ws + p.off_stats);
+    const int nparts = int(std::min<int64_t>(ceil_div(total, 256 * 16), kWidePartWords));
+    uint32_t *part = reinterpret_cast<uint32_t *>(ws + p.off_wpart);
     hipLaunchKernelGGL(lut_low_bits_kernel, dim3(nparts), dim3(256), 0, st, lut, total, part);
     const int tiles = (1 << (m_bits - 6)) * (1 << (m_bits - 6));
     hipLaunchKernelGGL(prep_rows_wide_kernel, dim3(std::min(tiles, 2048)), dim3(256), 0, st, lut, m_bits, part,
-                       nparts, reinterpret_cast<unsigned char *>(ws + p.off_rows), reinterpret_cast<int *>(ws + p.off_eb));
+                       nparts, stats_a(ws, p), n_a, stats_b(ws, p), n_b, narrow,
+                       reinterpret_cast<unsigned char *>(ws + p.off_rows), reinterpret_cast<int *>(ws + p.off_eb));
     return launch_status();
-}
-
-template <int OP>
-int launch_tab(const Plan &p, const TabArgs &a, dim3 grid, hipStream_t st)
-{
-    return tab_launch<OP>(p.tile, p.rl, a, grid, st) == hipSuccess ? AMSIM_OK : AMSIM_ERR_HIP;
 }
 
 TabArgs tab_args(const Plan &p, char *ws, const uint32_t *A, int64_t a_elems, const uint32_t *Bd, float *out, int R,
@@ -1241,13 +1432,30 @@ TabArgs tab_args(const Plan &p, char *ws, const uint32_t *A, int64_t a_elems, co
     a.pad_oh = p.pad_oh;
     a.pad_ow = p.pad_ow;
     a.splits = p.splits;
+    a.chunk = p.chunk;
     a.chunks_per_split = p.chunks_per_split;
     a.out_elems = p.out_elems;
     a.csplit = 1;
+    a.rec_c = p.rec_c;
+    a.vadd = 0u;
+    a.su = 1.0f;
+    a.sd = 1.0f;
     return a;
 }
 
+// The exact path's scaling for a format with fewer exponent bits (see tab_body).
+void set_format_scales(TabArgs &a, const Mode &md)
+{
+    if (md.native || md.e_bits == 8) return;
+    const int d2 = 2 * fmt_delta(md);  // 127 - beta, at most 126
+    a.vadd = uint32_t(d2) << 23;
+    a.su = std::ldexp(1.0f, d2);
+    a.sd = std::ldexp(1.0f, -d2);
+}
+
 // ------------------------------------------------------------------ kernel timer --------
+
+constexpr int kKernelKinds = 8;  // AMSIM_KERNEL_*
 
 struct KernelTimer {
     std::mutex mu;
@@ -1255,8 +1463,8 @@ struct KernelTimer {
     std::vector<hipEvent_t> begin, end;
     std::vector<int> kind;
     size_t used = 0;
-    int launches[4] = {0, 0, 0, 0};
-    double total_ms[4] = {0, 0, 0, 0};
+    int launches[kKernelKinds] = {};
+    double total_ms[kKernelKinds] = {};
 };
 
 KernelTimer &timer()
@@ -1304,42 +1512,32 @@ void destroy_events(KernelTimer &t)
 
 // ==================================================================== C entry points =====
 
-extern "C" {
+namespace {
 
-int amsim_gemm_workspace_size(int trans_a, int trans_b, int64_t m, int64_t n, int64_t k, int m_bits, size_t *bytes)
-{
-    (void)trans_a;
-    (void)trans_b;
-    if (!bytes) return AMSIM_ERR_INVALID_ARG;
-    if (!valid_m(m_bits)) return AMSIM_ERR_UNSUPPORTED;
-    if (m < 0 || n < 0 || k < 0) return AMSIM_ERR_INVALID_ARG;
-    if (m == 0 || n == 0 || k == 0) {
-        *bytes = 0;
-        return AMSIM_OK;
-    }
-    const Plan p = plan_gemm(m, n, k, m_bits);
-    *bytes = p.total;
-    return AMSIM_OK;
-}
+// The table kernel variant of a launch.
+inline int tab_variant(const Mode &md) { return md.native ? kTabNative : kTabApprox; }
 
-int approx_gemm(int trans_a, int trans_b, int64_t m, int64_t n, int64_t k, const float *A, int64_t lda,
-                const float *B, int64_t ldb, float *C, int64_t ldc, const uint32_t *lut, int m_bits, void *workspace,
-                size_t workspace_bytes, void *stream)
+// The table's row length for a call: the native multiply reads no table (its plan is M = 7's).
+inline int plan_m(const Mode &md, int m_bits) { return md.native ? 7 : m_bits; }
+
+int gemm_run(const Mode &md, int trans_a, int trans_b, int64_t m, int64_t n, int64_t k, const float *A, int64_t lda,
+             const float *B, int64_t ldb, float *C, int64_t ldc, const uint32_t *lut, int m_bits, void *workspace,
+             size_t workspace_bytes, hipStream_t st)
 {
-    if (!valid_m(m_bits)) return AMSIM_ERR_UNSUPPORTED;
+    if (!md.native && !valid_m(m_bits)) return AMSIM_ERR_UNSUPPORTED;
     if (m < 0 || n < 0 || k < 0) return AMSIM_ERR_INVALID_ARG;
     if (m == 0 || n == 0) return AMSIM_OK;
     if (!C || ldc < n) return AMSIM_ERR_INVALID_ARG;
     const int64_t lim = int64_t(1) << 31;
     if (m >= lim || n >= lim || k >= lim) return AMSIM_ERR_UNSUPPORTED;
-    hipStream_t st = static_cast<hipStream_t>(stream);
     if (k == 0) {
         hipLaunchKernelGGL(fill_kernel, dim3(grid_for(m * n)), dim3(256), 0, st, C, int(m), int(n), ldc, -0.0f);
         return launch_status();
     }
-    if (!A || !B || !lut) return AMSIM_ERR_INVALID_ARG;
+    if (!A || !B || (!lut && !md.native)) return AMSIM_ERR_INVALID_ARG;
     if (lda < (trans_a ? m : k) || ldb < (trans_b ? k : n)) return AMSIM_ERR_INVALID_ARG;
-    const Plan p = plan_gemm(m, n, k, m_bits);
+    const int mb = plan_m(md, m_bits);
+    const Plan p = plan_gemm(m, n, k, mb, md.native != 0);
     // decoded operands are addressed with 32-bit byte offsets
     if (k * p.a_ld >= (int64_t(1) << 29) || k * p.b_ld >= lim || int64_t(p.splits) * m * n >= lim ||
         p.b_ld / tab_cols(p.tile) > 65535)
@@ -1357,23 +1555,27 @@ int approx_gemm(int trans_a, int trans_b, int64_t m, int64_t n, int64_t k, const
     const dim3 grid_dt(unsigned(std::min<int64_t>(ceil_div(p.a_ld, 64), 128)),
                        unsigned(std::min<int64_t>(ceil_div(k, 64), 64)));  // <= kStatSlots workgroups
     const int grid_b = decode_grid(k * p.b_ld);
+    uint32_t *sa = md.native ? nullptr : stats_a(ws, p), *sb = md.native ? nullptr : stats_b(ws, p);
     hipLaunchKernelGGL(decode_t_kernel, grid_dt, dim3(256), 0, st, A, a_sr, a_sc, int(m), int(k), nullptr,
-                       int(p.a_ld), m_bits, shift_first(m_bits), 0u, stats_a(ws, p), Ad);
+                       int(p.a_ld), fmt_first(md, mb), sa, Ad);
     hipLaunchKernelGGL(decode_kernel, dim3(grid_b), dim3(256), 0, st, B, int64_t(0), b_sr, b_sc, 1, int(k), int(k),
-                       int(n), Bd, int(p.b_ld), m_bits, shift_second(m_bits), zidx_second(p), stats_b(ws, p),
-                       decode_vec(B, 0, b_sr, b_sc));
+                       int(n), Bd, int(p.b_ld), fmt_second(md, p, mb), sb, decode_vec(B, 0, b_sr, b_sc));
     if (launch_status() != AMSIM_OK) return AMSIM_ERR_HIP;
-    if (prep_rows(lut, m_bits, ws, p, int(grid_dt.x * grid_dt.y), grid_b, st) != AMSIM_OK) return AMSIM_ERR_HIP;
+    if (!md.native && prep_rows(lut, mb, ws, p, int(grid_dt.x * grid_dt.y), grid_b, md, st) != AMSIM_OK)
+        return AMSIM_ERR_HIP;
     int rc;
     {
         TabArgs a = tab_args(p, ws, Ad, 0, Bd, out, int(m), int(n));
-        a.a_bytes = uint32_t((k + 1) / 2 * p.a_ld * 12);
+        set_format_scales(a, md);
+        a.a_bytes = uint32_t(gemm_record_pairs(k) * p.a_ld * 12);
         a.ldc = p.splits > 1 ? n : ldc;  // partial sums are dense
         a.Mp = int(p.a_ld);
         a.K = int(k);
         dim3 grid(unsigned(p.a_ld / (int64_t(64) * t.wr * t.tm)), unsigned(p.b_ld / tab_cols(t)), unsigned(p.splits));
-        TimedLaunch tl(AMSIM_KERNEL_GEMM, st);
-        rc = launch_tab<OP_GEMM>(p, a, grid, st);
+        TimedLaunch tl(md.native ? AMSIM_KERNEL_GEMM_NATIVE : AMSIM_KERNEL_GEMM, st);
+        rc = tab_launch<OP_GEMM>(p.tile, p.rl, tab_variant(md), a, grid, st) == hipSuccess
+                 ? AMSIM_OK
+                 : AMSIM_ERR_HIP;
     }
     if (rc != AMSIM_OK) return AMSIM_ERR_HIP;
     if (p.splits > 1) {
@@ -1383,93 +1585,84 @@ int approx_gemm(int trans_a, int trans_b, int64_t m, int64_t n, int64_t k, const
     return AMSIM_OK;
 }
 
-int amsim_conv2d_workspace_size(const amsim_conv2d *desc, int pass, int m_bits, size_t *bytes)
+int conv_common(const Mode &md, const amsim_conv2d *desc, int pass, const void *in0, const void *in1, void *out,
+                const uint32_t *lut, int m_bits, void *workspace, size_t workspace_bytes, Plan *p)
 {
-    if (!bytes) return AMSIM_ERR_INVALID_ARG;
-    if (!valid_m(m_bits)) return AMSIM_ERR_UNSUPPORTED;
-    if (pass < AMSIM_CONV_FWD || pass > AMSIM_CONV_BWD_WEIGHT) return AMSIM_ERR_INVALID_ARG;
-    const int rc = check_conv(desc);
+    if (!md.native && !valid_m(m_bits)) return AMSIM_ERR_UNSUPPORTED;
+    const int rc = check_conv(desc, pass);
     if (rc != AMSIM_OK) return rc;
-    *bytes = plan_conv(desc, pass, m_bits).total;
-    return AMSIM_OK;
-}
-
-static int conv_common(const amsim_conv2d *desc, int pass, const void *in0, const void *in1, void *out,
-                       const uint32_t *lut, int m_bits, void *workspace, size_t workspace_bytes, Plan *p)
-{
-    if (!valid_m(m_bits)) return AMSIM_ERR_UNSUPPORTED;
-    const int rc = check_conv(desc);
-    if (rc != AMSIM_OK) return rc;
-    if (!in0 || !in1 || !out || !lut) return AMSIM_ERR_INVALID_ARG;
-    *p = plan_conv(desc, pass, m_bits);
+    if (!in0 || !in1 || !out || (!lut && !md.native)) return AMSIM_ERR_INVALID_ARG;
+    *p = plan_conv(desc, pass, plan_m(md, m_bits), md.native != 0);
     if (p->total > 0 && (!workspace || workspace_bytes < p->total)) return AMSIM_ERR_WORKSPACE;
     if (ensure_attributes() != AMSIM_OK) return AMSIM_ERR_HIP;
     return AMSIM_OK;
 }
 
-// Decoded copy of an NHWC tensor, zero-padded (table path) or as is (global path).  Returns the
-// number of workgroups (statistics words written when stats is not null).
-static int decode_nhwc(const float *src, int n, int h, int w, int c, int top, int left, int hp, int wp, uint32_t *dst,
-                       int m_bits, int shift, uint32_t *stats, hipStream_t st)
+// Step-pair records of an NHWC tensor inside its zero border (the backward-weight pass's x).
+// Returns the number of workgroups (statistics words written when stats is not null).
+int decode_pairs(const float *src, int n, int h, int w, int c, int top, int left, int hp, int wp, int sw, uint32_t *dst,
+                 const DecFmt &f, uint32_t *stats, hipStream_t st)
 {
     const int grid = int(std::min<int64_t>(int64_t(n) * hp, kStatSlots));  // one padded image row per workgroup
-    hipLaunchKernelGGL(decode_pad_kernel, dim3(grid), dim3(256), 0, st, src, n, h, w, c, top, left, hp, wp, dst,
-                       m_bits, shift, 0u, stats);
+    hipLaunchKernelGGL(decode_pad_pairs_kernel, dim3(grid), dim3(256), 0, st, src, n, h, w, c, top, left, hp, wp, sw,
+                       dst, f, stats);
     return grid;
 }
 
-static int decode_nhcw(const float *src, int n, int h, int w, int c, int top, int left, int hp, int wp, uint32_t *dst,
-                       int m_bits, int shift, uint32_t *stats, hipStream_t st)
+// rec_c: channels of a record row (cp = ceil(rec_c / 2) records).
+int decode_nhcw(const float *src, int n, int h, int w, int c, int top, int left, int hp, int wp, uint32_t *dst,
+                const DecFmt &f, uint32_t *stats, int rec_c, hipStream_t st)
 {
     int cc = std::max(2, std::min(c, kNhcwTile / (w | 1)));  // channels per LDS tile
     if (cc < c) cc &= ~1;  // chunks hold whole channel pairs
     const int grid = int(std::min<int64_t>(int64_t(n) * hp, kStatSlots));  // one padded image row at a time
     hipLaunchKernelGGL(decode_pad_nhcw_kernel, dim3(grid), dim3(256), size_t(cc) * (w | 1) * 4, st, src, n, h, w, c,
-                       top, left, hp, wp, dst, m_bits, shift, 0u, stats, cc);
+                       top, left, hp, wp, dst, f, stats, cc, (rec_c + 1) / 2);
     return grid;
 }
 
-int approx_conv2d_fwd(const amsim_conv2d *desc, const float *x, const float *w, float *y, const uint32_t *lut,
-                      int m_bits, void *workspace, size_t workspace_bytes, void *stream)
+int conv_fwd_run(const Mode &md, const amsim_conv2d *desc, const float *x, const float *w, float *y,
+                 const uint32_t *lut, int m_bits, void *workspace, size_t workspace_bytes, hipStream_t st)
 {
     Plan p;
-    int rc = conv_common(desc, AMSIM_CONV_FWD, x, w, y, lut, m_bits, workspace, workspace_bytes, &p);
+    int rc = conv_common(md, desc, AMSIM_CONV_FWD, x, w, y, lut, m_bits, workspace, workspace_bytes, &p);
     if (rc != AMSIM_OK) return rc;
-    hipStream_t st = static_cast<hipStream_t>(stream);
+    const int mb = plan_m(md, m_bits);
     const ConvShape s = shape_of(desc);
     char *ws = static_cast<char *>(workspace);
     uint32_t *Xd = reinterpret_cast<uint32_t *>(ws + p.off_a);
     uint32_t *Wd = reinterpret_cast<uint32_t *>(ws + p.off_b);
+    uint32_t *sa = md.native ? nullptr : stats_a(ws, p), *sb = md.native ? nullptr : stats_b(ws, p);
+    const Tile t = p.tile;
+    const int64_t rows = int64_t(s.n) * s.oh * s.ow;
+    float *out = p.splits > 1 ? reinterpret_cast<float *>(ws + p.off_part) : y;
+    TabArgs a = tab_args(p, ws, Xd, p.a_elems, Wd, out, int(rows), s.co);
     int n_a;
     if (p.unfold_w) {
         n_a = int(std::min<int64_t>(int64_t(s.n) * p.Hp, kStatSlots));  // one padded image row at a time
-        hipLaunchKernelGGL(decode_unfold_w_kernel, dim3(n_a), dim3(256), size_t(s.w) * s.ci * 4, st, x, s.n, s.h,
-                           s.w, s.ci, s.pt, s.pl, p.Hp, s.kw, s.sw, s.ow, Xd, m_bits, shift_first(m_bits),
-                           stats_a(ws, p));
+        hipLaunchKernelGGL(decode_unfold_w_kernel, dim3(n_a), dim3(256), size_t(s.w) * s.ci * 4, st, x, s.n, s.h, s.w,
+                           s.ci, s.pt, s.pl, p.Hp, s.kw, s.sw, s.ow, Xd, fmt_first(md, mb), sa);
     } else {
-        n_a = decode_nhcw(x, s.n, s.h, s.w, s.ci, s.pt, s.pl, p.Hp, p.Wp, Xd, m_bits, shift_first(m_bits),
-                          stats_a(ws, p), st);
+        n_a = decode_nhcw(x, s.n, s.h, s.w, s.ci, s.pt, s.pl, p.Hp, p.Wp, Xd, fmt_first(md, mb), sa, p.rec_c, st);
     }
     // w [kh][kw * ci][co] as batches kh of kw * ci rows (unfolded: padded to cu rows with +0)
     const int kwc = s.kw * s.ci, wrows = p.unfold_w ? unfolded_channels(s) : kwc;
     const int n_b = decode_grid(int64_t(s.kh) * wrows * p.b_ld);
     hipLaunchKernelGGL(decode_kernel, dim3(n_b), dim3(256), 0, st, w, int64_t(kwc) * s.co, int64_t(s.co), int64_t(1),
-                       s.kh, wrows, kwc, s.co, Wd, int(p.b_ld), m_bits, shift_second(m_bits), zidx_second(p),
-                       stats_b(ws, p), decode_vec(w, int64_t(kwc) * s.co, s.co, 1));
+                       s.kh, wrows, kwc, s.co, Wd, int(p.b_ld), fmt_second(md, p, mb), sb,
+                       decode_vec(w, int64_t(kwc) * s.co, s.co, 1));
     if (launch_status() != AMSIM_OK) return AMSIM_ERR_HIP;
-    if (prep_rows(lut, m_bits, ws, p, n_a, n_b, st) != AMSIM_OK) return AMSIM_ERR_HIP;
-    const Tile t = p.tile;
-    const int64_t rows = int64_t(s.n) * s.oh * s.ow;
-    float *out = p.splits > 1 ? reinterpret_cast<float *>(ws + p.off_part) : y;
-    TabArgs a = tab_args(p, ws, Xd, p.a_elems, Wd, out, int(rows), s.co);
+    if (!md.native && prep_rows(lut, mb, ws, p, n_a, n_b, md, st) != AMSIM_OK) return AMSIM_ERR_HIP;
+    set_format_scales(a, md);
     a.s = p.unfold_w ? unfolded_shape(s) : s;
-    a.rec_c = p.unfold_w ? unfolded_channels(s) : s.ci;
     a.csplit = p.csplit;
     dim3 grid(unsigned(ceil_div(rows, int64_t(64) * t.wr * t.tm)), unsigned(p.b_ld / tab_cols(t)),
               unsigned(p.splits));
     {
-        TimedLaunch tl(AMSIM_KERNEL_CONV_FWD, st);
-        rc = launch_tab<OP_FWD>(p, a, grid, st);
+        TimedLaunch tl(md.native ? AMSIM_KERNEL_CONV_FWD_NATIVE : AMSIM_KERNEL_CONV_FWD, st);
+        rc = tab_launch<OP_FWD>(p.tile, p.rl, tab_variant(md), a, grid, st) == hipSuccess
+                 ? AMSIM_OK
+                 : AMSIM_ERR_HIP;
     }
     if (rc != AMSIM_OK || p.splits == 1) return rc;
     launch_reduce(reinterpret_cast<const float *>(ws + p.off_part), p.splits, int(rows), s.co, y, int64_t(s.co), st);
@@ -1477,90 +1670,113 @@ int approx_conv2d_fwd(const amsim_conv2d *desc, const float *x, const float *w, 
 }
 
 // The backward-data pass of `desc` (the caller's, or the virtual unfolded one) under plan p, into dx.
-static int bwd_data_run(const amsim_conv2d *desc, const Plan &p, const float *dy, const float *w, float *dx,
-                        const uint32_t *lut, int m_bits, void *workspace, hipStream_t st)
+int bwd_data_run(const Mode &md, const amsim_conv2d *desc, const Plan &p, const float *dy, const float *w, float *dx,
+                 const uint32_t *lut, int m_bits, void *workspace, hipStream_t st)
 {
     int rc;
+    const int mb = plan_m(md, m_bits);
     const ConvShape s = shape_of(desc);
     char *ws = static_cast<char *>(workspace);
     uint32_t *Dyd = reinterpret_cast<uint32_t *>(ws + p.off_a);
     uint32_t *Wtd = reinterpret_cast<uint32_t *>(ws + p.off_b);
-    const int n_a = decode_nhcw(dy, s.n, s.oh, s.ow, s.co, p.pad_oh, p.pad_ow, p.OHp, p.OWp, Dyd, m_bits,
-                                shift_first(m_bits), stats_a(ws, p), st);
-    // w[kh][kw][ci][co] -> Wt[kh][kw][co][ci]: batches (kh,kw), rows co, cols ci
-    const int n_b = decode_grid(int64_t(s.kh) * s.kw * s.co * p.b_ld);
-    hipLaunchKernelGGL(decode_kernel, dim3(n_b), dim3(256), 0, st, w, int64_t(s.ci) * s.co, int64_t(1), int64_t(s.co),
-                       s.kh * s.kw, s.co, s.co, s.ci, Wtd, int(p.b_ld), m_bits, shift_second(m_bits), zidx_second(p),
-                       stats_b(ws, p), 0);
-    if (launch_status() != AMSIM_OK) return AMSIM_ERR_HIP;
-    if (prep_rows(lut, m_bits, ws, p, n_a, n_b, st) != AMSIM_OK) return AMSIM_ERR_HIP;
+    uint32_t *sa = md.native ? nullptr : stats_a(ws, p), *sb = md.native ? nullptr : stats_b(ws, p);
     const Tile t = p.tile;
     const int64_t rows = bwd_data_rows(s);
     float *out = p.splits > 1 ? reinterpret_cast<float *>(ws + p.off_part) : dx;
     TabArgs a = tab_args(p, ws, Dyd, p.a_elems, Wtd, out, int(rows), s.ci);
+    const int n_a = decode_nhcw(dy, s.n, s.oh, s.ow, s.co, p.pad_oh, p.pad_ow, p.OHp, p.OWp, Dyd, fmt_first(md, mb), sa,
+                                p.rec_c, st);
+    // w[kh][kw][ci][co] -> Wt[kh][kw][co][ci]: batches (kh,kw), rows co, cols ci
+    const int n_b = decode_grid(int64_t(s.kh) * s.kw * s.co * p.b_ld);
+    hipLaunchKernelGGL(decode_kernel, dim3(n_b), dim3(256), 0, st, w, int64_t(s.ci) * s.co, int64_t(1), int64_t(s.co),
+                       s.kh * s.kw, s.co, s.co, s.ci, Wtd, int(p.b_ld), fmt_second(md, p, mb), sb, 0);
+    if (launch_status() != AMSIM_OK) return AMSIM_ERR_HIP;
+    if (!md.native && prep_rows(lut, mb, ws, p, n_a, n_b, md, st) != AMSIM_OK) return AMSIM_ERR_HIP;
+    set_format_scales(a, md);
     a.s = s;
     a.csplit = p.csplit;
     dim3 grid(unsigned(ceil_div(rows, int64_t(64) * t.wr * t.tm)), unsigned(p.b_ld / tab_cols(t)),
               unsigned(s.sh * s.sw * p.splits));
     {
-        TimedLaunch tl(AMSIM_KERNEL_CONV_BWD_DATA, st);
-        rc = launch_tab<OP_BWD_DATA>(p, a, grid, st);
+        TimedLaunch tl(md.native ? AMSIM_KERNEL_CONV_BWD_DATA_NATIVE : AMSIM_KERNEL_CONV_BWD_DATA, st);
+        rc = tab_launch<OP_BWD_DATA>(p.tile, p.rl, tab_variant(md), a, grid, st) == hipSuccess
+                 ? AMSIM_OK
+                 : AMSIM_ERR_HIP;
     }
-    if (rc != AMSIM_OK || p.splits == 1) return rc;
-    launch_reduce(reinterpret_cast<const float *>(ws + p.off_part), p.splits, s.n * s.h * s.w, s.ci, dx, int64_t(s.ci),
-                  st);
+    if (rc != AMSIM_OK) return rc;
+    if (p.splits > 1) {
+        launch_reduce(reinterpret_cast<const float *>(ws + p.off_part), p.splits, s.n * s.h * s.w, s.ci, dx,
+                      int64_t(s.ci), st);
+        if (launch_status() != AMSIM_OK) return AMSIM_ERR_HIP;
+    }
+    if (s.sh * s.sw > 1) {  // the taps outside each output's stride phase (dilation zeros)
+        uint32_t *pf = reinterpret_cast<uint32_t *>(ws + p.off_bflags);
+        hipLaunchKernelGGL(zero_tap_flags_kernel, dim3(grid_for(int64_t(s.sh) * s.sw * s.ci)), dim3(256), 0, st, w,
+                           s.kh, s.kw, s.ci, s.co, s.sh, s.sw, s.pt, s.pl, fmt_hi(md), md.sat, pf, nullptr);
+        const int64_t total = int64_t(s.n) * s.h * s.w * s.ci;
+        hipLaunchKernelGGL(dilation_fixup_kernel, dim3(grid_for(total)), dim3(256), 0, st, dx, total, s.h, s.w, s.ci,
+                           s.sh, s.sw, pf);
+    }
     return launch_status();
 }
 
-int approx_conv2d_bwd_data(const amsim_conv2d *desc, const float *dy, const float *w, float *dx,
-                           const uint32_t *lut, int m_bits, void *workspace, size_t workspace_bytes, void *stream)
+int conv_bwd_data_run(const Mode &md, const amsim_conv2d *desc, const float *dy, const float *w, float *dx,
+                      const uint32_t *lut, int m_bits, void *workspace, size_t workspace_bytes, hipStream_t st)
 {
     Plan p;
-    int rc = conv_common(desc, AMSIM_CONV_BWD_DATA, dy, w, dx, lut, m_bits, workspace, workspace_bytes, &p);
+    int rc = conv_common(md, desc, AMSIM_CONV_BWD_DATA, dy, w, dx, lut, m_bits, workspace, workspace_bytes, &p);
     if (rc != AMSIM_OK) return rc;
-    hipStream_t st = static_cast<hipStream_t>(stream);
-    if (!p.unfold_w) return bwd_data_run(desc, p, dy, w, dx, lut, m_bits, workspace, st);
+    if (!p.unfold_w) return bwd_data_run(md, desc, p, dy, w, dx, lut, m_bits, workspace, st);
     // the unfolded input's gradient, then folded back onto x's pixels
     const amsim_conv2d v = unfolded_desc(desc);
     float *dxu = reinterpret_cast<float *>(static_cast<char *>(workspace) + p.off_unf);
-    rc = bwd_data_run(&v, p, dy, w, dxu, lut, m_bits, workspace, st);
+    rc = bwd_data_run(md, &v, p, dy, w, dxu, lut, m_bits, workspace, st);
     if (rc != AMSIM_OK) return rc;
+    // the zero products of the kw taps that reach no output column (see fold_w_kernel), after the
+    // virtual pass's phase flags
+    uint32_t *kf = reinterpret_cast<uint32_t *>(static_cast<char *>(workspace) + p.off_bflags) +
+                   size_t(v.stride_h) * v.stride_w * v.c_in;
+    hipLaunchKernelGGL(zero_tap_flags_kernel, dim3(grid_for(int64_t(desc->kw) * desc->c_in)), dim3(256), 0, st, w,
+                       desc->kh, desc->kw, desc->c_in, desc->c_out, 1, 1, 0, 0, fmt_hi(md), md.sat, nullptr, kf);
     const int64_t total = int64_t(desc->n) * desc->h * desc->w * desc->c_in;
     hipLaunchKernelGGL(fold_w_kernel, dim3(grid_for(total)), dim3(256), 0, st, dxu, desc->n, desc->h, desc->w,
-                       desc->c_in, desc->kw, desc->stride_w, desc->pad_left, v.w, dx);
+                       desc->c_in, desc->kw, desc->stride_w, desc->pad_left, v.w, kf, dx);
     return launch_status();
 }
 
-int approx_conv2d_bwd_weight(const amsim_conv2d *desc, const float *x, const float *dy, float *dw,
-                             const uint32_t *lut, int m_bits, void *workspace, size_t workspace_bytes, void *stream)
+int conv_bwd_weight_run(const Mode &md, const amsim_conv2d *desc, const float *x, const float *dy, float *dw,
+                        const uint32_t *lut, int m_bits, void *workspace, size_t workspace_bytes, hipStream_t st)
 {
     Plan p;
-    int rc = conv_common(desc, AMSIM_CONV_BWD_WEIGHT, x, dy, dw, lut, m_bits, workspace, workspace_bytes, &p);
+    int rc = conv_common(md, desc, AMSIM_CONV_BWD_WEIGHT, x, dy, dw, lut, m_bits, workspace, workspace_bytes, &p);
     if (rc != AMSIM_OK) return rc;
-    hipStream_t st = static_cast<hipStream_t>(stream);
+    const int mb = plan_m(md, m_bits);
     const ConvShape s = shape_of(desc);
     char *ws = static_cast<char *>(workspace);
     uint32_t *Xd = reinterpret_cast<uint32_t *>(ws + p.off_a);
     uint32_t *Dyd = reinterpret_cast<uint32_t *>(ws + p.off_b);
-    const int n_a = decode_nhwc(x, s.n, s.h, s.w, s.ci, s.pt, s.pl, p.Hp, p.Wp, Xd, m_bits, shift_first(m_bits),
-                                stats_a(ws, p), st);
+    uint32_t *sa = md.native ? nullptr : stats_a(ws, p), *sb = md.native ? nullptr : stats_b(ws, p);
+    const int n_a = decode_pairs(x, s.n, s.h, s.w, s.ci, s.pt, s.pl, p.Hp, p.Wp, s.sw, Xd, fmt_first(md, mb), sa, st);
     const int64_t npo = int64_t(s.n) * s.oh * s.ow;
     const int n_b = decode_grid(npo * p.b_ld);
     hipLaunchKernelGGL(decode_kernel, dim3(n_b), dim3(256), 0, st, dy, int64_t(0), int64_t(s.co), int64_t(1), 1,
-                       int(npo), int(npo), s.co, Dyd, int(p.b_ld), m_bits, shift_second(m_bits), zidx_second(p),
-                       stats_b(ws, p), decode_vec(dy, 0, s.co, 1));
+                       int(npo), int(npo), s.co, Dyd, int(p.b_ld), fmt_second(md, p, mb), sb,
+                       decode_vec(dy, 0, s.co, 1));
     if (launch_status() != AMSIM_OK) return AMSIM_ERR_HIP;
-    if (prep_rows(lut, m_bits, ws, p, n_a, n_b, st) != AMSIM_OK) return AMSIM_ERR_HIP;
+    if (!md.native && prep_rows(lut, mb, ws, p, n_a, n_b, md, st) != AMSIM_OK) return AMSIM_ERR_HIP;
     const Tile t = p.tile;
     const int R = s.kh * s.kw * s.ci;
     float *out = p.splits > 1 ? reinterpret_cast<float *>(ws + p.off_part) : dw;
     {
-        TimedLaunch tl(AMSIM_KERNEL_CONV_BWD_WEIGHT, st);
+        TimedLaunch tl(md.native ? AMSIM_KERNEL_CONV_BWD_WEIGHT_NATIVE : AMSIM_KERNEL_CONV_BWD_WEIGHT, st);
         TabArgs a = tab_args(p, ws, Xd, p.a_elems, Dyd, out, R, s.co);
+        set_format_scales(a, md);
         a.s = s;
         dim3 grid(unsigned(ceil_div(R, int64_t(64) * t.wr * t.tm)), unsigned(p.b_ld / tab_cols(t)),
                   unsigned(p.splits));
-        rc = launch_tab<OP_BWD_WEIGHT>(p, a, grid, st);
+        rc = tab_launch<OP_BWD_WEIGHT>(p.tile, p.rl, tab_variant(md), a, grid, st) == hipSuccess
+                 ? AMSIM_OK
+                 : AMSIM_ERR_HIP;
     }
     if (rc != AMSIM_OK) return AMSIM_ERR_HIP;
     if (p.splits > 1) {
@@ -1568,6 +1784,108 @@ int approx_conv2d_bwd_weight(const amsim_conv2d *desc, const float *x, const flo
         return launch_status();
     }
     return AMSIM_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int amsim_gemm_workspace_size(int trans_a, int trans_b, int64_t m, int64_t n, int64_t k, int m_bits, size_t *bytes)
+{
+    (void)trans_a;
+    (void)trans_b;
+    if (!bytes) return AMSIM_ERR_INVALID_ARG;
+    if (!valid_m(m_bits)) return AMSIM_ERR_UNSUPPORTED;
+    if (m < 0 || n < 0 || k < 0) return AMSIM_ERR_INVALID_ARG;
+    if (m == 0 || n == 0 || k == 0) {
+        *bytes = 0;
+        return AMSIM_OK;
+    }
+    // enough for every option of the call (the native multiply plans its own layout)
+    *bytes = std::max(plan_gemm(m, n, k, m_bits).total, plan_gemm(m, n, k, 7, true).total);
+    return AMSIM_OK;
+}
+
+int approx_gemm(int trans_a, int trans_b, int64_t m, int64_t n, int64_t k, const float *A, int64_t lda,
+                const float *B, int64_t ldb, float *C, int64_t ldc, const uint32_t *lut, int m_bits, void *workspace,
+                size_t workspace_bytes, void *stream)
+{
+    return gemm_run(Mode{}, trans_a, trans_b, m, n, k, A, lda, B, ldb, C, ldc, lut, m_bits, workspace,
+                    workspace_bytes, static_cast<hipStream_t>(stream));
+}
+
+int approx_gemm_ex(const amsim_options *opt, int trans_a, int trans_b, int64_t m, int64_t n, int64_t k,
+                   const float *A, int64_t lda, const float *B, int64_t ldb, float *C, int64_t ldc, const uint32_t *lut,
+                   int m_bits, void *workspace, size_t workspace_bytes, void *stream)
+{
+    Mode md;
+    const int rc = mode_of(opt, md);
+    if (rc != AMSIM_OK) return rc;
+    return gemm_run(md, trans_a, trans_b, m, n, k, A, lda, B, ldb, C, ldc, lut, m_bits, workspace, workspace_bytes,
+                    static_cast<hipStream_t>(stream));
+}
+
+int amsim_conv2d_workspace_size(const amsim_conv2d *desc, int pass, int m_bits, size_t *bytes)
+{
+    if (!bytes) return AMSIM_ERR_INVALID_ARG;
+    if (!valid_m(m_bits)) return AMSIM_ERR_UNSUPPORTED;
+    if (pass < AMSIM_CONV_FWD || pass > AMSIM_CONV_BWD_WEIGHT) return AMSIM_ERR_INVALID_ARG;
+    const int rc = check_conv(desc, pass);
+    if (rc != AMSIM_OK) return rc;
+    *bytes = std::max(plan_conv(desc, pass, m_bits).total, plan_conv(desc, pass, 7, true).total);
+    return AMSIM_OK;
+}
+
+int approx_conv2d_fwd(const amsim_conv2d *desc, const float *x, const float *w, float *y, const uint32_t *lut,
+                      int m_bits, void *workspace, size_t workspace_bytes, void *stream)
+{
+    return conv_fwd_run(Mode{}, desc, x, w, y, lut, m_bits, workspace, workspace_bytes,
+                        static_cast<hipStream_t>(stream));
+}
+
+int approx_conv2d_bwd_data(const amsim_conv2d *desc, const float *dy, const float *w, float *dx,
+                           const uint32_t *lut, int m_bits, void *workspace, size_t workspace_bytes, void *stream)
+{
+    return conv_bwd_data_run(Mode{}, desc, dy, w, dx, lut, m_bits, workspace, workspace_bytes,
+                             static_cast<hipStream_t>(stream));
+}
+
+int approx_conv2d_bwd_weight(const amsim_conv2d *desc, const float *x, const float *dy, float *dw,
+                             const uint32_t *lut, int m_bits, void *workspace, size_t workspace_bytes, void *stream)
+{
+    return conv_bwd_weight_run(Mode{}, desc, x, dy, dw, lut, m_bits, workspace, workspace_bytes,
+                               static_cast<hipStream_t>(stream));
+}
+
+int approx_conv2d_fwd_ex(const amsim_options *opt, const amsim_conv2d *desc, const float *x, const float *w, float *y,
+                         const uint32_t *lut, int m_bits, void *workspace, size_t workspace_bytes, void *stream)
+{
+    Mode md;
+    const int rc = mode_of(opt, md);
+    if (rc != AMSIM_OK) return rc;
+    return conv_fwd_run(md, desc, x, w, y, lut, m_bits, workspace, workspace_bytes, static_cast<hipStream_t>(stream));
+}
+
+int approx_conv2d_bwd_data_ex(const amsim_options *opt, const amsim_conv2d *desc, const float *dy, const float *w,
+                              float *dx, const uint32_t *lut, int m_bits, void *workspace, size_t workspace_bytes,
+                              void *stream)
+{
+    Mode md;
+    const int rc = mode_of(opt, md);
+    if (rc != AMSIM_OK) return rc;
+    return conv_bwd_data_run(md, desc, dy, w, dx, lut, m_bits, workspace, workspace_bytes,
+                             static_cast<hipStream_t>(stream));
+}
+
+int approx_conv2d_bwd_weight_ex(const amsim_options *opt, const amsim_conv2d *desc, const float *x, const float *dy,
+                                float *dw, const uint32_t *lut, int m_bits, void *workspace, size_t workspace_bytes,
+                                void *stream)
+{
+    Mode md;
+    const int rc = mode_of(opt, md);
+    if (rc != AMSIM_OK) return rc;
+    return conv_bwd_weight_run(md, desc, x, dy, dw, lut, m_bits, workspace, workspace_bytes,
+                               static_cast<hipStream_t>(stream));
 }
 
 int approx_gemm_direct(int mode, int m_bits, int64_t m, int64_t n, int64_t k, const float *A, int64_t lda,
@@ -1598,12 +1916,42 @@ int approx_gemm_direct(int mode, int m_bits, int64_t m, int64_t n, int64_t k, co
 
 int approx_mul_ew(int64_t n, const float *a, const float *b, float *c, const uint32_t *lut, int m_bits, void *stream)
 {
+    return approx_mul_ew_ex(nullptr, n, a, b, c, lut, m_bits, stream);
+}
+
+int approx_mul_ew_ex(const amsim_options *opt, int64_t n, const float *a, const float *b, float *c,
+                     const uint32_t *lut, int m_bits, void *stream)
+{
+    Mode md;
+    const int rc = mode_of(opt, md);
+    if (rc != AMSIM_OK) return rc;
+    if (md.native) return AMSIM_ERR_UNSUPPORTED;  // element-wise products are the table's
     if (!valid_m(m_bits)) return AMSIM_ERR_UNSUPPORTED;
     if (n < 0) return AMSIM_ERR_INVALID_ARG;
     if (n == 0) return AMSIM_OK;
     if (!a || !b || !c || !lut) return AMSIM_ERR_INVALID_ARG;
     hipStream_t st = static_cast<hipStream_t>(stream);
-    hipLaunchKernelGGL(mul_ew_kernel, dim3(grid_for(n)), dim3(256), 0, st, n, a, b, c, lut, m_bits);
+    TabArgs sc{};
+    sc.vadd = 0u;
+    sc.su = sc.sd = 1.0f;
+    set_format_scales(sc, md);
+    hipLaunchKernelGGL(mul_ew_kernel, dim3(grid_for(n)), dim3(256), 0, st, n, a, b, c, lut,
+                       dec_fmt(md, m_bits, m_bits, 0u), dec_fmt(md, m_bits, 0, 0u), sc.vadd, sc.su, sc.sd);
+    return launch_status();
+}
+
+int amsim_cast_exponent(int e_bits, int exp_cast, int m_bits, int64_t n, const float *x, float *y, void *stream)
+{
+    const amsim_options o{AMSIM_MULTIPLY_TABLE, e_bits, exp_cast};
+    Mode md;
+    const int rc = mode_of(&o, md);
+    if (rc != AMSIM_OK) return rc;
+    if (!valid_m(m_bits)) return AMSIM_ERR_UNSUPPORTED;
+    if (n < 0) return AMSIM_ERR_INVALID_ARG;
+    if (n == 0) return AMSIM_OK;
+    if (!x || !y) return AMSIM_ERR_INVALID_ARG;
+    DecFmt f = dec_fmt(md, m_bits, 0, 0u);
+    hipLaunchKernelGGL(cast_kernel, dim3(grid_for(n)), dim3(256), 0, static_cast<hipStream_t>(stream), n, x, y, f);
     return launch_status();
 }
 
@@ -1615,7 +1963,7 @@ int amsim_profile_start(int max_launches)
     t.active = false;
     destroy_events(t);
     t.used = 0;
-    for (int k = 0; k < 4; ++k) {
+    for (int k = 0; k < kKernelKinds; ++k) {
         t.launches[k] = 0;
         t.total_ms[k] = 0.0;
     }
@@ -1655,7 +2003,7 @@ int amsim_profile_stop(void)
 
 int amsim_profile_read(int kind, int *launches, double *total_ms)
 {
-    if (kind < 0 || kind > 3 || !launches || !total_ms) return AMSIM_ERR_INVALID_ARG;
+    if (kind < 0 || kind >= kKernelKinds || !launches || !total_ms) return AMSIM_ERR_INVALID_ARG;
     KernelTimer &t = timer();
     std::lock_guard<std::mutex> g(t.mu);
     *launches = t.launches[kind];

@@ -61,15 +61,20 @@ struct TabArgs {
     const unsigned char *rows;      // transposed table rows (exact path)
     const unsigned char *dot_rows;  // the same 1-byte rows in bf16-path staging order
     const unsigned char *hl_rows;   // 2-byte tables: entries split into bf16 halves (hi/lo path)
-    const int *eb;                  // [0] entry width, [1] 1 (2) when the bf16 (hi/lo) path may run
+    const int *eb;                  // [0] entry width, [1] 1 (2) when the bf16 (hi/lo) path may run,
+                                    // [2] 1 when the exact path rounds each product before adding it
+    uint32_t vadd;       // exact path, rounded form: table values scaled by 2^(vadd >> 23) ...
+    float su, sd;        // ... and each product by su, then added times sd (1, 1, 1 for FP32 operands)
     int R, N;            // result rows and columns
     int splits;          // reduction splits: tile z = (phase *) splits + split
-    int chunks_per_split;  // reduction chunks (8 steps each) per split
+    int chunk;           // steps per reduction chunk (8)
+    int chunks_per_split;  // reduction chunks per split
     int64_t out_elems;   // elements of one split's partial result (splits > 1)
     int Mp, K;           // GEMM
     ConvShape s;
     int Hp, Wp;          // zero-padded x (FWD, BWD_WEIGHT)
-    int rec_c;           // FWD: channels of x's record layout [n][hp][rec_c / 2][wp] (s.ci unless unfolded)
+    int rec_c;           // FWD / BWD_DATA: channels of the record layout [n][hp][rec_c / 2][wp] of x / dy
+                         // (s.ci / s.co, or the unfolded kw * ci rounded to even)
     int csplit;          // FWD / BWD_DATA: channel chunks; taps run chunk-major (csplit divides s.ci / s.co
                          // into multiples of 8)
     int OHp, OWp, pad_oh, pad_ow;  // zero-padded dy (BWD_DATA)
@@ -104,8 +109,17 @@ struct TabTap {
     int pbase;  // pair records: the tap's first record (records of pair j / 2 are ustride apart)
 };
 
-// The first operand of the GEMM and of the forward and backward-data passes (whose steps are
-// channels) is decoded into one 12-byte record per lane row and step pair (j, j + 1), j even,
+// Second-operand word of reduction row j (its table row, or with the native multiply its value)
+// for result column col.
+__device__ __forceinline__ uint32_t Bd_word(const TabArgs &a, int j, int col)
+{
+    return a.Bd[int64_t(j) * a.Np + col];
+}
+
+// The first operand of every operation is decoded into one 12-byte record per lane row and step
+// pair (j, j + 1), j even (backward weight: one record per pixel of the zero-bordered x and
+// channel, pairing it with the pixel one stride to its right, so that every kernel column's steps
+// pair up whatever its kw),
 // instead of one word per element: j's 16-bit table-index field (an LDS byte
 // offset on the bf16 path) as a word, the two mantissa-cleared operands as bf16
 // (pa(j) | pa(j+1) << 16), and j+1's index word.  The bf16 path loads a record with one
@@ -114,7 +128,7 @@ struct TabTap {
 template <int OP>
 constexpr bool split_a()
 {
-    return OP == OP_GEMM || OP == OP_FWD || OP == OP_BWD_DATA;
+    return OP == OP_GEMM || OP == OP_FWD || OP == OP_BWD_DATA || OP == OP_BWD_WEIGHT;
 }
 constexpr uint32_t kPairRecordBytes = 12;
 
@@ -227,9 +241,10 @@ __device__ __forceinline__ int tab_row_rec(const TabArgs &a, int row)
         int hq_n, wq_n;
         phase_dims(s, ph, pw, hq_n, wq_n);
         const int wq = row % wq_n, hq = (row / wq_n) % hq_n, n = row / (wq_n * hq_n);
-        return (n * a.OHp + hq) * ((s.co + 1) / 2) * a.OWp + wq;  // records [n][ohp][co/2][owp]
+        return (n * a.OHp + hq) * ((a.rec_c + 1) / 2) * a.OWp + wq;  // records [n][ohp][rec_c/2][owp]
     } else {
-        return 0;
+        const int ci = row % s.ci, kw = (row / s.ci) % s.kw, kh = row / (s.ci * s.kw);
+        return (kh * a.Wp + kw) * s.ci + ci;  // records [n][hp][wp][ci], one per element
     }
 }
 
@@ -297,14 +312,16 @@ __device__ __forceinline__ TabTap tab_tap_raw(const TabArgs &a, int tap)
         t.ubase = ((dh + a.pad_oh) * s.co + c0) * a.OWp + dw + a.pad_ow;  // >= 0: the padding covers every dh, dw
         t.ustride = a.OWp;
         t.bbase = (kh * s.kw + kw) * s.co + c0;
-        t.pbase = ((dh + a.pad_oh) * ((s.co + 1) / 2) + c0 / 2) * a.OWp + dw + a.pad_ow;
+        t.pbase = ((dh + a.pad_oh) * ((a.rec_c + 1) / 2) + c0 / 2) * a.OWp + dw + a.pad_ow;
     } else {
+        // step j = ow reads x at column ow * sw + kw: the record of step pair (j, j + 1) is the one of
+        // column j * sw + kw, 2 sw columns after the previous pair's
         const int n = tap / s.oh, oh = tap % s.oh;
         t.count = s.ow;
         t.ubase = (n * a.Hp + oh * s.sh) * a.Wp * s.ci;
-        t.ustride = s.sw * s.ci;
+        t.ustride = 2 * s.sw * s.ci;
         t.bbase = tap * s.ow;
-        t.pbase = 0;
+        t.pbase = t.ubase;
     }
     return t;
 }
@@ -387,7 +404,14 @@ __device__ __forceinline__ void tab_commit(const u32x4 (&stage)[CPT], const floa
 
 // Workgroup: NW waves as a WR x (NW/WR) grid -- WR row blocks of 64*TM rows, NW/WR column groups
 // of TN columns.  All waves share the LDS tables of the workgroup's TN * NW/WR columns.
-template <int OP, int TM, int TN, int WR, int EB, int NW, int RL>
+// Products: fma(v, pa * pb, acc) (ROUNDED = false), or t = v' * (pa * pb) rounded on its own, then
+// acc = fma(t * su, sd, acc) (ROUNDED = true).  With FP32 operands v' = v and su = sd = 1: the
+// product is Inf when the carry lifts its exponent to 255, whatever the sum.  With a narrower
+// exponent (the decode lowered the heads' exponents by delta, 2 delta = 127 - beta) v' = v * 2^(2
+// delta) makes t the format's product exactly, t * su = t * 2^(2 delta) overflows exactly when that
+// product reaches 2^(beta + 1) (Algorithm 2's overflow rule in the format's constants), and sd =
+// 2^(-2 delta) brings it back unchanged (Inf stays Inf).
+template <int OP, int TM, int TN, int WR, int EB, int NW, int RL, bool ROUNDED>
 __device__ __forceinline__ void tab_body(const TabArgs &a)
 {
     constexpr int NT = 64 * NW;
@@ -427,10 +451,11 @@ __device__ __forceinline__ void tab_body(const TabArgs &a)
     const AView<TM> av = make_aview<OP, TM>(a, abase);
     // this split's chunks, as positions p = tap * (8 * chunks per tap) + step
     const int count = tab_count<OP>(a);
-    const int cpt = (count + 7) / 8;  // chunks per tap
+    const int ch = a.chunk;  // steps per reduction chunk
+    const int cpt = (count + ch - 1) / ch;  // chunks per tap
     const int q_total = tab_taps<OP>(a) * cpt;
     const int q0 = tab_split(a) * a.chunks_per_split;
-    const int p_end = min(q_total, q0 + a.chunks_per_split) * 8;
+    const int p_end = min(q_total, q0 + a.chunks_per_split) * ch;
 
     u32x4 stage[CPT];
     float stage_pb[CPT];
@@ -439,8 +464,8 @@ __device__ __forceinline__ void tab_body(const TabArgs &a)
     uint32_t acur[TM];
     TabTap cur{0, 0, 0, 0, 0};
     int tap = q0 / max(cpt, 1);
-    int c0 = (q0 - tap * cpt) * 8;
-    bool have = q0 * 8 < p_end;
+    int c0 = (q0 - tap * cpt) * ch;
+    bool have = q0 * ch < p_end;
     if (have) {
         cur = tab_tap<OP>(a, tap);
         tab_fetch<TNW, EB, CPT, NT, RL>(stage, stage_pb, cur, c0, a.Bd, a.Np, colw, a.rows);
@@ -458,13 +483,13 @@ __device__ __forceinline__ void tab_body(const TabArgs &a)
             ntap = tap + 1;
             nc0 = 0;
         }
-        const bool has_next = ntap * cpt * 8 + nc0 < p_end;
+        const bool has_next = ntap * cpt * ch + nc0 < p_end;
         if (has_next && ntap != tap) nxt = tab_tap<OP>(a, ntap);
         if (has_next) tab_fetch<TNW, EB, CPT, NT, RL>(stage, stage_pb, nxt, nc0, a.Bd, a.Np, colw, a.rows);
         const unsigned char *tb = smem + buf * SLAB + cg * TN * ROWB;
         const float *pb_s = pbs + buf * KS * TNW + cg * TN;
         // the slab ends at the tap's end or, 8-step chunks being the unit of splits, at the split's
-        const int nslots = live ? min(min(KS, cur.count - c0), p_end - (tap * cpt * 8 + c0)) : 0;
+        const int nslots = live ? min(min(KS, cur.count - c0), p_end - (tap * cpt * ch + c0)) : 0;
         __builtin_amdgcn_s_setprio(3);  // computing waves first, as on the bf16 path
 #pragma unroll
         for (int slot = 0; slot < KS; ++slot) {
@@ -493,8 +518,14 @@ __device__ __forceinline__ void tab_body(const TabArgs &a)
                 const float pb = pb_s[slot * TNW + t];
 #pragma unroll
                 for (int r = 0; r < TM; ++r) {
-                    const float v = tab_value<EB>(vaddr[r] + (slot * TNW + t) * ROWB);
-                    acc[r][t] = __builtin_fmaf(v, pa[r] * pb, acc[r][t]);
+                    if constexpr (ROUNDED) {
+                        const float v = tab_value_scaled<EB>(vaddr[r] + (slot * TNW + t) * ROWB, a.vadd);
+                        const float c = v * (pa[r] * pb);
+                        acc[r][t] = __builtin_fmaf(c * a.su, a.sd, acc[r][t]);
+                    } else {
+                        const float v = tab_value<EB>(vaddr[r] + (slot * TNW + t) * ROWB);
+                        acc[r][t] = __builtin_fmaf(v, pa[r] * pb, acc[r][t]);
+                    }
                 }
             }
 #pragma unroll
@@ -519,6 +550,157 @@ __device__ __forceinline__ void tab_body(const TabArgs &a)
         int ab = 0;
         int64_t ob = 0;
         tab_row<OP>(a, row, ab, ob);  // the output offset, recomputed rather than kept in registers
+        float *dst = out + ob;
+#pragma unroll
+        for (int t = 0; t < TN; ++t) {
+            const int col = col0 + t;
+            if (col < a.N) dst[col] = acc[r][t];
+        }
+    }
+}
+
+// ------------------------------------------------------- native multiply (no table)
+// The same kernels with the native FP32 multiply (the paper's ATnG configuration: its custom kernels
+// with the `*` operator): operands are kept raw by the decode passes (pair records hold the two
+// steps' values in their first and last words), the slab stages the second operand's values only,
+// and every product is one fma into the sum.
+constexpr int kNativeSlabSteps = 16;
+
+template <int OP, int TM>
+__device__ __forceinline__ void load_a_raw(float (&dst)[TM], const AView<TM> &av, uint32_t so, int j)
+{
+#pragma unroll
+    for (int r = 0; r < TM; ++r) {
+        if constexpr (split_a<OP>()) {
+            const u32x2 d = __builtin_amdgcn_raw_buffer_load_b64(av.words, av.aoff[r], so + (j & 1) * 4u, 0);
+            dst[r] = __uint_as_float((j & 1) ? d.y : d.x);
+        } else {
+            dst[r] = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(av.words, av.aoff[r], so, 0));
+        }
+    }
+}
+
+template <int OP, int TM, int TN, int WR, int NW>
+__device__ __forceinline__ void tab_body_native(const TabArgs &a)
+{
+    constexpr int NT = 64 * NW;
+    constexpr int WC = NW / WR;
+    constexpr int TNW = TN * WC;
+    constexpr int KS = kNativeSlabSteps;
+    constexpr int CPT = (KS * TNW + NT - 1) / NT;  // staged values per thread per slab
+    extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
+    float *bs = reinterpret_cast<float *>(smem);  // [2][KS][TNW] second-operand values
+
+    const int R = tab_rows<OP>(a);
+    if (a.tx * 64 * TM * WR >= R) return;  // uniform over the workgroup
+    const int lane = threadIdx.x & 63;
+    const int wave = wave_id();
+    const int rg = wave % WR, cg = wave / WR;
+    const int row0 = a.tx * (64 * TM * WR) + rg * (64 * TM) + lane;
+    const bool live = row0 - lane < R;
+    const int colw = a.ty * TNW;
+    const int col0 = colw + cg * TN;
+    int abase[TM];
+#pragma unroll
+    for (int r = 0; r < TM; ++r) {
+        const int row = row0 + 64 * r;
+        int ab = 0;
+        int64_t ob = 0;
+        if (row < R) {
+            tab_row<OP>(a, row, ab, ob);
+            if constexpr (split_a<OP>()) ab = tab_row_rec<OP>(a, row);
+        }
+        abase[r] = ab;
+    }
+    const AView<TM> av = make_aview<OP, TM>(a, abase);
+    const int count = tab_count<OP>(a);
+    const int ch = a.chunk;
+    const int cpt = (count + ch - 1) / ch;
+    const int q_total = tab_taps<OP>(a) * cpt;
+    const int q0 = tab_split(a) * a.chunks_per_split;
+    const int p_end = min(q_total, q0 + a.chunks_per_split) * ch;
+
+    float stage[CPT];
+    auto fetch = [&](const TabTap &tp, int c) __attribute__((always_inline)) {
+#pragma unroll
+        for (int i = 0; i < CPT; ++i) {
+            const int e = int(threadIdx.x) + i * NT;
+            const int slot = e / TNW, t = e % TNW;
+            const int j = c + slot;
+            stage[i] = (e < KS * TNW && j < tp.count) ? __uint_as_float(Bd_word(a, tp.bbase + j, colw + t)) : 0.0f;
+        }
+    };
+    auto commit = [&](int buf) __attribute__((always_inline)) {
+#pragma unroll
+        for (int i = 0; i < CPT; ++i) {
+            const int e = int(threadIdx.x) + i * NT;
+            if (e < KS * TNW) bs[buf * KS * TNW + e] = stage[i];
+        }
+    };
+    float acc[TM][TN];
+    init_acc(acc);
+    TabTap cur{0, 0, 0, 0, 0};
+    int tap = q0 / max(cpt, 1);
+    int c0 = (q0 - tap * cpt) * ch;
+    bool have = q0 * ch < p_end;
+    if (have) {
+        cur = tab_tap<OP>(a, tap);
+        fetch(cur, c0);
+        commit(0);
+    }
+    __syncthreads();
+    int buf = 0;
+    while (have) {
+        uniform_cursor(cur, tap, c0);
+        TabTap nxt = cur;
+        int ntap = tap, nc0 = c0 + KS;
+        if (nc0 >= count) {
+            ntap = tap + 1;
+            nc0 = 0;
+        }
+        const bool has_next = ntap * cpt * ch + nc0 < p_end;
+        if (has_next && ntap != tap) nxt = tab_tap<OP>(a, ntap);
+        if (has_next) fetch(nxt, nc0);
+        const int nslots = live ? min(min(KS, cur.count - c0), p_end - (tap * cpt * ch + c0)) : 0;
+        const float *bsl = bs + buf * KS * TNW + cg * TN;
+        float av0[TM];
+        if (nslots > 0) load_a_raw<OP, TM>(av0, av, __builtin_amdgcn_readfirstlane(a_step_offset<OP>(cur, c0)), c0);
+#pragma unroll
+        for (int slot = 0; slot < KS; ++slot) {
+            if (slot >= nslots) break;
+            float an[TM];
+            if (slot + 1 < nslots) {
+                const uint32_t so = __builtin_amdgcn_readfirstlane(a_step_offset<OP>(cur, c0 + slot + 1));
+                load_a_raw<OP, TM>(an, av, so, c0 + slot + 1);
+            }
+#pragma unroll
+            for (int t = 0; t < TN; ++t) {
+                const float b = bsl[slot * TNW + t];
+#pragma unroll
+                for (int r = 0; r < TM; ++r) acc[r][t] = __builtin_fmaf(av0[r], b, acc[r][t]);
+            }
+            if (slot + 1 < nslots) {
+#pragma unroll
+                for (int r = 0; r < TM; ++r) av0[r] = an[r];
+            }
+        }
+        if (has_next) commit(buf ^ 1);
+        __syncthreads();
+        cur = nxt;
+        tap = ntap;
+        c0 = nc0;
+        buf ^= 1;
+        have = has_next;
+    }
+
+    float *out = a.out + int64_t(tab_split(a)) * a.out_elems;
+#pragma unroll
+    for (int r = 0; r < TM; ++r) {
+        const int row = row0 + 64 * r;
+        if (row >= R) continue;
+        int ab = 0;
+        int64_t ob = 0;
+        tab_row<OP>(a, row, ab, ob);
         float *dst = out + ob;
 #pragma unroll
         for (int t = 0; t < TN; ++t) {
@@ -674,7 +856,7 @@ __device__ __forceinline__ void dot_load_pair(uint32_t (&dst)[split_a<OP>() ? 3 
 // outputs (or of the split's partial sums).
 template <int OP, int TM, int TN>
 __device__ __forceinline__ void dot_finish(const TabArgs &a, float (&acc)[TM][TN], const AView<TM> &av, int row0,
-                                           int col0, int R, int q0, int cpt, int p_end)
+                                           int col0, int R, int q0, int cpt, int p_end, int ch)
 {
     // Signs of zero sums: -0 when every product of the split's range is -0, else +0.  The first
     // product that is not -0 (non-zero, or +0) settles an output as +0, so the pass stops once no
@@ -689,11 +871,11 @@ __device__ __forceinline__ void dot_finish(const TabArgs &a, float (&acc)[TM][TN
     const uint32_t zero = pending;
     if (__builtin_amdgcn_ballot_w64(pending != 0u) != 0u) {
         bool open = true;
-        for (int tp_i = q0 / max(cpt, 1); open && tp_i * cpt * 8 < p_end; ++tp_i) {
-            const int pbase = tp_i * cpt * 8;
+        for (int tp_i = q0 / max(cpt, 1); open && tp_i * cpt * ch < p_end; ++tp_i) {
+            const int pbase = tp_i * cpt * ch;
             const TabTap tp = tab_tap<OP>(a, tp_i);
             const int j1 = min(tp.count, p_end - pbase);
-            for (int j = max(q0 * 8 - pbase, 0); j < j1; ++j) {
+            for (int j = max(q0 * ch - pbase, 0); j < j1; ++j) {
                 uint32_t aw[TM];
                 load_a_words<OP, TM>(aw, av, __builtin_amdgcn_readfirstlane(a_step_offset<OP>(tp, j)), j);
                 const uint32_t *brow = a.Bd + int64_t(tp.bbase + j) * a.Np + col0;
@@ -771,10 +953,11 @@ __device__ __forceinline__ void tab_body_dot(const TabArgs &a)
     }
     const AView<TM> av = make_aview<OP, TM>(a, abase);
     const int count = tab_count<OP>(a);
-    const int cpt = (count + 7) / 8;
+    const int ch = a.chunk;
+    const int cpt = (count + ch - 1) / ch;
     const int q_total = tab_taps<OP>(a) * cpt;
     const int q0 = tab_split(a) * a.chunks_per_split;
-    const int p_end = min(q_total, q0 + a.chunks_per_split) * 8;
+    const int p_end = min(q_total, q0 + a.chunks_per_split) * ch;
 
     // Staging pipeline: while slab s is computed, the table bytes of slab s + 1 are fetched (its
     // second-operand words `sbw` having arrived during slab s - 1) and the second-operand words
@@ -807,13 +990,13 @@ __device__ __forceinline__ void tab_body_dot(const TabArgs &a)
             otap = tp_ + 1;
             oc = 0;
         }
-        ok = otap * cpt * 8 + oc < p_end;
+        ok = otap * cpt * ch + oc < p_end;
         if (ok && otap != tp_) o = tab_tap<OP>(a, otap);
     };
     TabTap cur{0, 0, 0, 0, 0};
     int tap = q0 / max(cpt, 1);
-    int c0 = (q0 - tap * cpt) * 8;
-    bool have = q0 * 8 < p_end;
+    int c0 = (q0 - tap * cpt) * ch;
+    bool have = q0 * ch < p_end;
     TabTap nxt{0, 0, 0, 0, 0};
     int ntap = 0, nc0 = 0;
     bool has_next = false;
@@ -848,7 +1031,7 @@ __device__ __forceinline__ void tab_body_dot(const TabArgs &a)
             dot_fetch_rows<DC>(srw, sbw, rres);
         }
         // the slab ends at the tap's end or, 8-step chunks being the unit of splits, at the split's
-        const int nslots = min(min(KS, cur.count - c0), p_end - (tap * cpt * 8 + c0));
+        const int nslots = min(min(KS, cur.count - c0), p_end - (tap * cpt * ch + c0));
         // a wave whose rows all lie past the end only stages and keeps the barriers
         const int npairs = live ? (nslots + 1) / 2 : 0;
         // Waves computing a slab issue ahead of waves staging the next one or waiting at the
@@ -930,7 +1113,7 @@ __device__ __forceinline__ void tab_body_dot(const TabArgs &a)
         slab(std::integral_constant<int, 1>{});
     }
 
-    dot_finish<OP, TM, TN>(a, acc, av, row0, col0, R, q0, cpt, p_end);
+    dot_finish<OP, TM, TN>(a, acc, av, row0, col0, R, q0, cpt, p_end, ch);
 }
 
 // ------------------------------------------------------- bf16 hi/lo path (2-byte tables)
@@ -1029,10 +1212,11 @@ __device__ __forceinline__ void tab_body_hl(const TabArgs &a)
     }
     const AView<TM> av = make_aview<OP, TM>(a, abase);
     const int count = tab_count<OP>(a);
-    const int cpt = (count + 7) / 8;
+    const int ch = a.chunk;
+    const int cpt = (count + ch - 1) / ch;
     const int q_total = tab_taps<OP>(a) * cpt;
     const int q0 = tab_split(a) * a.chunks_per_split;
-    const int p_end = min(q_total, q0 + a.chunks_per_split) * 8;
+    const int p_end = min(q_total, q0 + a.chunks_per_split) * ch;
 
     // while slab s is computed, slab s + 1's second-operand words and row halves are fetched
     u32x4 sbw[2];
@@ -1053,13 +1237,13 @@ __device__ __forceinline__ void tab_body_hl(const TabArgs &a)
             otap = tp_ + 1;
             oc = 0;
         }
-        ok = otap * cpt * 8 + oc < p_end;
+        ok = otap * cpt * ch + oc < p_end;
         if (ok && otap != tp_) o = tab_tap<OP>(a, otap);
     };
     TabTap cur{0, 0, 0, 0, 0};
     int tap = q0 / max(cpt, 1);
-    int c0 = (q0 - tap * cpt) * 8;
-    bool have = q0 * 8 < p_end;
+    int c0 = (q0 - tap * cpt) * ch;
+    bool have = q0 * ch < p_end;
     TabTap nxt{0, 0, 0, 0, 0};
     int ntap = 0, nc0 = 0;
     bool has_next = false;
@@ -1082,7 +1266,7 @@ __device__ __forceinline__ void tab_body_hl(const TabArgs &a)
             hl_fetch_b(sbw, nxt, nc0, a.Bd, a.Np, col0);
             hl_fetch_rows(srw, sbw, rres);
         }
-        const int nslots = min(min(KS, cur.count - c0), p_end - (tap * cpt * 8 + c0));
+        const int nslots = min(min(KS, cur.count - c0), p_end - (tap * cpt * ch + c0));
         const int npairs = live ? (nslots + 1) / 2 : 0;
         __builtin_amdgcn_s_setprio(3);  // computing waves first, as on the bf16 path
 #pragma unroll
@@ -1140,17 +1324,24 @@ __device__ __forceinline__ void tab_body_hl(const TabArgs &a)
         slab(std::integral_constant<int, 1>{});
     }
 
-    dot_finish<OP, TM, TN>(a, acc, av, row0, col0, R, q0, cpt, p_end);
+    dot_finish<OP, TM, TN>(a, acc, av, row0, col0, R, q0, cpt, p_end, ch);
 }
 
 // Four waves per SIMD: the register budget (<= 128 VGPRs) the tiles are sized for.  Without the
 // hint the scheduler minimises registers and serialises the LDS gathers.
 // RL: log2 of the table row length, 7 (rows padded to 128 entries) for M <= 7, else M.
-template <int OP, int TM, int TN, int WR, int NW, int RL>
+// VAR: kTabApprox (the table's products) or kTabNative (the native FP32 multiply, RL = 7 only).
+enum { kTabApprox = 0, kTabNative = 1 };
+
+template <int OP, int TM, int TN, int WR, int NW, int RL, int VAR>
 __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(4, 4))) void tab_kernel(TabArgs args)
 {
     TabArgs a = args;
     tab_tile_id(a.splits, a.tx, a.ty, a.tz);
+    if constexpr (VAR == kTabNative) {
+        tab_body_native<OP, TM, TN, WR, NW>(a);
+        return;
+    }
     const int eb = __builtin_amdgcn_readfirstlane(a.eb[0]);
     if constexpr (RL == 7 && dot_cols_ok(TN) && WR == NW) {
         const int path = __builtin_amdgcn_readfirstlane(a.eb[1]);
@@ -1165,12 +1356,22 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(4, 4)))
             }
         }
     }
-    if (eb == 1)
-        tab_body<OP, TM, TN, WR, 1, NW, RL>(a);
-    else if (eb == 2)
-        tab_body<OP, TM, TN, WR, 2, NW, RL>(a);
-    else
-        tab_body<OP, TM, TN, WR, 4, NW, RL>(a);
+    const int rounded = __builtin_amdgcn_readfirstlane(a.eb[2]);
+    if (rounded) {
+        if (eb == 1)
+            tab_body<OP, TM, TN, WR, 1, NW, RL, true>(a);
+        else if (eb == 2)
+            tab_body<OP, TM, TN, WR, 2, NW, RL, true>(a);
+        else
+            tab_body<OP, TM, TN, WR, 4, NW, RL, true>(a);
+    } else {
+        if (eb == 1)
+            tab_body<OP, TM, TN, WR, 1, NW, RL, false>(a);
+        else if (eb == 2)
+            tab_body<OP, TM, TN, WR, 2, NW, RL, false>(a);
+        else
+            tab_body<OP, TM, TN, WR, 4, NW, RL, false>(a);
+    }
 }
 
 // Dynamic LDS of a table kernel with TN columns per wave, WR of its NW waves along rows and rows
@@ -1180,6 +1381,11 @@ constexpr size_t tab_exact_lds_bytes(int tnw, int rl, int eb)
 {
     return size_t(2) * tab_slab_steps(tnw, rl, eb) * tnw * ((size_t(1) << rl) * eb) +
            size_t(2) * tab_slab_steps(tnw, rl, eb) * tnw * 4;
+}
+
+constexpr size_t tab_native_lds_bytes(int tn, int wr, int nw)
+{
+    return size_t(2) * kNativeSlabSteps * tn * (nw / wr) * 4;
 }
 
 constexpr size_t tab_lds_bytes(int tn, int wr, int nw, int rl)
@@ -1249,11 +1455,11 @@ static_assert(tab_cands_listed(kTabCands, 7, 7) && tab_cands_listed(kWideCands, 
 
 // Per operation (defined in amsim_tab.hip, one instantiation per operation): raise the dynamic
 // LDS limit of every instantiated tile's kernel and check that none uses static LDS; launch the
-// kernel of tile t with rows of 2^rl entries.  Both return the first HIP error, and the launch
+// kernel of tile t with rows of 2^rl entries and variant var (the native multiply: rl = 7).  Both return the first HIP error, and the launch
 // hipErrorInvalidConfiguration for a tile that is not instantiated.
 template <int OP>
 hipError_t tab_attributes();
 template <int OP>
-hipError_t tab_launch(const Tile &t, int rl, const TabArgs &a, dim3 grid, hipStream_t st);
+hipError_t tab_launch(const Tile &t, int rl, int var, const TabArgs &a, dim3 grid, hipStream_t st);
 
 }  // namespace amsim_detail

@@ -45,21 +45,32 @@ template <int OP>
 hipError_t tab_attributes()
 {
     hipError_t err = hipSuccess;
-#define X(TM, TN, WR, NW, RL) allow_lds(tab_kernel<OP, TM, TN, WR, NW, RL>, tab_lds_bytes(TN, WR, NW, RL), err);
+#define X(TM, TN, WR, NW, RL)                                                                              \
+    allow_lds(tab_kernel<OP, TM, TN, WR, NW, RL, kTabApprox>, tab_lds_bytes(TN, WR, NW, RL), err);          \
+    if constexpr (RL == 7)                                                                                  \
+        allow_lds(tab_kernel<OP, TM, TN, WR, NW, 7, kTabNative>, tab_native_lds_bytes(TN, WR, NW), err);
     AMSIM_FOR_TAB_TILES(X)
 #undef X
     return err;
 }
 
 template <int OP>
-hipError_t tab_launch(const Tile &t, int rl, const TabArgs &a, dim3 grid, hipStream_t st)
+hipError_t tab_launch(const Tile &t, int rl, int var, const TabArgs &a, dim3 grid, hipStream_t st)
 {
     bool launched = false;
     auto run = [&](auto tm, auto tn, auto wr, auto nw, auto rl_c) {
         constexpr int TM = decltype(tm)::value, TN = decltype(tn)::value, WR = decltype(wr)::value;
         constexpr int NW = decltype(nw)::value, RL = decltype(rl_c)::value;
-        hipLaunchKernelGGL((tab_kernel<OP, TM, TN, WR, NW, RL>), grid, dim3(64 * NW), tab_lds_bytes(TN, WR, NW, RL),
-                           st, a);
+        if (var == kTabNative) {
+            if constexpr (RL == 7) {
+                hipLaunchKernelGGL((tab_kernel<OP, TM, TN, WR, NW, 7, kTabNative>), grid, dim3(64 * NW),
+                                   tab_native_lds_bytes(TN, WR, NW), st, a);
+                launched = true;
+            }
+            return;
+        }
+        hipLaunchKernelGGL((tab_kernel<OP, TM, TN, WR, NW, RL, kTabApprox>), grid, dim3(64 * NW),
+                           tab_lds_bytes(TN, WR, NW, RL), st, a);
         launched = true;
     };
     dispatch_tab_tile(t, rl, run);
@@ -67,6 +78,6 @@ hipError_t tab_launch(const Tile &t, int rl, const TabArgs &a, dim3 grid, hipStr
 }
 
 template hipError_t tab_attributes<AMSIM_TAB_OP>();
-template hipError_t tab_launch<AMSIM_TAB_OP>(const Tile &, int, const TabArgs &, dim3, hipStream_t);
+template hipError_t tab_launch<AMSIM_TAB_OP>(const Tile &, int, int, const TabArgs &, dim3, hipStream_t);
 
 }  // namespace amsim_detail
