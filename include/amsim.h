@@ -49,6 +49,7 @@ extern "C" {
 #define AMSIM_ERR_WORKSPACE (-4)   /* workspace missing or smaller than the size query says */
 #define AMSIM_ERR_HIP (-5)         /* a HIP runtime call or kernel launch failed */
 #define AMSIM_ERR_IO (-6)          /* file could not be read/written or has a bad header */
+#define AMSIM_ERR_SCRATCH (-7)     /* approx_gemm_noalloc: the call needs more than the fixed buffer */
 
 /* Human-readable name of a status code (static string, never NULL). */
 const char *amsim_status_string(int status);
@@ -108,6 +109,24 @@ int amsim_gemm_workspace_size(int trans_a, int trans_b, int64_t m, int64_t n, in
 int approx_gemm(int trans_a, int trans_b, int64_t m, int64_t n, int64_t k, const float *A, int64_t lda,
                 const float *B, int64_t ldb, float *C, int64_t ldc, const uint32_t *lut, int m_bits,
                 void *workspace, size_t workspace_bytes, void *stream);
+
+/* approx_gemm_noalloc: approx_gemm without a workspace argument, for callers that cannot
+ * allocate device memory (code under HIP graph capture, tight serving loops, harnesses that forbid
+ * hipMalloc).  Same arguments, results and errors as approx_gemm (bit for bit the same C), but the
+ * workspace is a fixed buffer of AMSIM_NOALLOC_SCRATCH_BYTES bytes inside the library, one per GPU,
+ * held from the library's load until the process ends; the call allocates and frees nothing.
+ *   - Returns AMSIM_ERR_SCRATCH, before anything is launched, when the call's workspace
+ *     (amsim_gemm_workspace_size without options: the table path) exceeds the buffer.
+ *   - The buffer used is the current device's; `stream` must belong to that device.  The first
+ *     call on a device looks up its buffer's address (no allocation).
+ *   - Every call on one GPU shares that GPU's buffer and leaves its contents behind (nothing in
+ *     it has to start at zero).  Calls whose work overlaps on one GPU (other streams, other host
+ *     threads without ordering) race on it and give unspecified results: order them on one
+ *     stream or synchronise between them. */
+#define AMSIM_NOALLOC_SCRATCH_BYTES (64u << 20)
+int approx_gemm_noalloc(int trans_a, int trans_b, int64_t m, int64_t n, int64_t k, const float *A, int64_t lda,
+                        const float *B, int64_t ldb, float *C, int64_t ldc, const uint32_t *lut, int m_bits,
+                        void *stream);
 
 /* Direct evaluation: the GEMM with no table, for the comparison the paper draws for AMSim
  * (Sec. "AMSim", its figure of GEMM run time with AMSim, with a direct simulation of the

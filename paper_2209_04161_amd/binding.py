@@ -19,6 +19,8 @@ AMSIM_ERR_MODEL = -3
 AMSIM_ERR_WORKSPACE = -4
 AMSIM_ERR_HIP = -5
 AMSIM_ERR_IO = -6
+AMSIM_ERR_SCRATCH = -7
+AMSIM_NOALLOC_SCRATCH_BYTES = 64 << 20
 
 AMSIM_CONV_FWD = 0
 AMSIM_CONV_BWD_DATA = 1
@@ -105,6 +107,8 @@ def lib():
         "approx_conv2d_bwd_data": ([cp, vp, vp, vp, vp, ctypes.c_int, vp, sz, vp], ctypes.c_int),
         "approx_conv2d_bwd_weight": ([cp, vp, vp, vp, vp, ctypes.c_int, vp, sz, vp], ctypes.c_int),
         "approx_mul_ew": ([i64, vp, vp, vp, vp, ctypes.c_int, vp], ctypes.c_int),
+        "approx_gemm_noalloc": ([ctypes.c_int, ctypes.c_int, i64, i64, i64, vp, i64, vp, i64, vp, i64, vp,
+                                 ctypes.c_int, vp], ctypes.c_int),
         "approx_gemm_ex": ([op, ctypes.c_int, ctypes.c_int, i64, i64, i64, vp, i64, vp, i64, vp, i64, vp,
                             ctypes.c_int, vp, sz, vp], ctypes.c_int),
         "approx_conv2d_fwd_ex": ([op, cp, vp, vp, vp, vp, ctypes.c_int, vp, sz, vp], ctypes.c_int),
@@ -265,10 +269,11 @@ def _gemm_args(A, B, lut, m_bits, trans_a, trans_b, out, workspace, native=False
     if (out.dtype != torch.float32 or out.device != A.device or out.dim() != 2 or tuple(out.shape) != (m, n)
             or (m > 0 and n > 1 and out.stride(1) != 1) or (m > 1 and out.stride(0) < n)):
         raise ValueError("out must be a float32 (%d, %d) tensor on %s with unit column stride" % (m, n, A.device))
-    ws_bytes = amsim_gemm_workspace_size(trans_a, trans_b, m, n, k, m_bits if not native else 7)
-    if workspace is None:
-        workspace = _workspace(ws_bytes, A.device)
-    _check_workspace(workspace, ws_bytes, A.device)
+    if workspace is not False:  # False: the call brings no workspace
+        ws_bytes = amsim_gemm_workspace_size(trans_a, trans_b, m, n, k, m_bits if not native else 7)
+        if workspace is None:
+            workspace = _workspace(ws_bytes, A.device)
+        _check_workspace(workspace, ws_bytes, A.device)
     ldc = out.stride(0) if m > 1 else n
     return m, n, k, out, ldc, workspace
 
@@ -279,6 +284,18 @@ def approx_gemm(A, B, lut, m_bits, trans_a=False, trans_b=False, out=None, works
     _check(lib().approx_gemm(int(trans_a), int(trans_b), m, n, k, _ptr(A), A.shape[1], _ptr(B), B.shape[1],
                              _ptr(out), ldc, _ptr(lut), int(m_bits), _ptr(workspace), workspace.numel(), _stream()),
            "approx_gemm")
+    return out
+
+
+def approx_gemm_noalloc(A, B, lut, m_bits, out, trans_a=False, trans_b=False):
+    """approx_gemm on the library's fixed per-GPU scratch buffer, for callers that cannot allocate:
+    `out` is required and nothing is allocated.  Raises AmsimError (AMSIM_ERR_SCRATCH) when the
+    call needs more than AMSIM_NOALLOC_SCRATCH_BYTES of workspace."""
+    if out is None:
+        raise ValueError("approx_gemm_noalloc: out is required (the call allocates nothing)")
+    m, n, k, out, ldc, _ = _gemm_args(A, B, lut, m_bits, trans_a, trans_b, out, False)
+    _check(lib().approx_gemm_noalloc(int(trans_a), int(trans_b), m, n, k, _ptr(A), A.shape[1], _ptr(B), B.shape[1],
+                                     _ptr(out), ldc, _ptr(lut), int(m_bits), _stream()), "approx_gemm_noalloc")
     return out
 
 

@@ -42,6 +42,7 @@ const char *amsim_status_string(int status)
     case AMSIM_ERR_WORKSPACE: return "workspace missing or too small";
     case AMSIM_ERR_HIP: return "HIP runtime error";
     case AMSIM_ERR_IO: return "table file error";
+    case AMSIM_ERR_SCRATCH: return "call needs more than the fixed scratch buffer (AMSIM_NOALLOC_SCRATCH_BYTES)";
     default: return "unknown status";
     }
 }

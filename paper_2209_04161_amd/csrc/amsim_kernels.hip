@@ -1786,9 +1786,60 @@ int conv_bwd_weight_run(const Mode &md, const amsim_conv2d *desc, const float *x
     return AMSIM_OK;
 }
 
+// ------------------------------------------------------------------ fixed scratch -------
+// The workspace of approx_gemm_noalloc: one array per GPU, held from the library's load until the
+// process ends.  Host code never names it directly (its host-side name is a stand-in, not a
+// device address): scratch_address gets each device's address once, with that device current.
+constexpr size_t kScratchBytes = size_t(AMSIM_NOALLOC_SCRATCH_BYTES);
+static_assert(kScratchBytes % kAlign == 0, "the plans' offsets assume an aligned base");
+static __device__ __align__(256) unsigned char scratch[kScratchBytes];
+
+constexpr int kMaxScratchDevices = 64;
+std::mutex g_scratch_mu;
+void *g_scratch_ptr[kMaxScratchDevices] = {};
+
+// The current device's copy of `scratch` (looked up on the first call per device).
+int scratch_address(void **ptr)
+{
+    int dev = -1;
+    if (hipGetDevice(&dev) != hipSuccess) return AMSIM_ERR_HIP;
+    if (dev < 0 || dev >= kMaxScratchDevices) return AMSIM_ERR_UNSUPPORTED;
+    std::lock_guard<std::mutex> g(g_scratch_mu);
+    if (g_scratch_ptr[dev] == nullptr) {
+        void *p = nullptr;
+        if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || p == nullptr) return AMSIM_ERR_HIP;
+        g_scratch_ptr[dev] = p;
+    }
+    *ptr = g_scratch_ptr[dev];
+    return AMSIM_OK;
+}
+
 }  // namespace
 
 extern "C" {
+
+int approx_gemm_noalloc(int trans_a, int trans_b, int64_t m, int64_t n, int64_t k, const float *A, int64_t lda,
+                        const float *B, int64_t ldb, float *C, int64_t ldc, const uint32_t *lut, int m_bits,
+                        void *stream)
+{
+    // the same argument checks as approx_gemm, then the plan's size against the fixed buffer
+    if (!valid_m(m_bits)) return AMSIM_ERR_UNSUPPORTED;
+    if (m < 0 || n < 0 || k < 0) return AMSIM_ERR_INVALID_ARG;
+    size_t need = 0;
+    if (m > 0 && n > 0 && k > 0) {
+        const int64_t lim = int64_t(1) << 31;
+        if (m >= lim || n >= lim || k >= lim) return AMSIM_ERR_UNSUPPORTED;
+        need = plan_gemm(m, n, k, m_bits).total;
+    }
+    if (need > kScratchBytes) return AMSIM_ERR_SCRATCH;
+    void *ws = nullptr;
+    if (need > 0) {
+        const int rc = scratch_address(&ws);
+        if (rc != AMSIM_OK) return rc;
+    }
+    return gemm_run(Mode{}, trans_a, trans_b, m, n, k, A, lda, B, ldb, C, ldc, lut, m_bits, ws, kScratchBytes,
+                    static_cast<hipStream_t>(stream));
+}
 
 int amsim_gemm_workspace_size(int trans_a, int trans_b, int64_t m, int64_t n, int64_t k, int m_bits, size_t *bytes)
 {
