@@ -11,12 +11,18 @@ Prints one JSON line.  Besides the contract fields it carries
   roofline      the GEMM kernel (the dominant one): algorithmic FLOP (2 per approx-MAC) per
                 launch over its average launch duration, measured with HIP events recorded on
                 its stream inside the timed region, against the FP32 vector peak
-  kernels       per-kernel rates of the step (HIP events on the launch stream)
+  kernels       per-kernel rates of the step (HIP events on the launch stream), then, timed
+                after the step: the 4096^3 GEMM with the M = 11 (2048-entry-row) Mitchell table,
+                the three ResNet-50 layers (batch 32, each pass), the LeNet-5 stack (batch 64,
+                exact bfloat16-truncation table), the step's GEMM and convolution passes with
+                the native FP32 multiply in the same kernels, and the same four with the vendor
+                FP32 libraries torch calls (hipBLASLt / MIOpen, TF32 off).  None of these
+                launches the step GEMM's kernel (other template instances), so a kernel trace of
+                the run still times exactly the launches the roofline is quoted for.
   cpu_baseline  the CPU oracle timed on a seeded sample of the same step's outputs
-  extra         (with --extra only) the M = 11 (wide-table) GEMM, a GEMM size sweep, the
-                ResNet-50 layers and the LeNet-5 stack.  Off by default, so that the default
-                run launches each step kernel with the step's shapes only and a kernel trace of
-                it times exactly the kernels the roofline is quoted for.
+  extra         (with --extra only) a GEMM size sweep, the direct-evaluation GEMMs, a
+                post-ReLU input case, the exact-truncation table on the step and a LeNet-5
+                training step through the autograd layers.
 """
 import argparse
 import hashlib
@@ -82,6 +88,8 @@ def main():
                     help="fraction of each part's outputs the CPU oracle computes for cpu_baseline")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--extra", action="store_true", help="also time the other workloads (see above)")
+    ap.add_argument("--no-other-kernels", action="store_true",
+                    help="time the step only (no M = 11 GEMM, ResNet-50, LeNet-5, native or vendor entries)")
     ap.add_argument("--no-extra", action="store_true", help="(the default; kept for older command lines)")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="also run a plain 256 MiB device copy three times (reference for HBM byte counters)")
@@ -199,6 +207,19 @@ def main():
         "kernels": kernels,
     }
 
+    if not args.no_other_kernels:
+        other = other_kernels(B, W, torch, dev, lut, m_bits, A, Bm, C, cv, (x, w, dy), ws_g, ws_c)
+        native_step = sum(other["native_multiply"][k]["call_ms"] for k in ("gemm", "conv_fwd", "conv_bwd_data",
+                                                                          "conv_bwd_weight"))
+        vendor_step = sum(other["vendor_fp32"][k] for k in ("gemm_ms", "conv_fwd_ms", "conv_bwd_data_ms",
+                                                           "conv_bwd_weight_ms"))
+        other["step_time_ratios"] = {
+            "what": "time of the step's four calls over the vendor FP32 libraries' time for the same four",
+            "approx_over_vendor_fp32": round(out["ms_per_step"] / vendor_step, 2),
+            "native_multiply_over_vendor_fp32": round(native_step / vendor_step, 2),
+            "approx_over_native_multiply": round(out["ms_per_step"] / native_step, 2)}
+        kernels.update(other)
+
     if args.extra and not args.no_extra:
         out["extra"] = extras(B, W, torch, np, dev, lut, m_bits, A, Bm, C)
 
@@ -222,15 +243,119 @@ def _time_call(torch, fn, reps):
     return e0.elapsed_time(e1) / reps  # ms per call
 
 
+def _rates(macs, ms):
+    return {"gmacs_per_s": round(macs / ms / 1e6, 1),
+            "pct_fp32_vector_peak": round(100 * FLOP_PER_APPROX_MAC * macs / (ms * 1e-3) /
+                                          (FP32_VECTOR_PEAK_TFLOPS * 1e12), 2),
+            "pct_fp32_lane_rate": round(100 * macs / (ms * 1e-3) / (FP32_LANE_RATE_T * 1e12), 2)}
+
+
+def _time_main_kernel(B, torch, fn, reps, kind, macs):
+    """Average main-kernel time (the library's HIP-event timer) and whole-call time (events on
+    torch's stream, pre-passes included) of `reps` calls of fn, after one untimed call."""
+    call_ms = _time_call(torch, fn, reps)
+    B.amsim_profile_start(4 * reps + 4)
+    for _ in range(reps):
+        fn()
+    torch.cuda.synchronize()
+    B.amsim_profile_stop()
+    n, tot = B.amsim_profile_read(kind)
+    avg = tot / max(n, 1)
+    r = {"launches": n, "avg_ms": round(avg, 4), "call_ms": round(call_ms, 4)}
+    r.update(_rates(macs, avg))
+    return r
+
+
+def other_kernels(B, W, torch, dev, lut7, m7, A, Bm, C, cv, conv_t, ws_g, ws_c):
+    """The other configurations, timed after the step (not part of `value`)."""
+    ks = {}
+    M, N, K = A.shape[0], Bm.shape[1], A.shape[1]
+    # the step's GEMM with the M = 11 table (rows of 2048 entries staged per slab)
+    lut11 = B.device_lut(B.lut_build(11, "mitchell"), dev)
+    ws = torch.empty(B.amsim_gemm_workspace_size(0, 0, M, N, K, 11), dtype=torch.uint8, device=dev)
+    ks["gemm_4096_m11"] = _time_main_kernel(B, torch, lambda: B.approx_gemm(A, Bm, lut11, 11, out=C, workspace=ws),
+                                            3, "gemm", M * N * K)
+    del ws
+    log("M=11 GEMM done")
+    # ResNet-50 layers, batch 32, Mitchell M = 7, each pass
+    for cfg in W.RESNET50_LAYERS:
+        p = cfg["conv"]
+        x_h, w_h, dy_h = W.resnet_conv_inputs(p, seed=4000, stem=(cfg is W.RESNET50_LAYERS[0]))
+        x, w, dy = (torch.from_numpy(t).to(dev) for t in (x_h, w_h, dy_h))
+        macs = W.conv_macs(p)
+        for name, kind, fn in (("fwd", "conv_fwd", lambda: B.approx_conv2d_fwd(p, x, w, lut7, m7)),
+                               ("bwd_data", "conv_bwd_data", lambda: B.approx_conv2d_bwd_data(p, dy, w, lut7, m7)),
+                               ("bwd_weight", "conv_bwd_weight",
+                                lambda: B.approx_conv2d_bwd_weight(p, x, dy, lut7, m7))):
+            ks["%s_%s" % (cfg["name"], name)] = _time_main_kernel(B, torch, fn, 5, kind, macs)
+        del x, w, dy
+    log("ResNet-50 layers done")
+    ks["lenet5_b64_fwd_bwd"] = lenet_stack(B, W, torch, dev)
+    log("LeNet-5 stack done")
+    # the step with the native FP32 multiply in the same kernels
+    x, w, dy = conv_t
+    conv_macs = W.conv_macs(cv)
+    nat = {}
+    nat["gemm"] = _time_main_kernel(
+        B, torch, lambda: B.approx_gemm_ex(A, Bm, lut7, m7, out=C, workspace=ws_g, multiply="native"), 5,
+        "gemm_native", M * N * K)
+    for name, fn in (("conv_fwd", lambda: B.approx_conv2d_fwd_ex(cv, x, w, lut7, m7, workspace=ws_c[0],
+                                                                 multiply="native")),
+                     ("conv_bwd_data", lambda: B.approx_conv2d_bwd_data_ex(cv, dy, w, lut7, m7, workspace=ws_c[1],
+                                                                           multiply="native")),
+                     ("conv_bwd_weight", lambda: B.approx_conv2d_bwd_weight_ex(cv, x, dy, lut7, m7,
+                                                                               workspace=ws_c[2],
+                                                                               multiply="native"))):
+        nat[name] = _time_main_kernel(B, torch, fn, 5, name + "_native", conv_macs)
+    ks["native_multiply"] = nat
+    log("native-multiply step done")
+    ks["vendor_fp32"] = native_fp32(torch, W, dev, A, Bm, C)
+    log("vendor FP32 step done")
+    return ks
+
+
+def lenet_stack(B, W, torch, dev):
+    """LeNet-5 stack, batch 64, exact bfloat16-truncation table: forward and backward of every
+    approximate layer (whole calls, pre-passes included)."""
+    cfg = W.LENET5
+    mb = cfg["m_bits"]
+    lutb = B.device_lut(B.lut_build(mb, "exact_trunc"), dev)
+    c1, c2 = cfg["conv1"], cfg["conv2"]
+    x0 = torch.from_numpy(W.uniform((64, 28, 28, 1), 0, 1, 6000)).to(dev)
+    w1 = torch.from_numpy(W.glorot_uniform((5, 5, 1, 6), 25, 150, 6001)).to(dev)
+    w2 = torch.from_numpy(W.glorot_uniform((5, 5, 6, 16), 150, 400, 6002)).to(dev)
+    fcw = [torch.from_numpy(W.glorot_uniform((i, o), i, o, 6003 + j)).to(dev) for j, (i, o) in enumerate(cfg["fc"])]
+    g = torch.Generator(device="cpu").manual_seed(6020)
+    p1 = torch.rand((64, 14, 14, 6), generator=g).to(dev)
+    dy1 = torch.randn((64, 28, 28, 6), generator=g).to(dev)
+    dy2 = torch.randn((64, 10, 10, 16), generator=g).to(dev)
+    acts = [torch.rand((64, i), generator=g).to(dev) for i, _ in cfg["fc"]]
+    grads = [torch.randn((64, o), generator=g).to(dev) for _, o in cfg["fc"]]
+    macs = 2 * W.conv_macs(c1) + 3 * W.conv_macs(c2) + 3 * sum(64 * i * o for i, o in cfg["fc"])
+
+    def stack():
+        B.approx_conv2d_fwd(c1, x0, w1, lutb, mb)
+        B.approx_conv2d_fwd(c2, p1, w2, lutb, mb)
+        for a, wj in zip(acts, fcw):
+            B.approx_gemm(a, wj, lutb, mb)
+        for a, gj, wj in zip(acts, grads, fcw):
+            B.approx_gemm(a, gj, lutb, mb, trans_a=True)
+            B.approx_gemm(gj, wj, lutb, mb, trans_b=True)
+        B.approx_conv2d_bwd_weight(c2, p1, dy2, lutb, mb)
+        B.approx_conv2d_bwd_data(c2, dy2, w2, lutb, mb)
+        B.approx_conv2d_bwd_weight(c1, x0, dy1, lutb, mb)
+
+    ms = _time_call(torch, stack, 10)
+    r = {"call_ms": round(ms, 4), "approx_macs": macs, "calls": 14}
+    r.update(_rates(macs, ms))
+    return r
+
+
 def extras(B, W, torch, np, dev, lut7, m7, A, Bm, C):
-    """Rates of the other workloads (not part of the timed step)."""
+    """Rates of further workloads (not part of the timed step)."""
     ex = {}
     M, N, K = A.shape[0], Bm.shape[1], A.shape[1]
     lut11 = B.device_lut(B.lut_build(11, "mitchell"), dev)
-    ws = torch.empty(B.amsim_gemm_workspace_size(0, 0, M, N, K, 11), dtype=torch.uint8, device=dev)
-    ms = _time_call(torch, lambda: B.approx_gemm(A, Bm, lut11, 11, out=C, workspace=ws), 2)
-    ex["gemm_4096_m11_wide_table"] = {"ms": round(ms, 2), "gmacs_per_s": round(M * N * K / ms / 1e6, 1)}
-    log("M=11 GEMM done")
     # the same GEMM at smaller sizes, 128-entry table rows (M=7) and 2048-entry rows (M=11)
     sweep = {}
     for n in (64, 512, 1024, 2048):
@@ -277,55 +402,10 @@ def extras(B, W, torch, np, dev, lut7, m7, A, Bm, C):
         r["resnet_3x3_" + name] = {"ms": round(ms, 3), "gmacs_per_s": round(macs / ms / 1e6, 1)}
     ex["exact_trunc_two_byte_table"] = r
     log("exact-truncation table done")
-    for cfg in W.RESNET50_LAYERS:
-        p = cfg["conv"]
-        x_h, w_h, dy_h = W.resnet_conv_inputs(p, seed=4000, stem=(cfg is W.RESNET50_LAYERS[0]))
-        x, w, dy = (torch.from_numpy(t).to(dev) for t in (x_h, w_h, dy_h))
-        macs = W.conv_macs(p)
-        r = {}
-        for name, fn in (("fwd", lambda: B.approx_conv2d_fwd(p, x, w, lut7, m7)),
-                         ("bwd_data", lambda: B.approx_conv2d_bwd_data(p, dy, w, lut7, m7)),
-                         ("bwd_weight", lambda: B.approx_conv2d_bwd_weight(p, x, dy, lut7, m7))):
-            ms = _time_call(torch, fn, 5)
-            r[name] = {"ms": round(ms, 3), "gmacs_per_s": round(macs / ms / 1e6, 1)}
-        ex[cfg["name"]] = r
-    log("ResNet-50 layers done")
-    # LeNet-5 stack, batch 64, exact bfloat16-truncation table: fwd + bwd of the approximate layers
     cfg = W.LENET5
     lutb = B.device_lut(B.lut_build(cfg["m_bits"], "exact_trunc"), dev)
-    mb = cfg["m_bits"]
-    c1, c2 = cfg["conv1"], cfg["conv2"]
-    x0 = torch.from_numpy(W.uniform((64, 28, 28, 1), 0, 1, 6000)).to(dev)
-    w1 = torch.from_numpy(W.glorot_uniform((5, 5, 1, 6), 25, 150, 6001)).to(dev)
-    w2 = torch.from_numpy(W.glorot_uniform((5, 5, 6, 16), 150, 400, 6002)).to(dev)
-    fcw = [torch.from_numpy(W.glorot_uniform((i, o), i, o, 6003 + j)).to(dev) for j, (i, o) in enumerate(cfg["fc"])]
-    p1 = torch.rand((64, 14, 14, 6), device=dev)
-    dy1 = torch.randn((64, 28, 28, 6), device=dev)
-    dy2 = torch.randn((64, 10, 10, 16), device=dev)
-    acts = [torch.rand((64, i), device=dev) for i, _ in cfg["fc"]]
-    grads = [torch.randn((64, o), device=dev) for _, o in cfg["fc"]]
-    lenet_macs = 2 * W.conv_macs(c1) + 3 * W.conv_macs(c2) + 3 * sum(64 * i * o for i, o in cfg["fc"])
-
-    def lenet():
-        B.approx_conv2d_fwd(c1, x0, w1, lutb, mb)
-        B.approx_conv2d_fwd(c2, p1, w2, lutb, mb)
-        for a, wj in zip(acts, fcw):
-            B.approx_gemm(a, wj, lutb, mb)
-        for a, gj, wj in zip(acts, grads, fcw):
-            B.approx_gemm(a, gj, lutb, mb, trans_a=True)
-            B.approx_gemm(gj, wj, lutb, mb, trans_b=True)
-        B.approx_conv2d_bwd_weight(c2, p1, dy2, lutb, mb)
-        B.approx_conv2d_bwd_data(c2, dy2, w2, lutb, mb)
-        B.approx_conv2d_bwd_weight(c1, x0, dy1, lutb, mb)
-
-    ms = _time_call(torch, lenet, 10)
-    ex["lenet5_b64_fwd_bwd"] = {"ms": round(ms, 3), "approx_macs": lenet_macs,
-                               "gmacs_per_s": round(lenet_macs / ms / 1e6, 1)}
-    log("LeNet-5 stack done")
-    ex["lenet5_b64_train_step_layers"] = lenet_train_step(torch, W, np, dev, lutb, mb)
+    ex["lenet5_b64_train_step_layers"] = lenet_train_step(torch, W, np, dev, lutb, cfg["m_bits"])
     log("LeNet-5 training step done")
-    ex["native_fp32_vendor"] = native_fp32(torch, W, dev, A, Bm, C)
-    log("native FP32 vendor kernels done")
     return ex
 
 
@@ -365,7 +445,8 @@ def native_fp32(torch, W, dev, A, Bm, C):
     torch.backends.cuda.matmul.allow_tf32 = False  # full FP32 products
     torch.backends.cudnn.allow_tf32 = False
     try:
-        out = {"gemm_4096_ms": round(_time_call(torch, lambda: torch.matmul(A, Bm, out=C), 5), 3)}
+        out = {"what": "torch.matmul (hipBLASLt/rocBLAS) and MIOpen convolution in FP32 (TF32 off), whole calls",
+               "gemm_ms": round(_time_call(torch, lambda: torch.matmul(A, Bm, out=C), 5), 4)}
         cv = W.RESNET_3X3["conv"]
         x_h, w_h, dy_h = W.resnet_conv_inputs(cv, seed=3000)
         # NHWC data viewed as NCHW (channels-last strides), HWIO weights as OIHW
@@ -374,10 +455,10 @@ def native_fp32(torch, W, dev, A, Bm, C):
         dy = torch.from_numpy(dy_h).to(dev).permute(0, 3, 1, 2)
         pad = cv["pad_top"]
         F = torch.nn.functional
-        for name, fn in (("conv3x3_fwd_ms", lambda: F.conv2d(x, w, padding=pad)),
-                         ("conv3x3_bwd_data_ms", lambda: torch.nn.grad.conv2d_input(x.shape, w, dy, padding=pad)),
-                         ("conv3x3_bwd_weight_ms", lambda: torch.nn.grad.conv2d_weight(x, w.shape, dy, padding=pad))):
-            out[name] = round(_time_call(torch, fn, 5), 3)
+        for name, fn in (("conv_fwd_ms", lambda: F.conv2d(x, w, padding=pad)),
+                         ("conv_bwd_data_ms", lambda: torch.nn.grad.conv2d_input(x.shape, w, dy, padding=pad)),
+                         ("conv_bwd_weight_ms", lambda: torch.nn.grad.conv2d_weight(x, w.shape, dy, padding=pad))):
+            out[name] = round(_time_call(torch, fn, 5), 4)
         return out
     finally:
         torch.backends.cuda.matmul.allow_tf32, torch.backends.cudnn.allow_tf32 = mm, cd
