@@ -34,10 +34,9 @@ namespace amsim_detail __attribute__((visibility("hidden"))) {
 // and read by the table kernel, which runs the matching specialisation.
 
 // Which operation the table kernel evaluates.  Every one is a sum over "taps": runs of
-// consecutive reduction steps j = 0 .. count-1 whose first-operand word sits at
-//   A[lane row base + ubase + j * ustride]
-// (pair records: record pbase + (j / 2) * ustride from the row's record base) and whose
-// second-operand row is Bd[bbase + j].
+// consecutive reduction steps j = 0 .. count-1 whose first operand sits in the step-pair record
+//   A[lane row's record base + pbase + (j / 2) * ustride]
+// and whose second-operand row is Bd[bbase + j].
 //   GEMM         one tap of K steps: rows i, A = op(A) k-major, row base i
 //   FWD          tap = (kh, kw): rows (n, oh, ow), A = zero-padded x stored [n][h][ci][w], j = ci
 //   BWD_DATA     tap = valid (kh, kw) of the stride phase in tile z: rows (n, hq, wq),
@@ -105,8 +104,10 @@ __device__ __forceinline__ void tab_tile_id(int splits, int &tx, int &ty, int &t
 }
 
 struct TabTap {
-    int ubase, ustride, bbase, count;
-    int pbase;  // pair records: the tap's first record (records of pair j / 2 are ustride apart)
+    int pbase;    // the tap's first record, relative to the lane row's record base
+    int ustride;  // records between consecutive step pairs
+    int bbase;    // the second operand's row of step 0
+    int count;    // steps
 };
 
 // Second-operand word of reduction row j (its table row, or with the native multiply its value)
@@ -119,77 +120,65 @@ __device__ __forceinline__ uint32_t Bd_word(const TabArgs &a, int j, int col)
 // The first operand of every operation is decoded into one 12-byte record per lane row and step
 // pair (j, j + 1), j even (backward weight: one record per pixel of the zero-bordered x and
 // channel, pairing it with the pixel one stride to its right, so that every kernel column's steps
-// pair up whatever its kw),
-// instead of one word per element: j's 16-bit table-index field (an LDS byte
-// offset on the bf16 path) as a word, the two mantissa-cleared operands as bf16
-// (pa(j) | pa(j+1) << 16), and j+1's index word.  The bf16 path loads a record with one
-// instruction and uses it as loaded: no masking of the indices, no pairing of the heads.  A
-// single step is one 8-byte load at record offset 0 (j even) or 4 (j odd) and one byte permute.
-template <int OP>
-constexpr bool split_a()
-{
-    return OP == OP_GEMM || OP == OP_FWD || OP == OP_BWD_DATA || OP == OP_BWD_WEIGHT;
-}
+// pair up whatever its kw): j's 16-bit table-index field (an LDS byte offset on the bf16 path)
+// as a word, the two mantissa-cleared operands as bf16 (pa(j) | pa(j+1) << 16), and j+1's index
+// word (with the native multiply: the two raw operands in the first and last words).  The bf16
+// path loads a record with one instruction and uses it as loaded: no masking of the indices, no
+// pairing of the heads.  A single step is one 8-byte load at record offset 0 (j even) or 4
+// (j odd) and one byte permute.
 constexpr uint32_t kPairRecordBytes = 12;
 
 // First-operand buffer and the lane rows' byte offsets in it.
 template <int TM>
 struct AView {
-    __amdgpu_buffer_rsrc_t words;  // words, or pair records
-    uint32_t aoff[TM];             // per lane row: offset of its run (word or record)
+    __amdgpu_buffer_rsrc_t words;  // the pair records
+    uint32_t aoff[TM];             // per lane row: byte offset of its record base
 };
 
-// Byte offset of step j's word (pair records: of the record holding j) in the tap.
+// Byte offset of the record holding step j, relative to the lane row's record base.
 template <int OP>
-__device__ __forceinline__ uint32_t a_step_offset(const TabTap &tp, int j)
+__host__ __device__ __forceinline__ uint32_t a_step_offset(const TabTap &tp, int j)
 {
-    if constexpr (split_a<OP>())
-        return uint32_t(tp.pbase + (j >> 1) * tp.ustride) * kPairRecordBytes;
-    else
-        return uint32_t(tp.ubase + j * tp.ustride) * 4u;
+    return uint32_t(tp.pbase + (j >> 1) * tp.ustride) * kPairRecordBytes;
 }
 
-// The first operand's word of step j (head | index, as the one-word layout stores it) for each
-// lane row; so = a_step_offset of j (wave-uniform).  Pair records: j's index word with j's half
-// of the head pair moved into the high half.
+// The first operand's word of step j for each lane row (head | index: j's index word with j's
+// half of the head pair moved into the high half); so = a_step_offset of j (wave-uniform).
 template <int OP, int TM>
 __device__ __forceinline__ void load_a_words(uint32_t (&dst)[TM], const AView<TM> &av, uint32_t so, int j)
 {
 #pragma unroll
     for (int r = 0; r < TM; ++r) {
-        if constexpr (split_a<OP>()) {
-            // j even: (index, heads) -> index | pa(j) << 16; j odd: (heads, index) -> index | pa(j+1)'s half
-            const u32x2 d = __builtin_amdgcn_raw_buffer_load_b64(av.words, av.aoff[r], so + (j & 1) * 4u, 0);
-            dst[r] = __builtin_amdgcn_perm(d.y, d.x, (j & 1) ? 0x03020504u : 0x05040100u);
-        } else {
-            dst[r] = __builtin_amdgcn_raw_buffer_load_b32(av.words, av.aoff[r], so, 0);
-        }
+        // j even: (index, heads) -> index | pa(j) << 16; j odd: (heads, index) -> index | pa(j+1)'s half
+        const u32x2 d = __builtin_amdgcn_raw_buffer_load_b64(av.words, av.aoff[r], so + (j & 1) * 4u, 0);
+        dst[r] = __builtin_amdgcn_perm(d.y, d.x, (j & 1) ? 0x03020504u : 0x05040100u);
     }
 }
 
+// rec: the lane rows' record bases (tab_row_rec).
 template <int OP, int TM>
-__device__ __forceinline__ AView<TM> make_aview(const TabArgs &a, const int (&abase)[TM])
+__device__ __forceinline__ AView<TM> make_aview(const TabArgs &a, const int (&rec)[TM])
 {
     AView<TM> av;
     av.words = __builtin_amdgcn_make_buffer_rsrc(const_cast<uint32_t *>(a.A), 0, int(a.a_bytes), 0x00020000);
 #pragma unroll
-    for (int r = 0; r < TM; ++r) av.aoff[r] = uint32_t(abase[r]) * (split_a<OP>() ? kPairRecordBytes : 4u);
+    for (int r = 0; r < TM; ++r) av.aoff[r] = uint32_t(rec[r]) * kPairRecordBytes;
     return av;
 }
 
 // Rows of one stride phase of the backward-data pass.
-__device__ __forceinline__ void phase_dims(const ConvShape &s, int ph, int pw, int &hq_n, int &wq_n)
+__host__ __device__ __forceinline__ void phase_dims(const ConvShape &s, int ph, int pw, int &hq_n, int &wq_n)
 {
     hq_n = ph < s.h ? (s.h - ph + s.sh - 1) / s.sh : 0;
     wq_n = pw < s.w ? (s.w - pw + s.sw - 1) / s.sw : 0;
 }
 
 // tile z = phase * splits + split (phase only for BWD_DATA, else 0)
-__device__ __forceinline__ int tab_phase(const TabArgs &a) { return a.tz / a.splits; }
-__device__ __forceinline__ int tab_split(const TabArgs &a) { return a.tz % a.splits; }
+__host__ __device__ __forceinline__ int tab_phase(const TabArgs &a) { return a.tz / a.splits; }
+__host__ __device__ __forceinline__ int tab_split(const TabArgs &a) { return a.tz % a.splits; }
 
 template <int OP>
-__device__ __forceinline__ int tab_rows(const TabArgs &a)
+__host__ __device__ __forceinline__ int tab_rows(const TabArgs &a)
 {
     if constexpr (OP == OP_BWD_DATA) {
         int hq_n, wq_n;
@@ -200,35 +189,27 @@ __device__ __forceinline__ int tab_rows(const TabArgs &a)
     }
 }
 
-// Lane row -> (first-operand element offset of the row, result element offset).
+// Lane row -> result element offset.
 template <int OP>
-__device__ __forceinline__ void tab_row(const TabArgs &a, int row, int &abase, int64_t &obase)
+__host__ __device__ __forceinline__ int64_t tab_row_out(const TabArgs &a, int row)
 {
     const ConvShape &s = a.s;
     if constexpr (OP == OP_GEMM) {
-        abase = row;
-        obase = int64_t(row) * a.ldc;
-    } else if constexpr (OP == OP_FWD) {
-        const int ow = row % s.ow, oh = (row / s.ow) % s.oh, n = row / (s.ow * s.oh);
-        abase = (n * a.Hp + oh * s.sh) * s.ci * a.Wp + ow * s.sw;  // x as [n][hp][ci][wp]
-        obase = int64_t(row) * s.co;
+        return int64_t(row) * a.ldc;
     } else if constexpr (OP == OP_BWD_DATA) {
         const int ph = tab_phase(a) / s.sw, pw = tab_phase(a) % s.sw;
         int hq_n, wq_n;
         phase_dims(s, ph, pw, hq_n, wq_n);
         const int wq = row % wq_n, hq = (row / wq_n) % hq_n, n = row / (wq_n * hq_n);
-        abase = (n * a.OHp + hq) * s.co * a.OWp + wq;  // dy as [n][ohp][co][owp]; pads in the tap offset
-        obase = (int64_t(n * s.h + hq * s.sh + ph) * s.w + wq * s.sw + pw) * s.ci;
+        return ((int64_t(n) * s.h + hq * s.sh + ph) * s.w + wq * s.sw + pw) * s.ci;
     } else {
-        const int ci = row % s.ci, kw = (row / s.ci) % s.kw, kh = row / (s.ci * s.kw);
-        abase = (kh * a.Wp + kw) * s.ci + ci;
-        obase = int64_t(row) * s.co;
+        return int64_t(row) * s.co;  // FWD: (n, oh, ow) x co; BWD_WEIGHT: (kh, kw, ci) x co
     }
 }
 
-// Pair records: the lane row's record offset (element offset with the step axis halved).
+// Lane row -> its record base in the first operand's pair records.
 template <int OP>
-__device__ __forceinline__ int tab_row_rec(const TabArgs &a, int row)
+__host__ __device__ __forceinline__ int tab_row_rec(const TabArgs &a, int row)
 {
     const ConvShape &s = a.s;
     if constexpr (OP == OP_GEMM) {
@@ -250,7 +231,7 @@ __device__ __forceinline__ int tab_row_rec(const TabArgs &a, int row)
 
 // Taps of the reduction (BWD_DATA: of this workgroup's stride phase).
 template <int OP>
-__device__ __forceinline__ int tab_taps(const TabArgs &a)
+__host__ __device__ __forceinline__ int tab_taps(const TabArgs &a)
 {
     if constexpr (OP == OP_GEMM) {
         return 1;
@@ -270,7 +251,7 @@ __device__ __forceinline__ int tab_taps(const TabArgs &a)
 
 // Steps per tap (the same for every tap of an operation).
 template <int OP>
-__device__ __forceinline__ int tab_count(const TabArgs &a)
+__host__ __device__ __forceinline__ int tab_count(const TabArgs &a)
 {
     if constexpr (OP == OP_GEMM) return a.K;
     else if constexpr (OP == OP_FWD) return a.s.ci / a.csplit;
@@ -280,13 +261,12 @@ __device__ __forceinline__ int tab_count(const TabArgs &a)
 
 // The tap's fields are wave-uniform (they depend on the workgroup and the tap only).
 template <int OP>
-__device__ __forceinline__ TabTap tab_tap_raw(const TabArgs &a, int tap)
+__host__ __device__ __forceinline__ TabTap tab_tap_raw(const TabArgs &a, int tap)
 {
     const ConvShape &s = a.s;
     TabTap t;
     if constexpr (OP == OP_GEMM) {
         t.count = a.K;
-        t.ubase = 0;
         t.ustride = a.Mp;
         t.bbase = 0;
         t.pbase = 0;
@@ -296,7 +276,6 @@ __device__ __forceinline__ TabTap tab_tap_raw(const TabArgs &a, int tap)
         const int kk = tap % (s.kh * s.kw), chunk = tap / (s.kh * s.kw);
         const int kh = kk / s.kw, kw = kk % s.kw, cnt = s.ci / a.csplit, c0 = chunk * cnt;
         t.count = cnt;
-        t.ubase = (kh * s.ci + c0) * a.Wp + kw;
         t.ustride = a.Wp;
         t.bbase = kk * s.ci + c0;
         t.pbase = (kh * ((a.rec_c + 1) / 2) + c0 / 2) * a.Wp + kw;
@@ -309,19 +288,18 @@ __device__ __forceinline__ TabTap tab_tap_raw(const TabArgs &a, int tap)
         const int dh = (ph + s.pt - kh) / s.sh, dw = (pw + s.pl - kw) / s.sw;  // exact divisions
         const int cnt = s.co / a.csplit, c0 = chunk * cnt;
         t.count = cnt;
-        t.ubase = ((dh + a.pad_oh) * s.co + c0) * a.OWp + dw + a.pad_ow;  // >= 0: the padding covers every dh, dw
         t.ustride = a.OWp;
         t.bbase = (kh * s.kw + kw) * s.co + c0;
+        // >= 0: the padding covers every dh, dw
         t.pbase = ((dh + a.pad_oh) * ((a.rec_c + 1) / 2) + c0 / 2) * a.OWp + dw + a.pad_ow;
     } else {
         // step j = ow reads x at column ow * sw + kw: the record of step pair (j, j + 1) is the one of
         // column j * sw + kw, 2 sw columns after the previous pair's
         const int n = tap / s.oh, oh = tap % s.oh;
         t.count = s.ow;
-        t.ubase = (n * a.Hp + oh * s.sh) * a.Wp * s.ci;
         t.ustride = 2 * s.sw * s.ci;
         t.bbase = tap * s.ow;
-        t.pbase = t.ubase;
+        t.pbase = (n * a.Hp + oh * s.sh) * a.Wp * s.ci;
     }
     return t;
 }
@@ -330,9 +308,8 @@ template <int OP>
 __device__ __forceinline__ TabTap tab_tap(const TabArgs &a, int tap)
 {
     const TabTap t = tab_tap_raw<OP>(a, tap);
-    return TabTap{__builtin_amdgcn_readfirstlane(t.ubase), __builtin_amdgcn_readfirstlane(t.ustride),
-                  __builtin_amdgcn_readfirstlane(t.bbase), __builtin_amdgcn_readfirstlane(t.count),
-                  __builtin_amdgcn_readfirstlane(t.pbase)};
+    return TabTap{__builtin_amdgcn_readfirstlane(t.pbase), __builtin_amdgcn_readfirstlane(t.ustride),
+                  __builtin_amdgcn_readfirstlane(t.bbase), __builtin_amdgcn_readfirstlane(t.count)};
 }
 
 // The slab cursor is wave-uniform; saying so at the loop head keeps it, and the buffer loads'
@@ -340,9 +317,8 @@ __device__ __forceinline__ TabTap tab_tap(const TabArgs &a, int tap)
 // prove it through the backward-data phase math and would loop each load over the lanes).
 __device__ __forceinline__ void uniform_cursor(TabTap &cur, int &tap, int &c0)
 {
-    cur = TabTap{__builtin_amdgcn_readfirstlane(cur.ubase), __builtin_amdgcn_readfirstlane(cur.ustride),
-                 __builtin_amdgcn_readfirstlane(cur.bbase), __builtin_amdgcn_readfirstlane(cur.count),
-                 __builtin_amdgcn_readfirstlane(cur.pbase)};
+    cur = TabTap{__builtin_amdgcn_readfirstlane(cur.pbase), __builtin_amdgcn_readfirstlane(cur.ustride),
+                 __builtin_amdgcn_readfirstlane(cur.bbase), __builtin_amdgcn_readfirstlane(cur.count)};
     tap = __builtin_amdgcn_readfirstlane(tap);
     c0 = __builtin_amdgcn_readfirstlane(c0);
 }
@@ -436,17 +412,11 @@ __device__ __forceinline__ void tab_body(const TabArgs &a)
     // First-operand reads are raw buffer loads: voffset = the lane row's byte offset (range-checked,
     // reads past the buffer return 0), soffset = the wave-uniform step offset, which every tap keeps
     // non-negative and inside the tensor, since the hardware does not range-check it.
-    int abase[TM];  // element offset of each lane row's first-operand run
+    int abase[TM];  // each lane row's record base
 #pragma unroll
     for (int r = 0; r < TM; ++r) {
         const int row = row0 + 64 * r;
-        int ab = 0;
-        int64_t ob = 0;
-        if (row < R) {
-            tab_row<OP>(a, row, ab, ob);
-            if constexpr (split_a<OP>()) ab = tab_row_rec<OP>(a, row);
-        }
-        abase[r] = ab;
+        abase[r] = row < R ? tab_row_rec<OP>(a, row) : 0;  // rows past the end read record 0's run
     }
     const AView<TM> av = make_aview<OP, TM>(a, abase);
     // this split's chunks, as positions p = tap * (8 * chunks per tap) + step
@@ -462,7 +432,7 @@ __device__ __forceinline__ void tab_body(const TabArgs &a)
     float acc[TM][TN];
     init_acc(acc);
     uint32_t acur[TM];
-    TabTap cur{0, 0, 0, 0, 0};
+    TabTap cur{0, 0, 0, 0};
     int tap = q0 / max(cpt, 1);
     int c0 = (q0 - tap * cpt) * ch;
     bool have = q0 * ch < p_end;
@@ -547,10 +517,7 @@ __device__ __forceinline__ void tab_body(const TabArgs &a)
     for (int r = 0; r < TM; ++r) {
         const int row = row0 + 64 * r;
         if (row >= R) continue;
-        int ab = 0;
-        int64_t ob = 0;
-        tab_row<OP>(a, row, ab, ob);  // the output offset, recomputed rather than kept in registers
-        float *dst = out + ob;
+        float *dst = out + tab_row_out<OP>(a, row);  // recomputed rather than kept in registers
 #pragma unroll
         for (int t = 0; t < TN; ++t) {
             const int col = col0 + t;
@@ -571,12 +538,8 @@ __device__ __forceinline__ void load_a_raw(float (&dst)[TM], const AView<TM> &av
 {
 #pragma unroll
     for (int r = 0; r < TM; ++r) {
-        if constexpr (split_a<OP>()) {
-            const u32x2 d = __builtin_amdgcn_raw_buffer_load_b64(av.words, av.aoff[r], so + (j & 1) * 4u, 0);
-            dst[r] = __uint_as_float((j & 1) ? d.y : d.x);
-        } else {
-            dst[r] = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(av.words, av.aoff[r], so, 0));
-        }
+        const u32x2 d = __builtin_amdgcn_raw_buffer_load_b64(av.words, av.aoff[r], so + (j & 1) * 4u, 0);
+        dst[r] = __uint_as_float((j & 1) ? d.y : d.x);
     }
 }
 
@@ -604,13 +567,7 @@ __device__ __forceinline__ void tab_body_native(const TabArgs &a)
 #pragma unroll
     for (int r = 0; r < TM; ++r) {
         const int row = row0 + 64 * r;
-        int ab = 0;
-        int64_t ob = 0;
-        if (row < R) {
-            tab_row<OP>(a, row, ab, ob);
-            if constexpr (split_a<OP>()) ab = tab_row_rec<OP>(a, row);
-        }
-        abase[r] = ab;
+        abase[r] = row < R ? tab_row_rec<OP>(a, row) : 0;  // rows past the end read record 0's run
     }
     const AView<TM> av = make_aview<OP, TM>(a, abase);
     const int count = tab_count<OP>(a);
@@ -639,7 +596,7 @@ __device__ __forceinline__ void tab_body_native(const TabArgs &a)
     };
     float acc[TM][TN];
     init_acc(acc);
-    TabTap cur{0, 0, 0, 0, 0};
+    TabTap cur{0, 0, 0, 0};
     int tap = q0 / max(cpt, 1);
     int c0 = (q0 - tap * cpt) * ch;
     bool have = q0 * ch < p_end;
@@ -698,10 +655,7 @@ __device__ __forceinline__ void tab_body_native(const TabArgs &a)
     for (int r = 0; r < TM; ++r) {
         const int row = row0 + 64 * r;
         if (row >= R) continue;
-        int ab = 0;
-        int64_t ob = 0;
-        tab_row<OP>(a, row, ab, ob);
-        float *dst = out + ob;
+        float *dst = out + tab_row_out<OP>(a, row);  // recomputed rather than kept in registers
 #pragma unroll
         for (int t = 0; t < TN; ++t) {
             const int col = col0 + t;
@@ -820,35 +774,22 @@ __device__ __forceinline__ void dot_commit(const u32x4 (&bw)[2], const uint32_t 
     }
 }
 
-// First-operand data of the step pair (j, j + 1) per lane row: the two words, or (split layout)
-// the two indices and the head pair.  A step past the tap's end (the odd step of a pair, or a
+// First-operand data of the step pair (j, j + 1) per lane row: the two indices and the head pair.  A step past the tap's end (the odd step of a pair, or a
 // slab's unused slots) reads the tap's last step again: its slot in the slab holds +0 entries
 // (staged from a +0 second operand), so it adds signed zeros only, and the loads stay
 // branch-free and in bounds.
 template <int OP, int TM>
-__device__ __forceinline__ void dot_load_pair(uint32_t (&dst)[split_a<OP>() ? 3 : 2][TM], const AView<TM> &av,
-                                              const TabTap &tp, int j)
+__device__ __forceinline__ void dot_load_pair(uint32_t (&dst)[3][TM], const AView<TM> &av, const TabTap &tp, int j)
 {
-    const int j0 = min(j, tp.count - 1), j1 = min(j + 1, tp.count - 1);
-    if constexpr (split_a<OP>()) {
-        // j even: one record holds both steps (past the end: the last record; an odd count's
-        // last record has a decoded +0 for its missing step)
-        const uint32_t so = __builtin_amdgcn_readfirstlane(a_step_offset<OP>(tp, j0));
+    // j even: one record holds both steps (past the end: the last record; an odd count's last
+    // record has a decoded +0 for its missing step)
+    const uint32_t so = __builtin_amdgcn_readfirstlane(a_step_offset<OP>(tp, min(j, tp.count - 1)));
 #pragma unroll
-        for (int r = 0; r < TM; ++r) {
-            const u32x3 rec = __builtin_amdgcn_raw_buffer_load_b96(av.words, av.aoff[r], so, 0);
-            dst[0][r] = rec.x;
-            dst[1][r] = rec.z;
-            dst[2][r] = rec.y;
-        }
-    } else {
-        const uint32_t s0 = __builtin_amdgcn_readfirstlane(a_step_offset<OP>(tp, j0));
-        const uint32_t s1 = __builtin_amdgcn_readfirstlane(a_step_offset<OP>(tp, j1));
-#pragma unroll
-        for (int r = 0; r < TM; ++r) {
-            dst[0][r] = __builtin_amdgcn_raw_buffer_load_b32(av.words, av.aoff[r], s0, 0);
-            dst[1][r] = __builtin_amdgcn_raw_buffer_load_b32(av.words, av.aoff[r], s1, 0);
-        }
+    for (int r = 0; r < TM; ++r) {
+        const u32x3 rec = __builtin_amdgcn_raw_buffer_load_b96(av.words, av.aoff[r], so, 0);
+        dst[0][r] = rec.x;
+        dst[1][r] = rec.z;
+        dst[2][r] = rec.y;
     }
 }
 
@@ -904,10 +845,7 @@ __device__ __forceinline__ void dot_finish(const TabArgs &a, float (&acc)[TM][TN
     for (int r = 0; r < TM; ++r) {
         const int row = row0 + 64 * r;
         if (row >= R) continue;
-        int ab = 0;
-        int64_t ob = 0;
-        tab_row<OP>(a, row, ab, ob);  // the output offset, recomputed rather than kept in registers
-        float *dst = out + ob;
+        float *dst = out + tab_row_out<OP>(a, row);  // recomputed rather than kept in registers
 #pragma unroll
         for (int t = 0; t < TN; ++t) {
             const int col = col0 + t;
@@ -925,8 +863,7 @@ __device__ __forceinline__ void tab_body_dot(const TabArgs &a)
     constexpr int KS = dot_slab_steps(NW);
     constexpr int kDotSlab = KS * kDotStepBytes;
     constexpr int TN = DC;
-    constexpr bool SPLIT = split_a<OP>();
-    constexpr int NA = SPLIT ? 3 : 2;  // first-operand registers per step pair and lane row
+    constexpr int NA = 3;  // first-operand registers per step pair and lane row (one record)
     extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
 
     const int R = tab_rows<OP>(a);
@@ -943,13 +880,7 @@ __device__ __forceinline__ void tab_body_dot(const TabArgs &a)
 #pragma unroll
     for (int r = 0; r < TM; ++r) {
         const int row = row0 + 64 * r;
-        int ab = 0;
-        int64_t ob = 0;
-        if (row < R) {
-            tab_row<OP>(a, row, ab, ob);
-            if constexpr (split_a<OP>()) ab = tab_row_rec<OP>(a, row);
-        }
-        abase[r] = ab;
+        abase[r] = row < R ? tab_row_rec<OP>(a, row) : 0;  // rows past the end read record 0's run
     }
     const AView<TM> av = make_aview<OP, TM>(a, abase);
     const int count = tab_count<OP>(a);
@@ -993,11 +924,11 @@ __device__ __forceinline__ void tab_body_dot(const TabArgs &a)
         ok = otap * cpt * ch + oc < p_end;
         if (ok && otap != tp_) o = tab_tap<OP>(a, otap);
     };
-    TabTap cur{0, 0, 0, 0, 0};
+    TabTap cur{0, 0, 0, 0};
     int tap = q0 / max(cpt, 1);
     int c0 = (q0 - tap * cpt) * ch;
     bool have = q0 * ch < p_end;
-    TabTap nxt{0, 0, 0, 0, 0};
+    TabTap nxt{0, 0, 0, 0};
     int ntap = 0, nc0 = 0;
     bool has_next = false;
     if (have) {
@@ -1052,8 +983,8 @@ __device__ __forceinline__ void tab_body_dot(const TabArgs &a)
             for (int r = 0; r < TM; ++r) {
                 // entry byte offset = the mantissa field * 16 (the index plane, or the word's low
                 // half under its head) plus the slot's, which is a constant
-                const uint32_t o0 = SPLIT ? a0[r] : (a0[r] & 0xFFFFu);
-                const uint32_t o1 = SPLIT ? a1[r] : (a1[r] & 0xFFFFu);
+                const uint32_t o0 = a0[r];
+                const uint32_t o1 = a1[r];
                 uint32_t X[DC / 2], Y[DC / 2];
                 if constexpr (DC == 8) {
                     const u32x4 x4 = lds_load_b128(o0, BOFF + (2 * kp) * kDotStepBytes);
@@ -1072,11 +1003,7 @@ __device__ __forceinline__ void tab_body_dot(const TabArgs &a)
                         Y[q] = y2[q];
                     }
                 }
-                uint32_t pa;  // (pa(k), pa(k+1)) as bf16
-                if constexpr (SPLIT)
-                    pa = w[kp % RS][NA - 1][r];
-                else
-                    pa = __builtin_amdgcn_perm(a1[r], a0[r], 0x07060302u);
+                const uint32_t pa = w[kp % RS][NA - 1][r];  // (pa(k), pa(k+1)) as bf16
 #pragma unroll
                 for (int q = 0; q < TN / 2; ++q) {
                     acc[r][2 * q] = dot2_bf16(__builtin_amdgcn_perm(Y[q], X[q], 0x05040100u), pa, acc[r][2 * q]);
@@ -1184,8 +1111,7 @@ __device__ __forceinline__ void tab_body_hl(const TabArgs &a)
 {
     constexpr int NW = 8, TN = 8, KS = NW;
     constexpr int kSlab = KS * kHlStepBytes;
-    constexpr bool SPLIT = split_a<OP>();
-    constexpr int NA = SPLIT ? 3 : 2;  // first-operand registers per step pair and lane row
+    constexpr int NA = 3;  // first-operand registers per step pair and lane row (one record)
     extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
 
     const int R = tab_rows<OP>(a);
@@ -1202,13 +1128,7 @@ __device__ __forceinline__ void tab_body_hl(const TabArgs &a)
 #pragma unroll
     for (int r = 0; r < TM; ++r) {
         const int row = row0 + 64 * r;
-        int ab = 0;
-        int64_t ob = 0;
-        if (row < R) {
-            tab_row<OP>(a, row, ab, ob);
-            if constexpr (split_a<OP>()) ab = tab_row_rec<OP>(a, row);
-        }
-        abase[r] = ab;
+        abase[r] = row < R ? tab_row_rec<OP>(a, row) : 0;  // rows past the end read record 0's run
     }
     const AView<TM> av = make_aview<OP, TM>(a, abase);
     const int count = tab_count<OP>(a);
@@ -1240,11 +1160,11 @@ __device__ __forceinline__ void tab_body_hl(const TabArgs &a)
         ok = otap * cpt * ch + oc < p_end;
         if (ok && otap != tp_) o = tab_tap<OP>(a, otap);
     };
-    TabTap cur{0, 0, 0, 0, 0};
+    TabTap cur{0, 0, 0, 0};
     int tap = q0 / max(cpt, 1);
     int c0 = (q0 - tap * cpt) * ch;
     bool have = q0 * ch < p_end;
-    TabTap nxt{0, 0, 0, 0, 0};
+    TabTap nxt{0, 0, 0, 0};
     int ntap = 0, nc0 = 0;
     bool has_next = false;
     if (have) {
@@ -1280,13 +1200,9 @@ __device__ __forceinline__ void tab_body_hl(const TabArgs &a)
             const uint32_t(&a1)[TM] = w[kp % RS][1];
 #pragma unroll
             for (int r = 0; r < TM; ++r) {
-                const uint32_t o0 = SPLIT ? a0[r] : (a0[r] & 0xFFFFu);
-                const uint32_t o1 = SPLIT ? a1[r] : (a1[r] & 0xFFFFu);
-                uint32_t pp;  // (pa(k), pa(k+1)) as bf16
-                if constexpr (SPLIT)
-                    pp = w[kp % RS][NA - 1][r];
-                else
-                    pp = __builtin_amdgcn_perm(a1[r], a0[r], 0x07060302u);
+                const uint32_t o0 = a0[r];
+                const uint32_t o1 = a1[r];
+                const uint32_t pp = w[kp % RS][NA - 1][r];  // (pa(k), pa(k+1)) as bf16
                 const uint32_t pk0 = __builtin_amdgcn_perm(pp, pp, 0x01000100u);  // (pa(k), pa(k))
                 const uint32_t pk1 = __builtin_amdgcn_perm(pp, pp, 0x03020302u);  // (pa(k+1), pa(k+1))
                 const u32x4 x0 = lds_load_b128(o0, BOFF + (2 * kp) * kHlStepBytes);
