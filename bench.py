@@ -292,6 +292,8 @@ def other_kernels(B, W, torch, dev, lut7, m7, A, Bm, C, cv, conv_t, ws_g, ws_c):
     log("ResNet-50 layers done")
     ks["lenet5_b64_fwd_bwd"] = lenet_stack(B, W, torch, dev)
     log("LeNet-5 stack done")
+    ks["dense_batch1"] = dense_batch1(B, W, torch, dev, lut7, m7)
+    log("batch-1 dense layers done")
     # the step with the native FP32 multiply in the same kernels
     x, w, dy = conv_t
     conv_macs = W.conv_macs(cv)
@@ -312,6 +314,36 @@ def other_kernels(B, W, torch, dev, lut7, m7, A, Bm, C, cv, conv_t, ws_g, ws_c):
     ks["vendor_fp32"] = native_fp32(torch, W, dev, A, Bm, C)
     log("vendor FP32 step done")
     return ks
+
+
+def dense_batch1(B, W, torch, dev, lut, m_bits):
+    """Dense layers at batch 1 (the vector kernels): the ResNet-50 classifier 2048 -> 1000 forward
+    (1 x 2048 by 2048 x 1000), input gradient (1 x 1000 by the transposed weights) and weight
+    gradient (2048 x 1 by 1 x 1000, single products), and a 1 x 8192 by 8192 x 8192 product whose
+    8192^2 FP32 weights (256 MiB) set an HBM roofline: algorithmic bytes = the matrix, the vector
+    and the result, once each."""
+    r = {}
+    x = torch.from_numpy(W.uniform((1, 2048), 0.0, 1.0, 6100)).to(dev)
+    w = torch.from_numpy(W.glorot_uniform((2048, 1000), 2048, 1000, 6101)).to(dev)
+    dy = torch.from_numpy(W.normal((1, 1000), 0.01, 6102)).to(dev)
+    for name, fn in (("fc2048x1000_fwd", lambda: B.approx_gemm(x, w, lut, m_bits)),
+                     ("fc2048x1000_bwd_data", lambda: B.approx_gemm(dy, w, lut, m_bits, trans_b=True)),
+                     ("fc2048x1000_bwd_weight", lambda: B.approx_gemm(x, dy, lut, m_bits, trans_a=True))):
+        ms = _time_call(torch, fn, 20)
+        r[name] = {"call_ms": round(ms, 4), "gmacs_per_s": round(2048 * 1000 / ms / 1e6, 1)}
+    n = 8192
+    v = torch.from_numpy(W.normal((1, n), 1.0, 6103)).to(dev)
+    big = torch.from_numpy(W.normal((n, n), 0.01, 6104)).to(dev)
+    out = torch.empty((1, n), dtype=torch.float32, device=dev)
+    ws = torch.empty(max(1, B.amsim_gemm_workspace_size(0, 0, 1, n, n, m_bits)), dtype=torch.uint8, device=dev)
+    g = _time_main_kernel(B, torch, lambda: B.approx_gemm(v, big, lut, m_bits, out=out, workspace=ws), 10, "gemm",
+                          n * n)
+    nbytes = 4 * (n * n + 2 * n)
+    g["algorithmic_bytes"] = nbytes
+    g["hbm_gb_per_s"] = round(nbytes / (g["avg_ms"] * 1e-3) / 1e9, 1)
+    g["frac_of_8000_gb_per_s"] = round(nbytes / (g["avg_ms"] * 1e-3) / 8e12, 3)
+    r["gemv_1x8192x8192"] = g
+    return r
 
 
 def lenet_stack(B, W, torch, dev):

@@ -582,6 +582,359 @@ __global__ void mul_ew_kernel(int64_t n, const float *__restrict__ a, const floa
     }
 }
 
+// ------------------------------------------------------------------ vector GEMMs --------
+// One product a * b of the table's multiplier from the operands' bits (fa's index field ka << M,
+// fb's kb; the table in its canonical layout in global memory); NARROW: a format with fewer
+// exponent bits, scaled as the exact path scales it.
+template <bool NARROW>
+__device__ __forceinline__ float vec_product(uint32_t ua, uint32_t ub, const uint32_t *__restrict__ lut,
+                                             const DecFmt &fa, const DecFmt &fb, uint32_t vadd, float su, float sd)
+{
+    const uint32_t wa = amsim_decode_fmt(ua, fa), wb = amsim_decode_fmt(ub, fb);
+    const float v = __uint_as_float(((lut[(wa & kIdxMask) + (wb & kIdxMask)] & 0x00FFFFFFu) + 0x3F800000u) + vadd);
+    const float c = v * (head_value(wa) * head_value(wb));
+    return NARROW ? (c * su) * sd : c;
+}
+
+// GEMM with a vector operand (m == 1: op(A) is a row, the outputs are C's columns; n == 1:
+// op(B) is a column, the outputs are C's rows) -- a dense layer at batch 1.  The matrix element of
+// output o and step kk is mat[o * so + kk * sk], the vector's vec[kk * vs].  Every operand is
+// decoded where it is read, so the call is one of the two kernels below (and, when k is split,
+// the fixed-order reduction) only; split y of the grid covers steps [y * kchunk, (y + 1) * kchunk)
+// and writes its sums to part[y][o] when the grid splits k, else to out[o * os].  VEC_FIRST: the
+// vector is the first operand (the table's high index).  A product past the end of a run is
+// skipped, not added as a zero (a +0 product would turn a sum of -0 products into +0).
+//
+// MODE: GV_TAB_LDS (FP32 operands, M <= 7: each workgroup first stages the whole table into LDS
+// as the factors v = 2^carry * 1.mantissa, so a product is one LDS gather and two multiplies),
+// GV_TAB (FP32 operands, the table read from global memory), GV_NARROW (a (1, e, m) format, the
+// generic decode) or GV_NATIVE (the native FP32 multiply, one fma per product).
+enum { GV_NATIVE = 0, GV_TAB = 1, GV_TAB_LDS = 2, GV_NARROW = 3 };
+
+// An FP32 operand's head without branches: sign | exponent, with the quiet bit set for NaN (zeros
+// and denormals give +-0, Inf +-Inf: Algorithm 2's operand classes, as amsim_decode reads them).
+__device__ __forceinline__ float fp32_head(uint32_t u)
+{
+    return __uint_as_float((u & 0xFF800000u) | ((u & 0x7FFFFFFFu) > 0x7F800000u ? 0x00400000u : 0u));
+}
+
+struct GvCtx {
+    const uint32_t *lut;  // the table, canonical layout
+    const float *tab;     // GV_TAB_LDS: the staged factors
+    int m, shift;         // M, 23 - M
+    DecFmt fa, fb;        // GV_NARROW
+    uint32_t vadd;
+    float su, sd;
+};
+
+// One operand as the products use it: its bits, head and index field (ka << M for the first
+// operand, kb for the second).
+struct GvOp {
+    uint32_t u;
+    float p;
+    uint32_t i;
+};
+
+template <int MODE>
+__device__ __forceinline__ GvOp gv_operand(uint32_t u, bool first, const GvCtx &cx)
+{
+    GvOp o{u, 0.0f, 0u};
+    if constexpr (MODE == GV_TAB || MODE == GV_TAB_LDS) {
+        o.p = fp32_head(u);
+        o.i = ((u >> cx.shift) & ((1u << cx.m) - 1u)) << (first ? cx.m : 0);
+    }
+    return o;
+}
+
+template <int MODE>
+__device__ __forceinline__ float gv_mac(float acc, const GvOp &a, const GvOp &b, const GvCtx &cx)
+{
+    if constexpr (MODE == GV_NATIVE) {
+        return __builtin_fmaf(__uint_as_float(a.u), __uint_as_float(b.u), acc);
+    } else if constexpr (MODE == GV_NARROW) {
+        return acc + vec_product<true>(a.u, b.u, cx.lut, cx.fa, cx.fb, cx.vadd, cx.su, cx.sd);
+    } else {
+        const uint32_t idx = a.i | b.i;
+        const float v = MODE == GV_TAB_LDS ? cx.tab[idx]
+                                           : __uint_as_float((cx.lut[idx] & 0x00FFFFFFu) + 0x3F800000u);
+        return acc + v * (a.p * b.p);
+    }
+}
+
+template <bool VEC_FIRST, int MODE>
+__device__ __forceinline__ float gv_step(float acc, const GvOp &vop, uint32_t um, const GvCtx &cx)
+{
+    const GvOp mop = gv_operand<MODE>(um, !VEC_FIRST, cx);
+    return VEC_FIRST ? gv_mac<MODE>(acc, vop, mop, cx) : gv_mac<MODE>(acc, mop, vop, cx);
+}
+
+// GV_TAB_LDS without NaN operands: a product's factor v sits at LDS byte offset
+// (ka << (M + 2)) | (kb << 2), taken from each operand's bits with one shift and one mask, and its
+// head is the operand's sign and exponent bits alone (zeros and denormals +-0, Inf +-Inf); a
+// batch with a NaN operand takes the generic form instead (gv_step).
+struct GvFast {
+    int sh_m;        // matrix element: shift and mask of its index bits, already at their byte offset
+    uint32_t mk_m;
+    int sh_v;        // vector element: likewise
+    uint32_t mk_v;
+};
+
+template <bool VEC_FIRST>
+__device__ __forceinline__ GvFast gv_fast(const GvCtx &cx)
+{
+    const uint32_t mask = (1u << cx.m) - 1u;
+    const int hi = 21 - 2 * cx.m, lo = 21 - cx.m;  // shifts that leave ka at bit M + 2, kb at bit 2
+    return VEC_FIRST ? GvFast{lo, mask << 2, hi, mask << (cx.m + 2)} : GvFast{hi, mask << (cx.m + 2), lo, mask << 2};
+}
+
+__device__ __forceinline__ bool is_nan_bits(uint32_t u) { return (u & 0x7FFFFFFFu) > 0x7F800000u; }
+
+// The products of a batch of NV steps and NC outputs, added to acc[c] in step order: step i's
+// vector element uv[i] with the matrix element mat_at(i, c).  GV_TAB_LDS batches without a NaN
+// operand (checked over the wave) gather all their factors first, then multiply.
+template <bool VEC_FIRST, int MODE, int NV, int NC, class MatAt>
+__device__ __forceinline__ void gv_batch(float (&acc)[NC], const uint32_t (&uv)[NV], MatAt mat_at, const GvCtx &cx)
+{
+    if constexpr (MODE == GV_TAB_LDS) {
+        bool nan = false;
+#pragma unroll
+        for (int i = 0; i < NV; ++i) {
+            nan |= is_nan_bits(uv[i]);
+#pragma unroll
+            for (int c = 0; c < NC; ++c) nan |= is_nan_bits(mat_at(i, c));
+        }
+        if (__builtin_amdgcn_ballot_w64(nan) == 0) {
+            const GvFast f = gv_fast<VEC_FIRST>(cx);
+            const unsigned char *tb = reinterpret_cast<const unsigned char *>(cx.tab);
+            float v[NV][NC];
+#pragma unroll
+            for (int i = 0; i < NV; ++i) {
+                const uint32_t voff = (uv[i] >> f.sh_v) & f.mk_v;
+#pragma unroll
+                for (int c = 0; c < NC; ++c)
+                    v[i][c] = *reinterpret_cast<const float *>(tb + (((mat_at(i, c) >> f.sh_m) & f.mk_m) | voff));
+            }
+#pragma unroll
+            for (int i = 0; i < NV; ++i) {
+                const float pv = __uint_as_float(uv[i] & 0xFF800000u);
+#pragma unroll
+                for (int c = 0; c < NC; ++c) acc[c] += v[i][c] * (pv * __uint_as_float(mat_at(i, c) & 0xFF800000u));
+            }
+            return;
+        }
+    }
+#pragma unroll
+    for (int i = 0; i < NV; ++i) {
+        const GvOp vop = gv_operand<MODE>(uv[i], VEC_FIRST, cx);
+#pragma unroll
+        for (int c = 0; c < NC; ++c) acc[c] = gv_step<VEC_FIRST, MODE>(acc[c], vop, mat_at(i, c), cx);
+    }
+}
+
+// The table's factors into LDS (GV_TAB_LDS): 2^(2M) floats at the start of the dynamic LDS.
+template <int MODE>
+__device__ __forceinline__ const float *gv_stage(const GvCtx &cx, float *lds)
+{
+    if constexpr (MODE == GV_TAB_LDS) {
+        const int entries = 1 << (2 * cx.m);
+        for (int i = threadIdx.x; i < entries; i += blockDim.x)
+            lds[i] = __uint_as_float((cx.lut[i] & 0x00FFFFFFu) + 0x3F800000u);
+        __syncthreads();
+    }
+    return lds;
+}
+
+constexpr int kGemvUnroll = 8;  // steps whose loads a lane has in flight (column kernel)
+
+// Outputs contiguous in the matrix (so == 1): each lane owns kGemvCols consecutive outputs and
+// reads them with one 16-byte load per step (v4: mat 16-byte aligned and sk a multiple of 4;
+// otherwise, and for a last partial group, one load per element).  The vector's element of a
+// step is the same for the whole wave.  The waves of a workgroup (gv_waves) sum consecutive
+// parts of the split's steps for the same outputs, in step order, and their sums are added in
+// wave order.
+constexpr int gv_waves(int mode) { return mode == GV_TAB_LDS ? kGemvWavesLds : kGemvWavesGlobal; }
+
+template <bool VEC_FIRST, int MODE>
+__global__ __launch_bounds__(64 * gv_waves(MODE)) void gemv_cols_kernel(int64_t nout, int64_t k,
+                                                                    const float *__restrict__ vec, int64_t vs,
+                                                                    const float *__restrict__ mat, int64_t sk, int v4,
+                                                                    float *__restrict__ out, int64_t os,
+                                                                    float *__restrict__ part, int64_t kchunk, GvCtx cx)
+{
+    constexpr int WAVES = gv_waves(MODE);
+    extern __shared__ float gv_lds[];  // [table factors (GV_TAB_LDS)][WAVES][kGemvCols][64] sums
+    cx.tab = gv_stage<MODE>(cx, gv_lds);
+    float(*sums)[kGemvCols][64] =
+        reinterpret_cast<float(*)[kGemvCols][64]>(gv_lds + (MODE == GV_TAB_LDS ? (1 << (2 * cx.m)) : 0));
+    const int lane = threadIdx.x & 63, wave = wave_id();
+    const int64_t o0 = (int64_t(blockIdx.x) * 64 + lane) * kGemvCols;
+    const int64_t k0 = int64_t(blockIdx.y) * kchunk, k1 = min(k, k0 + kchunk);
+    const int64_t q = (k1 - k0 + WAVES - 1) / WAVES;
+    const int64_t s0 = min(k1, k0 + wave * q), s1 = min(k1, s0 + q);
+    float acc[kGemvCols];
+#pragma unroll
+    for (int c = 0; c < kGemvCols; ++c) acc[c] = -0.0f;
+    // every lane of the block owns kGemvCols outputs that 16-byte loads can read (uniform)
+    const bool block_full = v4 && (int64_t(blockIdx.x) + 1) * 64 * kGemvCols <= nout;
+    if (block_full) {
+        auto load = [&](int64_t k_at, uint32_t (&uv)[kGemvUnroll], u32x4 (&um)[kGemvUnroll]) {
+#pragma unroll
+            for (int i = 0; i < kGemvUnroll; ++i) {
+                uv[i] = __float_as_uint(vec[(k_at + i) * vs]);
+                um[i] = *reinterpret_cast<const u32x4 *>(mat + (k_at + i) * sk + o0);
+            }
+        };
+        // software pipeline over two register buffers: the next batch's loads are in flight while
+        // this batch's products run
+        uint32_t uv0[kGemvUnroll], uv1[kGemvUnroll];
+        u32x4 um0[kGemvUnroll], um1[kGemvUnroll];
+        auto run = [&](const uint32_t(&uv)[kGemvUnroll], const u32x4(&um)[kGemvUnroll]) {
+            gv_batch<VEC_FIRST, MODE, kGemvUnroll, kGemvCols>(acc, uv, [&](int i, int c) { return um[i][c]; }, cx);
+        };
+        int64_t kk = s0;
+        if (kk + kGemvUnroll <= s1) load(kk, uv0, um0);
+        while (kk + kGemvUnroll <= s1) {
+            const bool more = kk + 2 * kGemvUnroll <= s1;
+            if (more) load(kk + kGemvUnroll, uv1, um1);
+            run(uv0, um0);
+            kk += kGemvUnroll;
+            if (!more) break;
+            if (kk + 2 * kGemvUnroll <= s1) load(kk + kGemvUnroll, uv0, um0);
+            run(uv1, um1);
+            kk += kGemvUnroll;
+            if (!(kk + kGemvUnroll <= s1)) break;
+        }
+        for (; kk < s1; ++kk) {
+            const GvOp vop = gv_operand<MODE>(__float_as_uint(vec[kk * vs]), VEC_FIRST, cx);
+            const u32x4 um1 = *reinterpret_cast<const u32x4 *>(mat + kk * sk + o0);
+#pragma unroll
+            for (int c = 0; c < kGemvCols; ++c) acc[c] = gv_step<VEC_FIRST, MODE>(acc[c], vop, um1[c], cx);
+        }
+    } else if (o0 < nout) {  // the last block, or a matrix 16-byte loads cannot read: one load per element
+        const int nc = int(min<int64_t>(kGemvCols, nout - o0));
+        for (int64_t kk = s0; kk < s1; ++kk) {
+            const GvOp vop = gv_operand<MODE>(__float_as_uint(vec[kk * vs]), VEC_FIRST, cx);
+            const float *src = mat + kk * sk + o0;
+#pragma unroll
+            for (int c = 0; c < kGemvCols; ++c)
+                if (c < nc) acc[c] = gv_step<VEC_FIRST, MODE>(acc[c], vop, __float_as_uint(src[c]), cx);
+        }
+    }
+#pragma unroll
+    for (int c = 0; c < kGemvCols; ++c) sums[wave][c][lane] = acc[c];
+    __syncthreads();
+    if (wave != 0 || o0 >= nout) return;
+#pragma unroll
+    for (int c = 0; c < kGemvCols; ++c) {
+        const int64_t o = o0 + c;
+        if (o >= nout) break;
+        float r = sums[0][c][lane];
+#pragma unroll
+        for (int w = 1; w < WAVES; ++w) r += sums[w][c][lane];
+        if (part != nullptr)
+            part[int64_t(blockIdx.y) * nout + o] = r;
+        else
+            out[o * os] = r;
+    }
+}
+
+// Steps contiguous in the matrix (sk == 1): each wave owns kGemvRows outputs; its lanes take four
+// consecutive steps each (one 16-byte load per output when v4: mat 16-byte aligned and so a
+// multiple of 4), 256 steps per pass, and every lane sums its steps in order; a fixed butterfly
+// over the 64 lanes then adds the lanes' sums, and lane 0 stores them.  kchunk is a multiple of
+// 256, so the lanes' steps stay 4-aligned.
+template <bool VEC_FIRST, int MODE>
+__global__ __launch_bounds__(64 * gv_waves(MODE)) void gemv_rows_kernel(int64_t nout, int64_t k,
+                                                                    const float *__restrict__ vec, int64_t vs,
+                                                                    const float *__restrict__ mat, int64_t so, int v4,
+                                                                    float *__restrict__ out, int64_t os,
+                                                                    float *__restrict__ part, int64_t kchunk, GvCtx cx)
+{
+    constexpr int WAVES = gv_waves(MODE);
+    extern __shared__ float gv_lds[];  // table factors (GV_TAB_LDS)
+    cx.tab = gv_stage<MODE>(cx, gv_lds);
+    const int lane = threadIdx.x & 63, wave = wave_id();
+    const int64_t ob = (int64_t(blockIdx.x) * WAVES + wave) * kGemvRows;  // the wave's first output
+    if (ob >= nout) return;  // uniform over the wave (after the workgroup's staging)
+    const int64_t k0 = int64_t(blockIdx.y) * kchunk, k1 = min(k, k0 + kchunk);
+    const int nr = int(min<int64_t>(kGemvRows, nout - ob));
+    float acc[kGemvRows];
+#pragma unroll
+    for (int r = 0; r < kGemvRows; ++r) acc[r] = -0.0f;
+    // whole passes of 256 steps over kGemvRows outputs that 16-byte loads can read (uniform)
+    const bool fast = v4 && nr == kGemvRows;
+    const int64_t k_fast = fast ? k0 + (k1 - k0) / 256 * 256 : k0;
+    if (fast) {
+        auto load = [&](int64_t kb, uint32_t (&uv)[4], u32x4 (&um)[kGemvRows]) {
+            const int64_t kk = kb + 4 * lane;
+#pragma unroll
+            for (int i = 0; i < 4; ++i) uv[i] = __float_as_uint(vec[(kk + i) * vs]);
+#pragma unroll
+            for (int r = 0; r < kGemvRows; ++r) um[r] = *reinterpret_cast<const u32x4 *>(mat + (ob + r) * so + kk);
+        };
+        // software pipeline over two register buffers: the next pass's loads are in flight while
+        // this pass's products run
+        uint32_t uv0[4], uv1[4];
+        u32x4 um0[kGemvRows], um1[kGemvRows];
+        auto run = [&](const uint32_t(&uv)[4], const u32x4(&um)[kGemvRows]) {
+            gv_batch<VEC_FIRST, MODE, 4, kGemvRows>(acc, uv, [&](int i, int r) { return um[r][i]; }, cx);
+        };
+        int64_t kb = k0;
+        if (kb < k_fast) load(kb, uv0, um0);
+        while (kb < k_fast) {
+            const bool more = kb + 256 < k_fast;
+            if (more) load(kb + 256, uv1, um1);
+            run(uv0, um0);
+            kb += 256;
+            if (!more) break;
+            if (kb + 256 < k_fast) load(kb + 256, uv0, um0);
+            run(uv1, um1);
+            kb += 256;
+        }
+    }
+    // the rest (a last partial pass, fewer rows, or a matrix 16-byte loads cannot read): one load
+    // per element
+    for (int64_t kb = k_fast; kb < k1; kb += 256) {
+        const int64_t kk = kb + 4 * lane;
+        const int ns = int(max<int64_t>(0, min<int64_t>(4, k1 - kk)));
+        for (int i = 0; i < ns; ++i) {
+            const GvOp vop = gv_operand<MODE>(__float_as_uint(vec[(kk + i) * vs]), VEC_FIRST, cx);
+#pragma unroll
+            for (int r = 0; r < kGemvRows; ++r)
+                if (r < nr)
+                    acc[r] = gv_step<VEC_FIRST, MODE>(acc[r], vop, __float_as_uint(mat[(ob + r) * so + kk + i]), cx);
+        }
+    }
+#pragma unroll
+    for (int r = 0; r < kGemvRows; ++r)
+#pragma unroll
+        for (int off = 32; off > 0; off >>= 1) acc[r] += __shfl_xor(acc[r], off);
+    if (lane != 0) return;
+    for (int r = 0; r < nr; ++r) {
+        const int64_t o = ob + r;
+        if (part != nullptr)
+            part[int64_t(blockIdx.y) * nout + o] = acc[r];
+        else
+            out[o * os] = acc[r];
+    }
+}
+
+// GEMM with k == 1 (an outer product -- the weight gradient of a dense layer at batch 1): every
+// output is one product, C[i][j] = a_i * b_j (a sum of one product from -0.0 is that product).
+template <bool NATIVE, bool NARROW>
+__global__ __launch_bounds__(256) void outer_kernel(int64_t m, int64_t n, const float *__restrict__ a, int64_t as,
+                                                   const float *__restrict__ b, int64_t bs, float *__restrict__ C,
+                                                   int64_t ldc, const uint32_t *__restrict__ lut, DecFmt fa, DecFmt fb,
+                                                   uint32_t vadd, float su, float sd)
+{
+    for (int64_t t = int64_t(blockIdx.x) * 256 + threadIdx.x; t < m * n; t += int64_t(gridDim.x) * 256) {
+        const int64_t i = t / n, j = t - i * n;
+        const uint32_t ua = __float_as_uint(a[i * as]), ub = __float_as_uint(b[j * bs]);
+        C[i * ldc + j] = NATIVE ? __builtin_fmaf(__uint_as_float(ua), __uint_as_float(ub), -0.0f)
+                                : vec_product<NARROW>(ua, ub, lut, fa, fb, vadd, su, sd);
+    }
+}
+
 // The exponent cast on its own: y[i] = x[i] cast to the (1, e, m) format's range (see DecFmt),
 // as an FP32 value -- in range unchanged, below it a signed zero, above it a signed Inf or the
 // largest finite value (2 - 2^-m) * 2^beta; NaN and Inf as they are, denormals a signed zero.
@@ -863,10 +1216,12 @@ __global__ __launch_bounds__(256) void prep_rows_wide_kernel(const uint32_t *__r
 std::once_flag g_attr_once;
 hipError_t g_attr_err = hipSuccess;
 
+hipError_t gemv_attributes();
+
 void set_attributes()
 {
     for (hipError_t e : {tab_attributes<OP_GEMM>(), tab_attributes<OP_FWD>(), tab_attributes<OP_BWD_DATA>(),
-                         tab_attributes<OP_BWD_WEIGHT>()})
+                         tab_attributes<OP_BWD_WEIGHT>(), gemv_attributes()})
         if (e != hipSuccess && g_attr_err == hipSuccess) g_attr_err = e;
 }
 
@@ -1087,6 +1442,123 @@ inline int tab_variant(const Mode &md) { return md.native ? kTabNative : kTabApp
 // The table's row length for a call: the native multiply reads no table (its plan is M = 7's).
 inline int plan_m(const Mode &md, int m_bits) { return md.native ? 7 : m_bits; }
 
+// The column kernel's sums, per wave of its workgroup.
+inline size_t gemv_sum_bytes(int mode) { return size_t(gv_waves(mode)) * kGemvCols * 64 * 4; }
+
+inline size_t gemv_table_bytes(int mode, int m) { return mode == GV_TAB_LDS ? size_t(4) << (2 * m) : 0; }
+
+template <bool VEC_FIRST, int MODE>
+void launch_gemv(const VecPlan &vp, int64_t k, const float *vec, int64_t vs, const float *mat, int64_t so,
+                 int64_t sk, float *out, int64_t os, float *part, const GvCtx &cx, hipStream_t st)
+{
+    const bool aligned = reinterpret_cast<uintptr_t>(mat) % 16 == 0;
+    const size_t tab = gemv_table_bytes(MODE, cx.m);
+    const dim3 grid(unsigned(vp.blocks), unsigned(vp.splits));
+    if (!vp.rows) {  // so == 1
+        const int v4 = aligned && sk % 4 == 0 ? 1 : 0;
+        hipLaunchKernelGGL((gemv_cols_kernel<VEC_FIRST, MODE>), grid, dim3(64 * gv_waves(MODE)), tab + gemv_sum_bytes(MODE), st,
+                           vp.nout, k, vec, vs, mat, sk, v4, out, os, part, vp.kchunk, cx);
+    } else {  // sk == 1
+        const int v4 = aligned && so % 4 == 0 ? 1 : 0;
+        hipLaunchKernelGGL((gemv_rows_kernel<VEC_FIRST, MODE>), grid, dim3(64 * gv_waves(MODE)), tab, st, vp.nout, k,
+                           vec, vs, mat, so, v4, out, os, part, vp.kchunk, cx);
+    }
+}
+
+// m == 1: the vector op(A)(0, kk) = A[kk * a_sc], outputs C's columns; n == 1: the vector
+// op(B)(kk, 0) = B[kk * b_sr], outputs C's rows.
+template <int MODE>
+void launch_gemv_mode(const VecPlan &vp, int64_t m, int64_t k, const float *A, int64_t a_sr, int64_t a_sc,
+                      const float *B, int64_t b_sr, int64_t b_sc, float *C, int64_t ldc, float *part, const GvCtx &cx,
+                      hipStream_t st)
+{
+    if (m == 1)
+        launch_gemv<true, MODE>(vp, k, A, a_sc, B, b_sc, b_sr, C, 1, part, cx, st);
+    else
+        launch_gemv<false, MODE>(vp, k, B, b_sr, A, a_sr, a_sc, C, ldc, part, cx, st);
+}
+
+// Dynamic LDS beyond the default for the kernels that stage the table (called once).
+hipError_t gemv_attributes()
+{
+    const int cols = int(gemv_table_bytes(GV_TAB_LDS, 7) + gemv_sum_bytes(GV_TAB_LDS));
+    const int rows = int(gemv_table_bytes(GV_TAB_LDS, 7));
+    hipError_t e = hipSuccess;
+    for (hipError_t r :
+         {hipFuncSetAttribute(reinterpret_cast<const void *>(gemv_cols_kernel<true, GV_TAB_LDS>),
+                              hipFuncAttributeMaxDynamicSharedMemorySize, cols),
+          hipFuncSetAttribute(reinterpret_cast<const void *>(gemv_cols_kernel<false, GV_TAB_LDS>),
+                              hipFuncAttributeMaxDynamicSharedMemorySize, cols),
+          hipFuncSetAttribute(reinterpret_cast<const void *>(gemv_rows_kernel<true, GV_TAB_LDS>),
+                              hipFuncAttributeMaxDynamicSharedMemorySize, rows),
+          hipFuncSetAttribute(reinterpret_cast<const void *>(gemv_rows_kernel<false, GV_TAB_LDS>),
+                              hipFuncAttributeMaxDynamicSharedMemorySize, rows)})
+        if (r != hipSuccess && e == hipSuccess) e = r;
+    return e;
+}
+
+// Whether the vector kernels stage the table in LDS for a call (GV_TAB_LDS).
+inline bool gemv_lds(const Mode &md, int m_bits) { return !md.native && md.e_bits == 8 && m_bits <= 7; }
+
+// The GEMM with a vector operand or k == 1 (plan_vec): one kernel, plus the fixed-order
+// reduction when the vector kernel splits k.
+int vec_run(const Mode &md, const VecPlan &vp, int trans_a, int trans_b, int64_t m, int64_t n, int64_t k,
+            const float *A, int64_t lda, const float *B, int64_t ldb, float *C, int64_t ldc, const uint32_t *lut,
+            int m_bits, void *workspace, size_t workspace_bytes, hipStream_t st)
+{
+    if (vp.total > 0 && (!workspace || workspace_bytes < vp.total)) return AMSIM_ERR_WORKSPACE;
+    if (ensure_attributes() != AMSIM_OK) return AMSIM_ERR_HIP;
+    // op(A)(i, kk) = A[i * a_sr + kk * a_sc], op(B)(kk, j) = B[kk * b_sr + j * b_sc]
+    const int64_t a_sr = trans_a ? 1 : lda, a_sc = trans_a ? lda : 1;
+    const int64_t b_sr = trans_b ? 1 : ldb, b_sc = trans_b ? ldb : 1;
+    const int mb = plan_m(md, m_bits);
+    TabArgs sc{};
+    sc.vadd = 0u;
+    sc.su = sc.sd = 1.0f;
+    set_format_scales(sc, md);
+    GvCtx cx{};
+    cx.lut = lut;
+    cx.tab = nullptr;
+    cx.m = mb;
+    cx.shift = 23 - mb;
+    cx.fa = dec_fmt(md, mb, mb, 0u);  // index fields ka << M ...
+    cx.fb = dec_fmt(md, mb, 0, 0u);   // ... and kb
+    cx.vadd = sc.vadd;
+    cx.su = sc.su;
+    cx.sd = sc.sd;
+    const bool narrow = !md.native && md.e_bits < 8;
+    float *part = vp.kind == VEC_GEMV && vp.splits > 1 ? static_cast<float *>(workspace) : nullptr;
+    {
+        TimedLaunch tl(md.native ? AMSIM_KERNEL_GEMM_NATIVE : AMSIM_KERNEL_GEMM, st);
+        if (vp.kind == VEC_OUTER) {  // a_i = op(A)(i, 0), b_j = op(B)(0, j)
+            const dim3 g(unsigned(grid_for(m * n)));
+            if (md.native)
+                hipLaunchKernelGGL((outer_kernel<true, false>), g, dim3(256), 0, st, m, n, A, a_sr, B, b_sc, C, ldc,
+                                   lut, cx.fa, cx.fb, cx.vadd, cx.su, cx.sd);
+            else if (narrow)
+                hipLaunchKernelGGL((outer_kernel<false, true>), g, dim3(256), 0, st, m, n, A, a_sr, B, b_sc, C, ldc,
+                                   lut, cx.fa, cx.fb, cx.vadd, cx.su, cx.sd);
+            else
+                hipLaunchKernelGGL((outer_kernel<false, false>), g, dim3(256), 0, st, m, n, A, a_sr, B, b_sc, C, ldc,
+                                   lut, cx.fa, cx.fb, cx.vadd, cx.su, cx.sd);
+        } else if (md.native) {
+            launch_gemv_mode<GV_NATIVE>(vp, m, k, A, a_sr, a_sc, B, b_sr, b_sc, C, ldc, part, cx, st);
+        } else if (narrow) {
+            launch_gemv_mode<GV_NARROW>(vp, m, k, A, a_sr, a_sc, B, b_sr, b_sc, C, ldc, part, cx, st);
+        } else if (mb <= 7) {
+            launch_gemv_mode<GV_TAB_LDS>(vp, m, k, A, a_sr, a_sc, B, b_sr, b_sc, C, ldc, part, cx, st);
+        } else {
+            launch_gemv_mode<GV_TAB>(vp, m, k, A, a_sr, a_sc, B, b_sr, b_sc, C, ldc, part, cx, st);
+        }
+    }
+    if (launch_status() != AMSIM_OK) return AMSIM_ERR_HIP;
+    if (part != nullptr) {
+        launch_reduce(part, vp.splits, m == 1 ? 1 : int(m), m == 1 ? int(n) : 1, C, ldc, st);
+        return launch_status();
+    }
+    return AMSIM_OK;
+}
+
 int gemm_run(const Mode &md, int trans_a, int trans_b, int64_t m, int64_t n, int64_t k, const float *A, int64_t lda,
              const float *B, int64_t ldb, float *C, int64_t ldc, const uint32_t *lut, int m_bits, void *workspace,
              size_t workspace_bytes, hipStream_t st)
@@ -1103,6 +1575,10 @@ int gemm_run(const Mode &md, int trans_a, int trans_b, int64_t m, int64_t n, int
     }
     if (!A || !B || (!lut && !md.native)) return AMSIM_ERR_INVALID_ARG;
     if (lda < (trans_a ? m : k) || ldb < (trans_b ? k : n)) return AMSIM_ERR_INVALID_ARG;
+    const VecPlan vp = plan_vec(m, n, k, trans_a, trans_b, gemv_lds(md, m_bits));
+    if (vp.kind != VEC_NONE)
+        return vec_run(md, vp, trans_a, trans_b, m, n, k, A, lda, B, ldb, C, ldc, lut, m_bits, workspace,
+                       workspace_bytes, st);
     const int mb = plan_m(md, m_bits);
     const Plan p = plan_gemm(m, n, k, mb);
     if (!gemm_fits(p, m, n, k)) return AMSIM_ERR_UNSUPPORTED;
@@ -1376,7 +1852,8 @@ int approx_gemm_noalloc(int trans_a, int trans_b, int64_t m, int64_t n, int64_t 
     if (m > 0 && n > 0 && k > 0) {
         const int64_t lim = int64_t(1) << 31;
         if (m >= lim || n >= lim || k >= lim) return AMSIM_ERR_UNSUPPORTED;
-        need = plan_gemm(m, n, k, m_bits).total;
+        const VecPlan vp = plan_vec(m, n, k, trans_a, trans_b, gemv_lds(Mode{}, m_bits));
+        need = vp.kind != VEC_NONE ? vp.total : plan_gemm(m, n, k, m_bits).total;
     }
     if (need > kScratchBytes) return AMSIM_ERR_SCRATCH;
     void *ws = nullptr;
@@ -1390,8 +1867,6 @@ int approx_gemm_noalloc(int trans_a, int trans_b, int64_t m, int64_t n, int64_t 
 
 int amsim_gemm_workspace_size(int trans_a, int trans_b, int64_t m, int64_t n, int64_t k, int m_bits, size_t *bytes)
 {
-    (void)trans_a;
-    (void)trans_b;
     if (!bytes) return AMSIM_ERR_INVALID_ARG;
     if (!valid_m(m_bits)) return AMSIM_ERR_UNSUPPORTED;
     if (m < 0 || n < 0 || k < 0) return AMSIM_ERR_INVALID_ARG;
@@ -1400,7 +1875,10 @@ int amsim_gemm_workspace_size(int trans_a, int trans_b, int64_t m, int64_t n, in
         return AMSIM_OK;
     }
     // enough for every option of the call (the native multiply plans its own layout)
-    *bytes = std::max(plan_gemm(m, n, k, m_bits).total, plan_gemm(m, n, k, 7).total);
+    // (the vector kernels: whichever workgroup size the call's options choose)
+    const VecPlan v0 = plan_vec(m, n, k, trans_a, trans_b, false), v1 = plan_vec(m, n, k, trans_a, trans_b, true);
+    *bytes = v0.kind != VEC_NONE ? std::max(v0.total, v1.total)
+                                 : std::max(plan_gemm(m, n, k, m_bits).total, plan_gemm(m, n, k, 7).total);
     return AMSIM_OK;
 }
 

@@ -448,6 +448,64 @@ inline bool gemm_fits(const Plan &p, int64_t m, int64_t n, int64_t k)
            p.b_ld / tab_cols(p.tile) <= 65535;
 }
 
+// The vector GEMMs: m == 1 or n == 1 (one operand a vector: gemv_cols_kernel when the matrix's
+// outputs are contiguous, gemv_rows_kernel when its steps are) and k == 1 (an outer product,
+// outer_kernel).  k is split so that a launch holds about 2048 waves (8 per CU), each split at
+// least 32 steps (one 256-step pass of a wave for the row kernel); the splits' partial sums
+// [split][output] are the only workspace.
+// Waves per workgroup: 16 when the workgroup stages the whole table in LDS (M <= 7, FP32
+// operands: one 64 KiB copy then serves 16 waves), else 4.
+constexpr int kGemvWavesLds = 16, kGemvWavesGlobal = 4;
+inline int gemv_waves(bool lds) { return lds ? kGemvWavesLds : kGemvWavesGlobal; }
+constexpr int kGemvCols = 4;   // outputs per lane, column kernel
+constexpr int kGemvRows = 4;   // outputs per wave, row kernel
+
+enum { VEC_NONE = 0, VEC_GEMV = 1, VEC_OUTER = 2 };
+
+struct VecPlan {
+    int kind;
+    bool rows;       // the matrix's steps are contiguous (gemv_rows_kernel)
+    int64_t nout;    // outputs (n when m == 1, else m)
+    int64_t blocks;  // grid x
+    int splits;      // grid y
+    int64_t kchunk;  // steps per split
+    size_t total;    // workspace bytes
+};
+
+// lds: the vector kernel stages the table in LDS (gemv_waves)
+inline VecPlan plan_vec(int64_t m, int64_t n, int64_t k, int trans_a, int trans_b, bool lds)
+{
+    const int waves_wg = gemv_waves(lds);
+    VecPlan v{};
+    if (k == 1) {
+        v.kind = VEC_OUTER;
+        return v;
+    }
+    if (m != 1 && n != 1) return v;
+    v.kind = VEC_GEMV;
+    // m == 1: the matrix is B (steps contiguous when stored transposed); n == 1: A (steps
+    // contiguous unless stored transposed)
+    v.rows = m == 1 ? trans_b != 0 : trans_a == 0;
+    v.nout = m == 1 ? n : m;
+    int64_t waves, step_unit;
+    if (v.rows) {
+        v.blocks = ceil_div(v.nout, int64_t(waves_wg) * kGemvRows);
+        waves = ceil_div(v.nout, int64_t(kGemvRows));
+        step_unit = 256;
+    } else {
+        v.blocks = ceil_div(v.nout, int64_t(64) * kGemvCols);
+        waves = v.blocks * waves_wg;
+        step_unit = 32;
+    }
+    const int64_t want = std::max<int64_t>(1, ceil_div(2048, waves));
+    const int64_t most = std::max<int64_t>(1, ceil_div(k, step_unit));
+    v.kchunk = ceil_div(k, std::min(want, most));
+    if (v.rows) v.kchunk = round_up(v.kchunk, 256);
+    v.splits = int(ceil_div(k, v.kchunk));
+    v.total = v.splits > 1 ? align_up(size_t(v.splits) * size_t(v.nout) * 4) : 0;
+    return v;
+}
+
 // ------------------------------------------------------------------ kernel geometry ------
 // The table kernels' arguments apart from the pointers the launch fills in, and their grid.
 

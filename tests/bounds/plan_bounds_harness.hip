@@ -191,6 +191,36 @@ void check_gemm(Rng &rng, int64_t m, int64_t n, int64_t k, int mb)
     check_all_tiles<OP_GEMM>(rng, a, g, k, p.splits > 1 ? m * n : (m - 1) * n + n, n);
 }
 
+// The vector GEMMs (m == 1, n == 1, k == 1): split coverage, grid limits, partial sums inside the
+// workspace, and the 16-byte loads' alignment assumption for the row kernel's passes.
+void check_vec(int64_t m, int64_t n, int64_t k, int ta, int tb, bool lds)
+{
+    std::snprintf(g_case, sizeof g_case, "vector gemm m=%" PRId64 " n=%" PRId64 " k=%" PRId64 " ta=%d tb=%d lds=%d", m, n,
+                  k, ta, tb, int(lds));
+    const VecPlan v = plan_vec(m, n, k, ta, tb, lds);
+    if (k == 1) {
+        expect(v.kind == VEC_OUTER, "k == 1 is an outer product");
+        return;
+    }
+    if (m != 1 && n != 1) {
+        expect(v.kind == VEC_NONE, "not a vector shape");
+        return;
+    }
+    expect(v.kind == VEC_GEMV, "vector shape");
+    expect(v.nout == (m == 1 ? n : m), "outputs", v.nout, m == 1 ? n : m);
+    expect(v.splits >= 1 && v.splits <= 65535, "grid y", v.splits, 65535);
+    expect(v.kchunk >= 1 && int64_t(v.splits) * v.kchunk >= k, "splits cover k", int64_t(v.splits) * v.kchunk, k);
+    expect(int64_t(v.splits - 1) * v.kchunk < k, "no empty split", int64_t(v.splits - 1) * v.kchunk, k);
+    const int64_t per_block = v.rows ? int64_t(gemv_waves(lds)) * kGemvRows : int64_t(64) * kGemvCols;
+    expect(v.blocks >= 1 && v.blocks * per_block >= v.nout && (v.blocks - 1) * per_block < v.nout, "blocks cover outputs",
+           v.blocks, v.nout);
+    expect(v.blocks < (int64_t(1) << 31), "grid x", v.blocks, 0);
+    if (v.rows) expect(v.kchunk % 256 == 0, "row kernel passes stay 4-aligned", v.kchunk, 256);
+    const size_t part = v.splits > 1 ? size_t(v.splits) * size_t(v.nout) * 4 : 0;
+    expect(part <= v.total && v.total % kAlign == 0, "partial sums inside the workspace", int64_t(part), int64_t(v.total));
+    expect(int64_t(v.splits) * v.nout < (int64_t(1) << 31), "reduction indexes", int64_t(v.splits) * v.nout, 0);
+}
+
 void check_conv_pass(Rng &rng, const amsim_conv2d &d, int pass, int mb)
 {
     std::snprintf(g_case, sizeof g_case,
@@ -286,6 +316,12 @@ int main(int argc, char **argv)
         const int64_t n = rng.logu(1, big ? (int64_t(1) << 22) : 8192);
         const int64_t k = rng.logu(1, big ? (int64_t(1) << 22) : 8192);
         check_gemm(rng, m, n, k, mbs[rng.uniform(0, 8)]);
+        // the same sizes as vector shapes
+        const int ta = int(rng.uniform(0, 1)), tb = int(rng.uniform(0, 1));
+        const bool lds = rng.uniform(0, 1) != 0;
+        check_vec(1, n, k, ta, tb, lds);
+        check_vec(m, 1, k, ta, tb, lds);
+        check_vec(m, n, 1, ta, tb, lds);
         ++gemm_done;
     }
     while (conv_done < n_conv) {
