@@ -5,6 +5,9 @@ is a single product); sums within 1e-5 * sum|p| + 2^-126 per output.  Small shap
 on every output; the full-size workloads on seeded samples of outputs that the oracle
 computes one by one, in the same launch configuration the benchmark times.
 """
+import json
+import os
+
 import numpy as np
 import pytest
 
@@ -485,51 +488,94 @@ def _sample(total, count, seed):
     return np.sort(np.concatenate([idx, [0, total - 1]]).astype(np.int64))
 
 
-def _check_conv_full(B, p, m, seed, stem=False, samples=(2048, 2048, 512), relu=False, model="mitchell"):
+# Largest |gpu - oracle| / sum|p| of every full-size check, written as JSON to the path in
+# AMSIM_PARITY_REPORT (when set) at the end of the module.
+MAX_REL = {}
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _parity_report():
+    yield
+    path = os.environ.get("AMSIM_PARITY_REPORT")
+    if path and MAX_REL:
+        with open(path, "w") as f:
+            json.dump(MAX_REL, f, indent=1, sort_keys=True)
+
+
+def _record(name, got, ref, S, what):
+    rel = assert_within_tolerance(got, ref, S, what)
+    MAX_REL[name] = {"max_err_over_sum_abs_products": rel, "outputs_compared": int(np.size(ref))}
+    return rel
+
+
+def _check_conv_full(B, p, m, seed, stem=False, samples=(2048, 2048, 512), relu=False, model="mitchell", name=None):
+    """The three passes at full size.  samples: outputs compared per pass (seeded, plus the first
+    and last), or None for every output."""
     x, w, dy = W.resnet_conv_inputs(p, seed=seed, stem=stem)
     if relu:  # post-ReLU activations: about half exact zeros
         x = np.maximum(W.normal(x.shape, 1.0, seed + 7), 0.0).astype(np.float32)
     lut = dev_lut(B, model, m)
     om = MODELS[model]
+    name = name or "conv seed %d" % seed
     xd, wd, dyd = cuda(x), cuda(w), cuda(dy)
+
+    def pick(out, i, s):
+        return None if samples is None else _sample(out.size, samples[i], s)
+
     y = host(B.approx_conv2d_fwd(p, xd, wd, lut, m)).reshape(-1)
-    idx = _sample(y.size, samples[0], seed)
+    idx = pick(y, 0, seed)
     ref, S = oracle.conv2d_fwd(om, m, p, x, w, idx=idx)
-    assert_within_tolerance(y[idx], ref, S, "fwd")
+    _record(name + " fwd", y if idx is None else y[idx], ref, S, "fwd")
     dx = host(B.approx_conv2d_bwd_data(p, dyd, wd, lut, m)).reshape(-1)
-    idx = _sample(dx.size, samples[1], seed + 1)
+    idx = pick(dx, 1, seed + 1)
     ref, S = oracle.conv2d_bwd_data(om, m, p, dy, w, idx=idx)
-    assert_within_tolerance(dx[idx], ref, S, "bwd_data")
+    _record(name + " bwd_data", dx if idx is None else dx[idx], ref, S, "bwd_data")
     dw = host(B.approx_conv2d_bwd_weight(p, xd, dyd, lut, m)).reshape(-1)
-    idx = _sample(dw.size, samples[2], seed + 2)
+    idx = pick(dw, 2, seed + 2)
     ref, S = oracle.conv2d_bwd_weight(om, m, p, x, dy, idx=idx)
-    assert_within_tolerance(dw[idx], ref, S, "bwd_weight")
+    _record(name + " bwd_weight", dw if idx is None else dw[idx], ref, S, "bwd_weight")
     return y
 
 
-def test_resnet_3x3_conv_full_size(B):
+@pytest.mark.parametrize("pass_name", ["fwd", "bwd_data", "bwd_weight"])
+def test_resnet_3x3_conv_full_size(B, pass_name):
+    """ResNet 3x3 (batch 128, 64 -> 64 at 32x32) with the benchmark's inputs and launch: every
+    output of the pass against the oracle (about 30 s of oracle time per pass on 16 threads)."""
     cfg = W.RESNET_3X3
-    _check_conv_full(B, cfg["conv"], cfg["m_bits"], seed=3000)
+    p, m = cfg["conv"], cfg["m_bits"]
+    x, w, dy = W.resnet_conv_inputs(p, seed=3000)
+    lut = dev_lut(B, "mitchell", m)
+    if pass_name == "fwd":
+        got = host(B.approx_conv2d_fwd(p, cuda(x), cuda(w), lut, m))
+        ref, S = oracle.conv2d_fwd(oracle.MITCHELL, m, p, x, w)
+    elif pass_name == "bwd_data":
+        got = host(B.approx_conv2d_bwd_data(p, cuda(dy), cuda(w), lut, m))
+        ref, S = oracle.conv2d_bwd_data(oracle.MITCHELL, m, p, dy, w)
+    else:
+        got = host(B.approx_conv2d_bwd_weight(p, cuda(x), cuda(dy), lut, m))
+        ref, S = oracle.conv2d_bwd_weight(oracle.MITCHELL, m, p, x, dy)
+    _record("resnet 3x3 %s (all outputs)" % pass_name, got, ref, S, "resnet 3x3 " + pass_name)
 
 
 def test_resnet_3x3_conv_full_size_two_byte_table(B):
     """ResNet 3x3 at full size with the exact-truncation table (2-byte entries): the forward and
     backward-data passes take the hi/lo path, backward-weight the exact path."""
     cfg = W.RESNET_3X3
-    _check_conv_full(B, cfg["conv"], cfg["m_bits"], seed=3200, model="exact_trunc")
+    _check_conv_full(B, cfg["conv"], cfg["m_bits"], seed=3200, model="exact_trunc", name="resnet 3x3 exact_trunc")
 
 
 def test_resnet_3x3_relu_input_full_size(B):
     """The same layer with x = ReLU(N(0,1)): half the first operands of forward and backward-weight
     are exact zeros."""
     cfg = W.RESNET_3X3
-    _check_conv_full(B, cfg["conv"], cfg["m_bits"], seed=3100, relu=True)
+    _check_conv_full(B, cfg["conv"], cfg["m_bits"], seed=3100, relu=True, name="resnet 3x3 relu input")
 
 
 @pytest.mark.parametrize("li", range(len(W.RESNET50_LAYERS)))
 def test_resnet50_layers_full_size(B, li):
     cfg = W.RESNET50_LAYERS[li]
-    _check_conv_full(B, cfg["conv"], cfg["m_bits"], seed=4000 + 10 * li, stem=(li == 0), samples=(1024, 1024, 256))
+    _check_conv_full(B, cfg["conv"], cfg["m_bits"], seed=4000 + 10 * li, stem=(li == 0), samples=(1024, 1024, 256),
+                     name=cfg["name"])
 
 
 @pytest.mark.parametrize("m", [7, 11])
@@ -539,7 +585,7 @@ def test_gemm_4096_full_size(B, m):
     C = host(B.approx_gemm(cuda(A), cuda(Bm), dev_lut(B, "mitchell", m), m)).reshape(-1)
     idx = _sample(C.size, 1024, 5000 + m)
     ref, S = oracle.gemm(oracle.MITCHELL, m, A, Bm, idx=idx)
-    assert_within_tolerance(C[idx], ref, S, "gemm 4096 M=%d" % m)
+    _record("gemm 4096 M=%d" % m, C[idx], ref, S, "gemm 4096 M=%d" % m)
 
 
 def test_conv_deterministic(B):
