@@ -170,18 +170,22 @@ __global__ __launch_bounds__(256) void decode_pad_nhcw_kernel(const float *__res
 {
     extern __shared__ uint32_t tile[];  // cc * (w | 1) words (the launch sizes it)
     const int ws = w | 1;
+    const int nch = (c + cc - 1) / cc;  // channel chunks per row: a work item is (padded row, chunk)
     ExpStats st;
-    for (int rr = blockIdx.x; rr < n * hp; rr += gridDim.x) {
+    for (int item = blockIdx.x; item < n * hp * nch; item += gridDim.x) {
+        const int rr = item / nch, c0 = (item - rr * nch) * cc;
         const int b = rr / hp, y = rr - b * hp, ih = y - top;
-        uint32_t *dimg = dst + int64_t(rr) * cp * wp * 3;
+        const int ccn = min(cc, c - c0), qn = (ccn + 1) / 2;
+        // the chunk's records are one contiguous block [q][x] of the row's [cp][wp] records
+        uint32_t *dblk = dst + (int64_t(rr) * cp + c0 / 2) * wp * 3;
         if (unsigned(ih) >= unsigned(h)) {  // a padding row (uniform over the workgroup)
-            for (int i = threadIdx.x; i < cp * wp * 3; i += 256) dimg[i] = 0u;
+            for (int i = threadIdx.x; i < qn * wp * 3; i += 256) dblk[i] = 0u;
             continue;
         }
         const float *srow = src + (int64_t(b) * h + ih) * w * c;
-        for (int c0 = 0; c0 < c; c0 += cc) {
-            const int ccn = min(cc, c - c0), cnt = w * ccn;
-            __syncthreads();  // the previous chunk's stores have read the tile
+        {
+            const int cnt = w * ccn;
+            __syncthreads();  // the previous item's stores have read the tile
             for (int e0 = threadIdx.x; e0 < cnt; e0 += 256 * 8) {
                 uint32_t v[8];
                 int x[8], ch[8];
@@ -200,10 +204,7 @@ __global__ __launch_bounds__(256) void decode_pad_nhcw_kernel(const float *__res
                 }
             }
             __syncthreads();
-            // the chunk's records are one contiguous block [q][x]: consecutive threads write
-            // consecutive records
-            const int qn = (ccn + 1) / 2;
-            uint32_t *dblk = dimg + int64_t(c0 / 2) * wp * 3;
+            // consecutive threads write consecutive records
             const float inv_wp = 1.0f / float(wp);
             const bool small = qn * wp < (1 << 24);
             for (int rec = threadIdx.x; rec < qn * wp; rec += 256) {
@@ -291,44 +292,56 @@ __device__ __forceinline__ uint32_t zero_product_class(uint32_t u, int hi, int s
     return (u >> 31) ? 0u : kZeroPos;
 }
 
+// One workgroup per flag: its threads read the flag's weights (co innermost, contiguous) and OR
+// their classes.
 __global__ __launch_bounds__(256) void zero_tap_flags_kernel(const float *__restrict__ w, int KH, int KW, int CI, int CO,
                                                              int sh, int sw, int pt, int pl, int hi, int sat,
                                                              uint32_t *__restrict__ phase_flags,
                                                              uint32_t *__restrict__ kw_flags)
 {
+    __shared__ uint32_t s_or[4];
     const int nphase = phase_flags ? sh * sw * CI : 0, total = nphase + (kw_flags ? KW * CI : 0);
     const uint32_t *wu = reinterpret_cast<const uint32_t *>(w);
-    for (int t = blockIdx.x * blockDim.x + threadIdx.x; t < total; t += gridDim.x * blockDim.x) {
+    for (int t = blockIdx.x; t < total; t += gridDim.x) {
         uint32_t f = 0u;
-        if (t < nphase) {
+        if (t < nphase) {  // every (kh, kw, co) outside the phase's taps
             const int ci = t % CI, phase = t / CI, ph = phase / sw, pw = phase % sw;
-            for (int kh = 0; kh < KH; ++kh)
-                for (int kw = 0; kw < KW; ++kw) {
-                    if ((kh - ph - pt) % sh == 0 && (kw - pw - pl) % sw == 0) continue;  // a tap of the phase
-                    const uint32_t *wr = wu + (int64_t(kh * KW + kw) * CI + ci) * CO;
-                    for (int co = 0; co < CO; ++co) f |= zero_product_class(wr[co], hi, sat);
-                }
-            phase_flags[t] = f;
-        } else {
-            const int ci = (t - nphase) % CI, kw = (t - nphase) / CI;
-            for (int kh = 0; kh < KH; ++kh) {
-                const uint32_t *wr = wu + (int64_t(kh * KW + kw) * CI + ci) * CO;
-                for (int co = 0; co < CO; ++co) f |= zero_product_class(wr[co], hi, sat);
+            for (int j = threadIdx.x; j < KH * KW * CO; j += blockDim.x) {
+                const int co = j % CO, kk = j / CO, kh = kk / KW, kw = kk % KW;
+                if ((kh - ph - pt) % sh == 0 && (kw - pw - pl) % sw == 0) continue;  // a tap of the phase
+                f |= zero_product_class(wu[(int64_t(kk) * CI + ci) * CO + co], hi, sat);
             }
-            kw_flags[t - nphase] = f;
+        } else {  // every (kh, co) of the kernel column
+            const int ci = (t - nphase) % CI, kw = (t - nphase) / CI;
+            for (int j = threadIdx.x; j < KH * CO; j += blockDim.x) {
+                const int co = j % CO, kh = j / CO;
+                f |= zero_product_class(wu[(int64_t(kh * KW + kw) * CI + ci) * CO + co], hi, sat);
+            }
         }
+#pragma unroll
+        for (int o = 32; o > 0; o >>= 1) f |= uint32_t(__shfl_xor(int(f), o));
+        if ((threadIdx.x & 63) == 0) s_or[threadIdx.x >> 6] = f;
+        __syncthreads();
+        if (threadIdx.x == 0) {
+            const uint32_t r = s_or[0] | s_or[1] | s_or[2] | s_or[3];
+            if (t < nphase)
+                phase_flags[t] = r;
+            else
+                kw_flags[t - nphase] = r;
+        }
+        __syncthreads();  // s_or is reused by the next flag
     }
 }
 
 // Adds the products outside each output's stride phase (see zero_tap_flags_kernel) to dx
 // [n][H][W][CI]: NaN where one is NaN, +0 for an exactly -0 sum where one is +0.
-__global__ __launch_bounds__(256) void dilation_fixup_kernel(float *__restrict__ dx, int64_t total, int H, int Wd, int CI,
+// (total < 2^31: the convolution limits keep tensors below 2^29 elements)
+__global__ __launch_bounds__(256) void dilation_fixup_kernel(float *__restrict__ dx, int total, int H, int Wd, int CI,
                                                              int sh, int sw, const uint32_t *__restrict__ phase_flags)
 {
-    for (int64_t i = int64_t(blockIdx.x) * blockDim.x + threadIdx.x; i < total; i += int64_t(gridDim.x) * blockDim.x) {
-        const int ci = int(i % CI);
-        const int64_t t = i / CI;
-        const int x = int(t % Wd), y = int((t / Wd) % H);
+    for (int i = blockIdx.x * blockDim.x + threadIdx.x; i < total; i += gridDim.x * blockDim.x) {
+        const int ci = i % CI, t = i / CI;
+        const int x = t % Wd, y = (t / Wd) % H;
         const uint32_t f = phase_flags[((y % sh) * sw + x % sw) * CI + ci];
         if (f == 0u) continue;
         const uint32_t u = __float_as_uint(dx[i]);
@@ -344,18 +357,21 @@ __global__ __launch_bounds__(256) void dilation_fixup_kernel(float *__restrict__
 // dx[n][ih][iw][ci] = the sum, in ascending kw, of dxu[n][ih][ow][kw * c + ci] over the (kw, ow)
 // with ow * sw + kw - left = iw, 0 <= ow < ow_n; -0 (the empty sum) where there is none.  A kw with
 // no such ow reads zeros of the dilated, padded error at every kh: its products are those of
-// kw_flags (see zero_tap_flags_kernel).
+// kw_flags (see zero_tap_flags_kernel).  phase_flags (stride sh > 1): the virtual pass's flags per
+// row phase ih mod sh and unfolded channel, applied to each term as dilation_fixup_kernel would
+// apply them to dxu.  (n * h * w * c and the unfolded gradient stay below 2^31 elements.)
 __global__ __launch_bounds__(256) void fold_w_kernel(const float *__restrict__ dxu, int n, int h, int w, int c,
                                                      int kw_n, int sw, int left, int ow_n,
-                                                     const uint32_t *__restrict__ kw_flags, float *__restrict__ dx)
+                                                     const uint32_t *__restrict__ kw_flags,
+                                                     const uint32_t *__restrict__ phase_flags, int sh,
+                                                     float *__restrict__ dx)
 {
-    const int64_t total = int64_t(n) * h * w * c;
+    const int total = n * h * w * c;
     const int cu = kw_n * c;
-    for (int64_t i = int64_t(blockIdx.x) * blockDim.x + threadIdx.x; i < total; i += int64_t(gridDim.x) * blockDim.x) {
-        const int ci = int(i % c);
-        const int64_t t = i / c;
-        const int iw = int(t % w);
-        const int64_t row = t / w;  // n * h + ih
+    for (int i = blockIdx.x * blockDim.x + threadIdx.x; i < total; i += gridDim.x * blockDim.x) {
+        const int ci = i % c, t = i / c;
+        const int iw = t % w, row = t / w;  // row = n * h + ih
+        const uint32_t *pf = phase_flags ? phase_flags + (row % h % sh) * cu : nullptr;
         float acc = -0.0f;
         uint32_t zf = 0u;
         for (int k = 0; k < kw_n; ++k) {
@@ -365,7 +381,15 @@ __global__ __launch_bounds__(256) void fold_w_kernel(const float *__restrict__ d
                 zf |= kw_flags[k * c + ci];
                 continue;
             }
-            acc += dxu[(row * ow_n + ow) * cu + k * c + ci];
+            float term = dxu[(row * ow_n + ow) * cu + k * c + ci];
+            if (pf) {
+                const uint32_t f = pf[k * c + ci];
+                if (f & kZeroNan)
+                    term = __uint_as_float(0x7FC00000u);
+                else if ((f & kZeroPos) && __float_as_uint(term) == 0x80000000u)
+                    term = 0.0f;
+            }
+            acc += term;
         }
         if (zf & kZeroNan)
             acc = __uint_as_float(0x7FC00000u);
@@ -1649,8 +1673,12 @@ int decode_nhcw(const float *src, int n, int h, int w, int c, int top, int left,
                 const DecFmt &f, uint32_t *stats, int rec_c, hipStream_t st)
 {
     int cc = std::max(2, std::min(c, kNhcwTile / (w | 1)));  // channels per LDS tile
-    if (cc < c) cc &= ~1;  // chunks hold whole channel pairs
-    const int grid = int(std::min<int64_t>(int64_t(n) * hp, kStatSlots));  // one padded image row at a time
+    // few rows: narrower chunks, so that about 2048 (row, chunk) items keep the copy parallel
+    const int64_t rows = int64_t(n) * hp;
+    if (rows < 2048) cc = std::max(2, std::min(cc, int(ceil_div(c, ceil_div(2048, rows)))));
+    if (cc < c) cc = std::max(2, cc & ~1);  // chunks hold whole channel pairs
+    const int64_t items = rows * ceil_div(c, cc);
+    const int grid = int(std::min<int64_t>(items, kStatSlots));
     hipLaunchKernelGGL(decode_pad_nhcw_kernel, dim3(grid), dim3(256), size_t(cc) * (w | 1) * 4, st, src, n, h, w, c,
                        top, left, hp, wp, dst, f, stats, cc, (rec_c + 1) / 2);
     return grid;
@@ -1701,8 +1729,9 @@ int conv_fwd_run(const Mode &md, const amsim_conv2d *desc, const float *x, const
 }
 
 // The backward-data pass of `desc` (the caller's, or the virtual unfolded one) under plan p, into dx.
+// fixup: apply the dilation taps' products to dx here (the unfolded pass leaves them to the fold).
 int bwd_data_run(const Mode &md, const amsim_conv2d *desc, const Plan &p, const float *dy, const float *w, float *dx,
-                 const uint32_t *lut, int m_bits, void *workspace, hipStream_t st)
+                 const uint32_t *lut, int m_bits, void *workspace, hipStream_t st, bool fixup = true)
 {
     int rc;
     const int mb = plan_m(md, m_bits);
@@ -1735,11 +1764,12 @@ int bwd_data_run(const Mode &md, const amsim_conv2d *desc, const Plan &p, const 
                       int64_t(s.ci), st);
         if (launch_status() != AMSIM_OK) return AMSIM_ERR_HIP;
     }
-    if (s.sh * s.sw > 1) {  // the taps outside each output's stride phase (dilation zeros)
+    if (fixup && s.sh * s.sw > 1) {  // the taps outside each output's stride phase (dilation zeros)
         uint32_t *pf = reinterpret_cast<uint32_t *>(ws + p.off_bflags);
-        hipLaunchKernelGGL(zero_tap_flags_kernel, dim3(grid_for(int64_t(s.sh) * s.sw * s.ci)), dim3(256), 0, st, w,
-                           s.kh, s.kw, s.ci, s.co, s.sh, s.sw, s.pt, s.pl, fmt_hi(md), md.sat, pf, nullptr);
-        const int64_t total = int64_t(s.n) * s.h * s.w * s.ci;
+        const int nflags = s.sh * s.sw * s.ci;
+        hipLaunchKernelGGL(zero_tap_flags_kernel, dim3(std::min(nflags, 65535)), dim3(256), 0, st, w, s.kh, s.kw, s.ci,
+                           s.co, s.sh, s.sw, s.pt, s.pl, fmt_hi(md), md.sat, pf, nullptr);
+        const int total = s.n * s.h * s.w * s.ci;
         hipLaunchKernelGGL(dilation_fixup_kernel, dim3(grid_for(total)), dim3(256), 0, st, dx, total, s.h, s.w, s.ci,
                            s.sh, s.sw, pf);
     }
@@ -1756,17 +1786,21 @@ int conv_bwd_data_run(const Mode &md, const amsim_conv2d *desc, const float *dy,
     // the unfolded input's gradient, then folded back onto x's pixels
     const amsim_conv2d v = unfolded_desc(desc);
     float *dxu = reinterpret_cast<float *>(static_cast<char *>(workspace) + p.off_unf);
-    rc = bwd_data_run(md, &v, p, dy, w, dxu, lut, m_bits, workspace, st);
+    rc = bwd_data_run(md, &v, p, dy, w, dxu, lut, m_bits, workspace, st, false);
     if (rc != AMSIM_OK) return rc;
-    // the zero products of the kw taps that reach no output column (see fold_w_kernel), after the
-    // virtual pass's phase flags
-    uint32_t *kf = reinterpret_cast<uint32_t *>(static_cast<char *>(workspace) + p.off_bflags) +
-                   size_t(v.stride_h) * v.stride_w * v.c_in;
-    hipLaunchKernelGGL(zero_tap_flags_kernel, dim3(grid_for(int64_t(desc->kw) * desc->c_in)), dim3(256), 0, st, w,
-                       desc->kh, desc->kw, desc->c_in, desc->c_out, 1, 1, 0, 0, fmt_hi(md), md.sat, nullptr, kf);
-    const int64_t total = int64_t(desc->n) * desc->h * desc->w * desc->c_in;
+    // One flag launch over the virtual pass's weights [kh][kw * c][co] (the caller's [kh][kw][c][co]):
+    // the virtual pass's row-phase flags (stride_h > 1), then, per unfolded channel kw * c + ci, the
+    // flags of the kw taps that reach no output column (see fold_w_kernel).  The fold applies both.
+    uint32_t *pf = reinterpret_cast<uint32_t *>(static_cast<char *>(workspace) + p.off_bflags);
+    const int phases = v.stride_h;  // the virtual pass's stride along w is 1
+    uint32_t *kf = pf + size_t(phases) * v.c_in;
+    const int nflags = (phases > 1 ? phases * v.c_in : 0) + v.c_in;
+    hipLaunchKernelGGL(zero_tap_flags_kernel, dim3(std::min(nflags, 65535)), dim3(256), 0, st, w, v.kh, 1, v.c_in,
+                       v.c_out, v.stride_h, 1, v.pad_top, 0, fmt_hi(md), md.sat, phases > 1 ? pf : nullptr, kf);
+    const int total = desc->n * desc->h * desc->w * desc->c_in;
     hipLaunchKernelGGL(fold_w_kernel, dim3(grid_for(total)), dim3(256), 0, st, dxu, desc->n, desc->h, desc->w,
-                       desc->c_in, desc->kw, desc->stride_w, desc->pad_left, v.w, kf, dx);
+                       desc->c_in, desc->kw, desc->stride_w, desc->pad_left, v.w, kf, phases > 1 ? pf : nullptr,
+                       phases, dx);
     return launch_status();
 }
 
