@@ -45,7 +45,7 @@ FP32_LANE_RATE_T = 256 * 64 * 2.4e9 / 1e12
 TRAFFIC_PROFILE = os.path.join(ROOT, "profiles", "gemm_4096_m7_traffic.txt")
 # Device sources whose content the committed counters belong to (hashed in this order).
 KERNEL_SOURCES = [os.path.join(ROOT, "paper_2209_04161_amd", "csrc", f)
-                  for f in ("amsim_common.h", "amsim_tab.h", "amsim_tab.hip", "amsim_kernels.hip")]
+                  for f in ("amsim_common.h", "amsim_tab.h", "amsim_tab.hip", "amsim_kernels.hip", "amsim_plan.h")]
 
 
 def log(msg):
@@ -182,7 +182,7 @@ def main():
     roofline = {"bound": "alu", "achieved": round(achieved, 3), "peak": FP32_VECTOR_PEAK_TFLOPS,
                 "unit": "TFLOP/s", "frac": round(achieved / FP32_VECTOR_PEAK_TFLOPS, 4),
                 "traffic": read_traffic(),
-                "kernel": "tab_kernel<OP_GEMM, 4, 8, 8, 8, 7> (approx_gemm 4096^3, Mitchell M=7, bf16 pair path)"}
+                "kernel": "tab_kernel<OP_GEMM, 4, 8, 8, 8, 7, kTabApprox> (approx_gemm 4096^3, Mitchell M=7, bf16 pair path)"}
 
     out = {
         "metric": METRIC,
