@@ -380,6 +380,14 @@ def lenet_stack(B, W, torch, dev):
     ms = _time_call(torch, stack, 10)
     r = {"call_ms": round(ms, 4), "approx_macs": macs, "calls": 14}
     r.update(_rates(macs, ms))
+    # the same 14 calls captured once into a HIP graph and replayed: the host-side cost of the
+    # calls (argument checks, planning, torch allocations, launches) leaves the timed region
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        stack()
+    gms = _time_call(torch, graph.replay, 20)
+    r["graph_replay"] = {"call_ms": round(gms, 4)}
+    r["graph_replay"].update(_rates(macs, gms))
     return r
 
 
