@@ -91,7 +91,7 @@ __device__ __forceinline__ int wave_id() { return __builtin_amdgcn_readfirstlane
 // (which is exact only while no product can leave the normal range).  Finite non-zero operands
 // count; zeros and denormals (read as zeros) do not.  One packed word per workgroup:
 //   bits 0..7 smallest exponent field, 8..15 largest, bit 16 set if an Inf or NaN was seen.
-constexpr int kStatSlots = 8192;  // most workgroups of a decode launch that records them
+constexpr int kStatSlots = 8192;  // most workgroups of a decode job that records them
 
 struct ExpStats {
     uint32_t lo = 255u, hi = 0u, special = 0u;

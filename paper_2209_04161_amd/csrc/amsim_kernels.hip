@@ -67,23 +67,36 @@ __device__ __forceinline__ void store_record(uint32_t *d, uint32_t w0, uint32_t 
     d[2] = raw ? w1 : (w1 & 0xFFFFu);
 }
 
-// dst[(b * rows + r) * dld + c] = decode(src[b * sb + r * sr + c * sc]) for r < vrows, c < cols;
-// padding columns c in [cols, dld) and padding rows r in [vrows, rows) (whose source is not read)
-// are written as decoded +0.  dld is a multiple of 4 and
+// The pre-pass jobs below are workgroup bodies: `bid` of `nblk` workgroups of 256 threads take
+// the place of blockIdx.x and gridDim.x (see prepass_kernel).
+
+// The second operand's decode, dst[(b * rows + r) * dld + c] = decode(src[b * sb + r * sr + c * sc])
+// for r < vrows, c < cols; padding columns c in [cols, dld) and padding rows r in [vrows, rows)
+// (whose source is not read) are written as decoded +0.  dld is a multiple of 4 and
 // batches * rows * dld / 4 < 2^31: each thread takes groups of 4 columns (16-byte stores), two
 // groups per iteration so that 8 loads are in flight.  vec: sc == 1 and every row start is
 // 16-byte aligned, so a full group is one 16-byte load.
-__global__ __launch_bounds__(256) void decode_kernel(const float *__restrict__ src, int64_t sb, int64_t sr, int64_t sc,
-                                                     int batches, int rows, int vrows, int cols,
-                                                     uint32_t *__restrict__ dst,
-                                                     int dld, DecFmt f,
-                                                     uint32_t *__restrict__ stats, int vec)
+struct DecRows {
+    const float *src;
+    int64_t sb, sr, sc;
+    int batches, rows, vrows, cols;
+    uint32_t *dst;
+    int dld;
+    int vec;
+};
+
+__device__ __forceinline__ void decode_rows_body(const DecRows &d, DecFmt f, uint32_t *__restrict__ stats, uint32_t bid,
+                                                 uint32_t nblk)
 {
+    const float *__restrict__ src = d.src;
+    uint32_t *__restrict__ dst = d.dst;
+    const int64_t sb = d.sb, sr = d.sr, sc = d.sc;
+    const int rows = d.rows, vrows = d.vrows, cols = d.cols, dld = d.dld, vec = d.vec;
     const uint32_t qpr = uint32_t(dld) / 4u;
-    const uint32_t total = uint32_t(batches) * uint32_t(rows) * qpr;
-    const uint32_t step = gridDim.x * blockDim.x;
+    const uint32_t total = uint32_t(d.batches) * uint32_t(rows) * qpr;
+    const uint32_t step = nblk * 256u;
     ExpStats st;
-    for (uint32_t q0 = blockIdx.x * blockDim.x + threadIdx.x; q0 < total; q0 += 2u * step) {
+    for (uint32_t q0 = bid * 256u + threadIdx.x; q0 < total; q0 += 2u * step) {
         uint32_t w[2][4];
         uint32_t row[2], c[2];
         bool live[2];
@@ -121,21 +134,28 @@ __global__ __launch_bounds__(256) void decode_kernel(const float *__restrict__ s
             *reinterpret_cast<u32x4 *>(dst + int64_t(row[h]) * dld + c[h]) = o;
         }
     }
-    store_stats(st, stats, blockIdx.x);
+    store_stats(st, stats, int(bid));
 }
 
 // The backward-weight pass's first operand: the NHWC tensor inside its zero border as step-pair
 // records [n][hp][wp][c], record (b, y, x, ci) = the record of the decoded elements at columns x and
 // x + sw of padded row y (a column past the border, or outside x, a decoded +0).  A workgroup takes
 // one padded image row at a time; consecutive threads write consecutive records.
-__global__ __launch_bounds__(256) void decode_pad_pairs_kernel(const float *__restrict__ src, int n, int h, int w, int c,
-                                                               int top, int left, int hp, int wp, int sw,
-                                                               uint32_t *__restrict__ dst, DecFmt f,
-                                                               uint32_t *__restrict__ stats)
+struct DecPairs {
+    const float *src;
+    int n, h, w, c, top, left, hp, wp, sw;
+    uint32_t *dst;
+};
+
+__device__ __forceinline__ void decode_a_body(const DecPairs &d, DecFmt f, uint32_t *__restrict__ stats, int bid,
+                                              int nblk)
 {
+    const float *__restrict__ src = d.src;
+    uint32_t *__restrict__ dst = d.dst;
+    const int n = d.n, h = d.h, w = d.w, c = d.c, top = d.top, left = d.left, hp = d.hp, wp = d.wp, sw = d.sw;
     const int len = wp * c;
     ExpStats st;
-    for (int rr = blockIdx.x; rr < n * hp; rr += gridDim.x) {
+    for (int rr = bid; rr < n * hp; rr += nblk) {
         const int b = rr / hp, y = rr - b * hp, ih = y - top;
         const bool inside = unsigned(ih) < unsigned(h);  // uniform over the workgroup
         const float *srow = src + (int64_t(b) * h + ih) * w * c;
@@ -152,7 +172,7 @@ __global__ __launch_bounds__(256) void decode_pad_pairs_kernel(const float *__re
             store_record(drow + int64_t(i) * 3, amsim_decode_fmt(u0, f), amsim_decode_fmt(u1, f), f.raw);
         }
     }
-    store_stats(st, stats, blockIdx.x);
+    store_stats(st, stats, bid);
 }
 
 // Decoded NHWC tensor as step-pair records [n][hp][cp][wp] (cp = ceil(c / 2)) inside a zero
@@ -163,16 +183,25 @@ __global__ __launch_bounds__(256) void decode_pad_pairs_kernel(const float *__re
 // loads) goes through LDS as [channel][x] (row pitch w | 1, odd, so the transposing stores do not
 // collide in banks), then the workgroup writes the chunk's records, one per thread.
 
-__global__ __launch_bounds__(256) void decode_pad_nhcw_kernel(const float *__restrict__ src, int n, int h, int w, int c,
-                                                              int top, int left, int hp, int wp,
-                                                              uint32_t *__restrict__ dst, DecFmt f,
-                                                              uint32_t *__restrict__ stats, int cc, int cp)
+struct DecNhcw {
+    const float *src;
+    int n, h, w, c, top, left, hp, wp;
+    uint32_t *dst;
+    int cc, cp;
+};
+
+__device__ __forceinline__ void decode_a_body(const DecNhcw &d, DecFmt f, uint32_t *__restrict__ stats, int bid,
+                                              int nblk)
 {
     extern __shared__ uint32_t tile[];  // cc * (w | 1) words (the launch sizes it)
+    const float *__restrict__ src = d.src;
+    uint32_t *__restrict__ dst = d.dst;
+    const int n = d.n, h = d.h, w = d.w, c = d.c, top = d.top, left = d.left, hp = d.hp, wp = d.wp;
+    const int cc = d.cc, cp = d.cp;
     const int ws = w | 1;
     const int nch = (c + cc - 1) / cc;  // channel chunks per row: a work item is (padded row, chunk)
     ExpStats st;
-    for (int item = blockIdx.x; item < n * hp * nch; item += gridDim.x) {
+    for (int item = bid; item < n * hp * nch; item += nblk) {
         const int rr = item / nch, c0 = (item - rr * nch) * cc;
         const int b = rr / hp, y = rr - b * hp, ih = y - top;
         const int ccn = min(cc, c - c0), qn = (ccn + 1) / 2;
@@ -218,25 +247,33 @@ __global__ __launch_bounds__(256) void decode_pad_nhcw_kernel(const float *__res
             }
         }
     }
-    store_stats(st, stats, blockIdx.x);
+    store_stats(st, stats, bid);
 }
 
 // Forward pass with few input channels: x unfolded along w into the step-pair records of a
 // virtual input x'[n][y][ow][kw * c + ci] = x[n][y - top][ow * sw + kw - left][ci] (zero outside
-// x), laid out [n][hp][cp'][ow_n] (cp' = ceil(kw_n * c / 2)) like decode_pad_nhcw_kernel's
+// x), laid out [n][hp][cp'][ow_n] (cp' = ceil(kw_n * c / 2)) like the DecNhcw decode's
 // records; an odd kw_n * c leaves a padding channel, written as -0.  The forward pass of a
 // kh x kw kernel over x is then a sum over (kh, kw * c) steps whose records lie at one stride
 // (the host's unfolded_shape).  A workgroup takes one padded image row at a time and stages the
 // decoded source row (w * c <= kNhcwTile words) in LDS.
-__global__ __launch_bounds__(256) void decode_unfold_w_kernel(const float *__restrict__ src, int n, int h, int w, int c,
-                                                              int top, int left, int hp, int kw_n, int sw, int ow_n,
-                                                              uint32_t *__restrict__ dst, DecFmt f,
-                                                              uint32_t *__restrict__ stats)
+struct DecUnfold {
+    const float *src;
+    int n, h, w, c, top, left, hp, kw_n, sw, ow_n;
+    uint32_t *dst;
+};
+
+__device__ __forceinline__ void decode_a_body(const DecUnfold &d, DecFmt f, uint32_t *__restrict__ stats, int bid,
+                                              int nblk)
 {
     extern __shared__ uint32_t tile[];  // w * c words (the launch sizes it)
+    const float *__restrict__ src = d.src;
+    uint32_t *__restrict__ dst = d.dst;
+    const int n = d.n, h = d.h, w = d.w, c = d.c, top = d.top, left = d.left, hp = d.hp, kw_n = d.kw_n, sw = d.sw,
+              ow_n = d.ow_n;
     const int cu = kw_n * c, cp = (cu + 1) / 2;
     ExpStats st;
-    for (int rr = blockIdx.x; rr < n * hp; rr += gridDim.x) {
+    for (int rr = bid; rr < n * hp; rr += nblk) {
         const int b = rr / hp, y = rr - b * hp, ih = y - top;
         uint32_t *dimg = dst + int64_t(rr) * cp * ow_n * 3;
         if (unsigned(ih) >= unsigned(h)) {  // a padding row (uniform over the workgroup): +0, and the
@@ -270,7 +307,7 @@ __global__ __launch_bounds__(256) void decode_unfold_w_kernel(const float *__res
             store_record(dimg + int64_t(rec) * 3, wd[0], wd[1], f.raw);
         }
     }
-    store_stats(st, stats, blockIdx.x);
+    store_stats(st, stats, bid);
 }
 
 // Backward data: the products of the padded, dilated error (Algorithm 4) that the stride-phase
@@ -294,28 +331,35 @@ __device__ __forceinline__ uint32_t zero_product_class(uint32_t u, int hi, int s
 
 // One workgroup per flag: its threads read the flag's weights (co innermost, contiguous) and OR
 // their classes.
-__global__ __launch_bounds__(256) void zero_tap_flags_kernel(const float *__restrict__ w, int KH, int KW, int CI, int CO,
-                                                             int sh, int sw, int pt, int pl, int hi, int sat,
-                                                             uint32_t *__restrict__ phase_flags,
-                                                             uint32_t *__restrict__ kw_flags)
+struct ZeroTapFlags {
+    const float *w;
+    int KH, KW, CI, CO, sh, sw, pt, pl, hi, sat;
+    uint32_t *phase_flags, *kw_flags;
+    int total() const { return (phase_flags ? sh * sw * CI : 0) + (kw_flags ? KW * CI : 0); }
+};
+
+__device__ __forceinline__ void zero_tap_flags_body(const ZeroTapFlags &z, int bid, int nblk)
 {
     __shared__ uint32_t s_or[4];
+    const int KH = z.KH, KW = z.KW, CI = z.CI, CO = z.CO, sh = z.sh, sw = z.sw, pt = z.pt, pl = z.pl;
+    uint32_t *__restrict__ phase_flags = z.phase_flags;
+    uint32_t *__restrict__ kw_flags = z.kw_flags;
     const int nphase = phase_flags ? sh * sw * CI : 0, total = nphase + (kw_flags ? KW * CI : 0);
-    const uint32_t *wu = reinterpret_cast<const uint32_t *>(w);
-    for (int t = blockIdx.x; t < total; t += gridDim.x) {
+    const uint32_t *wu = reinterpret_cast<const uint32_t *>(z.w);
+    for (int t = bid; t < total; t += nblk) {
         uint32_t f = 0u;
         if (t < nphase) {  // every (kh, kw, co) outside the phase's taps
             const int ci = t % CI, phase = t / CI, ph = phase / sw, pw = phase % sw;
-            for (int j = threadIdx.x; j < KH * KW * CO; j += blockDim.x) {
+            for (int j = threadIdx.x; j < KH * KW * CO; j += 256) {
                 const int co = j % CO, kk = j / CO, kh = kk / KW, kw = kk % KW;
                 if ((kh - ph - pt) % sh == 0 && (kw - pw - pl) % sw == 0) continue;  // a tap of the phase
-                f |= zero_product_class(wu[(int64_t(kk) * CI + ci) * CO + co], hi, sat);
+                f |= zero_product_class(wu[(int64_t(kk) * CI + ci) * CO + co], z.hi, z.sat);
             }
         } else {  // every (kh, co) of the kernel column
             const int ci = (t - nphase) % CI, kw = (t - nphase) / CI;
-            for (int j = threadIdx.x; j < KH * CO; j += blockDim.x) {
+            for (int j = threadIdx.x; j < KH * CO; j += 256) {
                 const int co = j % CO, kh = j / CO;
-                f |= zero_product_class(wu[(int64_t(kh * KW + kw) * CI + ci) * CO + co], hi, sat);
+                f |= zero_product_class(wu[(int64_t(kh * KW + kw) * CI + ci) * CO + co], z.hi, z.sat);
             }
         }
 #pragma unroll
@@ -333,7 +377,7 @@ __global__ __launch_bounds__(256) void zero_tap_flags_kernel(const float *__rest
     }
 }
 
-// Adds the products outside each output's stride phase (see zero_tap_flags_kernel) to dx
+// Adds the products outside each output's stride phase (see zero_tap_flags_body) to dx
 // [n][H][W][CI]: NaN where one is NaN, +0 for an exactly -0 sum where one is +0.
 // (total < 2^31: the convolution limits keep tensors below 2^29 elements)
 __global__ __launch_bounds__(256) void dilation_fixup_kernel(float *__restrict__ dx, int total, int H, int Wd, int CI,
@@ -353,11 +397,11 @@ __global__ __launch_bounds__(256) void dilation_fixup_kernel(float *__restrict__
 }
 
 // Backward-data pass with few input channels, second half: the gradient of the w-unfolded input
-// (see decode_unfold_w_kernel), dxu[n][ih][ow][kw * c + ci], folded back onto x's pixels:
+// (see the DecUnfold decode), dxu[n][ih][ow][kw * c + ci], folded back onto x's pixels:
 // dx[n][ih][iw][ci] = the sum, in ascending kw, of dxu[n][ih][ow][kw * c + ci] over the (kw, ow)
 // with ow * sw + kw - left = iw, 0 <= ow < ow_n; -0 (the empty sum) where there is none.  A kw with
 // no such ow reads zeros of the dilated, padded error at every kh: its products are those of
-// kw_flags (see zero_tap_flags_kernel).  phase_flags (stride sh > 1): the virtual pass's flags per
+// kw_flags (see zero_tap_flags_body).  phase_flags (stride sh > 1): the virtual pass's flags per
 // row phase ih mod sh and unfolded channel, applied to each term as dilation_fixup_kernel would
 // apply them to dxu.  (n * h * w * c and the unfolded gradient stay below 2^31 elements.)
 __global__ __launch_bounds__(256) void fold_w_kernel(const float *__restrict__ dxu, int n, int h, int w, int c,
@@ -404,26 +448,44 @@ __global__ __launch_bounds__(256) void fold_w_kernel(const float *__restrict__ d
 // Pair records (records != null): records[(c / 2) * dld + r] = {index field of (r, c), head of
 // (r, c) | head of (r, c + 1) << 16 as bf16, index field of (r, c + 1)}, a column past the end
 // being a decoded +0.  The grid strides over 64 x 64 tiles in both directions.
-__global__ __launch_bounds__(256) void decode_t_kernel(const float *__restrict__ src, int64_t sr, int64_t sc, int rows,
-                                                       int cols, uint32_t *__restrict__ dst, int dld, DecFmt f,
-                                                       uint32_t *__restrict__ stats,
-                                                       uint32_t *__restrict__ records)
+// The workgroups form a gx x (nblk / gx) grid over the tiles, workgroup bid at (bid % gx, bid / gx).
+struct DecT {
+    const float *src;
+    int64_t sr, sc;
+    int rows, cols;
+    uint32_t *dst;
+    int dld;
+    uint32_t *records;
+    int gx;
+};
+
+__device__ __forceinline__ void decode_a_body(const DecT &d, DecFmt f, uint32_t *__restrict__ stats, int bid, int nblk)
 {
     __shared__ uint32_t tile[64][65];
+    const float *__restrict__ src = d.src;
+    uint32_t *__restrict__ dst = d.dst;
+    uint32_t *__restrict__ records = d.records;
+    const int64_t sr = d.sr, sc = d.sc;
+    const int rows = d.rows, cols = d.cols, dld = d.dld;
+    const int gx = d.gx, gy = nblk / d.gx, bx = bid % gx, by = bid / gx;
     const int tx = threadIdx.x & 63, ty = threadIdx.x >> 6;
     ExpStats st;
-    for (int r0 = blockIdx.x * 64; r0 < dld; r0 += gridDim.x * 64) {
-        for (int c0 = blockIdx.y * 64; c0 < cols; c0 += gridDim.y * 64) {
-            uint32_t u[16];
+    for (int r0 = bx * 64; r0 < dld; r0 += gx * 64) {
+        for (int c0 = by * 64; c0 < cols; c0 += gy * 64) {
+            // two halves of 8 loads: the registers of the second-operand decode it shares a launch with
+#pragma unroll 1
+            for (int hf = 0; hf < 16; hf += 8) {
+                uint32_t u[8];
 #pragma unroll
-            for (int i = 0; i < 16; ++i) {
-                const int r = r0 + ty + 4 * i, c = c0 + tx;
-                u[i] = (r < rows && c < cols) ? __float_as_uint(src[int64_t(r) * sr + int64_t(c) * sc]) : 0u;
-            }
+                for (int i = 0; i < 8; ++i) {
+                    const int r = r0 + ty + 4 * (hf + i), c = c0 + tx;
+                    u[i] = (r < rows && c < cols) ? __float_as_uint(src[int64_t(r) * sr + int64_t(c) * sc]) : 0u;
+                }
 #pragma unroll
-            for (int i = 0; i < 16; ++i) {
-                st.add(u[i]);
-                tile[ty + 4 * i][tx] = amsim_decode_fmt(u[i], f);
+                for (int i = 0; i < 8; ++i) {
+                    st.add(u[i]);
+                    tile[ty + 4 * (hf + i)][tx] = amsim_decode_fmt(u[i], f);
+                }
             }
             __syncthreads();
             if (records == nullptr) {
@@ -443,7 +505,7 @@ __global__ __launch_bounds__(256) void decode_t_kernel(const float *__restrict__
             __syncthreads();
         }
     }
-    store_stats(st, stats, blockIdx.y * gridDim.x + blockIdx.x);
+    store_stats(st, stats, bid);
 }
 
 // Direct evaluation, the comparison the paper draws for AMSim (Sec. "AMSim", its figure of GEMM
@@ -978,131 +1040,74 @@ __global__ void cast_kernel(int64_t n, const float *__restrict__ x, float *__res
 
 // ------------------------------------------------------------------ table preparation
 
-// The exact path's product form (flags[2]): 1 when a product must be rounded on its own before it
-// is added (t = v * (pa * pb), then the sum), 0 when fma(v, pa * pb, acc) gives the same result.
-// They differ only where v * (pa * pb) overflows to Inf -- exponent field Ea + Eb - 127 = 254 plus
-// a carry -- which an fma would fold into the sum unrounded: impossible when the largest finite
-// exponent fields of the two operands add up to at most 380.  Inf and NaN operands give the same
-// result either way, but their statistics carry no exponent range, so they take the rounded
-// form; so do formats with fewer exponent bits (`narrow`), whose products are scaled before the
-// add, and calls without statistics.
-__device__ __forceinline__ int exact_needs_rounded_products(bool have_stats, bool special, uint32_t a_hi,
-                                                            uint32_t b_hi, int narrow)
+// The table's transposed, width-reduced rows (M <= 7), one job of the pre-pass.  The entry width
+// eb is the fewest bytes that hold every entry's mantissa field: 1 when the low 16 bits of every
+// entry are zero, 2 when the low 8 are, else 4.  Row kb (kTabRowEntries * eb bytes) holds entry
+// (ka, kb) at byte ka * eb; with 1-byte entries dot_rows holds the same bytes in the order the
+// bf16 path stages them (byte 4 * (ka % 32) + ka / 32 of row kb), with 2-byte entries hl_rows the
+// entries split into bf16 halves for the hi/lo path.  Every workgroup ORs the whole table for eb
+// (a few tens of KiB, read from L2 after the first) and writes the rows kb of its share;
+// workgroup 0 also writes flags[0] = eb and the zero rows.
+struct TablePrep {
+    const uint32_t *lut;
+    int m;
+    int vec;               // lut 16-byte aligned
+    unsigned char *rows, *dot_rows;
+    uint32_t *hl_rows;
+    int *flags;
+    uint32_t *part;        // wide tables: one low-bits word per workgroup of the job
+};
+
+// Workgroups of the table job for M <= 7: rows of 8 entries kb each.
+inline int table_jobs(int m) { return std::max(1, std::min(16, (1 << m) / 8)); }
+
+__device__ __forceinline__ uint32_t block_or(uint32_t v, uint32_t *s4)
 {
-    return (narrow || !have_stats || special || a_hi + b_hi > 380u) ? 1 : 0;
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) v |= uint32_t(__shfl_xor(int(v), o));
+    if ((threadIdx.x & 63) == 0) s4[threadIdx.x >> 6] = v;
+    __syncthreads();
+    return s4[0] | s4[1] | s4[2] | s4[3];
 }
 
-constexpr int kPrepWorkgroups = 8;   // table preparation (M <= 7): workgroups sharing the rows
-
-// Transposed, width-reduced table: dst row kb (kTabRowEntries * EB bytes) holds entry
-// (ka, kb) at byte ka * EB.  With 1-byte entries it also writes dot_rows, the same bytes in the
-// order the bf16 path stages them: byte 4 * (ka % 32) + ka / 32 of row kb.  Then it reduces
-// the decode passes' exponent statistics (n_a words for the first operand, n_b for the second)
-// and decides whether the bf16 path is exact for this call.  Each workgroup reads the whole table
-// (the entry width depends on all of it) and writes its share of the rows; workgroup 0 also
-// reduces the statistics and writes flags[0] = the entry width, flags[1] = 1 when the bf16 path
-// may run, and the zero rows.
-__global__ __launch_bounds__(1024) void prep_rows_kernel(const uint32_t *__restrict__ lut, int m,
-                                                         unsigned char *__restrict__ dst,
-                                                         unsigned char *__restrict__ dot_rows,
-                                                         uint32_t *__restrict__ hl_rows,
-                                                         const uint32_t *__restrict__ stats_a, int n_a,
-                                                         const uint32_t *__restrict__ stats_b, int n_b,
-                                                         int narrow, int *__restrict__ flags)
+__device__ __forceinline__ void prep_table_body(const TablePrep &t, int bid, int nblk)
 {
-    __shared__ uint32_t slut[kTabRowEntries * kTabRowEntries];  // the table, canonical order
-    __shared__ uint32_t w_low[16], w_alo[16], w_ahs[16], w_blo[16], w_bhs[16];
-    __shared__ int s_eb;
-    const int n = 1 << m, total = n * n;
-    const int wave = int(threadIdx.x) >> 6;
-    uint32_t v[16];
-#pragma unroll
-    for (int i = 0; i < 16; ++i) {
-        const int k = int(threadIdx.x) + 1024 * i;
-        v[i] = k < total ? lut[k] : 0u;
-    }
-    const bool lead = blockIdx.x == 0;  // uniform over the workgroup
-    uint32_t sa[8], sb[8];
-#pragma unroll
-    for (int i = 0; i < 8; ++i) {
-        const int k = int(threadIdx.x) + 1024 * i;
-        sa[i] = lead && k < n_a ? stats_a[k] : 255u;
-        sb[i] = lead && k < n_b ? stats_b[k] : 255u;
-    }
-    uint32_t low = 0u, alo = 255u, ahs = 0u, blo = 255u, bhs = 0u;
-#pragma unroll
-    for (int i = 0; i < 16; ++i) {
-        const int k = int(threadIdx.x) + 1024 * i;
-        if (k < total) slut[k] = v[i];
-        low |= v[i] & 0xFFFFu;
-    }
-#pragma unroll
-    for (int i = 0; i < 8; ++i) {
-        // (special << 8 | largest exponent), as recorded by the decode passes
-        alo = min(alo, sa[i] & 0xFFu);
-        ahs = max(ahs, (sa[i] >> 8) & 0x1FFu);
-        blo = min(blo, sb[i] & 0xFFu);
-        bhs = max(bhs, (sb[i] >> 8) & 0x1FFu);
-    }
-#pragma unroll
-    for (int o = 32; o > 0; o >>= 1) low |= uint32_t(__shfl_xor(int(low), o));
-    alo = wave_min(alo);
-    ahs = wave_max(ahs);
-    blo = wave_min(blo);
-    bhs = wave_max(bhs);
-    if ((threadIdx.x & 63) == 0) {
-        w_low[wave] = low;
-        w_alo[wave] = alo;
-        w_ahs[wave] = ahs;
-        w_blo[wave] = blo;
-        w_bhs[wave] = bhs;
-    }
-    __syncthreads();
-    if (threadIdx.x == 0) {
-        uint32_t l = 0u, a_lo = 255u, a_hs = 0u, b_lo = 255u, b_hs = 0u;
-        for (int i = 0; i < int(blockDim.x) / 64; ++i) {
-            l |= w_low[i];
-            a_lo = min(a_lo, w_alo[i]);
-            a_hs = max(a_hs, w_ahs[i]);
-            b_lo = min(b_lo, w_blo[i]);
-            b_hs = max(b_hs, w_bhs[i]);
+    __shared__ uint32_t s_low[4];
+    const uint32_t *__restrict__ lut = t.lut;
+    const int n = 1 << t.m, total = n * n;
+    uint32_t low = 0u;
+    if (t.vec) {
+#pragma unroll 4
+        for (int i = threadIdx.x; i < total / 4; i += 256) {
+            const u32x4 q = reinterpret_cast<const u32x4 *>(lut)[i];
+            low |= q[0] | q[1] | q[2] | q[3];
         }
-        const int eb = l == 0u ? 1 : ((l & 0xFFu) == 0u ? 2 : 4);
-        s_eb = eb;
-        // Every product of finite non-zero operands then has exponent field
-        // Ea + Eb - 127 + carry in [1, 254], and v * pb (Eb + carry) stays below 255.
-        const uint32_t a_hi = a_hs & 0xFFu, b_hi = b_hs & 0xFFu;
-        const bool special = ((a_hs | b_hs) >> 8) != 0u;
-        const bool window = stats_a != nullptr && !special && a_lo + b_lo >= 128u && a_hi + b_hi <= 380u &&
-                            b_hi <= 253u;
-        // The hi/lo path (2-byte entries) also needs its low halves' products normal: v_lo >= 2^-15
-        // times pb normal as a bf16 (Eb >= 16) and times pa normal (Ea + Eb - 127 - 15 >= 1).
-        const bool window_hl = window && b_lo >= 16u && a_lo + b_lo >= 143u;
-        if (lead) {
-            flags[0] = eb;
-            flags[1] = narrow ? 0 : ((eb == 1 && window) ? 1 : ((eb == 2 && window_hl) ? 2 : 0));
-            flags[2] = exact_needs_rounded_products(stats_a != nullptr, special, a_hi, b_hi, narrow);
-        }
+        for (int i = (total / 4) * 4 + threadIdx.x; i < total; i += 256) low |= lut[i];
+    } else {
+#pragma unroll 4
+        for (int i = threadIdx.x; i < total; i += 256) low |= lut[i];
     }
-    __syncthreads();
-    const int eb = s_eb;
-    // Rows: thread -> (kb = consecutive threads, group of 4 entries), so that the LDS reads of a
-    // wave are consecutive words; each thread stores 4 entries.
-    const int tid = int(blockIdx.x * blockDim.x + threadIdx.x), nthreads = int(gridDim.x * blockDim.x);
-    for (int i = tid; i < n * ((n + 3) / 4); i += nthreads) {
-        const int kb = i % n, k4 = (i / n) * 4;
+    const uint32_t lb = block_or(low & 0xFFFFu, s_low);
+    const int eb = lb == 0u ? 1 : ((lb & 0xFFu) == 0u ? 2 : 4);
+    const bool lead = bid == 0;
+    if (lead && threadIdx.x == 0) t.flags[0] = eb;
+    const int per = (n + nblk - 1) / nblk, kb0 = bid * per, nk = max(0, min(n, kb0 + per) - kb0);
+    unsigned char *__restrict__ dst = t.rows;
+    // rows: thread -> (kb, group of 4 entries), consecutive threads along kb
+    for (int i = threadIdx.x; i < nk * ((n + 3) / 4); i += 256) {
+        const int kb = kb0 + i % nk, k4 = (i / nk) * 4;
         if (eb == 1) {
             uint32_t word = 0u;
 #pragma unroll
             for (int j = 0; j < 4; ++j)
-                if (k4 + j < n) word |= ((slut[(k4 + j) * n + kb] >> 16) & 0xFFu) << (8 * j);
+                if (k4 + j < n) word |= ((lut[(k4 + j) * n + kb] >> 16) & 0xFFu) << (8 * j);
             if (k4 + 4 <= n)
                 *reinterpret_cast<uint32_t *>(dst + size_t(kb) * kTabRowEntries + k4) = word;
             else
                 for (int j = 0; k4 + j < n; ++j) dst[size_t(kb) * kTabRowEntries + k4 + j] = (word >> (8 * j)) & 0xFFu;
         } else {
             for (int j = 0; j < 4 && k4 + j < n; ++j) {
-                const uint32_t e = slut[(k4 + j) * n + kb] & 0x00FFFFFFu;
+                const uint32_t e = lut[(k4 + j) * n + kb] & 0x00FFFFFFu;
                 unsigned char *row = dst + size_t(kb) * kTabRowEntries * eb;
                 if (eb == 2)
                     reinterpret_cast<uint16_t *>(row)[k4 + j] = static_cast<uint16_t>(e >> 8);
@@ -1113,22 +1118,25 @@ __global__ __launch_bounds__(1024) void prep_rows_kernel(const uint32_t *__restr
     }
     // the zero row
     if (lead) {
-        for (int i = threadIdx.x; i < kTabRowEntries * eb / 4; i += blockDim.x)
+        for (int i = threadIdx.x; i < kTabRowEntries * eb / 4; i += 256)
             reinterpret_cast<uint32_t *>(dst + size_t(kZeroRow) * kTabRowEntries * eb)[i] = 0u;
         if (eb == 1 && threadIdx.x < kTabRowEntries / 4)
-            reinterpret_cast<uint32_t *>(dot_rows + size_t(kZeroRow) * kTabRowEntries)[threadIdx.x] = 0u;
+            reinterpret_cast<uint32_t *>(t.dot_rows + size_t(kZeroRow) * kTabRowEntries)[threadIdx.x] = 0u;
     }
     // hi/lo rows (2-byte entries): words 2 g + i of row kb hold entry ka = g + 64 i as
     // (v_hi - 0x3F80) | (v_lo - 0x3F80) << 16 in bf16 bits; v_lo is never zero (see tab_body_hl).
+    // Workgroup 0 also writes the zero row's (kb = n).
     if (eb == 2) {
-        for (int i = tid; i < (n + 1) * 64; i += nthreads) {
-            const int kb = i / 64, g = i % 64;  // kb = n: the zero row
+        const int nr = nk + (lead ? 1 : 0);
+        for (int i = threadIdx.x; i < nr * 64; i += 256) {
+            const int r = i / 64, g = i % 64;
+            const int kb = r < nk ? kb0 + r : n;
             uint32_t word[2] = {0u, 0u};
 #pragma unroll
             for (int j = 0; j < 2; ++j) {
                 const int ka = g + 64 * j;
                 if (kb < n && ka < n) {
-                    const float v = __uint_as_float((slut[ka * n + kb] & 0x00FFFFFFu) + 0x3F800000u);
+                    const float v = __uint_as_float((lut[ka * n + kb] & 0x00FFFFFFu) + 0x3F800000u);
                     float hi = __uint_as_float(__float_as_uint(v) & 0xFFFF0000u);
                     float lo = v - hi;  // exact: the low 8 of v's 16 significant bits
                     if (lo == 0.0f) {   // one bf16 unit of v moves to the low half
@@ -1140,45 +1148,42 @@ __global__ __launch_bounds__(1024) void prep_rows_kernel(const uint32_t *__restr
                 }
             }
             const int row = kb < n ? kb : kZeroRow;
-            hl_rows[(row * 64 + g) * 2 + 0] = word[0];
-            hl_rows[(row * 64 + g) * 2 + 1] = word[1];
+            t.hl_rows[(row * 64 + g) * 2 + 0] = word[0];
+            t.hl_rows[(row * 64 + g) * 2 + 1] = word[1];
         }
     }
     // bf16-path rows: word g of row kb holds the bytes of entries g, g + 32, g + 64, g + 96.
     if (eb == 1) {
-        for (int i = tid; i < n * 32; i += nthreads) {
-            const int kb = i % n, g = i / n;
+        for (int i = threadIdx.x; i < nk * 32; i += 256) {
+            const int kb = kb0 + i % nk, g = i / nk;
             uint32_t word = 0u;
 #pragma unroll
             for (int j = 0; j < 4; ++j) {
                 const int ka = g + 32 * j;
-                if (ka < n) word |= ((slut[ka * n + kb] >> 16) & 0xFFu) << (8 * j);
+                if (ka < n) word |= ((lut[ka * n + kb] >> 16) & 0xFFu) << (8 * j);
             }
-            *reinterpret_cast<uint32_t *>(dot_rows + size_t(kb) * kTabRowEntries + 4 * g) = word;
+            *reinterpret_cast<uint32_t *>(t.dot_rows + size_t(kb) * kTabRowEntries + 4 * g) = word;
         }
     }
 }
 
-// Wide tables (M = 8..11, rows of 2^M entries, no bf16 path).  First pass: the OR of every entry's
-// low 16 mantissa bits, one word per workgroup.
-__global__ __launch_bounds__(256) void lut_low_bits_kernel(const uint32_t *__restrict__ lut, int total,
-                                                           uint32_t *__restrict__ part)
+// Wide tables (M = 8..11, rows of 2^M entries, no bf16 path).  The pre-pass job: the OR of the
+// entries' low 16 mantissa bits, one word per workgroup.
+__device__ __forceinline__ void lut_low_bits_body(const TablePrep &t, int bid, int nblk)
 {
     __shared__ uint32_t s_low[4];
+    const int total = 1 << (2 * t.m);
     uint32_t low = 0u;
-    for (int i = blockIdx.x * 256 + threadIdx.x; i < total; i += gridDim.x * 256) low |= lut[i] & 0xFFFFu;
-#pragma unroll
-    for (int o = 32; o > 0; o >>= 1) low |= uint32_t(__shfl_xor(int(low), o));
-    if ((threadIdx.x & 63) == 0) s_low[threadIdx.x >> 6] = low;
-    __syncthreads();
-    if (threadIdx.x == 0) part[blockIdx.x] = s_low[0] | s_low[1] | s_low[2] | s_low[3];
+    for (int i = bid * 256 + int(threadIdx.x); i < total; i += nblk * 256) low |= t.lut[i] & 0xFFFFu;
+    const uint32_t r = block_or(low, s_low);
+    if (threadIdx.x == 0) t.part[bid] = r;
 }
 
-// Second pass: the entry width from the nparts partial words, then the transposed rows -- row kb
-// (2^m entries of eb bytes) holds entry (ka, kb) at byte ka * eb -- through 64 x 64 LDS tiles
-// (loads along kb, stores along ka).  Workgroup 0 writes flags[0] = eb, flags[1] = 0 (no bf16
-// path for wide rows) and flags[2], the exact path's product form, from the decode statistics
-// (n_a and n_b words).
+// Second launch for wide tables: the entry width from the nparts partial words, then the
+// transposed rows -- row kb (2^m entries of eb bytes) holds entry (ka, kb) at byte ka * eb --
+// through 64 x 64 LDS tiles (loads along kb, stores along ka).  Workgroup 0 writes flags[0] = eb,
+// flags[1] = 0 (no bf16 path for wide rows) and flags[2], the exact path's product form, from
+// the decode statistics (n_a and n_b words; null for the native multiply).
 __global__ __launch_bounds__(256) void prep_rows_wide_kernel(const uint32_t *__restrict__ lut, int m,
                                                              const uint32_t *__restrict__ part, int nparts,
                                                              const uint32_t *__restrict__ stats_a, int n_a,
@@ -1188,31 +1193,33 @@ __global__ __launch_bounds__(256) void prep_rows_wide_kernel(const uint32_t *__r
 {
     __shared__ uint32_t tile[64][65];
     __shared__ uint32_t s_low[4], s_ahs[4], s_bhs[4];
-    uint32_t low = 0u, ahs = 0u, bhs = 0u;
+    uint32_t low = 0u;
     for (int i = threadIdx.x; i < nparts; i += 256) low |= part[i];
-    if (blockIdx.x == 0) {
-        for (int i = threadIdx.x; i < n_a; i += 256) ahs = max(ahs, (stats_a[i] >> 8) & 0x1FFu);
-        for (int i = threadIdx.x; i < n_b; i += 256) bhs = max(bhs, (stats_b[i] >> 8) & 0x1FFu);
-    }
-#pragma unroll
-    for (int o = 32; o > 0; o >>= 1) low |= uint32_t(__shfl_xor(int(low), o));
-    ahs = wave_max(ahs);
-    bhs = wave_max(bhs);
-    if ((threadIdx.x & 63) == 0) {
-        s_low[threadIdx.x >> 6] = low;
-        s_ahs[threadIdx.x >> 6] = ahs;
-        s_bhs[threadIdx.x >> 6] = bhs;
-    }
-    __syncthreads();
-    const uint32_t lb = s_low[0] | s_low[1] | s_low[2] | s_low[3];
+    const uint32_t lb = block_or(low, s_low);
     const int eb = lb == 0u ? 1 : ((lb & 0xFFu) == 0u ? 2 : 4);
-    if (blockIdx.x == 0 && threadIdx.x == 0) {
-        const uint32_t a_hs = max(max(s_ahs[0], s_ahs[1]), max(s_ahs[2], s_ahs[3]));
-        const uint32_t b_hs = max(max(s_bhs[0], s_bhs[1]), max(s_bhs[2], s_bhs[3]));
-        flags[0] = eb;
-        flags[1] = 0;
-        flags[2] = exact_needs_rounded_products(stats_a != nullptr && stats_b != nullptr, ((a_hs | b_hs) >> 8) != 0u,
-                                                a_hs & 0xFFu, b_hs & 0xFFu, narrow);
+    if (blockIdx.x == 0) {  // uniform
+        uint32_t alo = 255u, ahs = 0u, blo = 255u, bhs = 0u;
+        const bool have = stats_a != nullptr;
+        if (have) {
+            stats_fold<256>(stats_a, n_a, alo, ahs);
+            stats_fold<256>(stats_b, n_b, blo, bhs);
+        }
+        ahs = wave_max(ahs);
+        bhs = wave_max(bhs);
+        if ((threadIdx.x & 63) == 0) {
+            s_ahs[threadIdx.x >> 6] = ahs;
+            s_bhs[threadIdx.x >> 6] = bhs;
+        }
+        __syncthreads();
+        if (threadIdx.x == 0) {
+            const uint32_t a_hs = max(max(s_ahs[0], s_ahs[1]), max(s_ahs[2], s_ahs[3]));
+            const uint32_t b_hs = max(max(s_bhs[0], s_bhs[1]), max(s_bhs[2], s_bhs[3]));
+            int path, rounded;
+            decide_paths(eb, 0u, a_hs, 0u, b_hs, have, narrow, path, rounded);
+            flags[0] = eb;
+            flags[1] = 0;
+            flags[2] = rounded;
+        }
     }
     const int n = 1 << m, tiles_1d = n / 64;
     const int tx = threadIdx.x & 63, ty = threadIdx.x >> 6;
@@ -1232,6 +1239,86 @@ __global__ __launch_bounds__(256) void prep_rows_wide_kernel(const uint32_t *__r
         }
         __syncthreads();
     }
+}
+
+// The path flags of a call on rows of 128 entries whose table kernel reads them (kTabApprox):
+// flags[1] and flags[2] (decide_paths) from the decode statistics, once the pre-pass has written
+// the entry width flags[0].  One workgroup.
+__global__ __launch_bounds__(1024) void path_flags_kernel(const uint32_t *__restrict__ stats_a, int n_a,
+                                                          const uint32_t *__restrict__ stats_b, int n_b, int narrow,
+                                                          int *__restrict__ flags)
+{
+    __shared__ uint32_t red[16][4];
+    uint32_t alo = 255u, ahs = 0u, blo = 255u, bhs = 0u;
+    stats_fold<1024>(stats_a, n_a, alo, ahs);
+    stats_fold<1024>(stats_b, n_b, blo, bhs);
+    alo = wave_min(alo);
+    ahs = wave_max(ahs);
+    blo = wave_min(blo);
+    bhs = wave_max(bhs);
+    const int wave = int(threadIdx.x) >> 6;
+    if ((threadIdx.x & 63) == 0) {
+        red[wave][0] = alo;
+        red[wave][1] = ahs;
+        red[wave][2] = blo;
+        red[wave][3] = bhs;
+    }
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        uint32_t a_lo = 255u, a_hs = 0u, b_lo = 255u, b_hs = 0u;
+        for (int w = 0; w < 16; ++w) {
+            a_lo = min(a_lo, red[w][0]);
+            a_hs = max(a_hs, red[w][1]);
+            b_lo = min(b_lo, red[w][2]);
+            b_hs = max(b_hs, red[w][3]);
+        }
+        int path, rounded;
+        decide_paths(flags[0], a_lo, a_hs, b_lo, b_hs, true, narrow, path, rounded);
+        flags[1] = path;
+        flags[2] = rounded;
+    }
+}
+
+// ------------------------------------------------------------------ the pre-pass --------
+// One launch before each table kernel prepares everything it reads.  Its workgroups are dealt
+// out to four independent jobs, in this order: the table (prep_table_body, or the low-bits pass
+// of a wide table), the backward-data pass's zero-tap flags, the first operand's decode (one of
+// the decode_a_body layouts) and the second operand's (decode_rows_body).  The jobs write
+// disjoint parts of the workspace; the decode jobs' exponent statistics are reduced by the table
+// kernel's own workgroups (tab_paths), so nothing runs between the two launches.
+struct PrepJobs {
+    int n_tab, n_flag, n_a, n_b;  // workgroups of each job
+    int wide;                     // the table job is a wide table's low-bits pass
+    TablePrep t;
+    ZeroTapFlags z;
+    DecFmt fa, fb;
+    uint32_t *stats_a, *stats_b;  // decode statistics, or null (native multiply)
+    DecRows b;
+};
+
+template <class A>
+__global__ __launch_bounds__(256) void prepass_kernel(PrepJobs j, A a)
+{
+    int bid = int(blockIdx.x);
+    if (bid < j.n_tab) {
+        if (j.wide)
+            lut_low_bits_body(j.t, bid, j.n_tab);
+        else
+            prep_table_body(j.t, bid, j.n_tab);
+        return;
+    }
+    bid -= j.n_tab;
+    if (bid < j.n_flag) {
+        zero_tap_flags_body(j.z, bid, j.n_flag);
+        return;
+    }
+    bid -= j.n_flag;
+    if (bid < j.n_a) {
+        decode_a_body(a, j.fa, j.stats_a, bid, j.n_a);
+        return;
+    }
+    bid -= j.n_a;
+    decode_rows_body(j.b, j.fb, j.stats_b, uint32_t(bid), uint32_t(j.n_b));
 }
 
 // ------------------------------------------------------------------ host dispatch -------
@@ -1276,10 +1363,10 @@ inline int grid_for(int64_t total, int block = 256)
     return int(std::max<int64_t>(1, std::min<int64_t>(ceil_div(total, block), 8192)));
 }
 
-// Workgroups of decode_kernel for `words` output words (8 per thread and iteration).
+// Workgroups of a decode_rows_body job for `words` output words (8 per thread and iteration).
 inline int decode_grid(int64_t words) { return grid_for(ceil_div(words, 8)); }
 
-// decode_kernel's 16-byte load path: unit column stride and 16-byte aligned rows.
+// decode_rows_body's 16-byte load path: unit column stride and 16-byte aligned rows.
 inline int decode_vec(const float *src, int64_t sb, int64_t sr, int64_t sc)
 {
     return sc == 1 && reinterpret_cast<uintptr_t>(src) % 16 == 0 && sr % 4 == 0 && sb % 4 == 0 ? 1 : 0;
@@ -1348,28 +1435,61 @@ inline DecFmt fmt_second(const Mode &md, const Plan &p, int m_bits)
 inline uint32_t *stats_a(char *ws, const Plan &p) { return reinterpret_cast<uint32_t *>(ws + p.off_stats); }
 inline uint32_t *stats_b(char *ws, const Plan &p) { return reinterpret_cast<uint32_t *>(ws + p.off_stats) + kStatSlots; }
 
-// Launches the table preparation after both decode passes: rows, flags and the reduction of the
-// n_a / n_b statistics words.  Wide rows: a low-bits pass over the table, then the transposed rows.
-int prep_rows(const uint32_t *lut, int m_bits, char *ws, const Plan &p, int n_a, int n_b, const Mode &md,
-              hipStream_t st)
+// A call's pre-pass jobs without the decodes' geometry: the table job (none for the native
+// multiply; M <= 7 writes the rows itself, a wide table's low-bits pass is followed by
+// prep_rows_wide_kernel), the statistics and the operand formats.
+PrepJobs prep_jobs(const Mode &md, const uint32_t *lut, int mb, char *ws, const Plan &p)
 {
-    const int narrow = md.e_bits < 8 ? 1 : 0;
+    PrepJobs j{};
+    j.fa = fmt_first(md, mb);
+    j.fb = fmt_second(md, p, mb);
+    if (md.native) return j;
+    j.stats_a = stats_a(ws, p);
+    j.stats_b = stats_b(ws, p);
+    j.t.lut = lut;
+    j.t.m = mb;
+    j.t.vec = reinterpret_cast<uintptr_t>(lut) % 16 == 0 ? 1 : 0;
+    j.t.rows = reinterpret_cast<unsigned char *>(ws + p.off_rows);
+    j.t.dot_rows = reinterpret_cast<unsigned char *>(ws + p.off_dot_rows);
+    j.t.hl_rows = reinterpret_cast<uint32_t *>(ws + p.off_hl_rows);
+    j.t.flags = reinterpret_cast<int *>(ws + p.off_eb);
     if (p.rl == 7) {
-        hipLaunchKernelGGL(prep_rows_kernel, dim3(kPrepWorkgroups), dim3(1024), 0, st, lut, m_bits,
-                           reinterpret_cast<unsigned char *>(ws + p.off_rows),
-                           reinterpret_cast<unsigned char *>(ws + p.off_dot_rows),
-                           reinterpret_cast<uint32_t *>(ws + p.off_hl_rows), stats_a(ws, p), n_a, stats_b(ws, p), n_b,
-                           narrow, reinterpret_cast<int *>(ws + p.off_eb));
-        return launch_status();
+        j.n_tab = table_jobs(mb);
+    } else {
+        j.wide = 1;
+        j.t.part = reinterpret_cast<uint32_t *>(ws + p.off_wpart);
+        j.n_tab = int(std::min<int64_t>(ceil_div(int64_t(1) << (2 * mb), 256 * 16), kWidePartWords));
     }
-    const int total = 1 << (2 * m_bits);
-    const int nparts = int(std::min<int64_t>(ceil_div(total, 256 * 16), kWidePartWords));
-    uint32_t *part = reinterpret_cast<uint32_t *>(ws + p.off_wpart);
-    hipLaunchKernelGGL(lut_low_bits_kernel, dim3(nparts), dim3(256), 0, st, lut, total, part);
-    const int tiles = (1 << (m_bits - 6)) * (1 << (m_bits - 6));
-    hipLaunchKernelGGL(prep_rows_wide_kernel, dim3(std::min(tiles, 2048)), dim3(256), 0, st, lut, m_bits, part,
-                       nparts, stats_a(ws, p), n_a, stats_b(ws, p), n_b, narrow,
-                       reinterpret_cast<unsigned char *>(ws + p.off_rows), reinterpret_cast<int *>(ws + p.off_eb));
+    return j;
+}
+
+// The table kernel variant of a call of `macs` products: the native multiply's; for rows of 128
+// entries and fewer than kSelfMacs products the variant that decides its path itself (one launch
+// fewer, for calls whose launches take about as long as their work); else the one that reads the
+// path flags.
+constexpr int64_t kSelfMacs = int64_t(1) << 27;
+inline int tab_variant(const Mode &md, const Plan &p, int64_t macs)
+{
+    if (md.native) return kTabNative;
+    return p.rl == 7 && macs < kSelfMacs ? kTabApproxSelf : kTabApprox;
+}
+
+// Launches the pre-pass (first-operand decode a, lds its dynamic LDS bytes), then what the table
+// kernel variant `var` still needs: for a wide table the second table launch (which also writes
+// the path flags), for kTabApprox on rows of 128 entries the path flags.
+template <class A>
+int run_prepass(const PrepJobs &j, const A &a, size_t lds, int var, int narrow, hipStream_t st)
+{
+    const int blocks = j.n_tab + j.n_flag + j.n_a + j.n_b;
+    hipLaunchKernelGGL((prepass_kernel<A>), dim3(unsigned(blocks)), dim3(256), lds, st, j, a);
+    if (j.wide) {
+        const int tiles = (1 << (j.t.m - 6)) * (1 << (j.t.m - 6));
+        hipLaunchKernelGGL(prep_rows_wide_kernel, dim3(std::min(tiles, 2048)), dim3(256), 0, st, j.t.lut, j.t.m,
+                           j.t.part, j.n_tab, j.stats_a, j.n_a, j.stats_b, j.n_b, narrow, j.t.rows, j.t.flags);
+    } else if (var == kTabApprox) {
+        hipLaunchKernelGGL(path_flags_kernel, dim3(1), dim3(1024), 0, st, j.stats_a, j.n_a, j.stats_b, j.n_b, narrow,
+                           j.t.flags);
+    }
     return launch_status();
 }
 
@@ -1386,6 +1506,22 @@ TabArgs tab_args(TabArgs g, const Plan &p, char *ws, const uint32_t *A, const ui
     a.eb = reinterpret_cast<const int *>(ws + p.off_eb);
     return a;
 }
+
+// Operands cast to fewer exponent bits than FP32's (no bf16 path; products scaled before the add).
+inline int narrow_of(const Mode &md) { return !md.native && md.e_bits < 8 ? 1 : 0; }
+
+// The table kernel's view of the decode statistics (kTabApproxSelf decides its path from them).
+void set_stats(TabArgs &a, const PrepJobs &j, const Mode &md)
+{
+    a.stats_a = j.stats_a;
+    a.stats_b = j.stats_b;
+    a.n_a = j.n_a;
+    a.n_b = j.n_b;
+    a.narrow = narrow_of(md);
+}
+
+// Products of a convolution pass (the same for the three passes).
+inline int64_t conv_macs(const ConvShape &s) { return int64_t(s.n) * s.oh * s.ow * s.co * s.kh * s.kw * s.ci; }
 
 inline dim3 dim3_of(const TabGrid &g) { return dim3(g.x, g.y, g.z); }
 
@@ -1459,9 +1595,6 @@ void destroy_events(KernelTimer &t)
 // ==================================================================== C entry points =====
 
 namespace {
-
-// The table kernel variant of a launch.
-inline int tab_variant(const Mode &md) { return md.native ? kTabNative : kTabApprox; }
 
 // The table's row length for a call: the native multiply reads no table (its plan is M = 7's).
 inline int plan_m(const Mode &md, int m_bits) { return md.native ? 7 : m_bits; }
@@ -1615,24 +1748,22 @@ int gemm_run(const Mode &md, int trans_a, int trans_b, int64_t m, int64_t n, int
     // op(A)(i, kk): row stride / column stride in A's storage
     const int64_t a_sr = trans_a ? 1 : lda, a_sc = trans_a ? lda : 1;
     const int64_t b_sr = trans_b ? 1 : ldb, b_sc = trans_b ? ldb : 1;
-    const dim3 grid_dt(unsigned(std::min<int64_t>(ceil_div(p.a_ld, 64), 128)),
-                       unsigned(std::min<int64_t>(ceil_div(k, 64), 64)));  // <= kStatSlots workgroups
-    const int grid_b = decode_grid(k * p.b_ld);
-    uint32_t *sa = md.native ? nullptr : stats_a(ws, p), *sb = md.native ? nullptr : stats_b(ws, p);
-    hipLaunchKernelGGL(decode_t_kernel, grid_dt, dim3(256), 0, st, A, a_sr, a_sc, int(m), int(k), nullptr,
-                       int(p.a_ld), fmt_first(md, mb), sa, Ad);
-    hipLaunchKernelGGL(decode_kernel, dim3(grid_b), dim3(256), 0, st, B, int64_t(0), b_sr, b_sc, 1, int(k), int(k),
-                       int(n), Bd, int(p.b_ld), fmt_second(md, p, mb), sb, decode_vec(B, 0, b_sr, b_sc));
-    if (launch_status() != AMSIM_OK) return AMSIM_ERR_HIP;
-    if (!md.native && prep_rows(lut, mb, ws, p, int(grid_dt.x * grid_dt.y), grid_b, md, st) != AMSIM_OK)
-        return AMSIM_ERR_HIP;
+    PrepJobs j = prep_jobs(md, lut, mb, ws, p);
+    const int gx = int(std::min<int64_t>(ceil_div(p.a_ld, 64), 128)), gy = int(std::min<int64_t>(ceil_div(k, 64), 64));
+    const DecT da{A, a_sr, a_sc, int(m), int(k), nullptr, int(p.a_ld), Ad, gx};
+    j.n_a = gx * gy;  // <= kStatSlots
+    j.b = DecRows{B, 0, b_sr, b_sc, 1, int(k), int(k), int(n), Bd, int(p.b_ld), decode_vec(B, 0, b_sr, b_sc)};
+    j.n_b = decode_grid(k * p.b_ld);
+    const int var = tab_variant(md, p, m * n * k);
+    if (run_prepass(j, da, 0, var, narrow_of(md), st) != AMSIM_OK) return AMSIM_ERR_HIP;
     int rc;
     {
         TabArgs a = tab_args(gemm_geom(p, m, n, k, ldc), p, ws, Ad, Bd, out);
+        set_stats(a, j, md);
         set_format_scales(a, md);
         const dim3 grid = dim3_of(gemm_grid(p));
         TimedLaunch tl(md.native ? AMSIM_KERNEL_GEMM_NATIVE : AMSIM_KERNEL_GEMM, st);
-        rc = tab_launch<OP_GEMM>(p.tile, p.rl, tab_variant(md), a, grid, st) == hipSuccess
+        rc = tab_launch<OP_GEMM>(p.tile, p.rl, var, a, grid, st) == hipSuccess
                  ? AMSIM_OK
                  : AMSIM_ERR_HIP;
     }
@@ -1657,20 +1788,11 @@ int conv_common(const Mode &md, const amsim_conv2d *desc, int pass, const void *
     return AMSIM_OK;
 }
 
-// Step-pair records of an NHWC tensor inside its zero border (the backward-weight pass's x).
-// Returns the number of workgroups (statistics words written when stats is not null).
-int decode_pairs(const float *src, int n, int h, int w, int c, int top, int left, int hp, int wp, int sw, uint32_t *dst,
-                 const DecFmt &f, uint32_t *stats, hipStream_t st)
-{
-    const int grid = int(std::min<int64_t>(int64_t(n) * hp, kStatSlots));  // one padded image row per workgroup
-    hipLaunchKernelGGL(decode_pad_pairs_kernel, dim3(grid), dim3(256), 0, st, src, n, h, w, c, top, left, hp, wp, sw,
-                       dst, f, stats);
-    return grid;
-}
-
-// rec_c: channels of a record row (cp = ceil(rec_c / 2) records).
-int decode_nhcw(const float *src, int n, int h, int w, int c, int top, int left, int hp, int wp, uint32_t *dst,
-                const DecFmt &f, uint32_t *stats, int rec_c, hipStream_t st)
+// The first operand as step-pair records [n][hp][cp][wp] of an NHWC tensor inside its zero border
+// (decode_a_body for DecNhcw): the channels per LDS chunk and the workgroups (one (padded row,
+// chunk) item at a time); rec_c: channels of a record row (cp = ceil(rec_c / 2) records).
+DecNhcw nhcw_job(const float *src, int n, int h, int w, int c, int top, int left, int hp, int wp, uint32_t *dst,
+                 int rec_c, int *blocks, size_t *lds)
 {
     int cc = std::max(2, std::min(c, kNhcwTile / (w | 1)));  // channels per LDS tile
     // few rows: narrower chunks, so that about 2048 (row, chunk) items keep the copy parallel
@@ -1678,10 +1800,9 @@ int decode_nhcw(const float *src, int n, int h, int w, int c, int top, int left,
     if (rows < 2048) cc = std::max(2, std::min(cc, int(ceil_div(c, ceil_div(2048, rows)))));
     if (cc < c) cc = std::max(2, cc & ~1);  // chunks hold whole channel pairs
     const int64_t items = rows * ceil_div(c, cc);
-    const int grid = int(std::min<int64_t>(items, kStatSlots));
-    hipLaunchKernelGGL(decode_pad_nhcw_kernel, dim3(grid), dim3(256), size_t(cc) * (w | 1) * 4, st, src, n, h, w, c,
-                       top, left, hp, wp, dst, f, stats, cc, (rec_c + 1) / 2);
-    return grid;
+    *blocks = int(std::min<int64_t>(items, kStatSlots));
+    *lds = size_t(cc) * (w | 1) * 4;
+    return DecNhcw{src, n, h, w, c, top, left, hp, wp, dst, cc, (rec_c + 1) / 2};
 }
 
 int conv_fwd_run(const Mode &md, const amsim_conv2d *desc, const float *x, const float *w, float *y,
@@ -1695,31 +1816,32 @@ int conv_fwd_run(const Mode &md, const amsim_conv2d *desc, const float *x, const
     char *ws = static_cast<char *>(workspace);
     uint32_t *Xd = reinterpret_cast<uint32_t *>(ws + p.off_a);
     uint32_t *Wd = reinterpret_cast<uint32_t *>(ws + p.off_b);
-    uint32_t *sa = md.native ? nullptr : stats_a(ws, p), *sb = md.native ? nullptr : stats_b(ws, p);
     const int64_t rows = int64_t(s.n) * s.oh * s.ow;
     float *out = p.splits > 1 ? reinterpret_cast<float *>(ws + p.off_part) : y;
-    TabArgs a = tab_args(fwd_geom(p, s), p, ws, Xd, Wd, out);
-    int n_a;
-    if (p.unfold_w) {
-        n_a = int(std::min<int64_t>(int64_t(s.n) * p.Hp, kStatSlots));  // one padded image row at a time
-        hipLaunchKernelGGL(decode_unfold_w_kernel, dim3(n_a), dim3(256), size_t(s.w) * s.ci * 4, st, x, s.n, s.h, s.w,
-                           s.ci, s.pt, s.pl, p.Hp, s.kw, s.sw, s.ow, Xd, fmt_first(md, mb), sa);
-    } else {
-        n_a = decode_nhcw(x, s.n, s.h, s.w, s.ci, s.pt, s.pl, p.Hp, p.Wp, Xd, fmt_first(md, mb), sa, p.rec_c, st);
-    }
+    PrepJobs j = prep_jobs(md, lut, mb, ws, p);
     // w [kh][kw * ci][co] as batches kh of kw * ci rows (unfolded: padded to cu rows with +0)
     const int kwc = s.kw * s.ci, wrows = p.unfold_w ? unfolded_channels(s) : kwc;
-    const int n_b = decode_grid(int64_t(s.kh) * wrows * p.b_ld);
-    hipLaunchKernelGGL(decode_kernel, dim3(n_b), dim3(256), 0, st, w, int64_t(kwc) * s.co, int64_t(s.co), int64_t(1),
-                       s.kh, wrows, kwc, s.co, Wd, int(p.b_ld), fmt_second(md, p, mb), sb,
-                       decode_vec(w, int64_t(kwc) * s.co, s.co, 1));
-    if (launch_status() != AMSIM_OK) return AMSIM_ERR_HIP;
-    if (!md.native && prep_rows(lut, mb, ws, p, n_a, n_b, md, st) != AMSIM_OK) return AMSIM_ERR_HIP;
+    j.b = DecRows{w, int64_t(kwc) * s.co, int64_t(s.co), 1, s.kh, wrows, kwc, s.co, Wd, int(p.b_ld),
+                  decode_vec(w, int64_t(kwc) * s.co, s.co, 1)};
+    j.n_b = decode_grid(int64_t(s.kh) * wrows * p.b_ld);
+    const int var = tab_variant(md, p, conv_macs(s));
+    if (p.unfold_w) {
+        j.n_a = int(std::min<int64_t>(int64_t(s.n) * p.Hp, kStatSlots));  // one padded image row at a time
+        const DecUnfold da{x, s.n, s.h, s.w, s.ci, s.pt, s.pl, p.Hp, s.kw, s.sw, s.ow, Xd};
+        rc = run_prepass(j, da, size_t(s.w) * s.ci * 4, var, narrow_of(md), st);
+    } else {
+        size_t lds;
+        const DecNhcw da = nhcw_job(x, s.n, s.h, s.w, s.ci, s.pt, s.pl, p.Hp, p.Wp, Xd, p.rec_c, &j.n_a, &lds);
+        rc = run_prepass(j, da, lds, var, narrow_of(md), st);
+    }
+    if (rc != AMSIM_OK) return AMSIM_ERR_HIP;
+    TabArgs a = tab_args(fwd_geom(p, s), p, ws, Xd, Wd, out);
+    set_stats(a, j, md);
     set_format_scales(a, md);
     const dim3 grid = dim3_of(fwd_grid(p, s));
     {
         TimedLaunch tl(md.native ? AMSIM_KERNEL_CONV_FWD_NATIVE : AMSIM_KERNEL_CONV_FWD, st);
-        rc = tab_launch<OP_FWD>(p.tile, p.rl, tab_variant(md), a, grid, st) == hipSuccess
+        rc = tab_launch<OP_FWD>(p.tile, p.rl, var, a, grid, st) == hipSuccess
                  ? AMSIM_OK
                  : AMSIM_ERR_HIP;
     }
@@ -1730,8 +1852,9 @@ int conv_fwd_run(const Mode &md, const amsim_conv2d *desc, const float *x, const
 
 // The backward-data pass of `desc` (the caller's, or the virtual unfolded one) under plan p, into dx.
 // fixup: apply the dilation taps' products to dx here (the unfolded pass leaves them to the fold).
+// zf: the zero-tap flags the pre-pass computes (none when zf.total() == 0).
 int bwd_data_run(const Mode &md, const amsim_conv2d *desc, const Plan &p, const float *dy, const float *w, float *dx,
-                 const uint32_t *lut, int m_bits, void *workspace, hipStream_t st, bool fixup = true)
+                 const uint32_t *lut, int m_bits, void *workspace, hipStream_t st, bool fixup, const ZeroTapFlags &zf)
 {
     int rc;
     const int mb = plan_m(md, m_bits);
@@ -1739,22 +1862,25 @@ int bwd_data_run(const Mode &md, const amsim_conv2d *desc, const Plan &p, const 
     char *ws = static_cast<char *>(workspace);
     uint32_t *Dyd = reinterpret_cast<uint32_t *>(ws + p.off_a);
     uint32_t *Wtd = reinterpret_cast<uint32_t *>(ws + p.off_b);
-    uint32_t *sa = md.native ? nullptr : stats_a(ws, p), *sb = md.native ? nullptr : stats_b(ws, p);
     float *out = p.splits > 1 ? reinterpret_cast<float *>(ws + p.off_part) : dx;
-    TabArgs a = tab_args(bwd_data_geom(p, s), p, ws, Dyd, Wtd, out);
-    const int n_a = decode_nhcw(dy, s.n, s.oh, s.ow, s.co, p.pad_oh, p.pad_ow, p.OHp, p.OWp, Dyd, fmt_first(md, mb), sa,
-                                p.rec_c, st);
+    PrepJobs j = prep_jobs(md, lut, mb, ws, p);
+    j.z = zf;
+    j.n_flag = std::min(zf.total(), 65535);
+    size_t lds;
+    const DecNhcw da =
+        nhcw_job(dy, s.n, s.oh, s.ow, s.co, p.pad_oh, p.pad_ow, p.OHp, p.OWp, Dyd, p.rec_c, &j.n_a, &lds);
     // w[kh][kw][ci][co] -> Wt[kh][kw][co][ci]: batches (kh,kw), rows co, cols ci
-    const int n_b = decode_grid(int64_t(s.kh) * s.kw * s.co * p.b_ld);
-    hipLaunchKernelGGL(decode_kernel, dim3(n_b), dim3(256), 0, st, w, int64_t(s.ci) * s.co, int64_t(1), int64_t(s.co),
-                       s.kh * s.kw, s.co, s.co, s.ci, Wtd, int(p.b_ld), fmt_second(md, p, mb), sb, 0);
-    if (launch_status() != AMSIM_OK) return AMSIM_ERR_HIP;
-    if (!md.native && prep_rows(lut, mb, ws, p, n_a, n_b, md, st) != AMSIM_OK) return AMSIM_ERR_HIP;
+    j.b = DecRows{w, int64_t(s.ci) * s.co, 1, int64_t(s.co), s.kh * s.kw, s.co, s.co, s.ci, Wtd, int(p.b_ld), 0};
+    j.n_b = decode_grid(int64_t(s.kh) * s.kw * s.co * p.b_ld);
+    const int var = tab_variant(md, p, conv_macs(s));
+    if (run_prepass(j, da, lds, var, narrow_of(md), st) != AMSIM_OK) return AMSIM_ERR_HIP;
+    TabArgs a = tab_args(bwd_data_geom(p, s), p, ws, Dyd, Wtd, out);
+    set_stats(a, j, md);
     set_format_scales(a, md);
     const dim3 grid = dim3_of(bwd_data_grid(p, s));
     {
         TimedLaunch tl(md.native ? AMSIM_KERNEL_CONV_BWD_DATA_NATIVE : AMSIM_KERNEL_CONV_BWD_DATA, st);
-        rc = tab_launch<OP_BWD_DATA>(p.tile, p.rl, tab_variant(md), a, grid, st) == hipSuccess
+        rc = tab_launch<OP_BWD_DATA>(p.tile, p.rl, var, a, grid, st) == hipSuccess
                  ? AMSIM_OK
                  : AMSIM_ERR_HIP;
     }
@@ -1765,13 +1891,9 @@ int bwd_data_run(const Mode &md, const amsim_conv2d *desc, const Plan &p, const 
         if (launch_status() != AMSIM_OK) return AMSIM_ERR_HIP;
     }
     if (fixup && s.sh * s.sw > 1) {  // the taps outside each output's stride phase (dilation zeros)
-        uint32_t *pf = reinterpret_cast<uint32_t *>(ws + p.off_bflags);
-        const int nflags = s.sh * s.sw * s.ci;
-        hipLaunchKernelGGL(zero_tap_flags_kernel, dim3(std::min(nflags, 65535)), dim3(256), 0, st, w, s.kh, s.kw, s.ci,
-                           s.co, s.sh, s.sw, s.pt, s.pl, fmt_hi(md), md.sat, pf, nullptr);
         const int total = s.n * s.h * s.w * s.ci;
         hipLaunchKernelGGL(dilation_fixup_kernel, dim3(grid_for(total)), dim3(256), 0, st, dx, total, s.h, s.w, s.ci,
-                           s.sh, s.sw, pf);
+                           s.sh, s.sw, zf.phase_flags);
     }
     return launch_status();
 }
@@ -1782,21 +1904,26 @@ int conv_bwd_data_run(const Mode &md, const amsim_conv2d *desc, const float *dy,
     Plan p;
     int rc = conv_common(md, desc, AMSIM_CONV_BWD_DATA, dy, w, dx, lut, m_bits, workspace, workspace_bytes, &p);
     if (rc != AMSIM_OK) return rc;
-    if (!p.unfold_w) return bwd_data_run(md, desc, p, dy, w, dx, lut, m_bits, workspace, st);
-    // the unfolded input's gradient, then folded back onto x's pixels
+    uint32_t *pf = reinterpret_cast<uint32_t *>(static_cast<char *>(workspace) + p.off_bflags);
+    if (!p.unfold_w) {
+        ZeroTapFlags zf{};
+        if (desc->stride_h * desc->stride_w > 1)  // the taps outside each output's stride phase
+            zf = ZeroTapFlags{w,  desc->kh, desc->kw, desc->c_in, desc->c_out, desc->stride_h, desc->stride_w,
+                              desc->pad_top, desc->pad_left, fmt_hi(md), md.sat, pf, nullptr};
+        return bwd_data_run(md, desc, p, dy, w, dx, lut, m_bits, workspace, st, true, zf);
+    }
+    // the unfolded input's gradient, then folded back onto x's pixels.  The pre-pass computes the
+    // flags over the virtual pass's weights [kh][kw * c][co] (the caller's [kh][kw][c][co]): the
+    // virtual pass's row-phase flags (stride_h > 1), then, per unfolded channel kw * c + ci, the
+    // flags of the kw taps that reach no output column (see fold_w_kernel).  The fold applies both.
     const amsim_conv2d v = unfolded_desc(desc);
     float *dxu = reinterpret_cast<float *>(static_cast<char *>(workspace) + p.off_unf);
-    rc = bwd_data_run(md, &v, p, dy, w, dxu, lut, m_bits, workspace, st, false);
-    if (rc != AMSIM_OK) return rc;
-    // One flag launch over the virtual pass's weights [kh][kw * c][co] (the caller's [kh][kw][c][co]):
-    // the virtual pass's row-phase flags (stride_h > 1), then, per unfolded channel kw * c + ci, the
-    // flags of the kw taps that reach no output column (see fold_w_kernel).  The fold applies both.
-    uint32_t *pf = reinterpret_cast<uint32_t *>(static_cast<char *>(workspace) + p.off_bflags);
     const int phases = v.stride_h;  // the virtual pass's stride along w is 1
     uint32_t *kf = pf + size_t(phases) * v.c_in;
-    const int nflags = (phases > 1 ? phases * v.c_in : 0) + v.c_in;
-    hipLaunchKernelGGL(zero_tap_flags_kernel, dim3(std::min(nflags, 65535)), dim3(256), 0, st, w, v.kh, 1, v.c_in,
-                       v.c_out, v.stride_h, 1, v.pad_top, 0, fmt_hi(md), md.sat, phases > 1 ? pf : nullptr, kf);
+    const ZeroTapFlags zf{w, v.kh, 1, v.c_in, v.c_out, v.stride_h, 1, v.pad_top, 0, fmt_hi(md), md.sat,
+                          phases > 1 ? pf : nullptr, kf};
+    rc = bwd_data_run(md, &v, p, dy, w, dxu, lut, m_bits, workspace, st, false, zf);
+    if (rc != AMSIM_OK) return rc;
     const int total = desc->n * desc->h * desc->w * desc->c_in;
     hipLaunchKernelGGL(fold_w_kernel, dim3(grid_for(total)), dim3(256), 0, st, dxu, desc->n, desc->h, desc->w,
                        desc->c_in, desc->kw, desc->stride_w, desc->pad_left, v.w, kf, phases > 1 ? pf : nullptr,
@@ -1815,23 +1942,24 @@ int conv_bwd_weight_run(const Mode &md, const amsim_conv2d *desc, const float *x
     char *ws = static_cast<char *>(workspace);
     uint32_t *Xd = reinterpret_cast<uint32_t *>(ws + p.off_a);
     uint32_t *Dyd = reinterpret_cast<uint32_t *>(ws + p.off_b);
-    uint32_t *sa = md.native ? nullptr : stats_a(ws, p), *sb = md.native ? nullptr : stats_b(ws, p);
-    const int n_a = decode_pairs(x, s.n, s.h, s.w, s.ci, s.pt, s.pl, p.Hp, p.Wp, s.sw, Xd, fmt_first(md, mb), sa, st);
+    PrepJobs j = prep_jobs(md, lut, mb, ws, p);
+    // x as step-pair records inside its zero border, one padded image row per workgroup at a time
+    const DecPairs da{x, s.n, s.h, s.w, s.ci, s.pt, s.pl, p.Hp, p.Wp, s.sw, Xd};
+    j.n_a = int(std::min<int64_t>(int64_t(s.n) * p.Hp, kStatSlots));
     const int64_t npo = int64_t(s.n) * s.oh * s.ow;
-    const int n_b = decode_grid(npo * p.b_ld);
-    hipLaunchKernelGGL(decode_kernel, dim3(n_b), dim3(256), 0, st, dy, int64_t(0), int64_t(s.co), int64_t(1), 1,
-                       int(npo), int(npo), s.co, Dyd, int(p.b_ld), fmt_second(md, p, mb), sb,
-                       decode_vec(dy, 0, s.co, 1));
-    if (launch_status() != AMSIM_OK) return AMSIM_ERR_HIP;
-    if (!md.native && prep_rows(lut, mb, ws, p, n_a, n_b, md, st) != AMSIM_OK) return AMSIM_ERR_HIP;
+    j.b = DecRows{dy, 0, int64_t(s.co), 1, 1, int(npo), int(npo), s.co, Dyd, int(p.b_ld), decode_vec(dy, 0, s.co, 1)};
+    j.n_b = decode_grid(npo * p.b_ld);
+    const int var = tab_variant(md, p, conv_macs(s));
+    if (run_prepass(j, da, 0, var, narrow_of(md), st) != AMSIM_OK) return AMSIM_ERR_HIP;
     const int R = s.kh * s.kw * s.ci;
     float *out = p.splits > 1 ? reinterpret_cast<float *>(ws + p.off_part) : dw;
     {
         TimedLaunch tl(md.native ? AMSIM_KERNEL_CONV_BWD_WEIGHT_NATIVE : AMSIM_KERNEL_CONV_BWD_WEIGHT, st);
         TabArgs a = tab_args(bwd_weight_geom(p, s), p, ws, Xd, Dyd, out);
+        set_stats(a, j, md);
         set_format_scales(a, md);
         const dim3 grid = dim3_of(bwd_weight_grid(p, s));
-        rc = tab_launch<OP_BWD_WEIGHT>(p.tile, p.rl, tab_variant(md), a, grid, st) == hipSuccess
+        rc = tab_launch<OP_BWD_WEIGHT>(p.tile, p.rl, var, a, grid, st) == hipSuccess
                  ? AMSIM_OK
                  : AMSIM_ERR_HIP;
     }

@@ -62,6 +62,9 @@ struct TabArgs {
     const unsigned char *hl_rows;   // 2-byte tables: entries split into bf16 halves (hi/lo path)
     const int *eb;                  // [0] entry width, [1] 1 (2) when the bf16 (hi/lo) path may run,
                                     // [2] 1 when the exact path rounds each product before adding it
+    const uint32_t *stats_a, *stats_b;  // kTabApproxSelf: the decode passes' exponent statistics
+    int n_a, n_b;                       // (null: none), words of each operand, and whether the
+    int narrow;                         // operands are cast to fewer exponent bits than FP32's
     uint32_t vadd;       // exact path, rounded form: table values scaled by 2^(vadd >> 23) ...
     float su, sd;        // ... and each product by su, then added times sd (1, 1, 1 for FP32 operands)
     int R, N;            // result rows and columns
@@ -1247,7 +1250,105 @@ __device__ __forceinline__ void tab_body_hl(const TabArgs &a)
 // hint the scheduler minimises registers and serialises the LDS gathers.
 // RL: log2 of the table row length, 7 (rows padded to 128 entries) for M <= 7, else M.
 // VAR: kTabApprox (the table's products) or kTabNative (the native FP32 multiply, RL = 7 only).
-enum { kTabApprox = 0, kTabNative = 1 };
+// kTabApproxSelf: the table's products, with the path decided by the kernel itself (tab_paths)
+// instead of read from the flags -- for small calls, where one launch fewer matters more.
+enum { kTabApprox = 0, kTabNative = 1, kTabApproxSelf = 2 };
+
+// The exact path's product form: 1 when a product must be rounded on its own before it is added
+// (t = v * (pa * pb), then the sum), 0 when fma(v, pa * pb, acc) gives the same result.  They
+// differ only where v * (pa * pb) overflows to Inf -- exponent field Ea + Eb - 127 = 254 plus a
+// carry -- which an fma would fold into the sum unrounded: impossible when the largest finite
+// exponent fields of the two operands add up to at most 380.  Inf and NaN operands give the same
+// result either way, but their statistics carry no exponent range, so they take the rounded form;
+// so do formats with fewer exponent bits (`narrow`), whose products are scaled before the add,
+// and calls without statistics.
+__device__ __forceinline__ int exact_needs_rounded_products(bool have_stats, bool special, uint32_t a_hi,
+                                                            uint32_t b_hi, int narrow)
+{
+    return (narrow || !have_stats || special || a_hi + b_hi > 380u) ? 1 : 0;
+}
+
+// The call's path from the reduced decode statistics -- the smallest exponent field (lo) and the
+// largest with the Inf/NaN flag above it (hs = special << 8 | hi) of each operand's non-zero
+// operands -- and the table's entry width eb.  flags[1] and flags[2] of a call hold it.
+//   path 1, the bf16 path (1-byte entries): every product of finite non-zero operands has
+//     exponent field Ea + Eb - 127 + carry in [1, 254], and v * pb (Eb + carry) stays below 255;
+//   path 2, the hi/lo path (2-byte entries): also the low halves' products normal -- v_lo >=
+//     2^-15 times pb normal as a bf16 (Eb >= 16) and times pa normal (Ea + Eb - 127 - 15 >= 1);
+//   path 0, the exact path, whose product form is `rounded`.
+// have: the decode passes recorded statistics (not for the native multiply).
+__device__ __forceinline__ void decide_paths(int eb, uint32_t a_lo, uint32_t a_hs, uint32_t b_lo, uint32_t b_hs,
+                                             bool have, int narrow, int &path, int &rounded)
+{
+    const uint32_t a_hi = a_hs & 0xFFu, b_hi = b_hs & 0xFFu;
+    const bool special = ((a_hs | b_hs) >> 8) != 0u;
+    const bool window = have && !special && a_lo + b_lo >= 128u && a_hi + b_hi <= 380u && b_hi <= 253u;
+    const bool window_hl = window && b_lo >= 16u && a_lo + b_lo >= 143u;
+    path = narrow ? 0 : ((eb == 1 && window) ? 1 : ((eb == 2 && window_hl) ? 2 : 0));
+    rounded = exact_needs_rounded_products(have, special, a_hi, b_hi, narrow);
+}
+
+// Reduction of n statistics words (lo | hi << 8 | special << 16 per decode workgroup) into a
+// thread's lo / hs, NT threads striding, four loads in flight; a word past the end reads as that
+// of a workgroup that saw no operand.
+template <int NT>
+__device__ __forceinline__ void stats_fold(const uint32_t *__restrict__ stats, int n, uint32_t &lo, uint32_t &hs)
+{
+    for (int i0 = threadIdx.x; i0 < n; i0 += 4 * NT) {
+        uint32_t v[4];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) v[u] = i0 + u * NT < n ? stats[i0 + u * NT] : 0xFFu;
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+            lo = min(lo, v[u] & 0xFFu);
+            hs = max(hs, (v[u] >> 8) & 0x1FFu);
+        }
+    }
+}
+
+// The path decided by every workgroup of a kTabApproxSelf kernel at its start, from the decode
+// statistics (a.n_a + a.n_b words) -- so that no launch sits between the pre-pass and the table
+// kernel.  NW: waves of the workgroup; red: 4 NW + 2 words of LDS, free until the body's first
+// barrier.
+template <int NW>
+__device__ __forceinline__ void tab_paths(const TabArgs &a, int eb, uint32_t *red, int &path, int &rounded)
+{
+    uint32_t alo = 255u, ahs = 0u, blo = 255u, bhs = 0u;
+    const bool have = a.stats_a != nullptr;  // uniform
+    if (have) {
+        stats_fold<64 * NW>(a.stats_a, a.n_a, alo, ahs);
+        stats_fold<64 * NW>(a.stats_b, a.n_b, blo, bhs);
+    }
+    alo = wave_min(alo);
+    ahs = wave_max(ahs);
+    blo = wave_min(blo);
+    bhs = wave_max(bhs);
+    const int wave = int(threadIdx.x) >> 6;
+    if ((threadIdx.x & 63) == 0) {
+        red[4 * wave + 0] = alo;
+        red[4 * wave + 1] = ahs;
+        red[4 * wave + 2] = blo;
+        red[4 * wave + 3] = bhs;
+    }
+    __syncthreads();
+    if (threadIdx.x == 0) {  // the decision, handed to every wave through LDS
+        uint32_t a_lo = 255u, a_hs = 0u, b_lo = 255u, b_hs = 0u;
+        for (int w = 0; w < NW; ++w) {
+            a_lo = min(a_lo, red[4 * w + 0]);
+            a_hs = max(a_hs, red[4 * w + 1]);
+            b_lo = min(b_lo, red[4 * w + 2]);
+            b_hs = max(b_hs, red[4 * w + 3]);
+        }
+        int p, r;
+        decide_paths(eb, a_lo, a_hs, b_lo, b_hs, have, a.narrow, p, r);
+        red[4 * NW + 0] = uint32_t(p);
+        red[4 * NW + 1] = uint32_t(r);
+    }
+    __syncthreads();
+    path = __builtin_amdgcn_readfirstlane(int(red[4 * NW + 0]));
+    rounded = __builtin_amdgcn_readfirstlane(int(red[4 * NW + 1]));
+    __syncthreads();  // the body's first LDS stores may overwrite red
+}
 
 template <int OP, int TM, int TN, int WR, int NW, int RL, int VAR>
 __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(4, 4))) void tab_kernel(TabArgs args)
@@ -1259,8 +1360,13 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(4, 4)))
         return;
     }
     const int eb = __builtin_amdgcn_readfirstlane(a.eb[0]);
+    int self_path = 0, self_rounded = 0;
+    if constexpr (VAR == kTabApproxSelf) {
+        extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
+        tab_paths<NW>(a, eb, reinterpret_cast<uint32_t *>(smem), self_path, self_rounded);
+    }
     if constexpr (RL == 7 && dot_cols_ok(TN) && WR == NW) {
-        const int path = __builtin_amdgcn_readfirstlane(a.eb[1]);
+        const int path = VAR == kTabApproxSelf ? self_path : __builtin_amdgcn_readfirstlane(a.eb[1]);
         if (path == 1) {
             tab_body_dot<OP, TM, NW, TN>(a);
             return;
@@ -1272,7 +1378,7 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(4, 4)))
             }
         }
     }
-    const int rounded = __builtin_amdgcn_readfirstlane(a.eb[2]);
+    const int rounded = VAR == kTabApproxSelf ? self_rounded : __builtin_amdgcn_readfirstlane(a.eb[2]);
     if (rounded) {
         if (eb == 1)
             tab_body<OP, TM, TN, WR, 1, NW, RL, true>(a);
@@ -1371,7 +1477,7 @@ static_assert(tab_cands_listed(kTabCands, 7, 7) && tab_cands_listed(kWideCands, 
 
 // Per operation (defined in amsim_tab.hip, one instantiation per operation): raise the dynamic
 // LDS limit of every instantiated tile's kernel and check that none uses static LDS; launch the
-// kernel of tile t with rows of 2^rl entries and variant var (the native multiply: rl = 7).  Both return the first HIP error, and the launch
+// kernel of tile t with rows of 2^rl entries and variant var (kTabNative and kTabApproxSelf: rl = 7).  Both return the first HIP error, and the launch
 // hipErrorInvalidConfiguration for a tile that is not instantiated.
 template <int OP>
 hipError_t tab_attributes();

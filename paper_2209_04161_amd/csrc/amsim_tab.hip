@@ -47,8 +47,10 @@ hipError_t tab_attributes()
     hipError_t err = hipSuccess;
 #define X(TM, TN, WR, NW, RL)                                                                              \
     allow_lds(tab_kernel<OP, TM, TN, WR, NW, RL, kTabApprox>, tab_lds_bytes(TN, WR, NW, RL), err);          \
-    if constexpr (RL == 7)                                                                                  \
-        allow_lds(tab_kernel<OP, TM, TN, WR, NW, 7, kTabNative>, tab_native_lds_bytes(TN, WR, NW), err);
+    if constexpr (RL == 7) {                                                                                \
+        allow_lds(tab_kernel<OP, TM, TN, WR, NW, 7, kTabNative>, tab_native_lds_bytes(TN, WR, NW), err);    \
+        allow_lds(tab_kernel<OP, TM, TN, WR, NW, 7, kTabApproxSelf>, tab_lds_bytes(TN, WR, NW, 7), err);    \
+    }
     AMSIM_FOR_TAB_TILES(X)
 #undef X
     return err;
@@ -65,6 +67,14 @@ hipError_t tab_launch(const Tile &t, int rl, int var, const TabArgs &a, dim3 gri
             if constexpr (RL == 7) {
                 hipLaunchKernelGGL((tab_kernel<OP, TM, TN, WR, NW, 7, kTabNative>), grid, dim3(64 * NW),
                                    tab_native_lds_bytes(TN, WR, NW), st, a);
+                launched = true;
+            }
+            return;
+        }
+        if (var == kTabApproxSelf) {  // rows of 128 entries only
+            if constexpr (RL == 7) {
+                hipLaunchKernelGGL((tab_kernel<OP, TM, TN, WR, NW, 7, kTabApproxSelf>), grid, dim3(64 * NW),
+                                   tab_lds_bytes(TN, WR, NW, 7), st, a);
                 launched = true;
             }
             return;

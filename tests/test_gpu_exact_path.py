@@ -170,6 +170,46 @@ def test_gemm_window_thresholds_exact_trunc(B, ti):
     assert_within_tolerance(C[idx], ref, S, "hi/lo window %s" % name)
 
 
+# Calls of fewer than 2^27 products decide their path inside the table kernel; larger calls take it
+# from a flags launch after the pre-pass.  Both decisions, on every threshold and special case,
+# at both sizes: A is rows x 64, B 64 x cols.
+SIZES = {"small": (300, 96), "large": (4096, 1024)}   # 1.8M and 268M products
+
+
+def _sampled_gemm_check(B, A, Bm, model, what, seed):
+    C = host(B.approx_gemm(cuda(A), cuda(Bm), dev_lut(B, model, 7), 7)).reshape(-1)
+    idx = np.sort(np.random.default_rng(seed).choice(C.size, min(C.size, 20000), replace=False))
+    ref, S = oracle.gemm(MODELS[model], 7, A, Bm, idx=idx)
+    assert_within_tolerance(C[idx], ref, S, what)
+
+
+@pytest.mark.parametrize("size", sorted(SIZES))
+@pytest.mark.parametrize("case", [("mitchell",) + t for t in THRESHOLDS] + [("exact_trunc",) + t for t in HL_THRESHOLDS],
+                         ids=lambda c: "%s %s" % (c[0], c[1]))
+def test_window_thresholds_both_path_decisions(B, case, size):
+    model, name, ra, rb = case
+    rows, cols = SIZES[size]
+    rng = np.random.default_rng(1400 + len(name) + rows)
+    A = _window_operands(rng, (rows, 64), *ra)
+    Bm = _window_operands(rng, (64, cols), *rb)
+    _sampled_gemm_check(B, A, Bm, model, "%s window %s, %s call" % (model, name, size), 1500 + rows)
+
+
+@pytest.mark.parametrize("size", sorted(SIZES))
+@pytest.mark.parametrize("model", sorted(MODELS))
+def test_special_operands_both_path_decisions(B, model, size):
+    """NaN and +-Inf operands (no exponent window: the exact path, rounded products)."""
+    rows, cols = SIZES[size]
+    A = W.normal((rows, 64), 1.0, 1600 + rows)
+    Bm = W.normal((64, cols), 1.0, 1601 + rows)
+    A[3, 10] = np.nan
+    Bm[5, 7] = np.inf
+    Bm[40, 7] = -np.inf
+    Bm[20, 9] = np.inf
+    A[rows - 1, 20] = -np.inf
+    _sampled_gemm_check(B, A, Bm, model, "%s NaN/Inf, %s call" % (model, size), 1602 + rows)
+
+
 def _conv_case(seed, special):
     p = W.conv_desc(2, 9, 10, 12, 20, 3, 3, 1, 0)
     oh, ow = W.conv_out_hw(p)
@@ -204,6 +244,39 @@ def test_conv_passes_exact_path_multi_step(B, special):
     dw = host(B.approx_conv2d_bwd_weight(p, cuda(x), cuda(dy), lut, 7))
     ref, S = oracle.conv2d_bwd_weight(oracle.MITCHELL, 7, p, x, dy)
     assert_within_tolerance(dw, ref, S, "bwd_weight %s" % special)
+
+
+@pytest.mark.parametrize("special", ["huge", "naninf"])
+def test_conv_passes_exact_path_large_calls(B, special):
+    """The exact path on calls of more than 2^27 products (path flags from their own launch), each
+    pass on seeded sampled outputs: stride 2 and padding 1, 16 x 33 x 31 x 64 -> 64 channels."""
+    p = W.conv_desc(16, 33, 31, 64, 64, 3, 3, 2, 1)
+    oh, ow = W.conv_out_hw(p)
+    x = W.normal((16, 33, 31, 64), 1.0, 1700)
+    w = W.normal((3, 3, 64, 64), 1.0, 1701)
+    dy = W.normal((16, oh, ow, 64), 1.0, 1702)
+    assert W.conv_macs(p) > 2 ** 27
+    if special == "huge":
+        w[1, 1, 4, 9] = with_exponent(w[1, 1, 4, 9], 254)
+        dy[0, 3, 3, 2] = with_exponent(dy[0, 3, 3, 2], 254)
+        x[2, 7, 8, 5] = with_exponent(x[2, 7, 8, 5], 253)
+    else:
+        x[1, 5, 5, 2] = np.nan
+        w[0, 2, 7, 11] = np.inf
+        w[2, 0, 7, 11] = -np.inf
+        dy[0, 1, 2, 4] = np.inf
+        dy[1, 4, 4, 6] = -np.inf
+    lut = dev_lut(B, "mitchell", 7)
+    rng = np.random.default_rng(1703)
+    for name, got, fn, a0, a1 in (
+            ("fwd", B.approx_conv2d_fwd(p, cuda(x), cuda(w), lut, 7), oracle.conv2d_fwd, x, w),
+            ("bwd_data", B.approx_conv2d_bwd_data(p, cuda(dy), cuda(w), lut, 7), oracle.conv2d_bwd_data, dy, w),
+            ("bwd_weight", B.approx_conv2d_bwd_weight(p, cuda(x), cuda(dy), lut, 7), oracle.conv2d_bwd_weight,
+             x, dy)):
+        got = host(got).reshape(-1)
+        idx = np.sort(rng.choice(got.size, min(got.size, 3000), replace=False))
+        ref, S = fn(oracle.MITCHELL, 7, p, a0, a1, idx=idx)
+        assert_within_tolerance(got[idx], ref, S, "%s %s, large call" % (name, special))
 
 
 def test_conv_overflowing_product_next_to_opposite_sum(B):
