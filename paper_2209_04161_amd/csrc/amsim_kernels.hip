@@ -1463,15 +1463,13 @@ PrepJobs prep_jobs(const Mode &md, const uint32_t *lut, int mb, char *ws, const 
     return j;
 }
 
-// The table kernel variant of a call of `macs` products: the native multiply's; for rows of 128
-// entries and fewer than kSelfMacs products the variant that decides its path itself (one launch
-// fewer, for calls whose launches take about as long as their work); else the one that reads the
-// path flags.
-constexpr int64_t kSelfMacs = int64_t(1) << 27;
-inline int tab_variant(const Mode &md, const Plan &p, int64_t macs)
+// The table kernel variant of a call of `macs` products: the native multiply's; for a small call
+// (small_call) the variant that decides its path itself (one launch fewer, for calls whose
+// launches take about as long as their work); else the one that reads the path flags.
+inline int tab_variant(const Mode &md, const Plan &p, double macs)
 {
     if (md.native) return kTabNative;
-    return p.rl == 7 && macs < kSelfMacs ? kTabApproxSelf : kTabApprox;
+    return small_call(macs, p.rl) ? kTabApproxSelf : kTabApprox;
 }
 
 // Launches the pre-pass (first-operand decode a, lds its dynamic LDS bytes), then what the table
@@ -1521,7 +1519,7 @@ void set_stats(TabArgs &a, const PrepJobs &j, const Mode &md)
 }
 
 // Products of a convolution pass (the same for the three passes).
-inline int64_t conv_macs(const ConvShape &s) { return int64_t(s.n) * s.oh * s.ow * s.co * s.kh * s.kw * s.ci; }
+inline double conv_macs(const ConvShape &s) { return double(s.n) * s.oh * s.ow * s.co * s.kh * s.kw * s.ci; }
 
 inline dim3 dim3_of(const TabGrid &g) { return dim3(g.x, g.y, g.z); }
 
@@ -1754,7 +1752,7 @@ int gemm_run(const Mode &md, int trans_a, int trans_b, int64_t m, int64_t n, int
     j.n_a = gx * gy;  // <= kStatSlots
     j.b = DecRows{B, 0, b_sr, b_sc, 1, int(k), int(k), int(n), Bd, int(p.b_ld), decode_vec(B, 0, b_sr, b_sc)};
     j.n_b = decode_grid(k * p.b_ld);
-    const int var = tab_variant(md, p, m * n * k);
+    const int var = tab_variant(md, p, double(m) * double(n) * double(k));
     if (run_prepass(j, da, 0, var, narrow_of(md), st) != AMSIM_OK) return AMSIM_ERR_HIP;
     int rc;
     {

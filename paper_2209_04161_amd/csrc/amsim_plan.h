@@ -29,6 +29,16 @@ inline int64_t ceil_div(int64_t x, int64_t m) { return (x + m - 1) / m; }
 // log2 of the table row length: rows are padded to 128 entries for M <= 7.
 inline int row_log(int m_bits) { return m_bits > 7 ? m_bits : 7; }
 
+// Calls of fewer products than kSelfMacs on rows of 128 entries are "small": they run the
+// table-kernel variant that decides its path itself (one launch fewer), and they are planned as
+// launches whose slabs wait on their own fetches -- too few workgroups to hide the staging's
+// dependent loads, ~2.9 us a slab measured on MI355X (LeNet-5 layers, 3 to 60 workgroups)
+// against ~0.7 us when rounds of workgroups overlap -- so they split their reductions down to
+// single chunks.
+// (products as a double: m * n * k of the largest shapes overflows 64 bits)
+constexpr double kSelfMacs = double(int64_t(1) << 27);
+inline bool small_call(double macs, int rl) { return rl == 7 && macs < kSelfMacs; }
+
 // Cost per product used to choose among the candidate tiles (kTabCands and the wide-row lists):
 // the inner loop (~1.2 VALU ops on the bf16 pair path, which 8-column tiles with all waves on
 // rows take for 1-byte tables; 3 on the exact path), per-step overhead (~2.5 per row, ~4 per
@@ -45,10 +55,12 @@ inline int row_log(int m_bits) { return m_bits > 7 ? m_bits : 7; }
 // wave tile over 147 rows) leave the SIMDs idle, which scales their issue rate down (measured on
 // MI355X: the ResNet-50 stem's backward-weight 6%, the LeNet-5 stack 11% and an M = 11 1024^3
 // GEMM 17% faster than without the scaling).  Only a launch under one round is split (at least
-// min_chunks chunks per split).
-inline Tile choose_tab_tile(int64_t rows, int64_t cols, int64_t q, int64_t min_chunks, bool allow_split, int rl,
-                     int max_tm, int64_t phases)
+// 4 chunks per split, 1 for a small call).
+inline Tile choose_tab_tile(int64_t rows, int64_t cols, int64_t q, bool small, bool allow_split, int rl, int max_tm,
+                            int64_t phases)
 {
+    const int64_t min_chunks = small ? 1 : 4;
+    const double fetch_ns = small ? 2900.0 : 700.0;
     constexpr int kCUs = 256, kWavesPerCU = 16;
     constexpr size_t kLdsPerCU = 160 * 1024;
     Tile best{};
@@ -88,10 +100,10 @@ inline Tile choose_tab_tile(int64_t rows, int64_t cols, int64_t q, int64_t min_c
                                       ? std::max<int64_t>(1, std::min<int64_t>(q / std::max<int64_t>(1, min_chunks), 4096))
                                       : 1;
         // steps per slab (the bf16 path's, else a 2-byte table's) and a slab's time for one wave:
-        // the staging fetch (a dependent pair of loads, ~0.7 us) plus its products at ~1.15 (bf16
+        // the staging fetch (a dependent pair of loads, fetch_ns) plus its products at ~1.15 (bf16
         // path) or ~3.7 (exact path) VALU instructions each, 4 clocks per instruction at 2.4 GHz
         const double slab_steps = pair ? 2.0 * c.nw : double(tab_slab_steps(int(ctile), rl, 2));
-        const double slab_ns = 700.0 + double(c.tm * c.tn) * slab_steps * (pair ? 1.15 : 3.7) * 4.0 / 2.4;
+        const double slab_ns = fetch_ns + double(c.tm * c.tn) * slab_steps * (pair ? 1.15 : 3.7) * 4.0 / 2.4;
         // In ns, per round of workgroups: a workgroup's products at its share of the chip
         // (~20 T products/s, 28 cost units per ps, over all slots), or the slabs it walks through
         // one after another, whichever is longer; splits add their partial sums' traffic, a
@@ -196,7 +208,8 @@ inline Plan plan_gemm(int64_t m, int64_t n, int64_t k, int m_bits)
 {
     Plan p{};
     p.rl = row_log(m_bits);
-    p.tile = choose_tab_tile(m, n, ceil_div(k, 8), 4, true, p.rl, 8, 1);
+    p.tile = choose_tab_tile(m, n, ceil_div(k, 8), small_call(double(m) * double(n) * double(k), p.rl), true, p.rl, 8,
+                             1);
     p.a_ld = round_up(m, int64_t(64) * p.tile.wr * p.tile.tm);
     p.chunk = 8;
     p.b_ld = round_up(n, tab_cols(p.tile));
@@ -379,6 +392,7 @@ inline Plan plan_conv(const amsim_conv2d *d, int pass, int m_bits)
     p.chunk = 8;
     size_t o = table_area(p, 0);
     const int64_t npix_in = int64_t(s.n) * s.h * s.w, npix_out = int64_t(s.n) * s.oh * s.ow;
+    const bool small = small_call(double(npix_out) * s.co * s.kh * s.kw * s.ci, p.rl);
     p.Hp = d->h + d->pad_top + d->pad_bottom;
     p.Wp = d->w + d->pad_left + d->pad_right;
     if (pass == AMSIM_CONV_FWD) {
@@ -386,7 +400,7 @@ inline Plan plan_conv(const amsim_conv2d *d, int pass, int m_bits)
         const ConvShape v = p.unfold_w ? unfolded_shape(s) : s;
         if (p.unfold_w) p.Wp = s.ow;  // the unfolded x has no w border
         const int64_t q = int64_t(v.kh) * v.kw * ceil_div(v.ci, 8);
-        p.tile = choose_tab_tile(npix_out, s.co, q, 4, true, p.rl, 8, 1);
+        p.tile = choose_tab_tile(npix_out, s.co, q, small, true, p.rl, 8, 1);
         p.csplit = fwd_channel_chunks(s, p.unfold_w);
         plan_tab_split(p, int64_t(v.kh) * v.kw * p.csplit, v.ci / p.csplit);
         p.rec_c = p.unfold_w ? unfolded_channels(s) : s.ci;  // channels per record row block
@@ -400,7 +414,7 @@ inline Plan plan_conv(const amsim_conv2d *d, int pass, int m_bits)
     } else if (pass == AMSIM_CONV_BWD_DATA) {
         const int64_t rows = bwd_data_rows(s);
         const int64_t q = ceil_div(s.kh, s.sh) * ceil_div(s.kw, s.sw) * ceil_div(s.co, 8);  // largest phase
-        p.tile = choose_tab_tile(rows, s.ci, q, 4, true, p.rl, 4, int64_t(s.sh) * s.sw);  // 8-row tiles spill here
+        p.tile = choose_tab_tile(rows, s.ci, q, small, true, p.rl, 4, int64_t(s.sh) * s.sw);  // 8-row tiles spill here
         int top, bottom, left, right;
         bwd_data_dy_pads(s, top, bottom, left, right);
         p.pad_oh = top;
@@ -422,7 +436,7 @@ inline Plan plan_conv(const amsim_conv2d *d, int pass, int m_bits)
     } else {
         const int64_t R = int64_t(s.kh) * s.kw * s.ci;
         const int64_t q = int64_t(s.n) * s.oh * ceil_div(s.ow, 8);
-        p.tile = choose_tab_tile(R, s.co, q, 4, true, p.rl, 8, 1);
+        p.tile = choose_tab_tile(R, s.co, q, small, true, p.rl, 8, 1);
         plan_tab_split(p, int64_t(s.n) * s.oh, s.ow);
         p.b_ld = round_up(s.co, tab_cols(p.tile));
         p.a_elems = int64_t(s.n) * p.Hp * p.Wp * s.ci * 3;
