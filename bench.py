@@ -182,6 +182,9 @@ def main():
     roofline = {"bound": "alu", "achieved": round(achieved, 3), "peak": FP32_VECTOR_PEAK_TFLOPS,
                 "unit": "TFLOP/s", "frac": round(achieved / FP32_VECTOR_PEAK_TFLOPS, 4),
                 "traffic": read_traffic(),
+                "traffic_source": "not measured in this run: HBM bytes per launch from the committed rocprofv3 "
+                                  "FETCH_SIZE/WRITE_SIZE summary profiles/gemm_4096_m7_traffic.txt, used only while "
+                                  "its kernel_source_sha256 matches the kernel sources (else null)",
                 "kernel": "tab_kernel<OP_GEMM, 4, 8, 8, 8, 7, kTabApprox> (approx_gemm 4096^3, Mitchell M=7, bf16 pair path)"}
 
     out = {
