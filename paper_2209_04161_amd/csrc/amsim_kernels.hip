@@ -1659,7 +1659,7 @@ inline bool gemv_lds(const Mode &md, int m_bits) { return !md.native && md.e_bit
 // reduction when the vector kernel splits k.
 int vec_run(const Mode &md, const VecPlan &vp, int trans_a, int trans_b, int64_t m, int64_t n, int64_t k,
             const float *A, int64_t lda, const float *B, int64_t ldb, float *C, int64_t ldc, const uint32_t *lut,
-            int m_bits, void *workspace, size_t workspace_bytes, hipStream_t st)
+            int m_bits, void *workspace, size_t workspace_bytes, hipStream_t st, int timer_kind)
 {
     if (vp.total > 0 && (!workspace || workspace_bytes < vp.total)) return AMSIM_ERR_WORKSPACE;
     if (ensure_attributes() != AMSIM_OK) return AMSIM_ERR_HIP;
@@ -1684,7 +1684,7 @@ int vec_run(const Mode &md, const VecPlan &vp, int trans_a, int trans_b, int64_t
     const bool narrow = !md.native && md.e_bits < 8;
     float *part = vp.kind == VEC_GEMV && vp.splits > 1 ? static_cast<float *>(workspace) : nullptr;
     {
-        TimedLaunch tl(md.native ? AMSIM_KERNEL_GEMM_NATIVE : AMSIM_KERNEL_GEMM, st);
+        TimedLaunch tl(timer_kind, st);
         if (vp.kind == VEC_OUTER) {  // a_i = op(A)(i, 0), b_j = op(B)(0, j)
             const dim3 g(unsigned(grid_for(m * n)));
             if (md.native)
@@ -1714,10 +1714,12 @@ int vec_run(const Mode &md, const VecPlan &vp, int trans_a, int trans_b, int64_t
     return AMSIM_OK;
 }
 
+// timer_kind: the kernel timer's kind for the main kernel (-1: the GEMM's).
 int gemm_run(const Mode &md, int trans_a, int trans_b, int64_t m, int64_t n, int64_t k, const float *A, int64_t lda,
              const float *B, int64_t ldb, float *C, int64_t ldc, const uint32_t *lut, int m_bits, void *workspace,
-             size_t workspace_bytes, hipStream_t st)
+             size_t workspace_bytes, hipStream_t st, int timer_kind = -1)
 {
+    if (timer_kind < 0) timer_kind = md.native ? AMSIM_KERNEL_GEMM_NATIVE : AMSIM_KERNEL_GEMM;
     if (!md.native && !valid_m(m_bits)) return AMSIM_ERR_UNSUPPORTED;
     if (m < 0 || n < 0 || k < 0) return AMSIM_ERR_INVALID_ARG;
     if (m == 0 || n == 0) return AMSIM_OK;
@@ -1733,7 +1735,7 @@ int gemm_run(const Mode &md, int trans_a, int trans_b, int64_t m, int64_t n, int
     const VecPlan vp = plan_vec(m, n, k, trans_a, trans_b, gemv_lds(md, m_bits));
     if (vp.kind != VEC_NONE)
         return vec_run(md, vp, trans_a, trans_b, m, n, k, A, lda, B, ldb, C, ldc, lut, m_bits, workspace,
-                       workspace_bytes, st);
+                       workspace_bytes, st, timer_kind);
     const int mb = plan_m(md, m_bits);
     const Plan p = plan_gemm(m, n, k, mb);
     if (!gemm_fits(p, m, n, k)) return AMSIM_ERR_UNSUPPORTED;
@@ -1760,7 +1762,7 @@ int gemm_run(const Mode &md, int trans_a, int trans_b, int64_t m, int64_t n, int
         set_stats(a, j, md);
         set_format_scales(a, md);
         const dim3 grid = dim3_of(gemm_grid(p));
-        TimedLaunch tl(md.native ? AMSIM_KERNEL_GEMM_NATIVE : AMSIM_KERNEL_GEMM, st);
+        TimedLaunch tl(timer_kind, st);
         rc = tab_launch<OP_GEMM>(p.tile, p.rl, var, a, grid, st) == hipSuccess
                  ? AMSIM_OK
                  : AMSIM_ERR_HIP;
@@ -1771,6 +1773,32 @@ int gemm_run(const Mode &md, int trans_a, int trans_b, int64_t m, int64_t n, int
         if (launch_status() != AMSIM_OK) return AMSIM_ERR_HIP;
     }
     return AMSIM_OK;
+}
+
+// A convolution pass that runs as its GEMM (conv_runs_as_gemm): validated as a convolution, run as
+// the GEMM, timed as the pass.  in0 / in1: the pass's first and second operands, as for the
+// convolution.
+int conv_gemm_run(const Mode &md, const amsim_conv2d *desc, int pass, const float *in0, const float *in1, float *out,
+                  const uint32_t *lut, int m_bits, void *workspace, size_t workspace_bytes, hipStream_t st)
+{
+    if (!md.native && !valid_m(m_bits)) return AMSIM_ERR_UNSUPPORTED;
+    const int rc = check_conv(desc, pass);
+    if (rc != AMSIM_OK) return rc;
+    if (!in0 || !in1 || !out || (!lut && !md.native)) return AMSIM_ERR_INVALID_ARG;
+    static const int kinds[3][2] = {{AMSIM_KERNEL_CONV_FWD, AMSIM_KERNEL_CONV_FWD_NATIVE},
+                                    {AMSIM_KERNEL_CONV_BWD_DATA, AMSIM_KERNEL_CONV_BWD_DATA_NATIVE},
+                                    {AMSIM_KERNEL_CONV_BWD_WEIGHT, AMSIM_KERNEL_CONV_BWD_WEIGHT_NATIVE}};
+    const ConvGemm g = conv_gemm(desc, pass);
+    // backward data: the second operand w[ci][co] read transposed
+    return gemm_run(md, g.trans_a, g.trans_b, g.m, g.n, g.k, in0, g.lda, in1, g.ldb, out, g.ldc, lut, m_bits, workspace,
+                    workspace_bytes, st, kinds[pass][md.native ? 1 : 0]);
+}
+
+// Whether a call's pass runs as its GEMM: a valid pass that conv_runs_as_gemm accepts (the same
+// decision as the workspace query's; the native multiply's m_bits, which it ignores, counts as 7).
+inline bool pass_as_gemm(const amsim_conv2d *desc, int pass, int m_bits)
+{
+    return desc && check_conv(desc, pass) == AMSIM_OK && conv_runs_as_gemm(desc, pass, valid_m(m_bits) ? m_bits : 7);
 }
 
 int conv_common(const Mode &md, const amsim_conv2d *desc, int pass, const void *in0, const void *in1, void *out,
@@ -1806,6 +1834,8 @@ DecNhcw nhcw_job(const float *src, int n, int h, int w, int c, int top, int left
 int conv_fwd_run(const Mode &md, const amsim_conv2d *desc, const float *x, const float *w, float *y,
                  const uint32_t *lut, int m_bits, void *workspace, size_t workspace_bytes, hipStream_t st)
 {
+    if (pass_as_gemm(desc, AMSIM_CONV_FWD, m_bits))
+        return conv_gemm_run(md, desc, AMSIM_CONV_FWD, x, w, y, lut, m_bits, workspace, workspace_bytes, st);
     Plan p;
     int rc = conv_common(md, desc, AMSIM_CONV_FWD, x, w, y, lut, m_bits, workspace, workspace_bytes, &p);
     if (rc != AMSIM_OK) return rc;
@@ -1899,6 +1929,8 @@ int bwd_data_run(const Mode &md, const amsim_conv2d *desc, const Plan &p, const 
 int conv_bwd_data_run(const Mode &md, const amsim_conv2d *desc, const float *dy, const float *w, float *dx,
                       const uint32_t *lut, int m_bits, void *workspace, size_t workspace_bytes, hipStream_t st)
 {
+    if (pass_as_gemm(desc, AMSIM_CONV_BWD_DATA, m_bits))
+        return conv_gemm_run(md, desc, AMSIM_CONV_BWD_DATA, dy, w, dx, lut, m_bits, workspace, workspace_bytes, st);
     Plan p;
     int rc = conv_common(md, desc, AMSIM_CONV_BWD_DATA, dy, w, dx, lut, m_bits, workspace, workspace_bytes, &p);
     if (rc != AMSIM_OK) return rc;
@@ -1932,6 +1964,8 @@ int conv_bwd_data_run(const Mode &md, const amsim_conv2d *desc, const float *dy,
 int conv_bwd_weight_run(const Mode &md, const amsim_conv2d *desc, const float *x, const float *dy, float *dw,
                         const uint32_t *lut, int m_bits, void *workspace, size_t workspace_bytes, hipStream_t st)
 {
+    if (pass_as_gemm(desc, AMSIM_CONV_BWD_WEIGHT, m_bits))
+        return conv_gemm_run(md, desc, AMSIM_CONV_BWD_WEIGHT, x, dy, dw, lut, m_bits, workspace, workspace_bytes, st);
     Plan p;
     int rc = conv_common(md, desc, AMSIM_CONV_BWD_WEIGHT, x, dy, dw, lut, m_bits, workspace, workspace_bytes, &p);
     if (rc != AMSIM_OK) return rc;
@@ -2030,15 +2064,7 @@ int amsim_gemm_workspace_size(int trans_a, int trans_b, int64_t m, int64_t n, in
     if (!bytes) return AMSIM_ERR_INVALID_ARG;
     if (!valid_m(m_bits)) return AMSIM_ERR_UNSUPPORTED;
     if (m < 0 || n < 0 || k < 0) return AMSIM_ERR_INVALID_ARG;
-    if (m == 0 || n == 0 || k == 0) {
-        *bytes = 0;
-        return AMSIM_OK;
-    }
-    // enough for every option of the call (the native multiply plans its own layout)
-    // (the vector kernels: whichever workgroup size the call's options choose)
-    const VecPlan v0 = plan_vec(m, n, k, trans_a, trans_b, false), v1 = plan_vec(m, n, k, trans_a, trans_b, true);
-    *bytes = v0.kind != VEC_NONE ? std::max(v0.total, v1.total)
-                                 : std::max(plan_gemm(m, n, k, m_bits).total, plan_gemm(m, n, k, 7).total);
+    *bytes = gemm_workspace_bytes(trans_a, trans_b, m, n, k, m_bits);
     return AMSIM_OK;
 }
 
@@ -2068,6 +2094,11 @@ int amsim_conv2d_workspace_size(const amsim_conv2d *desc, int pass, int m_bits, 
     if (pass < AMSIM_CONV_FWD || pass > AMSIM_CONV_BWD_WEIGHT) return AMSIM_ERR_INVALID_ARG;
     const int rc = check_conv(desc, pass);
     if (rc != AMSIM_OK) return rc;
+    if (conv_runs_as_gemm(desc, pass, m_bits)) {
+        const ConvGemm g = conv_gemm(desc, pass);
+        *bytes = gemm_workspace_bytes(g.trans_a, g.trans_b, g.m, g.n, g.k, m_bits);
+        return AMSIM_OK;
+    }
     *bytes = std::max(plan_conv(desc, pass, m_bits).total, plan_conv(desc, pass, 7).total);
     return AMSIM_OK;
 }

@@ -462,6 +462,31 @@ inline bool gemm_fits(const Plan &p, int64_t m, int64_t n, int64_t k)
            p.b_ld / tab_cols(p.tile) <= 65535;
 }
 
+// A 1 x 1 convolution with stride 1 and no padding: its im2col matrix is the input itself
+// (Alg. 3), and there are no border or dilation zeros, so each pass is a plain GEMM over the
+// pixels with the pass's first operand first -- forward y[pix][co] = x[pix][ci] . w[ci][co],
+// backward data dx[pix][ci] = dy[pix][co] . w[ci][co]^T, backward weight
+// dw[ci][co] = x[pix][ci]^T . dy[pix][co] -- and runs as one (the GEMM's planning, workspace
+// and kernels).
+inline bool conv_is_gemm(const amsim_conv2d *d)
+{
+    return d->kh == 1 && d->kw == 1 && d->stride_h == 1 && d->stride_w == 1 && d->pad_top == 0 &&
+           d->pad_bottom == 0 && d->pad_left == 0 && d->pad_right == 0;
+}
+
+struct ConvGemm {
+    int trans_a, trans_b;
+    int64_t m, n, k, lda, ldb, ldc;
+};
+
+inline ConvGemm conv_gemm(const amsim_conv2d *d, int pass)
+{
+    const int64_t pix = int64_t(d->n) * d->h * d->w, ci = d->c_in, co = d->c_out;
+    if (pass == AMSIM_CONV_FWD) return ConvGemm{0, 0, pix, co, ci, ci, co, co};
+    if (pass == AMSIM_CONV_BWD_DATA) return ConvGemm{0, 1, pix, ci, co, co, co, ci};
+    return ConvGemm{1, 0, ci, co, pix, ci, co, co};
+}
+
 // The vector GEMMs: m == 1 or n == 1 (one operand a vector: gemv_cols_kernel when the matrix's
 // outputs are contiguous, gemv_rows_kernel when its steps are) and k == 1 (an outer product,
 // outer_kernel).  k is split so that a launch holds about 2048 waves (8 per CU), each split at
@@ -518,6 +543,27 @@ inline VecPlan plan_vec(int64_t m, int64_t n, int64_t k, int trans_a, int trans_
     v.splits = int(ceil_div(k, v.kchunk));
     v.total = v.splits > 1 ? align_up(size_t(v.splits) * size_t(v.nout) * 4) : 0;
     return v;
+}
+
+// Workspace bytes of a GEMM call, enough for every option of it: the table's M or the native
+// multiply's plan (M = 7), and the vector kernels with either workgroup size.
+inline size_t gemm_workspace_bytes(int trans_a, int trans_b, int64_t m, int64_t n, int64_t k, int m_bits)
+{
+    if (m == 0 || n == 0 || k == 0) return 0;
+    const VecPlan v0 = plan_vec(m, n, k, trans_a, trans_b, false), v1 = plan_vec(m, n, k, trans_a, trans_b, true);
+    return v0.kind != VEC_NONE ? std::max(v0.total, v1.total)
+                               : std::max(plan_gemm(m, n, k, m_bits).total, plan_gemm(m, n, k, 7).total);
+}
+
+// Whether a valid convolution pass runs as its GEMM (conv_is_gemm): when the GEMM's plans for the
+// call's M and for the native multiply (M = 7) both fit the GEMM's limits; larger 1 x 1 passes keep
+// the convolution path, whose limits are wider.
+inline bool conv_runs_as_gemm(const amsim_conv2d *d, int pass, int m_bits)
+{
+    if (!conv_is_gemm(d)) return false;
+    const ConvGemm g = conv_gemm(d, pass);
+    if (plan_vec(g.m, g.n, g.k, g.trans_a, g.trans_b, false).kind != VEC_NONE) return true;
+    return gemm_fits(plan_gemm(g.m, g.n, g.k, m_bits), g.m, g.n, g.k) && gemm_fits(plan_gemm(g.m, g.n, g.k, 7), g.m, g.n, g.k);
 }
 
 // ------------------------------------------------------------------ kernel geometry ------

@@ -228,6 +228,21 @@ void check_conv_pass(Rng &rng, const amsim_conv2d &d, int pass, int mb)
                   d.h, d.w, d.c_in, d.c_out, d.kh, d.kw, d.stride_h, d.stride_w, d.pad_top, d.pad_bottom, d.pad_left,
                   d.pad_right);
     if (check_conv(&d, pass) != AMSIM_OK) return;
+    if (conv_runs_as_gemm(&d, pass, mb)) {  // a 1 x 1, stride-1, unpadded pass runs as its GEMM
+        const ConvGemm g = conv_gemm(&d, pass);
+        char conv_case[sizeof g_case];
+        std::snprintf(conv_case, sizeof conv_case, "%s", g_case);
+        expect(g.m * g.n == (pass == AMSIM_CONV_BWD_WEIGHT ? int64_t(d.c_in) * d.c_out
+                                                             : int64_t(d.n) * d.h * d.w * (pass ? d.c_in : d.c_out)),
+               "the GEMM covers the pass's result", g.m * g.n, 0);
+        const bool vec = plan_vec(g.m, g.n, g.k, g.trans_a, g.trans_b, false).kind != VEC_NONE;
+        if (vec)
+            check_vec(g.m, g.n, g.k, g.trans_a, g.trans_b, mb <= 7);
+        else
+            check_gemm(rng, g.m, g.n, g.k, mb);
+        std::snprintf(g_case, sizeof g_case, "%s", conv_case);
+        return;
+    }
     const Plan p = plan_conv(&d, pass, mb);
     check_table_area(p);
     const ConvShape s0 = shape_of(&d);
@@ -298,6 +313,10 @@ amsim_conv2d random_desc(Rng &rng)
     d.pad_bottom = int(rng.uniform(0, d.kh));
     d.pad_left = int(rng.uniform(0, d.kw));
     d.pad_right = int(rng.uniform(0, d.kw));
+    if (rng.uniform(0, 7) == 0) {  // one in eight pointwise: 1 x 1, stride 1, no padding (the GEMM route)
+        d.kh = d.kw = d.stride_h = d.stride_w = 1;
+        d.pad_top = d.pad_bottom = d.pad_left = d.pad_right = 0;
+    }
     return d;
 }
 

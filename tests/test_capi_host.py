@@ -130,8 +130,10 @@ def test_workspace_size_queries(L):
     with pytest.raises(binding.AmsimError):
         binding.amsim_conv2d_workspace_size(dict(d, kh=11), 0, 7)   # kernel larger than padded image
     # the width limit of the channel-inside-row decode (w and OW below 4096)
+    # (this 1 x 1 pass runs as its GEMM, a one-step outer product that needs no workspace)
     wide = dict(d, n=1, h=1, w=4095, c_in=1, c_out=1, kh=1, kw=1, pad_top=0, pad_bottom=0, pad_left=0, pad_right=0)
-    assert binding.amsim_conv2d_workspace_size(wide, 0, 7) > 0
+    assert binding.amsim_conv2d_workspace_size(wide, 0, 7) == 0
+    assert binding.amsim_conv2d_workspace_size(dict(wide, stride_w=2), 0, 7) > 0  # the convolution path
     with pytest.raises(binding.AmsimError):
         binding.amsim_conv2d_workspace_size(dict(wide, w=4096), 0, 7)
     # single-channel x: its 12-byte step-pair records (one per pixel) must stay below 2^31 bytes,
