@@ -162,11 +162,15 @@ typedef struct amsim_conv2d {
 #define AMSIM_CONV_BWD_DATA 1
 #define AMSIM_CONV_BWD_WEIGHT 2
 
-/* Device workspace bytes a pass needs for this shape and M (0 allowed for NULL workspace). */
+/* Device workspace bytes a pass needs for this shape and M (0 allowed for NULL workspace).  A 1 x 1
+ * pass with stride 1 and no padding runs as its GEMM over the pixels (its im2col matrix is the
+ * input itself) and needs that GEMM's workspace. */
 int amsim_conv2d_workspace_size(const amsim_conv2d *desc, int pass, int m_bits, size_t *bytes);
 
 /* Forward propagation (Algorithm 3): y[n,oh,ow,co] = sum_{kh,kw,ci}
- * amul(x[n, oh*sh+kh-pt, ow*sw+kw-pl, ci], w[kh,kw,ci,co]); padded taps contribute nothing.
+ * amul(x[n, oh*sh+kh-pt, ow*sw+kw-pl, ci], w[kh,kw,ci,co]), where x outside the image is the
+ * zero border, +0, which is multiplied like any operand (a signed zero, or NaN against an Inf or
+ * NaN weight, as Algorithm 3's column matrix holds it).
  * x: device [n][h][w][c_in], w: device HWIO, y: device [n][OH][OW][c_out] (overwritten). */
 int approx_conv2d_fwd(const amsim_conv2d *desc, const float *x, const float *w, float *y, const uint32_t *lut,
                       int m_bits, void *workspace, size_t workspace_bytes, void *stream);
@@ -179,10 +183,10 @@ int approx_conv2d_fwd(const amsim_conv2d *desc, const float *x, const float *w, 
 int approx_conv2d_bwd_data(const amsim_conv2d *desc, const float *dy, const float *w, float *dx,
                            const uint32_t *lut, int m_bits, void *workspace, size_t workspace_bytes, void *stream);
 
-/* Weights gradient (Algorithm 4, first half): dw[kh,kw,ci,co] = sum over (n,oh,ow) whose tap
- * lies inside the image of amul(x[n, oh*sh+kh-pt, ow*sw+kw-pl, ci], dy[n,oh,ow,co]) -- the
- * stride dilation of the error is implicit.  x: device NHWC, dy: device [n][OH][OW][c_out],
- * dw: device HWIO (overwritten). */
+/* Weights gradient (Algorithm 4, first half): dw[kh,kw,ci,co] = sum over (n,oh,ow) of
+ * amul(x[n, oh*sh+kh-pt, ow*sw+kw-pl, ci], dy[n,oh,ow,co]), x outside the image being the zero
+ * border (+0, multiplied like any operand) -- the stride dilation of the error is implicit.
+ * x: device NHWC, dy: device [n][OH][OW][c_out], dw: device HWIO (overwritten). */
 int approx_conv2d_bwd_weight(const amsim_conv2d *desc, const float *x, const float *dy, float *dw,
                              const uint32_t *lut, int m_bits, void *workspace, size_t workspace_bytes,
                              void *stream);

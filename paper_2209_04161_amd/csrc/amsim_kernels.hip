@@ -1284,8 +1284,9 @@ __global__ __launch_bounds__(1024) void path_flags_kernel(const uint32_t *__rest
 // out to four independent jobs, in this order: the table (prep_table_body, or the low-bits pass
 // of a wide table), the backward-data pass's zero-tap flags, the first operand's decode (one of
 // the decode_a_body layouts) and the second operand's (decode_rows_body).  The jobs write
-// disjoint parts of the workspace; the decode jobs' exponent statistics are reduced by the table
-// kernel's own workgroups (tab_paths), so nothing runs between the two launches.
+// disjoint parts of the workspace.  The decode jobs' exponent statistics, which decide the table
+// kernel's path, are reduced by that kernel's own workgroups in a small call (tab_paths: nothing
+// runs between the two launches), else by path_flags_kernel or prep_rows_wide_kernel.
 struct PrepJobs {
     int n_tab, n_flag, n_a, n_b;  // workgroups of each job
     int wide;                     // the table job is a wide table's low-bits pass
@@ -1322,7 +1323,6 @@ __global__ __launch_bounds__(256) void prepass_kernel(PrepJobs j, A a)
 }
 
 // ------------------------------------------------------------------ host dispatch -------
-
 
 std::once_flag g_attr_once;
 hipError_t g_attr_err = hipSuccess;
