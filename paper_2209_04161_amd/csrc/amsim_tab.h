@@ -340,11 +340,12 @@ constexpr int tab_slab_steps(int tnw, int rl, int eb)
 
 // Slab staging: each thread copies CPT 16-byte pieces of the rows selected by the second
 // operand's mantissas (kb) for slots [0, nslots) of a slab, and that operand's head (pb).
-// TNW = result columns of the workgroup.
+// TNW = result columns of the workgroup.  Two parts, a slab apart: the second-operand words of
+// the thread's pieces (tab_fetch_words), then the row pieces they select (tab_fetch_rows), so
+// that a slab waits on one load latency rather than two dependent ones.
 template <int TNW, int EB, int CPT, int NT, int RL>
-__device__ __forceinline__ void tab_fetch(u32x4 (&stage)[CPT], float (&stage_pb)[CPT], const TabTap &tp, int c0,
-                                          const uint32_t *__restrict__ Bd, int Np, int col0,
-                                          const unsigned char *__restrict__ rows)
+__device__ __forceinline__ void tab_fetch_words(uint32_t (&bw)[CPT], const TabTap &tp, int c0,
+                                                const uint32_t *__restrict__ Bd, int Np, int col0)
 {
     constexpr int ROWB = (1 << RL) * EB;
     constexpr uint32_t kPad = RL == 7 ? kZeroRowWord : 0u;  // a padding step's second operand: +0
@@ -356,11 +357,25 @@ __device__ __forceinline__ void tab_fetch(u32x4 (&stage)[CPT], float (&stage_pb)
         if (CPT * NT > TOTAL && c >= TOTAL) break;  // the workgroup size does not divide the slab
         const int slot = c / (TNW * PIECES);
         const int t = (c / PIECES) % TNW;
-        const int piece = c % PIECES;
         const int j = c0 + slot;
-        const uint32_t bw = j < tp.count ? Bd[int64_t(tp.bbase + j) * Np + col0 + t] : kPad;
-        stage_pb[i] = head_value(bw);
-        stage[i] = *reinterpret_cast<const u32x4 *>(rows + (bw & kIdxMask) * EB + piece * 16);  // idx = kb << RL
+        bw[i] = j < tp.count ? Bd[int64_t(tp.bbase + j) * Np + col0 + t] : kPad;
+    }
+}
+
+template <int TNW, int EB, int CPT, int NT, int RL>
+__device__ __forceinline__ void tab_fetch_rows(u32x4 (&stage)[CPT], float (&stage_pb)[CPT], const uint32_t (&bw)[CPT],
+                                               const unsigned char *__restrict__ rows)
+{
+    constexpr int ROWB = (1 << RL) * EB;
+    constexpr int PIECES = ROWB / 16;
+    constexpr int TOTAL = tab_slab_steps(TNW, RL, EB) * TNW * PIECES;
+#pragma unroll
+    for (int i = 0; i < CPT; ++i) {
+        const int c = threadIdx.x + i * NT;
+        if (CPT * NT > TOTAL && c >= TOTAL) break;
+        const int piece = c % PIECES;
+        stage_pb[i] = head_value(bw[i]);
+        stage[i] = *reinterpret_cast<const u32x4 *>(rows + (bw[i] & kIdxMask) * EB + piece * 16);  // idx = kb << RL
     }
 }
 
@@ -430,35 +445,64 @@ __device__ __forceinline__ void tab_body(const TabArgs &a)
     const int q0 = tab_split(a) * a.chunks_per_split;
     const int p_end = min(q_total, q0 + a.chunks_per_split) * ch;
 
+    // Second-operand words a slab ahead of their rows (tab_fetch_words), where the table fits an
+    // XCD's L2 (rows of up to 1024 entries): measured on MI355X, the M = 10 GEMM 2048^3 14% and the
+    // 2-byte ResNet 3x3 backward-weight pass 3% faster.  The M = 11 table (8 MiB at 2 bytes) is
+    // read from beyond L2: with the words ahead its 4096^3 GEMM was 3% slower (19.15 against
+    // 18.6 ms); it fetches both in the same slab, and with the slab cursors kept a slab ahead as
+    // here it went to 17.85 ms.
+    constexpr bool WORDS_AHEAD = RL <= 10;
     u32x4 stage[CPT];
     float stage_pb[CPT];
+    uint32_t sbw[CPT];  // second-operand words of the next slab's pieces
     float acc[TM][TN];
     init_acc(acc);
     uint32_t acur[TM];
+    // The slab after (t, tp_, c): its tap, cursor and whether it is in this split's range.
+    auto advance = [&](const TabTap &t, int tp_, int c, TabTap &o, int &otap, int &oc, bool &ok)
+                       __attribute__((always_inline)) {
+        o = t;
+        otap = tp_;
+        oc = c + KS;
+        if (oc >= count) {
+            otap = tp_ + 1;
+            oc = 0;
+        }
+        ok = otap * cpt * ch + oc < p_end;
+        if (ok && otap != tp_) o = tab_tap<OP>(a, otap);
+    };
     TabTap cur{0, 0, 0, 0};
     int tap = q0 / max(cpt, 1);
     int c0 = (q0 - tap * cpt) * ch;
     bool have = q0 * ch < p_end;
+    TabTap nxt{0, 0, 0, 0};
+    int ntap = 0, nc0 = 0;
+    bool has_next = false;
     if (have) {
         cur = tab_tap<OP>(a, tap);
-        tab_fetch<TNW, EB, CPT, NT, RL>(stage, stage_pb, cur, c0, a.Bd, a.Np, colw, a.rows);
+        tab_fetch_words<TNW, EB, CPT, NT, RL>(sbw, cur, c0, a.Bd, a.Np, colw);
+        tab_fetch_rows<TNW, EB, CPT, NT, RL>(stage, stage_pb, sbw, a.rows);
         tab_commit<TNW, EB, CPT, NT, RL>(stage, stage_pb, smem, pbs, 0);
         load_a_words<OP, TM>(acur, av, __builtin_amdgcn_readfirstlane(a_step_offset<OP>(cur, c0)), c0);
+        advance(cur, tap, c0, nxt, ntap, nc0, has_next);
+        if (WORDS_AHEAD && has_next) tab_fetch_words<TNW, EB, CPT, NT, RL>(sbw, nxt, nc0, a.Bd, a.Np, colw);
     }
     __syncthreads();
     int buf = 0;
     while (have) {
         uniform_cursor(cur, tap, c0);
-        // the slab after this one
-        TabTap nxt = cur;
-        int ntap = tap, nc0 = c0 + KS;
-        if (nc0 >= count) {
-            ntap = tap + 1;
-            nc0 = 0;
+        uniform_cursor(nxt, ntap, nc0);
+        // the slab after the next one, whose words are loaded while this one is computed (the
+        // next slab's rows are fetched with the words loaded during the previous slab)
+        TabTap nxt2 = nxt;
+        int ntap2 = ntap, nc02 = nc0;
+        bool has_next2 = false;
+        if (has_next) advance(nxt, ntap, nc0, nxt2, ntap2, nc02, has_next2);
+        if (has_next) {
+            if constexpr (!WORDS_AHEAD) tab_fetch_words<TNW, EB, CPT, NT, RL>(sbw, nxt, nc0, a.Bd, a.Np, colw);
+            tab_fetch_rows<TNW, EB, CPT, NT, RL>(stage, stage_pb, sbw, a.rows);
         }
-        const bool has_next = ntap * cpt * ch + nc0 < p_end;
-        if (has_next && ntap != tap) nxt = tab_tap<OP>(a, ntap);
-        if (has_next) tab_fetch<TNW, EB, CPT, NT, RL>(stage, stage_pb, nxt, nc0, a.Bd, a.Np, colw, a.rows);
+        if (WORDS_AHEAD && has_next2) tab_fetch_words<TNW, EB, CPT, NT, RL>(sbw, nxt2, nc02, a.Bd, a.Np, colw);
         const unsigned char *tb = smem + buf * SLAB + cg * TN * ROWB;
         const float *pb_s = pbs + buf * KS * TNW + cg * TN;
         // the slab ends at the tap's end or, 8-step chunks being the unit of splits, at the split's
@@ -512,6 +556,10 @@ __device__ __forceinline__ void tab_body(const TabArgs &a)
         c0 = nc0;
         buf ^= 1;
         have = has_next;
+        nxt = nxt2;
+        ntap = ntap2;
+        nc0 = nc02;
+        has_next = has_next2;
     }
 
     // results (with splits, each split's partial result is laid out like the final one)
