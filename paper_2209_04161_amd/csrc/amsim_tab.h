@@ -1104,9 +1104,9 @@ __device__ __forceinline__ void tab_body_dot(const TabArgs &a)
 // (pa, pa) adds t_hi * pa + t_lo * pa = v * pb * pa, exact, to the sum: one instruction per
 // product and 4 bytes of LDS per product.  Exactness needs every half-product normal: pb's
 // exponent field >= 16 and Ea + Eb >= 143 (v_lo >= 2^-15), besides the bf16 path's upper bounds;
-// the table preparation checks it against the decode statistics.  8-wave, 8-column tiles only:
-// an 8-column entry is two 16-byte halves, each in a 2 KiB region of the step (so that the index
-// word, ka * 16, addresses both), and a slab holds NW steps.
+// the table preparation checks it against the decode statistics.  8-column tiles of 8 or 4 waves,
+// all along rows: an 8-column entry is two 16-byte halves, each in a 2 KiB region of the step (so
+// that the index word, ka * 16, addresses both), and a slab holds NW steps.
 constexpr int kHlStepBytes = 2 * kDotStepBytes;        // two 4-column halves of 128 entries x 16 bytes
 constexpr int kHlRowBytes = 64 * 2 * 4;                // per row kb: 64 groups x 2 entries x 4 bytes
 
@@ -1156,11 +1156,13 @@ __device__ __forceinline__ void hl_commit(const u32x4 (&bw)[2], const u32x2 (&rw
     }
 }
 
-// Workgroup: 8 waves along rows (64*TM rows each), all on the same 8 columns; slabs of 8 steps.
-template <int OP, int TM>
+// Workgroup: NW (8 or 4) waves along rows (64*TM rows each), all on the same 8 columns; slabs of
+// NW steps.
+template <int OP, int TM, int NW>
 __device__ __forceinline__ void tab_body_hl(const TabArgs &a)
 {
-    constexpr int NW = 8, TN = 8, KS = NW;
+    static_assert(NW == 8 || NW == 4, "8 or 4 waves");
+    constexpr int TN = 8, KS = NW;
     constexpr int kSlab = KS * kHlStepBytes;
     constexpr int NA = 3;  // first-operand registers per step pair and lane row (one record)
     extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
@@ -1194,9 +1196,10 @@ __device__ __forceinline__ void tab_body_hl(const TabArgs &a)
     u32x2 srw[8];
     float acc[TM][TN];
     init_acc(acc);
-    // the first operand's step pairs as a ring of four (pair kp in w[kp % 4]), loaded LA ahead
-    constexpr int RS = 4;
-    constexpr int LA = OP == OP_BWD_DATA ? 2 : 3;
+    // the first operand's step pairs as a ring of four (8 waves) or two (4 waves; pair kp in
+    // w[kp % RS]), loaded LA ahead
+    constexpr int RS = NW == 8 ? 4 : 2;
+    constexpr int LA = NW == 8 ? (OP == OP_BWD_DATA ? 2 : 3) : 1;
     static_assert((KS / 2) % RS == 0, "ring of step pairs");
     uint32_t w[RS][NA][TM];
     auto advance = [&](const TabTap &t, int tp_, int c, TabTap &o, int &otap, int &oc, bool &ok)
@@ -1419,9 +1422,9 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(4, 4)))
             tab_body_dot<OP, TM, NW, TN>(a);
             return;
         }
-        if constexpr (TN == 8 && NW == 8) {
+        if constexpr (TN == 8 && (NW == 8 || NW == 4)) {
             if (path == 2) {
-                tab_body_hl<OP, TM>(a);
+                tab_body_hl<OP, TM, NW>(a);
                 return;
             }
         }
@@ -1465,7 +1468,7 @@ constexpr size_t tab_lds_bytes(int tn, int wr, int nw, int rl)
     b = tab_exact_lds_bytes(tnw, rl, 2) > b ? tab_exact_lds_bytes(tnw, rl, 2) : b;
     b = tab_exact_lds_bytes(tnw, rl, 4) > b ? tab_exact_lds_bytes(tnw, rl, 4) : b;
     const size_t dot = (rl == 7 && dot_cols_ok(tn) && wr == nw) ? size_t(2) * dot_slab_steps(nw) * kDotStepBytes : 0;
-    const size_t hl = (rl == 7 && tn == 8 && nw == 8 && wr == nw) ? size_t(2) * nw * kHlStepBytes : 0;
+    const size_t hl = (rl == 7 && tn == 8 && (nw == 8 || nw == 4) && wr == nw) ? size_t(2) * nw * kHlStepBytes : 0;
     b = b > dot ? b : dot;
     return b > hl ? b : hl;
 }

@@ -388,3 +388,21 @@ def test_conv_border_products_zero_signs(B, ci, model):
         signs |= set(np.signbit(ref[zero]).tolist())
         _check_class_and_zero_signs(got, ref, S, "%s %s" % (fn.__name__, name))
     assert signs == {True, False}
+
+
+@pytest.mark.parametrize("pass_id", [0, 1, 2])
+def test_exact_trunc_conv_passes_on_four_wave_tiles(B, pass_id):
+    """The 2-byte (exact bfloat16-truncation) table on the hi/lo path in 4-wave tiles: the ResNet
+    3x3 shape at batch 8, whose backward-weight pass (576 rows) takes a 4-wave, 8-column tile;
+    seeded sampled outputs against the oracle."""
+    p = W.conv_desc(8, 32, 32, 64, 64, 3, 3, 1, 1)
+    x, w, dy = W.resnet_conv_inputs(p, seed=1800)
+    lut = dev_lut(B, "exact_trunc", 7)
+    rng = np.random.default_rng(1801 + pass_id)
+    fn, ref_fn, a0, a1 = [(B.approx_conv2d_fwd, oracle.conv2d_fwd, x, w),
+                          (B.approx_conv2d_bwd_data, oracle.conv2d_bwd_data, dy, w),
+                          (B.approx_conv2d_bwd_weight, oracle.conv2d_bwd_weight, x, dy)][pass_id]
+    got = host(fn(p, cuda(a0), cuda(a1), lut, 7)).reshape(-1)
+    idx = np.sort(rng.choice(got.size, min(got.size, 4000), replace=False))
+    ref, S = ref_fn(oracle.EXACT_TRUNC, 7, p, a0, a1, idx=idx)
+    assert_within_tolerance(got[idx], ref, S, "exact_trunc pass %d" % pass_id)
