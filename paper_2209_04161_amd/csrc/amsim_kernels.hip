@@ -1167,14 +1167,21 @@ __device__ __forceinline__ void prep_table_body(const TablePrep &t, int bid, int
     }
 }
 
-// Wide tables (M = 8..11, rows of 2^M entries, no bf16 path).  The pre-pass job: the OR of the
-// entries' low 16 mantissa bits, one word per workgroup.
+// Wide tables (M = 8..11, rows of 2^M entries, no bf16 path).  The pre-pass job, one word per
+// workgroup: the OR of the entries' low 16 mantissa bits, and bit 31 set when an entry (ka, kb)
+// differs from the entry of the same index sum s = ka + kb in row min(s, 2^M - 1) -- i.e. when the
+// table is not sum-indexed (T[ka][kb] = g(ka + kb)).
 __device__ __forceinline__ void lut_low_bits_body(const TablePrep &t, int bid, int nblk)
 {
     __shared__ uint32_t s_low[4];
-    const int total = 1 << (2 * t.m);
+    const int n = 1 << t.m, total = n * n;
     uint32_t low = 0u;
-    for (int i = bid * 256 + int(threadIdx.x); i < total; i += nblk * 256) low |= t.lut[i] & 0xFFFFu;
+    for (int i = bid * 256 + int(threadIdx.x); i < total; i += nblk * 256) {
+        const uint32_t e = t.lut[i];
+        const int s = (i >> t.m) + (i & (n - 1)), ka = min(s, n - 1);
+        low |= e & 0xFFFFu;
+        if (((e ^ t.lut[(ka << t.m) + (s - ka)]) & 0x00FFFFFFu) != 0u) low |= 0x80000000u;
+    }
     const uint32_t r = block_or(low, s_low);
     if (threadIdx.x == 0) t.part[bid] = r;
 }
@@ -1182,8 +1189,9 @@ __device__ __forceinline__ void lut_low_bits_body(const TablePrep &t, int bid, i
 // Second launch for wide tables: the entry width from the nparts partial words, then the
 // transposed rows -- row kb (2^m entries of eb bytes) holds entry (ka, kb) at byte ka * eb --
 // through 64 x 64 LDS tiles (loads along kb, stores along ka).  Workgroup 0 writes flags[0] = eb,
-// flags[1] = 0 (no bf16 path for wide rows) and flags[2], the exact path's product form, from
-// the decode statistics (n_a and n_b words; null for the native multiply).
+// flags[1] = 0 (no bf16 path for wide rows), flags[2], the exact path's product form, from
+// the decode statistics (n_a and n_b words; null for the native multiply), and flags[3] = 1 when
+// the table is sum-indexed.
 __global__ __launch_bounds__(256) void prep_rows_wide_kernel(const uint32_t *__restrict__ lut, int m,
                                                              const uint32_t *__restrict__ part, int nparts,
                                                              const uint32_t *__restrict__ stats_a, int n_a,
@@ -1196,7 +1204,7 @@ __global__ __launch_bounds__(256) void prep_rows_wide_kernel(const uint32_t *__r
     uint32_t low = 0u;
     for (int i = threadIdx.x; i < nparts; i += 256) low |= part[i];
     const uint32_t lb = block_or(low, s_low);
-    const int eb = lb == 0u ? 1 : ((lb & 0xFFu) == 0u ? 2 : 4);
+    const int eb = (lb & 0xFFFFu) == 0u ? 1 : ((lb & 0xFFu) == 0u ? 2 : 4);
     if (blockIdx.x == 0) {  // uniform
         uint32_t alo = 255u, ahs = 0u, blo = 255u, bhs = 0u;
         const bool have = stats_a != nullptr;
@@ -1219,6 +1227,7 @@ __global__ __launch_bounds__(256) void prep_rows_wide_kernel(const uint32_t *__r
             flags[0] = eb;
             flags[1] = 0;
             flags[2] = rounded;
+            flags[3] = (lb >> 31) == 0u ? 1 : 0;
         }
     }
     const int n = 1 << m, tiles_1d = n / 64;

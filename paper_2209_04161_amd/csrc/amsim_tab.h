@@ -61,7 +61,8 @@ struct TabArgs {
     const unsigned char *dot_rows;  // the same 1-byte rows in bf16-path staging order
     const unsigned char *hl_rows;   // 2-byte tables: entries split into bf16 halves (hi/lo path)
     const int *eb;                  // [0] entry width, [1] 1 (2) when the bf16 (hi/lo) path may run,
-                                    // [2] 1 when the exact path rounds each product before adding it
+                                    // [2] 1 when the exact path rounds each product before adding it,
+                                    // [3] (rows of 256 entries or more) 1 when the table is sum-indexed
     const uint32_t *stats_a, *stats_b;  // kTabApproxSelf: the decode passes' exponent statistics
     int n_a, n_b;                       // (null: none), words of each operand, and whether the
     int narrow;                         // operands are cast to fewer exponent bits than FP32's
@@ -569,6 +570,199 @@ __device__ __forceinline__ void tab_body(const TabArgs &a)
         const int row = row0 + 64 * r;
         if (row >= R) continue;
         float *dst = out + tab_row_out<OP>(a, row);  // recomputed rather than kept in registers
+#pragma unroll
+        for (int t = 0; t < TN; ++t) {
+            const int col = col0 + t;
+            if (col < a.N) dst[col] = acc[r][t];
+        }
+    }
+}
+
+// ------------------------------------------------------- sum-indexed wide tables
+// For many approximate multipliers -- Mitchell's at every M among them -- an entry depends on the
+// two mantissa indices only through their sum: T[ka][kb] = g(ka + kb), with
+// g(s) = T[min(s, 2^M - 1)][s - min(s, 2^M - 1)].  The table preparation checks every entry for it
+// (flags[3]).  Such a table is served from g alone: 2^(M+1) factors v (as floats, pre-scaled by vadd
+// in the rounded form) copied into LDS once per workgroup, where the exact path stages a 2^M-entry
+// row per column and step (4 KiB per column and step at M = 11, read from beyond L2).  Per product:
+// one address add (the lane row's ka, the column's kb, both as byte offsets), one LDS gather, and the
+// exact path's arithmetic.  The slabs hold only the second operand's (kb offset, head) pairs.
+constexpr int kSumSlabSteps = 16;
+
+constexpr size_t tab_sum_lds_bytes(int tnw, int rl)
+{
+    return (size_t(2) << rl) * 4 + size_t(2) * kSumSlabSteps * tnw * 8;
+}
+
+template <int OP, int TM, int TN, int WR, int NW, int RL, bool ROUNDED>
+__device__ __forceinline__ void tab_body_sum(const TabArgs &a, int eb)
+{
+    constexpr int NT = 64 * NW;
+    constexpr int WC = NW / WR;
+    constexpr int TNW = TN * WC;            // result columns of the workgroup
+    constexpr int KS = kSumSlabSteps;
+    constexpr int GN = 2 << RL;             // g's entries (the last one unused)
+    constexpr int WSLAB = KS * TNW;         // (kb offset, head) pairs per slab
+    constexpr int WPT = (WSLAB + NT - 1) / NT;
+    extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
+    float *g = reinterpret_cast<float *>(smem);
+    u32x2 *wds = reinterpret_cast<u32x2 *>(smem + GN * 4);  // [2][KS][TNW]
+
+    const int R = tab_rows<OP>(a);
+    if (a.tx * 64 * TM * WR >= R) return;  // uniform over the workgroup
+    const int lane = threadIdx.x & 63;
+    const int wave = wave_id();
+    const int rg = wave % WR, cg = wave / WR;
+    const int row0 = a.tx * (64 * TM * WR) + rg * (64 * TM) + lane;
+    const bool live = row0 - lane < R;  // wave-uniform: a wave past the end only stages
+    const int colw = a.ty * TNW;
+    const int col0 = colw + cg * TN;
+    int abase[TM];
+#pragma unroll
+    for (int r = 0; r < TM; ++r) {
+        const int row = row0 + 64 * r;
+        abase[r] = row < R ? tab_row_rec<OP>(a, row) : 0;
+    }
+    const AView<TM> av = make_aview<OP, TM>(a, abase);
+    const int count = tab_count<OP>(a);
+    const int ch = a.chunk;
+    const int cpt = (count + ch - 1) / ch;
+    const int q_total = tab_taps<OP>(a) * cpt;
+    const int q0 = tab_split(a) * a.chunks_per_split;
+    const int p_end = min(q_total, q0 + a.chunks_per_split) * ch;
+
+    // g from the transposed rows (row kb holds entry (ka, kb) at byte (kb * 2^RL + ka) * eb)
+    for (int s = threadIdx.x; s < GN; s += NT) {
+        const int ka = min(s, (1 << RL) - 1), kb = s - ka;
+        float v = 0.0f;
+        if (kb < (1 << RL)) {
+            const unsigned char *src = a.rows + ((size_t(kb) << RL) + size_t(ka)) * eb;
+            const uint32_t vadd = ROUNDED ? a.vadd : 0u;
+            v = eb == 1 ? tab_value_scaled<1>(src, vadd)
+                        : (eb == 2 ? tab_value_scaled<2>(src, vadd) : tab_value_scaled<4>(src, vadd));
+        }
+        g[s] = v;
+    }
+    // The second operand's pairs of a slab: thread -> (slot, column) c = threadIdx.x + i * NT.
+    // A second-operand index outside the table is a zero's (its product is a signed zero whatever
+    // it reads): it reads g(ka).
+    uint32_t sw[WPT];
+    auto fetch = [&](const TabTap &tp, int c0_) __attribute__((always_inline)) {
+#pragma unroll
+        for (int i = 0; i < WPT; ++i) {
+            const int c = threadIdx.x + i * NT;
+            const int slot = c / TNW, t = c % TNW, j = c0_ + slot;
+            sw[i] = (c < WSLAB && j < tp.count) ? Bd_word(a, tp.bbase + j, colw + t) : 0u;
+        }
+    };
+    auto commit = [&](int buf_) __attribute__((always_inline)) {
+#pragma unroll
+        for (int i = 0; i < WPT; ++i) {
+            const int c = threadIdx.x + i * NT;
+            if (WPT * NT > WSLAB && c >= WSLAB) break;
+            const uint32_t kb = (sw[i] & kIdxMask) >> RL;
+            wds[buf_ * WSLAB + c] = u32x2{(kb < (1u << RL) ? kb : 0u) * 4u, sw[i] & kHeadMask};
+        }
+    };
+    float acc[TM][TN];
+    init_acc(acc);
+    uint32_t acur[TM];
+    auto advance = [&](const TabTap &t, int tp_, int c, TabTap &o, int &otap, int &oc, bool &ok)
+                       __attribute__((always_inline)) {
+        o = t;
+        otap = tp_;
+        oc = c + KS;
+        if (oc >= count) {
+            otap = tp_ + 1;
+            oc = 0;
+        }
+        ok = otap * cpt * ch + oc < p_end;
+        if (ok && otap != tp_) o = tab_tap<OP>(a, otap);
+    };
+    TabTap cur{0, 0, 0, 0};
+    int tap = q0 / max(cpt, 1);
+    int c0 = (q0 - tap * cpt) * ch;
+    bool have = q0 * ch < p_end;
+    TabTap nxt{0, 0, 0, 0};
+    int ntap = 0, nc0 = 0;
+    bool has_next = false;
+    if (have) {
+        cur = tab_tap<OP>(a, tap);
+        fetch(cur, c0);
+        commit(0);
+        load_a_words<OP, TM>(acur, av, __builtin_amdgcn_readfirstlane(a_step_offset<OP>(cur, c0)), c0);
+        advance(cur, tap, c0, nxt, ntap, nc0, has_next);
+    }
+    __syncthreads();
+    int buf = 0;
+    while (have) {
+        uniform_cursor(cur, tap, c0);
+        uniform_cursor(nxt, ntap, nc0);
+        if (has_next) fetch(nxt, nc0);
+        const u32x2 *wb = wds + buf * WSLAB + cg * TN;
+        const int nslots = live ? min(min(KS, cur.count - c0), p_end - (tap * cpt * ch + c0)) : 0;
+        __builtin_amdgcn_s_setprio(3);
+        for (int slot = 0; slot < nslots; ++slot) {
+            uint32_t anext[TM];
+            const bool in_slab = slot + 1 < nslots;
+            const uint32_t unext = __builtin_amdgcn_readfirstlane(in_slab ? a_step_offset<OP>(cur, c0 + slot + 1)
+                                                                          : a_step_offset<OP>(nxt, nc0));
+            const int jnext = __builtin_amdgcn_readfirstlane(in_slab ? c0 + slot + 1 : nc0);
+            if (in_slab || has_next) {
+                load_a_words<OP, TM>(anext, av, unext, jnext);
+            } else {
+#pragma unroll
+                for (int r = 0; r < TM; ++r) anext[r] = 0u;
+            }
+            uint32_t ao[TM];
+            float pa[TM];
+#pragma unroll
+            for (int r = 0; r < TM; ++r) {
+                ao[r] = __builtin_amdgcn_ubfe(acur[r], 4, RL) * 4u;  // idx = ka << 4
+                pa[r] = head_value(acur[r]);
+            }
+            // every gather of the step before the first product: one LDS latency per step
+            float v[TM][TN], pb[TN];
+#pragma unroll
+            for (int t = 0; t < TN; ++t) {
+                const u32x2 w = wb[slot * TNW + t];
+                pb[t] = __uint_as_float(w.y);
+#pragma unroll
+                for (int r = 0; r < TM; ++r) v[r][t] = *reinterpret_cast<const float *>(smem + ao[r] + w.x);
+            }
+            __builtin_amdgcn_sched_barrier(0);  // the scheduler would interleave them with the products
+#pragma unroll
+            for (int t = 0; t < TN; ++t) {
+#pragma unroll
+                for (int r = 0; r < TM; ++r) {
+                    if constexpr (ROUNDED) {
+                        const float c = v[r][t] * (pa[r] * pb[t]);
+                        acc[r][t] = __builtin_fmaf(c * a.su, a.sd, acc[r][t]);
+                    } else {
+                        acc[r][t] = __builtin_fmaf(v[r][t], pa[r] * pb[t], acc[r][t]);
+                    }
+                }
+            }
+#pragma unroll
+            for (int r = 0; r < TM; ++r) acur[r] = anext[r];
+        }
+        __builtin_amdgcn_s_setprio(0);
+        if (has_next) commit(buf ^ 1);
+        __syncthreads();
+        cur = nxt;
+        tap = ntap;
+        c0 = nc0;
+        buf ^= 1;
+        have = has_next;
+        if (have) advance(cur, tap, c0, nxt, ntap, nc0, has_next);
+    }
+
+    float *out = a.out + int64_t(tab_split(a)) * a.out_elems;
+#pragma unroll
+    for (int r = 0; r < TM; ++r) {
+        const int row = row0 + 64 * r;
+        if (row >= R) continue;
+        float *dst = out + tab_row_out<OP>(a, row);
 #pragma unroll
         for (int t = 0; t < TN; ++t) {
             const int col = col0 + t;
@@ -1430,6 +1624,15 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(4, 4)))
         }
     }
     const int rounded = VAR == kTabApproxSelf ? self_rounded : __builtin_amdgcn_readfirstlane(a.eb[2]);
+    if constexpr (RL >= 8) {
+        if (__builtin_amdgcn_readfirstlane(a.eb[3]) == 1) {  // a sum-indexed table
+            if (rounded)
+                tab_body_sum<OP, TM, TN, WR, NW, RL, true>(a, eb);
+            else
+                tab_body_sum<OP, TM, TN, WR, NW, RL, false>(a, eb);
+            return;
+        }
+    }
     if (rounded) {
         if (eb == 1)
             tab_body<OP, TM, TN, WR, 1, NW, RL, true>(a);
@@ -1469,7 +1672,9 @@ constexpr size_t tab_lds_bytes(int tn, int wr, int nw, int rl)
     b = tab_exact_lds_bytes(tnw, rl, 4) > b ? tab_exact_lds_bytes(tnw, rl, 4) : b;
     const size_t dot = (rl == 7 && dot_cols_ok(tn) && wr == nw) ? size_t(2) * dot_slab_steps(nw) * kDotStepBytes : 0;
     const size_t hl = (rl == 7 && tn == 8 && (nw == 8 || nw == 4) && wr == nw) ? size_t(2) * nw * kHlStepBytes : 0;
+    const size_t sum = rl >= 8 ? tab_sum_lds_bytes(tnw, rl) : 0;
     b = b > dot ? b : dot;
+    b = b > sum ? b : sum;
     return b > hl ? b : hl;
 }
 

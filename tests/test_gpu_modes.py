@@ -207,7 +207,8 @@ def test_format_gemm_k1_products_bit_exact(B, e, sat, m):
 
 
 @pytest.mark.parametrize("e,sat,model,m", [(5, False, "exact_trunc", 10), (5, True, "mitchell", 7),
-                                           (4, False, "mitchell", 7), (7, False, "exact_trunc", 7)])
+                                           (4, False, "mitchell", 7), (7, False, "exact_trunc", 7),
+                                           (5, True, "mitchell", 10)])
 @pytest.mark.parametrize("shape", [(130, 70, 300), (4096, 256, 64)])
 def test_format_gemm_sums(B, e, sat, model, m, shape):
     M, N, K = shape

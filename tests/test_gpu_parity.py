@@ -305,14 +305,16 @@ GEMM_SHAPES = [(64, 64, 64), (1, 1, 1), (3, 17, 63), (65, 1000, 17), (130, 7, 30
 
 
 @pytest.mark.parametrize("shape", GEMM_SHAPES)
-@pytest.mark.parametrize("m", [7, 11])
-def test_gemm_matches_oracle(B, shape, m):
+@pytest.mark.parametrize("model,m", [("mitchell", 7), ("mitchell", 11), ("exact_trunc", 11)])
+def test_gemm_matches_oracle(B, shape, model, m):
+    """M = 11: Mitchell's table is sum-indexed (read from one g array), the exact truncated
+    product's is not (rows staged per column and step)."""
     M, N, K = shape
     A = W.uniform((M, K), -1, 1, 1000 + M)
     Bm = W.uniform((K, N), -1, 1, 2000 + N)
-    C = host(B.approx_gemm(cuda(A), cuda(Bm), dev_lut(B, "mitchell", m), m))
-    ref, S = oracle.gemm(oracle.MITCHELL, m, A, Bm)
-    assert_within_tolerance(C, ref, S, "gemm %s M=%d" % (shape, m))
+    C = host(B.approx_gemm(cuda(A), cuda(Bm), dev_lut(B, model, m), m))
+    ref, S = oracle.gemm(MODELS[model], m, A, Bm)
+    assert_within_tolerance(C, ref, S, "gemm %s %s M=%d" % (shape, model, m))
 
 
 @pytest.mark.parametrize("ta,tb", [(True, False), (False, True), (True, True)])
