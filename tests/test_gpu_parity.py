@@ -374,7 +374,8 @@ CONV_CASES = [
     W.conv_desc(2, 5, 4, 2, 3, 4, 4, 2, pads=(3, 3, 3, 3)),
     W.conv_desc(2, 5, 5, 300, 20, 3, 3, 1, 1),
     W.conv_desc(2, 6, 6, 24, 200, 3, 3, 2, 1),
-    W.conv_desc(1, 3, 70, 130, 9, 3, 3, 1, 1),   # x rows pass through LDS in two channel chunks
+    W.conv_desc(1, 3, 70, 130, 9, 3, 3, 1, 1),   # x rows pass through LDS in two channel chunks; backward
+                                                 # weight: rows of 9100 elements, beyond its LDS row stage
     W.conv_desc(1, 3, 70, 9, 130, 3, 3, 1, 1),   # dy rows (backward data) likewise
     W.conv_desc(1, 3, 1100, 8, 5, 3, 3, 1, 1),   # few channels, but a row too long to unfold along w
     W.conv_desc(2, 7, 9, 5, 6, 1, 4, 1, 3, pads=(0, 0, 2, 1)),  # 1 x 4 kernel, unfolded into 20 channels
