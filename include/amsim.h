@@ -164,7 +164,10 @@ typedef struct amsim_conv2d {
 
 /* Device workspace bytes a pass needs for this shape and M (0 allowed for NULL workspace).  A 1 x 1
  * pass with stride 1 and no padding runs as its GEMM over the pixels (its im2col matrix is the
- * input itself) and needs that GEMM's workspace. */
+ * input itself) and needs that GEMM's workspace.  A stride-1 backward-data pass with every pad at
+ * most the kernel extent minus one and c_out >= 16 runs as the forward pass over dy (padded by the
+ * kernel extent minus one minus each pad) with the weights reversed in both kernel axes and c_in,
+ * c_out exchanged -- the same products -- and needs that forward pass's workspace. */
 int amsim_conv2d_workspace_size(const amsim_conv2d *desc, int pass, int m_bits, size_t *bytes);
 
 /* Forward propagation (Algorithm 3): y[n,oh,ow,co] = sum_{kh,kw,ci}

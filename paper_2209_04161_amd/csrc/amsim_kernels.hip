@@ -1922,11 +1922,12 @@ DecNhcw nhcw_job(const float *src, int n, int h, int w, int c, int top, int left
     return DecNhcw{src, n, h, w, c, top, left, hp, wp, dst, cc, (rec_c + 1) / 2, vec};
 }
 
-int conv_fwd_run(const Mode &md, const amsim_conv2d *desc, const float *x, const float *w, float *y,
-                 const uint32_t *lut, int m_bits, void *workspace, size_t workspace_bytes, hipStream_t st)
+// The forward pass of desc.  flip_w: w is a backward-data pass's [kh][kw][c_out][c_in] weights (of
+// the caller's convolution, whose c_in / c_out are desc's c_out / c_in), read flipped in both
+// kernel axes and transposed (bwd_data_runs_as_fwd); timer_kind: the kernel timer's slot.
+int fwd_core(const Mode &md, const amsim_conv2d *desc, const float *x, const float *w, bool flip_w, float *y,
+             const uint32_t *lut, int m_bits, void *workspace, size_t workspace_bytes, hipStream_t st, int timer_kind)
 {
-    if (pass_as_gemm(desc, AMSIM_CONV_FWD, m_bits))
-        return conv_gemm_run(md, desc, AMSIM_CONV_FWD, x, w, y, lut, m_bits, workspace, workspace_bytes, st);
     Plan p;
     int rc = conv_common(md, desc, AMSIM_CONV_FWD, x, w, y, lut, m_bits, workspace, workspace_bytes, &p);
     if (rc != AMSIM_OK) return rc;
@@ -1940,8 +1941,13 @@ int conv_fwd_run(const Mode &md, const amsim_conv2d *desc, const float *x, const
     PrepJobs j = prep_jobs(md, lut, mb, ws, p);
     // w [kh][kw * ci][co] as batches kh of kw * ci rows (unfolded: padded to cu rows with +0)
     const int kwc = s.kw * s.ci, wrows = p.unfold_w ? unfolded_channels(s) : kwc;
-    j.b = DecRows{w, int64_t(kwc) * s.co, int64_t(s.co), 1, s.kh, wrows, kwc, s.co, Wd, int(p.b_ld),
-                  decode_vec(w, int64_t(kwc) * s.co, s.co, 1)};
+    if (flip_w)  // batches (kh, kw) of ci rows [kh][kw][ci][co] = w[KH-1-kh][KW-1-kw][co][ci]: the last
+                 // kernel position first, rows ci at unit stride, columns co at stride ci
+        j.b = DecRows{w + (int64_t(s.kh) * s.kw - 1) * s.ci * s.co, -int64_t(s.ci) * s.co, 1, int64_t(s.ci),
+                      s.kh * s.kw, s.ci, s.ci, s.co, Wd, int(p.b_ld), 0};
+    else
+        j.b = DecRows{w, int64_t(kwc) * s.co, int64_t(s.co), 1, s.kh, wrows, kwc, s.co, Wd, int(p.b_ld),
+                      decode_vec(w, int64_t(kwc) * s.co, s.co, 1)};
     j.n_b = decode_grid(int64_t(s.kh) * wrows * p.b_ld);
     const int var = tab_variant(md, p, conv_macs(s));
     if (p.unfold_w) {
@@ -1959,7 +1965,7 @@ int conv_fwd_run(const Mode &md, const amsim_conv2d *desc, const float *x, const
     set_format_scales(a, md);
     const dim3 grid = dim3_of(fwd_grid(p, s));
     {
-        TimedLaunch tl(md.native ? AMSIM_KERNEL_CONV_FWD_NATIVE : AMSIM_KERNEL_CONV_FWD, st);
+        TimedLaunch tl(timer_kind, st);
         rc = tab_launch<OP_FWD>(p.tile, p.rl, var, a, grid, st) == hipSuccess
                  ? AMSIM_OK
                  : AMSIM_ERR_HIP;
@@ -1967,6 +1973,15 @@ int conv_fwd_run(const Mode &md, const amsim_conv2d *desc, const float *x, const
     if (rc != AMSIM_OK || p.splits == 1) return rc;
     launch_reduce(reinterpret_cast<const float *>(ws + p.off_part), p.splits, int(rows), s.co, y, int64_t(s.co), st);
     return launch_status();
+}
+
+int conv_fwd_run(const Mode &md, const amsim_conv2d *desc, const float *x, const float *w, float *y,
+                 const uint32_t *lut, int m_bits, void *workspace, size_t workspace_bytes, hipStream_t st)
+{
+    if (pass_as_gemm(desc, AMSIM_CONV_FWD, m_bits))
+        return conv_gemm_run(md, desc, AMSIM_CONV_FWD, x, w, y, lut, m_bits, workspace, workspace_bytes, st);
+    return fwd_core(md, desc, x, w, false, y, lut, m_bits, workspace, workspace_bytes, st,
+                    md.native ? AMSIM_KERNEL_CONV_FWD_NATIVE : AMSIM_KERNEL_CONV_FWD);
 }
 
 // The backward-data pass of `desc` (the caller's, or the virtual unfolded one) under plan p, into dx.
@@ -2022,6 +2037,11 @@ int conv_bwd_data_run(const Mode &md, const amsim_conv2d *desc, const float *dy,
 {
     if (pass_as_gemm(desc, AMSIM_CONV_BWD_DATA, m_bits))
         return conv_gemm_run(md, desc, AMSIM_CONV_BWD_DATA, dy, w, dx, lut, m_bits, workspace, workspace_bytes, st);
+    if (desc && check_conv(desc, AMSIM_CONV_BWD_DATA) == AMSIM_OK && bwd_data_runs_as_fwd(desc)) {
+        const amsim_conv2d f = bwd_data_fwd_desc(desc);
+        return fwd_core(md, &f, dy, w, true, dx, lut, m_bits, workspace, workspace_bytes, st,
+                        md.native ? AMSIM_KERNEL_CONV_BWD_DATA_NATIVE : AMSIM_KERNEL_CONV_BWD_DATA);
+    }
     Plan p;
     int rc = conv_common(md, desc, AMSIM_CONV_BWD_DATA, dy, w, dx, lut, m_bits, workspace, workspace_bytes, &p);
     if (rc != AMSIM_OK) return rc;
@@ -2191,6 +2211,11 @@ int amsim_conv2d_workspace_size(const amsim_conv2d *desc, int pass, int m_bits, 
     if (conv_runs_as_gemm(desc, pass, m_bits)) {
         const ConvGemm g = conv_gemm(desc, pass);
         *bytes = gemm_workspace_bytes(g.trans_a, g.trans_b, g.m, g.n, g.k, m_bits);
+        return AMSIM_OK;
+    }
+    if (pass == AMSIM_CONV_BWD_DATA && bwd_data_runs_as_fwd(desc)) {
+        const amsim_conv2d f = bwd_data_fwd_desc(desc);
+        *bytes = std::max(plan_conv(&f, AMSIM_CONV_FWD, m_bits).total, plan_conv(&f, AMSIM_CONV_FWD, 7).total);
         return AMSIM_OK;
     }
     *bytes = std::max(plan_conv(desc, pass, m_bits).total, plan_conv(desc, pass, 7).total);

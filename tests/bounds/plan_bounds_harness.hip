@@ -50,6 +50,7 @@ char g_case[512];
 long g_checks = 0;
 int64_t g_max_a_bytes = 0;     // largest first-operand buffer planned
 int64_t g_max_offset = 0;      // largest record end formed (row base + step offset + 12)
+long g_bwd_as_fwd = 0;         // backward-data passes checked on the forward route
 
 [[noreturn]] void fail(const char *what, int64_t v1, int64_t v2)
 {
@@ -243,6 +244,27 @@ void check_conv_pass(Rng &rng, const amsim_conv2d &d, int pass, int mb)
         std::snprintf(g_case, sizeof g_case, "%s", conv_case);
         return;
     }
+    if (pass == AMSIM_CONV_BWD_DATA && bwd_data_runs_as_fwd(&d)) {  // stride 1: the forward pass over dy
+        const amsim_conv2d f = bwd_data_fwd_desc(&d);
+        const ConvShape sf = shape_of(&f);
+        expect(sf.oh == d.h && sf.ow == d.w && f.c_out == d.c_in && f.n == d.n, "the forward pass yields dx's shape",
+               int64_t(sf.oh) * sf.ow, int64_t(d.h) * d.w);
+        expect(f.c_in == sf.ci && !fwd_unfolds(sf, f.h + f.pad_top + f.pad_bottom), "dy's channels stay whole",
+               f.c_in, 0);
+        // the flipped, transposed weight reads: batch b of kh * kw (from the last kernel position), row
+        // r of c_out, column c of c_in, at (kh * kw - 1 - b) * ci * co + c * co + r of the caller's w
+        const int64_t nw = int64_t(d.kh) * d.kw * d.c_in * d.c_out, kk = int64_t(d.kh) * d.kw;
+        const int64_t base = (kk - 1) * d.c_in * d.c_out, sb = -int64_t(d.c_in) * d.c_out;
+        const int64_t lo = base + (kk - 1) * sb;                                       // last batch, row 0, column 0
+        const int64_t hi = base + (d.c_out - 1) + int64_t(d.c_in - 1) * d.c_out;       // batch 0, last row and column
+        expect(lo == 0 && hi == nw - 1, "flipped weight reads inside w", hi, nw);
+        ++g_bwd_as_fwd;
+        char bd_case[sizeof g_case];
+        std::snprintf(bd_case, sizeof bd_case, "%s", g_case);
+        check_conv_pass(rng, f, AMSIM_CONV_FWD, mb);
+        std::snprintf(g_case, sizeof g_case, "%s", bd_case);
+        return;
+    }
     const Plan p = plan_conv(&d, pass, mb);
     check_table_area(p);
     const ConvShape s0 = shape_of(&d);
@@ -316,6 +338,12 @@ amsim_conv2d random_desc(Rng &rng)
     if (rng.uniform(0, 7) == 0) {  // one in eight pointwise: 1 x 1, stride 1, no padding (the GEMM route)
         d.kh = d.kw = d.stride_h = d.stride_w = 1;
         d.pad_top = d.pad_bottom = d.pad_left = d.pad_right = 0;
+    } else if (rng.uniform(0, 7) == 0) {  // stride 1, pads within the kernel (backward data as a forward pass)
+        d.stride_h = d.stride_w = 1;
+        d.pad_top = std::min(d.pad_top, d.kh - 1);
+        d.pad_bottom = std::min(d.pad_bottom, d.kh - 1);
+        d.pad_left = std::min(d.pad_left, d.kw - 1);
+        d.pad_right = std::min(d.pad_right, d.kw - 1);
     }
     return d;
 }
@@ -359,7 +387,7 @@ int main(int argc, char **argv)
         }
     }
     std::printf("OK gemm_cases=%ld conv_cases=%ld conv_descriptors_drawn=%ld checks=%ld max_a_bytes=%" PRId64
-                " max_record_end=%" PRId64 "\n",
-                gemm_done, conv_done, conv_tried, g_checks, g_max_a_bytes, g_max_offset);
+                " max_record_end=%" PRId64 " bwd_data_as_fwd=%ld\n",
+                gemm_done, conv_done, conv_tried, g_checks, g_max_a_bytes, g_max_offset, g_bwd_as_fwd);
     return 0;
 }

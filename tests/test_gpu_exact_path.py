@@ -322,6 +322,9 @@ BORDER_CASES = [
     ("stride 2x3, asymmetric pads", dict(W.conv_desc(1, 11, 10, 10, 6, 5, 5, 2, pads=(2, 1, 0, 3)), stride_w=3)),
     ("few channels, unfolded", W.conv_desc(2, 9, 10, 3, 6, 3, 4, 1, 1)),
     ("few channels, unfolded, stride 2", W.conv_desc(2, 11, 12, 2, 5, 5, 5, 2, 2)),
+    # stride 1, pads within the kernel, 16 or more output channels: backward data on the forward route
+    ("pad 1, backward data as forward", W.conv_desc(2, 7, 8, 9, 20, 3, 3, 1, 1)),
+    ("asymmetric pads up to k - 1, backward data as forward", W.conv_desc(1, 8, 9, 6, 17, 4, 3, 1, pads=(3, 0, 1, 2))),
 ]
 
 

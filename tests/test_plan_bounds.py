@@ -43,3 +43,5 @@ def test_plans_and_taps_stay_in_bounds(harness, seed):
     assert int(fields["gemm_cases"]) == 10000 and int(fields["conv_cases"]) == 10000
     # the sampled shapes reach the 32-bit offset range the kernels rely on
     assert int(fields["max_a_bytes"]) > 2 ** 31, line[0]
+    # stride-1 backward-data passes that take the forward route are among them
+    assert int(fields["bwd_data_as_fwd"]) > 100, line[0]
