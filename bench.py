@@ -12,13 +12,15 @@ Prints one JSON line.  Besides the contract fields it carries
                 launch over its average launch duration, measured with HIP events recorded on
                 its stream inside the timed region, against the FP32 vector peak
   kernels       per-kernel rates of the step (HIP events on the launch stream), then, timed
-                after the step: the 4096^3 GEMM with the M = 11 (2048-entry-row) Mitchell table,
+                after the step: the 4096^3 GEMM with the M = 11 Mitchell table (sum-indexed: read
+                from one array of 4096 factors),
                 the three ResNet-50 layers (batch 32, each pass), the LeNet-5 stack (batch 64,
                 exact bfloat16-truncation table), the step's GEMM and convolution passes with
                 the native FP32 multiply in the same kernels, and the same four with the vendor
-                FP32 libraries torch calls (hipBLASLt / MIOpen, TF32 off).  None of these
-                launches the step GEMM's kernel (other template instances), so a kernel trace of
-                the run still times exactly the launches the roofline is quoted for.
+                FP32 libraries torch calls (hipBLASLt / MIOpen, TF32 off).  The ResNet-50 1x1
+                passes run as GEMMs and may launch the step GEMM's kernel instance, so a kernel
+                trace that is to time only the launches the roofline is quoted for is taken with
+                --no-other-kernels.
   cpu_baseline  the CPU oracle timed on a seeded sample of the same step's outputs
   extra         (with --extra only) a GEMM size sweep, the direct-evaluation GEMMs, a
                 post-ReLU input case, the exact-truncation table on the step and a LeNet-5
@@ -273,7 +275,7 @@ def other_kernels(B, W, torch, dev, lut7, m7, A, Bm, C, cv, conv_t, ws_g, ws_c):
     """The other configurations, timed after the step (not part of `value`)."""
     ks = {}
     M, N, K = A.shape[0], Bm.shape[1], A.shape[1]
-    # the step's GEMM with the M = 11 table (rows of 2048 entries staged per slab)
+    # the step's GEMM with the M = 11 table (sum-indexed: one array of 2^12 factors in LDS)
     lut11 = B.device_lut(B.lut_build(11, "mitchell"), dev)
     ws = torch.empty(B.amsim_gemm_workspace_size(0, 0, M, N, K, 11), dtype=torch.uint8, device=dev)
     ks["gemm_4096_m11"] = _time_main_kernel(B, torch, lambda: B.approx_gemm(A, Bm, lut11, 11, out=C, workspace=ws),
@@ -399,7 +401,7 @@ def extras(B, W, torch, np, dev, lut7, m7, A, Bm, C):
     ex = {}
     M, N, K = A.shape[0], Bm.shape[1], A.shape[1]
     lut11 = B.device_lut(B.lut_build(11, "mitchell"), dev)
-    # the same GEMM at smaller sizes, 128-entry table rows (M=7) and 2048-entry rows (M=11)
+    # the same GEMM at smaller sizes, with the M = 7 and the M = 11 table
     sweep = {}
     for n in (64, 512, 1024, 2048):
         a, b = (torch.from_numpy(t).to(dev) for t in W.gemm_inputs(n, n, n, "normal", seed=5100 + n))
