@@ -80,3 +80,32 @@ def test_conv_passes_write_only_their_results(B, ci):
         assert np.array_equal(b[GUARD:-GUARD], ref.cpu().numpy().view(np.int32).reshape(-1)), what + ": result differs"
         tail = wbuf[nbytes:].cpu().numpy()
         assert np.all(tail == WS_BYTE), what + ": a write past the workspace (%d bytes)" % nbytes
+
+
+GEMM_CASES = [
+    ("tiled", (300, 130, 257), 7),
+    ("split reduction", (64, 24, 20000), 7),
+    ("vector, m = 1", (1, 3000, 700), 7),
+    ("vector, n = 1", (3000, 1, 700), 7),
+    ("outer product, k = 1", (300, 200, 1), 7),
+    ("wide sum-indexed table", (200, 72, 300), 11),
+]
+
+
+@pytest.mark.parametrize("gi", range(len(GEMM_CASES)))
+def test_gemm_writes_only_its_result(B, gi):
+    name, (m, n, k), mb = GEMM_CASES[gi]
+    A = torch.from_numpy(W.normal((m, k), 1.0, 80 + gi)).cuda()
+    Bm = torch.from_numpy(W.normal((k, n), 1.0, 81 + gi)).cuda()
+    lut = B.device_lut(B.lut_build(mb, "mitchell"))
+    ref = B.approx_gemm(A, Bm, lut, mb)
+    buf, out = _guarded((m, n))
+    nbytes = B.amsim_gemm_workspace_size(0, 0, m, n, k, mb)
+    wbuf, ws = _guarded_workspace(nbytes)
+    B.approx_gemm(A, Bm, lut, mb, out=out, workspace=ws)
+    torch.cuda.synchronize()
+    b = buf.cpu().numpy()
+    sentinel = np.int32(np.uint32(SENTINEL).view(np.int32))
+    assert np.all(b[:GUARD] == sentinel) and np.all(b[-GUARD:] == sentinel), name + ": a write outside the result"
+    assert np.array_equal(b[GUARD:-GUARD], ref.cpu().numpy().view(np.int32).reshape(-1)), name + ": result differs"
+    assert np.all(wbuf[nbytes:].cpu().numpy() == WS_BYTE), name + ": a write past the workspace (%d bytes)" % nbytes
