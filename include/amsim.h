@@ -178,11 +178,12 @@ int amsim_conv2d_workspace_size(const amsim_conv2d *desc, int pass, int m_bits, 
 int approx_conv2d_fwd(const amsim_conv2d *desc, const float *x, const float *w, float *y, const uint32_t *lut,
                       int m_bits, void *workspace, size_t workspace_bytes, void *stream);
 
-/* Preceding-layer gradient (Algorithm 4, second half): dx[n,h,w,ci] = sum over (kh,kw,co) and
- * output positions (oh,ow) with oh*sh+kh-pt == h and ow*sw+kw-pl == w of
- * amul(dy[n,oh,ow,co], w[kh,kw,ci,co]) -- the padded, dilated error against the transposed and
- * reversed weights, without materialising either.  dy: device [n][OH][OW][c_out], w: device
- * HWIO, dx: device [n][h][w][c_in] (overwritten; positions no output reads get -0.0). */
+/* Preceding-layer gradient (Algorithm 4, second half): dx[n,h,w,ci] = sum over every (kh,kw,co)
+ * of amul(e, w[kh,kw,ci,co]), where e = dy[n,oh,ow,co] for the output position (oh,ow) with
+ * oh*sh+kh-pt == h and ow*sw+kw-pl == w when it exists, else +0 -- the padded, dilated error
+ * against the transposed and reversed weights, without materialising either; its zeros are
+ * multiplied like any operand (a signed zero, or NaN against an Inf or NaN weight).
+ * dy: device [n][OH][OW][c_out], w: device HWIO, dx: device [n][h][w][c_in] (overwritten). */
 int approx_conv2d_bwd_data(const amsim_conv2d *desc, const float *dy, const float *w, float *dx,
                            const uint32_t *lut, int m_bits, void *workspace, size_t workspace_bytes, void *stream);
 
