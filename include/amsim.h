@@ -259,7 +259,9 @@ int approx_mul_ew_ex(const amsim_options *opt, int64_t n, const float *a, const 
  * Measurement support (no paper counterpart; the paper reports per-batch wall time only).
  * Between amsim_profile_start and amsim_profile_stop, every launch of a main kernel -- the
  * GEMM kernel of approx_gemm and the three convolution kernels, not their decode pre-passes
- * -- is bracketed by two HIP events recorded on the stream it is launched on.
+ * -- is bracketed by two HIP events recorded on the stream it is launched on.  The events are
+ * timing-only (created without the system-scope fence on completion), so they add no cache
+ * writeback around the kernels they time; they order nothing for the host.
  *   amsim_profile_start(max_launches): creates that many event pairs (host-side HIP calls; do
  *     it outside any timed region) and starts recording; AMSIM_ERR_INVALID_ARG if
  *     max_launches < 1, AMSIM_ERR_HIP on event creation failure.  Launches beyond the

@@ -2357,12 +2357,20 @@ int amsim_profile_start(int max_launches)
     t.end.resize(size_t(max_launches));
     t.kind.assign(size_t(max_launches), 0);
     for (int i = 0; i < max_launches; ++i) {
-        if (hipEventCreate(&t.begin[size_t(i)]) != hipSuccess || hipEventCreate(&t.end[size_t(i)]) != hipSuccess) {
+        // Timing-only events: no system-scope fence when they complete.  That fence writes back and
+        // invalidates the caches; measured on MI355X, it left ~5.6 us idle on each side of a table
+        // kernel (where the step's launches otherwise follow one another with no gap).
+        hipEvent_t b = nullptr, e = nullptr;
+        if (hipEventCreateWithFlags(&b, hipEventDisableSystemFence) != hipSuccess ||
+            hipEventCreateWithFlags(&e, hipEventDisableSystemFence) != hipSuccess) {
+            if (b != nullptr) (void)hipEventDestroy(b);
             t.begin.resize(size_t(i));
             t.end.resize(size_t(i));
             destroy_events(t);
             return AMSIM_ERR_HIP;
         }
+        t.begin[size_t(i)] = b;
+        t.end[size_t(i)] = e;
     }
     t.active = true;
     return AMSIM_OK;
