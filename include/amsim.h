@@ -280,6 +280,10 @@ int approx_mul_ew_ex(const amsim_options *opt, int64_t n, const float *a, const 
 #define AMSIM_KERNEL_CONV_BWD_DATA_NATIVE 6
 #define AMSIM_KERNEL_CONV_BWD_WEIGHT_NATIVE 7
 int amsim_profile_start(int max_launches);
+/* amsim_profile_start, timing only the kernel kinds whose bit (1u << AMSIM_KERNEL_*) is set in
+ * kinds: every other launch gets no events, so it runs as it would unprofiled.
+ * AMSIM_ERR_INVALID_ARG for max_launches < 1, kinds == 0 or a bit above the last kind. */
+int amsim_profile_start_kinds(int max_launches, unsigned kinds);
 int amsim_profile_stop(void);
 int amsim_profile_read(int kind, int *launches, double *total_ms);
 

@@ -119,6 +119,7 @@ def lib():
         "approx_gemm_direct": ([ctypes.c_int, ctypes.c_int, i64, i64, i64, vp, i64, vp, i64, vp, i64, vp],
                                ctypes.c_int),
         "amsim_profile_start": ([ctypes.c_int], ctypes.c_int),
+        "amsim_profile_start_kinds": ([ctypes.c_int, ctypes.c_uint], ctypes.c_int),
         "amsim_profile_stop": ([], ctypes.c_int),
         "amsim_profile_read": ([ctypes.c_int, ctypes.POINTER(ctypes.c_int), ctypes.POINTER(ctypes.c_double)],
                                ctypes.c_int),
@@ -472,8 +473,15 @@ def amsim_cast_exponent(x, e_bits, exp_cast="inf", m_bits=7, out=None):
 
 # ------------------------------------------------------------------ kernel timing --------
 
-def amsim_profile_start(max_launches: int = 4096) -> None:
-    _check(lib().amsim_profile_start(int(max_launches)), "amsim_profile_start")
+def amsim_profile_start(max_launches: int = 4096, kinds=None) -> None:
+    """Start timing main-kernel launches; kinds: names or AMSIM_KERNEL_* values to time (default all)."""
+    if kinds is None:
+        _check(lib().amsim_profile_start(int(max_launches)), "amsim_profile_start")
+        return
+    mask = 0
+    for k in kinds:
+        mask |= 1 << (KERNEL_KINDS[k] if isinstance(k, str) else int(k))
+    _check(lib().amsim_profile_start_kinds(int(max_launches), mask), "amsim_profile_start_kinds")
 
 
 def amsim_profile_stop() -> None:

@@ -1629,6 +1629,7 @@ constexpr int kKernelKinds = 8;  // AMSIM_KERNEL_*
 struct KernelTimer {
     std::mutex mu;
     bool active = false;
+    unsigned kinds = 0u;  // bit k set: kernel kind k is timed
     std::vector<hipEvent_t> begin, end;
     std::vector<int> kind;
     size_t used = 0;
@@ -1649,7 +1650,7 @@ class TimedLaunch {
     {
         KernelTimer &t = timer();
         std::lock_guard<std::mutex> g(t.mu);
-        if (t.active && t.used < t.begin.size()) {
+        if (t.active && ((t.kinds >> kind) & 1u) && t.used < t.begin.size()) {
             slot_ = long(t.used++);
             t.kind[size_t(slot_)] = kind;
             (void)hipEventRecord(t.begin[size_t(slot_)], st_);
@@ -2341,12 +2342,15 @@ int amsim_cast_exponent(int e_bits, int exp_cast, int m_bits, int64_t n, const f
     return launch_status();
 }
 
-int amsim_profile_start(int max_launches)
+int amsim_profile_start(int max_launches) { return amsim_profile_start_kinds(max_launches, (1u << kKernelKinds) - 1u); }
+
+int amsim_profile_start_kinds(int max_launches, unsigned kinds)
 {
-    if (max_launches < 1) return AMSIM_ERR_INVALID_ARG;
+    if (max_launches < 1 || kinds == 0u || (kinds >> kKernelKinds) != 0u) return AMSIM_ERR_INVALID_ARG;
     KernelTimer &t = timer();
     std::lock_guard<std::mutex> g(t.mu);
     t.active = false;
+    t.kinds = kinds;
     destroy_events(t);
     t.used = 0;
     for (int k = 0; k < kKernelKinds; ++k) {

@@ -181,6 +181,10 @@ def test_device_entry_points_reject_bad_arguments_before_launching(L):
     assert L.approx_mul_ew(4, None, fake, fake, fake, 7, None) == binding.AMSIM_ERR_INVALID_ARG
     assert L.approx_mul_ew(4, fake, fake, fake, fake, 12, None) == binding.AMSIM_ERR_UNSUPPORTED
     assert L.approx_mul_ew(0, None, None, None, None, 7, None) == binding.AMSIM_OK
+    # the kernel timer's kind mask: at least one kind, none beyond the last
+    assert L.amsim_profile_start_kinds(0, 1) == binding.AMSIM_ERR_INVALID_ARG
+    assert L.amsim_profile_start_kinds(8, 0) == binding.AMSIM_ERR_INVALID_ARG
+    assert L.amsim_profile_start_kinds(8, 1 << 8) == binding.AMSIM_ERR_INVALID_ARG
     direct = L.approx_gemm_direct
     assert direct(2, 7, 4, 4, 4, fake, 4, fake, 4, fake, 4, None) == binding.AMSIM_ERR_INVALID_ARG
     assert direct(binding.AMSIM_DIRECT_MITCHELL, 12, 4, 4, 4, fake, 4, fake, 4, fake, 4, None) == binding.AMSIM_ERR_UNSUPPORTED

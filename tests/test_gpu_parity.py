@@ -674,3 +674,24 @@ def test_lenet5_stack_fwd_bwd(B):
     check(dW1, oracle.conv2d_bwd_weight(oracle.EXACT_TRUNC, m, c1, x0, dy1), "conv1 bwd_weight")
     dX0 = B.approx_conv2d_bwd_data(c1, dY1, cuda(w1), lut, m)
     check(dX0, oracle.conv2d_bwd_data(oracle.EXACT_TRUNC, m, c1, dy1, w1), "conv1 bwd_data")
+
+
+def test_kernel_timer_times_only_the_selected_kinds(B):
+    """amsim_profile_start_kinds: the GEMM kernel is timed, a convolution pass in the same
+    profiling window is not (and runs unbracketed); with every kind, both are."""
+    A = cuda(W.normal((256, 128), 1.0, 91))
+    Bm = cuda(W.normal((128, 64), 1.0, 92))
+    p = W.conv_desc(2, 9, 9, 16, 16, 3, 3, 1, 1)
+    oh, ow = W.conv_out_hw(p)
+    x = cuda(W.normal((2, 9, 9, 16), 1.0, 93))
+    w = cuda(W.normal((3, 3, 16, 16), 1.0, 94))
+    lut = dev_lut(B, "mitchell", 7)
+    for kinds, want in ((["gemm"], (1, 0)), (None, (1, 1))):
+        B.amsim_profile_start(16, kinds=kinds)
+        B.approx_gemm(A, Bm, lut, 7)
+        B.approx_conv2d_fwd(p, x, w, lut, 7)
+        torch.cuda.synchronize()
+        B.amsim_profile_stop()
+        got = (B.amsim_profile_read("gemm")[0], B.amsim_profile_read("conv_fwd")[0])
+        assert got == want, (kinds, got)
+        assert B.amsim_profile_read("gemm")[1] > 0.0
