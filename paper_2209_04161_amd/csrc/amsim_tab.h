@@ -1138,9 +1138,10 @@ __device__ __forceinline__ void tab_body_dot(const TabArgs &a)
     // Staging pipeline: while slab s is computed, the table bytes of slab s + 1 are fetched (its
     // second-operand words `sbw` having arrived during slab s - 1) and the second-operand words
     // of slab s + 2 are loaded into `sbw2`, so that the words' latency is not exposed once per
-    // slab (8-step slabs lose most, 16-step slabs ~1%).  The backward-data pass of 16-step slabs
-    // fetches both in slab s: its tap arithmetic leaves no registers for `sbw2`.
-    constexpr bool AHEAD2 = NW <= 4 || OP != OP_BWD_DATA;
+    // slab (8-step slabs lose most, 16-step slabs ~1%).  16-step slabs fetch both in slab s: their
+    // registers go to the second gather set of the pair loop (the backward-data pass's, to its tap
+    // arithmetic).
+    constexpr bool AHEAD2 = NW <= 4;
     u32x4 sbw[2], sbw2[2];
     uint32_t srw[DC];
     float acc[TM][TN];
@@ -1215,6 +1216,40 @@ __device__ __forceinline__ void tab_body_dot(const TabArgs &a)
         // priority): the gathers of the slowest waves keep the LDS busy, and a workgroup reaches
         // its barrier sooner.
         __builtin_amdgcn_s_setprio(3);
+        // The two gathers of lane row r of pair kp: the entry byte offset is the mantissa field
+        // * 16 (the index plane, or the word's low half under its head) plus the slot's, which is
+        // a constant.
+        auto gather = [&](int kp, int r, uint32_t(&X)[DC / 2], uint32_t(&Y)[DC / 2]) __attribute__((always_inline)) {
+            const uint32_t o0 = w[kp % RS][0][r];
+            const uint32_t o1 = w[kp % RS][1][r];
+            if constexpr (DC == 8) {
+                const u32x4 x4 = lds_load_b128(o0, BOFF + (2 * kp) * kDotStepBytes);
+                const u32x4 y4 = lds_load_b128(o1, BOFF + (2 * kp + 1) * kDotStepBytes);
+#pragma unroll
+                for (int q = 0; q < 4; ++q) {
+                    X[q] = x4[q];
+                    Y[q] = y4[q];
+                }
+            } else {
+                const u32x2 x2 = lds_load_b64(o0, BOFF + (2 * kp) * kDotStepBytes);
+                const u32x2 y2 = lds_load_b64(o1, BOFF + (2 * kp + 1) * kDotStepBytes);
+#pragma unroll
+                for (int q = 0; q < 2; ++q) {
+                    X[q] = x2[q];
+                    Y[q] = y2[q];
+                }
+            }
+        };
+        // Gathers run one lane row ahead of the products (two register sets), so that a wave's
+        // own permutes and dots cover part of its gathers' latency; scheduling barriers keep the
+        // compiler from hoisting more gathers (which costs registers).  The gather for the first
+        // row of pair kp + 1 is issued even when the slab ends at kp: its ring slot then holds a
+        // record already loaded (of this slab or the next), whose index words address this slab's
+        // buffer, and the entries read are not used.  The backward-data pass, whose tap
+        // arithmetic leaves no registers for the second set, gathers each row just before use.
+        constexpr bool PIPE = OP != OP_BWD_DATA;
+        uint32_t GX[2][DC / 2], GY[2][DC / 2];
+        if (PIPE && npairs > 0) gather(0, 0, GX[0], GY[0]);
 #pragma unroll
         for (int kp = 0; kp < KS / 2; ++kp) {
             if (kp >= npairs) break;
@@ -1222,32 +1257,21 @@ __device__ __forceinline__ void tab_body_dot(const TabArgs &a)
                 dot_load_pair<OP, TM>(w[(kp + LA) % RS], av, cur, c0 + 2 * (kp + LA));
             else
                 dot_load_pair<OP, TM>(w[(kp + LA) % RS], av, nxt, nc0 + 2 * (kp + LA - KS / 2));
-            const uint32_t(&a0)[TM] = w[kp % RS][0];
-            const uint32_t(&a1)[TM] = w[kp % RS][1];
 #pragma unroll
             for (int r = 0; r < TM; ++r) {
-                // entry byte offset = the mantissa field * 16 (the index plane, or the word's low
-                // half under its head) plus the slot's, which is a constant
-                const uint32_t o0 = a0[r];
-                const uint32_t o1 = a1[r];
-                uint32_t X[DC / 2], Y[DC / 2];
-                if constexpr (DC == 8) {
-                    const u32x4 x4 = lds_load_b128(o0, BOFF + (2 * kp) * kDotStepBytes);
-                    const u32x4 y4 = lds_load_b128(o1, BOFF + (2 * kp + 1) * kDotStepBytes);
-#pragma unroll
-                    for (int q = 0; q < 4; ++q) {
-                        X[q] = x4[q];
-                        Y[q] = y4[q];
-                    }
+                const int cb = PIPE ? (kp * TM + r) & 1 : 0;
+                if constexpr (PIPE) {
+                    __builtin_amdgcn_sched_barrier(0);
+                    if (r + 1 < TM)
+                        gather(kp, r + 1, GX[cb ^ 1], GY[cb ^ 1]);
+                    else if (kp + 1 < KS / 2)
+                        gather(kp + 1, 0, GX[cb ^ 1], GY[cb ^ 1]);
+                    __builtin_amdgcn_sched_barrier(0);
                 } else {
-                    const u32x2 x2 = lds_load_b64(o0, BOFF + (2 * kp) * kDotStepBytes);
-                    const u32x2 y2 = lds_load_b64(o1, BOFF + (2 * kp + 1) * kDotStepBytes);
-#pragma unroll
-                    for (int q = 0; q < 2; ++q) {
-                        X[q] = x2[q];
-                        Y[q] = y2[q];
-                    }
+                    gather(kp, r, GX[0], GY[0]);
                 }
+                const uint32_t(&X)[DC / 2] = GX[cb];
+                const uint32_t(&Y)[DC / 2] = GY[cb];
                 const uint32_t pa = w[kp % RS][NA - 1][r];  // (pa(k), pa(k+1)) as bf16
 #pragma unroll
                 for (int q = 0; q < TN / 2; ++q) {
